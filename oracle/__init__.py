@@ -1,0 +1,201 @@
+"""ctypes front end of the CPU oracle of the route-and-schedule tick.
+
+TEST INFRASTRUCTURE ONLY: the tests, the smoke check and the CPU-baseline leg
+of the benchmark may use it; the GPU library never does. The oracle is plain
+scalar C++ (oracle.cpp) with the policy MLP in fp64; see that file for the
+paper passages each step follows.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.cpp")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+KEY_MODES = {"slack": 0, "deadline": 1, "fcfs": 2}
+ERR_QIDX, ERR_COUNT, ERR_BUDGET, ERR_SVC, ERR_ACTION = 1, 2, 4, 8, 16
+
+
+def build(force: bool = True) -> str:
+    """Compile oracle.cpp into liboracle.so with g++ (no GPU involved)."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp"
+        subprocess.check_call(["g++", "-O2", "-std=c++17", "-fPIC", "-shared", "-pthread",
+                               "-ffp-contract=off", "-o", tmp, _SRC])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+class _Desc(ctypes.Structure):
+    _fields_ = [("E", ctypes.c_int32), ("M", ctypes.c_int32), ("K", ctypes.c_int32),
+                ("qcap", ctypes.c_int32), ("max_slots", ctypes.c_int32),
+                ("embed_dim", ctypes.c_int32), ("feat_dim", ctypes.c_int32),
+                ("n_layers", ctypes.c_int32), ("widths", ctypes.c_int32 * 4),
+                ("dtype", ctypes.c_int32), ("key_mode", ctypes.c_int32),
+                ("max_arrivals", ctypes.c_int32), ("budget_max", ctypes.c_int32),
+                ("Q", ctypes.c_int64)]
+
+
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build(force=False)
+        L = ctypes.CDLL(_LIB)
+        P = ctypes.c_void_p
+        L.orc_create.restype = P
+        L.orc_create.argtypes = [ctypes.POINTER(_Desc), P, P, P, P, P]
+        L.orc_destroy.argtypes = [P]
+        L.orc_tick.argtypes = [P]
+        L.orc_tick.restype = ctypes.c_int32
+        L.orc_error.argtypes = [P]
+        L.orc_error.restype = ctypes.c_int32
+        L.orc_clear_error.argtypes = [P]
+        L.orc_route.argtypes = [P, P, P, P, P, P, ctypes.c_int]
+        L.orc_schedule.argtypes = [P, ctypes.c_int32, P, P, P, P, P, ctypes.c_int]
+        L.orc_features.argtypes = [P, ctypes.c_int, ctypes.c_int32, ctypes.c_int32, P]
+        L.orc_round_bf16.argtypes = [ctypes.c_double]
+        L.orc_round_bf16.restype = ctypes.c_double
+        L.orc_round_bf16_array.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64]
+        L.orc_set_enabled.argtypes = [P, ctypes.c_int, ctypes.c_int, ctypes.c_int]
+        L.orc_set_capacity.argtypes = [P, ctypes.c_int, ctypes.c_int, ctypes.c_int]
+        L.orc_read_state.argtypes = [P] * 7
+        _lib = L
+    return _lib
+
+
+def _ptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def round_bf16(v: float) -> float:
+    return _load().orc_round_bf16(float(v))
+
+
+def round_bf16_array(x) -> np.ndarray:
+    """bf16 round-to-nearest-even of every element (fp64 in, fp64 out)."""
+    x = np.ascontiguousarray(x, np.float64)
+    out = np.empty_like(x)
+    _load().orc_round_bf16_array(_ptr(x), _ptr(out), x.size)
+    return out
+
+
+class Oracle:
+    """One oracle pool over E envs (cfg: a workload config dict).
+
+    W, b: lists of fp32 arrays (W[l] is [out, in]); emb_values: float32
+    [Q, E_d] (the value of each table entry); cap: int32 [E, M];
+    logit_bias: float32 [M] or None."""
+
+    def __init__(self, cfg, W, b, emb_values, cap, logit_bias=None, E=None, threads=1):
+        L = _load()
+        d = _Desc()
+        self.E = cfg["E"] if E is None else E
+        d.E, d.M, d.K = self.E, cfg["M"], cfg["K"]
+        d.qcap, d.max_slots = cfg["qcap"], cfg["max_slots"]
+        d.embed_dim, d.feat_dim, d.n_layers = cfg["embed_dim"], cfg["feat_dim"], len(cfg["widths"])
+        for i, w in enumerate(cfg["widths"]):
+            d.widths[i] = w
+        d.dtype = 1 if cfg["dtype"] == "bf16" else 0
+        d.key_mode = KEY_MODES[cfg["key_mode"]]
+        d.max_arrivals = cfg["max_arrivals"]
+        d.budget_max = cfg["budget_max"]
+        emb = np.ascontiguousarray(emb_values, np.float32)
+        d.Q = emb.shape[0]
+        self.cfg, self.M, self.K, self.A = cfg, cfg["M"], cfg["K"], cfg["M"] * cfg["K"]
+        self.qcap, self.S = cfg["qcap"], cfg["max_slots"]
+        self.threads = threads
+        self._W = [np.ascontiguousarray(w, np.float32) for w in W]
+        self._b = [np.ascontiguousarray(x, np.float32) for x in b]
+        Wp = (ctypes.c_void_p * len(W))(*[w.ctypes.data for w in self._W])
+        bp = (ctypes.c_void_p * len(b))(*[x.ctypes.data for x in self._b])
+        cap = np.ascontiguousarray(cap, np.int32).reshape(-1)
+        assert cap.size == self.E * self.M
+        lb = None if logit_bias is None else np.ascontiguousarray(logit_bias, np.float32)
+        self._d = d
+        self.p = L.orc_create(ctypes.byref(d), ctypes.cast(Wp, ctypes.c_void_p),
+                              ctypes.cast(bp, ctypes.c_void_p), _ptr(emb), _ptr(cap),
+                              None if lb is None else _ptr(lb))
+        self._lib = L
+
+    def __del__(self):
+        if getattr(self, "p", None):
+            self._lib.orc_destroy(self.p)
+            self.p = None
+
+    @property
+    def t(self) -> int:
+        return self._lib.orc_tick(self.p)
+
+    @property
+    def error(self) -> int:
+        return self._lib.orc_error(self.p)
+
+    def clear_error(self):
+        self._lib.orc_clear_error(self.p)
+
+    @staticmethod
+    def _arr(arr):
+        return (np.ascontiguousarray(arr["offsets"], np.int32),
+                np.ascontiguousarray(arr["q_idx"], np.int32),
+                np.ascontiguousarray(arr["budget"], np.int16),
+                np.ascontiguousarray(arr["base_svc"], np.int16))
+
+    def route(self, arr, want_logits=True):
+        """Returns (actions int32 [n], logits float64 [n, A] or None)."""
+        off, q, bud, _ = self._arr(arr)
+        assert off.size == self.E + 1
+        n = int(q.size)
+        act = np.empty(n, np.int32)
+        lg = np.empty((n, self.A), np.float64) if want_logits else None
+        self._lib.orc_route(self.p, _ptr(off), _ptr(q), _ptr(bud),
+                            None if lg is None else _ptr(lg), _ptr(act), self.threads)
+        return act, lg
+
+    def schedule(self, arr, actions):
+        off, q, bud, svc = self._arr(arr)
+        act = np.ascontiguousarray(actions, np.int32)
+        self._lib.orc_schedule(self.p, int(q.size), _ptr(off), _ptr(q), _ptr(bud), _ptr(svc),
+                               _ptr(act), self.threads)
+
+    def tick(self, arr):
+        act, _ = self.route(arr, want_logits=False)
+        self.schedule(arr, act)
+        return act
+
+    def features(self, e, q_idx, budget):
+        out = np.empty(self.cfg["feat_dim"], np.float64)
+        self._lib.orc_features(self.p, e, q_idx, budget, _ptr(out))
+        return out
+
+    def set_enabled(self, e, m, v):
+        self._lib.orc_set_enabled(self.p, e, m, int(bool(v)))
+
+    def set_capacity(self, e, m, c):
+        self._lib.orc_set_capacity(self.p, e, m, int(c))
+
+    def state(self) -> dict:
+        """Snapshot as a dict of numpy arrays (common test representation)."""
+        E, M, S, Qc, A = self.E, self.M, self.S, self.qcap, self.A
+        env_i32 = np.zeros(E, np.int32)
+        env_i64 = np.zeros((E, 2), np.int64)
+        mod = np.zeros((E, M, 13), np.int64)
+        slots = np.zeros((E, M, S, 4), np.int32)
+        queues = np.zeros((E, M, Qc, 5), np.int32)
+        hist = np.zeros((E, A), np.int64)
+        self._lib.orc_read_state(self.p, _ptr(env_i32), _ptr(env_i64), _ptr(mod), _ptr(slots),
+                                 _ptr(queues), _ptr(hist))
+        return dict(t=self.t, next_id=env_i32, arrived=env_i64[:, 0], rej_nomodel=env_i64[:, 1],
+                    qlen=mod[..., 0], busy=mod[..., 1], ewma=mod[..., 2], backlog=mod[..., 3],
+                    cap=mod[..., 4], enabled=mod[..., 5], rej_overflow=mod[..., 6],
+                    enqueued=mod[..., 7], started=mod[..., 8], completed=mod[..., 9],
+                    slo_met=mod[..., 10], lat_sum=mod[..., 11], wait_sum=mod[..., 12],
+                    slots=slots, queues=queues, hist=hist)

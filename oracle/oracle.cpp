@@ -1,0 +1,456 @@
+// Oracle of the batched route-and-schedule tick.
+//
+// TEST INFRASTRUCTURE ONLY. This is the plain, slow, scalar CPU definition
+// that the GPU library is checked against. Only the tests, the smoke check and
+// the CPU-baseline leg of the benchmark may load it. It shares no source,
+// header, table or constant generator with the GPU library.
+//
+// What it computes (per independent env e, per tick t), following the paper:
+//   Sec. 3 "State" (Eq. 1): the executor observes the query embedding, the
+//     remaining budget and per-model queue depth, latency and KV-cache load.
+//   Sec. 3 "Action": a joint action a in [0, N*|S|) decodes to model a / K and
+//     reasoning depth a % K.
+//   Sec. 4.2: a policy network scores every joint action; the build deploys
+//     it greedily (masked argmax) with a plain MLP in place of the
+//     dual-pathway network.
+//   Sec. 4.3: every model's queue is served earliest-deadline-first with the
+//     deadline t_arrive + budget; the default key is the latest start time
+//     (deadline - service time), i.e. the slack.
+//   Sec. 5.4: the latency signal is an exponential moving average of observed
+//     end-to-end latency.
+//   Table 5: each model serves a bounded number of sequences at once.
+// Where the paper is silent, the readings are the documented ones: integer
+// ticks, c_m concurrent service slots, ties broken by request id, tail-drop
+// admission, alpha = 1/8 Q8 fixed-point EWMA, features normalised by
+// reciprocals rounded once to fp32.
+//
+// Parity status: pinned by the golden example, closed-form invariants, a
+// textbook single-server simulator, brute force over forced actions and
+// library routines (see tests). The policy arithmetic is in fp64.
+
+#include <algorithm>
+#include <cfenv>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <thread>
+#include <vector>
+
+namespace {
+
+// ----- limits of the boundary the oracle mirrors --------------------------
+const int kSvcMax = 4095;      // base service time must lie in [1, kSvcMax]
+
+enum ErrBits {
+  ERR_QIDX = 1,      // q_idx outside [0, Q)
+  ERR_COUNT = 2,     // offsets not a valid CSR or n_e > max arrivals
+  ERR_BUDGET = 4,    // budget < 1
+  ERR_SVC = 8,       // base_svc outside [1, kSvcMax]
+  ERR_ACTION = 16,   // action outside [-1, A)
+};
+
+// ----- bf16 round-to-nearest-even of a real value ------------------------
+// bf16 keeps 8 significant bits and fp32's exponent range (normal numbers
+// down to 2^-126, subnormal quantum 2^-133). Round |v| to the nearest
+// multiple of its quantum, ties to even (the default FE_TONEAREST mode).
+double round_bf16(double v) {
+  if (v == 0.0 || !std::isfinite(v)) return v;
+  int e;
+  std::frexp(v, &e);                        // v = f * 2^e with 0.5 <= |f| < 1
+  int qexp = std::max(e - 8, -133);         // quantum of the bf16 grid at v
+  double r = std::nearbyint(std::ldexp(v, -qexp));
+  double out = std::ldexp(r, qexp);
+  const double kMax = std::ldexp(255.0, 120);  // largest finite bf16 (1.9921875 * 2^127)
+  if (std::fabs(out) > kMax) return std::copysign(INFINITY, v);
+  return out;
+}
+
+// ----- data -----------------------------------------------------------------
+struct Entry {            // a queued request
+  int32_t key;            // sort key (slack / deadline / arrival tick)
+  int32_t id;             // per-env request id, increasing in arrival order
+  int32_t t_arr;          // arrival tick
+  int32_t svc;            // service time in ticks = base_svc * (depth + 1)
+  int32_t budget;         // time budget in ticks
+};
+
+struct Slot {             // a service slot of a model
+  bool busy = false;
+  int32_t id = -1, t_arr = 0, rem = 0, budget = 0;
+};
+
+struct ModelState {
+  std::vector<Entry> queue;   // sorted by key, ties by id (head = index 0)
+  std::vector<Slot> slots;    // max_slots slots, only s < cap are filled
+  int32_t ewma_q8 = 0;        // latency EWMA in Q8 fixed point (ticks * 256)
+  int64_t backlog = 0;        // sum of svc over the queue
+  int32_t cap = 0;            // c_m, concurrent service slots
+  int32_t enabled = 1;
+  int64_t rej_overflow = 0, enqueued = 0, started = 0, completed = 0,
+          slo_met = 0, lat_sum = 0, wait_sum = 0;
+};
+
+struct EnvState {
+  std::vector<ModelState> models;
+  int32_t next_id = 0;
+  int64_t arrived = 0, rej_nomodel = 0;
+  std::vector<int64_t> hist;  // routed requests per joint action
+};
+
+}  // namespace
+
+extern "C" {
+
+// Pool description (the oracle's own struct; field order is its own).
+struct orc_desc {
+  int32_t E, M, K, qcap, max_slots, embed_dim, feat_dim, n_layers;
+  int32_t widths[4];
+  int32_t dtype;          // 0 fp32, 1 bf16 (weights, inputs, hidden rounded)
+  int32_t key_mode;       // 0 slack, 1 deadline, 2 fcfs
+  int32_t max_arrivals;
+  int32_t budget_max;
+  int64_t Q;
+};
+
+struct orc_pool {
+  orc_desc d;
+  int A;
+  std::vector<std::vector<double>> W;   // [layer] out x in, row-major
+  std::vector<std::vector<double>> b;   // [layer] out
+  std::vector<float> emb;               // Q x embed_dim (value of each entry)
+  std::vector<double> logit_bias;       // M (0 when absent)
+  std::vector<EnvState> envs;
+  int32_t t = 0;
+  int32_t err = 0;
+};
+
+}  // extern "C"
+
+namespace {
+
+// Feature vector of one request (Eq. 1 restated for the build):
+//   [ emb[q_idx] | qlen_m/QCAP | busy_m/c_m | ewma_m/(256 B) | backlog_m/(c_m B) |
+//     budget/B | 0 ... ]
+// with B = budget_max, stats laid out stat-major (all models' queue depth,
+// then all models' KV proxy, ...). Every reciprocal is computed in fp64 and
+// rounded once to fp32; each feature is one fp32 product. In bf16 pools the
+// vector is then rounded to bf16.
+void features(const orc_pool* p, const EnvState& env, int32_t q_idx, int32_t budget,
+              std::vector<double>& x) {
+  const orc_desc& d = p->d;
+  const int M = d.M;
+  x.assign(d.feat_dim, 0.0);
+  for (int k = 0; k < d.embed_dim; ++k)
+    x[k] = p->emb[(size_t)q_idx * d.embed_dim + k];
+  const float inv_qcap = (float)(1.0 / d.qcap);
+  const float inv_lat = (float)(1.0 / (256.0 * d.budget_max));
+  const float inv_bud = (float)(1.0 / d.budget_max);
+  for (int m = 0; m < M; ++m) {
+    const ModelState& ms = env.models[m];
+    int busy = 0;
+    for (const Slot& s : ms.slots) busy += s.busy ? 1 : 0;
+    const int c = std::max(ms.cap, 1);
+    const float inv_c = (float)(1.0 / c);
+    const float inv_clat = (float)(1.0 / ((double)c * d.budget_max));
+    float f_q = (float)ms.queue.size() * inv_qcap;
+    float f_kv = (float)busy * inv_c;
+    float f_lat = (float)ms.ewma_q8 * inv_lat;
+    float f_bl = (float)ms.backlog * inv_clat;
+    x[d.embed_dim + 0 * M + m] = f_q;
+    x[d.embed_dim + 1 * M + m] = f_kv;
+    x[d.embed_dim + 2 * M + m] = f_lat;
+    x[d.embed_dim + 3 * M + m] = f_bl;
+  }
+  float f_b = (float)budget * inv_bud;
+  x[d.embed_dim + 4 * M] = f_b;
+  if (d.dtype == 1)
+    for (double& v : x) v = round_bf16(v);
+}
+
+// Policy MLP in fp64: hidden layers ReLU(W h + b), output W h + b, then the
+// per-model logit bias. In bf16 pools every hidden activation is rounded to
+// bf16 after the ReLU (weights were rounded at creation).
+void mlp(const orc_pool* p, const std::vector<double>& x, std::vector<double>& z) {
+  std::vector<double> h = x, y;
+  const int L = p->d.n_layers;
+  for (int l = 0; l < L; ++l) {
+    const int out = p->d.widths[l];
+    const int in = (int)h.size();
+    y.assign(out, 0.0);
+    for (int o = 0; o < out; ++o) {
+      double s = p->b[l][o];
+      for (int i = 0; i < in; ++i) s += p->W[l][(size_t)o * in + i] * h[i];
+      y[o] = s;
+    }
+    if (l + 1 < L) {
+      for (double& v : y) {
+        v = v > 0.0 ? v : 0.0;
+        if (p->d.dtype == 1) v = round_bf16(v);
+      }
+    }
+    h.swap(y);
+  }
+  z = h;
+  for (int a = 0; a < p->A; ++a) z[a] += p->logit_bias[a / p->d.K];
+}
+
+bool model_valid(const orc_pool* p, const ModelState& ms) {
+  return ms.enabled != 0 && ms.cap > 0 && (int)ms.queue.size() < p->d.qcap;
+}
+
+int32_t sort_key(const orc_pool* p, int32_t t, int32_t budget, int32_t svc) {
+  const int32_t deadline = t + budget;          // Sec. 4.3: t_arrive + beta
+  switch (p->d.key_mode) {
+    case 1: return deadline;                    // EDF by deadline
+    case 2: return t;                           // FCFS
+    default: return deadline - svc;             // latest start time (slack)
+  }
+}
+
+// Route the requests of env e: logits (post-bias, pre-mask) and actions.
+void route_env(orc_pool* p, int e, const int32_t* off, const int32_t* q_idx,
+               const int16_t* budget, double* logits, int32_t* actions, int32_t* err) {
+  const EnvState& env = p->envs[e];
+  std::vector<double> x, z;
+  for (int32_t r = off[e]; r < off[e + 1]; ++r) {
+    if (q_idx[r] < 0 || (int64_t)q_idx[r] >= p->d.Q) {
+      *err |= ERR_QIDX;
+      actions[r] = -1;
+      if (logits) for (int a = 0; a < p->A; ++a) logits[(size_t)r * p->A + a] = 0.0;
+      continue;
+    }
+    features(p, env, q_idx[r], budget[r], x);
+    mlp(p, x, z);
+    int best = -1;
+    for (int a = 0; a < p->A; ++a) {
+      const ModelState& ms = env.models[a / p->d.K];
+      if (!model_valid(p, ms)) continue;
+      if (best < 0 || z[a] > z[best]) best = a;   // strict: lowest index wins ties
+    }
+    actions[r] = best;
+    if (logits) for (int a = 0; a < p->A; ++a) logits[(size_t)r * p->A + a] = z[a];
+  }
+}
+
+// Admission, queue insertion, service and accounting for env e at tick t.
+void schedule_env(orc_pool* p, int e, int32_t n_total, const int32_t* off,
+                  const int32_t* q_idx, const int16_t* budget, const int16_t* base_svc,
+                  const int32_t* actions, int32_t* err) {
+  const orc_desc& d = p->d;
+  EnvState& env = p->envs[e];
+  const int32_t lo = off[e], hi = off[e + 1];
+  // Validate the whole env first; an invalid env is left untouched this tick.
+  int bad = 0;
+  if (lo < 0 || hi < lo || hi > n_total || hi - lo > d.max_arrivals) bad |= ERR_COUNT;
+  if (!bad) {
+    for (int32_t r = lo; r < hi; ++r) {
+      if (q_idx[r] < 0 || (int64_t)q_idx[r] >= d.Q) bad |= ERR_QIDX;
+      if (budget[r] < 1) bad |= ERR_BUDGET;
+      if (base_svc[r] < 1 || base_svc[r] > kSvcMax) bad |= ERR_SVC;
+      if (actions[r] < -1 || actions[r] >= p->A) bad |= ERR_ACTION;
+    }
+  }
+  if (bad) { *err |= bad; return; }
+
+  const int32_t t = p->t;
+  const int32_t n = hi - lo;
+  env.arrived += n;
+  // S2: admission in id order, tail-drop beyond the queue capacity.
+  for (int m = 0; m < d.M; ++m) {
+    ModelState& ms = env.models[m];
+    const int room = d.qcap - (int)ms.queue.size();
+    std::vector<Entry> accepted;
+    int routed = 0;
+    for (int32_t r = lo; r < hi; ++r) {
+      const int32_t a = actions[r];
+      if (a < 0 || a / d.K != m) continue;
+      ++routed;
+      if ((int)accepted.size() >= room) { ms.rej_overflow += 1; continue; }
+      const int32_t depth = a % d.K;
+      Entry en;
+      en.id = env.next_id + (r - lo);
+      en.t_arr = t;
+      en.svc = (int32_t)base_svc[r] * (depth + 1);
+      en.budget = budget[r];
+      en.key = sort_key(p, t, en.budget, en.svc);
+      accepted.push_back(en);
+    }
+    (void)routed;
+    for (const Entry& en : accepted) { ms.backlog += en.svc; ms.enqueued += 1; }
+    // Stable sort of (existing queue ++ newcomers in id order) by key alone:
+    // equal keys keep their order, i.e. older ids first.
+    ms.queue.insert(ms.queue.end(), accepted.begin(), accepted.end());
+    std::stable_sort(ms.queue.begin(), ms.queue.end(),
+                     [](const Entry& a, const Entry& b) { return a.key < b.key; });
+  }
+  for (int32_t r = lo; r < hi; ++r) {
+    if (actions[r] < 0) env.rej_nomodel += 1;
+    else env.hist[actions[r]] += 1;
+  }
+  // S3: per model, fill empty slots s < c_m from the queue head, then advance
+  // every busy slot by one tick of service.
+  for (int m = 0; m < d.M; ++m) {
+    ModelState& ms = env.models[m];
+    for (int s = 0; s < ms.cap && s < d.max_slots; ++s) {
+      Slot& sl = ms.slots[s];
+      if (sl.busy || ms.queue.empty()) continue;
+      Entry en = ms.queue.front();
+      ms.queue.erase(ms.queue.begin());
+      sl.busy = true; sl.id = en.id; sl.t_arr = en.t_arr; sl.rem = en.svc; sl.budget = en.budget;
+      ms.backlog -= en.svc;
+      ms.started += 1;
+      ms.wait_sum += t - en.t_arr;
+    }
+    for (int s = 0; s < d.max_slots; ++s) {
+      Slot& sl = ms.slots[s];
+      if (!sl.busy) continue;
+      sl.rem -= 1;
+      if (sl.rem > 0) continue;
+      const int32_t lat = t - sl.t_arr + 1;
+      // EWMA with alpha = 1/8 in Q8: ewma += floor((256 lat - ewma) / 8)
+      const int64_t delta = (int64_t)lat * 256 - ms.ewma_q8;
+      const int64_t step = delta >= 0 ? delta / 8 : -((-delta + 7) / 8);
+      ms.ewma_q8 = (int32_t)(ms.ewma_q8 + step);
+      ms.completed += 1;
+      ms.lat_sum += lat;
+      ms.slo_met += (lat <= sl.budget) ? 1 : 0;
+      sl = Slot();
+    }
+  }
+  env.next_id += n;
+}
+
+template <class F>
+void for_envs(int E, int threads, F f) {
+  if (threads <= 1 || E < 2) { for (int e = 0; e < E; ++e) f(e); return; }
+  threads = std::min(threads, E);
+  std::vector<std::thread> th;
+  for (int k = 0; k < threads; ++k)
+    th.emplace_back([=, &f] { for (int e = k; e < E; e += threads) f(e); });
+  for (auto& x : th) x.join();
+}
+
+}  // namespace
+
+extern "C" {
+
+// W[l]: fp32 [widths[l] x in_l] row-major; b[l]: fp32 [widths[l]];
+// emb: Q x embed_dim float values; cap: [E*M]; logit_bias: [M] or NULL.
+orc_pool* orc_create(const orc_desc* d, const float* const* W, const float* const* b,
+                     const float* emb, const int32_t* cap, const float* logit_bias) {
+  orc_pool* p = new orc_pool();
+  p->d = *d;
+  p->A = d->M * d->K;
+  int in = d->feat_dim;
+  for (int l = 0; l < d->n_layers; ++l) {
+    const int out = d->widths[l];
+    std::vector<double> w((size_t)out * in), bb(out);
+    for (size_t i = 0; i < w.size(); ++i)
+      w[i] = d->dtype == 1 ? round_bf16((double)W[l][i]) : (double)W[l][i];
+    for (int o = 0; o < out; ++o) bb[o] = (double)b[l][o];
+    p->W.push_back(w);
+    p->b.push_back(bb);
+    in = out;
+  }
+  p->emb.assign(emb, emb + (size_t)d->Q * d->embed_dim);
+  p->logit_bias.assign(d->M, 0.0);
+  if (logit_bias) for (int m = 0; m < d->M; ++m) p->logit_bias[m] = (double)logit_bias[m];
+  p->envs.resize(d->E);
+  for (int e = 0; e < d->E; ++e) {
+    EnvState& env = p->envs[e];
+    env.models.resize(d->M);
+    env.hist.assign(p->A, 0);
+    for (int m = 0; m < d->M; ++m) {
+      env.models[m].slots.resize(d->max_slots);
+      env.models[m].cap = cap[e * d->M + m];
+    }
+  }
+  return p;
+}
+
+void orc_destroy(orc_pool* p) { delete p; }
+
+int32_t orc_tick(const orc_pool* p) { return p->t; }
+int32_t orc_error(const orc_pool* p) { return p->err; }
+void orc_clear_error(orc_pool* p) { p->err = 0; }
+
+void orc_route(orc_pool* p, const int32_t* off, const int32_t* q_idx, const int16_t* budget,
+               double* logits, int32_t* actions, int threads) {
+  std::vector<int32_t> errs(p->d.E, 0);
+  for_envs(p->d.E, threads, [&](int e) {
+    route_env(p, e, off, q_idx, budget, logits, actions, &errs[e]);
+  });
+  for (int32_t x : errs) p->err |= x;
+}
+
+void orc_schedule(orc_pool* p, int32_t n_total, const int32_t* off, const int32_t* q_idx,
+                  const int16_t* budget, const int16_t* base_svc, const int32_t* actions,
+                  int threads) {
+  std::vector<int32_t> errs(p->d.E, 0);
+  for_envs(p->d.E, threads, [&](int e) {
+    schedule_env(p, e, n_total, off, q_idx, budget, base_svc, actions, &errs[e]);
+  });
+  for (int32_t x : errs) p->err |= x;
+  p->t += 1;
+}
+
+// Feature vector of a request of env e as the route step builds it.
+void orc_features(const orc_pool* p, int e, int32_t q_idx, int32_t budget, double* out) {
+  std::vector<double> x;
+  features(p, p->envs[e], q_idx, budget, x);
+  std::copy(x.begin(), x.end(), out);
+}
+
+double orc_round_bf16(double v) { return round_bf16(v); }
+void orc_round_bf16_array(const double* in, double* out, int64_t n) {
+  for (int64_t i = 0; i < n; ++i) out[i] = round_bf16(in[i]);
+}
+
+void orc_set_enabled(orc_pool* p, int e, int m, int v) { p->envs[e].models[m].enabled = v ? 1 : 0; }
+void orc_set_capacity(orc_pool* p, int e, int m, int c) { p->envs[e].models[m].cap = c; }
+
+// State export in the oracle's own layout:
+//   env_i32 [E]      next_id
+//   env_i64 [E*2]    arrived, rej_nomodel
+//   mod_i64 [E*M*13] qlen, busy, ewma_q8, backlog, cap, enabled, rej_overflow,
+//                    enqueued, started, completed, slo_met, lat_sum, wait_sum
+//   slots   [E*M*max_slots*4] id(-1 if free), t_arr, rem, budget
+//   queues  [E*M*qcap*5] key, id, t_arr, svc, budget (zero beyond qlen)
+//   hist    [E*A]
+void orc_read_state(const orc_pool* p, int32_t* env_i32, int64_t* env_i64, int64_t* mod_i64,
+                    int32_t* slots, int32_t* queues, int64_t* hist) {
+  const orc_desc& d = p->d;
+  for (int e = 0; e < d.E; ++e) {
+    const EnvState& env = p->envs[e];
+    env_i32[e] = env.next_id;
+    env_i64[2 * e] = env.arrived;
+    env_i64[2 * e + 1] = env.rej_nomodel;
+    for (int a = 0; a < p->A; ++a) hist[(size_t)e * p->A + a] = env.hist[a];
+    for (int m = 0; m < d.M; ++m) {
+      const ModelState& ms = env.models[m];
+      const size_t em = (size_t)e * d.M + m;
+      int busy = 0;
+      for (const Slot& s : ms.slots) busy += s.busy ? 1 : 0;
+      int64_t* o = mod_i64 + em * 13;
+      o[0] = (int64_t)ms.queue.size(); o[1] = busy; o[2] = ms.ewma_q8; o[3] = ms.backlog;
+      o[4] = ms.cap; o[5] = ms.enabled; o[6] = ms.rej_overflow; o[7] = ms.enqueued;
+      o[8] = ms.started; o[9] = ms.completed; o[10] = ms.slo_met; o[11] = ms.lat_sum;
+      o[12] = ms.wait_sum;
+      for (int s = 0; s < d.max_slots; ++s) {
+        const Slot& sl = ms.slots[s];
+        int32_t* so = slots + (em * d.max_slots + s) * 4;
+        so[0] = sl.busy ? sl.id : -1; so[1] = sl.busy ? sl.t_arr : 0;
+        so[2] = sl.busy ? sl.rem : 0; so[3] = sl.busy ? sl.budget : 0;
+      }
+      int32_t* qo = queues + em * (size_t)d.qcap * 5;
+      std::memset(qo, 0, sizeof(int32_t) * (size_t)d.qcap * 5);
+      for (size_t i = 0; i < ms.queue.size(); ++i) {
+        const Entry& en = ms.queue[i];
+        qo[i * 5 + 0] = en.key; qo[i * 5 + 1] = en.id; qo[i * 5 + 2] = en.t_arr;
+        qo[i * 5 + 3] = en.svc; qo[i * 5 + 4] = en.budget;
+      }
+    }
+  }
+}
+
+}  // extern "C"

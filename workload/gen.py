@@ -1,0 +1,125 @@
+"""Seeded synthetic inputs for the route-and-schedule tick.
+
+This module only draws random inputs: policy weights, service capacities, the
+query-embedding table, Poisson arrival counts and per-request fields. It holds
+none of the tick's arithmetic (no features, no policy evaluation, no keys, no
+queue logic), so the oracle and the GPU path can both consume it without
+sharing any part of the method.
+
+Streams: numpy.random.default_rng(SeedSequence([seed, cfg index, stream]))
+  0 weights, 1 capacities, 2 embedding table, 3 Poisson counts [T, E],
+  4 request fields, one sub-stream per tick: SeedSequence([seed, idx, 4, t]).
+
+Inputs stand in for the paper's workloads (Sec. 5.1): the paper's LLM-quality
+benchmarks are replaced by N(0,1) query embeddings (Sec. 3 uses Sentence-BERT
+vectors), its req/min Poisson rates by per-env Poisson(lam) per tick.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+from . import configs as _configs
+
+
+def _rng(cfg: dict, seed: int, *stream: int) -> np.random.Generator:
+    return np.random.default_rng(np.random.SeedSequence([seed, cfg["index"], *stream]))
+
+
+def table_rows(cfg: dict) -> int:
+    """Embedding-table rows: min(expected total requests, 2^22), at least 16."""
+    total = int(math.ceil(cfg["lam"] * cfg["E"] * cfg["T"]))
+    return max(16, min(total, _configs.Q_CAP_ROWS))
+
+
+def weights(cfg: dict, seed: int = 0, bias_scale: float = 0.0):
+    """Glorot-uniform fp32 weights [out, in] per layer and fp32 biases.
+
+    Biases are U(-bias_scale, bias_scale) (0 in benchmarks, 0.1 in tests)."""
+    rng = _rng(cfg, seed, 0)
+    Ws, bs = [], []
+    fan_in = cfg["feat_dim"]
+    for out in cfg["widths"]:
+        lim = math.sqrt(6.0 / (fan_in + out))
+        Ws.append(rng.uniform(-lim, lim, size=(out, fan_in)).astype(np.float32))
+        if bias_scale > 0:
+            bs.append(rng.uniform(-bias_scale, bias_scale, size=out).astype(np.float32))
+        else:
+            bs.append(np.zeros(out, np.float32))
+        fan_in = out
+    return Ws, bs
+
+
+def capacities(cfg: dict, seed: int = 0) -> np.ndarray:
+    """Service slots c_m per (env, model): int32 [E, M], uniform in [cap_lo, cap_hi]."""
+    rng = _rng(cfg, seed, 1)
+    return rng.integers(cfg["cap_lo"], cfg["cap_hi"] + 1,
+                        size=(cfg["E"], cfg["M"])).astype(np.int32)
+
+
+def embedding(cfg: dict, seed: int = 0, rows: int | None = None):
+    """Query-embedding table [Q, E_d] of N(0,1) values.
+
+    Returns (table, values): for fp32 configs both are the same float32 array;
+    for bf16 configs `table` holds the bf16 bit patterns (uint16, rounded to
+    nearest-even by torch's conversion) and `values` the float32 value of each."""
+    Q = table_rows(cfg) if rows is None else rows
+    rng = _rng(cfg, seed, 2)
+    x = rng.standard_normal(size=(Q, cfg["embed_dim"]), dtype=np.float32)
+    if cfg["dtype"] == "f32":
+        return x, x
+    import torch
+    t = torch.from_numpy(x).to(torch.bfloat16)
+    bits = t.view(torch.int16).numpy().view(np.uint16).copy()
+    vals = t.to(torch.float32).numpy()
+    return bits, vals
+
+
+def counts(cfg: dict, seed: int = 0) -> np.ndarray:
+    """Poisson(lam) arrivals per (tick, env): int32 [T, E]."""
+    rng = _rng(cfg, seed, 3)
+    c = rng.poisson(cfg["lam"], size=(cfg["T"], cfg["E"]))
+    return np.minimum(c, cfg["max_arrivals"]).astype(np.int32)
+
+
+def tick(cfg: dict, seed: int, t: int, counts_row: np.ndarray, Q: int):
+    """Arrival records of tick t for all envs, in env-major (CSR) order.
+
+    Returns dict(offsets int32 [E+1], q_idx int32 [n], budget int16 [n],
+    base_svc int16 [n]). Within an env, records are in arrival order."""
+    rng = _rng(cfg, seed, 4, t)
+    n = int(counts_row.sum())
+    offsets = np.zeros(len(counts_row) + 1, np.int32)
+    np.cumsum(counts_row, out=offsets[1:])
+    q_idx = rng.integers(0, Q, size=n).astype(np.int32)
+    budget = rng.integers(cfg["budget_lo"], cfg["budget_hi"] + 1, size=n).astype(np.int16)
+    ln = rng.lognormal(cfg["svc_mu"], cfg["svc_sigma"], size=n)
+    base_svc = np.minimum(np.ceil(ln), _configs.SVC_MAX).astype(np.int16)
+    base_svc = np.maximum(base_svc, 1).astype(np.int16)
+    return dict(offsets=offsets, q_idx=q_idx, budget=budget, base_svc=base_svc)
+
+
+def subset(arr: dict, e0: int, e1: int) -> dict:
+    """The records of envs [e0, e1) of one tick, offsets rebased to 0."""
+    off = arr["offsets"]
+    lo, hi = int(off[e0]), int(off[e1])
+    return dict(offsets=(off[e0:e1 + 1] - lo).astype(np.int32),
+                q_idx=arr["q_idx"][lo:hi], budget=arr["budget"][lo:hi],
+                base_svc=arr["base_svc"][lo:hi])
+
+
+def logit_bias(cfg: dict):
+    """Per-model logit bias -s*ln(m+1) as float32 [M], or None."""
+    s = cfg.get("zipf_s")
+    if not s:
+        return None
+    return np.array([-s * math.log(m + 1) for m in range(cfg["M"])], np.float32)
+
+
+def trace(cfg: dict, seed: int = 0, Q: int | None = None, T: int | None = None):
+    """All ticks of a run: list of per-tick dicts (small configs only)."""
+    Q = table_rows(cfg) if Q is None else Q
+    cnt = counts(cfg, seed)
+    T = cfg["T"] if T is None else T
+    return [tick(cfg, seed, t, cnt[t], Q) for t in range(T)]
