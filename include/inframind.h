@@ -1,0 +1,219 @@
+/* inframind.h -- C ABI of the batched route-and-schedule tick on MI355X.
+ *
+ * A pool holds E independent simulated serving pools ("envs"), each with M
+ * models (LLM services) that own a request queue and c_m service slots.
+ * Every tick, for every env, in parallel on the GPU:
+ *   route    -- each arriving request (one agent step) gets a feature vector
+ *               from its query embedding, its budget and the env's live load
+ *               (Sec. 3 "State", Eq. 1: query embedding, remaining budget,
+ *               per-model queue depth, end-to-end latency, KV-cache use), a
+ *               policy MLP scores all M*K joint actions and a masked argmax
+ *               picks one (Sec. 3 "Action": model = a / K, depth = a % K;
+ *               Sec. 4.2 executor, deployed greedily);
+ *   schedule -- routed requests are admitted to their model's queue, which is
+ *               kept ordered by an integer key (Sec. 4.3: deadline
+ *               t_arrive + budget, earliest first; here by default the latest
+ *               start time = deadline - service time, ties by request id);
+ *               each model fills its free service slots from the queue head,
+ *               advances service by one tick and records completions (bounded
+ *               concurrency as vLLM's max_num_seqs, Table 5; latency signal
+ *               an exponential moving average, Sec. 5.4).
+ *
+ * Conventions for every call:
+ *   - Pointers marked "device" are device memory of the pool's GPU; "host"
+ *     pointers are ordinary host memory. Caller-owned buffers must stay valid
+ *     until the stream work that uses them has finished.
+ *   - `stream` is a hipStream_t (NULL = the default stream). All tick calls
+ *     are stream-ordered and asynchronous; only im_read_state, im_write_state,
+ *     im_get_error and im_pool_create/im_destroy synchronise.
+ *   - Invalid arguments return IM_EINVAL synchronously and change nothing.
+ *     Data-dependent errors found on the device (see IM_ERR_*) set a sticky
+ *     error word and leave the offending env's state untouched for that tick;
+ *     they are reported by im_get_error.
+ *   - A pool is not thread-safe; distinct pools are independent.
+ */
+#ifndef INFRAMIND_H
+#define INFRAMIND_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  IM_OK = 0,
+  IM_EINVAL = -1,      /* bad argument (nothing changed)                 */
+  IM_ENOMEM = -2,      /* device allocation failed                       */
+  IM_EHIP = -3,        /* a HIP runtime call or kernel launch failed     */
+  IM_EDEVICE = -4,     /* sticky device error word is non-zero           */
+  IM_ESTATE = -5,      /* im_write_state given an inconsistent snapshot  */
+  IM_EUNSUPPORTED = -6 /* valid description with no kernel for its shape */
+} im_status;
+
+typedef enum { IM_F32 = 0, IM_BF16 = 1 } im_dtype;
+
+/* Queue order (Sec. 4.3). SLACK: key = t_arrive + budget - svc (latest start
+ * time; ordering by it orders by slack at every tick). DEADLINE: key =
+ * t_arrive + budget (the paper's EDF). FCFS: key = t_arrive (the baseline of
+ * the Table 3 ablation). Ties are broken by request id in every mode. */
+typedef enum { IM_KEY_SLACK = 0, IM_KEY_DEADLINE = 1, IM_KEY_FCFS = 2 } im_key_mode;
+
+/* Bits of the sticky device error word. */
+#define IM_ERR_QIDX   1   /* q_idx outside [0, n_queries)                          */
+#define IM_ERR_COUNT  2   /* offsets not a CSR of n_total rows, or n_e > max       */
+#define IM_ERR_BUDGET 4   /* budget < 1                                            */
+#define IM_ERR_SVC    8   /* base_svc outside [1, IM_SVC_MAX]                      */
+#define IM_ERR_ACTION 16  /* action outside [-1, M*K)                              */
+
+/* Limits of this build. */
+#define IM_SVC_MAX     4095   /* largest base service time (ticks)              */
+#define IM_MAX_MODELS  32
+#define IM_MAX_DEPTHS  16
+#define IM_MAX_ACTIONS 64     /* M*K                                            */
+#define IM_MAX_SLOTS   8
+#define IM_MAX_QCAP    16384
+#define IM_MAX_FEAT    512
+
+/* Pool description.
+ *   n_envs        E >= 1 independent envs
+ *   n_models      M in [1, IM_MAX_MODELS]; n_depths K in [1, IM_MAX_DEPTHS]; M*K <= 64
+ *   queue_cap     per-(env, model) queue capacity in [1, IM_MAX_QCAP]
+ *   max_slots     slots per model in [1, IM_MAX_SLOTS]; capacities lie in [0, max_slots]
+ *   embed_dim     E_d, query-embedding width (>= 1)
+ *   feat_dim      D_in >= E_d + 4M + 1, <= IM_MAX_FEAT. Feature layout:
+ *                 [embedding (E_d) | queue depth of every model (M) | busy/c_m (M) |
+ *                  latency EWMA/(256 B) (M) | backlog/(c_m B) (M) | budget/B | 0...]
+ *                 with B = budget_max and every reciprocal rounded once to fp32.
+ *   n_layers      2 or 3; widths[0..n_layers-1] are the layer output widths,
+ *                 hidden widths equal, in {32, 64, 128, 256, 512} (512 bf16 only),
+ *                 widths[n_layers-1] == M*K
+ *   dtype         IM_F32: fp32 weights and activations; IM_BF16: bf16 weights,
+ *                 inputs and hidden activations (round to nearest even), fp32
+ *                 accumulation, biases and logits
+ *   key_mode      im_key_mode
+ *   max_arrivals_per_env_tick  largest n_e accepted (>= 1)
+ *   budget_max    B >= 1, normaliser of the budget and latency features */
+typedef struct {
+  int32_t n_envs, n_models, n_depths, queue_cap, max_slots;
+  int32_t embed_dim, feat_dim, n_layers;
+  int32_t widths[4];
+  int32_t dtype, key_mode, max_arrivals_per_env_tick, budget_max;
+} im_pool_desc;
+
+/* The arrivals of ONE tick, in env-major CSR order (all device memory).
+ *   offsets  [E+1]  rows of env e are [offsets[e], offsets[e+1]); offsets[0] = 0,
+ *                   offsets[E] = n_total
+ *   q_idx    [n]    row of the query-embedding table
+ *   budget   [n]    time budget in ticks (>= 1)
+ *   base_svc [n]    service time at depth 0 in ticks; at depth d it is base_svc*(d+1)
+ * Within an env, rows are in arrival order; request ids are assigned in that
+ * order, continuing from the env's next_id. */
+typedef struct {
+  const int32_t* offsets;
+  const int32_t* q_idx;
+  const int16_t* budget;
+  const int16_t* base_svc;
+  int32_t n_total;
+} im_arrivals;
+
+typedef struct im_pool im_pool;
+
+/* Create a pool (Sec. 4.2 policy weights, Sec. 4.3 queues, all state zero:
+ * empty queues and slots, tick 0, next_id 0, enabled = 1).
+ *   W[l]        host fp32 [widths[l] x in_l] row-major (in_0 = feat_dim);
+ *               copied (and rounded to bf16 for IM_BF16) into the pool
+ *   b[l]        host fp32 [widths[l]]; copied
+ *   emb         device [n_queries x embed_dim], fp32 (IM_F32) or bf16 bits
+ *               (IM_BF16), row-major; BORROWED: must outlive the pool
+ *   capacity    host int32 [E*M], c_m per (env, model) in [0, max_slots]
+ *   logit_bias  host fp32 [M] added to the logits of model m's actions, or NULL
+ * Returns IM_EINVAL / IM_EUNSUPPORTED / IM_ENOMEM / IM_EHIP on failure
+ * (*out untouched). Synchronises `stream`. */
+im_status im_pool_create(const im_pool_desc* desc, const float* const* W, const float* const* b,
+                         const void* emb, int64_t n_queries, const int32_t* capacity,
+                         const float* logit_bias, void* stream, im_pool** out);
+
+/* Route one tick (Sec. 3 Eq. 1 features, Sec. 4.2 policy, masked argmax).
+ * Reads the state left by the previous tick; does not change the state.
+ *   actions  device int32 [n_total] out: chosen joint action, -1 when no
+ *            action is valid (model disabled, c_m = 0 or its queue full) or
+ *            the row's q_idx is out of range (IM_ERR_QIDX is raised)
+ *   logits   device fp32 [n_total x M*K] out (post logit-bias, pre-mask), or NULL
+ * Argmax ties go to the lowest action index. */
+im_status im_route(im_pool* pool, const im_arrivals* arr, int32_t* actions, float* logits,
+                   void* stream);
+
+/* Schedule one tick with the given actions (any actions in [-1, M*K), e.g.
+ * sampled ones): admission in id order with tail-drop beyond queue_cap, keys
+ * per key_mode, service of every model, accounting; then the tick advances.
+ *   actions  device int32 [n_total] */
+im_status im_schedule(im_pool* pool, const im_arrivals* arr, const int32_t* actions, void* stream);
+
+/* im_route followed by im_schedule with the actions it chose.
+ *   actions_out  device int32 [n_total] receiving the actions, or NULL
+ *                (then a pool-owned buffer is used) */
+im_status im_tick(im_pool* pool, const im_arrivals* arr, int32_t* actions_out, void* stream);
+
+/* Free every resource of the pool (synchronises). NULL is ignored. */
+void im_destroy(im_pool* pool);
+
+/* ---- state snapshot (host memory; synchronises) -------------------------- */
+
+typedef struct {            /* a queued request, in service order             */
+  int32_t key, id, t_arr;   /* sort key, per-env request id, arrival tick     */
+  uint16_t svc, budget;     /* service time, budget (ticks)                   */
+} im_entry;
+
+typedef struct {            /* a service slot; id = -1 when free              */
+  int32_t id, t_arr, rem, budget;
+} im_slot;
+
+typedef struct {
+  int32_t qlen, busy, ewma_q8, backlog, capacity, enabled, _pad0, _pad1;
+  int64_t rej_overflow, enqueued, started, completed, slo_met, lat_sum, wait_sum, _pad2;
+} im_model_state;
+
+typedef struct {
+  int64_t arrived, rej_nomodel;
+  int32_t next_id, _pad;
+} im_env_state;
+
+/* Copy the state of envs [env_begin, env_begin + env_count) to host memory.
+ *   tick    out: ticks completed so far
+ *   envs    [count], models [count*M], slots [count*M*max_slots],
+ *   queues  [count*M*queue_cap] (entries beyond qlen are zeroed),
+ *   hist    [count*M*K] routed requests per action
+ * Any output pointer may be NULL to skip it. */
+im_status im_read_state(im_pool* pool, int32_t env_begin, int32_t env_count, int32_t* tick,
+                        im_env_state* envs, im_model_state* models, im_slot* slots,
+                        im_entry* queues, int64_t* hist);
+
+/* Overwrite the state of envs [env_begin, env_begin + env_count) and the tick
+ * from host memory (same layout as im_read_state; all pointers required).
+ * Returns IM_ESTATE without changing anything if the snapshot is
+ * inconsistent (unsorted queue, qlen/busy/backlog not matching, bounds). */
+im_status im_write_state(im_pool* pool, int32_t env_begin, int32_t env_count, int32_t tick,
+                         const im_env_state* envs, const im_model_state* models,
+                         const im_slot* slots, const im_entry* queues, const int64_t* hist);
+
+/* Host knobs (stream-ordered): take a model out of routing, or change its
+ * number of service slots (requests in slots >= the new capacity finish but
+ * are not replaced). */
+im_status im_set_enabled(im_pool* pool, int32_t env, int32_t model, int32_t enabled, void* stream);
+im_status im_set_capacity(im_pool* pool, int32_t env, int32_t model, int32_t capacity,
+                          void* stream);
+
+/* Sticky device error word (IM_ERR_* bits). Synchronises. Returns IM_EDEVICE
+ * when non-zero. im_clear_error zeroes it. */
+im_status im_get_error(im_pool* pool, int32_t* bits);
+im_status im_clear_error(im_pool* pool);
+
+/* Description of the last failing call on this pool (or of the last failed
+ * im_pool_create when pool is NULL). Never NULL. */
+const char* im_last_error(const im_pool* pool);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* INFRAMIND_H */

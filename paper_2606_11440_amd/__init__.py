@@ -1,0 +1,76 @@
+"""MI355X-native batched route-and-schedule tick (InfraMind's executor and
+budget-aware queues, vectorised over independent serving pools).
+
+The compute path is libinframind.so (HIP kernels for gfx950 behind the C ABI of
+include/inframind.h); this package only marshals arguments. Importing it does
+not load the library; the first call does, and fails loudly if it is missing."""
+from __future__ import annotations
+
+from . import _lib
+from ._lib import (EXPORTED, IMError, im_clear_error, im_destroy, im_get_error,  # noqa: F401
+                   im_last_error, im_pool_create, im_read_state, im_route, im_schedule,
+                   im_set_capacity, im_set_enabled, im_tick, im_write_state, make_arrivals,
+                   make_desc)
+
+
+def device_arrivals(arr: dict, device="cuda"):
+    """Upload one tick's numpy arrivals (offsets, q_idx, budget, base_svc)."""
+    import torch
+    t = lambda x, dt: torch.as_tensor(x, dtype=dt).to(device)  # noqa: E731
+    return make_arrivals(t(arr["offsets"], torch.int32), t(arr["q_idx"], torch.int32),
+                         t(arr["budget"], torch.int16), t(arr["base_svc"], torch.int16))
+
+
+class Pool:
+    """A pool of E envs on the current GPU, built from a workload config.
+
+    W, b: host float32 weights/biases per layer; emb: device tensor holding the
+    embedding table (float32, or bf16 bits as int16/uint16 for bf16 configs),
+    kept alive by this object; cap: int32 [E, M]; logit_bias: float32 [M] or None."""
+
+    def __init__(self, cfg, W, b, emb, cap, logit_bias=None, stream=None):
+        self.cfg = cfg
+        self.E, self.M, self.K = cfg["E"], cfg["M"], cfg["K"]
+        self.A, self.S, self.qcap = cfg["M"] * cfg["K"], cfg["max_slots"], cfg["qcap"]
+        self.emb = emb
+        self.desc = make_desc(cfg)
+        self.h = im_pool_create(self.desc, W, b, emb, emb.shape[0], cap, logit_bias, stream)
+
+    def route(self, arr, actions, logits=None, stream=None):
+        im_route(self.h, arr, actions, logits, stream)
+
+    def schedule(self, arr, actions, stream=None):
+        im_schedule(self.h, arr, actions, stream)
+
+    def tick(self, arr, actions_out=None, stream=None):
+        im_tick(self.h, arr, actions_out, stream)
+
+    def state(self, env_begin=0, env_count=None):
+        n = self.E - env_begin if env_count is None else env_count
+        return im_read_state(self.h, env_begin, n, self.M, self.A, self.S, self.qcap)
+
+    def write_state(self, env_begin, s):
+        im_write_state(self.h, env_begin, s)
+
+    def set_enabled(self, e, m, v, stream=None):
+        im_set_enabled(self.h, e, m, v, stream)
+
+    def set_capacity(self, e, m, c, stream=None):
+        im_set_capacity(self.h, e, m, c, stream)
+
+    def error(self) -> int:
+        return im_get_error(self.h)
+
+    def clear_error(self):
+        im_clear_error(self.h)
+
+    def close(self):
+        if getattr(self, "h", None):
+            im_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,257 @@
+"""ctypes binding of libinframind (include/inframind.h): argument marshalling
+only. Every step of the tick runs in the library's HIP kernels; torch tensors
+merely provide device memory and the current HIP stream.
+
+The functions keep the C names (im_pool_create, im_route, im_schedule,
+im_tick, im_destroy, im_read_state, im_write_state, im_set_enabled,
+im_set_capacity, im_get_error, im_clear_error, im_last_error)."""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libinframind.so")
+
+IM_OK, IM_EINVAL, IM_ENOMEM, IM_EHIP, IM_EDEVICE, IM_ESTATE, IM_EUNSUPPORTED = 0, -1, -2, -3, -4, -5, -6
+IM_F32, IM_BF16 = 0, 1
+KEY_MODES = {"slack": 0, "deadline": 1, "fcfs": 2}
+IM_ERR_QIDX, IM_ERR_COUNT, IM_ERR_BUDGET, IM_ERR_SVC, IM_ERR_ACTION = 1, 2, 4, 8, 16
+
+EXPORTED = ("im_pool_create", "im_route", "im_schedule", "im_tick", "im_destroy",
+            "im_read_state", "im_write_state", "im_set_enabled", "im_set_capacity",
+            "im_get_error", "im_clear_error", "im_last_error")
+
+
+class ImPoolDesc(ctypes.Structure):
+    _fields_ = [("n_envs", ctypes.c_int32), ("n_models", ctypes.c_int32),
+                ("n_depths", ctypes.c_int32), ("queue_cap", ctypes.c_int32),
+                ("max_slots", ctypes.c_int32), ("embed_dim", ctypes.c_int32),
+                ("feat_dim", ctypes.c_int32), ("n_layers", ctypes.c_int32),
+                ("widths", ctypes.c_int32 * 4), ("dtype", ctypes.c_int32),
+                ("key_mode", ctypes.c_int32), ("max_arrivals_per_env_tick", ctypes.c_int32),
+                ("budget_max", ctypes.c_int32)]
+
+
+class ImArrivals(ctypes.Structure):
+    _fields_ = [("offsets", ctypes.c_void_p), ("q_idx", ctypes.c_void_p),
+                ("budget", ctypes.c_void_p), ("base_svc", ctypes.c_void_p),
+                ("n_total", ctypes.c_int32)]
+
+
+ENTRY_DT = np.dtype([("key", "<i4"), ("id", "<i4"), ("t_arr", "<i4"), ("svc", "<u2"),
+                     ("budget", "<u2")])
+SLOT_DT = np.dtype([("id", "<i4"), ("t_arr", "<i4"), ("rem", "<i4"), ("budget", "<i4")])
+MODEL_DT = np.dtype([("qlen", "<i4"), ("busy", "<i4"), ("ewma_q8", "<i4"), ("backlog", "<i4"),
+                     ("capacity", "<i4"), ("enabled", "<i4"), ("_p0", "<i4"), ("_p1", "<i4"),
+                     ("rej_overflow", "<i8"), ("enqueued", "<i8"), ("started", "<i8"),
+                     ("completed", "<i8"), ("slo_met", "<i8"), ("lat_sum", "<i8"),
+                     ("wait_sum", "<i8"), ("_p2", "<i8")])
+ENV_DT = np.dtype([("arrived", "<i8"), ("rej_nomodel", "<i8"), ("next_id", "<i4"), ("_p", "<i4")])
+assert ENTRY_DT.itemsize == 16 and SLOT_DT.itemsize == 16
+assert MODEL_DT.itemsize == 96 and ENV_DT.itemsize == 24
+
+_lib = None
+
+
+def load() -> ctypes.CDLL:
+    """Load the in-tree libinframind.so; fails loudly when it is missing."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                           "(hipcc, gfx950); there is no fallback path")
+    L = ctypes.CDLL(LIB_PATH)
+    P, I32, I64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    L.im_pool_create.argtypes = [ctypes.POINTER(ImPoolDesc), P, P, P, I64, P, P, P,
+                                 ctypes.POINTER(P)]
+    L.im_route.argtypes = [P, ctypes.POINTER(ImArrivals), P, P, P]
+    L.im_schedule.argtypes = [P, ctypes.POINTER(ImArrivals), P, P]
+    L.im_tick.argtypes = [P, ctypes.POINTER(ImArrivals), P, P]
+    L.im_destroy.argtypes = [P]
+    L.im_destroy.restype = None
+    L.im_read_state.argtypes = [P, I32, I32, ctypes.POINTER(I32), P, P, P, P, P]
+    L.im_write_state.argtypes = [P, I32, I32, I32, P, P, P, P, P]
+    L.im_set_enabled.argtypes = [P, I32, I32, I32, P]
+    L.im_set_capacity.argtypes = [P, I32, I32, I32, P]
+    L.im_get_error.argtypes = [P, ctypes.POINTER(I32)]
+    L.im_clear_error.argtypes = [P]
+    L.im_last_error.argtypes = [P]
+    L.im_last_error.restype = ctypes.c_char_p
+    for name in EXPORTED:
+        if name not in ("im_destroy", "im_last_error"):
+            getattr(L, name).restype = ctypes.c_int
+    _lib = L
+    return L
+
+
+class IMError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__(f"status {status}: {msg}")
+        self.status = status
+
+
+def _check(status, pool=None):
+    if status != IM_OK:
+        raise IMError(status, load().im_last_error(pool).decode())
+    return status
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    return ctypes.c_void_p(int(stream))
+
+
+def _dptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _hptr(a):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def make_desc(cfg: dict) -> ImPoolDesc:
+    d = ImPoolDesc()
+    d.n_envs, d.n_models, d.n_depths = cfg["E"], cfg["M"], cfg["K"]
+    d.queue_cap, d.max_slots = cfg["qcap"], cfg["max_slots"]
+    d.embed_dim, d.feat_dim = cfg["embed_dim"], cfg["feat_dim"]
+    d.n_layers = len(cfg["widths"])
+    for i, w in enumerate(cfg["widths"]):
+        d.widths[i] = w
+    d.dtype = IM_BF16 if cfg["dtype"] == "bf16" else IM_F32
+    d.key_mode = KEY_MODES[cfg["key_mode"]]
+    d.max_arrivals_per_env_tick = cfg["max_arrivals"]
+    d.budget_max = cfg["budget_max"]
+    return d
+
+
+def make_arrivals(offsets, q_idx, budget, base_svc) -> ImArrivals:
+    """Arrivals of one tick from device tensors (int32, int32, int16, int16)."""
+    a = ImArrivals()
+    a.offsets = offsets.data_ptr()
+    a.q_idx = q_idx.data_ptr() if q_idx.numel() else None
+    a.budget = budget.data_ptr() if budget.numel() else None
+    a.base_svc = base_svc.data_ptr() if base_svc.numel() else None
+    a.n_total = int(q_idx.numel())
+    a._keep = (offsets, q_idx, budget, base_svc)
+    return a
+
+
+def im_pool_create(desc: ImPoolDesc, W, b, emb, n_queries: int, capacity, logit_bias=None,
+                   stream=None) -> ctypes.c_void_p:
+    """W, b: lists of host float32 arrays; emb: device tensor (borrowed: the
+    caller keeps it alive); capacity: host int32 [E*M]."""
+    L = load()
+    Wc = [np.ascontiguousarray(w, np.float32) for w in W]
+    bc = [np.ascontiguousarray(x, np.float32) for x in b]
+    Wp = (ctypes.c_void_p * len(Wc))(*[w.ctypes.data for w in Wc])
+    bp = (ctypes.c_void_p * len(bc))(*[x.ctypes.data for x in bc])
+    cap = np.ascontiguousarray(capacity, np.int32).reshape(-1)
+    lb = None if logit_bias is None else np.ascontiguousarray(logit_bias, np.float32)
+    out = ctypes.c_void_p()
+    _check(L.im_pool_create(ctypes.byref(desc), ctypes.cast(Wp, ctypes.c_void_p),
+                            ctypes.cast(bp, ctypes.c_void_p), _dptr(emb), int(n_queries),
+                            _hptr(cap), None if lb is None else _hptr(lb), _stream(stream),
+                            ctypes.byref(out)))
+    return out
+
+
+def im_route(pool, arr: ImArrivals, actions, logits=None, stream=None):
+    _check(load().im_route(pool, ctypes.byref(arr), _dptr(actions), _dptr(logits),
+                           _stream(stream)), pool)
+
+
+def im_schedule(pool, arr: ImArrivals, actions, stream=None):
+    _check(load().im_schedule(pool, ctypes.byref(arr), _dptr(actions), _stream(stream)), pool)
+
+
+def im_tick(pool, arr: ImArrivals, actions_out=None, stream=None):
+    _check(load().im_tick(pool, ctypes.byref(arr), _dptr(actions_out), _stream(stream)), pool)
+
+
+def im_destroy(pool):
+    if pool:
+        load().im_destroy(pool)
+
+
+def im_set_enabled(pool, env, model, enabled, stream=None):
+    _check(load().im_set_enabled(pool, env, model, int(bool(enabled)), _stream(stream)), pool)
+
+
+def im_set_capacity(pool, env, model, capacity, stream=None):
+    _check(load().im_set_capacity(pool, env, model, int(capacity), _stream(stream)), pool)
+
+
+def im_get_error(pool) -> int:
+    bits = ctypes.c_int32(0)
+    st = load().im_get_error(pool, ctypes.byref(bits))
+    if st not in (IM_OK, IM_EDEVICE):
+        _check(st, pool)
+    return int(bits.value)
+
+
+def im_clear_error(pool):
+    _check(load().im_clear_error(pool), pool)
+
+
+def im_last_error(pool=None) -> str:
+    return load().im_last_error(pool).decode()
+
+
+def im_read_state(pool, env_begin: int, env_count: int, M: int, A: int, S: int, qcap: int) -> dict:
+    """Snapshot of envs [env_begin, env_begin + env_count) as numpy arrays in
+    the layout the tests compare (same keys as the oracle's snapshot)."""
+    E = env_count
+    envs = np.zeros(E, ENV_DT)
+    models = np.zeros(E * M, MODEL_DT)
+    slots = np.zeros(E * M * S, SLOT_DT)
+    queues = np.zeros(E * M * qcap, ENTRY_DT)
+    hist = np.zeros(E * A, np.int64)
+    tick = ctypes.c_int32(0)
+    _check(load().im_read_state(pool, env_begin, env_count, ctypes.byref(tick), _hptr(envs),
+                                _hptr(models), _hptr(slots), _hptr(queues), _hptr(hist)), pool)
+    md = models.reshape(E, M)
+    q = queues.reshape(E, M, qcap)
+    qarr = np.stack([q["key"], q["id"], q["t_arr"], q["svc"].astype(np.int32),
+                     q["budget"].astype(np.int32)], axis=-1).astype(np.int32)
+    sl = slots.reshape(E, M, S)
+    sarr = np.stack([sl["id"], sl["t_arr"], sl["rem"], sl["budget"]], axis=-1).astype(np.int32)
+    out = dict(t=int(tick.value), next_id=envs["next_id"].copy(), arrived=envs["arrived"].copy(),
+               rej_nomodel=envs["rej_nomodel"].copy(), slots=sarr, queues=qarr,
+               hist=hist.reshape(E, A))
+    for k, f in (("qlen", "qlen"), ("busy", "busy"), ("ewma", "ewma_q8"), ("backlog", "backlog"),
+                 ("cap", "capacity"), ("enabled", "enabled"), ("rej_overflow", "rej_overflow"),
+                 ("enqueued", "enqueued"), ("started", "started"), ("completed", "completed"),
+                 ("slo_met", "slo_met"), ("lat_sum", "lat_sum"), ("wait_sum", "wait_sum")):
+        out[k] = md[f].astype(np.int64)
+    return out
+
+
+def im_write_state(pool, env_begin: int, s: dict):
+    """Inverse of im_read_state (same dict layout)."""
+    E, M = s["qlen"].shape
+    A = s["hist"].shape[1]
+    S = s["slots"].shape[2]
+    qcap = s["queues"].shape[2]
+    envs = np.zeros(E, ENV_DT)
+    envs["arrived"], envs["rej_nomodel"], envs["next_id"] = s["arrived"], s["rej_nomodel"], s["next_id"]
+    models = np.zeros((E, M), MODEL_DT)
+    for k, f in (("qlen", "qlen"), ("busy", "busy"), ("ewma", "ewma_q8"), ("backlog", "backlog"),
+                 ("cap", "capacity"), ("enabled", "enabled"), ("rej_overflow", "rej_overflow"),
+                 ("enqueued", "enqueued"), ("started", "started"), ("completed", "completed"),
+                 ("slo_met", "slo_met"), ("lat_sum", "lat_sum"), ("wait_sum", "wait_sum")):
+        models[f] = s[k]
+    slots = np.zeros((E, M, S), SLOT_DT)
+    for i, f in enumerate(("id", "t_arr", "rem", "budget")):
+        slots[f] = s["slots"][..., i]
+    queues = np.zeros((E, M, qcap), ENTRY_DT)
+    for i, f in enumerate(("key", "id", "t_arr", "svc", "budget")):
+        queues[f] = s["queues"][..., i]
+    hist = np.ascontiguousarray(s["hist"], np.int64)
+    _check(load().im_write_state(pool, env_begin, E, int(s["t"]), _hptr(envs), _hptr(models),
+                                 _hptr(slots), _hptr(queues), _hptr(hist)), pool)

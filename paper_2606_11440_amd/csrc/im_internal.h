@@ -1,0 +1,78 @@
+// Internal device data layout and kernel argument blocks of libinframind.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "inframind.h"
+
+namespace im {
+
+// Per-(env, model) state, 64 bytes. The queue of a model is split into a
+// sorted "front" (the smallest keys, at most kFront entries, occupying
+// front[fh .. fh+fn)) and an unsorted "pool" of the rest (pool[0 .. P)).
+// Every front key is smaller than every pool key; qlen = fn + P.
+struct alignas(64) ModelRec {
+  int32_t qlen, busy, ewma, backlog;   // snapshot fields read by the route step
+  int32_t cap, enabled, fh, fn;
+  int32_t P, next_id, pad0, pad1;
+  int32_t pad2, pad3, pad4, pad5;
+};
+static_assert(sizeof(ModelRec) == 64, "ModelRec layout");
+
+constexpr int kFront = 64;       // front capacity (one entry per lane)
+
+// Counter slots per (env, model), int64.
+enum { C_REJ_OVERFLOW = 0, C_ENQUEUED, C_STARTED, C_COMPLETED, C_SLO_MET, C_LAT_SUM,
+       C_WAIT_SUM, C_NUM = 8 };
+
+// Queue entry in device memory: {key, id, t_arr, svc | budget << 16}.
+// Slot in device memory: {id (-1 free), t_arr, rem, budget}.
+
+struct RouteArgs {
+  const int32_t* offsets;
+  const int32_t* q_idx;
+  const int16_t* budget;
+  int32_t n_total;
+  int32_t E, M, K, A;
+  int32_t embed_dim, feat_dim, k1;    // k1: layer-1 K steps (bf16: 16-wide, f32: 2-wide)
+  int32_t qcap;
+  int64_t Q;
+  const void* emb;
+  const void* W[3];                   // packed weights per layer
+  const float* bias[3];               // packed biases per layer (D-register order)
+  const ModelRec* ms;
+  float inv_qcap, inv_lat, inv_bud;
+  const float* inv_tab;               // device [2*(IM_MAX_SLOTS+1)]: 1/max(c,1), then
+                                      // 1/(max(c,1)*budget_max), for c = 0..IM_MAX_SLOTS
+  int32_t* actions;
+  float* logits;
+  int32_t* err;
+};
+
+struct SchedArgs {
+  const int32_t* offsets;
+  const int32_t* q_idx;
+  const int16_t* budget;
+  const int16_t* base_svc;
+  const int32_t* actions;
+  int32_t n_total;
+  int32_t E, M, K, A, S, qcap, max_arrivals, key_mode;
+  int64_t Q;
+  int32_t t;
+  ModelRec* ms;
+  int64_t* cnt;       // [E*M*C_NUM]
+  int64_t* env_cnt;   // [E*2] arrived, rej_nomodel
+  int64_t* hist;      // [E*A]
+  int4* slots;        // [E*M*S]
+  int4* front;        // [E*M*kFront]
+  int4* pool;         // [E*M*qcap]
+  int32_t* err;
+};
+
+// Host-side launchers (defined in the .hip files).
+bool route_supported(int dtype, int hidden, int n_layers, int out_tiles);
+hipError_t launch_route(const RouteArgs& a, int dtype, int hidden, int n_layers, int out_tiles,
+                        hipStream_t s);
+hipError_t launch_schedule(const SchedArgs& a, hipStream_t s);
+
+}  // namespace im

@@ -1,0 +1,549 @@
+// Host side of libinframind: the C ABI declared in inframind.h.
+//
+// Owns the device state of a pool, packs the policy weights into the MFMA
+// fragment order the route kernels read, validates arguments and launches the
+// route / schedule kernels on the caller's stream.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "im_internal.h"
+#include "inframind.h"
+
+using im::ModelRec;
+
+struct im_pool {
+  im_pool_desc d{};
+  int A = 0, S = 0, hidden = 0, n_layers = 0, out_tiles = 0, k1 = 0;
+  int64_t Q = 0;
+  int device = 0;
+  const void* emb = nullptr;
+  void* W[3] = {nullptr, nullptr, nullptr};
+  float* bias[3] = {nullptr, nullptr, nullptr};
+  float* inv_tab = nullptr;
+  float inv_qcap = 0, inv_lat = 0, inv_bud = 0;
+  ModelRec* ms = nullptr;
+  int64_t* cnt = nullptr;
+  int64_t* env_cnt = nullptr;
+  int64_t* hist = nullptr;
+  int4* slots = nullptr;
+  int4* front = nullptr;
+  int4* qpool = nullptr;
+  int32_t* err = nullptr;
+  int32_t* act_buf = nullptr;
+  int64_t act_cap = 0;
+  int32_t t = 0;
+  std::string last_error;
+};
+
+namespace {
+
+std::string g_create_error = "no error";
+
+im_status fail(im_pool* p, im_status s, const std::string& msg) {
+  if (p) p->last_error = msg; else g_create_error = msg;
+  return s;
+}
+
+im_status hip_fail(im_pool* p, hipError_t e, const char* what) {
+  return fail(p, e == hipErrorOutOfMemory ? IM_ENOMEM : IM_EHIP,
+              std::string(what) + ": " + hipGetErrorString(e));
+}
+
+#define IM_HIP(p, call)                                   \
+  do {                                                    \
+    hipError_t _e = (call);                               \
+    if (_e != hipSuccess) return hip_fail((p), _e, #call); \
+  } while (0)
+
+// fp32 -> bf16 bits, round to nearest even (NaN kept quiet).
+uint16_t to_bf16(float f) {
+  uint32_t u;
+  std::memcpy(&u, &f, 4);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+// Input feature read by k-slot (kb, lane group g, element j) of a K block.
+// Layer 0 reads the feature vector in natural order; deeper layers read the
+// previous layer's accumulator registers, whose feature order inside each
+// 16-wide block is 8*(j/4) + 4*g + j%4.
+int bf16_k(int layer, int kb, int g, int j) {
+  return layer == 0 ? 16 * kb + 8 * g + j : 16 * kb + 8 * (j >> 2) + 4 * g + (j & 3);
+}
+int f32_k(int layer, int i, int g) {
+  return layer == 0 ? 2 * i + g : 32 * (i >> 4) + 8 * ((i & 15) >> 2) + 4 * g + (i & 3);
+}
+
+template <class T>
+im_status upload(im_pool* p, T** dst, const std::vector<T>& src) {
+  IM_HIP(p, hipMalloc((void**)dst, std::max<size_t>(src.size(), 1) * sizeof(T)));
+  if (!src.empty()) IM_HIP(p, hipMemcpy(*dst, src.data(), src.size() * sizeof(T), hipMemcpyHostToDevice));
+  return IM_OK;
+}
+
+template <class T>
+im_status zalloc(im_pool* p, T** dst, size_t n) {
+  IM_HIP(p, hipMalloc((void**)dst, std::max<size_t>(n, 1) * sizeof(T)));
+  IM_HIP(p, hipMemset(*dst, 0, std::max<size_t>(n, 1) * sizeof(T)));
+  return IM_OK;
+}
+
+__global__ void set_field_kernel(int32_t* ptr, int32_t v) { *ptr = v; }
+
+im_status check_arrivals(im_pool* p, const im_arrivals* arr) {
+  if (!arr) return fail(p, IM_EINVAL, "arrivals is NULL");
+  if (arr->n_total < 0) return fail(p, IM_EINVAL, "n_total < 0");
+  if (!arr->offsets) return fail(p, IM_EINVAL, "offsets is NULL");
+  if (arr->n_total > 0 && (!arr->q_idx || !arr->budget || !arr->base_svc))
+    return fail(p, IM_EINVAL, "arrival field pointer is NULL");
+  if ((int64_t)arr->n_total > (int64_t)p->d.n_envs * p->d.max_arrivals_per_env_tick)
+    return fail(p, IM_EINVAL, "n_total exceeds n_envs * max_arrivals_per_env_tick");
+  return IM_OK;
+}
+
+void free_pool(im_pool* p) {
+  for (int l = 0; l < 3; ++l) {
+    if (p->W[l]) (void)hipFree(p->W[l]);
+    if (p->bias[l]) (void)hipFree(p->bias[l]);
+  }
+  void* bufs[] = {p->inv_tab, p->ms, p->cnt, p->env_cnt, p->hist, p->slots,
+                  p->front, p->qpool, p->err, p->act_buf};
+  for (void* b : bufs) if (b) (void)hipFree(b);
+  delete p;
+}
+
+}  // namespace
+
+extern "C" {
+
+im_status im_pool_create(const im_pool_desc* desc, const float* const* W, const float* const* b,
+                         const void* emb, int64_t n_queries, const int32_t* capacity,
+                         const float* logit_bias, void* stream, im_pool** out) {
+  if (!desc || !W || !b || !emb || !capacity || !out)
+    return fail(nullptr, IM_EINVAL, "NULL argument to im_pool_create");
+  const im_pool_desc& d = *desc;
+  const int A = d.n_models * d.n_depths;
+  if (d.n_envs < 1 || d.n_models < 1 || d.n_models > IM_MAX_MODELS || d.n_depths < 1 ||
+      d.n_depths > IM_MAX_DEPTHS || A > IM_MAX_ACTIONS)
+    return fail(nullptr, IM_EINVAL, "n_envs/n_models/n_depths out of range");
+  if (d.queue_cap < 1 || d.queue_cap > IM_MAX_QCAP) return fail(nullptr, IM_EINVAL, "queue_cap out of range");
+  if (d.max_slots < 1 || d.max_slots > IM_MAX_SLOTS) return fail(nullptr, IM_EINVAL, "max_slots out of range");
+  if (d.embed_dim < 1 || d.feat_dim > IM_MAX_FEAT || d.feat_dim < d.embed_dim + 4 * d.n_models + 1)
+    return fail(nullptr, IM_EINVAL, "feat_dim must be in [embed_dim + 4M + 1, IM_MAX_FEAT]");
+  if (d.n_layers != 2 && d.n_layers != 3) return fail(nullptr, IM_EINVAL, "n_layers must be 2 or 3");
+  if (d.widths[d.n_layers - 1] != A) return fail(nullptr, IM_EINVAL, "last width must be M*K");
+  if (d.n_layers == 3 && d.widths[0] != d.widths[1])
+    return fail(nullptr, IM_EUNSUPPORTED, "hidden widths must be equal");
+  if (d.dtype != IM_F32 && d.dtype != IM_BF16) return fail(nullptr, IM_EINVAL, "bad dtype");
+  if (d.key_mode < IM_KEY_SLACK || d.key_mode > IM_KEY_FCFS) return fail(nullptr, IM_EINVAL, "bad key_mode");
+  if (d.max_arrivals_per_env_tick < 1) return fail(nullptr, IM_EINVAL, "max_arrivals_per_env_tick < 1");
+  if (d.budget_max < 1) return fail(nullptr, IM_EINVAL, "budget_max < 1");
+  if (n_queries < 1 || n_queries > INT32_MAX) return fail(nullptr, IM_EINVAL, "n_queries out of range");
+  const int H = d.widths[0];
+  const int out_tiles = (A + 31) / 32;
+  if (!im::route_supported(d.dtype, H, d.n_layers, out_tiles))
+    return fail(nullptr, IM_EUNSUPPORTED, "no route kernel for this dtype / hidden width");
+  for (int64_t i = 0; i < (int64_t)d.n_envs * d.n_models; ++i)
+    if (capacity[i] < 0 || capacity[i] > d.max_slots)
+      return fail(nullptr, IM_EINVAL, "capacity outside [0, max_slots]");
+
+  im_pool* p = new im_pool();
+  p->d = d;
+  p->A = A;
+  p->S = d.max_slots;
+  p->hidden = H;
+  p->n_layers = d.n_layers;
+  p->out_tiles = out_tiles;
+  p->Q = n_queries;
+  p->emb = emb;
+  (void)hipGetDevice(&p->device);
+  hipStream_t s = (hipStream_t)stream;
+  im_status st = IM_OK;
+
+  // ---- pack weights and biases into fragment order ----
+  int in = d.feat_dim;
+  for (int l = 0; l < d.n_layers && st == IM_OK; ++l) {
+    const int outw = d.widths[l];
+    const int TO = (outw + 31) / 32;
+    const float* Wl = W[l];
+    if (!Wl || !b[l]) { st = fail(p, IM_EINVAL, "NULL weight or bias"); break; }
+    if (d.dtype == IM_BF16) {
+      const int KB = (in + 15) / 16;
+      if (l == 0) p->k1 = KB;
+      std::vector<uint16_t> pk((size_t)TO * KB * 64 * 8, 0);
+      for (int To = 0; To < TO; ++To)
+        for (int kb = 0; kb < KB; ++kb)
+          for (int lane = 0; lane < 64; ++lane)
+            for (int j = 0; j < 8; ++j) {
+              const int o = 32 * To + (lane & 31);
+              const int k = bf16_k(l, kb, lane >> 5, j);
+              if (o < outw && k < in)
+                pk[(((size_t)To * KB + kb) * 64 + lane) * 8 + j] = to_bf16(Wl[(size_t)o * in + k]);
+            }
+      st = upload(p, (uint16_t**)&p->W[l], pk);
+    } else {
+      const int KI = (in + 1) / 2;
+      if (l == 0) p->k1 = KI;
+      std::vector<float> pk((size_t)TO * KI * 64, 0.f);
+      for (int To = 0; To < TO; ++To)
+        for (int i = 0; i < KI; ++i)
+          for (int lane = 0; lane < 64; ++lane) {
+            const int o = 32 * To + (lane & 31);
+            const int k = f32_k(l, i, lane >> 5);
+            if (o < outw && k < in) pk[((size_t)To * KI + i) * 64 + lane] = Wl[(size_t)o * in + k];
+          }
+      st = upload(p, (float**)&p->W[l], pk);
+    }
+    if (st != IM_OK) break;
+    // Bias in accumulator-register order: [To][g][v] -> feature 32To + 8(v/4) + 4g + v%4.
+    std::vector<float> bp((size_t)TO * 2 * 16, 0.f);
+    for (int To = 0; To < TO; ++To)
+      for (int g = 0; g < 2; ++g)
+        for (int v = 0; v < 16; ++v) {
+          const int o = 32 * To + 8 * (v >> 2) + 4 * g + (v & 3);
+          if (o >= outw) continue;
+          float val = b[l][o];
+          if (l == d.n_layers - 1 && logit_bias) val += logit_bias[o / d.n_depths];
+          bp[((size_t)To * 2 + g) * 16 + v] = val;
+        }
+    st = upload(p, &p->bias[l], bp);
+    in = outw;
+  }
+  // ---- feature reciprocals, each rounded once from fp64 to fp32 ----
+  if (st == IM_OK) {
+    p->inv_qcap = (float)(1.0 / d.queue_cap);
+    p->inv_lat = (float)(1.0 / (256.0 * d.budget_max));
+    p->inv_bud = (float)(1.0 / d.budget_max);
+    std::vector<float> tab(2 * (IM_MAX_SLOTS + 1));
+    for (int c = 0; c <= IM_MAX_SLOTS; ++c) {
+      const int cc = std::max(c, 1);
+      tab[c] = (float)(1.0 / cc);
+      tab[IM_MAX_SLOTS + 1 + c] = (float)(1.0 / ((double)cc * d.budget_max));
+    }
+    st = upload(p, &p->inv_tab, tab);
+  }
+  // ---- state ----
+  const size_t EM = (size_t)d.n_envs * d.n_models;
+  if (st == IM_OK) {
+    std::vector<ModelRec> recs(EM);
+    std::memset(recs.data(), 0, EM * sizeof(ModelRec));
+    for (size_t i = 0; i < EM; ++i) { recs[i].cap = capacity[i]; recs[i].enabled = 1; }
+    st = upload(p, &p->ms, recs);
+  }
+  if (st == IM_OK) st = zalloc(p, &p->cnt, EM * im::C_NUM);
+  if (st == IM_OK) st = zalloc(p, &p->env_cnt, (size_t)d.n_envs * 2);
+  if (st == IM_OK) st = zalloc(p, &p->hist, (size_t)d.n_envs * A);
+  if (st == IM_OK) {
+    std::vector<int4> sl(EM * d.max_slots, make_int4(-1, 0, 0, 0));
+    st = upload(p, &p->slots, sl);
+  }
+  if (st == IM_OK) st = zalloc(p, &p->front, EM * im::kFront);
+  if (st == IM_OK) st = zalloc(p, &p->qpool, EM * (size_t)d.queue_cap);
+  if (st == IM_OK) st = zalloc(p, &p->err, 1);
+  if (st == IM_OK) {
+    p->act_cap = (int64_t)d.n_envs * d.max_arrivals_per_env_tick;
+    st = zalloc(p, &p->act_buf, (size_t)p->act_cap);
+  }
+  if (st == IM_OK) {
+    hipError_t e = hipStreamSynchronize(s);
+    if (e != hipSuccess) st = hip_fail(p, e, "hipStreamSynchronize");
+  }
+  if (st != IM_OK) {
+    g_create_error = p->last_error;
+    free_pool(p);
+    return st;
+  }
+  *out = p;
+  return IM_OK;
+}
+
+void im_destroy(im_pool* p) {
+  if (!p) return;
+  (void)hipDeviceSynchronize();
+  free_pool(p);
+}
+
+static im::RouteArgs route_args(im_pool* p, const im_arrivals* arr, int32_t* actions, float* logits) {
+  im::RouteArgs a{};
+  a.offsets = arr->offsets;
+  a.q_idx = arr->q_idx;
+  a.budget = arr->budget;
+  a.n_total = arr->n_total;
+  a.E = p->d.n_envs;
+  a.M = p->d.n_models;
+  a.K = p->d.n_depths;
+  a.A = p->A;
+  a.embed_dim = p->d.embed_dim;
+  a.feat_dim = p->d.feat_dim;
+  a.k1 = p->k1;
+  a.qcap = p->d.queue_cap;
+  a.Q = p->Q;
+  a.emb = p->emb;
+  for (int l = 0; l < 3; ++l) { a.W[l] = p->W[l]; a.bias[l] = p->bias[l]; }
+  a.ms = p->ms;
+  a.inv_qcap = p->inv_qcap;
+  a.inv_lat = p->inv_lat;
+  a.inv_bud = p->inv_bud;
+  a.inv_tab = p->inv_tab;
+  a.actions = actions;
+  a.logits = logits;
+  a.err = p->err;
+  return a;
+}
+
+im_status im_route(im_pool* p, const im_arrivals* arr, int32_t* actions, float* logits,
+                   void* stream) {
+  if (!p) return fail(nullptr, IM_EINVAL, "pool is NULL");
+  im_status st = check_arrivals(p, arr);
+  if (st != IM_OK) return st;
+  if (arr->n_total > 0 && !actions) return fail(p, IM_EINVAL, "actions is NULL");
+  const im::RouteArgs a = route_args(p, arr, actions, logits);
+  IM_HIP(p, im::launch_route(a, p->d.dtype, p->hidden, p->n_layers, p->out_tiles,
+                             (hipStream_t)stream));
+  return IM_OK;
+}
+
+im_status im_schedule(im_pool* p, const im_arrivals* arr, const int32_t* actions, void* stream) {
+  if (!p) return fail(nullptr, IM_EINVAL, "pool is NULL");
+  im_status st = check_arrivals(p, arr);
+  if (st != IM_OK) return st;
+  if (arr->n_total > 0 && !actions) return fail(p, IM_EINVAL, "actions is NULL");
+  if (p->t == INT32_MAX - 65536) return fail(p, IM_EINVAL, "tick counter exhausted");
+  im::SchedArgs a{};
+  a.offsets = arr->offsets;
+  a.q_idx = arr->q_idx;
+  a.budget = arr->budget;
+  a.base_svc = arr->base_svc;
+  a.actions = actions;
+  a.n_total = arr->n_total;
+  a.E = p->d.n_envs;
+  a.M = p->d.n_models;
+  a.K = p->d.n_depths;
+  a.A = p->A;
+  a.S = p->S;
+  a.qcap = p->d.queue_cap;
+  a.max_arrivals = p->d.max_arrivals_per_env_tick;
+  a.key_mode = p->d.key_mode;
+  a.Q = p->Q;
+  a.t = p->t;
+  a.ms = p->ms;
+  a.cnt = p->cnt;
+  a.env_cnt = p->env_cnt;
+  a.hist = p->hist;
+  a.slots = p->slots;
+  a.front = p->front;
+  a.pool = p->qpool;
+  a.err = p->err;
+  IM_HIP(p, im::launch_schedule(a, (hipStream_t)stream));
+  p->t += 1;
+  return IM_OK;
+}
+
+im_status im_tick(im_pool* p, const im_arrivals* arr, int32_t* actions_out, void* stream) {
+  if (!p) return fail(nullptr, IM_EINVAL, "pool is NULL");
+  im_status st = check_arrivals(p, arr);
+  if (st != IM_OK) return st;
+  int32_t* act = actions_out ? actions_out : p->act_buf;
+  st = im_route(p, arr, act, nullptr, stream);
+  if (st != IM_OK) return st;
+  return im_schedule(p, arr, act, stream);
+}
+
+im_status im_set_enabled(im_pool* p, int32_t env, int32_t model, int32_t enabled, void* stream) {
+  if (!p) return fail(nullptr, IM_EINVAL, "pool is NULL");
+  if (env < 0 || env >= p->d.n_envs || model < 0 || model >= p->d.n_models)
+    return fail(p, IM_EINVAL, "env/model out of range");
+  ModelRec* r = p->ms + (size_t)env * p->d.n_models + model;
+  hipLaunchKernelGGL(set_field_kernel, dim3(1), dim3(1), 0, (hipStream_t)stream, &r->enabled,
+                     enabled ? 1 : 0);
+  IM_HIP(p, hipGetLastError());
+  return IM_OK;
+}
+
+im_status im_set_capacity(im_pool* p, int32_t env, int32_t model, int32_t capacity, void* stream) {
+  if (!p) return fail(nullptr, IM_EINVAL, "pool is NULL");
+  if (env < 0 || env >= p->d.n_envs || model < 0 || model >= p->d.n_models)
+    return fail(p, IM_EINVAL, "env/model out of range");
+  if (capacity < 0 || capacity > p->S) return fail(p, IM_EINVAL, "capacity outside [0, max_slots]");
+  ModelRec* r = p->ms + (size_t)env * p->d.n_models + model;
+  hipLaunchKernelGGL(set_field_kernel, dim3(1), dim3(1), 0, (hipStream_t)stream, &r->cap, capacity);
+  IM_HIP(p, hipGetLastError());
+  return IM_OK;
+}
+
+im_status im_get_error(im_pool* p, int32_t* bits) {
+  if (!p || !bits) return fail(p, IM_EINVAL, "NULL argument");
+  IM_HIP(p, hipDeviceSynchronize());
+  IM_HIP(p, hipMemcpy(bits, p->err, sizeof(int32_t), hipMemcpyDeviceToHost));
+  return *bits ? IM_EDEVICE : IM_OK;
+}
+
+im_status im_clear_error(im_pool* p) {
+  if (!p) return fail(nullptr, IM_EINVAL, "pool is NULL");
+  IM_HIP(p, hipDeviceSynchronize());
+  IM_HIP(p, hipMemset(p->err, 0, sizeof(int32_t)));
+  IM_HIP(p, hipDeviceSynchronize());
+  return IM_OK;
+}
+
+const char* im_last_error(const im_pool* p) {
+  return p ? p->last_error.c_str() : g_create_error.c_str();
+}
+
+im_status im_read_state(im_pool* p, int32_t env_begin, int32_t env_count, int32_t* tick,
+                        im_env_state* envs, im_model_state* models, im_slot* slots,
+                        im_entry* queues, int64_t* hist) {
+  if (!p) return fail(nullptr, IM_EINVAL, "pool is NULL");
+  if (env_begin < 0 || env_count < 0 || (int64_t)env_begin + env_count > p->d.n_envs)
+    return fail(p, IM_EINVAL, "env range out of bounds");
+  IM_HIP(p, hipDeviceSynchronize());
+  if (tick) *tick = p->t;
+  const int M = p->d.n_models, S = p->S, qcap = p->d.queue_cap, A = p->A;
+  const size_t em0 = (size_t)env_begin * M, EMc = (size_t)env_count * M;
+  std::vector<ModelRec> recs(EMc);
+  std::vector<int64_t> cnt(EMc * im::C_NUM);
+  if (EMc) {
+    IM_HIP(p, hipMemcpy(recs.data(), p->ms + em0, EMc * sizeof(ModelRec), hipMemcpyDeviceToHost));
+    IM_HIP(p, hipMemcpy(cnt.data(), p->cnt + em0 * im::C_NUM, cnt.size() * 8, hipMemcpyDeviceToHost));
+  }
+  if (envs && env_count) {
+    std::vector<int64_t> ec((size_t)env_count * 2);
+    IM_HIP(p, hipMemcpy(ec.data(), p->env_cnt + (size_t)env_begin * 2, ec.size() * 8,
+                        hipMemcpyDeviceToHost));
+    for (int e = 0; e < env_count; ++e) {
+      envs[e].arrived = ec[2 * e];
+      envs[e].rej_nomodel = ec[2 * e + 1];
+      envs[e].next_id = recs[(size_t)e * M].next_id;
+      envs[e]._pad = 0;
+    }
+  }
+  if (models) {
+    for (size_t i = 0; i < EMc; ++i) {
+      im_model_state& o = models[i];
+      std::memset(&o, 0, sizeof(o));
+      o.qlen = recs[i].qlen; o.busy = recs[i].busy; o.ewma_q8 = recs[i].ewma;
+      o.backlog = recs[i].backlog; o.capacity = recs[i].cap; o.enabled = recs[i].enabled;
+      const int64_t* c = &cnt[i * im::C_NUM];
+      o.rej_overflow = c[im::C_REJ_OVERFLOW]; o.enqueued = c[im::C_ENQUEUED];
+      o.started = c[im::C_STARTED]; o.completed = c[im::C_COMPLETED]; o.slo_met = c[im::C_SLO_MET];
+      o.lat_sum = c[im::C_LAT_SUM]; o.wait_sum = c[im::C_WAIT_SUM];
+    }
+  }
+  if (slots && EMc)
+    IM_HIP(p, hipMemcpy(slots, p->slots + em0 * S, EMc * S * sizeof(int4), hipMemcpyDeviceToHost));
+  if (hist && env_count)
+    IM_HIP(p, hipMemcpy(hist, p->hist + (size_t)env_begin * A, (size_t)env_count * A * 8,
+                        hipMemcpyDeviceToHost));
+  if (queues && EMc) {
+    // Materialise each queue in service order: the sorted front, then the
+    // pool sorted by (key, id) (every pool key exceeds every front key).
+    std::vector<int4> fr(EMc * im::kFront), pl(EMc * (size_t)qcap);
+    IM_HIP(p, hipMemcpy(fr.data(), p->front + em0 * im::kFront, fr.size() * sizeof(int4),
+                        hipMemcpyDeviceToHost));
+    IM_HIP(p, hipMemcpy(pl.data(), p->qpool + em0 * qcap, pl.size() * sizeof(int4),
+                        hipMemcpyDeviceToHost));
+    std::memset(queues, 0, EMc * qcap * sizeof(im_entry));
+    std::vector<int4> tmp;
+    for (size_t i = 0; i < EMc; ++i) {
+      const ModelRec& r = recs[i];
+      tmp.assign(fr.begin() + i * im::kFront + r.fh, fr.begin() + i * im::kFront + r.fh + r.fn);
+      const size_t f = tmp.size();
+      tmp.insert(tmp.end(), pl.begin() + i * qcap, pl.begin() + i * qcap + r.P);
+      std::sort(tmp.begin() + f, tmp.end(), [](const int4& x, const int4& y) {
+        return x.x != y.x ? x.x < y.x : x.y < y.y;
+      });
+      im_entry* q = queues + i * qcap;
+      for (size_t k = 0; k < tmp.size() && k < (size_t)qcap; ++k) {
+        q[k].key = tmp[k].x; q[k].id = tmp[k].y; q[k].t_arr = tmp[k].z;
+        q[k].svc = (uint16_t)(tmp[k].w & 0xffff);
+        q[k].budget = (uint16_t)((uint32_t)tmp[k].w >> 16);
+      }
+    }
+  }
+  return IM_OK;
+}
+
+im_status im_write_state(im_pool* p, int32_t env_begin, int32_t env_count, int32_t tick,
+                         const im_env_state* envs, const im_model_state* models,
+                         const im_slot* slots, const im_entry* queues, const int64_t* hist) {
+  if (!p) return fail(nullptr, IM_EINVAL, "pool is NULL");
+  if (env_begin < 0 || env_count < 0 || (int64_t)env_begin + env_count > p->d.n_envs)
+    return fail(p, IM_EINVAL, "env range out of bounds");
+  if (!envs || !models || !slots || !queues || !hist) return fail(p, IM_EINVAL, "NULL argument");
+  if (tick < 0) return fail(p, IM_EINVAL, "tick < 0");
+  const int M = p->d.n_models, S = p->S, qcap = p->d.queue_cap, A = p->A;
+  const size_t EMc = (size_t)env_count * M, em0 = (size_t)env_begin * M;
+  std::vector<ModelRec> recs(EMc);
+  std::memset(recs.data(), 0, EMc * sizeof(ModelRec));
+  std::vector<int64_t> cnt(EMc * im::C_NUM, 0);
+  std::vector<int4> fr(EMc * im::kFront, make_int4(0, 0, 0, 0));
+  std::vector<int4> pl(EMc * (size_t)qcap, make_int4(0, 0, 0, 0));
+  std::vector<int4> sl(EMc * S);
+  for (size_t i = 0; i < EMc; ++i) {
+    const im_model_state& ms = models[i];
+    const int e = (int)(i / M);
+    if (ms.qlen < 0 || ms.qlen > qcap || ms.capacity < 0 || ms.capacity > S || ms.ewma_q8 < 0)
+      return fail(p, IM_ESTATE, "model state out of bounds");
+    const im_entry* q = queues + i * qcap;
+    int64_t bl = 0;
+    for (int k = 0; k < ms.qlen; ++k) {
+      bl += q[k].svc;
+      if (k > 0 && !(q[k - 1].key < q[k].key || (q[k - 1].key == q[k].key && q[k - 1].id < q[k].id)))
+        return fail(p, IM_ESTATE, "queue not strictly increasing in (key, id)");
+      if (q[k].id < 0 || q[k].id >= envs[e].next_id) return fail(p, IM_ESTATE, "queue id out of range");
+    }
+    if (bl != ms.backlog) return fail(p, IM_ESTATE, "backlog != sum of queued svc");
+    int busy = 0;
+    for (int s = 0; s < S; ++s) {
+      const im_slot& x = slots[i * S + s];
+      if (x.id >= 0) {
+        ++busy;
+        if (x.rem < 1) return fail(p, IM_ESTATE, "busy slot with rem < 1");
+      }
+      sl[i * S + s] = x.id >= 0 ? make_int4(x.id, x.t_arr, x.rem, x.budget) : make_int4(-1, 0, 0, 0);
+    }
+    if (busy != ms.busy) return fail(p, IM_ESTATE, "busy != occupied slots");
+    ModelRec& r = recs[i];
+    r.qlen = ms.qlen; r.busy = ms.busy; r.ewma = ms.ewma_q8; r.backlog = ms.backlog;
+    r.cap = ms.capacity; r.enabled = ms.enabled ? 1 : 0; r.next_id = envs[e].next_id;
+    r.fh = 0;
+    r.fn = std::min(ms.qlen, im::kFront);
+    r.P = ms.qlen - r.fn;
+    for (int k = 0; k < ms.qlen; ++k) {
+      const int4 v = make_int4(q[k].key, q[k].id, q[k].t_arr,
+                               (int32_t)((uint32_t)q[k].svc | ((uint32_t)q[k].budget << 16)));
+      if (k < im::kFront) fr[i * im::kFront + k] = v;
+      else pl[i * qcap + (k - im::kFront)] = v;
+    }
+    int64_t* c = &cnt[i * im::C_NUM];
+    c[im::C_REJ_OVERFLOW] = ms.rej_overflow; c[im::C_ENQUEUED] = ms.enqueued;
+    c[im::C_STARTED] = ms.started; c[im::C_COMPLETED] = ms.completed; c[im::C_SLO_MET] = ms.slo_met;
+    c[im::C_LAT_SUM] = ms.lat_sum; c[im::C_WAIT_SUM] = ms.wait_sum;
+  }
+  std::vector<int64_t> ec((size_t)env_count * 2);
+  for (int e = 0; e < env_count; ++e) { ec[2 * e] = envs[e].arrived; ec[2 * e + 1] = envs[e].rej_nomodel; }
+  IM_HIP(p, hipDeviceSynchronize());
+  if (EMc) {
+    IM_HIP(p, hipMemcpy(p->ms + em0, recs.data(), EMc * sizeof(ModelRec), hipMemcpyHostToDevice));
+    IM_HIP(p, hipMemcpy(p->cnt + em0 * im::C_NUM, cnt.data(), cnt.size() * 8, hipMemcpyHostToDevice));
+    IM_HIP(p, hipMemcpy(p->front + em0 * im::kFront, fr.data(), fr.size() * sizeof(int4), hipMemcpyHostToDevice));
+    IM_HIP(p, hipMemcpy(p->qpool + em0 * qcap, pl.data(), pl.size() * sizeof(int4), hipMemcpyHostToDevice));
+    IM_HIP(p, hipMemcpy(p->slots + em0 * S, sl.data(), sl.size() * sizeof(int4), hipMemcpyHostToDevice));
+  }
+  if (env_count) {
+    IM_HIP(p, hipMemcpy(p->env_cnt + (size_t)env_begin * 2, ec.data(), ec.size() * 8, hipMemcpyHostToDevice));
+    IM_HIP(p, hipMemcpy(p->hist + (size_t)env_begin * A, hist, (size_t)env_count * A * 8, hipMemcpyHostToDevice));
+  }
+  IM_HIP(p, hipDeviceSynchronize());
+  p->t = tick;
+  return IM_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,337 @@
+// Schedule step of the tick: admission, queue insertion, service, accounting.
+//
+// One wave owns one (env, model) queue; a block holds 4 such waves and the
+// waves never synchronise with each other (no block barriers), so every wave
+// runs its queue independently.
+//
+// Per queue, in the order the tick defines:
+//   admission  -- the env's routed requests for this model, in id order, are
+//                 accepted while the queue has room (tail-drop beyond the
+//                 capacity); stable partition by model = ballot + mbcnt.
+//   keys       -- svc = base_svc * (depth + 1); key = t + budget - svc (slack,
+//                 i.e. latest start time), t + budget (deadline, Sec. 4.3) or t
+//                 (arrival order). The queue order is (key, id).
+//   insertion  -- the queue is kept as a sorted front of at most 64 entries
+//                 (one per lane) holding the smallest keys, plus an unsorted
+//                 pool of the rest. A chunk of up to 64 newcomers is sorted with
+//                 a bitonic network; those below the front's largest key are
+//                 merged into the front (its overflow spills to the pool), the
+//                 others are appended to the pool. No suffix of a sorted array
+//                 is ever rewritten.
+//   service    -- free slots below c_m are filled in slot order from the front
+//                 head; when the front runs empty it is refilled with the 64
+//                 smallest pool entries (bitonic top-64 selection), and the
+//                 pool is compacted. Busy slots then advance one tick; a
+//                 request completes when its remaining time reaches 0 (latency
+//                 EWMA with alpha = 1/8 in Q8, Sec. 5.4; bounded concurrency
+//                 as in Table 5).
+#include "im_internal.h"
+#include "wave.h"
+
+namespace im {
+namespace {
+
+constexpr int64_t kKeyMax = 0x7fffffffffffffffll;
+
+__device__ __forceinline__ int64_t composite(int32_t key, int32_t id) {
+  return (int64_t)(((uint64_t)(uint32_t)key << 32) | (uint32_t)id);
+}
+__device__ __forceinline__ int32_t comp_key(int64_t c) { return (int32_t)(c >> 32); }
+__device__ __forceinline__ int32_t comp_id(int64_t c) { return (int32_t)(uint32_t)c; }
+
+// Number of entries of the ascending sequence X (lanes [0, len)) below v.
+__device__ __forceinline__ int count_below(int64_t X, int len, int64_t v) {
+  int pos = 0;
+#pragma unroll
+  for (int step = 64; step >= 1; step >>= 1) {
+    const int probe = pos + step - 1;
+    const int64_t xp = shfl(X, probe < 64 ? probe : 63);
+    if (probe < len && xp < v) pos += step;
+  }
+  return pos;
+}
+
+// Makes this wave's earlier global stores visible to its later loads.
+__device__ __forceinline__ void wave_mem_sync() { __threadfence_block(); }
+
+struct Queue {       // wave-uniform view of one (env, model) record
+  int32_t qlen, busy, ewma, backlog, cap, enabled, fh, fn, P, next_id;
+};
+
+// Insert up to 64 newcomers (valid lanes) into the front/pool structure.
+// Newcomer payload: key, id, t_arr, svc | budget << 16.
+__device__ void insert_batch(Queue& q, bool valid, int32_t key, int32_t id, int32_t t_arr,
+                             int32_t packed, int4* front, int4* pool) {
+  const int lane = lane_id();
+  const int k = popc64(ballot(valid));
+  if (k == 0) return;
+  int64_t ck = valid ? composite(key, id) : kKeyMax;
+  int32_t pay[1] = {packed};
+  bitonic_sort64<1>(ck, pay);           // lanes [0, k) now hold the newcomers sorted
+
+  int lim;
+  if (q.P == 0) {
+    lim = k;
+  } else if (q.fn == 0) {
+    lim = 0;
+  } else {
+    const int4 last = front[q.fh + q.fn - 1];
+    const int64_t fmax = composite(last.x, last.y);
+    lim = popc64(ballot(lane < k && ck < fmax));
+  }
+
+  if (lim > 0) {
+    // Merge the front (lanes [0, fn)) with newcomers [0, lim); positions in
+    // the merged order follow from counting the other sequence's smaller keys
+    // (all composite keys are distinct).
+    int4 fe = make_int4(0, 0, 0, 0);
+    int64_t fck = kKeyMax;
+    if (lane < q.fn) {
+      fe = front[q.fh + lane];
+      fck = composite(fe.x, fe.y);
+    }
+    const int64_t nck = lane < lim ? ck : kKeyMax;
+    const int posf = lane + count_below(nck, lim, fck);
+    const int posn = lane + count_below(fck, q.fn, nck);
+    const int total = q.fn + lim;
+    const int keep = total < kFront ? total : kFront;
+    if (lane < q.fn) {
+      if (posf < kFront) front[posf] = fe;
+      else pool[q.P + posf - kFront] = fe;
+    }
+    if (lane < lim) {
+      const int4 ne = make_int4(comp_key(ck), comp_id(ck), t_arr, pay[0]);
+      if (posn < kFront) front[posn] = ne;
+      else pool[q.P + posn - kFront] = ne;
+    }
+    q.P += total - keep;
+    q.fh = 0;
+    q.fn = keep;
+  }
+  if (lane >= lim && lane < k)
+    pool[q.P + lane - lim] = make_int4(comp_key(ck), comp_id(ck), t_arr, pay[0]);
+  q.P += k - lim;
+  wave_mem_sync();
+}
+
+// Refill the (empty) front with the min(64, P) smallest pool entries.
+__device__ void refill(Queue& q, int4* front, int4* pool) {
+  const int lane = lane_id();
+  const int P = q.P;
+  if (P <= kFront) {
+    int4 e = make_int4(0, 0, 0, 0);
+    int64_t ck = kKeyMax;
+    if (lane < P) { e = pool[lane]; ck = composite(e.x, e.y); }
+    int32_t pay[2] = {e.z, e.w};
+    bitonic_sort64<2>(ck, pay);
+    if (lane < P) front[lane] = make_int4(comp_key(ck), comp_id(ck), pay[0], pay[1]);
+    q.fh = 0;
+    q.fn = P;
+    q.P = 0;
+    wave_mem_sync();
+    return;
+  }
+  // Top-64 selection: keep the 64 smallest seen so far, sorted across lanes.
+  int64_t ck = composite(pool[lane].x, pool[lane].y);
+  int32_t idx[1] = {lane};
+  bitonic_sort64<1>(ck, idx);
+  for (int c0 = kFront; c0 < P; c0 += kFront) {
+    const int i = c0 + lane;
+    int64_t c2 = kKeyMax;
+    if (i < P) { const int4 e = pool[i]; c2 = composite(e.x, e.y); }
+    const int64_t thr = shfl(ck, 63);
+    const bool cand = c2 < thr;
+    if (ballot(cand) == 0) continue;
+    if (!cand) c2 = kKeyMax;
+    int32_t i2[1] = {i};
+    bitonic_sort64<1>(c2, i2);
+    // min(best[l], chunk[63 - l]) is bitonic and holds the 64 smallest.
+    const int64_t rc = shfl(c2, 63 - lane);
+    const int32_t ri = shfl(i2[0], 63 - lane);
+    if (rc < ck) { ck = rc; idx[0] = ri; }
+    bitonic_merge64<1>(ck, idx);
+  }
+  const int sel = idx[0];
+  const int4 e = pool[sel];
+  front[lane] = e;
+  // Compact the pool: selected entries below the new size are holes, filled
+  // with the unselected entries of the last 64 positions (same count).
+  const int Pn = P - kFront;
+  const uint64_t tail_sel = wave_or(sel >= Pn ? (1ull << (sel - Pn)) : 0ull);
+  const uint64_t fillers = ~tail_sel;
+  const uint64_t holes = ballot(sel < Pn);
+  int4 fill = make_int4(0, 0, 0, 0);
+  if (sel < Pn) {
+    const int f = nth_set_bit(fillers, prefix_count(holes));
+    fill = pool[Pn + f];
+  }
+  wave_mem_sync();
+  if (sel < Pn) pool[sel] = fill;
+  q.fh = 0;
+  q.fn = kFront;
+  q.P = Pn;
+  wave_mem_sync();
+}
+
+__global__ __launch_bounds__(256) void schedule_kernel(SchedArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int em = (int)blockIdx.x * 4 + (int)(threadIdx.x >> 6);
+  if (em >= a.E * a.M) return;
+  const int e = em / a.M;
+  const int m = em - e * a.M;
+
+  // ---- validate the env's input; an invalid env is skipped this tick ----
+  const int32_t lo = a.offsets[e], hi = a.offsets[e + 1];
+  int32_t bad = 0;
+  if (lo < 0 || hi < lo || hi > a.n_total || hi - lo > a.max_arrivals) bad = IM_ERR_COUNT;
+  if (!bad) {
+    for (int32_t base = lo; base < hi; base += 64) {
+      const int32_t i = base + lane;
+      int32_t b = 0;
+      if (i < hi) {
+        const int32_t qi = a.q_idx[i];
+        const int32_t bu = a.budget[i];
+        const int32_t sv = a.base_svc[i];
+        const int32_t ac = a.actions[i];
+        if (qi < 0 || (int64_t)qi >= a.Q) b |= IM_ERR_QIDX;
+        if (bu < 1) b |= IM_ERR_BUDGET;
+        if (sv < 1 || sv > IM_SVC_MAX) b |= IM_ERR_SVC;
+        if (ac < -1 || ac >= a.A) b |= IM_ERR_ACTION;
+      }
+      bad |= (int32_t)wave_or((uint64_t)(uint32_t)b);
+    }
+  }
+  if (bad) {
+    if (m == 0 && lane == 0) atomicOr(a.err, bad);
+    return;
+  }
+
+  ModelRec* rec = a.ms + em;
+  Queue q;
+  q.qlen = rec->qlen; q.busy = rec->busy; q.ewma = rec->ewma; q.backlog = rec->backlog;
+  q.cap = rec->cap; q.enabled = rec->enabled; q.fh = rec->fh; q.fn = rec->fn;
+  q.P = rec->P; q.next_id = rec->next_id;
+  int4* front = a.front + (size_t)em * kFront;
+  int4* pool = a.pool + (size_t)em * a.qcap;
+  const int32_t t = a.t;
+  const int32_t n = hi - lo;
+  const int32_t room = a.qcap - q.qlen;
+
+  // ---- admission and insertion, 64 arrivals at a time ----
+  int32_t routed = 0, accepted = 0, nomodel = 0;
+  int64_t svc_in = 0;
+  int64_t hist_add = 0;   // lane d < K: routed requests with depth d
+  for (int32_t base = lo; base < hi; base += 64) {
+    const int32_t i = base + lane;
+    const bool in = i < hi;
+    const int32_t ac = in ? a.actions[i] : -1;
+    const int32_t mdl = ac >= 0 ? ac / a.K : -1;
+    const bool mine = in && mdl == m;
+    const uint64_t bal = ballot(mine);
+    const int32_t rank = routed + prefix_count(bal);
+    const bool acc = mine && rank < room;
+    routed += popc64(bal);
+    if (m == 0) nomodel += popc64(ballot(in && ac < 0));
+    const int32_t d = mine ? ac - m * a.K : -1;
+    for (int dd = 0; dd < a.K; ++dd) {
+      const int cnt = popc64(ballot(d == dd));
+      if (lane == dd) hist_add += cnt;
+    }
+    int32_t key = 0, packed = 0, svc = 0;
+    if (acc) {
+      const int32_t bu = a.budget[i];
+      svc = (int32_t)a.base_svc[i] * (d + 1);
+      key = a.key_mode == IM_KEY_DEADLINE ? t + bu : (a.key_mode == IM_KEY_FCFS ? t : t + bu - svc);
+      packed = (int32_t)((uint32_t)svc | ((uint32_t)bu << 16));
+    }
+    accepted += popc64(ballot(acc));
+    svc_in += wave_sum(acc ? svc : 0);
+    insert_batch(q, acc, key, q.next_id + (i - lo), t, packed, front, pool);
+  }
+  q.qlen += accepted;
+  q.backlog += (int32_t)svc_in;
+
+  // ---- service: fill free slots below c_m from the queue head ----
+  int4 sl = make_int4(-1, 0, 0, 0);
+  if (lane < a.S) sl = a.slots[(size_t)em * a.S + lane];
+  const int capc = q.cap < a.S ? q.cap : a.S;
+  uint64_t empty = ballot(lane < capc && sl.x < 0);
+  int32_t started = 0;
+  int64_t wait_add = 0, svc_out = 0;
+  while (empty != 0 && q.qlen > 0) {
+    if (q.fn == 0) refill(q, front, pool);
+    if (q.fn == 0) break;   // unreachable while qlen == fn + P holds; never spin
+    const int need = popc64(empty);
+    const int take = need < q.fn ? need : q.fn;
+    const bool mine_slot = ((empty >> lane) & 1ull) && prefix_count(empty) < take;
+    if (mine_slot) {
+      const int4 en = front[q.fh + prefix_count(empty)];
+      const int32_t svc = en.w & 0xffff;
+      const int32_t bu = (int32_t)((uint32_t)en.w >> 16);
+      sl = make_int4(en.y, en.z, svc, bu);
+    }
+    wait_add += wave_sum(mine_slot ? (int64_t)(t - sl.y) : 0);
+    svc_out += wave_sum(mine_slot ? (int64_t)sl.z : 0);
+    empty &= ~ballot(mine_slot);
+    q.fh += take;
+    q.fn -= take;
+    q.qlen -= take;
+    started += take;
+  }
+  q.backlog -= (int32_t)svc_out;
+
+  // ---- one tick of service; completions in slot order ----
+  const bool busy_slot = lane < a.S && sl.x >= 0;
+  if (busy_slot) sl.z -= 1;
+  const bool done = busy_slot && sl.z == 0;
+  const uint64_t done_mask = ballot(done);
+  const int32_t lat = t - sl.y + 1;
+  uint64_t dm = done_mask;
+  int32_t ewma = q.ewma;
+  while (dm) {
+    const int s = __builtin_ctzll(dm);
+    dm &= dm - 1;
+    const int32_t ls = shfl((int32_t)lat, s);
+    const int64_t delta = (int64_t)ls * 256 - ewma;
+    const int64_t stepv = delta >= 0 ? (delta >> 3) : -((-delta + 7) >> 3);
+    ewma = (int32_t)(ewma + stepv);
+  }
+  const int32_t completed = popc64(done_mask);
+  const int64_t lat_add = wave_sum(done ? (int64_t)lat : 0);
+  const int32_t slo_add = popc64(ballot(done && lat <= sl.w));
+  if (done) sl = make_int4(-1, 0, 0, 0);
+  q.busy = popc64(ballot(lane < a.S && sl.x >= 0));
+  q.ewma = ewma;
+  q.next_id += n;
+
+  // ---- write back ----
+  if (lane < a.S) a.slots[(size_t)em * a.S + lane] = sl;
+  int64_t* cnt = a.cnt + (size_t)em * C_NUM;
+  if (lane == 0) {
+    rec->qlen = q.qlen; rec->busy = q.busy; rec->ewma = q.ewma; rec->backlog = q.backlog;
+    rec->fh = q.fh; rec->fn = q.fn; rec->P = q.P; rec->next_id = q.next_id;
+    cnt[C_REJ_OVERFLOW] += routed - accepted;
+    cnt[C_ENQUEUED] += accepted;
+    cnt[C_STARTED] += started;
+    cnt[C_COMPLETED] += completed;
+    cnt[C_SLO_MET] += slo_add;
+    cnt[C_LAT_SUM] += lat_add;
+    cnt[C_WAIT_SUM] += wait_add;
+    if (m == 0) {
+      a.env_cnt[(size_t)e * 2] += n;
+      a.env_cnt[(size_t)e * 2 + 1] += nomodel;
+    }
+  }
+  if (lane < a.K) a.hist[(size_t)e * a.A + m * a.K + lane] += hist_add;
+}
+
+}  // namespace
+
+hipError_t launch_schedule(const SchedArgs& a, hipStream_t s) {
+  const int64_t waves = (int64_t)a.E * a.M;
+  const unsigned blocks = (unsigned)((waves + 3) / 4);
+  hipLaunchKernelGGL(schedule_kernel, dim3(blocks), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace im

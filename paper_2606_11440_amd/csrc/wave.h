@@ -1,0 +1,113 @@
+// Wavefront primitives for gfx950 (64-lane waves).
+//
+// Ballot / prefix counts (mbcnt), cross-lane exchanges, a 64-lane bitonic
+// sort network on 64-bit keys, and fp32 -> bf16 round-to-nearest-even.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace im {
+
+constexpr int kWave = 64;
+
+__device__ __forceinline__ int lane_id() { return __lane_id(); }
+
+// 64-bit mask of lanes where pred holds.
+__device__ __forceinline__ uint64_t ballot(bool pred) { return __ballot(pred); }
+
+// Number of set bits of `mask` strictly below this lane.
+__device__ __forceinline__ int prefix_count(uint64_t mask) {
+  uint32_t lo = (uint32_t)mask, hi = (uint32_t)(mask >> 32);
+  return (int)__builtin_amdgcn_mbcnt_hi(hi, __builtin_amdgcn_mbcnt_lo(lo, 0u));
+}
+
+__device__ __forceinline__ int popc64(uint64_t m) { return __popcll(m); }
+
+// Position of the r-th (0-based) set bit of m; m must have more than r bits.
+__device__ __forceinline__ int nth_set_bit(uint64_t m, int r) {
+  int pos = 0;
+#pragma unroll
+  for (int w = 32; w >= 1; w >>= 1) {
+    uint64_t low = m & ((w == 64) ? ~0ull : ((1ull << w) - 1ull));
+    int c = __popcll(low);
+    if (r >= c) { r -= c; m >>= w; pos += w; }
+    else { m = low; }
+  }
+  return pos;
+}
+
+__device__ __forceinline__ int32_t shfl(int32_t v, int src) { return __shfl(v, src, kWave); }
+__device__ __forceinline__ int64_t shfl(int64_t v, int src) {
+  int32_t lo = __shfl((int32_t)(uint32_t)v, src, kWave);
+  int32_t hi = __shfl((int32_t)(v >> 32), src, kWave);
+  return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+}
+__device__ __forceinline__ int32_t shfl_xor(int32_t v, int m) { return __shfl_xor(v, m, kWave); }
+__device__ __forceinline__ int64_t shfl_xor(int64_t v, int m) {
+  int32_t lo = __shfl_xor((int32_t)(uint32_t)v, m, kWave);
+  int32_t hi = __shfl_xor((int32_t)(v >> 32), m, kWave);
+  return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+}
+
+// Wave-wide sums (every lane gets the result).
+__device__ __forceinline__ int64_t wave_sum(int64_t v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v += shfl_xor(v, m);
+  return v;
+}
+__device__ __forceinline__ uint64_t wave_or(uint64_t v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v |= (uint64_t)shfl_xor((int64_t)v, m);
+  return v;
+}
+
+// One compare-exchange stage of a bitonic network: this lane keeps the
+// smaller key if it is the "low" end of an ascending pair.
+template <int NP>
+__device__ __forceinline__ void cmpx(int64_t& k, int32_t (&p)[NP], int stride, bool ascending) {
+  const int lane = lane_id();
+  int64_t pk = shfl_xor(k, stride);
+  int32_t pp[NP];
+#pragma unroll
+  for (int i = 0; i < NP; ++i) pp[i] = shfl_xor(p[i], stride);
+  const bool low = (lane & stride) == 0;
+  const bool take = (low == ascending) ? (pk < k) : (pk > k);
+  if (take) {
+    k = pk;
+#pragma unroll
+    for (int i = 0; i < NP; ++i) p[i] = pp[i];
+  }
+}
+
+// Ascending bitonic sort of 64 keys (one per lane), payload carried along.
+template <int NP>
+__device__ __forceinline__ void bitonic_sort64(int64_t& k, int32_t (&p)[NP]) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int size = 2; size <= kWave; size <<= 1) {
+#pragma unroll
+    for (int stride = size >> 1; stride > 0; stride >>= 1)
+      cmpx<NP>(k, p, stride, (lane & size) == 0 || size == kWave);
+  }
+}
+
+// Ascending sort of a bitonic sequence of 64 keys.
+template <int NP>
+__device__ __forceinline__ void bitonic_merge64(int64_t& k, int32_t (&p)[NP]) {
+#pragma unroll
+  for (int stride = kWave >> 1; stride > 0; stride >>= 1) cmpx<NP>(k, p, stride, true);
+}
+
+// fp32 -> bf16 bits, round to nearest even (NaN kept quiet).
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) {
+  return __uint_as_float((uint32_t)h << 16);
+}
+
+}  // namespace im
