@@ -1,0 +1,235 @@
+"""Benchmark of the batched route-and-schedule tick on one MI355X.
+
+A step is one tick of the whole hot path over one batch of synthetic input:
+im_route (features, policy MLP, masked argmax) then im_schedule (admission,
+keys, queue insertion, service, accounting) over every env. Inputs for all
+ticks are generated up front and resident in HBM before timing starts.
+
+Prints ONE JSON line (see the keys below). `roofline` is computed for the
+kernel that takes the larger share of the timed region, from its average
+duration measured with HIP events recorded on the launch stream around every
+launch. `cpu_baseline` is the oracle (plain C++, fp64 policy) timed on the
+host cores over a bounded sample of the same workload."""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "env-ticks/s and routed requests/s at 4096 envs; % of HBM/MFMA roofline"
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+PEAK_F32_TFLOPS = 157.3        # MI355X fp32 matrix/vector
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+
+
+def algorithmic_flops_per_tick(cfg, n_requests):
+    """Minimal policy FLOPs of one tick: per request the MLP without the
+    per-env load-statistics columns of layer 1, plus once per env those 4M
+    columns (they are shared by every request of the env)."""
+    widths = cfg["widths"]
+    H1 = widths[0]
+    per_req = 2 * (cfg["embed_dim"] + 1) * H1
+    prev = H1
+    for w in widths[1:]:
+        per_req += 2 * prev * w
+        prev = w
+    per_env = 2 * 4 * cfg["M"] * H1
+    return per_req * n_requests + per_env * cfg["E"]
+
+
+def algorithmic_bytes_schedule(cfg, n_requests, n_enqueued, n_started):
+    """Bytes the schedule step must move: per request its record (budget,
+    base_svc, action = 8 B); 16 B per queue entry written at enqueue and read
+    at dequeue; per (env, model) its 64 B record and its slots, read and
+    written; per env its counters."""
+    EM = cfg["E"] * cfg["M"]
+    return (8 * n_requests + 16 * (n_enqueued + n_started)
+            + EM * 2 * (64 + 16 * cfg["max_slots"] + 8 * 8) + cfg["E"] * 2 * 16)
+
+
+def source_hash(*names):
+    h = hashlib.sha256()
+    for n in names:
+        with open(os.path.join(ROOT, "paper_2606_11440_amd", "csrc", n), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(kernel, workload_tag, src_hash):
+    """HBM bytes per launch from a committed rocprofv3 --pmc summary, or None
+    when there is none or the kernel source changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload_tag}_pmc.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        d = json.load(f)
+    if d.get("source_hash") != src_hash:
+        return None
+    return d.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(cfg, W, b, emb_vals, cap, lb, ticks, Q, budget_s=15.0):
+    """The oracle on the host cores over a bounded sample: the first
+    `envs` envs over as many of the timed ticks as fit in ~budget_s."""
+    import oracle
+    import workload
+    threads = max(1, min(16, os.cpu_count() or 1))
+    envs = min(cfg["E"], 8 * threads)
+    o = oracle.Oracle(cfg, W, b, emb_vals, cap[:envs], lb, E=envs, threads=threads)
+    subs = [workload.gen.subset(a, 0, envs) for a in ticks]
+    t0 = time.perf_counter()
+    done = 0
+    for a in subs:
+        o.tick(a)
+        done += 1
+        if time.perf_counter() - t0 > budget_s:
+            break
+    dt = time.perf_counter() - t0
+    nreq = sum(int(s["q_idx"].size) for s in subs[:done])
+    return {"value": envs * done / dt, "unit": "env-ticks/s", "cores": threads, "kind": "oracle",
+            "sample": f"envs [0,{envs}) x first {done} ticks ({nreq} requests), "
+                      f"{dt:.1f} s wall, {nreq / dt:.0f} routed req/s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=None)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", default="c2")
+    ap.add_argument("--lam", type=float, default=None)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1 "
+                          "(envs shard across GPUs with no per-tick exchange, see the design notes)"}))
+        sys.exit(2)
+
+    import torch
+
+    import paper_2606_11440_amd as P
+    import workload
+
+    over = {}
+    if args.lam is not None:
+        over["lam"] = args.lam
+    cfg = workload.configs.get(args.config, **over)
+    T = cfg["T"]
+    W_ = args.warmup
+    K = args.steps if args.steps is not None else T - W_
+    if W_ + K > T:
+        over["T"] = W_ + K
+        cfg = workload.configs.get(args.config, **over)
+        T = cfg["T"]
+
+    # ---- inputs (host generation, then resident in HBM) ----
+    t_gen = time.perf_counter()
+    W, b = workload.gen.weights(cfg, args.seed)
+    Q = workload.gen.table_rows(cfg)
+    table, emb_vals = workload.gen.embedding(cfg, args.seed, rows=Q)
+    cap = workload.gen.capacities(cfg, args.seed)
+    lb = workload.gen.logit_bias(cfg)
+    counts = workload.gen.counts(cfg, args.seed)
+    ticks = [workload.gen.tick(cfg, args.seed, t, counts[t], Q) for t in range(W_ + K)]
+    emb_dev = torch.from_numpy(table.view(np.int16) if cfg["dtype"] == "bf16" else table).cuda()
+    dev = [P.device_arrivals(a) for a in ticks]
+    n_req = [int(a["q_idx"].size) for a in ticks]
+    acts = torch.empty(max(max(n_req), 1), dtype=torch.int32, device="cuda")
+    pool = P.Pool(cfg, W, b, emb_dev, cap, lb)
+    torch.cuda.synchronize()
+    gen_s = time.perf_counter() - t_gen
+
+    stream = torch.cuda.current_stream()
+    for t in range(W_):
+        pool.route(dev[t], acts, None, stream.cuda_stream)
+        pool.schedule(dev[t], acts, stream.cuda_stream)
+    torch.cuda.synchronize()
+
+    # ---- timed region: K ticks, events around every launch on the stream ----
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for k in range(K):
+        t = W_ + k
+        ev[k][0].record(stream)
+        pool.route(dev[t], acts, None, stream.cuda_stream)
+        ev[k][1].record(stream)
+        pool.schedule(dev[t], acts, stream.cuda_stream)
+        ev[k][2].record(stream)
+    end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    gpu_ms = start.elapsed_time(end)
+    route_ms = [ev[k][0].elapsed_time(ev[k][1]) for k in range(K)]
+    sched_ms = [ev[k][1].elapsed_time(ev[k][2]) for k in range(K)]
+    assert pool.error() == 0, "device error during the benchmark"
+
+    ms_per_step = gpu_ms / K
+    env_ticks = cfg["E"] * K
+    routed = sum(n_req[W_:W_ + K])
+    value = env_ticks / (gpu_ms / 1e3)
+
+    # ---- roofline of the dominant kernel ----
+    st = pool.state(0, cfg["E"], with_queues=False)
+    route_avg = float(np.mean(route_ms))
+    sched_avg = float(np.mean(sched_ms))
+    flops = np.mean([algorithmic_flops_per_tick(cfg, n) for n in n_req[W_:W_ + K]])
+    peak_f = PEAK_BF16_TFLOPS if cfg["dtype"] == "bf16" else PEAK_F32_TFLOPS
+    tag = f"{args.config}_lam{int(cfg['lam'])}"
+    if route_avg >= sched_avg:
+        achieved = flops / (route_avg * 1e-3) / 1e12
+        roof = {"kernel": "route_" + cfg["dtype"], "bound": "mfma", "achieved": achieved,
+                "peak": peak_f, "unit": "TFLOP/s", "frac": achieved / peak_f,
+                "traffic": load_traffic("route", tag, source_hash("route.hip")),
+                "avg_launch_us": route_avg * 1e3,
+                "algorithmic_per_launch": f"{flops:.4g} FLOP"}
+    else:
+        enq = int(st["enqueued"].sum())
+        sta = int(st["started"].sum())
+        byts = algorithmic_bytes_schedule(cfg, routed / K, enq / T, sta / T)
+        achieved = byts / (sched_avg * 1e-3) / 1e9
+        roof = {"kernel": "schedule", "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS,
+                "traffic": load_traffic("schedule", tag, source_hash("schedule.hip")),
+                "avg_launch_us": sched_avg * 1e3,
+                "algorithmic_per_launch": f"{byts:.4g} B"}
+
+    line = {
+        "metric": METRIC, "value": value, "unit": "env-ticks/s", "n_gpus": 1, "steps": K,
+        "warmup": W_, "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": cfg["dtype"], "data": "synthetic",
+        "config": {"workload": f"{args.config}: {cfg['E']} envs, M={cfg['M']} K={cfg['K']}, "
+                               f"lambda={cfg['lam']:g}/tick, qcap {cfg['qcap']}, MLP "
+                               f"{cfg['feat_dim']}->" + "->".join(map(str, cfg["widths"])) +
+                               f" {cfg['dtype']}, ticks {W_}..{W_ + K - 1} of {T}",
+                   "envs": cfg["E"], "requests_per_tick": routed / K, "parallelism": "single GPU"},
+        "routed_req_per_s": routed / (gpu_ms / 1e3),
+        "kernels_us": {"route_avg": route_avg * 1e3, "schedule_avg": sched_avg * 1e3,
+                       "host_wall_ms": wall * 1e3},
+        "roofline": roof,
+        "input_gen_s": gen_s,
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(cfg, W, b, emb_vals, cap, lb, ticks[W_:W_ + K], Q,
+                                            args.cpu_seconds)
+    else:
+        line["cpu_baseline"] = None
+    pool.close()
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -45,9 +45,9 @@ class Pool:
     def tick(self, arr, actions_out=None, stream=None):
         im_tick(self.h, arr, actions_out, stream)
 
-    def state(self, env_begin=0, env_count=None):
+    def state(self, env_begin=0, env_count=None, with_queues=True):
         n = self.E - env_begin if env_count is None else env_count
-        return im_read_state(self.h, env_begin, n, self.M, self.A, self.S, self.qcap)
+        return im_read_state(self.h, env_begin, n, self.M, self.A, self.S, self.qcap, with_queues)
 
     def write_state(self, env_begin, s):
         im_write_state(self.h, env_begin, s)

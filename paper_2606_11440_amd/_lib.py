@@ -203,22 +203,27 @@ def im_last_error(pool=None) -> str:
     return load().im_last_error(pool).decode()
 
 
-def im_read_state(pool, env_begin: int, env_count: int, M: int, A: int, S: int, qcap: int) -> dict:
+def im_read_state(pool, env_begin: int, env_count: int, M: int, A: int, S: int, qcap: int,
+                  with_queues: bool = True) -> dict:
     """Snapshot of envs [env_begin, env_begin + env_count) as numpy arrays in
-    the layout the tests compare (same keys as the oracle's snapshot)."""
+    the layout the tests compare (same keys as the oracle's snapshot).
+    with_queues=False skips the queue contents (then "queues" is None)."""
     E = env_count
     envs = np.zeros(E, ENV_DT)
     models = np.zeros(E * M, MODEL_DT)
     slots = np.zeros(E * M * S, SLOT_DT)
-    queues = np.zeros(E * M * qcap, ENTRY_DT)
+    queues = np.zeros(E * M * (qcap if with_queues else 1), ENTRY_DT)
     hist = np.zeros(E * A, np.int64)
     tick = ctypes.c_int32(0)
     _check(load().im_read_state(pool, env_begin, env_count, ctypes.byref(tick), _hptr(envs),
-                                _hptr(models), _hptr(slots), _hptr(queues), _hptr(hist)), pool)
+                                _hptr(models), _hptr(slots),
+                                _hptr(queues) if with_queues else None, _hptr(hist)), pool)
     md = models.reshape(E, M)
-    q = queues.reshape(E, M, qcap)
-    qarr = np.stack([q["key"], q["id"], q["t_arr"], q["svc"].astype(np.int32),
-                     q["budget"].astype(np.int32)], axis=-1).astype(np.int32)
+    qarr = None
+    if with_queues:
+        q = queues.reshape(E, M, qcap)
+        qarr = np.stack([q["key"], q["id"], q["t_arr"], q["svc"].astype(np.int32),
+                         q["budget"].astype(np.int32)], axis=-1).astype(np.int32)
     sl = slots.reshape(E, M, S)
     sarr = np.stack([sl["id"], sl["t_arr"], sl["rem"], sl["budget"]], axis=-1).astype(np.int32)
     out = dict(t=int(tick.value), next_id=envs["next_id"].copy(), arrived=envs["arrived"].copy(),
