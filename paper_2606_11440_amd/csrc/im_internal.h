@@ -21,6 +21,18 @@ static_assert(sizeof(ModelRec) == 64, "ModelRec layout");
 
 constexpr int kFront = 64;       // front capacity (one entry per lane)
 
+// Per-env snapshot row read by the route step, written by the schedule step
+// (and by snapshot_kernel after host-side state changes): the 4M load-stat
+// features in stat-major order as fp32 (each one product of an integer and a
+// reciprocal rounded once to fp32), then one validity byte per model (enabled,
+// c_m > 0 and queue below capacity), padded so 8 consecutive floats can always
+// be read from any feature index < 4M.
+__host__ __device__ inline int snap_stride(int M) {
+  const int n = 4 * M + (M + 3) / 4 + 8;
+  return (n + 7) & ~7;
+}
+__host__ __device__ inline int snap_valid_offset(int M) { return 4 * M; }   // in floats
+
 // Counter slots per (env, model), int64.
 enum { C_REJ_OVERFLOW = 0, C_ENQUEUED, C_STARTED, C_COMPLETED, C_SLO_MET, C_LAT_SUM,
        C_WAIT_SUM, C_NUM = 8 };
@@ -41,12 +53,12 @@ struct RouteArgs {
   const void* W[3];                   // packed weights per layer
   const float* bias[3];               // packed biases per layer (D-register order)
   const ModelRec* ms;
-  float inv_qcap, inv_lat, inv_bud;
-  const float* inv_tab;               // device [2*(IM_MAX_SLOTS+1)]: 1/max(c,1), then
-                                      // 1/(max(c,1)*budget_max), for c = 0..IM_MAX_SLOTS
+  const float* snap;                  // [E * snap_stride(M)]
+  float inv_bud;
   int32_t* actions;
   float* logits;
   int32_t* err;
+  int32_t persistent_blocks;          // grid of the persistent kernels (0: never use them)
 };
 
 struct SchedArgs {
@@ -67,6 +79,9 @@ struct SchedArgs {
   int4* front;        // [E*M*kFront]
   int4* pool;         // [E*M*qcap]
   int32_t* err;
+  float* snap;        // [E * snap_stride(M)]
+  float inv_qcap, inv_lat;
+  const float* inv_tab;  // [2*(IM_MAX_SLOTS+1)]: 1/max(c,1), then 1/(max(c,1)*budget_max)
 };
 
 // Host-side launchers (defined in the .hip files).
@@ -74,5 +89,7 @@ bool route_supported(int dtype, int hidden, int n_layers, int out_tiles);
 hipError_t launch_route(const RouteArgs& a, int dtype, int hidden, int n_layers, int out_tiles,
                         hipStream_t s);
 hipError_t launch_schedule(const SchedArgs& a, hipStream_t s);
+// Recompute the snapshot rows of envs [e0, e0 + ne) from the model records.
+hipError_t launch_snapshot(const SchedArgs& a, int e0, int ne, hipStream_t s);
 
 }  // namespace im

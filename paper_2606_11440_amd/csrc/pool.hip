@@ -34,12 +34,16 @@ struct im_pool {
   int4* slots = nullptr;
   int4* front = nullptr;
   int4* qpool = nullptr;
+  float* snap = nullptr;
   int32_t* err = nullptr;
   int32_t* act_buf = nullptr;
   int64_t act_cap = 0;
   int32_t t = 0;
+  int32_t cu_count = 0;
   std::string last_error;
 };
+
+static im::SchedArgs sched_args(im_pool* p);
 
 namespace {
 
@@ -114,7 +118,7 @@ void free_pool(im_pool* p) {
     if (p->bias[l]) (void)hipFree(p->bias[l]);
   }
   void* bufs[] = {p->inv_tab, p->ms, p->cnt, p->env_cnt, p->hist, p->slots,
-                  p->front, p->qpool, p->err, p->act_buf};
+                  p->front, p->qpool, p->snap, p->err, p->act_buf};
   for (void* b : bufs) if (b) (void)hipFree(b);
   delete p;
 }
@@ -164,6 +168,9 @@ im_status im_pool_create(const im_pool_desc* desc, const float* const* W, const 
   p->Q = n_queries;
   p->emb = emb;
   (void)hipGetDevice(&p->device);
+  if (hipDeviceGetAttribute(&p->cu_count, hipDeviceAttributeMultiprocessorCount, p->device) !=
+      hipSuccess)
+    p->cu_count = 0;
   hipStream_t s = (hipStream_t)stream;
   im_status st = IM_OK;
 
@@ -246,14 +253,17 @@ im_status im_pool_create(const im_pool_desc* desc, const float* const* W, const 
   }
   if (st == IM_OK) st = zalloc(p, &p->front, EM * im::kFront);
   if (st == IM_OK) st = zalloc(p, &p->qpool, EM * (size_t)d.queue_cap);
+  if (st == IM_OK) st = zalloc(p, &p->snap, (size_t)d.n_envs * im::snap_stride(d.n_models));
   if (st == IM_OK) st = zalloc(p, &p->err, 1);
   if (st == IM_OK) {
     p->act_cap = (int64_t)d.n_envs * d.max_arrivals_per_env_tick;
     st = zalloc(p, &p->act_buf, (size_t)p->act_cap);
   }
   if (st == IM_OK) {
-    hipError_t e = hipStreamSynchronize(s);
-    if (e != hipSuccess) st = hip_fail(p, e, "hipStreamSynchronize");
+    hipError_t e = hipDeviceSynchronize();
+    if (e == hipSuccess) e = im::launch_snapshot(sched_args(p), 0, d.n_envs, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) st = hip_fail(p, e, "initial snapshot");
   }
   if (st != IM_OK) {
     g_create_error = p->last_error;
@@ -288,13 +298,12 @@ static im::RouteArgs route_args(im_pool* p, const im_arrivals* arr, int32_t* act
   a.emb = p->emb;
   for (int l = 0; l < 3; ++l) { a.W[l] = p->W[l]; a.bias[l] = p->bias[l]; }
   a.ms = p->ms;
-  a.inv_qcap = p->inv_qcap;
-  a.inv_lat = p->inv_lat;
+  a.snap = p->snap;
   a.inv_bud = p->inv_bud;
-  a.inv_tab = p->inv_tab;
   a.actions = actions;
   a.logits = logits;
   a.err = p->err;
+  a.persistent_blocks = p->cu_count;
   return a;
 }
 
@@ -316,13 +325,20 @@ im_status im_schedule(im_pool* p, const im_arrivals* arr, const int32_t* actions
   if (st != IM_OK) return st;
   if (arr->n_total > 0 && !actions) return fail(p, IM_EINVAL, "actions is NULL");
   if (p->t == INT32_MAX - 65536) return fail(p, IM_EINVAL, "tick counter exhausted");
-  im::SchedArgs a{};
+  im::SchedArgs a = sched_args(p);
   a.offsets = arr->offsets;
   a.q_idx = arr->q_idx;
   a.budget = arr->budget;
   a.base_svc = arr->base_svc;
   a.actions = actions;
   a.n_total = arr->n_total;
+  IM_HIP(p, im::launch_schedule(a, (hipStream_t)stream));
+  p->t += 1;
+  return IM_OK;
+}
+
+static im::SchedArgs sched_args(im_pool* p) {
+  im::SchedArgs a{};
   a.E = p->d.n_envs;
   a.M = p->d.n_models;
   a.K = p->d.n_depths;
@@ -341,9 +357,11 @@ im_status im_schedule(im_pool* p, const im_arrivals* arr, const int32_t* actions
   a.front = p->front;
   a.pool = p->qpool;
   a.err = p->err;
-  IM_HIP(p, im::launch_schedule(a, (hipStream_t)stream));
-  p->t += 1;
-  return IM_OK;
+  a.snap = p->snap;
+  a.inv_qcap = p->inv_qcap;
+  a.inv_lat = p->inv_lat;
+  a.inv_tab = p->inv_tab;
+  return a;
 }
 
 im_status im_tick(im_pool* p, const im_arrivals* arr, int32_t* actions_out, void* stream) {
@@ -364,6 +382,7 @@ im_status im_set_enabled(im_pool* p, int32_t env, int32_t model, int32_t enabled
   hipLaunchKernelGGL(set_field_kernel, dim3(1), dim3(1), 0, (hipStream_t)stream, &r->enabled,
                      enabled ? 1 : 0);
   IM_HIP(p, hipGetLastError());
+  IM_HIP(p, im::launch_snapshot(sched_args(p), env, 1, (hipStream_t)stream));
   return IM_OK;
 }
 
@@ -375,6 +394,7 @@ im_status im_set_capacity(im_pool* p, int32_t env, int32_t model, int32_t capaci
   ModelRec* r = p->ms + (size_t)env * p->d.n_models + model;
   hipLaunchKernelGGL(set_field_kernel, dim3(1), dim3(1), 0, (hipStream_t)stream, &r->cap, capacity);
   IM_HIP(p, hipGetLastError());
+  IM_HIP(p, im::launch_snapshot(sched_args(p), env, 1, (hipStream_t)stream));
   return IM_OK;
 }
 
@@ -541,6 +561,7 @@ im_status im_write_state(im_pool* p, int32_t env_begin, int32_t env_count, int32
     IM_HIP(p, hipMemcpy(p->env_cnt + (size_t)env_begin * 2, ec.data(), ec.size() * 8, hipMemcpyHostToDevice));
     IM_HIP(p, hipMemcpy(p->hist + (size_t)env_begin * A, hist, (size_t)env_count * A * 8, hipMemcpyHostToDevice));
   }
+  IM_HIP(p, im::launch_snapshot(sched_args(p), env_begin, env_count, nullptr));
   IM_HIP(p, hipDeviceSynchronize());
   p->t = tick;
   return IM_OK;

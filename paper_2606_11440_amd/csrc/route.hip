@@ -45,6 +45,17 @@ struct RowCtx {
   uint64_t amask;   // bit a set when action a is valid
 };
 
+// Valid actions of env e: bit a set when model a / K is valid in the env's
+// snapshot row (enabled, c_m > 0, queue below capacity).
+__device__ __forceinline__ uint64_t action_mask(const RouteArgs& a, int e) {
+  const uint8_t* v = (const uint8_t*)(a.snap + (size_t)e * snap_stride(a.M) + snap_valid_offset(a.M));
+  const uint64_t kmask = (a.K >= 64) ? ~0ull : ((1ull << a.K) - 1ull);
+  uint64_t am = 0;
+  for (int m = 0; m < a.M; ++m)
+    if (v[m]) am |= kmask << (m * a.K);
+  return am;
+}
+
 __device__ __forceinline__ RowCtx row_setup(const RouteArgs& a, int32_t r) {
   RowCtx c;
   c.r = r;
@@ -61,59 +72,59 @@ __device__ __forceinline__ RowCtx row_setup(const RouteArgs& a, int32_t r) {
   c.bad_q = q < 0 || (int64_t)q >= a.Q;
   c.q = c.bad_q ? 0 : q;
   c.budget = a.budget[rr];
-  // Valid actions: model enabled, c_m > 0 and its queue below capacity.
-  const ModelRec* ms = a.ms + (size_t)c.e * a.M;
-  const uint64_t kmask = (a.K >= 64) ? ~0ull : ((1ull << a.K) - 1ull);
-  uint64_t am = 0;
-  for (int m = 0; m < a.M; ++m) {
-    const bool ok = ms[m].enabled != 0 && ms[m].cap > 0 && ms[m].qlen < a.qcap;
-    if (ok) am |= kmask << (m * a.K);
-  }
-  c.amask = am;
+  c.amask = action_mask(a, c.e);
   return c;
 }
 
-// Feature k >= embed_dim of a row: load statistics of the row's env (stat-major:
-// queue depth of all models, then busy/c_m, latency EWMA, backlog), then the
-// normalised budget, then zeros. Each is one fp32 product of an integer and a
-// reciprocal rounded once to fp32 on the host.
-__device__ __forceinline__ float tail_feature(const RouteArgs& a, const RowCtx& c, int k,
-                                              const float* inv_tab) {
+// Feature k >= embed_dim of a row: the env's load statistics (stat-major:
+// queue depth of all models, busy/c_m, latency EWMA, backlog; read from the
+// snapshot row), then the normalised budget, then zeros.
+__device__ __forceinline__ float tail_feature(const RouteArgs& a, const RowCtx& c, int k) {
   const int k2 = k - a.embed_dim;
-  if (k2 < 4 * a.M) {
-    const int s = k2 / a.M;
-    const int m = k2 - s * a.M;
-    const ModelRec& x = a.ms[(size_t)c.e * a.M + m];
-    int cap = x.cap < 0 ? 0 : (x.cap > IM_MAX_SLOTS ? IM_MAX_SLOTS : x.cap);
-    switch (s) {
-      case 0: return (float)x.qlen * a.inv_qcap;
-      case 1: return (float)x.busy * inv_tab[cap];
-      case 2: return (float)x.ewma * a.inv_lat;
-      default: return (float)x.backlog * inv_tab[IM_MAX_SLOTS + 1 + cap];
-    }
-  }
+  if (k2 < 4 * a.M) return a.snap[(size_t)c.e * snap_stride(a.M) + k2];
   if (k2 == 4 * a.M) return (float)c.budget * a.inv_bud;
   return 0.f;
 }
 
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+// Two fp32 values to packed bf16 (round to nearest even), one
+// v_cvt_pk_bf16_f32; element 0 in the low half.
 __device__ __forceinline__ uint32_t pack2(float lo, float hi) {
-  return (uint32_t)f32_to_bf16_rne(lo) | ((uint32_t)f32_to_bf16_rne(hi) << 16);
+  const f32x2 v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
 }
 
 // Layer-1 B fragment of K block kb (bf16): features 16 kb + 8 g + j, j = 0..7.
-__device__ __forceinline__ u32x4 gather_bf16(const RouteArgs& a, const RowCtx& c, int kb, int g,
-                                             const float* inv_tab) {
+__device__ __forceinline__ u32x4 gather_bf16(const RouteArgs& a, const RowCtx& c, int kb, int g) {
   const int k0 = 16 * kb + 8 * g;
   const uint16_t* emb = (const uint16_t*)a.emb;
-  if (k0 + 8 <= a.embed_dim && (a.embed_dim & 7) == 0) {
+  const bool aligned = (a.embed_dim & 7) == 0;
+  if (aligned && k0 + 8 <= a.embed_dim)
     return *(const u32x4*)(emb + (size_t)c.q * a.embed_dim + k0);
-  }
   float f[8];
+  if (aligned && k0 >= a.embed_dim) {
+    // 8 tail features: two aligned float4 loads of the snapshot row, then
+    // the budget feature and zero padding selected by index.
+    const int k2 = k0 - a.embed_dim;
+    const float* row = a.snap + (size_t)c.e * snap_stride(a.M) + k2;
+    const float4 lo = *(const float4*)row;
+    const float4 hi = *(const float4*)(row + 4);
+    const float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+    const float fb = (float)c.budget * a.inv_bud;
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const int k = k0 + j;
-    f[j] = k < a.embed_dim ? bf16_to_f32(emb[(size_t)c.q * a.embed_dim + k])
-                           : tail_feature(a, c, k, inv_tab);
+    for (int j = 0; j < 8; ++j) {
+      const int kk = k2 + j;
+      f[j] = kk < 4 * a.M ? v[j] : (kk == 4 * a.M ? fb : 0.f);
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int k = k0 + j;
+      f[j] = k < a.embed_dim ? bf16_to_f32(emb[(size_t)c.q * a.embed_dim + k])
+                             : tail_feature(a, c, k);
+    }
   }
   u32x4 v;
   v.x = pack2(f[0], f[1]);
@@ -176,7 +187,6 @@ __device__ __forceinline__ void tile_to_frags(const f32x16& acc, const float* bi
 
 template <int H, int NL, int AT>
 __global__ __launch_bounds__(256) void route_bf16(RouteArgs a) {
-  const float* inv_tab = a.inv_tab;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n = lane & 31, g = lane >> 5;
   const int32_t row0 = (int32_t)(blockIdx.x * 4 + wave) * 32;
@@ -189,7 +199,7 @@ __global__ __launch_bounds__(256) void route_bf16(RouteArgs a) {
 #pragma unroll
   for (int T = 0; T < TH; ++T) acc[T] = f32x16{};
   for (int kb = 0; kb < a.k1; ++kb) {
-    const u32x4 xb = gather_bf16(a, c, kb, g, inv_tab);
+    const u32x4 xb = gather_bf16(a, c, kb, g);
 #pragma unroll
     for (int T = 0; T < TH; ++T) acc[T] = mfma_bf16(W1[(T * a.k1 + kb) * 64 + lane], xb, acc[T]);
   }
@@ -243,7 +253,6 @@ __global__ __launch_bounds__(256) void route_bf16(RouteArgs a) {
 
 template <int H, int NL, int AT>
 __global__ __launch_bounds__(256) void route_f32(RouteArgs a) {
-  const float* inv_tab = a.inv_tab;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n = lane & 31, g = lane >> 5;
   const int32_t row0 = (int32_t)(blockIdx.x * 4 + wave) * 32;
@@ -259,7 +268,7 @@ __global__ __launch_bounds__(256) void route_f32(RouteArgs a) {
   for (int i = 0; i < a.k1; ++i) {
     const int k = 2 * i + g;
     const float x = k < a.embed_dim ? emb[(size_t)c.q * a.embed_dim + k]
-                                    : tail_feature(a, c, k, inv_tab);
+                                    : tail_feature(a, c, k);
 #pragma unroll
     for (int T = 0; T < TH; ++T) acc[T] = mfma_f32(W1[(T * a.k1 + i) * 64 + lane], x, acc[T]);
   }
@@ -312,6 +321,217 @@ __global__ __launch_bounds__(256) void route_f32(RouteArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Persistent variant for policies whose deeper layers fit in LDS.
+//
+// Each block (4 waves, one per SIMD) copies the packed weights of layers >= 2
+// (and of layer 1 when it also fits) into LDS once, then loops over 256-row
+// tiles. A wave owns 64 rows as two 32-row MFMA column tiles, so every weight
+// fragment read from LDS feeds two MFMAs. Layer outputs are produced in chunks
+// of 128 features; each hidden chunk is rounded to bf16 fragments right away.
+// ---------------------------------------------------------------------------
+
+// Env of rows r (two per lane) for a wave whose rows lie in [rfirst, rlast]:
+// one coalesced load of a 64-entry window of offsets around an interpolated
+// guess; a uniform binary search when the guess misses.
+__device__ __forceinline__ int32_t find_env_bsearch(const RouteArgs& a, int32_t r) {
+  int lo = 0, hi = a.E;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (a.offsets[mid] <= r) lo = mid; else hi = mid - 1;
+  }
+  return lo < a.E ? lo : a.E - 1;
+}
+
+__device__ __forceinline__ void find_envs2(const RouteArgs& a, int32_t rfirst, int32_t rlast,
+                                           const int32_t (&r)[2], int32_t (&e)[2]) {
+  const int lane = lane_id();
+  const int64_t guess = (int64_t)rfirst * a.E / a.n_total;
+  int32_t e_lo = (int32_t)guess - 16;
+  e_lo = e_lo < 0 ? 0 : (e_lo > a.E - 1 ? a.E - 1 : e_lo);
+  int32_t wi = e_lo + lane;
+  int32_t ow = a.offsets[wi < a.E ? wi : a.E];
+  bool ok = shfl(ow, 0) <= rfirst && rlast < shfl(ow, 63);
+  if (!ok) {
+    e_lo = find_env_bsearch(a, rfirst);
+    wi = e_lo + lane;
+    ow = a.offsets[wi < a.E ? wi : a.E];
+    ok = rlast < shfl(ow, 63);
+  }
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    int pos = 0;
+#pragma unroll
+    for (int step = 64; step >= 1; step >>= 1) {
+      const int probe = pos + step - 1;
+      const int32_t v = shfl(ow, probe < 64 ? probe : 63);
+      if (probe < 64 && v <= r[j]) pos += step;
+    }
+    int32_t ej = e_lo + pos - 1;
+    if (!ok && pos == 64) ej = find_env_bsearch(a, r[j]);
+    e[j] = ej < 0 ? 0 : (ej > a.E - 1 ? a.E - 1 : ej);
+  }
+}
+
+__device__ __forceinline__ RowCtx row_setup_env(const RouteArgs& a, int32_t r, int32_t e) {
+  RowCtx c;
+  c.r = r;
+  c.live = r < a.n_total;
+  const int32_t rr = c.live ? r : a.n_total - 1;
+  c.e = e;
+  const int32_t q = a.q_idx[rr];
+  c.bad_q = q < 0 || (int64_t)q >= a.Q;
+  c.q = c.bad_q ? 0 : q;
+  c.budget = a.budget[rr];
+  c.amask = action_mask(a, e);
+  return c;
+}
+
+template <int H, int NL, int AT, int KB1, bool W1L>
+__global__ __launch_bounds__(256, 1) void route_bf16_lds(RouteArgs a) {
+  constexpr int TH = H / 32;
+  constexpr int KH = H / 16;
+  constexpr int N_W1 = TH * KB1 * 64;
+  constexpr int N_W2 = (NL == 3 ? TH : AT) * KH * 64;
+  constexpr int N_W3 = NL == 3 ? AT * KH * 64 : 0;
+  constexpr int N_LDS = (W1L ? N_W1 : 0) + N_W2 + N_W3;
+  __shared__ u32x4 lds[N_LDS];
+  {
+    int off = 0;
+    if (W1L) {
+      const u32x4* s1 = (const u32x4*)a.W[0];
+      for (int i = threadIdx.x; i < N_W1; i += 256) lds[i] = s1[i];
+      off = N_W1;
+    }
+    const u32x4* s2 = (const u32x4*)a.W[1];
+    for (int i = threadIdx.x; i < N_W2; i += 256) lds[off + i] = s2[i];
+    if (NL == 3) {
+      const u32x4* s3 = (const u32x4*)a.W[2];
+      for (int i = threadIdx.x; i < N_W3; i += 256) lds[off + N_W2 + i] = s3[i];
+    }
+  }
+  __syncthreads();
+  const u32x4* w1 = W1L ? (const u32x4*)lds : (const u32x4*)a.W[0];
+  const u32x4* w2 = lds + (W1L ? N_W1 : 0);
+  const u32x4* w3 = w2 + N_W2;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int n = lane & 31, g = lane >> 5;
+  const int n_tiles = (a.n_total + 255) / 256;
+  constexpr int C1 = TH < 2 ? TH : 2;       // layer-1 output tiles per chunk
+  constexpr int C2 = TH < 2 ? TH : 2;       // layer-2 output tiles per chunk
+
+  for (int tile = blockIdx.x; tile < n_tiles; tile += gridDim.x) {
+    // Keeps loop-invariant loads (biases, weights) inside the loop: hoisted
+    // out of it they would stay live in registers for the whole kernel.
+    asm volatile("" ::: "memory");
+    const int32_t r0 = tile * 256 + wave * 64;
+    if (r0 >= a.n_total) continue;
+    const int32_t rlast = (r0 + 63 < a.n_total ? r0 + 63 : a.n_total - 1);
+    const int32_t rows[2] = {r0 + n, r0 + 32 + n};
+    int32_t envs[2];
+    find_envs2(a, r0, rlast, rows, envs);
+    RowCtx c0 = row_setup_env(a, rows[0], envs[0]);
+    RowCtx c1 = row_setup_env(a, rows[1], envs[1]);
+
+    u32x4 x0[KB1], x1[KB1];
+#pragma unroll
+    for (int kb = 0; kb < KB1; ++kb) {
+      x0[kb] = gather_bf16(a, c0, kb, g);
+      x1[kb] = gather_bf16(a, c1, kb, g);
+    }
+    u32x4 h0[KH], h1[KH];
+#pragma unroll
+    for (int cc = 0; cc < TH / C1; ++cc) {
+      f32x16 p0[C1], p1[C1];
+#pragma unroll
+      for (int T = 0; T < C1; ++T) { p0[T] = f32x16{}; p1[T] = f32x16{}; }
+      u32x4 wc[C1];
+#pragma unroll
+      for (int T = 0; T < C1; ++T) wc[T] = w1[((cc * C1 + T) * KB1) * 64 + lane];
+#pragma unroll
+      for (int kb = 0; kb < KB1; ++kb) {
+        u32x4 wn[C1];
+#pragma unroll
+        for (int T = 0; T < C1; ++T)
+          wn[T] = w1[((cc * C1 + T) * KB1 + (kb + 1 < KB1 ? kb + 1 : kb)) * 64 + lane];
+#pragma unroll
+        for (int T = 0; T < C1; ++T) {
+          p0[T] = mfma_bf16(wc[T], x0[kb], p0[T]);
+          p1[T] = mfma_bf16(wc[T], x1[kb], p1[T]);
+        }
+#pragma unroll
+        for (int T = 0; T < C1; ++T) wc[T] = wn[T];
+        __builtin_amdgcn_sched_barrier(0);
+      }
+#pragma unroll
+      for (int T = 0; T < C1; ++T) {
+        const int Tg = cc * C1 + T;
+        tile_to_frags(p0[T], a.bias[0], Tg, g, h0[2 * Tg], h0[2 * Tg + 1]);
+        tile_to_frags(p1[T], a.bias[0], Tg, g, h1[2 * Tg], h1[2 * Tg + 1]);
+      }
+    }
+    f32x16 o0[AT], o1[AT];
+#pragma unroll
+    for (int T = 0; T < AT; ++T) { o0[T] = f32x16{}; o1[T] = f32x16{}; }
+    if constexpr (NL == 2) {
+#pragma unroll
+      for (int kb = 0; kb < KH; ++kb) {
+#pragma unroll
+        for (int T = 0; T < AT; ++T) {
+          const u32x4 w = w2[(T * KH + kb) * 64 + lane];
+          o0[T] = mfma_bf16(w, h0[kb], o0[T]);
+          o1[T] = mfma_bf16(w, h1[kb], o1[T]);
+        }
+      }
+      epilogue<AT>(a, c0, o0, a.bias[1], g);
+      epilogue<AT>(a, c1, o1, a.bias[1], g);
+    } else {
+#pragma unroll
+      for (int cc = 0; cc < TH / C2; ++cc) {
+        f32x16 p0[C2], p1[C2];
+#pragma unroll
+        for (int T = 0; T < C2; ++T) { p0[T] = f32x16{}; p1[T] = f32x16{}; }
+        u32x4 wc[C2];
+#pragma unroll
+        for (int T = 0; T < C2; ++T) wc[T] = w2[((cc * C2 + T) * KH) * 64 + lane];
+#pragma unroll
+        for (int kb = 0; kb < KH; ++kb) {
+          u32x4 wn[C2];
+#pragma unroll
+          for (int T = 0; T < C2; ++T)
+            wn[T] = w2[((cc * C2 + T) * KH + (kb + 1 < KH ? kb + 1 : kb)) * 64 + lane];
+#pragma unroll
+          for (int T = 0; T < C2; ++T) {
+            p0[T] = mfma_bf16(wc[T], h0[kb], p0[T]);
+            p1[T] = mfma_bf16(wc[T], h1[kb], p1[T]);
+          }
+#pragma unroll
+          for (int T = 0; T < C2; ++T) wc[T] = wn[T];
+          __builtin_amdgcn_sched_barrier(0);
+        }
+#pragma unroll
+        for (int T = 0; T < C2; ++T) {
+          const int Tg = cc * C2 + T;
+          u32x4 f00, f01, f10, f11;
+          tile_to_frags(p0[T], a.bias[1], Tg, g, f00, f01);
+          tile_to_frags(p1[T], a.bias[1], Tg, g, f10, f11);
+#pragma unroll
+          for (int To = 0; To < AT; ++To) {
+            const u32x4 wa = w3[(To * KH + 2 * Tg) * 64 + lane];
+            const u32x4 wb = w3[(To * KH + 2 * Tg + 1) * 64 + lane];
+            o0[To] = mfma_bf16(wa, f00, o0[To]);
+            o1[To] = mfma_bf16(wa, f10, o1[To]);
+            o0[To] = mfma_bf16(wb, f01, o0[To]);
+            o1[To] = mfma_bf16(wb, f11, o1[To]);
+          }
+        }
+      }
+      epilogue<AT>(a, c0, o0, a.bias[2], g);
+      epilogue<AT>(a, c1, o1, a.bias[2], g);
+    }
+  }
+}
+
 typedef void (*RouteKernel)(RouteArgs);
 
 template <int H, int NL>
@@ -340,6 +560,17 @@ RouteKernel pick(int dtype, int hidden, int at) {
   return nullptr;
 }
 
+// Persistent LDS-resident variants for the shapes that fit (bytes of packed
+// weights in LDS <= 160 KiB): returns nullptr when none applies.
+RouteKernel pick_lds(int dtype, int hidden, int n_layers, int out_tiles, int k1) {
+  if (dtype != IM_BF16) return nullptr;
+  if (hidden == 256 && n_layers == 3 && out_tiles == 1 && k1 == 6)
+    return route_bf16_lds<256, 3, 1, 6, false>;
+  if (hidden == 256 && n_layers == 2 && out_tiles == 1 && k1 == 7)
+    return route_bf16_lds<256, 2, 1, 7, true>;
+  return nullptr;
+}
+
 }  // namespace
 
 bool route_supported(int dtype, int hidden, int n_layers, int out_tiles) {
@@ -351,6 +582,16 @@ bool route_supported(int dtype, int hidden, int n_layers, int out_tiles) {
 
 hipError_t launch_route(const RouteArgs& a, int dtype, int hidden, int n_layers, int out_tiles,
                         hipStream_t s) {
+  if (a.n_total <= 0) return hipSuccess;
+  if (a.persistent_blocks > 0) {
+    RouteKernel kl = pick_lds(dtype, hidden, n_layers, out_tiles, a.k1);
+    if (kl) {
+      const int n_tiles = (a.n_total + 255) / 256;
+      const unsigned blocks = (unsigned)(n_tiles < a.persistent_blocks ? n_tiles : a.persistent_blocks);
+      hipLaunchKernelGGL(kl, dim3(blocks), dim3(256), 0, s, a);
+      return hipGetLastError();
+    }
+  }
   RouteKernel k = nullptr;
   if (out_tiles >= 1 && out_tiles <= 2) {
     if (n_layers == 2) k = pick<2>(dtype, hidden, out_tiles);

@@ -173,6 +173,38 @@ __device__ void refill(Queue& q, int4* front, int4* pool) {
   wave_mem_sync();
 }
 
+// Snapshot row entry of model m of env e from its state (one fp32 product
+// per load statistic; validity byte). `part` selects which value to write
+// (0..3: the four statistics, 4: validity), so lanes can share the work.
+__device__ __forceinline__ void write_snap_part(const SchedArgs& a, int e, int m, int part,
+                                                int32_t qlen, int32_t busy, int32_t ewma,
+                                                int32_t backlog, int32_t cap, int32_t enabled) {
+  float* row = a.snap + (size_t)e * snap_stride(a.M);
+  const int c = cap < 0 ? 0 : (cap > IM_MAX_SLOTS ? IM_MAX_SLOTS : cap);
+  switch (part) {
+    case 0: row[m] = (float)qlen * a.inv_qcap; break;
+    case 1: row[a.M + m] = (float)busy * a.inv_tab[c]; break;
+    case 2: row[2 * a.M + m] = (float)ewma * a.inv_lat; break;
+    case 3: row[3 * a.M + m] = (float)backlog * a.inv_tab[IM_MAX_SLOTS + 1 + c]; break;
+    case 4: {
+      uint8_t* v = (uint8_t*)(row + snap_valid_offset(a.M));
+      v[m] = (enabled != 0 && cap > 0 && qlen < a.qcap) ? 1 : 0;
+      break;
+    }
+    default: break;
+  }
+}
+
+__global__ void snapshot_kernel(SchedArgs a, int e0, int ne) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (int64_t)ne * a.M) return;
+  const int64_t em = (int64_t)e0 * a.M + i;
+  const int e = (int)(em / a.M), m = (int)(em - (int64_t)e * a.M);
+  const ModelRec r = a.ms[em];
+  for (int part = 0; part < 5; ++part)
+    write_snap_part(a, e, m, part, r.qlen, r.busy, r.ewma, r.backlog, r.cap, r.enabled);
+}
+
 __global__ __launch_bounds__(256) void schedule_kernel(SchedArgs a) {
   const int lane = threadIdx.x & 63;
   const int em = (int)blockIdx.x * 4 + (int)(threadIdx.x >> 6);
@@ -323,9 +355,18 @@ __global__ __launch_bounds__(256) void schedule_kernel(SchedArgs a) {
     }
   }
   if (lane < a.K) a.hist[(size_t)e * a.A + m * a.K + lane] += hist_add;
+  // Snapshot row for the next tick's route step.
+  if (lane < 5) write_snap_part(a, e, m, lane, q.qlen, q.busy, q.ewma, q.backlog, q.cap, q.enabled);
 }
 
 }  // namespace
+
+hipError_t launch_snapshot(const SchedArgs& a, int e0, int ne, hipStream_t s) {
+  const int64_t n = (int64_t)ne * a.M;
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(snapshot_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a, e0, ne);
+  return hipGetLastError();
+}
 
 hipError_t launch_schedule(const SchedArgs& a, hipStream_t s) {
   const int64_t waves = (int64_t)a.E * a.M;

@@ -209,3 +209,41 @@ def test_forced_actions_exhaustive():
         check_invariants(s, cfg, ctx=f"tick {ti}")
     assert gpu.error() == 0
     gpu.close()
+
+
+def test_bf16_hidden_rounding_matches_rne():
+    """The device's fp32 -> bf16 rounding of hidden activations, pinned to
+    round-to-nearest-even: with 0/1 selection weights each logit equals one
+    rounded hidden unit bf16(emb_a + b1_a), whose fp32 pre-image is known."""
+    torch = need_gpu()
+    import paper_2606_11440_amd as P
+    cfg = tiny_cfg(M=4, K=8, qcap=8, cap_hi=1, embed_dim=32, widths=[32, 32], dtype="bf16",
+                   E=1, max_arrivals=512)
+    A, Ed, D = cfg["A"], 32, cfg["feat_dim"]
+    rng = np.random.default_rng(9)
+    W1 = np.zeros((32, D), np.float32)
+    W1[np.arange(32), np.arange(32)] = 1.0
+    W2 = np.eye(32, dtype=np.float32)
+    b2 = np.zeros(32, np.float32)
+    # embedding values (bf16) in [1, 2) and fp32 biases with low mantissa bits
+    # set, so the sums exercise ties and both rounding directions
+    Q = 512
+    emb_f = (1.0 + rng.integers(0, 128, (Q, Ed)) / 128.0).astype(np.float32)
+    emb_bits = torch.from_numpy(emb_f).to(torch.bfloat16).view(torch.int16).numpy()
+    b1 = (rng.integers(0, 1 << 16, 32) * 2.0 ** -23).astype(np.float32)
+    b1[:4] = [2.0 ** -9, 3 * 2.0 ** -9, 2.0 ** -8, 2.0 ** -9 + 2.0 ** -20]
+    pool = P.Pool(cfg, [W1, W2], [b1, b2], torch.from_numpy(emb_bits).cuda(),
+                  np.ones((1, cfg["M"]), np.int32))
+    n = Q
+    arr = dict(offsets=np.array([0, n], np.int32), q_idx=np.arange(n, dtype=np.int32),
+               budget=np.full(n, 5, np.int16), base_svc=np.ones(n, np.int16))
+    dev = P.device_arrivals(arr)
+    act = torch.zeros(n, dtype=torch.int32, device="cuda")
+    lg = torch.zeros((n, A), dtype=torch.float32, device="cuda")
+    pool.route(dev, act, lg)
+    torch.cuda.synchronize()
+    got = lg.cpu().numpy().astype(np.float64)
+    pre = (emb_f + b1[None, :]).astype(np.float32)          # fp32 sums, RNE
+    exp = oracle.round_bf16_array(np.maximum(pre, 0).astype(np.float64))
+    np.testing.assert_array_equal(got, exp)
+    pool.close()
