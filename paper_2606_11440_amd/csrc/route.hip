@@ -387,8 +387,30 @@ __device__ __forceinline__ RowCtx row_setup_env(const RouteArgs& a, int32_t r, i
   return c;
 }
 
-template <int H, int NL, int AT, int KB1, bool W1L>
-__global__ __launch_bounds__(256, 1) void route_bf16_lds(RouteArgs a) {
+// Copies n 16-byte words from global memory to LDS with `nthreads` threads,
+// batches of 8 loads in flight per thread.
+template <int N, int NTHREADS>
+__device__ __forceinline__ void copy_to_lds(u32x4* dst, const u32x4* src) {
+  constexpr int PER = (N + NTHREADS - 1) / NTHREADS;
+  constexpr int B = 8;
+#pragma unroll
+  for (int b0 = 0; b0 < PER; b0 += B) {
+    u32x4 v[B];
+#pragma unroll
+    for (int j = 0; j < B; ++j) {
+      const int i = (b0 + j) * NTHREADS + (int)threadIdx.x;
+      if (b0 + j < PER && i < N) v[j] = src[i];
+    }
+#pragma unroll
+    for (int j = 0; j < B; ++j) {
+      const int i = (b0 + j) * NTHREADS + (int)threadIdx.x;
+      if (b0 + j < PER && i < N) dst[i] = v[j];
+    }
+  }
+}
+
+template <int H, int NL, int AT, int KB1, bool W1L, int NW>
+__global__ __launch_bounds__(NW * 64, 1) void route_bf16_lds(RouteArgs a) {
   constexpr int TH = H / 32;
   constexpr int KH = H / 16;
   constexpr int N_W1 = TH * KB1 * 64;
@@ -396,35 +418,30 @@ __global__ __launch_bounds__(256, 1) void route_bf16_lds(RouteArgs a) {
   constexpr int N_W3 = NL == 3 ? AT * KH * 64 : 0;
   constexpr int N_LDS = (W1L ? N_W1 : 0) + N_W2 + N_W3;
   __shared__ u32x4 lds[N_LDS];
-  {
-    int off = 0;
-    if (W1L) {
-      const u32x4* s1 = (const u32x4*)a.W[0];
-      for (int i = threadIdx.x; i < N_W1; i += 256) lds[i] = s1[i];
-      off = N_W1;
-    }
-    const u32x4* s2 = (const u32x4*)a.W[1];
-    for (int i = threadIdx.x; i < N_W2; i += 256) lds[off + i] = s2[i];
-    if (NL == 3) {
-      const u32x4* s3 = (const u32x4*)a.W[2];
-      for (int i = threadIdx.x; i < N_W3; i += 256) lds[off + N_W2 + i] = s3[i];
-    }
-  }
+  if constexpr (W1L) copy_to_lds<N_W1, NW * 64>(lds, (const u32x4*)a.W[0]);
+  copy_to_lds<N_W2, NW * 64>(lds + (W1L ? N_W1 : 0), (const u32x4*)a.W[1]);
+  if constexpr (NL == 3) copy_to_lds<N_W3, NW * 64>(lds + (W1L ? N_W1 : 0) + N_W2, (const u32x4*)a.W[2]);
   __syncthreads();
   const u32x4* w1 = W1L ? (const u32x4*)lds : (const u32x4*)a.W[0];
   const u32x4* w2 = lds + (W1L ? N_W1 : 0);
   const u32x4* w3 = w2 + N_W2;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n = lane & 31, g = lane >> 5;
-  const int n_tiles = (a.n_total + 255) / 256;
-  constexpr int C1 = TH < 2 ? TH : 2;       // layer-1 output tiles per chunk
-  constexpr int C2 = TH < 2 ? TH : 2;       // layer-2 output tiles per chunk
+  constexpr int ROWS = NW * 64;             // rows per block tile
+  const int n_tiles = (a.n_total + ROWS - 1) / ROWS;
+  constexpr int C1 = 1;                     // layer-1 output tiles per chunk
+  constexpr int C2 = 1;                     // layer-2 output tiles per chunk
 
   for (int tile = blockIdx.x; tile < n_tiles; tile += gridDim.x) {
     // Keeps loop-invariant loads (biases, weights) inside the loop: hoisted
     // out of it they would stay live in registers for the whole kernel.
     asm volatile("" ::: "memory");
-    const int32_t r0 = tile * 256 + wave * 64;
+    // Per-iteration copies of the lane index: every fragment address derived
+    // from them is recomputed inside the iteration instead of being hoisted
+    // (and kept live) across the whole loop.
+    int ln = lane, gg = g;
+    asm volatile("" : "+v"(ln), "+v"(gg));
+    const int32_t r0 = tile * ROWS + wave * 64;
     if (r0 >= a.n_total) continue;
     const int32_t rlast = (r0 + 63 < a.n_total ? r0 + 63 : a.n_total - 1);
     const int32_t rows[2] = {r0 + n, r0 + 32 + n};
@@ -436,8 +453,8 @@ __global__ __launch_bounds__(256, 1) void route_bf16_lds(RouteArgs a) {
     u32x4 x0[KB1], x1[KB1];
 #pragma unroll
     for (int kb = 0; kb < KB1; ++kb) {
-      x0[kb] = gather_bf16(a, c0, kb, g);
-      x1[kb] = gather_bf16(a, c1, kb, g);
+      x0[kb] = gather_bf16(a, c0, kb, gg);
+      x1[kb] = gather_bf16(a, c1, kb, gg);
     }
     u32x4 h0[KH], h1[KH];
 #pragma unroll
@@ -447,13 +464,13 @@ __global__ __launch_bounds__(256, 1) void route_bf16_lds(RouteArgs a) {
       for (int T = 0; T < C1; ++T) { p0[T] = f32x16{}; p1[T] = f32x16{}; }
       u32x4 wc[C1];
 #pragma unroll
-      for (int T = 0; T < C1; ++T) wc[T] = w1[((cc * C1 + T) * KB1) * 64 + lane];
+      for (int T = 0; T < C1; ++T) wc[T] = w1[((cc * C1 + T) * KB1) * 64 + ln];
 #pragma unroll
       for (int kb = 0; kb < KB1; ++kb) {
         u32x4 wn[C1];
 #pragma unroll
         for (int T = 0; T < C1; ++T)
-          wn[T] = w1[((cc * C1 + T) * KB1 + (kb + 1 < KB1 ? kb + 1 : kb)) * 64 + lane];
+          wn[T] = w1[((cc * C1 + T) * KB1 + (kb + 1 < KB1 ? kb + 1 : kb)) * 64 + ln];
 #pragma unroll
         for (int T = 0; T < C1; ++T) {
           p0[T] = mfma_bf16(wc[T], x0[kb], p0[T]);
@@ -466,8 +483,8 @@ __global__ __launch_bounds__(256, 1) void route_bf16_lds(RouteArgs a) {
 #pragma unroll
       for (int T = 0; T < C1; ++T) {
         const int Tg = cc * C1 + T;
-        tile_to_frags(p0[T], a.bias[0], Tg, g, h0[2 * Tg], h0[2 * Tg + 1]);
-        tile_to_frags(p1[T], a.bias[0], Tg, g, h1[2 * Tg], h1[2 * Tg + 1]);
+        tile_to_frags(p0[T], a.bias[0], Tg, gg, h0[2 * Tg], h0[2 * Tg + 1]);
+        tile_to_frags(p1[T], a.bias[0], Tg, gg, h1[2 * Tg], h1[2 * Tg + 1]);
       }
     }
     f32x16 o0[AT], o1[AT];
@@ -478,13 +495,13 @@ __global__ __launch_bounds__(256, 1) void route_bf16_lds(RouteArgs a) {
       for (int kb = 0; kb < KH; ++kb) {
 #pragma unroll
         for (int T = 0; T < AT; ++T) {
-          const u32x4 w = w2[(T * KH + kb) * 64 + lane];
+          const u32x4 w = w2[(T * KH + kb) * 64 + ln];
           o0[T] = mfma_bf16(w, h0[kb], o0[T]);
           o1[T] = mfma_bf16(w, h1[kb], o1[T]);
         }
       }
-      epilogue<AT>(a, c0, o0, a.bias[1], g);
-      epilogue<AT>(a, c1, o1, a.bias[1], g);
+      epilogue<AT>(a, c0, o0, a.bias[1], gg);
+      epilogue<AT>(a, c1, o1, a.bias[1], gg);
     } else {
 #pragma unroll
       for (int cc = 0; cc < TH / C2; ++cc) {
@@ -493,13 +510,13 @@ __global__ __launch_bounds__(256, 1) void route_bf16_lds(RouteArgs a) {
         for (int T = 0; T < C2; ++T) { p0[T] = f32x16{}; p1[T] = f32x16{}; }
         u32x4 wc[C2];
 #pragma unroll
-        for (int T = 0; T < C2; ++T) wc[T] = w2[((cc * C2 + T) * KH) * 64 + lane];
+        for (int T = 0; T < C2; ++T) wc[T] = w2[((cc * C2 + T) * KH) * 64 + ln];
 #pragma unroll
         for (int kb = 0; kb < KH; ++kb) {
           u32x4 wn[C2];
 #pragma unroll
           for (int T = 0; T < C2; ++T)
-            wn[T] = w2[((cc * C2 + T) * KH + (kb + 1 < KH ? kb + 1 : kb)) * 64 + lane];
+            wn[T] = w2[((cc * C2 + T) * KH + (kb + 1 < KH ? kb + 1 : kb)) * 64 + ln];
 #pragma unroll
           for (int T = 0; T < C2; ++T) {
             p0[T] = mfma_bf16(wc[T], h0[kb], p0[T]);
@@ -513,12 +530,12 @@ __global__ __launch_bounds__(256, 1) void route_bf16_lds(RouteArgs a) {
         for (int T = 0; T < C2; ++T) {
           const int Tg = cc * C2 + T;
           u32x4 f00, f01, f10, f11;
-          tile_to_frags(p0[T], a.bias[1], Tg, g, f00, f01);
-          tile_to_frags(p1[T], a.bias[1], Tg, g, f10, f11);
+          tile_to_frags(p0[T], a.bias[1], Tg, gg, f00, f01);
+          tile_to_frags(p1[T], a.bias[1], Tg, gg, f10, f11);
 #pragma unroll
           for (int To = 0; To < AT; ++To) {
-            const u32x4 wa = w3[(To * KH + 2 * Tg) * 64 + lane];
-            const u32x4 wb = w3[(To * KH + 2 * Tg + 1) * 64 + lane];
+            const u32x4 wa = w3[(To * KH + 2 * Tg) * 64 + ln];
+            const u32x4 wb = w3[(To * KH + 2 * Tg + 1) * 64 + ln];
             o0[To] = mfma_bf16(wa, f00, o0[To]);
             o1[To] = mfma_bf16(wa, f10, o1[To]);
             o0[To] = mfma_bf16(wb, f01, o0[To]);
@@ -526,8 +543,8 @@ __global__ __launch_bounds__(256, 1) void route_bf16_lds(RouteArgs a) {
           }
         }
       }
-      epilogue<AT>(a, c0, o0, a.bias[2], g);
-      epilogue<AT>(a, c1, o1, a.bias[2], g);
+      epilogue<AT>(a, c0, o0, a.bias[2], gg);
+      epilogue<AT>(a, c1, o1, a.bias[2], gg);
     }
   }
 }
@@ -560,14 +577,16 @@ RouteKernel pick(int dtype, int hidden, int at) {
   return nullptr;
 }
 
+constexpr int kLdsWaves = 8;   // waves per block of the persistent kernels (2 per SIMD)
+
 // Persistent LDS-resident variants for the shapes that fit (bytes of packed
 // weights in LDS <= 160 KiB): returns nullptr when none applies.
 RouteKernel pick_lds(int dtype, int hidden, int n_layers, int out_tiles, int k1) {
   if (dtype != IM_BF16) return nullptr;
   if (hidden == 256 && n_layers == 3 && out_tiles == 1 && k1 == 6)
-    return route_bf16_lds<256, 3, 1, 6, false>;
+    return route_bf16_lds<256, 3, 1, 6, false, kLdsWaves>;
   if (hidden == 256 && n_layers == 2 && out_tiles == 1 && k1 == 7)
-    return route_bf16_lds<256, 2, 1, 7, true>;
+    return route_bf16_lds<256, 2, 1, 7, true, kLdsWaves>;
   return nullptr;
 }
 
@@ -586,9 +605,9 @@ hipError_t launch_route(const RouteArgs& a, int dtype, int hidden, int n_layers,
   if (a.persistent_blocks > 0) {
     RouteKernel kl = pick_lds(dtype, hidden, n_layers, out_tiles, a.k1);
     if (kl) {
-      const int n_tiles = (a.n_total + 255) / 256;
+      const int n_tiles = (a.n_total + kLdsWaves * 64 - 1) / (kLdsWaves * 64);
       const unsigned blocks = (unsigned)(n_tiles < a.persistent_blocks ? n_tiles : a.persistent_blocks);
-      hipLaunchKernelGGL(kl, dim3(blocks), dim3(256), 0, s, a);
+      hipLaunchKernelGGL(kl, dim3(blocks), dim3(kLdsWaves * 64), 0, s, a);
       return hipGetLastError();
     }
   }
