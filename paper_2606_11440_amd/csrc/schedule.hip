@@ -59,9 +59,11 @@ struct Queue {       // wave-uniform view of one (env, model) record
 };
 
 // Insert up to 64 newcomers (valid lanes) into the front/pool structure.
-// Newcomer payload: key, id, t_arr, svc | budget << 16.
+// Newcomer payload: key, id, t_arr, svc | budget << 16. `fe` holds the current
+// front in lane order (lane i < fn: front[fh + i]); it is updated to the new
+// front when the front changes (then lane i < fn holds front[i], fh = 0).
 __device__ void insert_batch(Queue& q, bool valid, int32_t key, int32_t id, int32_t t_arr,
-                             int32_t packed, int4* front, int4* pool) {
+                             int32_t packed, int4& fe, int4* front, int4* pool) {
   const int lane = lane_id();
   const int k = popc64(ballot(valid));
   if (k == 0) return;
@@ -69,14 +71,14 @@ __device__ void insert_batch(Queue& q, bool valid, int32_t key, int32_t id, int3
   int32_t pay[1] = {packed};
   bitonic_sort64<1>(ck, pay);           // lanes [0, k) now hold the newcomers sorted
 
+  const int64_t fck = lane < q.fn ? composite(fe.x, fe.y) : kKeyMax;
   int lim;
   if (q.P == 0) {
     lim = k;
   } else if (q.fn == 0) {
     lim = 0;
   } else {
-    const int4 last = front[q.fh + q.fn - 1];
-    const int64_t fmax = composite(last.x, last.y);
+    const int64_t fmax = shfl(fck, q.fn - 1);
     lim = popc64(ballot(lane < k && ck < fmax));
   }
 
@@ -84,12 +86,6 @@ __device__ void insert_batch(Queue& q, bool valid, int32_t key, int32_t id, int3
     // Merge the front (lanes [0, fn)) with newcomers [0, lim); positions in
     // the merged order follow from counting the other sequence's smaller keys
     // (all composite keys are distinct).
-    int4 fe = make_int4(0, 0, 0, 0);
-    int64_t fck = kKeyMax;
-    if (lane < q.fn) {
-      fe = front[q.fh + lane];
-      fck = composite(fe.x, fe.y);
-    }
     const int64_t nck = lane < lim ? ck : kKeyMax;
     const int posf = lane + count_below(nck, lim, fck);
     const int posn = lane + count_below(fck, q.fn, nck);
@@ -107,6 +103,8 @@ __device__ void insert_batch(Queue& q, bool valid, int32_t key, int32_t id, int3
     q.P += total - keep;
     q.fh = 0;
     q.fn = keep;
+    wave_mem_sync();
+    fe = lane < keep ? front[lane] : make_int4(0, 0, 0, 0);
   }
   if (lane >= lim && lane < k)
     pool[q.P + lane - lim] = make_int4(comp_key(ck), comp_id(ck), t_arr, pay[0]);
@@ -212,10 +210,29 @@ __global__ __launch_bounds__(256) void schedule_kernel(SchedArgs a) {
   const int e = em / a.M;
   const int m = em - e * a.M;
 
-  // ---- validate the env's input; an invalid env is skipped this tick ----
+  // ---- independent loads first: the env's CSR bounds, this queue's record,
+  // slots, counters, histogram entries and front ----
   const int32_t lo = a.offsets[e], hi = a.offsets[e + 1];
+  ModelRec* rec = a.ms + em;
+  Queue q;
+  q.qlen = rec->qlen; q.busy = rec->busy; q.ewma = rec->ewma; q.backlog = rec->backlog;
+  q.cap = rec->cap; q.enabled = rec->enabled; q.fh = rec->fh; q.fn = rec->fn;
+  q.P = rec->P; q.next_id = rec->next_id;
+  int4 sl = make_int4(-1, 0, 0, 0);
+  if (lane < a.S) sl = a.slots[(size_t)em * a.S + lane];
+  int64_t* cnt = a.cnt + (size_t)em * C_NUM;
+  const int64_t cnt_old = lane < C_NUM ? cnt[lane] : 0;
+  int64_t* hist_p = a.hist + (size_t)e * a.A + m * a.K;
+  const int64_t hist_old = lane < a.K ? hist_p[lane] : 0;
+  int4* front = a.front + (size_t)em * kFront;
+  int4* pool = a.pool + (size_t)em * a.qcap;
+  int4 fe = lane < q.fn ? front[q.fh + lane] : make_int4(0, 0, 0, 0);
+
+  // ---- validate the env's input; an invalid env is skipped this tick ----
   int32_t bad = 0;
   if (lo < 0 || hi < lo || hi > a.n_total || hi - lo > a.max_arrivals) bad = IM_ERR_COUNT;
+  // the first chunk of arrivals stays in registers for admission
+  int32_t ac0 = -1, bu0 = 0, sv0 = 0;
   if (!bad) {
     for (int32_t base = lo; base < hi; base += 64) {
       const int32_t i = base + lane;
@@ -229,6 +246,7 @@ __global__ __launch_bounds__(256) void schedule_kernel(SchedArgs a) {
         if (bu < 1) b |= IM_ERR_BUDGET;
         if (sv < 1 || sv > IM_SVC_MAX) b |= IM_ERR_SVC;
         if (ac < -1 || ac >= a.A) b |= IM_ERR_ACTION;
+        if (base == lo) { ac0 = ac; bu0 = bu; sv0 = sv; }
       }
       bad |= (int32_t)wave_or((uint64_t)(uint32_t)b);
     }
@@ -238,13 +256,6 @@ __global__ __launch_bounds__(256) void schedule_kernel(SchedArgs a) {
     return;
   }
 
-  ModelRec* rec = a.ms + em;
-  Queue q;
-  q.qlen = rec->qlen; q.busy = rec->busy; q.ewma = rec->ewma; q.backlog = rec->backlog;
-  q.cap = rec->cap; q.enabled = rec->enabled; q.fh = rec->fh; q.fn = rec->fn;
-  q.P = rec->P; q.next_id = rec->next_id;
-  int4* front = a.front + (size_t)em * kFront;
-  int4* pool = a.pool + (size_t)em * a.qcap;
   const int32_t t = a.t;
   const int32_t n = hi - lo;
   const int32_t room = a.qcap - q.qlen;
@@ -256,7 +267,12 @@ __global__ __launch_bounds__(256) void schedule_kernel(SchedArgs a) {
   for (int32_t base = lo; base < hi; base += 64) {
     const int32_t i = base + lane;
     const bool in = i < hi;
-    const int32_t ac = in ? a.actions[i] : -1;
+    int32_t ac = ac0, bu = bu0, sv = sv0;
+    if (base != lo) {
+      ac = in ? a.actions[i] : -1;
+      bu = in ? a.budget[i] : 0;
+      sv = in ? a.base_svc[i] : 0;
+    }
     const int32_t mdl = ac >= 0 ? ac / a.K : -1;
     const bool mine = in && mdl == m;
     const uint64_t bal = ballot(mine);
@@ -266,38 +282,47 @@ __global__ __launch_bounds__(256) void schedule_kernel(SchedArgs a) {
     if (m == 0) nomodel += popc64(ballot(in && ac < 0));
     const int32_t d = mine ? ac - m * a.K : -1;
     for (int dd = 0; dd < a.K; ++dd) {
-      const int cnt = popc64(ballot(d == dd));
-      if (lane == dd) hist_add += cnt;
+      const int c = popc64(ballot(d == dd));
+      if (lane == dd) hist_add += c;
     }
     int32_t key = 0, packed = 0, svc = 0;
     if (acc) {
-      const int32_t bu = a.budget[i];
-      svc = (int32_t)a.base_svc[i] * (d + 1);
+      svc = sv * (d + 1);
       key = a.key_mode == IM_KEY_DEADLINE ? t + bu : (a.key_mode == IM_KEY_FCFS ? t : t + bu - svc);
       packed = (int32_t)((uint32_t)svc | ((uint32_t)bu << 16));
     }
     accepted += popc64(ballot(acc));
     svc_in += wave_sum(acc ? svc : 0);
-    insert_batch(q, acc, key, q.next_id + (i - lo), t, packed, front, pool);
+    insert_batch(q, acc, key, q.next_id + (i - lo), t, packed, fe, front, pool);
   }
   q.qlen += accepted;
   q.backlog += (int32_t)svc_in;
 
   // ---- service: fill free slots below c_m from the queue head ----
-  int4 sl = make_int4(-1, 0, 0, 0);
-  if (lane < a.S) sl = a.slots[(size_t)em * a.S + lane];
   const int capc = q.cap < a.S ? q.cap : a.S;
   uint64_t empty = ballot(lane < capc && sl.x < 0);
   int32_t started = 0;
   int64_t wait_add = 0, svc_out = 0;
+  bool fe_valid = true;   // fe mirrors front[fh + lane] until a refill
+  int fe_base = q.fh;
   while (empty != 0 && q.qlen > 0) {
-    if (q.fn == 0) refill(q, front, pool);
+    if (q.fn == 0) { refill(q, front, pool); fe_valid = false; }
     if (q.fn == 0) break;   // unreachable while qlen == fn + P holds; never spin
     const int need = popc64(empty);
     const int take = need < q.fn ? need : q.fn;
     const bool mine_slot = ((empty >> lane) & 1ull) && prefix_count(empty) < take;
+    int4 en = make_int4(0, 0, 0, 0);
+    if (fe_valid) {
+      // head entries are already in registers: lane (fh - fe_base + r) holds rank r
+      const int src = q.fh - fe_base + prefix_count(empty);
+      en.x = shfl((int32_t)fe.x, src & 63);
+      en.y = shfl((int32_t)fe.y, src & 63);
+      en.z = shfl((int32_t)fe.z, src & 63);
+      en.w = shfl((int32_t)fe.w, src & 63);
+    } else if (mine_slot) {
+      en = front[q.fh + prefix_count(empty)];
+    }
     if (mine_slot) {
-      const int4 en = front[q.fh + prefix_count(empty)];
       const int32_t svc = en.w & 0xffff;
       const int32_t bu = (int32_t)((uint32_t)en.w >> 16);
       sl = make_int4(en.y, en.z, svc, bu);
@@ -338,23 +363,28 @@ __global__ __launch_bounds__(256) void schedule_kernel(SchedArgs a) {
 
   // ---- write back ----
   if (lane < a.S) a.slots[(size_t)em * a.S + lane] = sl;
-  int64_t* cnt = a.cnt + (size_t)em * C_NUM;
   if (lane == 0) {
     rec->qlen = q.qlen; rec->busy = q.busy; rec->ewma = q.ewma; rec->backlog = q.backlog;
     rec->fh = q.fh; rec->fn = q.fn; rec->P = q.P; rec->next_id = q.next_id;
-    cnt[C_REJ_OVERFLOW] += routed - accepted;
-    cnt[C_ENQUEUED] += accepted;
-    cnt[C_STARTED] += started;
-    cnt[C_COMPLETED] += completed;
-    cnt[C_SLO_MET] += slo_add;
-    cnt[C_LAT_SUM] += lat_add;
-    cnt[C_WAIT_SUM] += wait_add;
     if (m == 0) {
       a.env_cnt[(size_t)e * 2] += n;
       a.env_cnt[(size_t)e * 2 + 1] += nomodel;
     }
   }
-  if (lane < a.K) a.hist[(size_t)e * a.A + m * a.K + lane] += hist_add;
+  if (lane < C_NUM - 1) {
+    int64_t add = 0;
+    switch (lane) {
+      case C_REJ_OVERFLOW: add = routed - accepted; break;
+      case C_ENQUEUED: add = accepted; break;
+      case C_STARTED: add = started; break;
+      case C_COMPLETED: add = completed; break;
+      case C_SLO_MET: add = slo_add; break;
+      case C_LAT_SUM: add = lat_add; break;
+      default: add = wait_add; break;
+    }
+    cnt[lane] = cnt_old + add;
+  }
+  if (lane < a.K) hist_p[lane] = hist_old + hist_add;
   // Snapshot row for the next tick's route step.
   if (lane < 5) write_snap_part(a, e, m, lane, q.qlen, q.busy, q.ewma, q.backlog, q.cap, q.enabled);
 }
