@@ -109,6 +109,9 @@ def main():
     ap.add_argument("--lam", type=float, default=None)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--eager", action="store_true",
+                    help="launch the timed ticks one by one instead of replaying them "
+                         "from a captured HIP graph")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run 5 device-to-device copies of MIB MiB (calibrates "
@@ -172,13 +175,26 @@ def main():
 
     # ---- timed region: K ticks of im_tick, events only at the two ends ----
     warm(pool)
+    graph = None
+    if not args.eager:
+        # The K ticks (two kernels each) are captured into one HIP graph
+        # outside the timed region and replayed once inside it: the same
+        # kernels on the same inputs, without per-launch host overhead.
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            for k in range(K):
+                pool.tick(dev[W_ + k], acts)
+        torch.cuda.synchronize()
     start = torch.cuda.Event(enable_timing=True)
     end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     start.record(stream)
-    for k in range(K):
-        pool.tick(dev[W_ + k], acts, stream.cuda_stream)
+    if graph is not None:
+        graph.replay()
+    else:
+        for k in range(K):
+            pool.tick(dev[W_ + k], acts, stream.cuda_stream)
     end.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -244,7 +260,9 @@ def main():
                                f"lambda={cfg['lam']:g}/tick, qcap {cfg['qcap']}, MLP "
                                f"{cfg['feat_dim']}->" + "->".join(map(str, cfg["widths"])) +
                                f" {cfg['dtype']}, ticks {W_}..{W_ + K - 1} of {T}",
-                   "envs": cfg["E"], "requests_per_tick": routed / K, "parallelism": "single GPU"},
+                   "envs": cfg["E"], "requests_per_tick": routed / K, "parallelism": "single GPU",
+                   "launch": "eager" if args.eager else f"one HIP graph of {K} ticks, captured "
+                                                        "before the timed region"},
         "routed_req_per_s": routed / (gpu_ms / 1e3),
         "kernels_us": {"route_avg": route_avg * 1e3, "schedule_avg": sched_avg * 1e3,
                        "note": "HIP events around each launch, separate identical pass",

@@ -14,7 +14,7 @@ namespace im {
 struct alignas(64) ModelRec {
   int32_t qlen, busy, ewma, backlog;   // snapshot fields read by the route step
   int32_t cap, enabled, fh, fn;
-  int32_t P, next_id, pad0, pad1;
+  int32_t P, next_id, t, pad1;         // t: ticks completed by this env (same in all M records)
   int32_t pad2, pad3, pad4, pad5;
 };
 static_assert(sizeof(ModelRec) == 64, "ModelRec layout");
@@ -70,7 +70,6 @@ struct SchedArgs {
   int32_t n_total;
   int32_t E, M, K, A, S, qcap, max_arrivals, key_mode;
   int64_t Q;
-  int32_t t;
   ModelRec* ms;
   int64_t* cnt;       // [E*M*C_NUM]
   int64_t* env_cnt;   // [E*2] arrived, rej_nomodel

@@ -348,7 +348,6 @@ static im::SchedArgs sched_args(im_pool* p) {
   a.max_arrivals = p->d.max_arrivals_per_env_tick;
   a.key_mode = p->d.key_mode;
   a.Q = p->Q;
-  a.t = p->t;
   a.ms = p->ms;
   a.cnt = p->cnt;
   a.env_cnt = p->env_cnt;
@@ -424,7 +423,6 @@ im_status im_read_state(im_pool* p, int32_t env_begin, int32_t env_count, int32_
   if (env_begin < 0 || env_count < 0 || (int64_t)env_begin + env_count > p->d.n_envs)
     return fail(p, IM_EINVAL, "env range out of bounds");
   IM_HIP(p, hipDeviceSynchronize());
-  if (tick) *tick = p->t;
   const int M = p->d.n_models, S = p->S, qcap = p->d.queue_cap, A = p->A;
   const size_t em0 = (size_t)env_begin * M, EMc = (size_t)env_count * M;
   std::vector<ModelRec> recs(EMc);
@@ -432,7 +430,9 @@ im_status im_read_state(im_pool* p, int32_t env_begin, int32_t env_count, int32_
   if (EMc) {
     IM_HIP(p, hipMemcpy(recs.data(), p->ms + em0, EMc * sizeof(ModelRec), hipMemcpyDeviceToHost));
     IM_HIP(p, hipMemcpy(cnt.data(), p->cnt + em0 * im::C_NUM, cnt.size() * 8, hipMemcpyDeviceToHost));
+    p->t = recs[0].t;   // every env advances every tick; graph replays advance it too
   }
+  if (tick) *tick = p->t;
   if (envs && env_count) {
     std::vector<int64_t> ec((size_t)env_count * 2);
     IM_HIP(p, hipMemcpy(ec.data(), p->env_cnt + (size_t)env_begin * 2, ec.size() * 8,
@@ -533,6 +533,7 @@ im_status im_write_state(im_pool* p, int32_t env_begin, int32_t env_count, int32
     ModelRec& r = recs[i];
     r.qlen = ms.qlen; r.busy = ms.busy; r.ewma = ms.ewma_q8; r.backlog = ms.backlog;
     r.cap = ms.capacity; r.enabled = ms.enabled ? 1 : 0; r.next_id = envs[e].next_id;
+    r.t = tick;
     r.fh = 0;
     r.fn = std::min(ms.qlen, im::kFront);
     r.P = ms.qlen - r.fn;

@@ -58,19 +58,13 @@ struct Queue {       // wave-uniform view of one (env, model) record
   int32_t qlen, busy, ewma, backlog, cap, enabled, fh, fn, P, next_id;
 };
 
-// Insert up to 64 newcomers (valid lanes) into the front/pool structure.
-// Newcomer payload: key, id, t_arr, svc | budget << 16. `fe` holds the current
-// front in lane order (lane i < fn: front[fh + i]); it is updated to the new
-// front when the front changes (then lane i < fn holds front[i], fh = 0).
-__device__ void insert_batch(Queue& q, bool valid, int32_t key, int32_t id, int32_t t_arr,
-                             int32_t packed, int4& fe, int4* front, int4* pool) {
+// Insert k newcomers, already sorted by (key, id) in lanes [0, k), into the
+// front/pool structure. Newcomer payload: ck = (key, id), pay = svc | budget << 16.
+// `fe` holds the current front in lane order (lane i < fn: front[fh + i]); it
+// is updated to the new front when the front changes (then fh = 0).
+__device__ void insert_sorted(Queue& q, int k, int64_t ck, int32_t pay, int32_t t_arr, int4& fe,
+                              int4* front, int4* pool) {
   const int lane = lane_id();
-  const int k = popc64(ballot(valid));
-  if (k == 0) return;
-  int64_t ck = valid ? composite(key, id) : kKeyMax;
-  int32_t pay[1] = {packed};
-  bitonic_sort64<1>(ck, pay);           // lanes [0, k) now hold the newcomers sorted
-
   const int64_t fck = lane < q.fn ? composite(fe.x, fe.y) : kKeyMax;
   int lim;
   if (q.P == 0) {
@@ -81,7 +75,6 @@ __device__ void insert_batch(Queue& q, bool valid, int32_t key, int32_t id, int3
     const int64_t fmax = shfl(fck, q.fn - 1);
     lim = popc64(ballot(lane < k && ck < fmax));
   }
-
   if (lim > 0) {
     // Merge the front (lanes [0, fn)) with newcomers [0, lim); positions in
     // the merged order follow from counting the other sequence's smaller keys
@@ -96,7 +89,7 @@ __device__ void insert_batch(Queue& q, bool valid, int32_t key, int32_t id, int3
       else pool[q.P + posf - kFront] = fe;
     }
     if (lane < lim) {
-      const int4 ne = make_int4(comp_key(ck), comp_id(ck), t_arr, pay[0]);
+      const int4 ne = make_int4(comp_key(ck), comp_id(ck), t_arr, pay);
       if (posn < kFront) front[posn] = ne;
       else pool[q.P + posn - kFront] = ne;
     }
@@ -107,7 +100,7 @@ __device__ void insert_batch(Queue& q, bool valid, int32_t key, int32_t id, int3
     fe = lane < keep ? front[lane] : make_int4(0, 0, 0, 0);
   }
   if (lane >= lim && lane < k)
-    pool[q.P + lane - lim] = make_int4(comp_key(ck), comp_id(ck), t_arr, pay[0]);
+    pool[q.P + lane - lim] = make_int4(comp_key(ck), comp_id(ck), t_arr, pay);
   q.P += k - lim;
   wave_mem_sync();
 }
@@ -203,36 +196,34 @@ __global__ void snapshot_kernel(SchedArgs a, int e0, int ne) {
     write_snap_part(a, e, m, part, r.qlen, r.busy, r.ewma, r.backlog, r.cap, r.enabled);
 }
 
-__global__ __launch_bounds__(256) void schedule_kernel(SchedArgs a) {
-  const int lane = threadIdx.x & 63;
-  const int em = (int)blockIdx.x * 4 + (int)(threadIdx.x >> 6);
-  if (em >= a.E * a.M) return;
-  const int e = em / a.M;
-  const int m = em - e * a.M;
+__device__ __forceinline__ int32_t wave_sum32(int32_t v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v += shfl_xor(v, m);
+  return v;
+}
 
-  // ---- independent loads first: the env's CSR bounds, this queue's record,
-  // slots, counters, histogram entries and front ----
-  const int32_t lo = a.offsets[e], hi = a.offsets[e + 1];
-  ModelRec* rec = a.ms + em;
-  Queue q;
-  q.qlen = rec->qlen; q.busy = rec->busy; q.ewma = rec->ewma; q.backlog = rec->backlog;
-  q.cap = rec->cap; q.enabled = rec->enabled; q.fh = rec->fh; q.fn = rec->fn;
-  q.P = rec->P; q.next_id = rec->next_id;
-  int4 sl = make_int4(-1, 0, 0, 0);
-  if (lane < a.S) sl = a.slots[(size_t)em * a.S + lane];
-  int64_t* cnt = a.cnt + (size_t)em * C_NUM;
-  const int64_t cnt_old = lane < C_NUM ? cnt[lane] : 0;
-  int64_t* hist_p = a.hist + (size_t)e * a.A + m * a.K;
-  const int64_t hist_old = lane < a.K ? hist_p[lane] : 0;
-  int4* front = a.front + (size_t)em * kFront;
-  int4* pool = a.pool + (size_t)em * a.qcap;
-  int4 fe = lane < q.fn ? front[q.fh + lane] : make_int4(0, 0, 0, 0);
+constexpr int kStageChunks = 4;   // arrival chunks (of 64) staged in LDS per round
+
+// One wave per env. The env's arrivals are validated once; then, 64 at a time,
+// they are partitioned by model (ballot + mbcnt ranks in id order give the
+// tail-drop admission) and sorted once by (model, key, id) with a 64-lane
+// bitonic network, so each model's newcomers form one sorted segment (a
+// segmented sort). The sorted chunks are staged in LDS; each model then
+// merges its segments into its queue, serves its slots and writes back.
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void schedule_kernel(SchedArgs a) {
+  __shared__ int4 stage[4][kStageChunks * 64];
+  const int lane = threadIdx.x & 63;
+  const int wv = threadIdx.x >> 6;
+  const int e = (int)blockIdx.x * 4 + wv;
+  if (e >= a.E) return;
+  int4* st = stage[wv];
+  const int M = a.M, K = a.K;
 
   // ---- validate the env's input; an invalid env is skipped this tick ----
+  const int32_t lo = a.offsets[e], hi = a.offsets[e + 1];
   int32_t bad = 0;
   if (lo < 0 || hi < lo || hi > a.n_total || hi - lo > a.max_arrivals) bad = IM_ERR_COUNT;
-  // the first chunk of arrivals stays in registers for admission
-  int32_t ac0 = -1, bu0 = 0, sv0 = 0;
+  int32_t ac0 = -1, bu0 = 0, sv0 = 0;   // first chunk stays in registers
   if (!bad) {
     for (int32_t base = lo; base < hi; base += 64) {
       const int32_t i = base + lane;
@@ -251,142 +242,231 @@ __global__ __launch_bounds__(256) void schedule_kernel(SchedArgs a) {
       bad |= (int32_t)wave_or((uint64_t)(uint32_t)b);
     }
   }
+  ModelRec* recs = a.ms + (size_t)e * M;
+  // The tick lives in device memory (one copy per record of the env), so a
+  // captured sequence of ticks replays with the right time.
+  const int32_t t = recs[0].t;
   if (bad) {
-    if (m == 0 && lane == 0) atomicOr(a.err, bad);
+    if (lane == 0) atomicOr(a.err, bad);
+    if (lane < M) recs[lane].t = t + 1;   // the env's state is untouched; time still advances
     return;
   }
 
-  const int32_t t = a.t;
   const int32_t n = hi - lo;
-  const int32_t room = a.qcap - q.qlen;
+  // lane m < M: room left in model m's queue at the snapshot
+  const int32_t room_l = lane < M ? a.qcap - recs[lane].qlen : 0;
+  const int32_t next_id = recs[0].next_id;
+  int64_t* hist_p = a.hist + (size_t)e * a.A;
+  const int64_t hist_old = lane < a.A ? hist_p[lane] : 0;
+  int32_t prior_l = 0;      // lane m: requests routed to model m so far (id order)
+  int32_t acc_l = 0;        // lane m: requests accepted by model m so far
+  int32_t hist_l = 0;       // lane a: requests routed with action a
+  int32_t nomodel = 0;
+  const int n_chunks = (n + 63) / 64;
+  const int rounds = n_chunks > 0 ? (n_chunks + kStageChunks - 1) / kStageChunks : 1;
 
-  // ---- admission and insertion, 64 arrivals at a time ----
-  int32_t routed = 0, accepted = 0, nomodel = 0;
-  int64_t svc_in = 0;
-  int64_t hist_add = 0;   // lane d < K: routed requests with depth d
-  for (int32_t base = lo; base < hi; base += 64) {
-    const int32_t i = base + lane;
-    const bool in = i < hi;
-    int32_t ac = ac0, bu = bu0, sv = sv0;
-    if (base != lo) {
-      ac = in ? a.actions[i] : -1;
-      bu = in ? a.budget[i] : 0;
-      sv = in ? a.base_svc[i] : 0;
+  for (int r = 0; r < rounds; ++r) {
+    const int c0 = r * kStageChunks;
+    const int nch = n_chunks - c0 < kStageChunks ? n_chunks - c0 : kStageChunks;
+    // ---- partition, admission and one sort per chunk ----
+    for (int c = 0; c < nch; ++c) {
+      const int32_t base = lo + (c0 + c) * 64;
+      const int32_t i = base + lane;
+      const bool in = i < hi;
+      int32_t ac = ac0, bu = bu0, sv = sv0;
+      if (c0 + c != 0) {
+        ac = in ? a.actions[i] : -1;
+        bu = in ? a.budget[i] : 0;
+        sv = in ? a.base_svc[i] : 0;
+      }
+      const int32_t mdl = ac >= 0 ? ac / K : -1;
+      nomodel += popc64(ballot(in && ac < 0));
+      for (int x = 0; x < a.A; ++x) {
+        const int cnt = popc64(ballot(in && ac == x));
+        if (lane == x) hist_l += cnt;
+      }
+      int32_t rank = 0;
+      for (int m = 0; m < M; ++m) {
+        const uint64_t bal = ballot(in && mdl == m);
+        if (bal == 0) continue;
+        const int32_t pm = __builtin_amdgcn_readlane(prior_l, m);
+        if (mdl == m) rank = pm + prefix_count(bal);
+        if (lane == m) prior_l += popc64(bal);
+      }
+      const int32_t room = shfl(room_l, mdl >= 0 ? mdl : 0);
+      const bool acc = in && mdl >= 0 && rank < room;
+      const int32_t d = ac - mdl * K;
+      const int32_t svc = sv * (d + 1);
+      const int32_t key = a.key_mode == IM_KEY_DEADLINE ? t + bu
+                          : (a.key_mode == IM_KEY_FCFS ? t : t + bu - svc);
+      // sort key: model (63 for rejected rows) | key biased to unsigned | lane
+      int64_t sk = (int64_t)(((uint64_t)(acc ? mdl : 63) << 38) |
+                             ((uint64_t)((uint32_t)key ^ 0x80000000u) << 6) | (uint64_t)lane);
+      int32_t pay[1] = {(int32_t)((uint32_t)svc | ((uint32_t)bu << 16))};
+      bitonic_sort64<1>(sk, pay);
+      const int32_t skey = (int32_t)((uint32_t)((uint64_t)sk >> 6) ^ 0x80000000u);
+      const int32_t sid = next_id + (base - lo) + (int32_t)(sk & 63);
+      st[c * 64 + lane] = make_int4(skey, sid, pay[0], (int32_t)((uint64_t)sk >> 38));
     }
-    const int32_t mdl = ac >= 0 ? ac / a.K : -1;
-    const bool mine = in && mdl == m;
-    const uint64_t bal = ballot(mine);
-    const int32_t rank = routed + prefix_count(bal);
-    const bool acc = mine && rank < room;
-    routed += popc64(bal);
-    if (m == 0) nomodel += popc64(ballot(in && ac < 0));
-    const int32_t d = mine ? ac - m * a.K : -1;
-    for (int dd = 0; dd < a.K; ++dd) {
-      const int c = popc64(ballot(d == dd));
-      if (lane == dd) hist_add += c;
+    const bool last = r == rounds - 1;
+
+    // ---- per model: insert its sorted segments, serve, write back ----
+    // The record and front of model m+1 are fetched while model m is processed.
+    auto load_rec = [&](int mm, Queue& qq) {
+      const ModelRec* r = recs + mm;
+      qq.qlen = r->qlen; qq.busy = r->busy; qq.ewma = r->ewma; qq.backlog = r->backlog;
+      qq.cap = r->cap; qq.enabled = r->enabled; qq.fh = r->fh; qq.fn = r->fn;
+      qq.P = r->P; qq.next_id = r->next_id;
+    };
+    // The whole front array is read without waiting for the record (the load
+    // is independent of fh); the live window [fh, fh + fn) is then rotated to
+    // lanes [0, fn) with lane shuffles.
+    auto load_front = [&](int mm, const Queue& qq) -> int4 {
+      const int4 all = a.front[((size_t)e * M + mm) * kFront + lane];
+      const int src = (qq.fh + lane) & 63;
+      int4 v;
+      v.x = shfl((int32_t)all.x, src);
+      v.y = shfl((int32_t)all.y, src);
+      v.z = shfl((int32_t)all.z, src);
+      v.w = shfl((int32_t)all.w, src);
+      return lane < qq.fn ? v : make_int4(0, 0, 0, 0);
+    };
+    for (int m = 0; m < M; ++m) {
+      const int em = e * M + m;
+      ModelRec* rec = recs + m;
+      Queue q;
+      load_rec(m, q);
+      int4* front = a.front + (size_t)em * kFront;
+      int4* pool = a.pool + (size_t)em * a.qcap;
+      int4 fe = load_front(m, q);
+      int4 sl = make_int4(-1, 0, 0, 0);
+      int64_t* cnt = a.cnt + (size_t)em * C_NUM;
+      int64_t cnt_old = 0;
+      if (last) {
+        if (lane < a.S) sl = a.slots[(size_t)em * a.S + lane];
+        cnt_old = lane < C_NUM ? cnt[lane] : 0;
+      }
+      int32_t added = 0, svc_in = 0;
+      for (int c = 0; c < nch; ++c) {
+        const int4 en = st[c * 64 + lane];
+        const int seg_lo = popc64(ballot(en.w < m));
+        const int k = popc64(ballot(en.w == m));
+        if (k == 0) continue;
+        const int src = (seg_lo + lane) & 63;
+        const int32_t kk = shfl((int32_t)en.x, src);
+        const int32_t id = shfl((int32_t)en.y, src);
+        const int32_t pay = shfl((int32_t)en.z, src);
+        const int64_t ck = lane < k ? composite(kk, id) : kKeyMax;
+        insert_sorted(q, k, ck, pay, t, fe, front, pool);
+        added += k;
+        svc_in += wave_sum32(lane < k ? (pay & 0xffff) : 0);
+      }
+      q.qlen += added;
+      q.backlog += svc_in;
+      if (lane == m) acc_l += added;
+      if (!last) {
+        if (lane == 0) {
+          rec->qlen = q.qlen; rec->backlog = q.backlog;
+          rec->fh = q.fh; rec->fn = q.fn; rec->P = q.P;
+        }
+        if (m == M - 1) wave_mem_sync();   // the next round re-reads these records
+        continue;
+      }
+
+      // ---- service: fill free slots below c_m from the queue head ----
+      const int capc = q.cap < a.S ? q.cap : a.S;
+      uint64_t empty = ballot(lane < capc && sl.x < 0);
+      int32_t started = 0;
+      int32_t wait_add = 0, svc_out = 0;
+      bool fe_valid = true;   // fe mirrors front[fh + lane] until a refill
+      const int fe_base = q.fh;
+      while (empty != 0 && q.qlen > 0) {
+        if (q.fn == 0) { refill(q, front, pool); fe_valid = false; }
+        if (q.fn == 0) break;   // unreachable while qlen == fn + P holds; never spin
+        const int need = popc64(empty);
+        const int take = need < q.fn ? need : q.fn;
+        const int rnk = prefix_count(empty);
+        const bool mine_slot = ((empty >> lane) & 1ull) && rnk < take;
+        int4 en = make_int4(0, 0, 0, 0);
+        if (fe_valid) {
+          const int src = (q.fh - fe_base + rnk) & 63;
+          en.x = shfl((int32_t)fe.x, src);
+          en.y = shfl((int32_t)fe.y, src);
+          en.z = shfl((int32_t)fe.z, src);
+          en.w = shfl((int32_t)fe.w, src);
+        } else if (mine_slot) {
+          en = front[q.fh + rnk];
+        }
+        if (mine_slot) {
+          const int32_t svc = en.w & 0xffff;
+          const int32_t bu = (int32_t)((uint32_t)en.w >> 16);
+          sl = make_int4(en.y, en.z, svc, bu);
+        }
+        wait_add += wave_sum32(mine_slot ? t - sl.y : 0);
+        svc_out += wave_sum32(mine_slot ? sl.z : 0);
+        empty &= ~ballot(mine_slot);
+        q.fh += take;
+        q.fn -= take;
+        q.qlen -= take;
+        started += take;
+      }
+      q.backlog -= svc_out;
+
+      // ---- one tick of service; completions in slot order ----
+      const bool busy_slot = lane < a.S && sl.x >= 0;
+      if (busy_slot) sl.z -= 1;
+      const bool done = busy_slot && sl.z == 0;
+      const uint64_t done_mask = ballot(done);
+      const int32_t lat = t - sl.y + 1;
+      uint64_t dm = done_mask;
+      int32_t ewma = q.ewma;
+      while (dm) {
+        const int s = __builtin_ctzll(dm);
+        dm &= dm - 1;
+        const int32_t ls = shfl((int32_t)lat, s);
+        const int64_t delta = (int64_t)ls * 256 - ewma;
+        const int64_t stepv = delta >= 0 ? (delta >> 3) : -((-delta + 7) >> 3);
+        ewma = (int32_t)(ewma + stepv);
+      }
+      const int32_t completed = popc64(done_mask);
+      const int32_t lat_add = wave_sum32(done ? lat : 0);
+      const int32_t slo_add = popc64(ballot(done && lat <= sl.w));
+      if (done) sl = make_int4(-1, 0, 0, 0);
+      q.busy = popc64(ballot(lane < a.S && sl.x >= 0));
+      q.ewma = ewma;
+      q.next_id += n;
+
+      // ---- write back ----
+      if (lane < a.S) a.slots[(size_t)em * a.S + lane] = sl;
+      if (lane == 0) {
+        rec->qlen = q.qlen; rec->busy = q.busy; rec->ewma = q.ewma; rec->backlog = q.backlog;
+        rec->fh = q.fh; rec->fn = q.fn; rec->P = q.P; rec->next_id = q.next_id;
+        rec->t = t + 1;
+      }
+      const int32_t routed_m = __builtin_amdgcn_readlane(prior_l, m);
+      const int32_t acc_m = __builtin_amdgcn_readlane(acc_l, m);
+      if (lane < C_NUM - 1) {
+        int64_t add = 0;
+        switch (lane) {
+          case C_REJ_OVERFLOW: add = routed_m - acc_m; break;
+          case C_ENQUEUED: add = acc_m; break;
+          case C_STARTED: add = started; break;
+          case C_COMPLETED: add = completed; break;
+          case C_SLO_MET: add = slo_add; break;
+          case C_LAT_SUM: add = lat_add; break;
+          default: add = wait_add; break;
+        }
+        cnt[lane] = cnt_old + add;
+      }
+      // Snapshot row for the next tick's route step.
+      if (lane < 5) write_snap_part(a, e, m, lane, q.qlen, q.busy, q.ewma, q.backlog, q.cap, q.enabled);
     }
-    int32_t key = 0, packed = 0, svc = 0;
-    if (acc) {
-      svc = sv * (d + 1);
-      key = a.key_mode == IM_KEY_DEADLINE ? t + bu : (a.key_mode == IM_KEY_FCFS ? t : t + bu - svc);
-      packed = (int32_t)((uint32_t)svc | ((uint32_t)bu << 16));
-    }
-    accepted += popc64(ballot(acc));
-    svc_in += wave_sum(acc ? svc : 0);
-    insert_batch(q, acc, key, q.next_id + (i - lo), t, packed, fe, front, pool);
   }
-  q.qlen += accepted;
-  q.backlog += (int32_t)svc_in;
-
-  // ---- service: fill free slots below c_m from the queue head ----
-  const int capc = q.cap < a.S ? q.cap : a.S;
-  uint64_t empty = ballot(lane < capc && sl.x < 0);
-  int32_t started = 0;
-  int64_t wait_add = 0, svc_out = 0;
-  bool fe_valid = true;   // fe mirrors front[fh + lane] until a refill
-  int fe_base = q.fh;
-  while (empty != 0 && q.qlen > 0) {
-    if (q.fn == 0) { refill(q, front, pool); fe_valid = false; }
-    if (q.fn == 0) break;   // unreachable while qlen == fn + P holds; never spin
-    const int need = popc64(empty);
-    const int take = need < q.fn ? need : q.fn;
-    const bool mine_slot = ((empty >> lane) & 1ull) && prefix_count(empty) < take;
-    int4 en = make_int4(0, 0, 0, 0);
-    if (fe_valid) {
-      // head entries are already in registers: lane (fh - fe_base + r) holds rank r
-      const int src = q.fh - fe_base + prefix_count(empty);
-      en.x = shfl((int32_t)fe.x, src & 63);
-      en.y = shfl((int32_t)fe.y, src & 63);
-      en.z = shfl((int32_t)fe.z, src & 63);
-      en.w = shfl((int32_t)fe.w, src & 63);
-    } else if (mine_slot) {
-      en = front[q.fh + prefix_count(empty)];
-    }
-    if (mine_slot) {
-      const int32_t svc = en.w & 0xffff;
-      const int32_t bu = (int32_t)((uint32_t)en.w >> 16);
-      sl = make_int4(en.y, en.z, svc, bu);
-    }
-    wait_add += wave_sum(mine_slot ? (int64_t)(t - sl.y) : 0);
-    svc_out += wave_sum(mine_slot ? (int64_t)sl.z : 0);
-    empty &= ~ballot(mine_slot);
-    q.fh += take;
-    q.fn -= take;
-    q.qlen -= take;
-    started += take;
-  }
-  q.backlog -= (int32_t)svc_out;
-
-  // ---- one tick of service; completions in slot order ----
-  const bool busy_slot = lane < a.S && sl.x >= 0;
-  if (busy_slot) sl.z -= 1;
-  const bool done = busy_slot && sl.z == 0;
-  const uint64_t done_mask = ballot(done);
-  const int32_t lat = t - sl.y + 1;
-  uint64_t dm = done_mask;
-  int32_t ewma = q.ewma;
-  while (dm) {
-    const int s = __builtin_ctzll(dm);
-    dm &= dm - 1;
-    const int32_t ls = shfl((int32_t)lat, s);
-    const int64_t delta = (int64_t)ls * 256 - ewma;
-    const int64_t stepv = delta >= 0 ? (delta >> 3) : -((-delta + 7) >> 3);
-    ewma = (int32_t)(ewma + stepv);
-  }
-  const int32_t completed = popc64(done_mask);
-  const int64_t lat_add = wave_sum(done ? (int64_t)lat : 0);
-  const int32_t slo_add = popc64(ballot(done && lat <= sl.w));
-  if (done) sl = make_int4(-1, 0, 0, 0);
-  q.busy = popc64(ballot(lane < a.S && sl.x >= 0));
-  q.ewma = ewma;
-  q.next_id += n;
-
-  // ---- write back ----
-  if (lane < a.S) a.slots[(size_t)em * a.S + lane] = sl;
   if (lane == 0) {
-    rec->qlen = q.qlen; rec->busy = q.busy; rec->ewma = q.ewma; rec->backlog = q.backlog;
-    rec->fh = q.fh; rec->fn = q.fn; rec->P = q.P; rec->next_id = q.next_id;
-    if (m == 0) {
-      a.env_cnt[(size_t)e * 2] += n;
-      a.env_cnt[(size_t)e * 2 + 1] += nomodel;
-    }
+    a.env_cnt[(size_t)e * 2] += n;
+    a.env_cnt[(size_t)e * 2 + 1] += nomodel;
   }
-  if (lane < C_NUM - 1) {
-    int64_t add = 0;
-    switch (lane) {
-      case C_REJ_OVERFLOW: add = routed - accepted; break;
-      case C_ENQUEUED: add = accepted; break;
-      case C_STARTED: add = started; break;
-      case C_COMPLETED: add = completed; break;
-      case C_SLO_MET: add = slo_add; break;
-      case C_LAT_SUM: add = lat_add; break;
-      default: add = wait_add; break;
-    }
-    cnt[lane] = cnt_old + add;
-  }
-  if (lane < a.K) hist_p[lane] = hist_old + hist_add;
-  // Snapshot row for the next tick's route step.
-  if (lane < 5) write_snap_part(a, e, m, lane, q.qlen, q.busy, q.ewma, q.backlog, q.cap, q.enabled);
+  if (lane < a.A) hist_p[lane] = hist_old + hist_l;
 }
 
 }  // namespace
@@ -399,7 +479,7 @@ hipError_t launch_snapshot(const SchedArgs& a, int e0, int ne, hipStream_t s) {
 }
 
 hipError_t launch_schedule(const SchedArgs& a, hipStream_t s) {
-  const int64_t waves = (int64_t)a.E * a.M;
+  const int64_t waves = (int64_t)a.E;
   const unsigned blocks = (unsigned)((waves + 3) / 4);
   hipLaunchKernelGGL(schedule_kernel, dim3(blocks), dim3(256), 0, s, a);
   return hipGetLastError();
