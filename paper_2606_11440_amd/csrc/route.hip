@@ -145,7 +145,7 @@ __device__ __forceinline__ void epilogue(const RouteArgs& a, const RowCtx& c, f3
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
       const int act = 32 * T + 8 * (v >> 2) + 4 * g + (v & 3);
-      const float z = acc[T][v] + bias[(T * 2 + g) * 16 + v];
+      const float z = bias ? acc[T][v] + bias[(T * 2 + g) * 16 + v] : acc[T][v];
       acc[T][v] = z;
       if (act < a.A && ((c.amask >> act) & 1ull)) {
         if (ba < 0 || z > best) { best = z; ba = act; }
@@ -179,6 +179,17 @@ __device__ __forceinline__ void tile_to_frags(const f32x16& acc, const float* bi
   float h[16];
 #pragma unroll
   for (int v = 0; v < 16; ++v) h[v] = fmaxf(acc[v] + bias[(T * 2 + g) * 16 + v], 0.f);
+  f0.x = pack2(h[0], h[1]);   f0.y = pack2(h[2], h[3]);
+  f0.z = pack2(h[4], h[5]);   f0.w = pack2(h[6], h[7]);
+  f1.x = pack2(h[8], h[9]);   f1.y = pack2(h[10], h[11]);
+  f1.z = pack2(h[12], h[13]); f1.w = pack2(h[14], h[15]);
+}
+
+// ReLU + bf16 rounding of one accumulator tile (bias already included).
+__device__ __forceinline__ void relu_to_frags(const f32x16& acc, u32x4& f0, u32x4& f1) {
+  float h[16];
+#pragma unroll
+  for (int v = 0; v < 16; ++v) h[v] = fmaxf(acc[v], 0.f);
   f0.x = pack2(h[0], h[1]);   f0.y = pack2(h[2], h[3]);
   f0.z = pack2(h[4], h[5]);   f0.w = pack2(h[6], h[7]);
   f1.x = pack2(h[8], h[9]);   f1.y = pack2(h[10], h[11]);
@@ -417,11 +428,19 @@ __global__ __launch_bounds__(NW * 64, 1) void route_bf16_lds(RouteArgs a) {
   constexpr int N_W2 = (NL == 3 ? TH : AT) * KH * 64;
   constexpr int N_W3 = NL == 3 ? AT * KH * 64 : 0;
   constexpr int N_LDS = (W1L ? N_W1 : 0) + N_W2 + N_W3;
+  // biases in accumulator-register order: [tile][g][16] floats per layer
+  constexpr int NB0 = TH * 32, NB1 = (NL == 3 ? TH : AT) * 32, NB2 = NL == 3 ? AT * 32 : 0;
   __shared__ u32x4 lds[N_LDS];
+  __shared__ float lbias[NB0 + NB1 + NB2];
   if constexpr (W1L) copy_to_lds<N_W1, NW * 64>(lds, (const u32x4*)a.W[0]);
   copy_to_lds<N_W2, NW * 64>(lds + (W1L ? N_W1 : 0), (const u32x4*)a.W[1]);
   if constexpr (NL == 3) copy_to_lds<N_W3, NW * 64>(lds + (W1L ? N_W1 : 0) + N_W2, (const u32x4*)a.W[2]);
+  for (int i = threadIdx.x; i < NB0 + NB1 + NB2; i += NW * 64)
+    lbias[i] = i < NB0 ? a.bias[0][i] : (i < NB0 + NB1 ? a.bias[1][i - NB0] : a.bias[2][i - NB0 - NB1]);
   __syncthreads();
+  const float* lb0 = lbias;
+  const float* lb1 = lbias + NB0;
+  const float* lb2 = lbias + NB0 + NB1;
   const u32x4* w1 = W1L ? (const u32x4*)lds : (const u32x4*)a.W[0];
   const u32x4* w2 = lds + (W1L ? N_W1 : 0);
   const u32x4* w3 = w2 + N_W2;
@@ -429,8 +448,6 @@ __global__ __launch_bounds__(NW * 64, 1) void route_bf16_lds(RouteArgs a) {
   const int n = lane & 31, g = lane >> 5;
   constexpr int ROWS = NW * 64;             // rows per block tile
   const int n_tiles = (a.n_total + ROWS - 1) / ROWS;
-  constexpr int C1 = 1;                     // layer-1 output tiles per chunk
-  constexpr int C2 = 1;                     // layer-2 output tiles per chunk
 
   for (int tile = blockIdx.x; tile < n_tiles; tile += gridDim.x) {
     // Keeps loop-invariant loads (biases, weights) inside the loop: hoisted
@@ -458,38 +475,28 @@ __global__ __launch_bounds__(NW * 64, 1) void route_bf16_lds(RouteArgs a) {
     }
     u32x4 h0[KH], h1[KH];
 #pragma unroll
-    for (int cc = 0; cc < TH / C1; ++cc) {
-      f32x16 p0[C1], p1[C1];
+    for (int cc = 0; cc < TH; ++cc) {
+      // all layer-1 fragments of this output tile in flight at once
+      u32x4 wk[KB1];
 #pragma unroll
-      for (int T = 0; T < C1; ++T) { p0[T] = f32x16{}; p1[T] = f32x16{}; }
-      u32x4 wc[C1];
-#pragma unroll
-      for (int T = 0; T < C1; ++T) wc[T] = w1[((cc * C1 + T) * KB1) * 64 + ln];
+      for (int kb = 0; kb < KB1; ++kb) wk[kb] = w1[(cc * KB1 + kb) * 64 + ln];
+      f32x16 p0 = *(const f32x16*)(lb0 + (cc * 2 + gg) * 16);
+      f32x16 p1 = p0;
 #pragma unroll
       for (int kb = 0; kb < KB1; ++kb) {
-        u32x4 wn[C1];
-#pragma unroll
-        for (int T = 0; T < C1; ++T)
-          wn[T] = w1[((cc * C1 + T) * KB1 + (kb + 1 < KB1 ? kb + 1 : kb)) * 64 + ln];
-#pragma unroll
-        for (int T = 0; T < C1; ++T) {
-          p0[T] = mfma_bf16(wc[T], x0[kb], p0[T]);
-          p1[T] = mfma_bf16(wc[T], x1[kb], p1[T]);
-        }
-#pragma unroll
-        for (int T = 0; T < C1; ++T) wc[T] = wn[T];
-        __builtin_amdgcn_sched_barrier(0);
+        p0 = mfma_bf16(wk[kb], x0[kb], p0);
+        p1 = mfma_bf16(wk[kb], x1[kb], p1);
       }
-#pragma unroll
-      for (int T = 0; T < C1; ++T) {
-        const int Tg = cc * C1 + T;
-        tile_to_frags(p0[T], a.bias[0], Tg, gg, h0[2 * Tg], h0[2 * Tg + 1]);
-        tile_to_frags(p1[T], a.bias[0], Tg, gg, h1[2 * Tg], h1[2 * Tg + 1]);
-      }
+      relu_to_frags(p0, h0[2 * cc], h0[2 * cc + 1]);
+      relu_to_frags(p1, h1[2 * cc], h1[2 * cc + 1]);
+      __builtin_amdgcn_sched_barrier(0);
     }
     f32x16 o0[AT], o1[AT];
 #pragma unroll
-    for (int T = 0; T < AT; ++T) { o0[T] = f32x16{}; o1[T] = f32x16{}; }
+    for (int T = 0; T < AT; ++T) {
+      o0[T] = *(const f32x16*)((NL == 2 ? lb1 : lb2) + (T * 2 + gg) * 16);
+      o1[T] = o0[T];
+    }
     if constexpr (NL == 2) {
 #pragma unroll
       for (int kb = 0; kb < KH; ++kb) {
@@ -500,51 +507,40 @@ __global__ __launch_bounds__(NW * 64, 1) void route_bf16_lds(RouteArgs a) {
           o1[T] = mfma_bf16(w, h1[kb], o1[T]);
         }
       }
-      epilogue<AT>(a, c0, o0, a.bias[1], gg);
-      epilogue<AT>(a, c1, o1, a.bias[1], gg);
+      epilogue<AT>(a, c0, o0, nullptr, gg);
+      epilogue<AT>(a, c1, o1, nullptr, gg);
     } else {
 #pragma unroll
-      for (int cc = 0; cc < TH / C2; ++cc) {
-        f32x16 p0[C2], p1[C2];
-#pragma unroll
-        for (int T = 0; T < C2; ++T) { p0[T] = f32x16{}; p1[T] = f32x16{}; }
-        u32x4 wc[C2];
-#pragma unroll
-        for (int T = 0; T < C2; ++T) wc[T] = w2[((cc * C2 + T) * KH) * 64 + ln];
+      for (int cc = 0; cc < TH; ++cc) {
+        f32x16 p0 = *(const f32x16*)(lb1 + (cc * 2 + gg) * 16);
+        f32x16 p1 = p0;
+        // LDS fragments two K steps ahead of the MFMAs that use them
+        u32x4 w_0 = w2[(cc * KH + 0) * 64 + ln];
+        u32x4 w_1 = w2[(cc * KH + 1) * 64 + ln];
 #pragma unroll
         for (int kb = 0; kb < KH; ++kb) {
-          u32x4 wn[C2];
-#pragma unroll
-          for (int T = 0; T < C2; ++T)
-            wn[T] = w2[((cc * C2 + T) * KH + (kb + 1 < KH ? kb + 1 : kb)) * 64 + ln];
-#pragma unroll
-          for (int T = 0; T < C2; ++T) {
-            p0[T] = mfma_bf16(wc[T], h0[kb], p0[T]);
-            p1[T] = mfma_bf16(wc[T], h1[kb], p1[T]);
-          }
-#pragma unroll
-          for (int T = 0; T < C2; ++T) wc[T] = wn[T];
+          const u32x4 w_2 = w2[(cc * KH + (kb + 2 < KH ? kb + 2 : KH - 1)) * 64 + ln];
+          p0 = mfma_bf16(w_0, h0[kb], p0);
+          p1 = mfma_bf16(w_0, h1[kb], p1);
+          w_0 = w_1;
+          w_1 = w_2;
           __builtin_amdgcn_sched_barrier(0);
         }
+        u32x4 f00, f01, f10, f11;
+        relu_to_frags(p0, f00, f01);
+        relu_to_frags(p1, f10, f11);
 #pragma unroll
-        for (int T = 0; T < C2; ++T) {
-          const int Tg = cc * C2 + T;
-          u32x4 f00, f01, f10, f11;
-          tile_to_frags(p0[T], a.bias[1], Tg, gg, f00, f01);
-          tile_to_frags(p1[T], a.bias[1], Tg, gg, f10, f11);
-#pragma unroll
-          for (int To = 0; To < AT; ++To) {
-            const u32x4 wa = w3[(To * KH + 2 * Tg) * 64 + ln];
-            const u32x4 wb = w3[(To * KH + 2 * Tg + 1) * 64 + ln];
-            o0[To] = mfma_bf16(wa, f00, o0[To]);
-            o1[To] = mfma_bf16(wa, f10, o1[To]);
-            o0[To] = mfma_bf16(wb, f01, o0[To]);
-            o1[To] = mfma_bf16(wb, f11, o1[To]);
-          }
+        for (int To = 0; To < AT; ++To) {
+          const u32x4 wa = w3[(To * KH + 2 * cc) * 64 + ln];
+          const u32x4 wb = w3[(To * KH + 2 * cc + 1) * 64 + ln];
+          o0[To] = mfma_bf16(wa, f00, o0[To]);
+          o1[To] = mfma_bf16(wa, f10, o1[To]);
+          o0[To] = mfma_bf16(wb, f01, o0[To]);
+          o1[To] = mfma_bf16(wb, f11, o1[To]);
         }
       }
-      epilogue<AT>(a, c0, o0, a.bias[2], gg);
-      epilogue<AT>(a, c1, o1, a.bias[2], gg);
+      epilogue<AT>(a, c0, o0, nullptr, gg);
+      epilogue<AT>(a, c1, o1, nullptr, gg);
     }
   }
 }
