@@ -134,6 +134,50 @@ __device__ __forceinline__ u32x4 gather_bf16(const RouteArgs& a, const RowCtx& c
   return v;
 }
 
+// Layer-1 B fragment of K block KB with the embedding width ED known at
+// compile time (ED % 16 == 0): each block is either all embedding (one 16-byte
+// load) or all tail features (two float4 loads of the snapshot row, then the
+// budget feature and zero padding selected by index).
+template <int ED, int KB>
+__device__ __forceinline__ u32x4 gather_ct(const RouteArgs& a, const RowCtx& c, int g) {
+  static_assert(ED % 16 == 0, "embedding width must be a multiple of 16");
+  const int k0 = 16 * KB + 8 * g;
+  if constexpr (16 * KB + 16 <= ED) {
+    const uint16_t* emb = (const uint16_t*)a.emb;
+    return *(const u32x4*)(emb + (size_t)c.q * ED + k0);
+  } else {
+    const int k2 = k0 - ED;
+    const float* row = a.snap + (size_t)c.e * snap_stride(a.M) + k2;
+    const float4 lo = *(const float4*)row;
+    const float4 hi = *(const float4*)(row + 4);
+    const float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+    const float fb = (float)c.budget * a.inv_bud;
+    const int n4 = 4 * a.M;
+    float f[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int kk = k2 + j;
+      f[j] = kk < n4 ? v[j] : (kk == n4 ? fb : 0.f);
+    }
+    u32x4 r;
+    r.x = pack2(f[0], f[1]);
+    r.y = pack2(f[2], f[3]);
+    r.z = pack2(f[4], f[5]);
+    r.w = pack2(f[6], f[7]);
+    return r;
+  }
+}
+
+template <int ED, int KB, int N>
+__device__ __forceinline__ void gather_all(const RouteArgs& a, const RowCtx& c0, const RowCtx& c1,
+                                           int g, u32x4 (&x0)[N], u32x4 (&x1)[N]) {
+  if constexpr (KB < N) {
+    x0[KB] = gather_ct<ED, KB>(a, c0, g);
+    x1[KB] = gather_ct<ED, KB>(a, c1, g);
+    gather_all<ED, KB + 1, N>(a, c0, c1, g, x0, x1);
+  }
+}
+
 // Masked argmax over the lane pair (n, n + 32), logits store, action store.
 template <int AT>
 __device__ __forceinline__ void epilogue(const RouteArgs& a, const RowCtx& c, f32x16 (&acc)[AT],
@@ -420,7 +464,7 @@ __device__ __forceinline__ void copy_to_lds(u32x4* dst, const u32x4* src) {
   }
 }
 
-template <int H, int NL, int AT, int KB1, bool W1L, int NW>
+template <int H, int NL, int AT, int KB1, bool W1L, int NW, int ED>
 __global__ __launch_bounds__(NW * 64, 1) void route_bf16_lds(RouteArgs a) {
   constexpr int TH = H / 32;
   constexpr int KH = H / 16;
@@ -468,11 +512,7 @@ __global__ __launch_bounds__(NW * 64, 1) void route_bf16_lds(RouteArgs a) {
     RowCtx c1 = row_setup_env(a, rows[1], envs[1]);
 
     u32x4 x0[KB1], x1[KB1];
-#pragma unroll
-    for (int kb = 0; kb < KB1; ++kb) {
-      x0[kb] = gather_bf16(a, c0, kb, gg);
-      x1[kb] = gather_bf16(a, c1, kb, gg);
-    }
+    gather_all<ED, 0, KB1>(a, c0, c1, gg, x0, x1);
     u32x4 h0[KH], h1[KH];
 #pragma unroll
     for (int cc = 0; cc < TH; ++cc) {
@@ -577,12 +617,12 @@ constexpr int kLdsWaves = 8;   // waves per block of the persistent kernels (2 p
 
 // Persistent LDS-resident variants for the shapes that fit (bytes of packed
 // weights in LDS <= 160 KiB): returns nullptr when none applies.
-RouteKernel pick_lds(int dtype, int hidden, int n_layers, int out_tiles, int k1) {
+RouteKernel pick_lds(int dtype, int hidden, int n_layers, int out_tiles, int k1, int ed) {
   if (dtype != IM_BF16) return nullptr;
-  if (hidden == 256 && n_layers == 3 && out_tiles == 1 && k1 == 6)
-    return route_bf16_lds<256, 3, 1, 6, false, kLdsWaves>;
-  if (hidden == 256 && n_layers == 2 && out_tiles == 1 && k1 == 7)
-    return route_bf16_lds<256, 2, 1, 7, true, kLdsWaves>;
+  if (hidden == 256 && n_layers == 3 && out_tiles == 1 && k1 == 6 && ed == 64)
+    return route_bf16_lds<256, 3, 1, 6, false, kLdsWaves, 64>;
+  if (hidden == 256 && n_layers == 2 && out_tiles == 1 && k1 == 7 && ed == 64)
+    return route_bf16_lds<256, 2, 1, 7, true, kLdsWaves, 64>;
   return nullptr;
 }
 
@@ -599,7 +639,7 @@ hipError_t launch_route(const RouteArgs& a, int dtype, int hidden, int n_layers,
                         hipStream_t s) {
   if (a.n_total <= 0) return hipSuccess;
   if (a.persistent_blocks > 0) {
-    RouteKernel kl = pick_lds(dtype, hidden, n_layers, out_tiles, a.k1);
+    RouteKernel kl = pick_lds(dtype, hidden, n_layers, out_tiles, a.k1, a.embed_dim);
     if (kl) {
       const int n_tiles = (a.n_total + kLdsWaves * 64 - 1) / (kLdsWaves * 64);
       const unsigned blocks = (unsigned)(n_tiles < a.persistent_blocks ? n_tiles : a.persistent_blocks);
