@@ -100,6 +100,38 @@ def cpu_baseline(cfg, W, b, emb_vals, cap, lb, ticks, Q, budget_s=15.0):
                       f"{dt:.1f} s wall, {nreq / dt:.0f} routed req/s"}
 
 
+def measured_peaks(torch):
+    """Achievable peaks on this device, measured with library kernels: a
+    8192^3 bf16 GEMM (torch.matmul on hipBLASLt) and a 1 GiB device copy."""
+    n = 8192
+    a = torch.randn(n, n, device="cuda", dtype=torch.bfloat16)
+    b = torch.randn(n, n, device="cuda", dtype=torch.bfloat16)
+    for _ in range(3):
+        a @ b
+    torch.cuda.synchronize()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s.record()
+    for _ in range(10):
+        a @ b
+    e.record()
+    torch.cuda.synchronize()
+    gemm_tflops = 10 * 2 * n ** 3 / (s.elapsed_time(e) * 1e-3) / 1e12
+    src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(2):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    s.record()
+    for _ in range(5):
+        dst.copy_(src)
+    e.record()
+    torch.cuda.synchronize()
+    copy_gbs = 5 * 2 * (1 << 30) / (s.elapsed_time(e) * 1e-3) / 1e9
+    del a, b, src, dst
+    torch.cuda.empty_cache()
+    return {"bf16_gemm_tflops": gemm_tflops, "copy_gbs_read_plus_write": copy_gbs}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -113,6 +145,8 @@ def main():
                     help="launch the timed ticks one by one instead of replaying them "
                          "from a captured HIP graph")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-peak-probe", action="store_true",
+                    help="skip the measured-peak probes (a large bf16 GEMM and a device copy)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run 5 device-to-device copies of MIB MiB (calibrates "
                          "the HBM byte counters of a profiler against a known size)")
@@ -251,6 +285,14 @@ def main():
                 "traffic": load_traffic("schedule", tag, source_hash("schedule.hip")),
                 "avg_launch_us": sched_avg * 1e3,
                 "algorithmic_per_launch": f"{byts:.4g} B"}
+
+    if not args.no_peak_probe:
+        mp = measured_peaks(torch)
+        roof["measured_peak"] = mp
+        if roof["unit"] == "TFLOP/s":
+            roof["frac_of_measured"] = roof["achieved"] / mp["bf16_gemm_tflops"]
+        else:
+            roof["frac_of_measured"] = roof["achieved"] / mp["copy_gbs_read_plus_write"]
 
     line = {
         "metric": METRIC, "value": value, "unit": "env-ticks/s", "n_gpus": 1, "steps": K,

@@ -169,12 +169,10 @@ __device__ __forceinline__ u32x4 gather_ct(const RouteArgs& a, const RowCtx& c, 
 }
 
 template <int ED, int KB, int N>
-__device__ __forceinline__ void gather_all(const RouteArgs& a, const RowCtx& c0, const RowCtx& c1,
-                                           int g, u32x4 (&x0)[N], u32x4 (&x1)[N]) {
+__device__ __forceinline__ void gather_row(const RouteArgs& a, const RowCtx& c, int g, u32x4 (&x)[N]) {
   if constexpr (KB < N) {
-    x0[KB] = gather_ct<ED, KB>(a, c0, g);
-    x1[KB] = gather_ct<ED, KB>(a, c1, g);
-    gather_all<ED, KB + 1, N>(a, c0, c1, g, x0, x1);
+    x[KB] = gather_ct<ED, KB>(a, c, g);
+    gather_row<ED, KB + 1, N>(a, c, g, x);
   }
 }
 
@@ -398,8 +396,9 @@ __device__ __forceinline__ int32_t find_env_bsearch(const RouteArgs& a, int32_t 
   return lo < a.E ? lo : a.E - 1;
 }
 
-__device__ __forceinline__ void find_envs2(const RouteArgs& a, int32_t rfirst, int32_t rlast,
-                                           const int32_t (&r)[2], int32_t (&e)[2]) {
+template <int NR>
+__device__ __forceinline__ void find_envs(const RouteArgs& a, int32_t rfirst, int32_t rlast,
+                                          const int32_t (&r)[NR], int32_t (&e)[NR]) {
   const int lane = lane_id();
   const int64_t guess = (int64_t)rfirst * a.E / a.n_total;
   int32_t e_lo = (int32_t)guess - 16;
@@ -414,7 +413,7 @@ __device__ __forceinline__ void find_envs2(const RouteArgs& a, int32_t rfirst, i
     ok = rlast < shfl(ow, 63);
   }
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
+  for (int j = 0; j < NR; ++j) {
     int pos = 0;
 #pragma unroll
     for (int step = 64; step >= 1; step >>= 1) {
@@ -464,7 +463,7 @@ __device__ __forceinline__ void copy_to_lds(u32x4* dst, const u32x4* src) {
   }
 }
 
-template <int H, int NL, int AT, int KB1, bool W1L, int NW, int ED>
+template <int H, int NL, int AT, int KB1, bool W1L, int NW, int ED, int NR>
 __global__ __launch_bounds__(NW * 64, 1) void route_bf16_lds(RouteArgs a) {
   constexpr int TH = H / 32;
   constexpr int KH = H / 16;
@@ -474,6 +473,8 @@ __global__ __launch_bounds__(NW * 64, 1) void route_bf16_lds(RouteArgs a) {
   constexpr int N_LDS = (W1L ? N_W1 : 0) + N_W2 + N_W3;
   // biases in accumulator-register order: [tile][g][16] floats per layer
   constexpr int NB0 = TH * 32, NB1 = (NL == 3 ? TH : AT) * 32, NB2 = NL == 3 ? AT * 32 : 0;
+  constexpr int WROWS = 32 * NR;            // rows per wave
+  constexpr int ROWS = NW * WROWS;          // rows per block tile
   __shared__ u32x4 lds[N_LDS];
   __shared__ float lbias[NB0 + NB1 + NB2];
   if constexpr (W1L) copy_to_lds<N_W1, NW * 64>(lds, (const u32x4*)a.W[0]);
@@ -490,7 +491,6 @@ __global__ __launch_bounds__(NW * 64, 1) void route_bf16_lds(RouteArgs a) {
   const u32x4* w3 = w2 + N_W2;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n = lane & 31, g = lane >> 5;
-  constexpr int ROWS = NW * 64;             // rows per block tile
   const int n_tiles = (a.n_total + ROWS - 1) / ROWS;
 
   for (int tile = blockIdx.x; tile < n_tiles; tile += gridDim.x) {
@@ -502,40 +502,46 @@ __global__ __launch_bounds__(NW * 64, 1) void route_bf16_lds(RouteArgs a) {
     // (and kept live) across the whole loop.
     int ln = lane, gg = g;
     asm volatile("" : "+v"(ln), "+v"(gg));
-    const int32_t r0 = tile * ROWS + wave * 64;
+    const int32_t r0 = tile * ROWS + wave * WROWS;
     if (r0 >= a.n_total) continue;
-    const int32_t rlast = (r0 + 63 < a.n_total ? r0 + 63 : a.n_total - 1);
-    const int32_t rows[2] = {r0 + n, r0 + 32 + n};
-    int32_t envs[2];
-    find_envs2(a, r0, rlast, rows, envs);
-    RowCtx c0 = row_setup_env(a, rows[0], envs[0]);
-    RowCtx c1 = row_setup_env(a, rows[1], envs[1]);
+    const int32_t rlast = (r0 + WROWS - 1 < a.n_total ? r0 + WROWS - 1 : a.n_total - 1);
+    int32_t rows[NR], envs[NR];
+#pragma unroll
+    for (int j = 0; j < NR; ++j) rows[j] = r0 + 32 * j + n;
+    find_envs<NR>(a, r0, rlast, rows, envs);
+    RowCtx c[NR];
+#pragma unroll
+    for (int j = 0; j < NR; ++j) c[j] = row_setup_env(a, rows[j], envs[j]);
+    u32x4 x[NR][KB1];
+#pragma unroll
+    for (int j = 0; j < NR; ++j) gather_row<ED, 0, KB1>(a, c[j], gg, x[j]);
 
-    u32x4 x0[KB1], x1[KB1];
-    gather_all<ED, 0, KB1>(a, c0, c1, gg, x0, x1);
-    u32x4 h0[KH], h1[KH];
+    u32x4 h[NR][KH];
 #pragma unroll
     for (int cc = 0; cc < TH; ++cc) {
       // all layer-1 fragments of this output tile in flight at once
       u32x4 wk[KB1];
 #pragma unroll
       for (int kb = 0; kb < KB1; ++kb) wk[kb] = w1[(cc * KB1 + kb) * 64 + ln];
-      f32x16 p0 = *(const f32x16*)(lb0 + (cc * 2 + gg) * 16);
-      f32x16 p1 = p0;
+      f32x16 p[NR];
+      p[0] = *(const f32x16*)(lb0 + (cc * 2 + gg) * 16);
+#pragma unroll
+      for (int j = 1; j < NR; ++j) p[j] = p[0];
 #pragma unroll
       for (int kb = 0; kb < KB1; ++kb) {
-        p0 = mfma_bf16(wk[kb], x0[kb], p0);
-        p1 = mfma_bf16(wk[kb], x1[kb], p1);
+#pragma unroll
+        for (int j = 0; j < NR; ++j) p[j] = mfma_bf16(wk[kb], x[j][kb], p[j]);
       }
-      relu_to_frags(p0, h0[2 * cc], h0[2 * cc + 1]);
-      relu_to_frags(p1, h1[2 * cc], h1[2 * cc + 1]);
+#pragma unroll
+      for (int j = 0; j < NR; ++j) relu_to_frags(p[j], h[j][2 * cc], h[j][2 * cc + 1]);
       __builtin_amdgcn_sched_barrier(0);
     }
-    f32x16 o0[AT], o1[AT];
+    f32x16 o[NR][AT];
 #pragma unroll
     for (int T = 0; T < AT; ++T) {
-      o0[T] = *(const f32x16*)((NL == 2 ? lb1 : lb2) + (T * 2 + gg) * 16);
-      o1[T] = o0[T];
+      o[0][T] = *(const f32x16*)((NL == 2 ? lb1 : lb2) + (T * 2 + gg) * 16);
+#pragma unroll
+      for (int j = 1; j < NR; ++j) o[j][T] = o[0][T];
     }
     if constexpr (NL == 2) {
 #pragma unroll
@@ -543,45 +549,46 @@ __global__ __launch_bounds__(NW * 64, 1) void route_bf16_lds(RouteArgs a) {
 #pragma unroll
         for (int T = 0; T < AT; ++T) {
           const u32x4 w = w2[(T * KH + kb) * 64 + ln];
-          o0[T] = mfma_bf16(w, h0[kb], o0[T]);
-          o1[T] = mfma_bf16(w, h1[kb], o1[T]);
+#pragma unroll
+          for (int j = 0; j < NR; ++j) o[j][T] = mfma_bf16(w, h[j][kb], o[j][T]);
         }
       }
-      epilogue<AT>(a, c0, o0, nullptr, gg);
-      epilogue<AT>(a, c1, o1, nullptr, gg);
     } else {
 #pragma unroll
       for (int cc = 0; cc < TH; ++cc) {
-        f32x16 p0 = *(const f32x16*)(lb1 + (cc * 2 + gg) * 16);
-        f32x16 p1 = p0;
+        f32x16 p[NR];
+        p[0] = *(const f32x16*)(lb1 + (cc * 2 + gg) * 16);
+#pragma unroll
+        for (int j = 1; j < NR; ++j) p[j] = p[0];
         // LDS fragments two K steps ahead of the MFMAs that use them
         u32x4 w_0 = w2[(cc * KH + 0) * 64 + ln];
         u32x4 w_1 = w2[(cc * KH + 1) * 64 + ln];
 #pragma unroll
         for (int kb = 0; kb < KH; ++kb) {
           const u32x4 w_2 = w2[(cc * KH + (kb + 2 < KH ? kb + 2 : KH - 1)) * 64 + ln];
-          p0 = mfma_bf16(w_0, h0[kb], p0);
-          p1 = mfma_bf16(w_0, h1[kb], p1);
+#pragma unroll
+          for (int j = 0; j < NR; ++j) p[j] = mfma_bf16(w_0, h[j][kb], p[j]);
           w_0 = w_1;
           w_1 = w_2;
           __builtin_amdgcn_sched_barrier(0);
         }
-        u32x4 f00, f01, f10, f11;
-        relu_to_frags(p0, f00, f01);
-        relu_to_frags(p1, f10, f11);
+        u32x4 f[NR][2];
+#pragma unroll
+        for (int j = 0; j < NR; ++j) relu_to_frags(p[j], f[j][0], f[j][1]);
 #pragma unroll
         for (int To = 0; To < AT; ++To) {
           const u32x4 wa = w3[(To * KH + 2 * cc) * 64 + ln];
           const u32x4 wb = w3[(To * KH + 2 * cc + 1) * 64 + ln];
-          o0[To] = mfma_bf16(wa, f00, o0[To]);
-          o1[To] = mfma_bf16(wa, f10, o1[To]);
-          o0[To] = mfma_bf16(wb, f01, o0[To]);
-          o1[To] = mfma_bf16(wb, f11, o1[To]);
+#pragma unroll
+          for (int j = 0; j < NR; ++j) {
+            o[j][To] = mfma_bf16(wa, f[j][0], o[j][To]);
+            o[j][To] = mfma_bf16(wb, f[j][1], o[j][To]);
+          }
         }
       }
-      epilogue<AT>(a, c0, o0, nullptr, gg);
-      epilogue<AT>(a, c1, o1, nullptr, gg);
     }
+#pragma unroll
+    for (int j = 0; j < NR; ++j) epilogue<AT>(a, c[j], o[j], nullptr, gg);
   }
 }
 
@@ -613,16 +620,19 @@ RouteKernel pick(int dtype, int hidden, int at) {
   return nullptr;
 }
 
-constexpr int kLdsWaves = 8;   // waves per block of the persistent kernels (2 per SIMD)
+// Persistent kernels: kLdsWaves waves per block, kLdsRows row tiles (32 rows
+// each) per wave.
+constexpr int kLdsWaves = 16;
+constexpr int kLdsRows = 1;
 
 // Persistent LDS-resident variants for the shapes that fit (bytes of packed
 // weights in LDS <= 160 KiB): returns nullptr when none applies.
 RouteKernel pick_lds(int dtype, int hidden, int n_layers, int out_tiles, int k1, int ed) {
   if (dtype != IM_BF16) return nullptr;
   if (hidden == 256 && n_layers == 3 && out_tiles == 1 && k1 == 6 && ed == 64)
-    return route_bf16_lds<256, 3, 1, 6, false, kLdsWaves, 64>;
+    return route_bf16_lds<256, 3, 1, 6, false, kLdsWaves, 64, kLdsRows>;
   if (hidden == 256 && n_layers == 2 && out_tiles == 1 && k1 == 7 && ed == 64)
-    return route_bf16_lds<256, 2, 1, 7, true, kLdsWaves, 64>;
+    return route_bf16_lds<256, 2, 1, 7, true, kLdsWaves, 64, kLdsRows>;
   return nullptr;
 }
 
@@ -641,7 +651,8 @@ hipError_t launch_route(const RouteArgs& a, int dtype, int hidden, int n_layers,
   if (a.persistent_blocks > 0) {
     RouteKernel kl = pick_lds(dtype, hidden, n_layers, out_tiles, a.k1, a.embed_dim);
     if (kl) {
-      const int n_tiles = (a.n_total + kLdsWaves * 64 - 1) / (kLdsWaves * 64);
+      const int rows = kLdsWaves * 32 * kLdsRows;
+      const int n_tiles = (a.n_total + rows - 1) / rows;
       const unsigned blocks = (unsigned)(n_tiles < a.persistent_blocks ? n_tiles : a.persistent_blocks);
       hipLaunchKernelGGL(kl, dim3(blocks), dim3(kLdsWaves * 64), 0, s, a);
       return hipGetLastError();
