@@ -1,8 +1,8 @@
 // Schedule step of the tick: admission, queue insertion, service, accounting.
 //
-// One wave owns one (env, model) queue; a block holds 4 such waves and the
-// waves never synchronise with each other (no block barriers), so every wave
-// runs its queue independently.
+// One wave owns one env (all of its model queues); a block holds 4 such waves
+// and the waves never synchronise with each other (no block barriers), so
+// every wave runs its env independently.
 //
 // Per queue, in the order the tick defines:
 //   admission  -- the env's routed requests for this model, in id order, are
@@ -212,11 +212,17 @@ constexpr int kStageChunks = 4;   // arrival chunks (of 64) staged in LDS per ro
 // merges its segments into its queue, serves its slots and writes back.
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void schedule_kernel(SchedArgs a) {
   __shared__ int4 stage[4][kStageChunks * 64];
+  __shared__ int32_t hist_lds[4][IM_MAX_ACTIONS];
+  __shared__ int32_t svc_lds[4][IM_MAX_MODELS];
   const int lane = threadIdx.x & 63;
   const int wv = threadIdx.x >> 6;
   const int e = (int)blockIdx.x * 4 + wv;
   if (e >= a.E) return;
   int4* st = stage[wv];
+  int32_t* hist_s = hist_lds[wv];
+  int32_t* svc_s = svc_lds[wv];
+  hist_s[lane] = 0;                     // IM_MAX_ACTIONS == 64 lanes
+  if (lane < IM_MAX_MODELS) svc_s[lane] = 0;
   const int M = a.M, K = a.K;
 
   // ---- validate the env's input; an invalid env is skipped this tick ----
@@ -239,7 +245,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         if (ac < -1 || ac >= a.A) b |= IM_ERR_ACTION;
         if (base == lo) { ac0 = ac; bu0 = bu; sv0 = sv; }
       }
-      bad |= (int32_t)wave_or((uint64_t)(uint32_t)b);
+      // wave-wide OR of the five error bits, one ballot each
+      if (ballot(b & IM_ERR_QIDX)) bad |= IM_ERR_QIDX;
+      if (ballot(b & IM_ERR_BUDGET)) bad |= IM_ERR_BUDGET;
+      if (ballot(b & IM_ERR_SVC)) bad |= IM_ERR_SVC;
+      if (ballot(b & IM_ERR_ACTION)) bad |= IM_ERR_ACTION;
     }
   }
   ModelRec* recs = a.ms + (size_t)e * M;
@@ -257,10 +267,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
   const int32_t room_l = lane < M ? a.qcap - recs[lane].qlen : 0;
   const int32_t next_id = recs[0].next_id;
   int64_t* hist_p = a.hist + (size_t)e * a.A;
-  const int64_t hist_old = lane < a.A ? hist_p[lane] : 0;
   int32_t prior_l = 0;      // lane m: requests routed to model m so far (id order)
   int32_t acc_l = 0;        // lane m: requests accepted by model m so far
-  int32_t hist_l = 0;       // lane a: requests routed with action a
   int32_t nomodel = 0;
   const int n_chunks = (n + 63) / 64;
   const int rounds = n_chunks > 0 ? (n_chunks + kStageChunks - 1) / kStageChunks : 1;
@@ -281,10 +289,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
       }
       const int32_t mdl = ac >= 0 ? ac / K : -1;
       nomodel += popc64(ballot(in && ac < 0));
-      for (int x = 0; x < a.A; ++x) {
-        const int cnt = popc64(ballot(in && ac == x));
-        if (lane == x) hist_l += cnt;
-      }
+      if (in && ac >= 0) atomicAdd(&hist_s[ac], 1);   // routed requests per action
       int32_t rank = 0;
       for (int m = 0; m < M; ++m) {
         const uint64_t bal = ballot(in && mdl == m);
@@ -297,6 +302,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
       const bool acc = in && mdl >= 0 && rank < room;
       const int32_t d = ac - mdl * K;
       const int32_t svc = sv * (d + 1);
+      if (acc) atomicAdd(&svc_s[mdl], svc);          // service time admitted per model
       const int32_t key = a.key_mode == IM_KEY_DEADLINE ? t + bu
                           : (a.key_mode == IM_KEY_FCFS ? t : t + bu - svc);
       // sort key: model (63 for rejected rows) | key biased to unsigned | lane
@@ -341,12 +347,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
       int4 fe = load_front(m, q);
       int4 sl = make_int4(-1, 0, 0, 0);
       int64_t* cnt = a.cnt + (size_t)em * C_NUM;
-      int64_t cnt_old = 0;
-      if (last) {
-        if (lane < a.S) sl = a.slots[(size_t)em * a.S + lane];
-        cnt_old = lane < C_NUM ? cnt[lane] : 0;
-      }
-      int32_t added = 0, svc_in = 0;
+      if (last && lane < a.S) sl = a.slots[(size_t)em * a.S + lane];
+      int32_t added = 0;
       for (int c = 0; c < nch; ++c) {
         const int4 en = st[c * 64 + lane];
         const int seg_lo = popc64(ballot(en.w < m));
@@ -359,8 +361,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         const int64_t ck = lane < k ? composite(kk, id) : kKeyMax;
         insert_sorted(q, k, ck, pay, t, fe, front, pool);
         added += k;
-        svc_in += wave_sum32(lane < k ? (pay & 0xffff) : 0);
       }
+      const int32_t svc_in = svc_s[m];
+      if (lane == 0) svc_s[m] = 0;          // LDS accesses of one wave stay in order
       q.qlen += added;
       q.backlog += svc_in;
       if (lane == m) acc_l += added;
@@ -402,9 +405,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
           const int32_t bu = (int32_t)((uint32_t)en.w >> 16);
           sl = make_int4(en.y, en.z, svc, bu);
         }
-        wait_add += wave_sum32(mine_slot ? t - sl.y : 0);
-        svc_out += wave_sum32(mine_slot ? sl.z : 0);
-        empty &= ~ballot(mine_slot);
+        uint64_t popped = ballot(mine_slot);
+        empty &= ~popped;
+        while (popped) {                       // at most max_slots lanes
+          const int sp = __builtin_ctzll(popped);
+          popped &= popped - 1;
+          wait_add += t - __builtin_amdgcn_readlane(sl.y, sp);
+          svc_out += __builtin_amdgcn_readlane(sl.z, sp);
+        }
         q.fh += take;
         q.fn -= take;
         q.qlen -= take;
@@ -420,16 +428,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
       const int32_t lat = t - sl.y + 1;
       uint64_t dm = done_mask;
       int32_t ewma = q.ewma;
+      int32_t lat_add = 0;
       while (dm) {
         const int s = __builtin_ctzll(dm);
         dm &= dm - 1;
-        const int32_t ls = shfl((int32_t)lat, s);
+        const int32_t ls = __builtin_amdgcn_readlane(lat, s);
+        lat_add += ls;
         const int64_t delta = (int64_t)ls * 256 - ewma;
         const int64_t stepv = delta >= 0 ? (delta >> 3) : -((-delta + 7) >> 3);
         ewma = (int32_t)(ewma + stepv);
       }
       const int32_t completed = popc64(done_mask);
-      const int32_t lat_add = wave_sum32(done ? lat : 0);
       const int32_t slo_add = popc64(ballot(done && lat <= sl.w));
       if (done) sl = make_int4(-1, 0, 0, 0);
       q.busy = popc64(ballot(lane < a.S && sl.x >= 0));
@@ -456,7 +465,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
           case C_LAT_SUM: add = lat_add; break;
           default: add = wait_add; break;
         }
-        cnt[lane] = cnt_old + add;
+        cnt[lane] += add;
       }
       // Snapshot row for the next tick's route step.
       if (lane < 5) write_snap_part(a, e, m, lane, q.qlen, q.busy, q.ewma, q.backlog, q.cap, q.enabled);
@@ -466,7 +475,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     a.env_cnt[(size_t)e * 2] += n;
     a.env_cnt[(size_t)e * 2 + 1] += nomodel;
   }
-  if (lane < a.A) hist_p[lane] = hist_old + hist_l;
+  if (lane < a.A) hist_p[lane] += hist_s[lane];
 }
 
 }  // namespace

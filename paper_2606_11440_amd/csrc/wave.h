@@ -72,11 +72,10 @@ __device__ __forceinline__ void cmpx(int64_t& k, int32_t (&p)[NP], int stride, b
   for (int i = 0; i < NP; ++i) pp[i] = shfl_xor(p[i], stride);
   const bool low = (lane & stride) == 0;
   const bool take = (low == ascending) ? (pk < k) : (pk > k);
-  if (take) {
-    k = pk;
+  // selects, not a branch: the whole network stays straight-line code
+  k = take ? pk : k;
 #pragma unroll
-    for (int i = 0; i < NP; ++i) p[i] = pp[i];
-  }
+  for (int i = 0; i < NP; ++i) p[i] = take ? pp[i] : p[i];
 }
 
 // Ascending bitonic sort of 64 keys (one per lane), payload carried along.
