@@ -106,7 +106,9 @@ __device__ void insert_sorted(Queue& q, int k, int64_t ck, int32_t pay, int32_t 
 }
 
 // Refill the (empty) front with the min(64, P) smallest pool entries.
-__device__ void refill(Queue& q, int4* front, int4* pool) {
+// `pk`/`pi` are this wave's LDS staging rows (64 keys, 64 pool indices), `kb`
+// its LDS buffer for 4 chunks of pool keys.
+__device__ void refill(Queue& q, int4* front, int4* pool, int64_t* pk, int32_t* pi, int2* kb) {
   const int lane = lane_id();
   const int P = q.P;
   if (P <= kFront) {
@@ -122,26 +124,59 @@ __device__ void refill(Queue& q, int4* front, int4* pool) {
     wave_mem_sync();
     return;
   }
-  // Top-64 selection: keep the 64 smallest seen so far, sorted across lanes.
-  int64_t ck = composite(pool[lane].x, pool[lane].y);
+  // Top-64 selection. `ck`/`idx` hold the 64 smallest keys seen so far,
+  // ascending across lanes; thr is the largest of them. Later pool entries
+  // below thr are collected in LDS and merged 64 at a time: a sorted batch,
+  // reversed, taken elementwise-min with the best set gives a bitonic
+  // sequence holding the 64 smallest of both, which one merge network sorts.
+  const int4 e0 = pool[lane];
+  int64_t ck = composite(e0.x, e0.y);
   int32_t idx[1] = {lane};
   bitonic_sort64<1>(ck, idx);
-  for (int c0 = kFront; c0 < P; c0 += kFront) {
-    const int i = c0 + lane;
-    int64_t c2 = kKeyMax;
-    if (i < P) { const int4 e = pool[i]; c2 = composite(e.x, e.y); }
-    const int64_t thr = shfl(ck, 63);
-    const bool cand = c2 < thr;
-    if (ballot(cand) == 0) continue;
-    if (!cand) c2 = kKeyMax;
-    int32_t i2[1] = {i};
-    bitonic_sort64<1>(c2, i2);
-    // min(best[l], chunk[63 - l]) is bitonic and holds the 64 smallest.
-    const int64_t rc = shfl(c2, 63 - lane);
-    const int32_t ri = shfl(i2[0], 63 - lane);
-    if (rc < ck) { ck = rc; idx[0] = ri; }
+  int64_t thr = readlane64(ck, 63);
+  int np = 0;   // candidates staged in pk/pi[0, np)
+  auto flush = [&]() {
+    int64_t bk = lane < np ? pk[lane] : kKeyMax;
+    int32_t bi[1] = {lane < np ? pi[lane] : 0};
+    bitonic_sort64<1>(bk, bi);
+    const int64_t rk = shfl(bk, 63 - lane);
+    const int32_t ri = shfl(bi[0], 63 - lane);
+    if (rk < ck) { ck = rk; idx[0] = ri; }
     bitonic_merge64<1>(ck, idx);
+    thr = readlane64(ck, 63);
+    np = 0;
+  };
+  constexpr int G = 4;   // pool chunks whose loads are in flight together
+  const int2* keys = reinterpret_cast<const int2*>(pool);   // (key, id) of entry i at keys[2 i]
+  for (int c0 = kFront; c0 < P; c0 += G * kFront) {
+    int2 kv[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const int i = c0 + g * kFront + lane;
+      kv[g] = i < P ? keys[2 * i] : make_int2(0x7fffffff, -1);   // (max, max) pads
+    }
+#pragma unroll
+    for (int g = 0; g < G; ++g) kb[g * kFront + lane] = kv[g];
+#pragma unroll 1
+    for (int g = 0; g < G; ++g) {
+      const int2 v = kb[g * kFront + lane];
+      const int64_t kc = composite(v.x, v.y);
+      uint64_t cm = ballot(kc < thr);
+      if (cm == 0) continue;
+      if (np + popc64(cm) > kFront) {
+        flush();
+        cm = ballot(kc < thr);
+        if (cm == 0) continue;
+      }
+      if ((cm >> lane) & 1ull) {
+        const int pos = np + prefix_count(cm);
+        pk[pos] = kc;
+        pi[pos] = c0 + g * kFront + lane;
+      }
+      np += popc64(cm);
+    }
   }
+  if (np > 0) flush();
   const int sel = idx[0];
   const int4 e = pool[sel];
   front[lane] = e;
@@ -214,6 +249,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
   __shared__ int4 stage[4][kStageChunks * 64];
   __shared__ int32_t hist_lds[4][IM_MAX_ACTIONS];
   __shared__ int32_t svc_lds[4][IM_MAX_MODELS];
+  __shared__ int64_t pend_k[4][kFront];   // refill candidate staging
+  __shared__ int32_t pend_i[4][kFront];
+  __shared__ int2 pend_kb[4][4 * kFront];
   const int lane = threadIdx.x & 63;
   const int wv = threadIdx.x >> 6;
   const int e = (int)blockIdx.x * 4 + wv;
@@ -381,25 +419,23 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
       uint64_t empty = ballot(lane < capc && sl.x < 0);
       int32_t started = 0;
       int32_t wait_add = 0, svc_out = 0;
-      bool fe_valid = true;   // fe mirrors front[fh + lane] until a refill
-      const int fe_base = q.fh;
+      int fe_base = q.fh;     // fe mirrors front[fe_base + lane]
       while (empty != 0 && q.qlen > 0) {
-        if (q.fn == 0) { refill(q, front, pool); fe_valid = false; }
+        if (q.fn == 0) { refill(q, front, pool, pend_k[wv], pend_i[wv], pend_kb[wv]);
+          fe = lane < q.fn ? front[lane] : make_int4(0, 0, 0, 0);   // new front, fh = 0
+          fe_base = 0;
+        }
         if (q.fn == 0) break;   // unreachable while qlen == fn + P holds; never spin
         const int need = popc64(empty);
         const int take = need < q.fn ? need : q.fn;
         const int rnk = prefix_count(empty);
         const bool mine_slot = ((empty >> lane) & 1ull) && rnk < take;
-        int4 en = make_int4(0, 0, 0, 0);
-        if (fe_valid) {
-          const int src = (q.fh - fe_base + rnk) & 63;
-          en.x = shfl((int32_t)fe.x, src);
-          en.y = shfl((int32_t)fe.y, src);
-          en.z = shfl((int32_t)fe.z, src);
-          en.w = shfl((int32_t)fe.w, src);
-        } else if (mine_slot) {
-          en = front[q.fh + rnk];
-        }
+        int4 en;
+        const int src = (q.fh - fe_base + rnk) & 63;
+        en.x = shfl((int32_t)fe.x, src);
+        en.y = shfl((int32_t)fe.y, src);
+        en.z = shfl((int32_t)fe.z, src);
+        en.w = shfl((int32_t)fe.w, src);
         if (mine_slot) {
           const int32_t svc = en.w & 0xffff;
           const int32_t bu = (int32_t)((uint32_t)en.w >> 16);

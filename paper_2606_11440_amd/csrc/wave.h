@@ -42,6 +42,12 @@ __device__ __forceinline__ int64_t shfl(int64_t v, int src) {
   int32_t hi = __shfl((int32_t)(v >> 32), src, kWave);
   return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
 }
+// Value of a 64-bit variable in lane `src` (wave-uniform result).
+__device__ __forceinline__ int64_t readlane64(int64_t v, int src) {
+  const uint32_t lo = __builtin_amdgcn_readlane((int32_t)(uint32_t)v, src);
+  const uint32_t hi = __builtin_amdgcn_readlane((int32_t)(v >> 32), src);
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
 __device__ __forceinline__ int32_t shfl_xor(int32_t v, int m) { return __shfl_xor(v, m, kWave); }
 __device__ __forceinline__ int64_t shfl_xor(int64_t v, int m) {
   int32_t lo = __shfl_xor((int32_t)(uint32_t)v, m, kWave);
