@@ -12,12 +12,13 @@
 //                 i.e. latest start time), t + budget (deadline, Sec. 4.3) or t
 //                 (arrival order). The queue order is (key, id).
 //   insertion  -- the queue is kept as a sorted front of at most 64 entries
-//                 (one per lane) holding the smallest keys, plus an unsorted
-//                 pool of the rest. A chunk of up to 64 newcomers is sorted with
-//                 a bitonic network; those below the front's largest key are
-//                 merged into the front (its overflow spills to the pool), the
-//                 others are appended to the pool. No suffix of a sorted array
-//                 is ever rewritten.
+//                 (one per lane, held in registers while the wave works on the
+//                 queue) with the smallest keys, plus an unsorted pool of the
+//                 rest. The env's arrivals are sorted 64 at a time by (model,
+//                 key, id); a model's newcomers below the front's largest key
+//                 are merged into the front with a bitonic merge network (its
+//                 overflow spills to the pool), the others are appended to the
+//                 pool. The front array is written once per tick, if changed.
 //   service    -- free slots below c_m are filled in slot order from the front
 //                 head; when the front runs empty it is refilled with the 64
 //                 smallest pool entries (bitonic top-64 selection), and the
@@ -39,18 +40,6 @@ __device__ __forceinline__ int64_t composite(int32_t key, int32_t id) {
 __device__ __forceinline__ int32_t comp_key(int64_t c) { return (int32_t)(c >> 32); }
 __device__ __forceinline__ int32_t comp_id(int64_t c) { return (int32_t)(uint32_t)c; }
 
-// Number of entries of the ascending sequence X (lanes [0, len)) below v.
-__device__ __forceinline__ int count_below(int64_t X, int len, int64_t v) {
-  int pos = 0;
-#pragma unroll
-  for (int step = 64; step >= 1; step >>= 1) {
-    const int probe = pos + step - 1;
-    const int64_t xp = shfl(X, probe < 64 ? probe : 63);
-    if (probe < len && xp < v) pos += step;
-  }
-  return pos;
-}
-
 // Makes this wave's earlier global stores visible to its later loads.
 __device__ __forceinline__ void wave_mem_sync() { __threadfence_block(); }
 
@@ -58,70 +47,61 @@ struct Queue {       // wave-uniform view of one (env, model) record
   int32_t qlen, busy, ewma, backlog, cap, enabled, fh, fn, P, next_id;
 };
 
-// Insert k newcomers, already sorted by (key, id) in lanes [0, k), into the
-// front/pool structure. Newcomer payload: ck = (key, id), pay = svc | budget << 16.
-// `fe` holds the current front in lane order (lane i < fn: front[fh + i]); it
-// is updated to the new front when the front changes (then fh = 0).
-__device__ void insert_sorted(Queue& q, int k, int64_t ck, int32_t pay, int32_t t_arr, int4& fe,
-                              int4* front, int4* pool) {
+// Merge `lim` newcomers into the front held in registers (`fe`, lane i <
+// q.fn), all of them below the front's largest key or the pool empty. `seg`
+// is the model's sorted segment of a staged chunk in LDS (entries (key, id,
+// svc | budget << 16, model)); newcomers arrive at tick t. The front followed
+// by the reversed newcomers is a bitonic sequence of 128; its half-cleaner
+// leaves the 64 smallest in `lo` (bitonic, sorted by one merge network) and
+// the rest in `hi`, whose real entries spill to the pool.
+__device__ __forceinline__ void merge_front(Queue& q, int4& fe, const int4* seg, int lim,
+                                            int32_t t, int4* pool) {
   const int lane = lane_id();
-  const int64_t fck = lane < q.fn ? composite(fe.x, fe.y) : kKeyMax;
-  int lim;
-  if (q.P == 0) {
-    lim = k;
-  } else if (q.fn == 0) {
-    lim = 0;
-  } else {
-    const int64_t fmax = shfl(fck, q.fn - 1);
-    lim = popc64(ballot(lane < k && ck < fmax));
+  const int r = 63 - lane;
+  int64_t kb = kKeyMax;
+  int32_t pb[2] = {0, 0};
+  if (r < lim) {
+    const int4 v = seg[r];
+    kb = composite(v.x, v.y);
+    pb[0] = t;
+    pb[1] = v.z;
   }
-  if (lim > 0) {
-    // Merge the front (lanes [0, fn)) with newcomers [0, lim); positions in
-    // the merged order follow from counting the other sequence's smaller keys
-    // (all composite keys are distinct).
-    const int64_t nck = lane < lim ? ck : kKeyMax;
-    const int posf = lane + count_below(nck, lim, fck);
-    const int posn = lane + count_below(fck, q.fn, nck);
-    const int total = q.fn + lim;
-    const int keep = total < kFront ? total : kFront;
-    if (lane < q.fn) {
-      if (posf < kFront) front[posf] = fe;
-      else pool[q.P + posf - kFront] = fe;
-    }
-    if (lane < lim) {
-      const int4 ne = make_int4(comp_key(ck), comp_id(ck), t_arr, pay);
-      if (posn < kFront) front[posn] = ne;
-      else pool[q.P + posn - kFront] = ne;
-    }
-    q.P += total - keep;
-    q.fh = 0;
-    q.fn = keep;
-    wave_mem_sync();
-    fe = lane < keep ? front[lane] : make_int4(0, 0, 0, 0);
-  }
-  if (lane >= lim && lane < k)
-    pool[q.P + lane - lim] = make_int4(comp_key(ck), comp_id(ck), t_arr, pay);
-  q.P += k - lim;
-  wave_mem_sync();
+  const int64_t ka = lane < q.fn ? composite(fe.x, fe.y) : kKeyMax;
+  const bool sw = kb < ka;
+  int64_t klo = sw ? kb : ka;
+  const int64_t khi = sw ? ka : kb;
+  int32_t plo[2] = {sw ? pb[0] : fe.z, sw ? pb[1] : fe.w};
+  const int32_t phi0 = sw ? fe.z : pb[0], phi1 = sw ? fe.w : pb[1];
+  bitonic_merge64<2>(klo, plo);
+  const int total = q.fn + lim;
+  const int keep = total < kFront ? total : kFront;
+  const bool spill = khi != kKeyMax;
+  const uint64_t sm = ballot(spill);
+  if (spill) pool[q.P + prefix_count(sm)] = make_int4(comp_key(khi), comp_id(khi), phi0, phi1);
+  q.P += total - keep;
+  q.fh = 0;
+  q.fn = keep;
+  fe = lane < keep ? make_int4(comp_key(klo), comp_id(klo), plo[0], plo[1]) : make_int4(0, 0, 0, 0);
 }
 
-// Refill the (empty) front with the min(64, P) smallest pool entries.
+// Refill the (empty) front with the min(64, P) smallest pool entries; the new
+// front is returned in `fe` (lane i: entry i), the front array is not written.
 // `pk`/`pi` are this wave's LDS staging rows (64 keys, 64 pool indices), `kb`
 // its LDS buffer for 4 chunks of pool keys.
-__device__ void refill(Queue& q, int4* front, int4* pool, int64_t* pk, int32_t* pi, int2* kb) {
+__device__ void refill(Queue& q, int4& fe, int4* pool, int64_t* pk, int32_t* pi, int2* kb) {
   const int lane = lane_id();
   const int P = q.P;
+  wave_mem_sync();   // this tick's pool appends are read below
   if (P <= kFront) {
     int4 e = make_int4(0, 0, 0, 0);
     int64_t ck = kKeyMax;
     if (lane < P) { e = pool[lane]; ck = composite(e.x, e.y); }
     int32_t pay[2] = {e.z, e.w};
     bitonic_sort64<2>(ck, pay);
-    if (lane < P) front[lane] = make_int4(comp_key(ck), comp_id(ck), pay[0], pay[1]);
+    fe = lane < P ? make_int4(comp_key(ck), comp_id(ck), pay[0], pay[1]) : make_int4(0, 0, 0, 0);
     q.fh = 0;
     q.fn = P;
     q.P = 0;
-    wave_mem_sync();
     return;
   }
   // Top-64 selection. `ck`/`idx` hold the 64 smallest keys seen so far,
@@ -178,8 +158,7 @@ __device__ void refill(Queue& q, int4* front, int4* pool, int64_t* pk, int32_t* 
   }
   if (np > 0) flush();
   const int sel = idx[0];
-  const int4 e = pool[sel];
-  front[lane] = e;
+  fe = pool[sel];
   // Compact the pool: selected entries below the new size are holes, filled
   // with the unselected entries of the last 64 positions (same count).
   const int Pn = P - kFront;
@@ -196,7 +175,6 @@ __device__ void refill(Queue& q, int4* front, int4* pool, int64_t* pk, int32_t* 
   q.fh = 0;
   q.fn = kFront;
   q.P = Pn;
-  wave_mem_sync();
 }
 
 // Snapshot row entry of model m of env e from its state (one fp32 product
@@ -383,21 +361,37 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
       int4* front = a.front + (size_t)em * kFront;
       int4* pool = a.pool + (size_t)em * a.qcap;
       int4 fe = load_front(m, q);
+      int fe_base = q.fh;     // fe lane i mirrors front[fe_base + i]
       int4 sl = make_int4(-1, 0, 0, 0);
       int64_t* cnt = a.cnt + (size_t)em * C_NUM;
       if (last && lane < a.S) sl = a.slots[(size_t)em * a.S + lane];
       int32_t added = 0;
+      bool dirty = false;   // the front in registers differs from the front array
       for (int c = 0; c < nch; ++c) {
         const int4 en = st[c * 64 + lane];
-        const int seg_lo = popc64(ballot(en.w < m));
-        const int k = popc64(ballot(en.w == m));
+        const bool mine = en.w == m;
+        const int k = popc64(ballot(mine));
         if (k == 0) continue;
-        const int src = (seg_lo + lane) & 63;
-        const int32_t kk = shfl((int32_t)en.x, src);
-        const int32_t id = shfl((int32_t)en.y, src);
-        const int32_t pay = shfl((int32_t)en.z, src);
-        const int64_t ck = lane < k ? composite(kk, id) : kKeyMax;
-        insert_sorted(q, k, ck, pay, t, fe, front, pool);
+        const int seg_lo = popc64(ballot(en.w < m));
+        const int o = lane - seg_lo;   // offset in the model's sorted segment
+        // newcomers merged into the front: those below its largest key, or
+        // all of them while the pool is empty (the front then holds the queue)
+        int lim;
+        if (q.P == 0) {
+          lim = k;
+        } else if (q.fn == 0) {
+          lim = 0;
+        } else {
+          const int64_t fmax = readlane64(composite(fe.x, fe.y), q.fn - 1);
+          lim = popc64(ballot(mine && composite(en.x, en.y) < fmax));
+        }
+        if (mine && o >= lim) pool[q.P + o - lim] = make_int4(en.x, en.y, t, en.z);
+        q.P += k - lim;
+        if (lim > 0) {
+          merge_front(q, fe, st + c * 64 + seg_lo, lim, t, pool);
+          fe_base = 0;
+          dirty = true;
+        }
         added += k;
       }
       const int32_t svc_in = svc_s[m];
@@ -406,6 +400,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
       q.backlog += svc_in;
       if (lane == m) acc_l += added;
       if (!last) {
+        if (dirty && lane >= q.fh - fe_base && lane < q.fh - fe_base + q.fn)
+          front[fe_base + lane] = fe;   // the live window [fh, fh + fn)
         if (lane == 0) {
           rec->qlen = q.qlen; rec->backlog = q.backlog;
           rec->fh = q.fh; rec->fn = q.fn; rec->P = q.P;
@@ -419,11 +415,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
       uint64_t empty = ballot(lane < capc && sl.x < 0);
       int32_t started = 0;
       int32_t wait_add = 0, svc_out = 0;
-      int fe_base = q.fh;     // fe mirrors front[fe_base + lane]
       while (empty != 0 && q.qlen > 0) {
-        if (q.fn == 0) { refill(q, front, pool, pend_k[wv], pend_i[wv], pend_kb[wv]);
-          fe = lane < q.fn ? front[lane] : make_int4(0, 0, 0, 0);   // new front, fh = 0
+        if (q.fn == 0) {
+          refill(q, fe, pool, pend_k[wv], pend_i[wv], pend_kb[wv]);
           fe_base = 0;
+          dirty = true;
         }
         if (q.fn == 0) break;   // unreachable while qlen == fn + P holds; never spin
         const int need = popc64(empty);
@@ -482,6 +478,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
       q.next_id += n;
 
       // ---- write back ----
+      if (dirty && lane >= q.fh - fe_base && lane < q.fh - fe_base + q.fn)
+          front[fe_base + lane] = fe;   // the live window [fh, fh + fn)
       if (lane < a.S) a.slots[(size_t)em * a.S + lane] = sl;
       if (lane == 0) {
         rec->qlen = q.qlen; rec->busy = q.busy; rec->ewma = q.ewma; rec->backlog = q.backlog;

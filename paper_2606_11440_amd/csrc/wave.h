@@ -67,16 +67,48 @@ __device__ __forceinline__ uint64_t wave_or(uint64_t v) {
   return v;
 }
 
-// One compare-exchange stage of a bitonic network: this lane keeps the
-// smaller key if it is the "low" end of an ascending pair.
-template <int NP>
-__device__ __forceinline__ void cmpx(int64_t& k, int32_t (&p)[NP], int stride, bool ascending) {
-  const int lane = lane_id();
-  int64_t pk = shfl_xor(k, stride);
+// Value of v in lane (lane ^ S), S a power of two up to 32, with no LDS
+// traffic: DPP moves inside rows of 16 lanes, the gfx950 permlane swaps
+// across rows. Every lane of the wave must be active.
+template <int S>
+__device__ __forceinline__ int32_t xshfl(int32_t v) {
+  static_assert(S == 1 || S == 2 || S == 4 || S == 8 || S == 16 || S == 32, "xor distance");
+  if constexpr (S == 1) {
+    return __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xf, 0xf, false);    // quad_perm [1,0,3,2]
+  } else if constexpr (S == 2) {
+    return __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xf, 0xf, false);    // quad_perm [2,3,0,1]
+  } else if constexpr (S == 4) {
+    // i ^ 4 == 7 - (i ^ 3) inside each 8 lanes: quad_perm [3,2,1,0], then half-row mirror
+    const int32_t r = __builtin_amdgcn_update_dpp(0, v, 0x1B, 0xf, 0xf, false);
+    return __builtin_amdgcn_update_dpp(0, r, 0x141, 0xf, 0xf, false);
+  } else if constexpr (S == 8) {
+    return __builtin_amdgcn_update_dpp(0, v, 0x128, 0xf, 0xf, false);   // row_ror:8
+  } else if constexpr (S == 16) {
+    // swap(odd rows of a, even rows of b) with a = b = v: a' = rows (0,0,2,2), b' = (1,1,3,3)
+    const auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+    return (lane_id() & 16) ? (int32_t)r[0] : (int32_t)r[1];
+  } else {
+    // swap(upper half of a, lower half of b): a' = (lo, lo), b' = (hi, hi)
+    const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+    return (lane_id() & 32) ? (int32_t)r[0] : (int32_t)r[1];
+  }
+}
+template <int S>
+__device__ __forceinline__ int64_t xshfl(int64_t v) {
+  const int32_t lo = xshfl<S>((int32_t)(uint32_t)v);
+  const int32_t hi = xshfl<S>((int32_t)(v >> 32));
+  return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+}
+
+// One compare-exchange stage of a bitonic network at xor distance S: this
+// lane keeps the smaller key if it is the low end of an ascending pair.
+template <int S, int NP>
+__device__ __forceinline__ void cmpx(int64_t& k, int32_t (&p)[NP], bool ascending) {
+  const int64_t pk = xshfl<S>(k);
   int32_t pp[NP];
 #pragma unroll
-  for (int i = 0; i < NP; ++i) pp[i] = shfl_xor(p[i], stride);
-  const bool low = (lane & stride) == 0;
+  for (int i = 0; i < NP; ++i) pp[i] = xshfl<S>(p[i]);
+  const bool low = (lane_id() & S) == 0;
   const bool take = (low == ascending) ? (pk < k) : (pk > k);
   // selects, not a branch: the whole network stays straight-line code
   k = take ? pk : k;
@@ -84,23 +116,39 @@ __device__ __forceinline__ void cmpx(int64_t& k, int32_t (&p)[NP], int stride, b
   for (int i = 0; i < NP; ++i) p[i] = take ? pp[i] : p[i];
 }
 
+// Ascending sort of a bitonic sequence of 64 keys (a half-cleaner cascade).
+template <int NP>
+__device__ __forceinline__ void bitonic_merge64(int64_t& k, int32_t (&p)[NP]) {
+  cmpx<32, NP>(k, p, true);
+  cmpx<16, NP>(k, p, true);
+  cmpx<8, NP>(k, p, true);
+  cmpx<4, NP>(k, p, true);
+  cmpx<2, NP>(k, p, true);
+  cmpx<1, NP>(k, p, true);
+}
+
+// Merge stages of block size SIZE: ascending where lane & SIZE is 0 (or for
+// the full 64), descending otherwise.
+template <int SIZE, int NP>
+__device__ __forceinline__ void bitonic_block(int64_t& k, int32_t (&p)[NP]) {
+  const bool asc = SIZE == kWave || (lane_id() & SIZE) == 0;
+  if constexpr (SIZE >= 64) cmpx<32, NP>(k, p, asc);
+  if constexpr (SIZE >= 32) cmpx<16, NP>(k, p, asc);
+  if constexpr (SIZE >= 16) cmpx<8, NP>(k, p, asc);
+  if constexpr (SIZE >= 8) cmpx<4, NP>(k, p, asc);
+  if constexpr (SIZE >= 4) cmpx<2, NP>(k, p, asc);
+  cmpx<1, NP>(k, p, asc);
+}
+
 // Ascending bitonic sort of 64 keys (one per lane), payload carried along.
 template <int NP>
 __device__ __forceinline__ void bitonic_sort64(int64_t& k, int32_t (&p)[NP]) {
-  const int lane = lane_id();
-#pragma unroll
-  for (int size = 2; size <= kWave; size <<= 1) {
-#pragma unroll
-    for (int stride = size >> 1; stride > 0; stride >>= 1)
-      cmpx<NP>(k, p, stride, (lane & size) == 0 || size == kWave);
-  }
-}
-
-// Ascending sort of a bitonic sequence of 64 keys.
-template <int NP>
-__device__ __forceinline__ void bitonic_merge64(int64_t& k, int32_t (&p)[NP]) {
-#pragma unroll
-  for (int stride = kWave >> 1; stride > 0; stride >>= 1) cmpx<NP>(k, p, stride, true);
+  bitonic_block<2, NP>(k, p);
+  bitonic_block<4, NP>(k, p);
+  bitonic_block<8, NP>(k, p);
+  bitonic_block<16, NP>(k, p);
+  bitonic_block<32, NP>(k, p);
+  bitonic_block<64, NP>(k, p);
 }
 
 // fp32 -> bf16 bits, round to nearest even (NaN kept quiet).
