@@ -96,6 +96,22 @@ __device__ __forceinline__ uint32_t pack2(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
 }
 
+// ReLU of a float as one integer max on its bits: every negative value
+// (and -0) has the sign bit set, so it is below 0 as an int32.
+__device__ __forceinline__ float relu(float x) {
+  return __int_as_float(max(__float_as_int(x), 0));
+}
+
+// bf16(ReLU(lo)), bf16(ReLU(hi)) packed. Rounding to nearest even keeps the
+// sign (a negative value rounds to a negative value or -0), so the ReLU is
+// applied after rounding, to both halves at once, as a packed signed 16-bit
+// max with 0.
+__device__ __forceinline__ uint32_t relu_pack2(float lo, float hi) {
+  typedef short s16x2 __attribute__((ext_vector_type(2)));
+  const s16x2 r = __builtin_bit_cast(s16x2, pack2(lo, hi));
+  return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(r, (s16x2){0, 0}));
+}
+
 // Layer-1 B fragment of K block kb (bf16): features 16 kb + 8 g + j, j = 0..7.
 __device__ __forceinline__ u32x4 gather_bf16(const RouteArgs& a, const RowCtx& c, int kb, int g) {
   const int k0 = 16 * kb + 8 * g;
@@ -220,22 +236,19 @@ __device__ __forceinline__ void tile_to_frags(const f32x16& acc, const float* bi
                                               u32x4& f0, u32x4& f1) {
   float h[16];
 #pragma unroll
-  for (int v = 0; v < 16; ++v) h[v] = fmaxf(acc[v] + bias[(T * 2 + g) * 16 + v], 0.f);
-  f0.x = pack2(h[0], h[1]);   f0.y = pack2(h[2], h[3]);
-  f0.z = pack2(h[4], h[5]);   f0.w = pack2(h[6], h[7]);
-  f1.x = pack2(h[8], h[9]);   f1.y = pack2(h[10], h[11]);
-  f1.z = pack2(h[12], h[13]); f1.w = pack2(h[14], h[15]);
+  for (int v = 0; v < 16; ++v) h[v] = acc[v] + bias[(T * 2 + g) * 16 + v];
+  f0.x = relu_pack2(h[0], h[1]);   f0.y = relu_pack2(h[2], h[3]);
+  f0.z = relu_pack2(h[4], h[5]);   f0.w = relu_pack2(h[6], h[7]);
+  f1.x = relu_pack2(h[8], h[9]);   f1.y = relu_pack2(h[10], h[11]);
+  f1.z = relu_pack2(h[12], h[13]); f1.w = relu_pack2(h[14], h[15]);
 }
 
 // ReLU + bf16 rounding of one accumulator tile (bias already included).
 __device__ __forceinline__ void relu_to_frags(const f32x16& acc, u32x4& f0, u32x4& f1) {
-  float h[16];
-#pragma unroll
-  for (int v = 0; v < 16; ++v) h[v] = fmaxf(acc[v], 0.f);
-  f0.x = pack2(h[0], h[1]);   f0.y = pack2(h[2], h[3]);
-  f0.z = pack2(h[4], h[5]);   f0.w = pack2(h[6], h[7]);
-  f1.x = pack2(h[8], h[9]);   f1.y = pack2(h[10], h[11]);
-  f1.z = pack2(h[12], h[13]); f1.w = pack2(h[14], h[15]);
+  f0.x = relu_pack2(acc[0], acc[1]);   f0.y = relu_pack2(acc[2], acc[3]);
+  f0.z = relu_pack2(acc[4], acc[5]);   f0.w = relu_pack2(acc[6], acc[7]);
+  f1.x = relu_pack2(acc[8], acc[9]);   f1.y = relu_pack2(acc[10], acc[11]);
+  f1.z = relu_pack2(acc[12], acc[13]); f1.w = relu_pack2(acc[14], acc[15]);
 }
 
 template <int H, int NL, int AT>
@@ -328,7 +341,7 @@ __global__ __launch_bounds__(256) void route_f32(RouteArgs a) {
 #pragma unroll
   for (int T = 0; T < TH; ++T) {
 #pragma unroll
-    for (int v = 0; v < 16; ++v) acc[T][v] = fmaxf(acc[T][v] + a.bias[0][(T * 2 + g) * 16 + v], 0.f);
+    for (int v = 0; v < 16; ++v) acc[T][v] = relu(acc[T][v] + a.bias[0][(T * 2 + g) * 16 + v]);
   }
   f32x16 out[AT];
 #pragma unroll
@@ -362,7 +375,7 @@ __global__ __launch_bounds__(256) void route_f32(RouteArgs a) {
         const int Tg = cc * TC + T;
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          const float h = fmaxf(acc2[T][v] + a.bias[1][(Tg * 2 + g) * 16 + v], 0.f);
+          const float h = relu(acc2[T][v] + a.bias[1][(Tg * 2 + g) * 16 + v]);
           const int i3 = 16 * Tg + v;
 #pragma unroll
           for (int To = 0; To < AT; ++To)
