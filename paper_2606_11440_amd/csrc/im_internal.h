@@ -14,8 +14,12 @@ namespace im {
 struct alignas(64) ModelRec {
   int32_t qlen, busy, ewma, backlog;   // snapshot fields read by the route step
   int32_t cap, enabled, fh, fn;
-  int32_t P, next_id, t, pad1;         // t: ticks completed by this env (same in all M records)
-  int32_t pad2, pad3, pad4, pad5;
+  int32_t P;
+  int32_t next_id, t;                  // the env's next request id and ticks completed
+                                       // (kept in the env's first record only)
+  int32_t busy_mask;                   // bit s: slot s busy
+  int32_t next_done;                   // earliest completion tick of a busy slot
+  int32_t pad3, pad4, pad5;
 };
 static_assert(sizeof(ModelRec) == 64, "ModelRec layout");
 
@@ -38,7 +42,8 @@ enum { C_REJ_OVERFLOW = 0, C_ENQUEUED, C_STARTED, C_COMPLETED, C_SLO_MET, C_LAT_
        C_WAIT_SUM, C_NUM = 8 };
 
 // Queue entry in device memory: {key, id, t_arr, svc | budget << 16}.
-// Slot in device memory: {id (-1 free), t_arr, rem, budget}.
+// Slot in device memory: {id (-1 free), t_arr, tick at which it completes, budget};
+// the state export reports the service ticks left instead of the completion tick.
 
 struct RouteArgs {
   const int32_t* offsets;

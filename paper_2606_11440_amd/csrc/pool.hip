@@ -241,7 +241,11 @@ im_status im_pool_create(const im_pool_desc* desc, const float* const* W, const 
   if (st == IM_OK) {
     std::vector<ModelRec> recs(EM);
     std::memset(recs.data(), 0, EM * sizeof(ModelRec));
-    for (size_t i = 0; i < EM; ++i) { recs[i].cap = capacity[i]; recs[i].enabled = 1; }
+    for (size_t i = 0; i < EM; ++i) {
+      recs[i].cap = capacity[i];
+      recs[i].enabled = 1;
+      recs[i].next_done = INT32_MAX;
+    }
     st = upload(p, &p->ms, recs);
   }
   if (st == IM_OK) st = zalloc(p, &p->cnt, EM * im::C_NUM);
@@ -456,8 +460,21 @@ im_status im_read_state(im_pool* p, int32_t env_begin, int32_t env_count, int32_
       o.lat_sum = c[im::C_LAT_SUM]; o.wait_sum = c[im::C_WAIT_SUM];
     }
   }
-  if (slots && EMc)
-    IM_HIP(p, hipMemcpy(slots, p->slots + em0 * S, EMc * S * sizeof(int4), hipMemcpyDeviceToHost));
+  if (slots && EMc) {
+    // The device keeps a busy slot's completion tick; the state reports the
+    // service ticks left after the env's last completed tick.
+    std::vector<int4> sl(EMc * S);
+    IM_HIP(p, hipMemcpy(sl.data(), p->slots + em0 * S, sl.size() * sizeof(int4), hipMemcpyDeviceToHost));
+    for (size_t i = 0; i < EMc; ++i) {
+      const int32_t t_env = recs[(i / M) * M].t;
+      for (int s = 0; s < S; ++s) {
+        const int4 v = sl[i * S + s];
+        im_slot& o = slots[i * S + s];
+        if (v.x >= 0) { o.id = v.x; o.t_arr = v.y; o.rem = v.z - t_env + 1; o.budget = v.w; }
+        else { o.id = -1; o.t_arr = 0; o.rem = 0; o.budget = 0; }
+      }
+    }
+  }
   if (hist && env_count)
     IM_HIP(p, hipMemcpy(hist, p->hist + (size_t)env_begin * A, (size_t)env_count * A * 8,
                         hipMemcpyDeviceToHost));
@@ -520,20 +537,27 @@ im_status im_write_state(im_pool* p, int32_t env_begin, int32_t env_count, int32
       if (q[k].id < 0 || q[k].id >= envs[e].next_id) return fail(p, IM_ESTATE, "queue id out of range");
     }
     if (bl != ms.backlog) return fail(p, IM_ESTATE, "backlog != sum of queued svc");
-    int busy = 0;
+    int busy = 0, busy_mask = 0, next_done = INT32_MAX;
     for (int s = 0; s < S; ++s) {
       const im_slot& x = slots[i * S + s];
       if (x.id >= 0) {
         ++busy;
         if (x.rem < 1) return fail(p, IM_ESTATE, "busy slot with rem < 1");
+        if ((int64_t)x.rem + tick - 1 > INT32_MAX) return fail(p, IM_ESTATE, "slot rem too large");
+        busy_mask |= 1 << s;
+        next_done = std::min(next_done, x.rem + tick - 1);
       }
-      sl[i * S + s] = x.id >= 0 ? make_int4(x.id, x.t_arr, x.rem, x.budget) : make_int4(-1, 0, 0, 0);
+      // device slot: {id, t_arr, completion tick, budget}
+      sl[i * S + s] = x.id >= 0 ? make_int4(x.id, x.t_arr, x.rem + tick - 1, x.budget)
+                                : make_int4(-1, 0, 0, 0);
     }
     if (busy != ms.busy) return fail(p, IM_ESTATE, "busy != occupied slots");
     ModelRec& r = recs[i];
     r.qlen = ms.qlen; r.busy = ms.busy; r.ewma = ms.ewma_q8; r.backlog = ms.backlog;
     r.cap = ms.capacity; r.enabled = ms.enabled ? 1 : 0; r.next_id = envs[e].next_id;
     r.t = tick;
+    r.busy_mask = busy_mask;
+    r.next_done = next_done;
     r.fh = 0;
     r.fn = std::min(ms.qlen, im::kFront);
     r.P = ms.qlen - r.fn;

@@ -44,7 +44,7 @@ __device__ __forceinline__ int32_t comp_id(int64_t c) { return (int32_t)(uint32_
 __device__ __forceinline__ void wave_mem_sync() { __threadfence_block(); }
 
 struct Queue {       // wave-uniform view of one (env, model) record
-  int32_t qlen, busy, ewma, backlog, cap, enabled, fh, fn, P, next_id;
+  int32_t qlen, busy, ewma, backlog, cap, enabled, fh, fn, P, busy_mask, next_done;
 };
 
 // Merge `lim` newcomers into the front held in registers (`fe`, lane i <
@@ -227,6 +227,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
   __shared__ int4 stage[4][kStageChunks * 64];
   __shared__ int32_t hist_lds[4][IM_MAX_ACTIONS];
   __shared__ int32_t svc_lds[4][IM_MAX_MODELS];
+  __shared__ int32_t acc_lds[4][IM_MAX_MODELS];
   __shared__ int64_t pend_k[4][kFront];   // refill candidate staging
   __shared__ int32_t pend_i[4][kFront];
   __shared__ int2 pend_kb[4][4 * kFront];
@@ -237,8 +238,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
   int4* st = stage[wv];
   int32_t* hist_s = hist_lds[wv];
   int32_t* svc_s = svc_lds[wv];
+  int32_t* acc_s = acc_lds[wv];
   hist_s[lane] = 0;                     // IM_MAX_ACTIONS == 64 lanes
-  if (lane < IM_MAX_MODELS) svc_s[lane] = 0;
+  if (lane < IM_MAX_MODELS) { svc_s[lane] = 0; acc_s[lane] = 0; }
   const int M = a.M, K = a.K;
 
   // ---- validate the env's input; an invalid env is skipped this tick ----
@@ -269,12 +271,28 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     }
   }
   ModelRec* recs = a.ms + (size_t)e * M;
-  // The tick lives in device memory (one copy per record of the env), so a
-  // captured sequence of ticks replays with the right time.
+  // The tick and the next request id live in the env's first record in
+  // device memory, so a captured sequence of ticks replays with the right time.
   const int32_t t = recs[0].t;
   if (bad) {
-    if (lane == 0) atomicOr(a.err, bad);
-    if (lane < M) recs[lane].t = t + 1;   // the env's state is untouched; time still advances
+    // The env's state is untouched and time still advances: busy slots keep
+    // their remaining service, so their completion ticks move one tick later.
+    if (lane == 0) {
+      atomicOr(a.err, bad);
+      recs[0].t = t + 1;
+    }
+    for (int m = 0; m < M; ++m) {
+      if (recs[m].busy_mask == 0) continue;
+      int4* sl = a.slots + (size_t)(e * M + m) * a.S;
+      if (lane < a.S) {
+        int4 v = sl[lane];
+        if (v.x >= 0) {
+          v.z += 1;
+          sl[lane] = v;
+        }
+      }
+      if (lane == 0) recs[m].next_done += 1;
+    }
     return;
   }
 
@@ -318,7 +336,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
       const bool acc = in && mdl >= 0 && rank < room;
       const int32_t d = ac - mdl * K;
       const int32_t svc = sv * (d + 1);
-      if (acc) atomicAdd(&svc_s[mdl], svc);          // service time admitted per model
+      if (acc) {                                     // admitted count and service time per model
+        atomicAdd(&acc_s[mdl], 1);
+        atomicAdd(&svc_s[mdl], svc);
+      }
       const int32_t key = a.key_mode == IM_KEY_DEADLINE ? t + bu
                           : (a.key_mode == IM_KEY_FCFS ? t : t + bu - svc);
       // sort key: model (63 for rejected rows) | key biased to unsigned | lane
@@ -333,78 +354,78 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     const bool last = r == rounds - 1;
 
     // ---- per model: insert its sorted segments, serve, write back ----
-    // The record and front of model m+1 are fetched while model m is processed.
-    auto load_rec = [&](int mm, Queue& qq) {
-      const ModelRec* r = recs + mm;
-      qq.qlen = r->qlen; qq.busy = r->busy; qq.ewma = r->ewma; qq.backlog = r->backlog;
-      qq.cap = r->cap; qq.enabled = r->enabled; qq.fh = r->fh; qq.fn = r->fn;
-      qq.P = r->P; qq.next_id = r->next_id;
-    };
-    // The whole front array is read without waiting for the record (the load
-    // is independent of fh); the live window [fh, fh + fn) is then rotated to
-    // lanes [0, fn) with lane shuffles.
-    auto load_front = [&](int mm, const Queue& qq) -> int4 {
-      const int4 all = a.front[((size_t)e * M + mm) * kFront + lane];
-      const int src = (qq.fh + lane) & 63;
-      int4 v;
-      v.x = shfl((int32_t)all.x, src);
-      v.y = shfl((int32_t)all.y, src);
-      v.z = shfl((int32_t)all.z, src);
-      v.w = shfl((int32_t)all.w, src);
-      return lane < qq.fn ? v : make_int4(0, 0, 0, 0);
-    };
+    // A model with no newcomers, no free slot to fill and no completion due
+    // this tick is settled from its record alone: nothing is loaded or written.
     for (int m = 0; m < M; ++m) {
       const int em = e * M + m;
       ModelRec* rec = recs + m;
       Queue q;
-      load_rec(m, q);
+      q.qlen = rec->qlen; q.busy = rec->busy; q.ewma = rec->ewma; q.backlog = rec->backlog;
+      q.cap = rec->cap; q.enabled = rec->enabled; q.fh = rec->fh; q.fn = rec->fn;
+      q.P = rec->P; q.busy_mask = rec->busy_mask; q.next_done = rec->next_done;
+      const Queue q0 = q;
       int4* front = a.front + (size_t)em * kFront;
       int4* pool = a.pool + (size_t)em * a.qcap;
-      int4 fe = load_front(m, q);
-      int fe_base = q.fh;     // fe lane i mirrors front[fe_base + i]
-      int4 sl = make_int4(-1, 0, 0, 0);
-      int64_t* cnt = a.cnt + (size_t)em * C_NUM;
-      if (last && lane < a.S) sl = a.slots[(size_t)em * a.S + lane];
-      int32_t added = 0;
-      bool dirty = false;   // the front in registers differs from the front array
-      for (int c = 0; c < nch; ++c) {
-        const int4 en = st[c * 64 + lane];
-        const bool mine = en.w == m;
-        const int k = popc64(ballot(mine));
-        if (k == 0) continue;
-        const int seg_lo = popc64(ballot(en.w < m));
-        const int o = lane - seg_lo;   // offset in the model's sorted segment
-        // newcomers merged into the front: those below its largest key, or
-        // all of them while the pool is empty (the front then holds the queue)
-        int lim;
-        if (q.P == 0) {
-          lim = k;
-        } else if (q.fn == 0) {
-          lim = 0;
-        } else {
-          const int64_t fmax = readlane64(composite(fe.x, fe.y), q.fn - 1);
-          lim = popc64(ballot(mine && composite(en.x, en.y) < fmax));
-        }
-        if (mine && o >= lim) pool[q.P + o - lim] = make_int4(en.x, en.y, t, en.z);
-        q.P += k - lim;
-        if (lim > 0) {
-          merge_front(q, fe, st + c * 64 + seg_lo, lim, t, pool);
-          fe_base = 0;
-          dirty = true;
-        }
-        added += k;
-      }
+      const int32_t k_tot = acc_s[m];        // newcomers admitted this round
       const int32_t svc_in = svc_s[m];
-      if (lane == 0) svc_s[m] = 0;          // LDS accesses of one wave stay in order
-      q.qlen += added;
-      q.backlog += svc_in;
-      if (lane == m) acc_l += added;
+      if (lane == 0) { acc_s[m] = 0; svc_s[m] = 0; }   // LDS accesses of one wave stay in order
+      // The front is read only when it is needed; the live window
+      // [fh, fh + fn) is rotated to lanes [0, fn) with lane shuffles.
+      bool have_front = false;
+      int4 fe = make_int4(0, 0, 0, 0);
+      int fe_base = 0;                       // fe lane i mirrors front[fe_base + i]
+      auto get_front = [&]() {
+        const int4 all = front[lane];
+        const int src = (q.fh + lane) & 63;
+        fe.x = shfl((int32_t)all.x, src);
+        fe.y = shfl((int32_t)all.y, src);
+        fe.z = shfl((int32_t)all.z, src);
+        fe.w = shfl((int32_t)all.w, src);
+        if (lane >= q.fn) fe = make_int4(0, 0, 0, 0);
+        fe_base = q.fh;
+        have_front = true;
+      };
+      bool dirty = false;   // the front in registers differs from the front array
+      if (k_tot > 0) {
+        get_front();
+        for (int c = 0; c < nch; ++c) {
+          const int4 en = st[c * 64 + lane];
+          const bool mine = en.w == m;
+          const int k = popc64(ballot(mine));
+          if (k == 0) continue;
+          const int seg_lo = popc64(ballot(en.w < m));
+          const int o = lane - seg_lo;   // offset in the model's sorted segment
+          // newcomers merged into the front: those below its largest key, or
+          // all of them while the pool is empty (the front then holds the queue)
+          int lim;
+          if (q.P == 0) {
+            lim = k;
+          } else if (q.fn == 0) {
+            lim = 0;
+          } else {
+            const int64_t fmax = readlane64(composite(fe.x, fe.y), q.fn - 1);
+            lim = popc64(ballot(mine && composite(en.x, en.y) < fmax));
+          }
+          if (mine && o >= lim) pool[q.P + o - lim] = make_int4(en.x, en.y, t, en.z);
+          q.P += k - lim;
+          if (lim > 0) {
+            merge_front(q, fe, st + c * 64 + seg_lo, lim, t, pool);
+            fe_base = 0;
+            dirty = true;
+          }
+        }
+        q.qlen += k_tot;
+        q.backlog += svc_in;
+        if (lane == m) acc_l += k_tot;
+      }
       if (!last) {
-        if (dirty && lane >= q.fh - fe_base && lane < q.fh - fe_base + q.fn)
-          front[fe_base + lane] = fe;   // the live window [fh, fh + fn)
-        if (lane == 0) {
-          rec->qlen = q.qlen; rec->backlog = q.backlog;
-          rec->fh = q.fh; rec->fn = q.fn; rec->P = q.P;
+        if (k_tot > 0) {
+          if (dirty && lane >= q.fh - fe_base && lane < q.fh - fe_base + q.fn)
+            front[fe_base + lane] = fe;   // the live window [fh, fh + fn)
+          if (lane == 0) {
+            rec->qlen = q.qlen; rec->backlog = q.backlog;
+            rec->fh = q.fh; rec->fn = q.fn; rec->P = q.P;
+          }
         }
         if (m == M - 1) wave_mem_sync();   // the next round re-reads these records
         continue;
@@ -412,104 +433,129 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
 
       // ---- service: fill free slots below c_m from the queue head ----
       const int capc = q.cap < a.S ? q.cap : a.S;
-      uint64_t empty = ballot(lane < capc && sl.x < 0);
-      int32_t started = 0;
-      int32_t wait_add = 0, svc_out = 0;
-      while (empty != 0 && q.qlen > 0) {
-        if (q.fn == 0) {
-          refill(q, fe, pool, pend_k[wv], pend_i[wv], pend_kb[wv]);
-          fe_base = 0;
-          dirty = true;
+      const uint32_t free_m = ~(uint32_t)q.busy_mask & ((1u << capc) - 1u);
+      const bool pops = free_m != 0 && q.qlen > 0;
+      const bool due = q.busy_mask != 0 && q.next_done <= t;
+      int32_t started = 0, wait_add = 0, svc_out = 0;
+      int32_t completed = 0, slo_add = 0, lat_add = 0;
+      if (pops || due) {
+        // slot: {id, t_arr, tick of completion, budget}; id -1 = empty
+        int4 sl = lane < a.S ? a.slots[(size_t)em * a.S + lane] : make_int4(-1, 0, 0, 0);
+        if (pops) {
+          if (!have_front) get_front();
+          uint64_t empty = (uint64_t)free_m;
+          while (empty != 0 && q.qlen > 0) {
+            if (q.fn == 0) {
+              refill(q, fe, pool, pend_k[wv], pend_i[wv], pend_kb[wv]);
+              fe_base = 0;
+              dirty = true;
+            }
+            if (q.fn == 0) break;   // unreachable while qlen == fn + P holds; never spin
+            const int need = popc64(empty);
+            const int take = need < q.fn ? need : q.fn;
+            const int rnk = prefix_count(empty);
+            const bool mine_slot = ((empty >> lane) & 1ull) && rnk < take;
+            int4 en;
+            const int src = (q.fh - fe_base + rnk) & 63;
+            en.x = shfl((int32_t)fe.x, src);
+            en.y = shfl((int32_t)fe.y, src);
+            en.z = shfl((int32_t)fe.z, src);
+            en.w = shfl((int32_t)fe.w, src);
+            const int32_t svc = en.w & 0xffff;
+            if (mine_slot) sl = make_int4(en.y, en.z, t + svc - 1, (int32_t)((uint32_t)en.w >> 16));
+            uint64_t popped = ballot(mine_slot);
+            empty &= ~popped;
+            while (popped) {                       // at most max_slots lanes
+              const int sp = __builtin_ctzll(popped);
+              popped &= popped - 1;
+              wait_add += t - __builtin_amdgcn_readlane(en.z, sp);
+              svc_out += __builtin_amdgcn_readlane(svc, sp);
+            }
+            q.fh += take;
+            q.fn -= take;
+            q.qlen -= take;
+            started += take;
+          }
+          q.backlog -= svc_out;
         }
-        if (q.fn == 0) break;   // unreachable while qlen == fn + P holds; never spin
-        const int need = popc64(empty);
-        const int take = need < q.fn ? need : q.fn;
-        const int rnk = prefix_count(empty);
-        const bool mine_slot = ((empty >> lane) & 1ull) && rnk < take;
-        int4 en;
-        const int src = (q.fh - fe_base + rnk) & 63;
-        en.x = shfl((int32_t)fe.x, src);
-        en.y = shfl((int32_t)fe.y, src);
-        en.z = shfl((int32_t)fe.z, src);
-        en.w = shfl((int32_t)fe.w, src);
-        if (mine_slot) {
-          const int32_t svc = en.w & 0xffff;
-          const int32_t bu = (int32_t)((uint32_t)en.w >> 16);
-          sl = make_int4(en.y, en.z, svc, bu);
+        // ---- one tick of service; completions in slot order ----
+        const bool busy_slot = lane < a.S && sl.x >= 0;
+        const bool done = busy_slot && sl.z <= t;   // == t in every valid state
+        const uint64_t done_mask = ballot(done);
+        const int32_t lat = t - sl.y + 1;
+        uint64_t dm = done_mask;
+        int32_t ewma = q.ewma;
+        while (dm) {
+          const int s = __builtin_ctzll(dm);
+          dm &= dm - 1;
+          const int32_t ls = __builtin_amdgcn_readlane(lat, s);
+          lat_add += ls;
+          const int64_t delta = (int64_t)ls * 256 - ewma;
+          const int64_t stepv = delta >= 0 ? (delta >> 3) : -((-delta + 7) >> 3);
+          ewma = (int32_t)(ewma + stepv);
         }
-        uint64_t popped = ballot(mine_slot);
-        empty &= ~popped;
-        while (popped) {                       // at most max_slots lanes
-          const int sp = __builtin_ctzll(popped);
-          popped &= popped - 1;
-          wait_add += t - __builtin_amdgcn_readlane(sl.y, sp);
-          svc_out += __builtin_amdgcn_readlane(sl.z, sp);
-        }
-        q.fh += take;
-        q.fn -= take;
-        q.qlen -= take;
-        started += take;
+        completed = popc64(done_mask);
+        slo_add = popc64(ballot(done && lat <= sl.w));
+        if (done) sl = make_int4(-1, 0, 0, 0);
+        const uint64_t bm = ballot(lane < a.S && sl.x >= 0);
+        q.busy = popc64(bm);
+        q.busy_mask = (int32_t)(uint32_t)bm;
+        q.ewma = ewma;
+        // earliest completion tick among the busy slots (min over 8 lanes)
+        int32_t nd = (lane < a.S && sl.x >= 0) ? sl.z : 0x7fffffff;
+        nd = min(nd, xshfl<1>(nd));
+        nd = min(nd, xshfl<2>(nd));
+        nd = min(nd, xshfl<4>(nd));
+        q.next_done = __builtin_amdgcn_readlane(nd, 0);
+        if (lane < a.S) a.slots[(size_t)em * a.S + lane] = sl;
       }
-      q.backlog -= svc_out;
 
-      // ---- one tick of service; completions in slot order ----
-      const bool busy_slot = lane < a.S && sl.x >= 0;
-      if (busy_slot) sl.z -= 1;
-      const bool done = busy_slot && sl.z == 0;
-      const uint64_t done_mask = ballot(done);
-      const int32_t lat = t - sl.y + 1;
-      uint64_t dm = done_mask;
-      int32_t ewma = q.ewma;
-      int32_t lat_add = 0;
-      while (dm) {
-        const int s = __builtin_ctzll(dm);
-        dm &= dm - 1;
-        const int32_t ls = __builtin_amdgcn_readlane(lat, s);
-        lat_add += ls;
-        const int64_t delta = (int64_t)ls * 256 - ewma;
-        const int64_t stepv = delta >= 0 ? (delta >> 3) : -((-delta + 7) >> 3);
-        ewma = (int32_t)(ewma + stepv);
-      }
-      const int32_t completed = popc64(done_mask);
-      const int32_t slo_add = popc64(ballot(done && lat <= sl.w));
-      if (done) sl = make_int4(-1, 0, 0, 0);
-      q.busy = popc64(ballot(lane < a.S && sl.x >= 0));
-      q.ewma = ewma;
-      q.next_id += n;
-
-      // ---- write back ----
+      // ---- write back what changed ----
       if (dirty && lane >= q.fh - fe_base && lane < q.fh - fe_base + q.fn)
-          front[fe_base + lane] = fe;   // the live window [fh, fh + fn)
-      if (lane < a.S) a.slots[(size_t)em * a.S + lane] = sl;
-      if (lane == 0) {
+        front[fe_base + lane] = fe;   // the live window [fh, fh + fn)
+      const bool stats = q.qlen != q0.qlen || q.busy != q0.busy || q.ewma != q0.ewma ||
+                         q.backlog != q0.backlog;
+      if (lane == 0 && (stats || q.fh != q0.fh || q.fn != q0.fn || q.P != q0.P ||
+                        q.busy_mask != q0.busy_mask || q.next_done != q0.next_done)) {
         rec->qlen = q.qlen; rec->busy = q.busy; rec->ewma = q.ewma; rec->backlog = q.backlog;
-        rec->fh = q.fh; rec->fn = q.fn; rec->P = q.P; rec->next_id = q.next_id;
-        rec->t = t + 1;
+        rec->fh = q.fh; rec->fn = q.fn; rec->P = q.P;
+        rec->busy_mask = q.busy_mask; rec->next_done = q.next_done;
       }
       const int32_t routed_m = __builtin_amdgcn_readlane(prior_l, m);
       const int32_t acc_m = __builtin_amdgcn_readlane(acc_l, m);
-      if (lane < C_NUM - 1) {
-        int64_t add = 0;
-        switch (lane) {
-          case C_REJ_OVERFLOW: add = routed_m - acc_m; break;
-          case C_ENQUEUED: add = acc_m; break;
-          case C_STARTED: add = started; break;
-          case C_COMPLETED: add = completed; break;
-          case C_SLO_MET: add = slo_add; break;
-          case C_LAT_SUM: add = lat_add; break;
-          default: add = wait_add; break;
+      if (routed_m != 0 || started != 0 || completed != 0) {
+        int64_t* cnt = a.cnt + (size_t)em * C_NUM;
+        if (lane < C_NUM - 1) {
+          int64_t add = 0;
+          switch (lane) {
+            case C_REJ_OVERFLOW: add = routed_m - acc_m; break;
+            case C_ENQUEUED: add = acc_m; break;
+            case C_STARTED: add = started; break;
+            case C_COMPLETED: add = completed; break;
+            case C_SLO_MET: add = slo_add; break;
+            case C_LAT_SUM: add = lat_add; break;
+            default: add = wait_add; break;
+          }
+          if (add != 0) cnt[lane] += add;
         }
-        cnt[lane] += add;
       }
       // Snapshot row for the next tick's route step.
-      if (lane < 5) write_snap_part(a, e, m, lane, q.qlen, q.busy, q.ewma, q.backlog, q.cap, q.enabled);
+      if (stats && lane < 5)
+        write_snap_part(a, e, m, lane, q.qlen, q.busy, q.ewma, q.backlog, q.cap, q.enabled);
     }
   }
   if (lane == 0) {
-    a.env_cnt[(size_t)e * 2] += n;
-    a.env_cnt[(size_t)e * 2 + 1] += nomodel;
+    recs[0].t = t + 1;
+    if (n > 0) {
+      recs[0].next_id = next_id + n;
+      a.env_cnt[(size_t)e * 2] += n;
+      a.env_cnt[(size_t)e * 2 + 1] += nomodel;
+    }
   }
-  if (lane < a.A) hist_p[lane] += hist_s[lane];
+  if (n > 0 && lane < a.A) {
+    const int32_t h = hist_s[lane];
+    if (h != 0) hist_p[lane] += h;
+  }
 }
 
 }  // namespace
