@@ -50,6 +50,7 @@ struct RouteArgs {
   const int32_t* q_idx;
   const int16_t* budget;
   int32_t n_total;
+  float envs_per_row;                 // E / n_total: first guess of a row's env
   int32_t E, M, K, A;
   int32_t embed_dim, feat_dim, k1;    // k1: layer-1 K steps (bf16: 16-wide, f32: 2-wide)
   int32_t qcap;

@@ -290,6 +290,7 @@ static im::RouteArgs route_args(im_pool* p, const im_arrivals* arr, int32_t* act
   a.q_idx = arr->q_idx;
   a.budget = arr->budget;
   a.n_total = arr->n_total;
+  a.envs_per_row = arr->n_total > 0 ? (float)((double)p->d.n_envs / arr->n_total) : 0.f;
   a.E = p->d.n_envs;
   a.M = p->d.n_models;
   a.K = p->d.n_depths;

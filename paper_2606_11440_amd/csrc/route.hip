@@ -56,18 +56,68 @@ __device__ __forceinline__ uint64_t action_mask(const RouteArgs& a, int e) {
   return am;
 }
 
-__device__ __forceinline__ RowCtx row_setup(const RouteArgs& a, int32_t r) {
+// Env of rows r[] (per lane) for a wave whose rows lie in [rfirst, rlast]:
+// one coalesced load of a 64-entry window of offsets around an interpolated
+// guess; a uniform binary search when the guess misses.
+__device__ __forceinline__ int32_t find_env_bsearch(const RouteArgs& a, int32_t r) {
+  int lo = 0, hi = a.E;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (a.offsets[mid] <= r) lo = mid; else hi = mid - 1;
+  }
+  return lo < a.E ? lo : a.E - 1;
+}
+
+template <int NR>
+__device__ __forceinline__ void find_envs(const RouteArgs& a, int32_t rfirst, int32_t rlast,
+                                          const int32_t (&r)[NR], int32_t (&e)[NR]) {
+  const int lane = lane_id();
+  int32_t e_lo = (int32_t)((float)rfirst * a.envs_per_row) - 16;
+  e_lo = e_lo < 0 ? 0 : (e_lo > a.E - 1 ? a.E - 1 : e_lo);
+  int32_t wi = e_lo + lane;
+  int32_t ow = a.offsets[wi < a.E ? wi : a.E];
+  bool ok = __builtin_amdgcn_readfirstlane(ow) <= rfirst &&
+            rlast < __builtin_amdgcn_readlane(ow, 63);
+  if (!ok) {
+    e_lo = find_env_bsearch(a, rfirst);
+    wi = e_lo + lane;
+    ow = a.offsets[wi < a.E ? wi : a.E];
+    ok = rlast < __builtin_amdgcn_readlane(ow, 63);
+  }
+  if (ok) {
+    // The window's offsets are ascending. The env of row x is e_lo - 1 plus
+    // the number of window offsets <= x: those <= rfirst (one ballot), plus
+    // the env boundaries inside the wave's rows (rfirst, rlast], few per wave.
+    const int base = e_lo - 1 + popc64(ballot(ow <= rfirst));
+#pragma unroll
+    for (int j = 0; j < NR; ++j) e[j] = base;
+    uint64_t bnd = ballot(ow > rfirst && ow <= rlast);
+    while (bnd) {
+      const int b = __builtin_ctzll(bnd);
+      bnd &= bnd - 1;
+      const int32_t ob = __builtin_amdgcn_readlane(ow, b);
+#pragma unroll
+      for (int j = 0; j < NR; ++j) e[j] += ob <= r[j] ? 1 : 0;
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < NR; ++j) e[j] = find_env_bsearch(a, r[j] < a.n_total ? r[j] : a.n_total - 1);
+  }
+#pragma unroll
+  for (int j = 0; j < NR; ++j) e[j] = e[j] < 0 ? 0 : (e[j] > a.E - 1 ? a.E - 1 : e[j]);
+}
+
+// Row context of row r (per lane) in a wave whose rows lie in [row0, row0 + 31].
+__device__ __forceinline__ RowCtx row_setup(const RouteArgs& a, int32_t row0, int32_t r) {
   RowCtx c;
   c.r = r;
   c.live = r < a.n_total;
   const int32_t rr = c.live ? r : a.n_total - 1;
-  // env: the largest e in [0, E] with offsets[e] <= rr
-  int lo = 0, hi = a.E;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (a.offsets[mid] <= rr) lo = mid; else hi = mid - 1;
-  }
-  c.e = lo < a.E ? lo : a.E - 1;
+  const int32_t rl = row0 + 31 < a.n_total ? row0 + 31 : a.n_total - 1;
+  const int32_t rows[1] = {rr};
+  int32_t env[1];
+  find_envs<1>(a, row0, rl, rows, env);
+  c.e = env[0];
   const int32_t q = a.q_idx[rr];
   c.bad_q = q < 0 || (int64_t)q >= a.Q;
   c.q = c.bad_q ? 0 : q;
@@ -257,7 +307,7 @@ __global__ __launch_bounds__(256) void route_bf16(RouteArgs a) {
   const int n = lane & 31, g = lane >> 5;
   const int32_t row0 = (int32_t)(blockIdx.x * 4 + wave) * 32;
   if (row0 >= a.n_total) return;
-  const RowCtx c = row_setup(a, row0 + n);
+  const RowCtx c = row_setup(a, row0, row0 + n);
   constexpr int TH = H / 32;        // hidden tiles
   constexpr int KH = H / 16;        // K blocks over a hidden layer
   const u32x4* W1 = (const u32x4*)a.W[0];
@@ -323,7 +373,7 @@ __global__ __launch_bounds__(256) void route_f32(RouteArgs a) {
   const int n = lane & 31, g = lane >> 5;
   const int32_t row0 = (int32_t)(blockIdx.x * 4 + wave) * 32;
   if (row0 >= a.n_total) return;
-  const RowCtx c = row_setup(a, row0 + n);
+  const RowCtx c = row_setup(a, row0, row0 + n);
   constexpr int TH = H / 32;
   constexpr int KH = H / 2;         // 2-wide K steps over a hidden layer
   const float* W1 = (const float*)a.W[0];
@@ -396,49 +446,6 @@ __global__ __launch_bounds__(256) void route_f32(RouteArgs a) {
 // fragment read from LDS feeds two MFMAs. Layer outputs are produced in chunks
 // of 128 features; each hidden chunk is rounded to bf16 fragments right away.
 // ---------------------------------------------------------------------------
-
-// Env of rows r (two per lane) for a wave whose rows lie in [rfirst, rlast]:
-// one coalesced load of a 64-entry window of offsets around an interpolated
-// guess; a uniform binary search when the guess misses.
-__device__ __forceinline__ int32_t find_env_bsearch(const RouteArgs& a, int32_t r) {
-  int lo = 0, hi = a.E;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (a.offsets[mid] <= r) lo = mid; else hi = mid - 1;
-  }
-  return lo < a.E ? lo : a.E - 1;
-}
-
-template <int NR>
-__device__ __forceinline__ void find_envs(const RouteArgs& a, int32_t rfirst, int32_t rlast,
-                                          const int32_t (&r)[NR], int32_t (&e)[NR]) {
-  const int lane = lane_id();
-  const int64_t guess = (int64_t)rfirst * a.E / a.n_total;
-  int32_t e_lo = (int32_t)guess - 16;
-  e_lo = e_lo < 0 ? 0 : (e_lo > a.E - 1 ? a.E - 1 : e_lo);
-  int32_t wi = e_lo + lane;
-  int32_t ow = a.offsets[wi < a.E ? wi : a.E];
-  bool ok = shfl(ow, 0) <= rfirst && rlast < shfl(ow, 63);
-  if (!ok) {
-    e_lo = find_env_bsearch(a, rfirst);
-    wi = e_lo + lane;
-    ow = a.offsets[wi < a.E ? wi : a.E];
-    ok = rlast < shfl(ow, 63);
-  }
-#pragma unroll
-  for (int j = 0; j < NR; ++j) {
-    int pos = 0;
-#pragma unroll
-    for (int step = 64; step >= 1; step >>= 1) {
-      const int probe = pos + step - 1;
-      const int32_t v = shfl(ow, probe < 64 ? probe : 63);
-      if (probe < 64 && v <= r[j]) pos += step;
-    }
-    int32_t ej = e_lo + pos - 1;
-    if (!ok && pos == 64) ej = find_env_bsearch(a, r[j]);
-    e[j] = ej < 0 ? 0 : (ej > a.E - 1 ? a.E - 1 : ej);
-  }
-}
 
 __device__ __forceinline__ RowCtx row_setup_env(const RouteArgs& a, int32_t r, int32_t e) {
   RowCtx c;
