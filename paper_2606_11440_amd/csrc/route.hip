@@ -612,6 +612,157 @@ __global__ __launch_bounds__(NW * 64, 1) void route_bf16_lds(RouteArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Streaming variant for wide three-layer policies whose weights do not fit in
+// LDS (c3: 193 -> 512 -> 512 -> 64, 784 KB in bf16).
+//
+// A block of NW waves routes NW x 32 rows per step; each wave keeps its
+// rows' whole first hidden layer in registers as bf16 B fragments. The
+// weights pass through a double-buffered LDS ring in stages: two layer-1
+// output tiles, or one layer-2 output tile together with the layer-3
+// fragments that consume it (layer-2 outputs are never stored). The next
+// stage is brought in by the LDS DMA path (global_load_lds, no registers)
+// while the current one is multiplied; one barrier per stage.
+// ---------------------------------------------------------------------------
+
+// One 1 KB fragment (64 lanes x 16 B) from global memory into LDS; `dst` is
+// wave-uniform, lane l's 16 bytes land at dst + 16 l.
+__device__ __forceinline__ void dma_frag(u32x4* dst, const u32x4* src, int lane) {
+  __builtin_amdgcn_global_load_lds((const void*)(src + lane),
+                                   (__attribute__((address_space(3))) void*)dst, 16, 0, 0);
+}
+
+template <int H, int AT, int KB1, int ED, int NW>
+__global__ __launch_bounds__(NW * 64, 1) void route_bf16_stream(RouteArgs a) {
+  constexpr int TH = H / 32, KH = H / 16;
+  constexpr int S1 = TH / 2;                  // layer-1 stages (two output tiles each)
+  constexpr int NST = S1 + TH;                // stages per block step
+  constexpr int F1 = 2 * KB1;                 // fragments of a layer-1 stage
+  constexpr int F2 = KH + 2 * AT;             // fragments of a layer-2 stage
+  constexpr int FS = F1 > F2 ? F1 : F2;
+  constexpr int NB0 = TH * 32, NB1 = TH * 32, NB2 = AT * 32;
+  constexpr int ROWS = NW * 32;
+  static_assert(NST % 2 == 0, "stage parity must repeat every block step");
+  static_assert(KH % NW == 0 && 2 * AT <= NW, "layer-2 stage split over the waves");
+  __shared__ u32x4 ring[2][FS * 64];
+  __shared__ float lbias[NB0 + NB1 + NB2];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int g = lane >> 5;
+  const u32x4* W1 = (const u32x4*)a.W[0];
+  const u32x4* W2 = (const u32x4*)a.W[1];
+  const u32x4* W3 = (const u32x4*)a.W[2];
+  // Fragments of stage st into ring buffer b: wave wv copies fragments
+  // wv, wv + NW, ...; a wave with fewer fragments than the others copies the
+  // stage's last one again (the same bytes to the same place), so the code
+  // has no branches.
+  auto issue = [&](int st, int b, int wv, int ln) {
+    u32x4* dst = ring[b];
+    if (st < S1) {
+#pragma unroll
+      for (int i = 0; i < (F1 + NW - 1) / NW; ++i) {
+        const int f = min(wv + NW * i, F1 - 1);
+        dma_frag(dst + f * 64, W1 + (st * F1 + f) * 64, ln);
+      }
+    } else {
+      const int j = st - S1;
+#pragma unroll
+      for (int i = 0; i < KH / NW; ++i) {
+        const int f = wv + NW * i;
+        dma_frag(dst + f * 64, W2 + (j * KH + f) * 64, ln);
+      }
+      const int f3 = min(wv, 2 * AT - 1);   // layer-3 fragment (To, 2 j + d) with f3 = 2 To + d
+      dma_frag(dst + (KH + f3) * 64, W3 + ((f3 >> 1) * KH + 2 * j + (f3 & 1)) * 64, ln);
+    }
+  };
+  for (int i = threadIdx.x; i < NB0 + NB1 + NB2; i += NW * 64)
+    lbias[i] = i < NB0 ? a.bias[0][i] : (i < NB0 + NB1 ? a.bias[1][i - NB0] : a.bias[2][i - NB0 - NB1]);
+  issue(0, 0, __builtin_amdgcn_readfirstlane(wave), lane);
+  const int n_tiles = (a.n_total + ROWS - 1) / ROWS;
+  for (int tile = blockIdx.x; tile < n_tiles; tile += gridDim.x) {
+    // Per-iteration copies of the lane and wave indices: the fragment and
+    // bias addresses derived from them are recomputed in each block step
+    // instead of being hoisted out of the loop and kept live across it.
+    asm volatile("" ::: "memory");
+    int ln = lane, gg = g;
+    int wv = __builtin_amdgcn_readfirstlane(wave);
+    asm volatile("" : "+v"(ln), "+v"(gg));
+    asm volatile("" : "+s"(wv));
+    const int32_t r0 = tile * ROWS + wv * 32;
+    const int32_t rf = r0 < a.n_total ? r0 : a.n_total - 1;   // waves past the end idle on a clamped row
+    const int32_t rl = r0 + 31 < a.n_total ? r0 + 31 : a.n_total - 1;
+    const int32_t rows[1] = {r0 + (ln & 31)};
+    int32_t envs[1];
+    find_envs<1>(a, rf, rl, rows, envs);
+    const RowCtx c = row_setup_env(a, rows[0], envs[0]);
+    u32x4 x[KB1];
+    gather_row<ED, 0, KB1>(a, c, gg, x);
+    u32x4 h[KH];
+    f32x16 z[AT];
+#pragma unroll
+    for (int s = 0; s < NST; ++s) {
+      // stage s is in ring[s & 1]; every wave is done with ring[(s + 1) & 1]
+      __builtin_amdgcn_s_waitcnt(0);
+      __syncthreads();
+      {
+        // the DMA source addresses are formed here, not hoisted to the step's start
+        int lns = ln;
+        asm volatile("" : "+v"(lns));
+        issue(s + 1 < NST ? s + 1 : 0, (s + 1) & 1, wv, lns);
+      }
+      const u32x4* wb = ring[s & 1];
+      if (s < S1) {
+        // fragment q = t * KB1 + kb, two LDS reads ahead of its MFMA
+        u32x4 w_0 = wb[0 * 64 + ln];
+        u32x4 w_1 = wb[1 * 64 + ln];
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+          const int T = 2 * s + t;
+          f32x16 p = *(const f32x16*)(lbias + (T * 2 + gg) * 16);
+#pragma unroll
+          for (int kb = 0; kb < KB1; ++kb) {
+            const int q = t * KB1 + kb;
+            const u32x4 w_2 = wb[(q + 2 < F1 ? q + 2 : F1 - 1) * 64 + ln];
+            p = mfma_bf16(w_0, x[kb], p);
+            w_0 = w_1;
+            w_1 = w_2;
+            __builtin_amdgcn_sched_barrier(0);
+          }
+          relu_to_frags(p, h[2 * T], h[2 * T + 1]);
+        }
+        if (s == S1 - 1) {
+#pragma unroll
+          for (int To = 0; To < AT; ++To) z[To] = *(const f32x16*)(lbias + NB0 + NB1 + (To * 2 + gg) * 16);
+        }
+      } else {
+        const int j = s - S1;
+        f32x16 p = *(const f32x16*)(lbias + NB0 + (j * 2 + gg) * 16);
+        u32x4 w_0 = wb[0 * 64 + ln];
+        u32x4 w_1 = wb[1 * 64 + ln];
+#pragma unroll
+        for (int kb = 0; kb < KH; ++kb) {
+          const u32x4 w_2 = wb[(kb + 2 < F2 ? kb + 2 : F2 - 1) * 64 + ln];
+          p = mfma_bf16(w_0, h[kb], p);
+          w_0 = w_1;
+          w_1 = w_2;
+          __builtin_amdgcn_sched_barrier(0);
+        }
+        u32x4 f0, f1;
+        relu_to_frags(p, f0, f1);
+        // w_0, w_1 now hold fragments KH and KH + 1 (layer 3, To = 0)
+#pragma unroll
+        for (int To = 0; To < AT; ++To) {
+          const u32x4 wa = To == 0 ? w_0 : wb[(KH + 2 * To) * 64 + ln];
+          const u32x4 wc = To == 0 ? w_1 : wb[(KH + 2 * To + 1) * 64 + ln];
+          z[To] = mfma_bf16(wa, f0, z[To]);
+          z[To] = mfma_bf16(wc, f1, z[To]);
+        }
+      }
+    }
+    epilogue<AT>(a, c, z, nullptr, gg);
+  }
+  __builtin_amdgcn_s_waitcnt(0);   // the prefetched first stage of a step that does not exist
+}
+
 typedef void (*RouteKernel)(RouteArgs);
 
 template <int H, int NL>
@@ -647,6 +798,16 @@ constexpr int kLdsRows = 1;
 
 // Persistent LDS-resident variants for the shapes that fit (bytes of packed
 // weights in LDS <= 160 KiB): returns nullptr when none applies.
+constexpr int kStreamWaves = 8;
+
+// Streaming kernels: kStreamWaves waves per block, 32 rows per wave.
+RouteKernel pick_stream(int dtype, int hidden, int n_layers, int out_tiles, int k1, int ed) {
+  if (dtype != IM_BF16) return nullptr;
+  if (hidden == 512 && n_layers == 3 && out_tiles == 2 && k1 == 13 && ed == 128)
+    return route_bf16_stream<512, 2, 13, 128, kStreamWaves>;
+  return nullptr;
+}
+
 RouteKernel pick_lds(int dtype, int hidden, int n_layers, int out_tiles, int k1, int ed) {
   if (dtype != IM_BF16) return nullptr;
   if (hidden == 256 && n_layers == 3 && out_tiles == 1 && k1 == 6 && ed == 64)
@@ -675,6 +836,16 @@ hipError_t launch_route(const RouteArgs& a, int dtype, int hidden, int n_layers,
       const int n_tiles = (a.n_total + rows - 1) / rows;
       const unsigned blocks = (unsigned)(n_tiles < a.persistent_blocks ? n_tiles : a.persistent_blocks);
       hipLaunchKernelGGL(kl, dim3(blocks), dim3(kLdsWaves * 64), 0, s, a);
+      return hipGetLastError();
+    }
+  }
+  if (a.persistent_blocks > 0) {
+    RouteKernel ks = pick_stream(dtype, hidden, n_layers, out_tiles, a.k1, a.embed_dim);
+    if (ks) {
+      const int rows = kStreamWaves * 32;
+      const int n_tiles = (a.n_total + rows - 1) / rows;
+      const unsigned blocks = (unsigned)(n_tiles < a.persistent_blocks ? n_tiles : a.persistent_blocks);
+      hipLaunchKernelGGL(ks, dim3(blocks), dim3(kStreamWaves * 64), 0, s, a);
       return hipGetLastError();
     }
   }
