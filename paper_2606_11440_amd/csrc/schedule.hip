@@ -304,6 +304,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
   int32_t prior_l = 0;      // lane m: requests routed to model m so far (id order)
   int32_t acc_l = 0;        // lane m: requests accepted by model m so far
   int32_t nomodel = 0;
+  // lane m: model m's load statistics after the tick, its capacity and
+  // enable flag (for the snapshot row written once at the end)
+  int32_t st_q = 0, st_b = 0, st_w = 0, st_k = 0, st_c = 0, st_en = 0;
+  if (lane < M) {
+    st_q = recs[lane].qlen; st_b = recs[lane].busy; st_w = recs[lane].ewma; st_k = recs[lane].backlog;
+    st_c = recs[lane].cap; st_en = recs[lane].enabled;
+  }
+  bool snap_dirty = false;
   const int n_chunks = (n + 63) / 64;
   const int rounds = n_chunks > 0 ? (n_chunks + kStageChunks - 1) / kStageChunks : 1;
 
@@ -353,6 +361,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     }
     const bool last = r == rounds - 1;
 
+    // lane m: newcomers admitted by model m this round and their service time
+    const int32_t acc_round_l = lane < IM_MAX_MODELS ? acc_s[lane] : 0;
+    const int32_t svc_round_l = lane < IM_MAX_MODELS ? svc_s[lane] : 0;
+    if (lane < IM_MAX_MODELS) { acc_s[lane] = 0; svc_s[lane] = 0; }   // LDS accesses of one wave stay in order
+
     // ---- per model: insert its sorted segments, serve, write back ----
     // A model with no newcomers, no free slot to fill and no completion due
     // this tick is settled from its record alone: nothing is loaded or written.
@@ -366,9 +379,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
       const Queue q0 = q;
       int4* front = a.front + (size_t)em * kFront;
       int4* pool = a.pool + (size_t)em * a.qcap;
-      const int32_t k_tot = acc_s[m];        // newcomers admitted this round
-      const int32_t svc_in = svc_s[m];
-      if (lane == 0) { acc_s[m] = 0; svc_s[m] = 0; }   // LDS accesses of one wave stay in order
+      const int32_t k_tot = __builtin_amdgcn_readlane(acc_round_l, m);   // newcomers admitted this round
+      const int32_t svc_in = __builtin_amdgcn_readlane(svc_round_l, m);
       // The front is read only when it is needed; the live window
       // [fh, fh + fn) is rotated to lanes [0, fn) with lane shuffles.
       bool have_front = false;
@@ -539,9 +551,34 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
           if (add != 0) cnt[lane] += add;
         }
       }
-      // Snapshot row for the next tick's route step.
-      if (stats && lane < 5)
-        write_snap_part(a, e, m, lane, q.qlen, q.busy, q.ewma, q.backlog, q.cap, q.enabled);
+      if (lane == m) { st_q = q.qlen; st_b = q.busy; st_w = q.ewma; st_k = q.backlog; }
+      snap_dirty |= stats;
+    }
+  }
+  // Snapshot row for the next tick's route step: lane i < 4M writes
+  // statistic i / M of model i % M, lanes m < M the validity bytes.
+  if (snap_dirty) {
+    float* row = a.snap + (size_t)e * snap_stride(M);
+    for (int i0 = 0; i0 < 4 * M; i0 += 64) {
+      const int i = i0 + lane;
+      const int sidx = i / M, mm = i - sidx * M;
+      const int32_t vq = shfl(st_q, mm), vb = shfl(st_b, mm), vw = shfl(st_w, mm), vk = shfl(st_k, mm);
+      const int32_t cm = shfl(st_c, mm);
+      const int c = cm < 0 ? 0 : (cm > IM_MAX_SLOTS ? IM_MAX_SLOTS : cm);
+      if (i < 4 * M) {
+        float v;
+        switch (sidx) {
+          case 0: v = (float)vq * a.inv_qcap; break;
+          case 1: v = (float)vb * a.inv_tab[c]; break;
+          case 2: v = (float)vw * a.inv_lat; break;
+          default: v = (float)vk * a.inv_tab[IM_MAX_SLOTS + 1 + c]; break;
+        }
+        row[i] = v;
+      }
+    }
+    if (lane < M) {
+      uint8_t* vb8 = (uint8_t*)(row + snap_valid_offset(M));
+      vb8[lane] = (st_en != 0 && st_c > 0 && st_q < a.qcap) ? 1 : 0;
     }
   }
   if (lane == 0) {

@@ -108,8 +108,12 @@ __device__ __forceinline__ void cmpx(int64_t& k, int32_t (&p)[NP], bool ascendin
   int32_t pp[NP];
 #pragma unroll
   for (int i = 0; i < NP; ++i) pp[i] = xshfl<S>(p[i]);
-  const bool low = (lane_id() & S) == 0;
-  const bool take = (low == ascending) ? (pk < k) : (pk > k);
+  // The lane takes its partner's key when that is the smaller one (low end
+  // of an ascending pair) or the larger one (otherwise). For distinct keys
+  // "larger" is "not smaller"; equal keys only occur as padding, whose
+  // payloads are never used, so one compare and a flip suffice.
+  const bool flip = ((lane_id() & S) != 0) == ascending;
+  const bool take = (pk < k) != flip;
   // selects, not a branch: the whole network stays straight-line code
   k = take ? pk : k;
 #pragma unroll
