@@ -40,6 +40,16 @@ __device__ __forceinline__ int64_t composite(int32_t key, int32_t id) {
 __device__ __forceinline__ int32_t comp_key(int64_t c) { return (int32_t)(c >> 32); }
 __device__ __forceinline__ int32_t comp_id(int64_t c) { return (int32_t)(uint32_t)c; }
 
+// Arrival tick of a queue entry from its key and packed (svc | budget << 16):
+// the key is t_arr + budget - svc (slack), t_arr + budget (deadline) or t_arr
+// (arrival order), so the arrival tick never has to travel with the entry
+// through a sort network.
+__device__ __forceinline__ int32_t t_arr_of(int32_t key, int32_t svcbud, int key_mode) {
+  const uint32_t svc = (uint32_t)svcbud & 0xffffu, bud = (uint32_t)svcbud >> 16;
+  const uint32_t k = (uint32_t)key;
+  return (int32_t)(key_mode == IM_KEY_DEADLINE ? k - bud : (key_mode == IM_KEY_FCFS ? k : k - bud + svc));
+}
+
 // Makes this wave's earlier global stores visible to its later loads.
 __device__ __forceinline__ void wave_mem_sync() { __threadfence_block(); }
 
@@ -50,45 +60,51 @@ struct Queue {       // wave-uniform view of one (env, model) record
 // Merge `lim` newcomers into the front held in registers (`fe`, lane i <
 // q.fn), all of them below the front's largest key or the pool empty. `seg`
 // is the model's sorted segment of a staged chunk in LDS (entries (key, id,
-// svc | budget << 16, model)); newcomers arrive at tick t. The front followed
+// svc | budget << 16, model)). Only the key and the packed service/budget word
+// pass through the network; arrival ticks are recovered from them. The front followed
 // by the reversed newcomers is a bitonic sequence of 128; its half-cleaner
 // leaves the 64 smallest in `lo` (bitonic, sorted by one merge network) and
 // the rest in `hi`, whose real entries spill to the pool.
 __device__ __forceinline__ void merge_front(Queue& q, int4& fe, const int4* seg, int lim,
-                                            int32_t t, int4* pool) {
+                                            int key_mode, int4* pool) {
   const int lane = lane_id();
   const int r = 63 - lane;
   int64_t kb = kKeyMax;
-  int32_t pb[2] = {0, 0};
+  int32_t pb = 0;
   if (r < lim) {
     const int4 v = seg[r];
     kb = composite(v.x, v.y);
-    pb[0] = t;
-    pb[1] = v.z;
+    pb = v.z;
   }
   const int64_t ka = lane < q.fn ? composite(fe.x, fe.y) : kKeyMax;
   const bool sw = kb < ka;
   int64_t klo = sw ? kb : ka;
   const int64_t khi = sw ? ka : kb;
-  int32_t plo[2] = {sw ? pb[0] : fe.z, sw ? pb[1] : fe.w};
-  const int32_t phi0 = sw ? fe.z : pb[0], phi1 = sw ? fe.w : pb[1];
-  bitonic_merge64<2>(klo, plo);
+  int32_t plo[1] = {sw ? pb : fe.w};
+  const int32_t phi = sw ? fe.w : pb;
+  bitonic_merge64<1>(klo, plo);
   const int total = q.fn + lim;
   const int keep = total < kFront ? total : kFront;
   const bool spill = khi != kKeyMax;
   const uint64_t sm = ballot(spill);
-  if (spill) pool[q.P + prefix_count(sm)] = make_int4(comp_key(khi), comp_id(khi), phi0, phi1);
+  if (spill) {
+    const int32_t kk = comp_key(khi);
+    pool[q.P + prefix_count(sm)] = make_int4(kk, comp_id(khi), t_arr_of(kk, phi, key_mode), phi);
+  }
   q.P += total - keep;
   q.fh = 0;
   q.fn = keep;
-  fe = lane < keep ? make_int4(comp_key(klo), comp_id(klo), plo[0], plo[1]) : make_int4(0, 0, 0, 0);
+  const int32_t kl = comp_key(klo);
+  fe = lane < keep ? make_int4(kl, comp_id(klo), t_arr_of(kl, plo[0], key_mode), plo[0])
+                   : make_int4(0, 0, 0, 0);
 }
 
 // Refill the (empty) front with the min(64, P) smallest pool entries; the new
 // front is returned in `fe` (lane i: entry i), the front array is not written.
 // `pk`/`pi` are this wave's LDS staging rows (64 keys, 64 pool indices), `kb`
-// its LDS buffer for 4 chunks of pool keys.
-__device__ void refill(Queue& q, int4& fe, int4* pool, int64_t* pk, int32_t* pi, int2* kb) {
+// its LDS buffer for 8 chunks of pool keys.
+__device__ void refill(Queue& q, int4& fe, int4* pool, int64_t* pk, int32_t* pi, int2* kb,
+                       int key_mode) {
   const int lane = lane_id();
   const int P = q.P;
   wave_mem_sync();   // this tick's pool appends are read below
@@ -96,9 +112,11 @@ __device__ void refill(Queue& q, int4& fe, int4* pool, int64_t* pk, int32_t* pi,
     int4 e = make_int4(0, 0, 0, 0);
     int64_t ck = kKeyMax;
     if (lane < P) { e = pool[lane]; ck = composite(e.x, e.y); }
-    int32_t pay[2] = {e.z, e.w};
-    bitonic_sort64<2>(ck, pay);
-    fe = lane < P ? make_int4(comp_key(ck), comp_id(ck), pay[0], pay[1]) : make_int4(0, 0, 0, 0);
+    int32_t pay[1] = {e.w};
+    bitonic_sort64<1>(ck, pay);
+    const int32_t kk = comp_key(ck);
+    fe = lane < P ? make_int4(kk, comp_id(ck), t_arr_of(kk, pay[0], key_mode), pay[0])
+                  : make_int4(0, 0, 0, 0);
     q.fh = 0;
     q.fn = P;
     q.P = 0;
@@ -126,7 +144,7 @@ __device__ void refill(Queue& q, int4& fe, int4* pool, int64_t* pk, int32_t* pi,
     thr = readlane64(ck, 63);
     np = 0;
   };
-  constexpr int G = 4;   // pool chunks whose loads are in flight together
+  constexpr int G = 8;   // pool chunks whose loads are in flight together
   const int2* keys = reinterpret_cast<const int2*>(pool);   // (key, id) of entry i at keys[2 i]
   for (int c0 = kFront; c0 < P; c0 += G * kFront) {
     int2 kv[G];
@@ -217,12 +235,33 @@ __device__ __forceinline__ int32_t wave_sum32(int32_t v) {
 
 constexpr int kStageChunks = 4;   // arrival chunks (of 64) staged in LDS per round
 
-// One wave per env. The env's arrivals are validated once; then, 64 at a time,
-// they are partitioned by model (ballot + mbcnt ranks in id order give the
-// tail-drop admission) and sorted once by (model, key, id) with a 64-lane
-// bitonic network, so each model's newcomers form one sorted segment (a
-// segmented sort). The sorted chunks are staged in LDS; each model then
-// merges its segments into its queue, serves its slots and writes back.
+// Per-model state of the env, one model per lane (lane m: model m) in
+// registers for the whole tick; read wave-uniformly with readlane.
+struct LaneState {
+  int32_t qlen, busy, ewma, backlog, cap, enabled, fh, fn, P, busy_mask, next_done;
+};
+
+__device__ __forceinline__ int32_t rl(int32_t v, int m) { return __builtin_amdgcn_readlane(v, m); }
+
+// Inputs of one model fetched ahead of its turn: the live front window
+// (lane i: front[fh + i]), its slots (lane s < S) and counters (lane c).
+struct ModelIn {
+  int4 front;
+  int4 slot;
+  int64_t cnt;
+};
+
+// One wave per env. Every load that does not depend on the arrivals (the
+// model records, one per lane) is issued with the offsets; the env's arrivals
+// are then loaded once (the first kStageChunks chunks stay in registers) and
+// validated. 64 at a time, they are partitioned by model (ballot + mbcnt
+// ranks in id order give the tail-drop admission) and sorted once by (model,
+// key, id) with a 64-lane bitonic network, so each model's newcomers form one
+// sorted segment (a segmented sort), staged in LDS. The models are then
+// processed in order with the next model's front, slots and counters already
+// in flight: merge its segments into the queue, serve its slots, write back.
+// Record, counter, histogram and snapshot updates are plain stores of values
+// held in registers (no read-modify-write round trips).
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void schedule_kernel(SchedArgs a) {
   __shared__ int4 stage[4][kStageChunks * 64];
   __shared__ int32_t hist_lds[4][IM_MAX_ACTIONS];
@@ -230,7 +269,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
   __shared__ int32_t acc_lds[4][IM_MAX_MODELS];
   __shared__ int64_t pend_k[4][kFront];   // refill candidate staging
   __shared__ int32_t pend_i[4][kFront];
-  __shared__ int2 pend_kb[4][4 * kFront];
+  __shared__ int2 pend_kb[4][8 * kFront];
   const int lane = threadIdx.x & 63;
   const int wv = threadIdx.x >> 6;
   const int e = (int)blockIdx.x * 4 + wv;
@@ -239,41 +278,74 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
   int32_t* hist_s = hist_lds[wv];
   int32_t* svc_s = svc_lds[wv];
   int32_t* acc_s = acc_lds[wv];
-  hist_s[lane] = 0;                     // IM_MAX_ACTIONS == 64 lanes
-  if (lane < IM_MAX_MODELS) { svc_s[lane] = 0; acc_s[lane] = 0; }
-  const int M = a.M, K = a.K;
+  const int M = a.M, K = a.K, S = a.S;
+  ModelRec* recs = a.ms + (size_t)e * M;
 
-  // ---- validate the env's input; an invalid env is skipped this tick ----
+  // ---- model records (lane m: model m), issued before anything else ----
+  int4 r0 = make_int4(0, 0, 0, 0), r1 = r0, r2 = r0, r3 = r0;
+  if (lane < M) {
+    const int4* rp = reinterpret_cast<const int4*>(recs + lane);
+    r0 = rp[0];
+    r1 = rp[1];
+    r2 = rp[2];
+    r3 = rp[3];
+  }
   const int32_t lo = a.offsets[e], hi = a.offsets[e + 1];
   int32_t bad = 0;
   if (lo < 0 || hi < lo || hi > a.n_total || hi - lo > a.max_arrivals) bad = IM_ERR_COUNT;
-  int32_t ac0 = -1, bu0 = 0, sv0 = 0;   // first chunk stays in registers
-  if (!bad) {
-    for (int32_t base = lo; base < hi; base += 64) {
-      const int32_t i = base + lane;
-      int32_t b = 0;
-      if (i < hi) {
-        const int32_t qi = a.q_idx[i];
-        const int32_t bu = a.budget[i];
-        const int32_t sv = a.base_svc[i];
-        const int32_t ac = a.actions[i];
-        if (qi < 0 || (int64_t)qi >= a.Q) b |= IM_ERR_QIDX;
-        if (bu < 1) b |= IM_ERR_BUDGET;
-        if (sv < 1 || sv > IM_SVC_MAX) b |= IM_ERR_SVC;
-        if (ac < -1 || ac >= a.A) b |= IM_ERR_ACTION;
-        if (base == lo) { ac0 = ac; bu0 = bu; sv0 = sv; }
-      }
-      // wave-wide OR of the five error bits, one ballot each
-      if (ballot(b & IM_ERR_QIDX)) bad |= IM_ERR_QIDX;
-      if (ballot(b & IM_ERR_BUDGET)) bad |= IM_ERR_BUDGET;
-      if (ballot(b & IM_ERR_SVC)) bad |= IM_ERR_SVC;
-      if (ballot(b & IM_ERR_ACTION)) bad |= IM_ERR_ACTION;
+  const int32_t n = bad ? 0 : hi - lo;
+
+  // ---- the env's arrivals: loaded once, validated; the first chunks kept ----
+  constexpr int kKeep = 2;                            // chunks kept in registers
+  int32_t c_ac[kKeep], c_bs[kKeep];                   // action; budget << 16 | base_svc (16 bits each)
+#pragma unroll
+  for (int c = 0; c < kKeep; ++c) {
+    c_ac[c] = -1;
+    c_bs[c] = 0;
+  }
+  int32_t berr = 0;
+  auto check = [&](int32_t i, int32_t& ac, int32_t& bs) {
+    const int32_t qi = a.q_idx[i];
+    const int32_t bu = a.budget[i];
+    const int32_t sv = a.base_svc[i];
+    ac = a.actions[i];
+    if (qi < 0 || (int64_t)qi >= a.Q) berr |= IM_ERR_QIDX;
+    if (bu < 1) berr |= IM_ERR_BUDGET;
+    if (sv < 1 || sv > IM_SVC_MAX) berr |= IM_ERR_SVC;
+    if (ac < -1 || ac >= a.A) berr |= IM_ERR_ACTION;
+    bs = (int32_t)(((uint32_t)bu << 16) | ((uint32_t)sv & 0xffffu));
+  };
+#pragma unroll
+  for (int c = 0; c < kKeep; ++c) {
+    if (c * 64 < n) {
+      const int32_t i = lo + c * 64 + lane;
+      if (i < hi) check(i, c_ac[c], c_bs[c]);
     }
   }
-  ModelRec* recs = a.ms + (size_t)e * M;
+  for (int32_t base = lo + kKeep * 64; base < lo + n; base += 64) {
+    const int32_t i = base + lane;
+    int32_t ac, bs;
+    if (i < hi) check(i, ac, bs);
+  }
+  if (n > 0) {
+    // wave-wide OR of the error bits, one ballot each
+    if (ballot(berr & IM_ERR_QIDX)) bad |= IM_ERR_QIDX;
+    if (ballot(berr & IM_ERR_BUDGET)) bad |= IM_ERR_BUDGET;
+    if (ballot(berr & IM_ERR_SVC)) bad |= IM_ERR_SVC;
+    if (ballot(berr & IM_ERR_ACTION)) bad |= IM_ERR_ACTION;
+  }
+
+  LaneState L;
+  L.qlen = r0.x; L.busy = r0.y; L.ewma = r0.z; L.backlog = r0.w;
+  L.cap = r1.x; L.enabled = r1.y; L.fh = r1.z; L.fn = r1.w;
+  L.P = r2.x; L.busy_mask = r2.w; L.next_done = r3.x;
   // The tick and the next request id live in the env's first record in
   // device memory, so a captured sequence of ticks replays with the right time.
-  const int32_t t = recs[0].t;
+  const int32_t next_id = rl(r2.y, 0);
+  const int32_t t = rl(r2.z, 0);
+  // lane m: which parts of model m's record changed (bit 0: load statistics,
+  // 1: front window, 2: pool size or busy slots, 3: next completion tick)
+  int32_t chg = 0;
   if (bad) {
     // The env's state is untouched and time still advances: busy slots keep
     // their remaining service, so their completion ticks move one tick later.
@@ -282,36 +354,27 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
       recs[0].t = t + 1;
     }
     for (int m = 0; m < M; ++m) {
-      if (recs[m].busy_mask == 0) continue;
-      int4* sl = a.slots + (size_t)(e * M + m) * a.S;
-      if (lane < a.S) {
+      if (rl(L.busy_mask, m) == 0) continue;
+      int4* sl = a.slots + (size_t)(e * M + m) * S;
+      if (lane < S) {
         int4 v = sl[lane];
         if (v.x >= 0) {
           v.z += 1;
           sl[lane] = v;
         }
       }
-      if (lane == 0) recs[m].next_done += 1;
     }
+    if (lane < M && L.busy_mask != 0) recs[lane].next_done = L.next_done + 1;
     return;
   }
 
-  const int32_t n = hi - lo;
+  hist_s[lane] = 0;                     // IM_MAX_ACTIONS == 64 lanes
+  if (lane < IM_MAX_MODELS) { svc_s[lane] = 0; acc_s[lane] = 0; }
   // lane m < M: room left in model m's queue at the snapshot
-  const int32_t room_l = lane < M ? a.qcap - recs[lane].qlen : 0;
-  const int32_t next_id = recs[0].next_id;
-  int64_t* hist_p = a.hist + (size_t)e * a.A;
+  const int32_t room_l = lane < M ? a.qcap - L.qlen : 0;
   int32_t prior_l = 0;      // lane m: requests routed to model m so far (id order)
   int32_t acc_l = 0;        // lane m: requests accepted by model m so far
   int32_t nomodel = 0;
-  // lane m: model m's load statistics after the tick, its capacity and
-  // enable flag (for the snapshot row written once at the end)
-  int32_t st_q = 0, st_b = 0, st_w = 0, st_k = 0, st_c = 0, st_en = 0;
-  if (lane < M) {
-    st_q = recs[lane].qlen; st_b = recs[lane].busy; st_w = recs[lane].ewma; st_k = recs[lane].backlog;
-    st_c = recs[lane].cap; st_en = recs[lane].enabled;
-  }
-  bool snap_dirty = false;
   const int n_chunks = (n + 63) / 64;
   const int rounds = n_chunks > 0 ? (n_chunks + kStageChunks - 1) / kStageChunks : 1;
 
@@ -319,16 +382,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     const int c0 = r * kStageChunks;
     const int nch = n_chunks - c0 < kStageChunks ? n_chunks - c0 : kStageChunks;
     // ---- partition, admission and one sort per chunk ----
-    for (int c = 0; c < nch; ++c) {
+#pragma unroll
+    for (int c = 0; c < kStageChunks; ++c) {
+      if (c >= nch) break;
       const int32_t base = lo + (c0 + c) * 64;
       const int32_t i = base + lane;
       const bool in = i < hi;
-      int32_t ac = ac0, bu = bu0, sv = sv0;
-      if (c0 + c != 0) {
+      int32_t ac = c < kKeep ? c_ac[c < kKeep ? c : 0] : -1;
+      int32_t bs = c < kKeep ? c_bs[c < kKeep ? c : 0] : 0;
+      if (r != 0 || c >= kKeep) {
         ac = in ? a.actions[i] : -1;
-        bu = in ? a.budget[i] : 0;
-        sv = in ? a.base_svc[i] : 0;
+        bs = in ? (int32_t)(((uint32_t)a.budget[i] << 16) | ((uint32_t)a.base_svc[i] & 0xffffu)) : 0;
       }
+      const int32_t bu = bs >> 16, sv = bs & 0xffff;
       const int32_t mdl = ac >= 0 ? ac / K : -1;
       nomodel += popc64(ballot(in && ac < 0));
       if (in && ac >= 0) atomicAdd(&hist_s[ac], 1);   // routed requests per action
@@ -336,7 +402,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
       for (int m = 0; m < M; ++m) {
         const uint64_t bal = ballot(in && mdl == m);
         if (bal == 0) continue;
-        const int32_t pm = __builtin_amdgcn_readlane(prior_l, m);
+        const int32_t pm = rl(prior_l, m);
         if (mdl == m) rank = pm + prefix_count(bal);
         if (lane == m) prior_l += popc64(bal);
       }
@@ -348,16 +414,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         atomicAdd(&acc_s[mdl], 1);
         atomicAdd(&svc_s[mdl], svc);
       }
-      const int32_t key = a.key_mode == IM_KEY_DEADLINE ? t + bu
-                          : (a.key_mode == IM_KEY_FCFS ? t : t + bu - svc);
-      // sort key: model (63 for rejected rows) | key biased to unsigned | lane
-      int64_t sk = (int64_t)(((uint64_t)(acc ? mdl : 63) << 38) |
-                             ((uint64_t)((uint32_t)key ^ 0x80000000u) << 6) | (uint64_t)lane);
-      int32_t pay[1] = {(int32_t)((uint32_t)svc | ((uint32_t)bu << 16))};
-      bitonic_sort64<1>(sk, pay);
-      const int32_t skey = (int32_t)((uint32_t)((uint64_t)sk >> 6) ^ 0x80000000u);
-      const int32_t sid = next_id + (base - lo) + (int32_t)(sk & 63);
-      st[c * 64 + lane] = make_int4(skey, sid, pay[0], (int32_t)((uint64_t)sk >> 38));
+      // Sort key (32 bits): model (63 for rows not admitted) | key - t biased by
+      // 2^16 | lane. Every row of the chunk arrives at t, so ordering by key - t
+      // is ordering by key; with budget in [1, 32767] and svc in [1, 65520],
+      // key - t lies in [-65519, 32766] (17 bits once biased). The lane keeps
+      // ties in id order and locates the row's packed service/budget word.
+      const int32_t rk = a.key_mode == IM_KEY_DEADLINE ? bu : (a.key_mode == IM_KEY_FCFS ? 0 : bu - svc);
+      uint32_t sk = ((uint32_t)(acc ? mdl : 63) << 23) | (((uint32_t)(rk + 65536) & 0x1ffffu) << 6) |
+                    (uint32_t)lane;
+      const int32_t pay = (int32_t)((uint32_t)svc | ((uint32_t)bu << 16));
+      bitonic_sort64(sk);
+      const int src = (int)(sk & 63u);
+      const int32_t skey = t + (int32_t)((sk >> 6) & 0x1ffffu) - 65536;
+      const int32_t sid = next_id + (base - lo) + src;
+      st[c * 64 + lane] = make_int4(skey, sid, shfl(pay, src), (int32_t)(sk >> 23));
     }
     const bool last = r == rounds - 1;
 
@@ -366,40 +436,56 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     const int32_t svc_round_l = lane < IM_MAX_MODELS ? svc_s[lane] : 0;
     if (lane < IM_MAX_MODELS) { acc_s[lane] = 0; svc_s[lane] = 0; }   // LDS accesses of one wave stay in order
 
-    // ---- per model: insert its sorted segments, serve, write back ----
-    // A model with no newcomers, no free slot to fill and no completion due
-    // this tick is settled from its record alone: nothing is loaded or written.
+    // What each model touches this round (lane m): its front (newcomers to
+    // insert, or slots to fill), its slots (fills or a completion due) and its
+    // counters. A model needing none of them is settled from its registers.
+    const int capc_l = L.cap < S ? (L.cap < 0 ? 0 : L.cap) : S;
+    const uint32_t free_l = ~(uint32_t)L.busy_mask & ((1u << capc_l) - 1u);
+    const bool pops_l = last && free_l != 0 && L.qlen + acc_round_l > 0;
+    const bool due_l = last && L.busy_mask != 0 && L.next_done <= t;
+    const uint64_t need_front = ballot(lane < M && (acc_round_l > 0 || pops_l));
+    const uint64_t need_slots = ballot(lane < M && (pops_l || due_l));
+    const uint64_t need_cnt = ballot(lane < M && last && (prior_l != 0 || pops_l || due_l));
+    auto fetch = [&](int mm, ModelIn& in) {
+      const size_t em = (size_t)e * M + mm;
+      in.front = make_int4(0, 0, 0, 0);
+      in.slot = make_int4(-1, 0, 0, 0);
+      in.cnt = 0;
+      if ((need_front >> mm) & 1ull) {
+        const int fh = rl(L.fh, mm), fn = rl(L.fn, mm);
+        if (lane < fn) in.front = a.front[em * kFront + fh + lane];   // fh + fn <= kFront
+      }
+      if ((need_slots >> mm) & 1ull) {
+        if (lane < S) in.slot = a.slots[em * S + lane];
+      }
+      if ((need_cnt >> mm) & 1ull) {
+        if (lane < C_NUM - 1) in.cnt = a.cnt[em * C_NUM + lane];
+      }
+    };
+    if (r > 0) wave_mem_sync();   // the fronts written in the previous round
+    // ---- per model with work this round, in model order: insert its sorted
+    // segments, serve, write back (the next such model's inputs in flight) ----
+    const uint64_t busy_models = need_front | need_slots | need_cnt;
+    ModelIn nxt;
+    fetch(0, nxt);
     for (int m = 0; m < M; ++m) {
-      const int em = e * M + m;
-      ModelRec* rec = recs + m;
+      const ModelIn cur = nxt;
+      if (m + 1 < M) fetch(m + 1, nxt);
+      if (((busy_models >> m) & 1ull) == 0) continue;   // nothing to insert, serve or count
+      const size_t em = (size_t)e * M + m;
       Queue q;
-      q.qlen = rec->qlen; q.busy = rec->busy; q.ewma = rec->ewma; q.backlog = rec->backlog;
-      q.cap = rec->cap; q.enabled = rec->enabled; q.fh = rec->fh; q.fn = rec->fn;
-      q.P = rec->P; q.busy_mask = rec->busy_mask; q.next_done = rec->next_done;
-      const Queue q0 = q;
-      int4* front = a.front + (size_t)em * kFront;
-      int4* pool = a.pool + (size_t)em * a.qcap;
-      const int32_t k_tot = __builtin_amdgcn_readlane(acc_round_l, m);   // newcomers admitted this round
-      const int32_t svc_in = __builtin_amdgcn_readlane(svc_round_l, m);
-      // The front is read only when it is needed; the live window
-      // [fh, fh + fn) is rotated to lanes [0, fn) with lane shuffles.
-      bool have_front = false;
-      int4 fe = make_int4(0, 0, 0, 0);
-      int fe_base = 0;                       // fe lane i mirrors front[fe_base + i]
-      auto get_front = [&]() {
-        const int4 all = front[lane];
-        const int src = (q.fh + lane) & 63;
-        fe.x = shfl((int32_t)all.x, src);
-        fe.y = shfl((int32_t)all.y, src);
-        fe.z = shfl((int32_t)all.z, src);
-        fe.w = shfl((int32_t)all.w, src);
-        if (lane >= q.fn) fe = make_int4(0, 0, 0, 0);
-        fe_base = q.fh;
-        have_front = true;
-      };
+      q.qlen = rl(L.qlen, m); q.busy = rl(L.busy, m); q.ewma = rl(L.ewma, m);
+      q.backlog = rl(L.backlog, m); q.cap = rl(L.cap, m); q.enabled = rl(L.enabled, m);
+      q.fh = rl(L.fh, m); q.fn = rl(L.fn, m); q.P = rl(L.P, m);
+      q.busy_mask = rl(L.busy_mask, m); q.next_done = rl(L.next_done, m);
+      int4* front = a.front + em * kFront;
+      int4* pool = a.pool + em * a.qcap;
+      const int32_t k_tot = rl(acc_round_l, m);   // newcomers admitted this round
+      const int32_t svc_in = rl(svc_round_l, m);
+      int4 fe = cur.front;                         // lane i mirrors front[fe_base + i]
+      int fe_base = q.fh;
       bool dirty = false;   // the front in registers differs from the front array
       if (k_tot > 0) {
-        get_front();
         for (int c = 0; c < nch; ++c) {
           const int4 en = st[c * 64 + lane];
           const bool mine = en.w == m;
@@ -415,13 +501,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
           } else if (q.fn == 0) {
             lim = 0;
           } else {
+            // merges come before any pop of the tick: the window starts at lane 0
             const int64_t fmax = readlane64(composite(fe.x, fe.y), q.fn - 1);
             lim = popc64(ballot(mine && composite(en.x, en.y) < fmax));
           }
           if (mine && o >= lim) pool[q.P + o - lim] = make_int4(en.x, en.y, t, en.z);
           q.P += k - lim;
           if (lim > 0) {
-            merge_front(q, fe, st + c * 64 + seg_lo, lim, t, pool);
+            merge_front(q, fe, st + c * 64 + seg_lo, lim, a.key_mode, pool);
             fe_base = 0;
             dirty = true;
           }
@@ -431,20 +518,18 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         if (lane == m) acc_l += k_tot;
       }
       if (!last) {
-        if (k_tot > 0) {
-          if (dirty && lane >= q.fh - fe_base && lane < q.fh - fe_base + q.fn)
-            front[fe_base + lane] = fe;   // the live window [fh, fh + fn)
-          if (lane == 0) {
-            rec->qlen = q.qlen; rec->backlog = q.backlog;
-            rec->fh = q.fh; rec->fn = q.fn; rec->P = q.P;
-          }
+        if (dirty && lane >= q.fh - fe_base && lane < q.fh - fe_base + q.fn)
+          front[fe_base + lane] = fe;   // the live window [fh, fh + fn)
+        if (lane == m) {
+          chg |= (q.qlen != L.qlen || q.backlog != L.backlog ? 1 : 0) | (q.fh != L.fh || q.fn != L.fn ? 2 : 0) |
+                 (q.P != L.P ? 4 : 0);
+          L.qlen = q.qlen; L.backlog = q.backlog; L.fh = q.fh; L.fn = q.fn; L.P = q.P;
         }
-        if (m == M - 1) wave_mem_sync();   // the next round re-reads these records
         continue;
       }
 
       // ---- service: fill free slots below c_m from the queue head ----
-      const int capc = q.cap < a.S ? q.cap : a.S;
+      const int capc = q.cap < S ? (q.cap < 0 ? 0 : q.cap) : S;
       const uint32_t free_m = ~(uint32_t)q.busy_mask & ((1u << capc) - 1u);
       const bool pops = free_m != 0 && q.qlen > 0;
       const bool due = q.busy_mask != 0 && q.next_done <= t;
@@ -452,13 +537,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
       int32_t completed = 0, slo_add = 0, lat_add = 0;
       if (pops || due) {
         // slot: {id, t_arr, tick of completion, budget}; id -1 = empty
-        int4 sl = lane < a.S ? a.slots[(size_t)em * a.S + lane] : make_int4(-1, 0, 0, 0);
+        int4 sl = cur.slot;
         if (pops) {
-          if (!have_front) get_front();
           uint64_t empty = (uint64_t)free_m;
           while (empty != 0 && q.qlen > 0) {
             if (q.fn == 0) {
-              refill(q, fe, pool, pend_k[wv], pend_i[wv], pend_kb[wv]);
+              refill(q, fe, pool, pend_k[wv], pend_i[wv], pend_kb[wv], a.key_mode);
               fe_base = 0;
               dirty = true;
             }
@@ -480,8 +564,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
             while (popped) {                       // at most max_slots lanes
               const int sp = __builtin_ctzll(popped);
               popped &= popped - 1;
-              wait_add += t - __builtin_amdgcn_readlane(en.z, sp);
-              svc_out += __builtin_amdgcn_readlane(svc, sp);
+              wait_add += t - rl(en.z, sp);
+              svc_out += rl(svc, sp);
             }
             q.fh += take;
             q.fn -= take;
@@ -491,7 +575,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
           q.backlog -= svc_out;
         }
         // ---- one tick of service; completions in slot order ----
-        const bool busy_slot = lane < a.S && sl.x >= 0;
+        const bool busy_slot = lane < S && sl.x >= 0;
         const bool done = busy_slot && sl.z <= t;   // == t in every valid state
         const uint64_t done_mask = ballot(done);
         const int32_t lat = t - sl.y + 1;
@@ -500,7 +584,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         while (dm) {
           const int s = __builtin_ctzll(dm);
           dm &= dm - 1;
-          const int32_t ls = __builtin_amdgcn_readlane(lat, s);
+          const int32_t ls = rl(lat, s);
           lat_add += ls;
           const int64_t delta = (int64_t)ls * 256 - ewma;
           const int64_t stepv = delta >= 0 ? (delta >> 3) : -((-delta + 7) >> 3);
@@ -509,61 +593,72 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         completed = popc64(done_mask);
         slo_add = popc64(ballot(done && lat <= sl.w));
         if (done) sl = make_int4(-1, 0, 0, 0);
-        const uint64_t bm = ballot(lane < a.S && sl.x >= 0);
+        const uint64_t bm = ballot(lane < S && sl.x >= 0);
         q.busy = popc64(bm);
         q.busy_mask = (int32_t)(uint32_t)bm;
         q.ewma = ewma;
         // earliest completion tick among the busy slots (min over 8 lanes)
-        int32_t nd = (lane < a.S && sl.x >= 0) ? sl.z : 0x7fffffff;
+        int32_t nd = (lane < S && sl.x >= 0) ? sl.z : 0x7fffffff;
         nd = min(nd, xshfl<1>(nd));
         nd = min(nd, xshfl<2>(nd));
         nd = min(nd, xshfl<4>(nd));
-        q.next_done = __builtin_amdgcn_readlane(nd, 0);
-        if (lane < a.S) a.slots[(size_t)em * a.S + lane] = sl;
+        q.next_done = rl(nd, 0);
+        if (lane < S) a.slots[em * S + lane] = sl;
       }
 
       // ---- write back what changed ----
       if (dirty && lane >= q.fh - fe_base && lane < q.fh - fe_base + q.fn)
         front[fe_base + lane] = fe;   // the live window [fh, fh + fn)
-      const bool stats = q.qlen != q0.qlen || q.busy != q0.busy || q.ewma != q0.ewma ||
-                         q.backlog != q0.backlog;
-      if (lane == 0 && (stats || q.fh != q0.fh || q.fn != q0.fn || q.P != q0.P ||
-                        q.busy_mask != q0.busy_mask || q.next_done != q0.next_done)) {
-        rec->qlen = q.qlen; rec->busy = q.busy; rec->ewma = q.ewma; rec->backlog = q.backlog;
-        rec->fh = q.fh; rec->fn = q.fn; rec->P = q.P;
-        rec->busy_mask = q.busy_mask; rec->next_done = q.next_done;
-      }
-      const int32_t routed_m = __builtin_amdgcn_readlane(prior_l, m);
-      const int32_t acc_m = __builtin_amdgcn_readlane(acc_l, m);
+      const int32_t routed_m = rl(prior_l, m);
+      const int32_t acc_m = rl(acc_l, m);
       if (routed_m != 0 || started != 0 || completed != 0) {
-        int64_t* cnt = a.cnt + (size_t)em * C_NUM;
-        if (lane < C_NUM - 1) {
-          int64_t add = 0;
-          switch (lane) {
-            case C_REJ_OVERFLOW: add = routed_m - acc_m; break;
-            case C_ENQUEUED: add = acc_m; break;
-            case C_STARTED: add = started; break;
-            case C_COMPLETED: add = completed; break;
-            case C_SLO_MET: add = slo_add; break;
-            case C_LAT_SUM: add = lat_add; break;
-            default: add = wait_add; break;
-          }
-          if (add != 0) cnt[lane] += add;
+        int64_t add = 0;
+        switch (lane) {
+          case C_REJ_OVERFLOW: add = routed_m - acc_m; break;
+          case C_ENQUEUED: add = acc_m; break;
+          case C_STARTED: add = started; break;
+          case C_COMPLETED: add = completed; break;
+          case C_SLO_MET: add = slo_add; break;
+          case C_LAT_SUM: add = lat_add; break;
+          case C_WAIT_SUM: add = wait_add; break;
+          default: break;
         }
+        if (add != 0) a.cnt[em * C_NUM + lane] = cur.cnt + add;
       }
-      if (lane == m) { st_q = q.qlen; st_b = q.busy; st_w = q.ewma; st_k = q.backlog; }
-      snap_dirty |= stats;
+      if (lane == m) {
+        chg |= (q.qlen != L.qlen || q.busy != L.busy || q.ewma != L.ewma || q.backlog != L.backlog ? 1 : 0) |
+               (q.fh != L.fh || q.fn != L.fn ? 2 : 0) | (q.P != L.P || q.busy_mask != L.busy_mask ? 4 : 0) |
+               (q.next_done != L.next_done ? 8 : 0);
+        L.qlen = q.qlen; L.busy = q.busy; L.ewma = q.ewma; L.backlog = q.backlog;
+        L.fh = q.fh; L.fn = q.fn; L.P = q.P; L.busy_mask = q.busy_mask; L.next_done = q.next_done;
+      }
     }
+  }
+
+  // ---- records of the models whose state changed (lane m: model m) ----
+  if (lane < M) {
+    int4* rp = reinterpret_cast<int4*>(recs + lane);
+    if (chg & 1) rp[0] = make_int4(L.qlen, L.busy, L.ewma, L.backlog);
+    if (chg & 2) rp[1] = make_int4(L.cap, L.enabled, L.fh, L.fn);
+    if (lane == 0) {
+      rp[2] = make_int4(L.P, next_id + n, t + 1, L.busy_mask);
+    } else if (chg & 4) {
+      recs[lane].P = L.P;
+      recs[lane].busy_mask = L.busy_mask;
+    }
+    if (chg & 8) recs[lane].next_done = L.next_done;
   }
   // Snapshot row for the next tick's route step: lane i < 4M writes
   // statistic i / M of model i % M, lanes m < M the validity bytes.
+  const bool snap_dirty = ballot(lane < M && (chg & 1)) != 0;
   if (snap_dirty) {
     float* row = a.snap + (size_t)e * snap_stride(M);
     for (int i0 = 0; i0 < 4 * M; i0 += 64) {
       const int i = i0 + lane;
       const int sidx = i / M, mm = i - sidx * M;
-      const int32_t vq = shfl(st_q, mm), vb = shfl(st_b, mm), vw = shfl(st_w, mm), vk = shfl(st_k, mm);
-      const int32_t cm = shfl(st_c, mm);
+      const int32_t vq = shfl(L.qlen, mm), vb = shfl(L.busy, mm), vw = shfl(L.ewma, mm),
+                    vk = shfl(L.backlog, mm);
+      const int32_t cm = shfl(L.cap, mm);
       const int c = cm < 0 ? 0 : (cm > IM_MAX_SLOTS ? IM_MAX_SLOTS : cm);
       if (i < 4 * M) {
         float v;
@@ -578,20 +673,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     }
     if (lane < M) {
       uint8_t* vb8 = (uint8_t*)(row + snap_valid_offset(M));
-      vb8[lane] = (st_en != 0 && st_c > 0 && st_q < a.qcap) ? 1 : 0;
+      vb8[lane] = (L.enabled != 0 && L.cap > 0 && L.qlen < a.qcap) ? 1 : 0;
     }
   }
-  if (lane == 0) {
-    recs[0].t = t + 1;
-    if (n > 0) {
-      recs[0].next_id = next_id + n;
-      a.env_cnt[(size_t)e * 2] += n;
-      a.env_cnt[(size_t)e * 2 + 1] += nomodel;
+  if (n > 0) {
+    int64_t* hist_p = a.hist + (size_t)e * a.A;
+    int64_t* envc_p = a.env_cnt + (size_t)e * 2;
+    if (lane < 2) envc_p[lane] += lane == 0 ? n : nomodel;
+    if (lane < a.A) {
+      const int32_t h = hist_s[lane];
+      if (h != 0) hist_p[lane] += h;
     }
-  }
-  if (n > 0 && lane < a.A) {
-    const int32_t h = hist_s[lane];
-    if (h != 0) hist_p[lane] += h;
   }
 }
 
