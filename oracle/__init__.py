@@ -38,7 +38,7 @@ class _Desc(ctypes.Structure):
                 ("n_layers", ctypes.c_int32), ("widths", ctypes.c_int32 * 4),
                 ("dtype", ctypes.c_int32), ("key_mode", ctypes.c_int32),
                 ("max_arrivals", ctypes.c_int32), ("budget_max", ctypes.c_int32),
-                ("Q", ctypes.c_int64)]
+                ("value_head", ctypes.c_int32), ("Q", ctypes.c_int64)]
 
 
 _lib = None
@@ -68,12 +68,33 @@ def _load():
         L.orc_set_enabled.argtypes = [P, ctypes.c_int, ctypes.c_int, ctypes.c_int]
         L.orc_set_capacity.argtypes = [P, ctypes.c_int, ctypes.c_int, ctypes.c_int]
         L.orc_read_state.argtypes = [P] * 7
+        U32 = ctypes.c_uint32
+        L.orc_route_rl.argtypes = [P, ctypes.c_int, P, P, P, U32, U32, ctypes.c_int, P, P, P, P, P,
+                                   ctypes.c_int]
+        L.orc_philox4x32_10.argtypes = [P, P, P]
+        L.orc_gumbel.argtypes = [U32, U32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int]
+        L.orc_gumbel.restype = ctypes.c_double
         _lib = L
     return _lib
 
 
 def _ptr(a: np.ndarray):
     return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def philox4x32_10(ctr, key) -> np.ndarray:
+    """One Philox4x32-10 block: uint32 [4] from counter uint32 [4], key uint32 [2]."""
+    c = np.ascontiguousarray(ctr, np.uint32)
+    k = np.ascontiguousarray(key, np.uint32)
+    out = np.empty(4, np.uint32)
+    _load().orc_philox4x32_10(_ptr(c), _ptr(k), _ptr(out))
+    return out
+
+
+def gumbel(seed: int, req_id: int, env: int, action: int) -> float:
+    """Gumbel noise the sampler adds to the logit of `action` of request
+    `req_id` of env `env` (global env index) under `seed`."""
+    return _load().orc_gumbel(seed & 0xffffffff, (seed >> 32) & 0xffffffff, req_id, env, action)
 
 
 def round_bf16(v: float) -> float:
@@ -108,6 +129,9 @@ class Oracle:
         d.key_mode = KEY_MODES[cfg["key_mode"]]
         d.max_arrivals = cfg["max_arrivals"]
         d.budget_max = cfg["budget_max"]
+        vh = 1 if cfg.get("value_head") else 0
+        d.value_head = vh
+        d.widths[len(cfg["widths"]) - 1] = cfg["widths"][-1] + vh
         emb = np.ascontiguousarray(emb_values, np.float32)
         d.Q = emb.shape[0]
         self.cfg, self.M, self.K, self.A = cfg, cfg["M"], cfg["K"], cfg["M"] * cfg["K"]
@@ -159,6 +183,22 @@ class Oracle:
         self._lib.orc_route(self.p, _ptr(off), _ptr(q), _ptr(bud),
                             None if lg is None else _ptr(lg), _ptr(act), self.threads)
         return act, lg
+
+    def route_rl(self, arr, seed: int, greedy: bool = False, env_base: int = 0):
+        """RL-rollout route: dict of actions int32 [n], logits, logp, entropy,
+        value (float64). `env_base` is the global index of this oracle's env 0
+        (the Philox counter uses global env indices)."""
+        off, q, bud, _ = self._arr(arr)
+        assert off.size == self.E + 1
+        n = int(q.size)
+        out = dict(actions=np.empty(n, np.int32), logits=np.empty((n, self.A), np.float64),
+                   logp=np.empty(n, np.float64), entropy=np.empty(n, np.float64),
+                   value=np.empty(n, np.float64))
+        self._lib.orc_route_rl(self.p, env_base, _ptr(off), _ptr(q), _ptr(bud),
+                               seed & 0xffffffff, (seed >> 32) & 0xffffffff, int(bool(greedy)),
+                               _ptr(out["logits"]), _ptr(out["actions"]), _ptr(out["logp"]),
+                               _ptr(out["entropy"]), _ptr(out["value"]), self.threads)
+        return out
 
     def schedule(self, arr, actions):
         off, q, bud, svc = self._arr(arr)

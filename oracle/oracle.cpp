@@ -12,7 +12,12 @@
 //     reasoning depth a % K.
 //   Sec. 4.2: a policy network scores every joint action; the build deploys
 //     it greedily (masked argmax) with a plain MLP in place of the
-//     dual-pathway network.
+//     dual-pathway network. For RL rollouts (Sec. 4.4, Eq. 5 consumes
+//     log pi, the entropy and V) the policy pi(a|s) is the softmax of the
+//     logits over the valid actions, sampled with the Gumbel-max trick from
+//     Philox4x32-10 noise (Salmon et al., SC 2011), and an optional value row
+//     V(s) = w_val . h + b_val shares the last hidden layer h (Sec. 4.2
+//     "Decision").
 //   Sec. 4.3: every model's queue is served earliest-deadline-first with the
 //     deadline t_arrive + budget; the default key is the latest start time
 //     (deadline - service time), i.e. the slack.
@@ -109,6 +114,7 @@ struct orc_desc {
   int32_t key_mode;       // 0 slack, 1 deadline, 2 fcfs
   int32_t max_arrivals;
   int32_t budget_max;
+  int32_t value_head;     // 1: the last layer has M*K + 1 rows, row M*K is V(s)
   int64_t Q;
 };
 
@@ -207,6 +213,43 @@ int32_t sort_key(const orc_pool* p, int32_t t, int32_t budget, int32_t svc) {
   }
 }
 
+// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, "Parallel random numbers: as
+// easy as 1, 2, 3", SC 2011): ten rounds of two 32x32->64-bit multiplies by
+// the round multipliers, the high halves xored with the other two counter
+// words and the key; the key is bumped by the Weyl constants between rounds.
+void philox4x32_10(const uint32_t ctr_in[4], const uint32_t key_in[2], uint32_t out[4]) {
+  const uint64_t kMul0 = 0xD2511F53u, kMul1 = 0xCD9E8D57u;
+  const uint32_t kWeyl0 = 0x9E3779B9u, kWeyl1 = 0xBB67AE85u;
+  uint32_t c[4] = {ctr_in[0], ctr_in[1], ctr_in[2], ctr_in[3]};
+  uint32_t k[2] = {key_in[0], key_in[1]};
+  for (int round = 0; round < 10; ++round) {
+    if (round > 0) { k[0] += kWeyl0; k[1] += kWeyl1; }
+    const uint64_t p0 = kMul0 * (uint64_t)c[0];
+    const uint64_t p1 = kMul1 * (uint64_t)c[2];
+    const uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
+    const uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
+    const uint32_t n0 = hi1 ^ c[1] ^ k[0];
+    const uint32_t n2 = hi0 ^ c[3] ^ k[1];
+    c[0] = n0; c[1] = lo1; c[2] = n2; c[3] = lo0;
+  }
+  for (int i = 0; i < 4; ++i) out[i] = c[i];
+}
+
+// Uniform in (0, 1) from a 32-bit word: its top 24 bits plus one half, times
+// 2^-24 (exact in fp32 and fp64, never 0 or 1).
+double uniform24(uint32_t x) { return ((double)(x >> 8) + 0.5) * (1.0 / 16777216.0); }
+
+// Gumbel noise of joint action a of request `id` of env `env`: word a % 4 of
+// the Philox block with counter (id, env, a / 4, 0) and key (seed_lo, seed_hi).
+double gumbel(uint32_t seed_lo, uint32_t seed_hi, int32_t id, int32_t env, int a) {
+  const uint32_t ctr[4] = {(uint32_t)id, (uint32_t)env, (uint32_t)(a / 4), 0u};
+  const uint32_t key[2] = {seed_lo, seed_hi};
+  uint32_t w[4];
+  philox4x32_10(ctr, key, w);
+  const double u = uniform24(w[a % 4]);
+  return -std::log(-std::log(u));
+}
+
 // Route the requests of env e: logits (post-bias, pre-mask) and actions.
 void route_env(orc_pool* p, int e, const int32_t* off, const int32_t* q_idx,
                const int16_t* budget, double* logits, int32_t* actions, int32_t* err) {
@@ -229,6 +272,61 @@ void route_env(orc_pool* p, int e, const int32_t* off, const int32_t* q_idx,
     }
     actions[r] = best;
     if (logits) for (int a = 0; a < p->A; ++a) logits[(size_t)r * p->A + a] = z[a];
+  }
+}
+
+// RL-rollout route of env e (global index env_base + e): besides the logits,
+// the action drawn from pi(.|s) = softmax of the logits over the valid actions
+// (Gumbel-max: argmax over valid a of z_a + G_a, lowest index on ties) or, if
+// greedy, the masked argmax; log pi of that action; the entropy of pi; and
+// the value row. No valid action: action -1, log-prob 0, entropy 0.
+void route_env_rl(orc_pool* p, int e, int env_base, const int32_t* off, const int32_t* q_idx,
+                  const int16_t* budget, uint32_t seed_lo, uint32_t seed_hi, int greedy,
+                  double* logits, int32_t* actions, double* logp, double* entropy,
+                  double* value, int32_t* err) {
+  const EnvState& env = p->envs[e];
+  const int A = p->A;
+  std::vector<double> x, z;
+  for (int32_t r = off[e]; r < off[e + 1]; ++r) {
+    if (q_idx[r] < 0 || (int64_t)q_idx[r] >= p->d.Q) {
+      *err |= ERR_QIDX;
+      actions[r] = -1;
+      logp[r] = 0.0; entropy[r] = 0.0; value[r] = 0.0;
+      if (logits) for (int a = 0; a < A; ++a) logits[(size_t)r * A + a] = 0.0;
+      continue;
+    }
+    features(p, env, q_idx[r], budget[r], x);
+    mlp(p, x, z);
+    value[r] = p->d.value_head ? z[A] : 0.0;
+    if (logits) for (int a = 0; a < A; ++a) logits[(size_t)r * A + a] = z[a];
+    std::vector<int> valid;
+    for (int a = 0; a < A; ++a)
+      if (model_valid(p, env.models[a / p->d.K])) valid.push_back(a);
+    if (valid.empty()) {
+      actions[r] = -1; logp[r] = 0.0; entropy[r] = 0.0;
+      continue;
+    }
+    // log-sum-exp over the valid actions, shifted by their largest logit
+    double zmax = z[valid[0]];
+    for (int a : valid) zmax = std::max(zmax, z[a]);
+    double s = 0.0;
+    for (int a : valid) s += std::exp(z[a] - zmax);
+    const double lse = zmax + std::log(s);
+    double h = 0.0;                         // -sum pi log pi
+    for (int a : valid) {
+      const double lp = z[a] - lse;
+      h -= std::exp(lp) * lp;
+    }
+    const int32_t id = env.next_id + (r - off[e]);
+    int best = -1;
+    double best_score = 0.0;
+    for (int a : valid) {
+      const double sc = greedy ? z[a] : z[a] + gumbel(seed_lo, seed_hi, id, env_base + e, a);
+      if (best < 0 || sc > best_score) { best = a; best_score = sc; }
+    }
+    actions[r] = best;
+    logp[r] = z[best] - lse;
+    entropy[r] = h;
   }
 }
 
@@ -392,6 +490,26 @@ void orc_schedule(orc_pool* p, int32_t n_total, const int32_t* off, const int32_
   });
   for (int32_t x : errs) p->err |= x;
   p->t += 1;
+}
+
+void orc_route_rl(orc_pool* p, int env_base, const int32_t* off, const int32_t* q_idx,
+                  const int16_t* budget, uint32_t seed_lo, uint32_t seed_hi, int greedy,
+                  double* logits, int32_t* actions, double* logp, double* entropy, double* value,
+                  int threads) {
+  std::vector<int32_t> errs(p->d.E, 0);
+  for_envs(p->d.E, threads, [&](int e) {
+    route_env_rl(p, e, env_base, off, q_idx, budget, seed_lo, seed_hi, greedy, logits, actions,
+                 logp, entropy, value, &errs[e]);
+  });
+  for (int32_t x : errs) p->err |= x;
+}
+
+void orc_philox4x32_10(const uint32_t* ctr, const uint32_t* key, uint32_t* out) {
+  philox4x32_10(ctr, key, out);
+}
+
+double orc_gumbel(uint32_t seed_lo, uint32_t seed_hi, int32_t id, int32_t env, int a) {
+  return gumbel(seed_lo, seed_hi, id, env, a);
 }
 
 // Feature vector of a request of env e as the route step builds it.

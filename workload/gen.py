@@ -8,7 +8,8 @@ sharing any part of the method.
 
 Streams: numpy.random.default_rng(SeedSequence([seed, cfg index, stream]))
   0 weights, 1 capacities, 2 embedding table, 3 Poisson counts [T, E],
-  4 request fields, one sub-stream per tick: SeedSequence([seed, idx, 4, t]).
+  4 request fields, one sub-stream per tick: SeedSequence([seed, idx, 4, t]),
+  5 the value-head row (pools with cfg["value_head"]).
 
 Inputs stand in for the paper's workloads (Sec. 5.1): the paper's LLM-quality
 benchmarks are replaced by N(0,1) query embeddings (Sec. 3 uses Sentence-BERT
@@ -36,7 +37,10 @@ def table_rows(cfg: dict) -> int:
 def weights(cfg: dict, seed: int = 0, bias_scale: float = 0.0):
     """Glorot-uniform fp32 weights [out, in] per layer and fp32 biases.
 
-    Biases are U(-bias_scale, bias_scale) (0 in benchmarks, 0.1 in tests)."""
+    Biases are U(-bias_scale, bias_scale) (0 in benchmarks, 0.1 in tests).
+    With cfg["value_head"], one more row (the value head, its own stream,
+    Glorot-uniform with fan_out 1) is appended to the last layer, so the
+    policy rows are the same with and without it."""
     rng = _rng(cfg, seed, 0)
     Ws, bs = [], []
     fan_in = cfg["feat_dim"]
@@ -48,6 +52,15 @@ def weights(cfg: dict, seed: int = 0, bias_scale: float = 0.0):
         else:
             bs.append(np.zeros(out, np.float32))
         fan_in = out
+    if cfg.get("value_head"):
+        vr = _rng(cfg, seed, 5)
+        h_last = Ws[-1].shape[1]
+        lim = math.sqrt(6.0 / (h_last + 1))
+        w_val = vr.uniform(-lim, lim, size=(1, h_last)).astype(np.float32)
+        b_val = (vr.uniform(-bias_scale, bias_scale, size=1) if bias_scale > 0
+                 else np.zeros(1)).astype(np.float32)
+        Ws[-1] = np.concatenate([Ws[-1], w_val], axis=0)
+        bs[-1] = np.concatenate([bs[-1], b_val])
     return Ws, bs
 
 
