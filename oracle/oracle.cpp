@@ -235,9 +235,9 @@ void philox4x32_10(const uint32_t ctr_in[4], const uint32_t key_in[2], uint32_t 
   for (int i = 0; i < 4; ++i) out[i] = c[i];
 }
 
-// Uniform in (0, 1) from a 32-bit word: its top 24 bits plus one half, times
-// 2^-24 (exact in fp32 and fp64, never 0 or 1).
-double uniform24(uint32_t x) { return ((double)(x >> 8) + 0.5) * (1.0 / 16777216.0); }
+// Uniform in (0, 1) from a 32-bit word: its top 23 bits plus one half, times
+// 2^-23 (exact in fp32 and fp64, never 0 or 1).
+double uniform23(uint32_t x) { return ((double)(x >> 9) + 0.5) * (1.0 / 8388608.0); }
 
 // Gumbel noise of joint action a of request `id` of env `env`: word a % 4 of
 // the Philox block with counter (id, env, a / 4, 0) and key (seed_lo, seed_hi).
@@ -246,7 +246,7 @@ double gumbel(uint32_t seed_lo, uint32_t seed_hi, int32_t id, int32_t env, int a
   const uint32_t key[2] = {seed_lo, seed_hi};
   uint32_t w[4];
   philox4x32_10(ctr, key, w);
-  const double u = uniform24(w[a % 4]);
+  const double u = uniform23(w[a % 4]);
   return -std::log(-std::log(u));
 }
 
