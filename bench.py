@@ -34,8 +34,11 @@ PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 def algorithmic_flops_per_tick(cfg, n_requests):
     """Minimal policy FLOPs of one tick: per request the MLP without the
     per-env load-statistics columns of layer 1, plus once per env those 4M
-    columns (they are shared by every request of the env)."""
-    widths = cfg["widths"]
+    columns (they are shared by every request of the env). A value head adds
+    one more output row of the last layer."""
+    widths = list(cfg["widths"])
+    if cfg.get("value_head"):
+        widths[-1] += 1
     H1 = widths[0]
     per_req = 2 * (cfg["embed_dim"] + 1) * H1
     prev = H1
@@ -145,6 +148,9 @@ def main():
                     help="launch the timed ticks one by one instead of replaying them "
                          "from a captured HIP graph")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--sample", action="store_true",
+                    help="RL-rollout tick: im_route_sample (Gumbel-max sample, log-prob, entropy, "
+                         "value head) then im_schedule with the sampled actions")
     ap.add_argument("--no-peak-probe", action="store_true",
                     help="skip the measured-peak probes (a large bf16 GEMM and a device copy)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
@@ -174,6 +180,8 @@ def main():
     over = {}
     if args.lam is not None:
         over["lam"] = args.lam
+    if args.sample:
+        over["value_head"] = True
     cfg = workload.configs.get(args.config, **over)
     T = cfg["T"]
     W_ = args.warmup
@@ -196,7 +204,18 @@ def main():
     dev = [P.device_arrivals(a) for a in ticks]
     n_req = [int(a["q_idx"].size) for a in ticks]
     acts = torch.empty(max(max(n_req), 1), dtype=torch.int32, device="cuda")
+    f32 = dict(dtype=torch.float32, device="cuda")
+    rl_out = [torch.empty(max(max(n_req), 1), **f32) for _ in range(3)] if args.sample else None
     pool = P.Pool(cfg, W, b, emb_dev, cap, lb)
+
+    def route_step(pl, t, st=None, with_schedule=True):
+        """One tick: im_tick, or im_route_sample + im_schedule (RL rollout)."""
+        if args.sample:
+            pl.route_sample(dev[t], 1000 + t, acts, *rl_out, stream=st)
+            if with_schedule:
+                pl.schedule(dev[t], acts, st)
+        else:
+            pl.tick(dev[t], acts, st)
     torch.cuda.synchronize()
     gen_s = time.perf_counter() - t_gen
 
@@ -204,7 +223,7 @@ def main():
 
     def warm(pl):
         for t in range(W_):
-            pl.tick(dev[t], acts, stream.cuda_stream)
+            route_step(pl, t, stream.cuda_stream)
         torch.cuda.synchronize()
 
     # ---- timed region: K ticks of im_tick, events only at the two ends ----
@@ -217,7 +236,7 @@ def main():
         graph = torch.cuda.CUDAGraph()
         with torch.cuda.graph(graph):
             for k in range(K):
-                pool.tick(dev[W_ + k], acts)
+                route_step(pool, W_ + k)
         torch.cuda.synchronize()
     start = torch.cuda.Event(enable_timing=True)
     end = torch.cuda.Event(enable_timing=True)
@@ -228,7 +247,7 @@ def main():
         graph.replay()
     else:
         for k in range(K):
-            pool.tick(dev[W_ + k], acts, stream.cuda_stream)
+            route_step(pool, W_ + k, stream.cuda_stream)
     end.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -247,7 +266,10 @@ def main():
     for k in range(K):
         t = W_ + k
         ev[k][0].record(stream)
-        pool2.route(dev[t], acts, None, stream.cuda_stream)
+        if args.sample:
+            route_step(pool2, t, stream.cuda_stream, with_schedule=False)
+        else:
+            pool2.route(dev[t], acts, None, stream.cuda_stream)
         ev[k][1].record(stream)
         pool2.schedule(dev[t], acts, stream.cuda_stream)
         ev[k][2].record(stream)
@@ -267,10 +289,11 @@ def main():
     sched_avg = float(np.mean(sched_ms))
     flops = np.mean([algorithmic_flops_per_tick(cfg, n) for n in n_req[W_:W_ + K]])
     peak_f = PEAK_BF16_TFLOPS if cfg["dtype"] == "bf16" else PEAK_F32_TFLOPS
-    tag = f"{args.config}_lam{int(cfg['lam'])}"
+    tag = f"{args.config}_lam{int(cfg['lam'])}" + ("_sample" if args.sample else "")
     if route_avg >= sched_avg:
         achieved = flops / (route_avg * 1e-3) / 1e12
-        roof = {"kernel": "route_" + cfg["dtype"], "bound": "mfma", "achieved": achieved,
+        roof = {"kernel": ("route_sample_" if args.sample else "route_") + cfg["dtype"],
+                "bound": "mfma", "achieved": achieved,
                 "peak": peak_f, "unit": "TFLOP/s", "frac": achieved / peak_f,
                 "traffic": load_traffic("route", tag, source_hash("route.hip")),
                 "avg_launch_us": route_avg * 1e3,
@@ -301,7 +324,9 @@ def main():
         "config": {"workload": f"{args.config}: {cfg['E']} envs, M={cfg['M']} K={cfg['K']}, "
                                f"lambda={cfg['lam']:g}/tick, qcap {cfg['qcap']}, MLP "
                                f"{cfg['feat_dim']}->" + "->".join(map(str, cfg["widths"])) +
-                               f" {cfg['dtype']}, ticks {W_}..{W_ + K - 1} of {T}",
+                               f" {cfg['dtype']}, ticks {W_}..{W_ + K - 1} of {T}" +
+                               ("; RL rollout: Gumbel-max sampled actions, log-probs, entropies, "
+                                "value head" if args.sample else ""),
                    "envs": cfg["E"], "requests_per_tick": routed / K, "parallelism": "single GPU",
                    "launch": "eager" if args.eager else f"one HIP graph of {K} ticks, captured "
                                                         "before the timed region"},

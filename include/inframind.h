@@ -87,18 +87,23 @@ typedef enum { IM_KEY_SLACK = 0, IM_KEY_DEADLINE = 1, IM_KEY_FCFS = 2 } im_key_m
  *                 with B = budget_max and every reciprocal rounded once to fp32.
  *   n_layers      2 or 3; widths[0..n_layers-1] are the layer output widths,
  *                 hidden widths equal, in {32, 64, 128, 256, 512} (512 bf16 only),
- *                 widths[n_layers-1] == M*K
+ *                 widths[n_layers-1] == M*K + value_head
  *   dtype         IM_F32: fp32 weights and activations; IM_BF16: bf16 weights,
  *                 inputs and hidden activations (round to nearest even), fp32
  *                 accumulation, biases and logits
  *   key_mode      im_key_mode
  *   max_arrivals_per_env_tick  largest n_e accepted (>= 1)
- *   budget_max    B >= 1, normaliser of the budget and latency features */
+ *   budget_max    B >= 1, normaliser of the budget and latency features
+ *   value_head    0 or 1. With 1 the last layer has one more row, row M*K,
+ *                 whose output is the state value V(s) = w_val . h + b_val of
+ *                 the last hidden layer h (Sec. 4.2 "Decision"); it gets no
+ *                 logit bias and takes no part in routing. */
 typedef struct {
   int32_t n_envs, n_models, n_depths, queue_cap, max_slots;
   int32_t embed_dim, feat_dim, n_layers;
   int32_t widths[4];
   int32_t dtype, key_mode, max_arrivals_per_env_tick, budget_max;
+  int32_t value_head;
 } im_pool_desc;
 
 /* The arrivals of ONE tick, in env-major CSR order (all device memory).
@@ -143,6 +148,32 @@ im_status im_pool_create(const im_pool_desc* desc, const float* const* W, const 
  * Argmax ties go to the lowest action index. */
 im_status im_route(im_pool* pool, const im_arrivals* arr, int32_t* actions, float* logits,
                    void* stream);
+
+/* Outputs of im_route_sample (device memory, caller-owned; one entry per
+ * arrival row). Any pointer but `actions` may be NULL to skip that output. */
+typedef struct {
+  int32_t* actions;   /* int32 [n_total]: chosen joint action, -1 as in im_route          */
+  float* logp;        /* fp32 [n_total]: log pi(action | s); 0 when the action is -1      */
+  float* entropy;     /* fp32 [n_total]: entropy of pi(. | s); 0 when no action is valid  */
+  float* value;       /* fp32 [n_total]: V(s) (pools with value_head = 1 only)            */
+  float* logits;      /* fp32 [n_total x M*K]: as in im_route                             */
+} im_policy_out;
+
+/* Route one tick for an RL rollout (Sec. 4.4: the executor's PPO objective,
+ * Eq. 5, needs the action's log-probability, the policy entropy and the state
+ * value). pi(a | s) is the softmax of the logits over the valid actions
+ * (masked as in im_route). With greedy = 0 the action is drawn from pi by the
+ * Gumbel-max trick: argmax over valid a of z_a + G_a with
+ * G_a = -ln(-ln U_a), U_a = (top 23 bits of word a % 4 of the Philox4x32-10
+ * block (Salmon et al., SC 2011) with counter (request id, env, a / 4, 0) and
+ * key (seed low 32 bits, seed high 32 bits)) + 1/2, times 2^-23. Request ids
+ * are the per-env ids im_schedule assigns (next_id + position in the env's
+ * rows), so every request gets its own noise for a given seed. With
+ * greedy = 1 the action is the masked argmax of im_route. Reads the state,
+ * does not change it. IM_EINVAL if value is requested from a pool without a
+ * value head. */
+im_status im_route_sample(im_pool* pool, const im_arrivals* arr, uint64_t seed, int32_t greedy,
+                          const im_policy_out* out, void* stream);
 
 /* Schedule one tick with the given actions (any actions in [-1, M*K), e.g.
  * sampled ones): admission in id order with tail-drop beyond queue_cap, keys

@@ -8,7 +8,8 @@ from __future__ import annotations
 
 from . import _lib
 from ._lib import (EXPORTED, IMError, im_clear_error, im_destroy, im_get_error,  # noqa: F401
-                   im_last_error, im_pool_create, im_read_state, im_route, im_schedule,
+                   im_last_error, im_pool_create, im_read_state, im_route, im_route_sample,
+                   im_schedule,
                    im_set_capacity, im_set_enabled, im_tick, im_write_state, make_arrivals,
                    make_desc)
 
@@ -38,6 +39,10 @@ class Pool:
 
     def route(self, arr, actions, logits=None, stream=None):
         im_route(self.h, arr, actions, logits, stream)
+
+    def route_sample(self, arr, seed, actions, logp=None, entropy=None, value=None, logits=None,
+                     greedy=False, stream=None):
+        im_route_sample(self.h, arr, seed, greedy, actions, logp, entropy, value, logits, stream)
 
     def schedule(self, arr, actions, stream=None):
         im_schedule(self.h, arr, actions, stream)

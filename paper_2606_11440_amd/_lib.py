@@ -2,9 +2,9 @@
 only. Every step of the tick runs in the library's HIP kernels; torch tensors
 merely provide device memory and the current HIP stream.
 
-The functions keep the C names (im_pool_create, im_route, im_schedule,
-im_tick, im_destroy, im_read_state, im_write_state, im_set_enabled,
-im_set_capacity, im_get_error, im_clear_error, im_last_error)."""
+The functions keep the C names (im_pool_create, im_route, im_route_sample,
+im_schedule, im_tick, im_destroy, im_read_state, im_write_state,
+im_set_enabled, im_set_capacity, im_get_error, im_clear_error, im_last_error)."""
 from __future__ import annotations
 
 import ctypes
@@ -20,7 +20,7 @@ IM_F32, IM_BF16 = 0, 1
 KEY_MODES = {"slack": 0, "deadline": 1, "fcfs": 2}
 IM_ERR_QIDX, IM_ERR_COUNT, IM_ERR_BUDGET, IM_ERR_SVC, IM_ERR_ACTION = 1, 2, 4, 8, 16
 
-EXPORTED = ("im_pool_create", "im_route", "im_schedule", "im_tick", "im_destroy",
+EXPORTED = ("im_pool_create", "im_route", "im_route_sample", "im_schedule", "im_tick", "im_destroy",
             "im_read_state", "im_write_state", "im_set_enabled", "im_set_capacity",
             "im_get_error", "im_clear_error", "im_last_error")
 
@@ -32,13 +32,19 @@ class ImPoolDesc(ctypes.Structure):
                 ("feat_dim", ctypes.c_int32), ("n_layers", ctypes.c_int32),
                 ("widths", ctypes.c_int32 * 4), ("dtype", ctypes.c_int32),
                 ("key_mode", ctypes.c_int32), ("max_arrivals_per_env_tick", ctypes.c_int32),
-                ("budget_max", ctypes.c_int32)]
+                ("budget_max", ctypes.c_int32), ("value_head", ctypes.c_int32)]
 
 
 class ImArrivals(ctypes.Structure):
     _fields_ = [("offsets", ctypes.c_void_p), ("q_idx", ctypes.c_void_p),
                 ("budget", ctypes.c_void_p), ("base_svc", ctypes.c_void_p),
                 ("n_total", ctypes.c_int32)]
+
+
+class ImPolicyOut(ctypes.Structure):
+    _fields_ = [("actions", ctypes.c_void_p), ("logp", ctypes.c_void_p),
+                ("entropy", ctypes.c_void_p), ("value", ctypes.c_void_p),
+                ("logits", ctypes.c_void_p)]
 
 
 ENTRY_DT = np.dtype([("key", "<i4"), ("id", "<i4"), ("t_arr", "<i4"), ("svc", "<u2"),
@@ -69,6 +75,8 @@ def load() -> ctypes.CDLL:
     L.im_pool_create.argtypes = [ctypes.POINTER(ImPoolDesc), P, P, P, I64, P, P, P,
                                  ctypes.POINTER(P)]
     L.im_route.argtypes = [P, ctypes.POINTER(ImArrivals), P, P, P]
+    L.im_route_sample.argtypes = [P, ctypes.POINTER(ImArrivals), ctypes.c_uint64, I32,
+                                  ctypes.POINTER(ImPolicyOut), P]
     L.im_schedule.argtypes = [P, ctypes.POINTER(ImArrivals), P, P]
     L.im_tick.argtypes = [P, ctypes.POINTER(ImArrivals), P, P]
     L.im_destroy.argtypes = [P]
@@ -127,6 +135,9 @@ def make_desc(cfg: dict) -> ImPoolDesc:
     d.key_mode = KEY_MODES[cfg["key_mode"]]
     d.max_arrivals_per_env_tick = cfg["max_arrivals"]
     d.budget_max = cfg["budget_max"]
+    vh = 1 if cfg.get("value_head") else 0
+    d.value_head = vh
+    d.widths[d.n_layers - 1] = cfg["widths"][-1] + vh
     return d
 
 
@@ -164,6 +175,14 @@ def im_pool_create(desc: ImPoolDesc, W, b, emb, n_queries: int, capacity, logit_
 def im_route(pool, arr: ImArrivals, actions, logits=None, stream=None):
     _check(load().im_route(pool, ctypes.byref(arr), _dptr(actions), _dptr(logits),
                            _stream(stream)), pool)
+
+
+def im_route_sample(pool, arr: ImArrivals, seed: int, greedy: bool, actions, logp=None,
+                    entropy=None, value=None, logits=None, stream=None):
+    """RL-rollout route: device tensors for the outputs (None to skip)."""
+    out = ImPolicyOut(_dptr(actions), _dptr(logp), _dptr(entropy), _dptr(value), _dptr(logits))
+    _check(load().im_route_sample(pool, ctypes.byref(arr), int(seed) & 0xffffffffffffffff,
+                                  int(bool(greedy)), ctypes.byref(out), _stream(stream)), pool)
 
 
 def im_schedule(pool, arr: ImArrivals, actions, stream=None):

@@ -65,6 +65,13 @@ struct RouteArgs {
   float* logits;
   int32_t* err;
   int32_t persistent_blocks;          // grid of the persistent kernels (0: never use them)
+  // RL-rollout outputs (im_route_sample)
+  int32_t rl;                         // 1: log-prob, entropy, value; sampled or greedy action
+  int32_t greedy;                     // with rl: 1 = masked argmax, 0 = Gumbel-max sample
+  uint32_t seed_lo, seed_hi;          // Philox key
+  float* logp;
+  float* entropy;
+  float* value;                       // row A of the last layer (value head), or NULL
 };
 
 struct SchedArgs {

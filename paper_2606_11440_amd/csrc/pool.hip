@@ -142,7 +142,9 @@ im_status im_pool_create(const im_pool_desc* desc, const float* const* W, const 
   if (d.embed_dim < 1 || d.feat_dim > IM_MAX_FEAT || d.feat_dim < d.embed_dim + 4 * d.n_models + 1)
     return fail(nullptr, IM_EINVAL, "feat_dim must be in [embed_dim + 4M + 1, IM_MAX_FEAT]");
   if (d.n_layers != 2 && d.n_layers != 3) return fail(nullptr, IM_EINVAL, "n_layers must be 2 or 3");
-  if (d.widths[d.n_layers - 1] != A) return fail(nullptr, IM_EINVAL, "last width must be M*K");
+  if (d.value_head != 0 && d.value_head != 1) return fail(nullptr, IM_EINVAL, "value_head must be 0 or 1");
+  if (d.widths[d.n_layers - 1] != A + d.value_head)
+    return fail(nullptr, IM_EINVAL, "last width must be M*K + value_head");
   if (d.n_layers == 3 && d.widths[0] != d.widths[1])
     return fail(nullptr, IM_EUNSUPPORTED, "hidden widths must be equal");
   if (d.dtype != IM_F32 && d.dtype != IM_BF16) return fail(nullptr, IM_EINVAL, "bad dtype");
@@ -151,7 +153,7 @@ im_status im_pool_create(const im_pool_desc* desc, const float* const* W, const 
   if (d.budget_max < 1) return fail(nullptr, IM_EINVAL, "budget_max < 1");
   if (n_queries < 1 || n_queries > INT32_MAX) return fail(nullptr, IM_EINVAL, "n_queries out of range");
   const int H = d.widths[0];
-  const int out_tiles = (A + 31) / 32;
+  const int out_tiles = (A + d.value_head + 31) / 32;
   if (!im::route_supported(d.dtype, H, d.n_layers, out_tiles))
     return fail(nullptr, IM_EUNSUPPORTED, "no route kernel for this dtype / hidden width");
   for (int64_t i = 0; i < (int64_t)d.n_envs * d.n_models; ++i)
@@ -217,7 +219,7 @@ im_status im_pool_create(const im_pool_desc* desc, const float* const* W, const 
           const int o = 32 * To + 8 * (v >> 2) + 4 * g + (v & 3);
           if (o >= outw) continue;
           float val = b[l][o];
-          if (l == d.n_layers - 1 && logit_bias) val += logit_bias[o / d.n_depths];
+          if (l == d.n_layers - 1 && logit_bias && o < A) val += logit_bias[o / d.n_depths];
           bp[((size_t)To * 2 + g) * 16 + v] = val;
         }
     st = upload(p, &p->bias[l], bp);
@@ -319,6 +321,27 @@ im_status im_route(im_pool* p, const im_arrivals* arr, int32_t* actions, float* 
   if (st != IM_OK) return st;
   if (arr->n_total > 0 && !actions) return fail(p, IM_EINVAL, "actions is NULL");
   const im::RouteArgs a = route_args(p, arr, actions, logits);
+  IM_HIP(p, im::launch_route(a, p->d.dtype, p->hidden, p->n_layers, p->out_tiles,
+                             (hipStream_t)stream));
+  return IM_OK;
+}
+
+im_status im_route_sample(im_pool* p, const im_arrivals* arr, uint64_t seed, int32_t greedy,
+                          const im_policy_out* out, void* stream) {
+  if (!p) return fail(nullptr, IM_EINVAL, "pool is NULL");
+  im_status st = check_arrivals(p, arr);
+  if (st != IM_OK) return st;
+  if (!out) return fail(p, IM_EINVAL, "out is NULL");
+  if (arr->n_total > 0 && !out->actions) return fail(p, IM_EINVAL, "actions is NULL");
+  if (out->value && !p->d.value_head) return fail(p, IM_EINVAL, "value requested from a pool without a value head");
+  im::RouteArgs a = route_args(p, arr, out->actions, out->logits);
+  a.rl = 1;
+  a.greedy = greedy ? 1 : 0;
+  a.seed_lo = (uint32_t)seed;
+  a.seed_hi = (uint32_t)(seed >> 32);
+  a.logp = out->logp;
+  a.entropy = out->entropy;
+  a.value = out->value;
   IM_HIP(p, im::launch_route(a, p->d.dtype, p->hidden, p->n_layers, p->out_tiles,
                              (hipStream_t)stream));
   return IM_OK;

@@ -242,8 +242,92 @@ __device__ __forceinline__ void gather_row(const RouteArgs& a, const RowCtx& c, 
   }
 }
 
-// Masked argmax over the lane pair (n, n + 32), logits store, action store.
+// Philox4x32-10 block (Salmon, Moraes, Dror, Shaw, SC 2011): ten rounds of
+// two 32x32 -> 64-bit products by the round multipliers, whose high halves are
+// xored with the other two counter words and the key; the key advances by the
+// Weyl constants after every round.
+__device__ __forceinline__ uint4 philox10(uint4 c, uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int i = 0; i < 10; ++i) {
+    const uint32_t lo0 = 0xD2511F53u * c.x, hi0 = __umulhi(0xD2511F53u, c.x);
+    const uint32_t lo1 = 0xCD9E8D57u * c.z, hi1 = __umulhi(0xCD9E8D57u, c.z);
+    c = make_uint4(hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0);
+    k0 += 0x9E3779B9u;
+    k1 += 0xBB67AE85u;
+  }
+  return c;
+}
+
+// Gumbel noise -ln(-ln U) of a 32-bit word, U = (top 23 bits + 1/2) 2^-23
+// (exact in fp32). -ln U goes through log1p above U = 1/2, where 1 - U is
+// exact and ln U would lose its relative precision.
+__device__ __forceinline__ float gumbel_of(uint32_t w) {
+  const uint32_t k = w >> 9;
+  const float e = k < (1u << 22) ? -logf(((float)k + 0.5f) * (1.0f / 8388608.0f))
+                                 : -log1pf(-(((float)(8388608u - k) - 0.5f) * (1.0f / 8388608.0f)));
+  return -logf(e);
+}
+
+// RL-rollout outputs of one row from its logits (lane pair n, n + 32 holds
+// the row's actions 32 T + 8 (v / 4) + 4 g + v % 4): pi is the softmax of
+// the logits over the valid actions, shifted by their largest logit `zmax`
+// (action `amax`, -1 when none is valid); the action is the Gumbel-max draw
+// (or `amax` when greedy), its log-probability z_a - logsumexp, the entropy
+// logsumexp - sum pi z, and the value head's row A.
 template <int AT>
+__device__ __forceinline__ void rl_outputs(const RouteArgs& a, const RowCtx& c,
+                                           const f32x16 (&acc)[AT], int g, float zmax, int amax) {
+  const bool sample = a.greedy == 0;
+  uint32_t id = 0;
+  if (sample) {
+    const int32_t rr = c.live ? c.r : a.n_total - 1;
+    id = (uint32_t)(a.ms[(size_t)c.e * a.M].next_id + (rr - a.offsets[c.e]));
+  }
+  float s = 0.f, sz = 0.f, val = 0.f, bs = 0.f, bz = 0.f;
+  int bsa = -1;
+#pragma unroll
+  for (int T = 0; T < AT; ++T) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int a0 = 32 * T + 8 * j + 4 * g;   // this lane's 4 consecutive actions: one Philox block
+      uint4 w = make_uint4(0, 0, 0, 0);
+      if (sample && a0 < a.A) w = philox10(make_uint4(id, (uint32_t)c.e, (uint32_t)(a0 >> 2), 0u), a.seed_lo, a.seed_hi);
+      const uint32_t wv[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int act = a0 + i;
+        const float z = acc[T][4 * j + i];
+        if (act == a.A) val = z;
+        if (act < a.A && ((c.amask >> act) & 1ull)) {
+          const float ex = __expf(z - zmax);
+          s += ex;
+          sz += ex * z;
+          const float sc = sample ? z + gumbel_of(wv[i]) : z;
+          if (bsa < 0 || sc > bs) { bs = sc; bsa = act; bz = z; }   // actions ascend: ties keep the lowest
+        }
+      }
+    }
+  }
+  s += __shfl_xor(s, 32, 64);
+  sz += __shfl_xor(sz, 32, 64);
+  val += __shfl_xor(val, 32, 64);                  // one lane of the pair holds row A
+  const float obs = __shfl_xor(bs, 32, 64), obz = __shfl_xor(bz, 32, 64);
+  const int obsa = __shfl_xor(bsa, 32, 64);
+  if (obsa >= 0 && (bsa < 0 || obs > bs || (obs == bs && obsa < bsa))) { bs = obs; bsa = obsa; bz = obz; }
+  if (!c.live || g != 0) return;
+  const bool any = amax >= 0 && !c.bad_q;
+  const float lse = any ? zmax + __logf(s) : 0.f;
+  a.actions[c.r] = any ? bsa : -1;
+  if (c.bad_q) atomicOr(a.err, IM_ERR_QIDX);
+  if (a.logp) a.logp[c.r] = any ? bz - lse : 0.f;
+  if (a.entropy) a.entropy[c.r] = any ? lse - sz / s : 0.f;
+  if (a.value) a.value[c.r] = c.bad_q ? 0.f : val;
+}
+
+// Masked argmax over the lane pair (n, n + 32), logits store, action store
+// (or the RL-rollout outputs). RL: 0 = greedy route only, 1 = RL outputs
+// only, 2 = either, chosen by a.rl at run time.
+template <int AT, int RL = 2>
 __device__ __forceinline__ void epilogue(const RouteArgs& a, const RowCtx& c, f32x16 (&acc)[AT],
                                          const float* bias, int g) {
   float best = 0.f;
@@ -263,11 +347,13 @@ __device__ __forceinline__ void epilogue(const RouteArgs& a, const RowCtx& c, f3
   const float ob = __shfl_xor(best, 32, 64);
   const int oa = __shfl_xor(ba, 32, 64);
   if (oa >= 0 && (ba < 0 || ob > best || (ob == best && oa < ba))) { best = ob; ba = oa; }
-  if (!c.live) return;
-  if (g == 0) {
+  if (RL == 1 || (RL == 2 && a.rl)) {
+    rl_outputs<AT>(a, c, acc, g, best, ba);
+  } else if (c.live && g == 0) {
     a.actions[c.r] = c.bad_q ? -1 : ba;
     if (c.bad_q) atomicOr(a.err, IM_ERR_QIDX);
   }
+  if (!c.live) return;
   if (a.logits) {
     float* out = a.logits + (size_t)c.r * a.A;
 #pragma unroll
@@ -483,7 +569,7 @@ __device__ __forceinline__ void copy_to_lds(u32x4* dst, const u32x4* src) {
   }
 }
 
-template <int H, int NL, int AT, int KB1, bool W1L, int NW, int ED, int NR>
+template <int H, int NL, int AT, int KB1, bool W1L, int NW, int ED, int NR, int RL>
 __global__ __launch_bounds__(NW * 64, 1) void route_bf16_lds(RouteArgs a) {
   constexpr int TH = H / 32;
   constexpr int KH = H / 16;
@@ -608,7 +694,7 @@ __global__ __launch_bounds__(NW * 64, 1) void route_bf16_lds(RouteArgs a) {
       }
     }
 #pragma unroll
-    for (int j = 0; j < NR; ++j) epilogue<AT>(a, c[j], o[j], nullptr, gg);
+    for (int j = 0; j < NR; ++j) epilogue<AT, RL>(a, c[j], o[j], nullptr, gg);
   }
 }
 
@@ -632,7 +718,7 @@ __device__ __forceinline__ void dma_frag(u32x4* dst, const u32x4* src, int lane)
                                    (__attribute__((address_space(3))) void*)dst, 16, 0, 0);
 }
 
-template <int H, int AT, int KB1, int ED, int NW>
+template <int H, int AT, int KB1, int ED, int NW, int RL>
 __global__ __launch_bounds__(NW * 64, 1) void route_bf16_stream(RouteArgs a) {
   constexpr int TH = H / 32, KH = H / 16;
   constexpr int S1 = TH / 2;                  // layer-1 stages (two output tiles each)
@@ -758,7 +844,7 @@ __global__ __launch_bounds__(NW * 64, 1) void route_bf16_stream(RouteArgs a) {
         }
       }
     }
-    epilogue<AT>(a, c, z, nullptr, gg);
+    epilogue<AT, RL>(a, c, z, nullptr, gg);
   }
   __builtin_amdgcn_s_waitcnt(0);   // the prefetched first stage of a step that does not exist
 }
@@ -766,9 +852,13 @@ __global__ __launch_bounds__(NW * 64, 1) void route_bf16_stream(RouteArgs a) {
 typedef void (*RouteKernel)(RouteArgs);
 
 template <int H, int NL>
-RouteKernel pick_bf16(int at) { return at == 1 ? route_bf16<H, NL, 1> : route_bf16<H, NL, 2>; }
+RouteKernel pick_bf16(int at) {
+  return at == 1 ? route_bf16<H, NL, 1> : (at == 2 ? route_bf16<H, NL, 2> : route_bf16<H, NL, 3>);
+}
 template <int H, int NL>
-RouteKernel pick_f32(int at) { return at == 1 ? route_f32<H, NL, 1> : route_f32<H, NL, 2>; }
+RouteKernel pick_f32(int at) {
+  return at == 1 ? route_f32<H, NL, 1> : (at == 2 ? route_f32<H, NL, 2> : route_f32<H, NL, 3>);
+}
 
 template <int NL>
 RouteKernel pick(int dtype, int hidden, int at) {
@@ -800,27 +890,35 @@ constexpr int kLdsRows = 1;
 // weights in LDS <= 160 KiB): returns nullptr when none applies.
 constexpr int kStreamWaves = 8;
 
-// Streaming kernels: kStreamWaves waves per block, 32 rows per wave.
-RouteKernel pick_stream(int dtype, int hidden, int n_layers, int out_tiles, int k1, int ed) {
+// Streaming kernels: kStreamWaves waves per block, 32 rows per wave. The
+// greedy route and the RL outputs are separate instantiations, so each keeps
+// only the registers its own epilogue needs.
+RouteKernel pick_stream(int dtype, int hidden, int n_layers, int out_tiles, int k1, int ed, bool rl) {
   if (dtype != IM_BF16) return nullptr;
   if (hidden == 512 && n_layers == 3 && out_tiles == 2 && k1 == 13 && ed == 128)
-    return route_bf16_stream<512, 2, 13, 128, kStreamWaves>;
+    return rl ? route_bf16_stream<512, 2, 13, 128, kStreamWaves, 1>
+              : route_bf16_stream<512, 2, 13, 128, kStreamWaves, 0>;
+  if (hidden == 512 && n_layers == 3 && out_tiles == 3 && k1 == 13 && ed == 128)
+    return rl ? route_bf16_stream<512, 3, 13, 128, kStreamWaves, 1>
+              : route_bf16_stream<512, 3, 13, 128, kStreamWaves, 0>;
   return nullptr;
 }
 
-RouteKernel pick_lds(int dtype, int hidden, int n_layers, int out_tiles, int k1, int ed) {
+RouteKernel pick_lds(int dtype, int hidden, int n_layers, int out_tiles, int k1, int ed, bool rl) {
   if (dtype != IM_BF16) return nullptr;
   if (hidden == 256 && n_layers == 3 && out_tiles == 1 && k1 == 6 && ed == 64)
-    return route_bf16_lds<256, 3, 1, 6, false, kLdsWaves, 64, kLdsRows>;
+    return rl ? route_bf16_lds<256, 3, 1, 6, false, kLdsWaves, 64, kLdsRows, 1>
+              : route_bf16_lds<256, 3, 1, 6, false, kLdsWaves, 64, kLdsRows, 0>;
   if (hidden == 256 && n_layers == 2 && out_tiles == 1 && k1 == 7 && ed == 64)
-    return route_bf16_lds<256, 2, 1, 7, true, kLdsWaves, 64, kLdsRows>;
+    return rl ? route_bf16_lds<256, 2, 1, 7, true, kLdsWaves, 64, kLdsRows, 1>
+              : route_bf16_lds<256, 2, 1, 7, true, kLdsWaves, 64, kLdsRows, 0>;
   return nullptr;
 }
 
 }  // namespace
 
 bool route_supported(int dtype, int hidden, int n_layers, int out_tiles) {
-  if (out_tiles < 1 || out_tiles > 2) return false;
+  if (out_tiles < 1 || out_tiles > 3) return false;
   RouteKernel k = n_layers == 2 ? pick<2>(dtype, hidden, out_tiles)
                  : n_layers == 3 ? pick<3>(dtype, hidden, out_tiles) : nullptr;
   return k != nullptr;
@@ -830,7 +928,7 @@ hipError_t launch_route(const RouteArgs& a, int dtype, int hidden, int n_layers,
                         hipStream_t s) {
   if (a.n_total <= 0) return hipSuccess;
   if (a.persistent_blocks > 0) {
-    RouteKernel kl = pick_lds(dtype, hidden, n_layers, out_tiles, a.k1, a.embed_dim);
+    RouteKernel kl = pick_lds(dtype, hidden, n_layers, out_tiles, a.k1, a.embed_dim, a.rl != 0);
     if (kl) {
       const int rows = kLdsWaves * 32 * kLdsRows;
       const int n_tiles = (a.n_total + rows - 1) / rows;
@@ -840,7 +938,7 @@ hipError_t launch_route(const RouteArgs& a, int dtype, int hidden, int n_layers,
     }
   }
   if (a.persistent_blocks > 0) {
-    RouteKernel ks = pick_stream(dtype, hidden, n_layers, out_tiles, a.k1, a.embed_dim);
+    RouteKernel ks = pick_stream(dtype, hidden, n_layers, out_tiles, a.k1, a.embed_dim, a.rl != 0);
     if (ks) {
       const int rows = kStreamWaves * 32;
       const int n_tiles = (a.n_total + rows - 1) / rows;
@@ -850,7 +948,7 @@ hipError_t launch_route(const RouteArgs& a, int dtype, int hidden, int n_layers,
     }
   }
   RouteKernel k = nullptr;
-  if (out_tiles >= 1 && out_tiles <= 2) {
+  if (out_tiles >= 1 && out_tiles <= 3) {
     if (n_layers == 2) k = pick<2>(dtype, hidden, out_tiles);
     else if (n_layers == 3) k = pick<3>(dtype, hidden, out_tiles);
   }

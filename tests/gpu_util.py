@@ -86,6 +86,74 @@ class Pair:
         self.orc.schedule(sub, g_act)
         return g_act
 
+    def step_rl(self, arr, seed, greedy=False):
+        """One lockstep tick of im_route_sample (sampled or greedy) followed by
+        im_schedule with the GPU's actions. Logits, log-probs, entropies and
+        values are checked against the oracle within the tolerance; a sampled
+        action may differ from the oracle's only where the oracle's perturbed
+        scores (logit + its Gumbel noise) of the two are within twice the
+        logit tolerance, and the oracle then follows the GPU's action."""
+        torch, P = self.torch, self.P
+        cfg = self.cfg
+        A = cfg["A"]
+        vh = bool(cfg.get("value_head"))
+        dev = P.device_arrivals(arr)
+        n = int(arr["q_idx"].size)
+        nn = max(n, 1)
+        f32 = dict(dtype=torch.float32, device="cuda")
+        act = torch.full((nn,), -7, dtype=torch.int32, device="cuda")
+        logp = torch.full((nn,), float("nan"), **f32)
+        ent = torch.full((nn,), float("nan"), **f32)
+        val = torch.full((nn,), float("nan"), **f32) if vh else None
+        lg = torch.full((nn, A), float("nan"), **f32)
+        self.gpu.route_sample(dev, seed, act, logp, ent, val, lg, greedy=greedy)
+        torch.cuda.synchronize()
+        sub = workload.gen.subset(arr, self.e0, self.e1)
+        lo = int(arr["offsets"][self.e0])
+        ns = int(sub["q_idx"].size)
+        sl = slice(lo, lo + ns)
+        g_act = act[sl].cpu().numpy()
+        g_lg = lg[sl].cpu().numpy().astype(np.float64)
+        g_lp = logp[sl].cpu().numpy().astype(np.float64)
+        g_en = ent[sl].cpu().numpy().astype(np.float64)
+        next_id = self.orc.state()["next_id"]
+        o = self.orc.route_rl(sub, seed, greedy=greedy, env_base=self.e0)
+        rtol = rtol_of(cfg)
+        if ns:
+            ok = logits_close(g_lg, o["logits"], rtol)
+            if not ok.all():
+                r = int(np.argmin(ok))
+                raise AssertionError(f"logits outside tolerance at row {r}")
+        off = sub["offsets"]
+        env_of = np.repeat(np.arange(self.e1 - self.e0), np.diff(off))
+        for r in range(ns):
+            z = o["logits"][r]
+            scale = float(np.max(np.abs(z)))
+            ga, oa = int(g_act[r]), int(o["actions"][r])
+            lse = z[oa] - o["logp"][r] if oa >= 0 else 0.0
+            if ga != oa:
+                assert ga >= 0 and oa >= 0, (r, ga, oa)
+                e = int(env_of[r])
+                rid = int(next_id[e]) + r - int(off[e])
+                gn = (lambda a: 0.0) if greedy else (
+                    lambda a: oracle.gumbel(seed, rid, self.e0 + e, a))
+                margin = (z[oa] + gn(oa)) - (z[ga] + gn(ga))
+                assert margin <= 2 * rtol * scale + 1e-5, (r, ga, oa, margin)
+                self.flips += 1
+            o_lp = z[ga] - lse if ga >= 0 else 0.0
+            assert abs(g_lp[r] - o_lp) <= 2 * rtol * scale + 1e-5, ("logp", r, g_lp[r], o_lp)
+            tol_h = 2 * np.log(max(A, 2)) * rtol * scale + 1e-5
+            assert abs(g_en[r] - o["entropy"][r]) <= tol_h, ("entropy", r, g_en[r], o["entropy"][r])
+        if vh and ns:
+            g_v = val[sl].cpu().numpy().astype(np.float64)
+            scale = np.max(np.abs(o["logits"]), axis=1)
+            bad = np.abs(g_v - o["value"]) > rtol * (scale + np.abs(o["value"])) + 1e-5
+            assert not bad.any(), ("value", np.argmax(bad), g_v[bad][:3], o["value"][bad][:3])
+        self.rows_checked += ns
+        self.gpu.schedule(dev, act)
+        self.orc.schedule(sub, g_act)
+        return g_act
+
     def _check_actions(self, g_act, o_act, o_lg, g_lg):
         rtol = rtol_of(self.cfg)
         if g_lg is not None and g_act.size:
