@@ -249,23 +249,28 @@ __device__ __forceinline__ void gather_row(const RouteArgs& a, const RowCtx& c, 
 __device__ __forceinline__ uint4 philox10(uint4 c, uint32_t k0, uint32_t k1) {
 #pragma unroll
   for (int i = 0; i < 10; ++i) {
-    const uint32_t lo0 = 0xD2511F53u * c.x, hi0 = __umulhi(0xD2511F53u, c.x);
-    const uint32_t lo1 = 0xCD9E8D57u * c.z, hi1 = __umulhi(0xCD9E8D57u, c.z);
-    c = make_uint4(hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0);
+    // one 32x32 -> 64-bit product each (a single v_mad_u64_u32)
+    const uint64_t p0 = (uint64_t)0xD2511F53u * c.x;
+    const uint64_t p1 = (uint64_t)0xCD9E8D57u * c.z;
+    c = make_uint4((uint32_t)(p1 >> 32) ^ c.y ^ k0, (uint32_t)p1, (uint32_t)(p0 >> 32) ^ c.w ^ k1,
+                   (uint32_t)p0);
     k0 += 0x9E3779B9u;
     k1 += 0xBB67AE85u;
   }
   return c;
 }
 
-// Gumbel noise -ln(-ln U) of a 32-bit word, U = (top 23 bits + 1/2) 2^-23
-// (exact in fp32). -ln U goes through log1p above U = 1/2, where 1 - U is
-// exact and ln U would lose its relative precision.
-__device__ __forceinline__ float gumbel_of(uint32_t w) {
+// Exponential variate E = -ln U of a 32-bit word, U = (top 23 bits + 1/2)
+// 2^-23 (exact in fp32). Above U = 15/16, 1 - U = d is exact and -ln(1 - d)
+// is summed as d + d^2/2 + ... + d^7/7 (the rest is below 2^-24 d), so E keeps
+// its relative precision however close U is to 1.
+__device__ __forceinline__ float expo_of(uint32_t w) {
   const uint32_t k = w >> 9;
-  const float e = k < (1u << 22) ? -logf(((float)k + 0.5f) * (1.0f / 8388608.0f))
-                                 : -log1pf(-(((float)(8388608u - k) - 0.5f) * (1.0f / 8388608.0f)));
-  return -logf(e);
+  const float u = ((float)k + 0.5f) * (1.0f / 8388608.0f);
+  const float d = ((float)(8388608u - k) - 0.5f) * (1.0f / 8388608.0f);
+  const float series =
+      d * (1.f + d * (0.5f + d * (1.f / 3.f + d * (0.25f + d * (0.2f + d * (1.f / 6.f + d * (1.f / 7.f)))))));
+  return d < 0.0625f ? series : -__logf(u);
 }
 
 // RL-rollout outputs of one row from its logits (lane pair n, n + 32 holds
@@ -273,7 +278,9 @@ __device__ __forceinline__ float gumbel_of(uint32_t w) {
 // the logits over the valid actions, shifted by their largest logit `zmax`
 // (action `amax`, -1 when none is valid); the action is the Gumbel-max draw
 // (or `amax` when greedy), its log-probability z_a - logsumexp, the entropy
-// logsumexp - sum pi z, and the value head's row A.
+// logsumexp - sum pi z, and the value head's row A. The Gumbel-max draw
+// argmax z_a - ln(E_a), E_a = -ln U_a, is taken as the equivalent argmax of
+// exp(z_a - zmax) / E_a (one logarithm per action instead of two).
 template <int AT>
 __device__ __forceinline__ void rl_outputs(const RouteArgs& a, const RowCtx& c,
                                            const f32x16 (&acc)[AT], int g, float zmax, int amax) {
@@ -302,7 +309,7 @@ __device__ __forceinline__ void rl_outputs(const RouteArgs& a, const RowCtx& c,
           const float ex = __expf(z - zmax);
           s += ex;
           sz += ex * z;
-          const float sc = sample ? z + gumbel_of(wv[i]) : z;
+          const float sc = sample ? __fdividef(ex, expo_of(wv[i])) : z;
           if (bsa < 0 || sc > bs) { bs = sc; bsa = act; bz = z; }   // actions ascend: ties keep the lowest
         }
       }
