@@ -103,9 +103,37 @@ def cpu_baseline(cfg, W, b, emb_vals, cap, lb, ticks, Q, budget_s=15.0):
                       f"{dt:.1f} s wall, {nreq / dt:.0f} routed req/s"}
 
 
+def mfma_probe(torch, zeros=False):
+    """bf16 MFMA throughput of a register-resident 32x32x16 MFMA loop on every
+    SIMD (paper_2606_11440_amd/csrc/peak_probe.hip), N(0,1) operands (or
+    zeros): the matrix cores' achievable rate on this device with no memory
+    traffic."""
+    import ctypes
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2606_11440_amd", "libimprobe.so"))
+    lib.im_probe_mfma_bf16.restype = ctypes.c_double
+    lib.im_probe_mfma_bf16.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int,
+                                       ctypes.c_int, ctypes.c_void_p]
+    src = (torch.zeros if zeros else torch.randn)(1024, device="cuda", dtype=torch.bfloat16)
+    blocks, iters = 1024, 20000
+    sink = torch.empty(blocks * 4, device="cuda", dtype=torch.float32)
+    st = torch.cuda.current_stream().cuda_stream
+    run = lambda: lib.im_probe_mfma_bf16(src.data_ptr(), sink.data_ptr(), blocks, iters, st)  # noqa: E731
+    run()
+    torch.cuda.synchronize()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s.record()
+    flops = sum(run() for _ in range(3))
+    e.record()
+    torch.cuda.synchronize()
+    return flops / (s.elapsed_time(e) * 1e-3) / 1e12
+
+
 def measured_peaks(torch):
-    """Achievable peaks on this device, measured with library kernels: a
-    8192^3 bf16 GEMM (torch.matmul on hipBLASLt) and a 1 GiB device copy."""
+    """Achievable peaks on this device: the MFMA probe (random and zero
+    operands), a 8192^3 bf16 GEMM (torch.matmul on hipBLASLt) and a 1 GiB
+    device copy."""
+    mfma_rand = mfma_probe(torch)
+    mfma_zero = mfma_probe(torch, zeros=True)
     n = 8192
     a = torch.randn(n, n, device="cuda", dtype=torch.bfloat16)
     b = torch.randn(n, n, device="cuda", dtype=torch.bfloat16)
@@ -132,7 +160,8 @@ def measured_peaks(torch):
     copy_gbs = 5 * 2 * (1 << 30) / (s.elapsed_time(e) * 1e-3) / 1e9
     del a, b, src, dst
     torch.cuda.empty_cache()
-    return {"bf16_gemm_tflops": gemm_tflops, "copy_gbs_read_plus_write": copy_gbs}
+    return {"mfma_bf16_tflops_random": mfma_rand, "mfma_bf16_tflops_zero": mfma_zero,
+            "bf16_gemm_tflops": gemm_tflops, "copy_gbs_read_plus_write": copy_gbs}
 
 
 def main():
@@ -313,7 +342,8 @@ def main():
         mp = measured_peaks(torch)
         roof["measured_peak"] = mp
         if roof["unit"] == "TFLOP/s":
-            roof["frac_of_measured"] = roof["achieved"] / mp["bf16_gemm_tflops"]
+            roof["frac_of_measured"] = roof["achieved"] / mp["mfma_bf16_tflops_random"]
+            roof["frac_of_measured_gemm"] = roof["achieved"] / mp["bf16_gemm_tflops"]
         else:
             roof["frac_of_measured"] = roof["achieved"] / mp["copy_gbs_read_plus_write"]
 
