@@ -102,7 +102,7 @@ __device__ __forceinline__ void merge_front(Queue& q, int4& fe, const int4* seg,
 // Refill the (empty) front with the min(64, P) smallest pool entries; the new
 // front is returned in `fe` (lane i: entry i), the front array is not written.
 // `pk`/`pi` are this wave's LDS staging rows (64 keys, 64 pool indices), `kb`
-// its LDS buffer for 8 chunks of pool keys.
+// its LDS buffer for 4 chunks of pool keys.
 __device__ void refill(Queue& q, int4& fe, int4* pool, int64_t* pk, int32_t* pi, int2* kb,
                        int key_mode) {
   const int lane = lane_id();
@@ -144,7 +144,7 @@ __device__ void refill(Queue& q, int4& fe, int4* pool, int64_t* pk, int32_t* pi,
     thr = readlane64(ck, 63);
     np = 0;
   };
-  constexpr int G = 8;   // pool chunks whose loads are in flight together
+  constexpr int G = 4;   // pool chunks whose loads are in flight together
   const int2* keys = reinterpret_cast<const int2*>(pool);   // (key, id) of entry i at keys[2 i]
   for (int c0 = kFront; c0 < P; c0 += G * kFront) {
     int2 kv[G];
@@ -269,7 +269,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
   __shared__ int32_t acc_lds[4][IM_MAX_MODELS];
   __shared__ int64_t pend_k[4][kFront];   // refill candidate staging
   __shared__ int32_t pend_i[4][kFront];
-  __shared__ int2 pend_kb[4][8 * kFront];
+  __shared__ int2 pend_kb[4][4 * kFront];
   const int lane = threadIdx.x & 63;
   const int wv = threadIdx.x >> 6;
   const int e = (int)blockIdx.x * 4 + wv;
