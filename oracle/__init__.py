@@ -74,6 +74,7 @@ def _load():
         L.orc_philox4x32_10.argtypes = [P, P, P]
         L.orc_gumbel.argtypes = [U32, U32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int]
         L.orc_gumbel.restype = ctypes.c_double
+        L.orc_dual_update.argtypes = [P, ctypes.c_double, ctypes.c_double, P]
         _lib = L
     return _lib
 
@@ -200,6 +201,12 @@ class Oracle:
                                _ptr(out["entropy"]), _ptr(out["value"]), self.threads)
         return out
 
+    def dual_update(self, lam: float, eta: float, lambda_max: float) -> float:
+        """Eq. 7 over the completions since the previous call; returns lambda."""
+        x = np.array([lam], np.float64)
+        self._lib.orc_dual_update(self.p, float(eta), float(lambda_max), _ptr(x))
+        return float(x[0])
+
     def schedule(self, arr, actions):
         off, q, bud, svc = self._arr(arr)
         act = np.ascontiguousarray(actions, np.int32)
@@ -227,7 +234,7 @@ class Oracle:
         E, M, S, Qc, A = self.E, self.M, self.S, self.qcap, self.A
         env_i32 = np.zeros(E, np.int32)
         env_i64 = np.zeros((E, 2), np.int64)
-        mod = np.zeros((E, M, 13), np.int64)
+        mod = np.zeros((E, M, 14), np.int64)
         slots = np.zeros((E, M, S, 4), np.int32)
         queues = np.zeros((E, M, Qc, 5), np.int32)
         hist = np.zeros((E, A), np.int64)
@@ -238,4 +245,5 @@ class Oracle:
                     cap=mod[..., 4], enabled=mod[..., 5], rej_overflow=mod[..., 6],
                     enqueued=mod[..., 7], started=mod[..., 8], completed=mod[..., 9],
                     slo_met=mod[..., 10], lat_sum=mod[..., 11], wait_sum=mod[..., 12],
+                    cost_q16=mod[..., 13],
                     slots=slots, queues=queues, hist=hist)

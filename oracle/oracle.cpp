@@ -93,6 +93,7 @@ struct ModelState {
   int32_t enabled = 1;
   int64_t rej_overflow = 0, enqueued = 0, started = 0, completed = 0,
           slo_met = 0, lat_sum = 0, wait_sum = 0;
+  int64_t cost_q16 = 0;       // sum over completions of floor(2^16 latency / budget)
 };
 
 struct EnvState {
@@ -128,6 +129,7 @@ struct orc_pool {
   std::vector<EnvState> envs;
   int32_t t = 0;
   int32_t err = 0;
+  int64_t dual_completed = 0, dual_cost_q16 = 0;   // totals at the last dual update
 };
 
 }  // extern "C"
@@ -412,6 +414,8 @@ void schedule_env(orc_pool* p, int e, int32_t n_total, const int32_t* off,
       ms.completed += 1;
       ms.lat_sum += lat;
       ms.slo_met += (lat <= sl.budget) ? 1 : 0;
+      // Sec. 3 cost C_k = latency / budget (Eq. 2), accumulated in Q16 for the dual update
+      ms.cost_q16 += ((int64_t)lat << 16) / sl.budget;
       sl = Slot();
     }
   }
@@ -504,6 +508,24 @@ void orc_route_rl(orc_pool* p, int env_base, const int32_t* off, const int32_t* 
   for (int32_t x : errs) p->err |= x;
 }
 
+// Dual update of the Lagrange multiplier (Eq. 7): over the completions since
+// the previous update, C_bar = mean latency / budget (each term floor(2^16
+// l / beta) / 2^16), and lambda <- clip(lambda + eta (C_bar - 1), 0, lambda_max).
+// No completion since the previous update leaves lambda unchanged.
+void orc_dual_update(orc_pool* p, double eta, double lambda_max, double* lambda) {
+  int64_t n = 0, cost = 0;
+  for (const EnvState& env : p->envs)
+    for (const ModelState& ms : env.models) { n += ms.completed; cost += ms.cost_q16; }
+  const int64_t dn = n - p->dual_completed, dc = cost - p->dual_cost_q16;
+  p->dual_completed = n;
+  p->dual_cost_q16 = cost;
+  if (dn <= 0) return;
+  const double cbar = (double)dc / (65536.0 * (double)dn);
+  double l = *lambda + eta * (cbar - 1.0);
+  l = l < 0.0 ? 0.0 : (l > lambda_max ? lambda_max : l);
+  *lambda = l;
+}
+
 void orc_philox4x32_10(const uint32_t* ctr, const uint32_t* key, uint32_t* out) {
   philox4x32_10(ctr, key, out);
 }
@@ -530,8 +552,8 @@ void orc_set_capacity(orc_pool* p, int e, int m, int c) { p->envs[e].models[m].c
 // State export in the oracle's own layout:
 //   env_i32 [E]      next_id
 //   env_i64 [E*2]    arrived, rej_nomodel
-//   mod_i64 [E*M*13] qlen, busy, ewma_q8, backlog, cap, enabled, rej_overflow,
-//                    enqueued, started, completed, slo_met, lat_sum, wait_sum
+//   mod_i64 [E*M*14] qlen, busy, ewma_q8, backlog, cap, enabled, rej_overflow,
+//                    enqueued, started, completed, slo_met, lat_sum, wait_sum, cost_q16
 //   slots   [E*M*max_slots*4] id(-1 if free), t_arr, rem, budget
 //   queues  [E*M*qcap*5] key, id, t_arr, svc, budget (zero beyond qlen)
 //   hist    [E*A]
@@ -549,11 +571,11 @@ void orc_read_state(const orc_pool* p, int32_t* env_i32, int64_t* env_i64, int64
       const size_t em = (size_t)e * d.M + m;
       int busy = 0;
       for (const Slot& s : ms.slots) busy += s.busy ? 1 : 0;
-      int64_t* o = mod_i64 + em * 13;
+      int64_t* o = mod_i64 + em * 14;
       o[0] = (int64_t)ms.queue.size(); o[1] = busy; o[2] = ms.ewma_q8; o[3] = ms.backlog;
       o[4] = ms.cap; o[5] = ms.enabled; o[6] = ms.rej_overflow; o[7] = ms.enqueued;
       o[8] = ms.started; o[9] = ms.completed; o[10] = ms.slo_met; o[11] = ms.lat_sum;
-      o[12] = ms.wait_sum;
+      o[12] = ms.wait_sum; o[13] = ms.cost_q16;
       for (int s = 0; s < d.max_slots; ++s) {
         const Slot& sl = ms.slots[s];
         int32_t* so = slots + (em * d.max_slots + s) * 4;
