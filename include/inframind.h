@@ -202,7 +202,8 @@ typedef struct {            /* a service slot; id = -1 when free              */
 
 typedef struct {
   int32_t qlen, busy, ewma_q8, backlog, capacity, enabled, _pad0, _pad1;
-  int64_t rej_overflow, enqueued, started, completed, slo_met, lat_sum, wait_sum, _pad2;
+  int64_t rej_overflow, enqueued, started, completed, slo_met, lat_sum, wait_sum;
+  int64_t cost_q16;         /* sum over completions of floor(2^16 latency / budget) */
 } im_model_state;
 
 typedef struct {
@@ -227,6 +228,16 @@ im_status im_read_state(im_pool* pool, int32_t env_begin, int32_t env_count, int
 im_status im_write_state(im_pool* pool, int32_t env_begin, int32_t env_count, int32_t tick,
                          const im_env_state* envs, const im_model_state* models,
                          const im_slot* slots, const im_entry* queues, const int64_t* hist);
+
+/* Dual update of the Lagrange multiplier (Sec. 4.4, Eq. 7; App. C with no
+ * monetary budget): over the requests completed since the previous call (or
+ * since pool creation), C_bar = mean of latency / budget (each term
+ * floor(2^16 latency / budget) / 2^16, the cost of Eq. 2), then
+ * lambda <- clip(lambda + eta (C_bar - 1), 0, lambda_max) in fp64. With no
+ * completion in between, lambda is unchanged.
+ *   lambda  device fp64 [1], in/out
+ * Stream-ordered; IM_EINVAL for eta < 0 or lambda_max < 0. */
+im_status im_dual_update(im_pool* pool, double eta, double lambda_max, double* lambda, void* stream);
 
 /* Host knobs (stream-ordered): take a model out of routing, or change its
  * number of service slots (requests in slots >= the new capacity finish but

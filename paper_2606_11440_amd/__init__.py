@@ -7,7 +7,8 @@ not load the library; the first call does, and fails loudly if it is missing."""
 from __future__ import annotations
 
 from . import _lib
-from ._lib import (EXPORTED, IMError, im_clear_error, im_destroy, im_get_error,  # noqa: F401
+from ._lib import (EXPORTED, IMError, im_clear_error, im_destroy, im_dual_update,  # noqa: F401
+                   im_get_error,
                    im_last_error, im_pool_create, im_read_state, im_route, im_route_sample,
                    im_schedule,
                    im_set_capacity, im_set_enabled, im_tick, im_write_state, make_arrivals,
@@ -43,6 +44,9 @@ class Pool:
     def route_sample(self, arr, seed, actions, logp=None, entropy=None, value=None, logits=None,
                      greedy=False, stream=None):
         im_route_sample(self.h, arr, seed, greedy, actions, logp, entropy, value, logits, stream)
+
+    def dual_update(self, eta, lambda_max, lam, stream=None):
+        im_dual_update(self.h, eta, lambda_max, lam, stream)
 
     def schedule(self, arr, actions, stream=None):
         im_schedule(self.h, arr, actions, stream)

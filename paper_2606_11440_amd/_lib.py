@@ -21,6 +21,7 @@ KEY_MODES = {"slack": 0, "deadline": 1, "fcfs": 2}
 IM_ERR_QIDX, IM_ERR_COUNT, IM_ERR_BUDGET, IM_ERR_SVC, IM_ERR_ACTION = 1, 2, 4, 8, 16
 
 EXPORTED = ("im_pool_create", "im_route", "im_route_sample", "im_schedule", "im_tick", "im_destroy",
+            "im_dual_update",
             "im_read_state", "im_write_state", "im_set_enabled", "im_set_capacity",
             "im_get_error", "im_clear_error", "im_last_error")
 
@@ -54,7 +55,7 @@ MODEL_DT = np.dtype([("qlen", "<i4"), ("busy", "<i4"), ("ewma_q8", "<i4"), ("bac
                      ("capacity", "<i4"), ("enabled", "<i4"), ("_p0", "<i4"), ("_p1", "<i4"),
                      ("rej_overflow", "<i8"), ("enqueued", "<i8"), ("started", "<i8"),
                      ("completed", "<i8"), ("slo_met", "<i8"), ("lat_sum", "<i8"),
-                     ("wait_sum", "<i8"), ("_p2", "<i8")])
+                     ("wait_sum", "<i8"), ("cost_q16", "<i8")])
 ENV_DT = np.dtype([("arrived", "<i8"), ("rej_nomodel", "<i8"), ("next_id", "<i4"), ("_p", "<i4")])
 assert ENTRY_DT.itemsize == 16 and SLOT_DT.itemsize == 16
 assert MODEL_DT.itemsize == 96 and ENV_DT.itemsize == 24
@@ -80,6 +81,7 @@ def load() -> ctypes.CDLL:
     L.im_schedule.argtypes = [P, ctypes.POINTER(ImArrivals), P, P]
     L.im_tick.argtypes = [P, ctypes.POINTER(ImArrivals), P, P]
     L.im_destroy.argtypes = [P]
+    L.im_dual_update.argtypes = [P, ctypes.c_double, ctypes.c_double, P, P]
     L.im_destroy.restype = None
     L.im_read_state.argtypes = [P, I32, I32, ctypes.POINTER(I32), P, P, P, P, P]
     L.im_write_state.argtypes = [P, I32, I32, I32, P, P, P, P, P]
@@ -193,6 +195,11 @@ def im_tick(pool, arr: ImArrivals, actions_out=None, stream=None):
     _check(load().im_tick(pool, ctypes.byref(arr), _dptr(actions_out), _stream(stream)), pool)
 
 
+def im_dual_update(pool, eta: float, lambda_max: float, lam, stream=None):
+    """Eq. 7 on the device; `lam` is a device float64 tensor [1] (in/out)."""
+    _check(load().im_dual_update(pool, float(eta), float(lambda_max), _dptr(lam), _stream(stream)), pool)
+
+
 def im_destroy(pool):
     if pool:
         load().im_destroy(pool)
@@ -251,7 +258,8 @@ def im_read_state(pool, env_begin: int, env_count: int, M: int, A: int, S: int, 
     for k, f in (("qlen", "qlen"), ("busy", "busy"), ("ewma", "ewma_q8"), ("backlog", "backlog"),
                  ("cap", "capacity"), ("enabled", "enabled"), ("rej_overflow", "rej_overflow"),
                  ("enqueued", "enqueued"), ("started", "started"), ("completed", "completed"),
-                 ("slo_met", "slo_met"), ("lat_sum", "lat_sum"), ("wait_sum", "wait_sum")):
+                 ("slo_met", "slo_met"), ("lat_sum", "lat_sum"), ("wait_sum", "wait_sum"),
+                 ("cost_q16", "cost_q16")):
         out[k] = md[f].astype(np.int64)
     return out
 
@@ -268,7 +276,8 @@ def im_write_state(pool, env_begin: int, s: dict):
     for k, f in (("qlen", "qlen"), ("busy", "busy"), ("ewma", "ewma_q8"), ("backlog", "backlog"),
                  ("cap", "capacity"), ("enabled", "enabled"), ("rej_overflow", "rej_overflow"),
                  ("enqueued", "enqueued"), ("started", "started"), ("completed", "completed"),
-                 ("slo_met", "slo_met"), ("lat_sum", "lat_sum"), ("wait_sum", "wait_sum")):
+                 ("slo_met", "slo_met"), ("lat_sum", "lat_sum"), ("wait_sum", "wait_sum"),
+                 ("cost_q16", "cost_q16")):
         models[f] = s[k]
     slots = np.zeros((E, M, S), SLOT_DT)
     for i, f in enumerate(("id", "t_arr", "rem", "budget")):

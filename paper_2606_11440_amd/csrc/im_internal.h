@@ -37,9 +37,10 @@ __host__ __device__ inline int snap_stride(int M) {
 }
 __host__ __device__ inline int snap_valid_offset(int M) { return 4 * M; }   // in floats
 
-// Counter slots per (env, model), int64.
+// Counter slots per (env, model), int64. C_COST_Q16 sums floor(2^16 latency /
+// budget) over completions (the cost of Eq. 2, for the dual update of Eq. 7).
 enum { C_REJ_OVERFLOW = 0, C_ENQUEUED, C_STARTED, C_COMPLETED, C_SLO_MET, C_LAT_SUM,
-       C_WAIT_SUM, C_NUM = 8 };
+       C_WAIT_SUM, C_COST_Q16, C_NUM = 8 };
 
 // Queue entry in device memory: {key, id, t_arr, svc | budget << 16}.
 // Slot in device memory: {id (-1 free), t_arr, tick at which it completes, budget};
@@ -97,6 +98,10 @@ struct SchedArgs {
 };
 
 // Host-side launchers (defined in the .hip files).
+// Dual update (Eq. 7): acc [2] device accumulators (zero between calls), last
+// [2] totals at the previous update, lambda device in/out.
+hipError_t launch_dual_update(const int64_t* cnt, int64_t n_em, unsigned long long* acc, int64_t* last,
+                              double eta, double lambda_max, double* lambda, hipStream_t s);
 bool route_supported(int dtype, int hidden, int n_layers, int out_tiles);
 hipError_t launch_route(const RouteArgs& a, int dtype, int hidden, int n_layers, int out_tiles,
                         hipStream_t s);

@@ -38,6 +38,8 @@ struct im_pool {
   int32_t* err = nullptr;
   int32_t* act_buf = nullptr;
   int64_t act_cap = 0;
+  unsigned long long* dual_acc = nullptr;   // [2] completions, Q16 cost (zero between calls)
+  int64_t* dual_last = nullptr;             // [2] totals at the previous dual update
   int32_t t = 0;
   int32_t cu_count = 0;
   std::string last_error;
@@ -118,7 +120,7 @@ void free_pool(im_pool* p) {
     if (p->bias[l]) (void)hipFree(p->bias[l]);
   }
   void* bufs[] = {p->inv_tab, p->ms, p->cnt, p->env_cnt, p->hist, p->slots,
-                  p->front, p->qpool, p->snap, p->err, p->act_buf};
+                  p->front, p->qpool, p->snap, p->err, p->act_buf, p->dual_acc, p->dual_last};
   for (void* b : bufs) if (b) (void)hipFree(b);
   delete p;
 }
@@ -261,6 +263,8 @@ im_status im_pool_create(const im_pool_desc* desc, const float* const* W, const 
   if (st == IM_OK) st = zalloc(p, &p->qpool, EM * (size_t)d.queue_cap);
   if (st == IM_OK) st = zalloc(p, &p->snap, (size_t)d.n_envs * im::snap_stride(d.n_models));
   if (st == IM_OK) st = zalloc(p, &p->err, 1);
+  if (st == IM_OK) st = zalloc(p, &p->dual_acc, 2);
+  if (st == IM_OK) st = zalloc(p, &p->dual_last, 2);
   if (st == IM_OK) {
     p->act_cap = (int64_t)d.n_envs * d.max_arrivals_per_env_tick;
     st = zalloc(p, &p->act_buf, (size_t)p->act_cap);
@@ -401,6 +405,15 @@ im_status im_tick(im_pool* p, const im_arrivals* arr, int32_t* actions_out, void
   return im_schedule(p, arr, act, stream);
 }
 
+im_status im_dual_update(im_pool* p, double eta, double lambda_max, double* lambda, void* stream) {
+  if (!p) return fail(nullptr, IM_EINVAL, "pool is NULL");
+  if (!lambda) return fail(p, IM_EINVAL, "lambda is NULL");
+  if (!(eta >= 0.0) || !(lambda_max >= 0.0)) return fail(p, IM_EINVAL, "eta and lambda_max must be >= 0");
+  IM_HIP(p, im::launch_dual_update(p->cnt, (int64_t)p->d.n_envs * p->d.n_models, p->dual_acc,
+                                   p->dual_last, eta, lambda_max, lambda, (hipStream_t)stream));
+  return IM_OK;
+}
+
 im_status im_set_enabled(im_pool* p, int32_t env, int32_t model, int32_t enabled, void* stream) {
   if (!p) return fail(nullptr, IM_EINVAL, "pool is NULL");
   if (env < 0 || env >= p->d.n_envs || model < 0 || model >= p->d.n_models)
@@ -482,6 +495,7 @@ im_status im_read_state(im_pool* p, int32_t env_begin, int32_t env_count, int32_
       o.rej_overflow = c[im::C_REJ_OVERFLOW]; o.enqueued = c[im::C_ENQUEUED];
       o.started = c[im::C_STARTED]; o.completed = c[im::C_COMPLETED]; o.slo_met = c[im::C_SLO_MET];
       o.lat_sum = c[im::C_LAT_SUM]; o.wait_sum = c[im::C_WAIT_SUM];
+      o.cost_q16 = c[im::C_COST_Q16];
     }
   }
   if (slots && EMc) {
@@ -595,6 +609,7 @@ im_status im_write_state(im_pool* p, int32_t env_begin, int32_t env_count, int32
     c[im::C_REJ_OVERFLOW] = ms.rej_overflow; c[im::C_ENQUEUED] = ms.enqueued;
     c[im::C_STARTED] = ms.started; c[im::C_COMPLETED] = ms.completed; c[im::C_SLO_MET] = ms.slo_met;
     c[im::C_LAT_SUM] = ms.lat_sum; c[im::C_WAIT_SUM] = ms.wait_sum;
+    c[im::C_COST_Q16] = ms.cost_q16;
   }
   std::vector<int64_t> ec((size_t)env_count * 2);
   for (int e = 0; e < env_count; ++e) { ec[2 * e] = envs[e].arrived; ec[2 * e + 1] = envs[e].rej_nomodel; }

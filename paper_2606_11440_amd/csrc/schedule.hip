@@ -459,7 +459,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         if (lane < S) in.slot = a.slots[em * S + lane];
       }
       if ((need_cnt >> mm) & 1ull) {
-        if (lane < C_NUM - 1) in.cnt = a.cnt[em * C_NUM + lane];
+        if (lane < C_NUM) in.cnt = a.cnt[em * C_NUM + lane];
       }
     };
     if (r > 0) wave_mem_sync();   // the fronts written in the previous round
@@ -535,6 +535,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
       const bool due = q.busy_mask != 0 && q.next_done <= t;
       int32_t started = 0, wait_add = 0, svc_out = 0;
       int32_t completed = 0, slo_add = 0, lat_add = 0;
+      int64_t cost_add = 0;
       if (pops || due) {
         // slot: {id, t_arr, tick of completion, budget}; id -1 = empty
         int4 sl = cur.slot;
@@ -586,6 +587,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
           dm &= dm - 1;
           const int32_t ls = rl(lat, s);
           lat_add += ls;
+          // cost latency / budget of Eq. 2 in Q16 (budget >= 1)
+          cost_add += (int64_t)(((uint64_t)(uint32_t)ls << 16) / (uint32_t)rl(sl.w, s));
           const int64_t delta = (int64_t)ls * 256 - ewma;
           const int64_t stepv = delta >= 0 ? (delta >> 3) : -((-delta + 7) >> 3);
           ewma = (int32_t)(ewma + stepv);
@@ -621,6 +624,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
           case C_SLO_MET: add = slo_add; break;
           case C_LAT_SUM: add = lat_add; break;
           case C_WAIT_SUM: add = wait_add; break;
+          case C_COST_Q16: add = cost_add; break;
           default: break;
         }
         if (add != 0) a.cnt[em * C_NUM + lane] = cur.cnt + add;
@@ -687,7 +691,61 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
   }
 }
 
+// Dual update, step 1: exact int64 sums of completions and Q16 cost over every
+// (env, model) counter row (order-independent: integer atomics).
+__global__ void dual_reduce_kernel(const int64_t* cnt, int64_t n_em, unsigned long long* acc) {
+  uint64_t n = 0, c = 0;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_em;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    n += (uint64_t)cnt[i * C_NUM + C_COMPLETED];
+    c += (uint64_t)cnt[i * C_NUM + C_COST_Q16];
+  }
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) {
+    n += (uint64_t)shfl_xor((int64_t)n, m);
+    c += (uint64_t)shfl_xor((int64_t)c, m);
+  }
+  if ((threadIdx.x & 63) == 0 && (n | c) != 0) {
+    atomicAdd(acc, (unsigned long long)n);
+    atomicAdd(acc + 1, (unsigned long long)c);
+  }
+}
+
+// Dual update, step 2 (one thread): over the completions since the previous
+// update, C_bar = cost / (2^16 n) and lambda <- clip(lambda + eta (C_bar - 1),
+// 0, lambda_max) in correctly rounded fp64 steps; no completion leaves lambda
+// unchanged. Resets the accumulators for the next call.
+__global__ void dual_finish_kernel(unsigned long long* acc, int64_t* last, double eta,
+                                   double lambda_max, double* lambda) {
+  const int64_t n = (int64_t)acc[0], c = (int64_t)acc[1];
+  acc[0] = 0;
+  acc[1] = 0;
+  const int64_t dn = n - last[0], dc = c - last[1];
+  last[0] = n;
+  last[1] = c;
+  if (dn <= 0) return;
+  {
+    // one rounding per operation, as written (no fused multiply-add)
+#pragma clang fp contract(off)
+    const double cbar = (double)dc / (65536.0 * (double)dn);
+    double l = *lambda + eta * (cbar - 1.0);
+    l = l < 0.0 ? 0.0 : (l > lambda_max ? lambda_max : l);
+    *lambda = l;
+  }
+}
+
 }  // namespace
+
+hipError_t launch_dual_update(const int64_t* cnt, int64_t n_em, unsigned long long* acc, int64_t* last,
+                              double eta, double lambda_max, double* lambda, hipStream_t s) {
+  const int64_t want = (n_em + 255) / 256;
+  const unsigned blocks = (unsigned)(want < 1024 ? (want < 1 ? 1 : want) : 1024);
+  hipLaunchKernelGGL(dual_reduce_kernel, dim3(blocks), dim3(256), 0, s, cnt, n_em, acc);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(dual_finish_kernel, dim3(1), dim3(1), 0, s, acc, last, eta, lambda_max, lambda);
+  return hipGetLastError();
+}
 
 hipError_t launch_snapshot(const SchedArgs& a, int e0, int ne, hipStream_t s) {
   const int64_t n = (int64_t)ne * a.M;

@@ -7,7 +7,7 @@ import numpy as np
 import oracle
 import workload
 
-STATE_INT_KEYS = ("next_id", "arrived", "rej_nomodel", "qlen", "busy", "ewma", "backlog",
+STATE_INT_KEYS = ("next_id", "arrived", "rej_nomodel", "qlen", "busy", "ewma", "backlog", "cost_q16",
                   "cap", "enabled", "rej_overflow", "enqueued", "started", "completed",
                   "slo_met", "lat_sum", "wait_sum", "hist", "slots")
 
