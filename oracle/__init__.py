@@ -75,6 +75,8 @@ def _load():
         L.orc_gumbel.argtypes = [U32, U32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int]
         L.orc_gumbel.restype = ctypes.c_double
         L.orc_dual_update.argtypes = [P, ctypes.c_double, ctypes.c_double, P]
+        L.orc_set_rpm_limit.argtypes = [P, ctypes.c_int, ctypes.c_int, ctypes.c_int]
+        L.orc_read_rpm.argtypes = [P, P, P, P]
         _lib = L
     return _lib
 
@@ -229,6 +231,9 @@ class Oracle:
     def set_capacity(self, e, m, c):
         self._lib.orc_set_capacity(self.p, e, m, int(c))
 
+    def set_rpm_limit(self, e, m, r):
+        self._lib.orc_set_rpm_limit(self.p, e, m, int(r))
+
     def state(self) -> dict:
         """Snapshot as a dict of numpy arrays (common test representation)."""
         E, M, S, Qc, A = self.E, self.M, self.S, self.qcap, self.A
@@ -240,10 +245,15 @@ class Oracle:
         hist = np.zeros((E, A), np.int64)
         self._lib.orc_read_state(self.p, _ptr(env_i32), _ptr(env_i64), _ptr(mod), _ptr(slots),
                                  _ptr(queues), _ptr(hist))
+        rpm_lim = np.zeros((E, M), np.int32)
+        rpm_cnt = np.zeros((E, M), np.int32)
+        rpm_hist = np.zeros((E, M, 60), np.uint8)
+        self._lib.orc_read_rpm(self.p, _ptr(rpm_lim), _ptr(rpm_cnt), _ptr(rpm_hist))
         return dict(t=self.t, next_id=env_i32, arrived=env_i64[:, 0], rej_nomodel=env_i64[:, 1],
                     qlen=mod[..., 0], busy=mod[..., 1], ewma=mod[..., 2], backlog=mod[..., 3],
                     cap=mod[..., 4], enabled=mod[..., 5], rej_overflow=mod[..., 6],
                     enqueued=mod[..., 7], started=mod[..., 8], completed=mod[..., 9],
                     slo_met=mod[..., 10], lat_sum=mod[..., 11], wait_sum=mod[..., 12],
-                    cost_q16=mod[..., 13],
+                    cost_q16=mod[..., 13], rpm_limit=rpm_lim.astype(np.int64),
+                    rpm_count=rpm_cnt.astype(np.int64), rpm_hist=rpm_hist,
                     slots=slots, queues=queues, hist=hist)

@@ -45,6 +45,7 @@ namespace {
 
 // ----- limits of the boundary the oracle mirrors --------------------------
 const int kSvcMax = 4095;      // base service time must lie in [1, kSvcMax]
+const int kRpmWindow = 60;     // App. C: 60-second (tick) sliding window of dispatches
 
 enum ErrBits {
   ERR_QIDX = 1,      // q_idx outside [0, Q)
@@ -94,7 +95,20 @@ struct ModelState {
   int64_t rej_overflow = 0, enqueued = 0, started = 0, completed = 0,
           slo_met = 0, lat_sum = 0, wait_sum = 0;
   int64_t cost_q16 = 0;       // sum over completions of floor(2^16 latency / budget)
+  // Blackbox proxy (Sec. 5.5, App. C): with rpm_limit > 0 the model is an API
+  // behind a rate limit; every dispatch (a request entering a service slot)
+  // is timestamped, and a request is dispatched only while fewer than
+  // rpm_limit dispatches fall in the last kRpmWindow ticks.
+  int32_t rpm_limit = 0;
+  std::vector<int32_t> dispatch_ticks;
 };
+
+// Dispatches of a model at ticks in (t_end - kRpmWindow, t_end].
+int rpm_count(const ModelState& ms, int32_t t_end) {
+  int n = 0;
+  for (int32_t tau : ms.dispatch_ticks) n += (tau > t_end - kRpmWindow && tau <= t_end) ? 1 : 0;
+  return n;
+}
 
 struct EnvState {
   std::vector<ModelState> models;
@@ -160,7 +174,11 @@ void features(const orc_pool* p, const EnvState& env, int32_t q_idx, int32_t bud
     const int c = std::max(ms.cap, 1);
     const float inv_c = (float)(1.0 / c);
     const float inv_clat = (float)(1.0 / ((double)c * d.budget_max));
-    float f_q = (float)ms.queue.size() * inv_qcap;
+    // queue-depth signal: recent dispatches / RPM limit for a blackbox model
+    // (Sec. 5.5), the queue depth / QCAP otherwise; the window ends at the
+    // last completed tick (the route step reads the state after it)
+    float f_q = ms.rpm_limit > 0 ? (float)rpm_count(ms, p->t - 1) * (float)(1.0 / ms.rpm_limit)
+                                 : (float)ms.queue.size() * inv_qcap;
     float f_kv = (float)busy * inv_c;
     float f_lat = (float)ms.ewma_q8 * inv_lat;
     float f_bl = (float)ms.backlog * inv_clat;
@@ -391,9 +409,16 @@ void schedule_env(orc_pool* p, int e, int32_t n_total, const int32_t* off,
   // every busy slot by one tick of service.
   for (int m = 0; m < d.M; ++m) {
     ModelState& ms = env.models[m];
+    // forget dispatches that have left every window still to come
+    ms.dispatch_ticks.erase(std::remove_if(ms.dispatch_ticks.begin(), ms.dispatch_ticks.end(),
+                                           [t](int32_t tau) { return tau <= t - kRpmWindow; }),
+                            ms.dispatch_ticks.end());
+    int recent = ms.rpm_limit > 0 ? rpm_count(ms, t) : 0;   // dispatches in the window ending at t
     for (int s = 0; s < ms.cap && s < d.max_slots; ++s) {
       Slot& sl = ms.slots[s];
       if (sl.busy || ms.queue.empty()) continue;
+      if (ms.rpm_limit > 0 && recent >= ms.rpm_limit) break;   // held back: rate limit reached
+      if (ms.rpm_limit > 0) { ms.dispatch_ticks.push_back(t); ++recent; }
       Entry en = ms.queue.front();
       ms.queue.erase(ms.queue.begin());
       sl.busy = true; sl.id = en.id; sl.t_arr = en.t_arr; sl.rem = en.svc; sl.budget = en.budget;
@@ -548,6 +573,25 @@ void orc_round_bf16_array(const double* in, double* out, int64_t n) {
 
 void orc_set_enabled(orc_pool* p, int e, int m, int v) { p->envs[e].models[m].enabled = v ? 1 : 0; }
 void orc_set_capacity(orc_pool* p, int e, int m, int c) { p->envs[e].models[m].cap = c; }
+void orc_set_rpm_limit(orc_pool* p, int e, int m, int r) { p->envs[e].models[m].rpm_limit = r; }
+
+// Blackbox window export: limit, dispatches in the window ending at the last
+// completed tick, and the per-tick counts hist[k] of tick (t - 1 - k), k < 60.
+void orc_read_rpm(const orc_pool* p, int32_t* limit, int32_t* count, uint8_t* hist) {
+  const orc_desc& d = p->d;
+  for (int e = 0; e < d.E; ++e)
+    for (int m = 0; m < d.M; ++m) {
+      const ModelState& ms = p->envs[e].models[m];
+      const size_t em = (size_t)e * d.M + m;
+      limit[em] = ms.rpm_limit;
+      count[em] = rpm_count(ms, p->t - 1);
+      for (int k = 0; k < kRpmWindow; ++k) hist[em * kRpmWindow + k] = 0;
+      for (int32_t tau : ms.dispatch_ticks) {
+        const int k = p->t - 1 - tau;
+        if (k >= 0 && k < kRpmWindow) hist[em * kRpmWindow + k] += 1;
+      }
+    }
+}
 
 // State export in the oracle's own layout:
 //   env_i32 [E]      next_id
