@@ -204,6 +204,10 @@ typedef struct {
   int32_t qlen, busy, ewma_q8, backlog, capacity, enabled, _pad0, _pad1;
   int64_t rej_overflow, enqueued, started, completed, slo_met, lat_sum, wait_sum;
   int64_t cost_q16;         /* sum over completions of floor(2^16 latency / budget) */
+  int32_t rpm_limit;        /* blackbox rate limit per 60 ticks (0: not rate-limited)   */
+  int32_t rpm_count;        /* dispatches in the 60 ticks up to the last completed tick */
+  uint8_t rpm_hist[60];     /* rpm_hist[k]: dispatches at tick (tick - 1 - k)           */
+  int32_t _pad2;
 } im_model_state;
 
 typedef struct {
@@ -241,10 +245,21 @@ im_status im_dual_update(im_pool* pool, double eta, double lambda_max, double* l
 
 /* Host knobs (stream-ordered): take a model out of routing, or change its
  * number of service slots (requests in slots >= the new capacity finish but
- * are not replaced). */
+ * are not replaced), or make it a blackbox (API) model with a rate limit
+ * (Sec. 5.5, App. C): with rpm_limit > 0 a queued request enters a free slot
+ * only while fewer than rpm_limit requests entered its slots in the last 60
+ * ticks (the rest wait in its queue), and its queue-depth feature becomes
+ * (requests dispatched in the last 60 ticks) * fp32(1 / rpm_limit) instead of
+ * queue length / queue_cap. 0 restores the white-box model; dispatches stop
+ * being recorded and the window empties as they age out. rpm_limit in
+ * [0, 2^30]. The first limit > 0 set on a pool switches its schedule step to
+ * the variant that tracks the windows; schedule calls captured into a graph
+ * before that keep the variant they were captured with. */
 im_status im_set_enabled(im_pool* pool, int32_t env, int32_t model, int32_t enabled, void* stream);
 im_status im_set_capacity(im_pool* pool, int32_t env, int32_t model, int32_t capacity,
                           void* stream);
+im_status im_set_rpm_limit(im_pool* pool, int32_t env, int32_t model, int32_t rpm_limit,
+                           void* stream);
 
 /* Sticky device error word (IM_ERR_* bits). Synchronises. Returns IM_EDEVICE
  * when non-zero. im_clear_error zeroes it. */

@@ -11,7 +11,8 @@ from ._lib import (EXPORTED, IMError, im_clear_error, im_destroy, im_dual_update
                    im_get_error,
                    im_last_error, im_pool_create, im_read_state, im_route, im_route_sample,
                    im_schedule,
-                   im_set_capacity, im_set_enabled, im_tick, im_write_state, make_arrivals,
+                   im_set_capacity, im_set_enabled, im_set_rpm_limit, im_tick, im_write_state,
+                   make_arrivals,
                    make_desc)
 
 
@@ -66,6 +67,9 @@ class Pool:
 
     def set_capacity(self, e, m, c, stream=None):
         im_set_capacity(self.h, e, m, c, stream)
+
+    def set_rpm_limit(self, e, m, r, stream=None):
+        im_set_rpm_limit(self.h, e, m, r, stream)
 
     def error(self) -> int:
         return im_get_error(self.h)

@@ -21,7 +21,7 @@ KEY_MODES = {"slack": 0, "deadline": 1, "fcfs": 2}
 IM_ERR_QIDX, IM_ERR_COUNT, IM_ERR_BUDGET, IM_ERR_SVC, IM_ERR_ACTION = 1, 2, 4, 8, 16
 
 EXPORTED = ("im_pool_create", "im_route", "im_route_sample", "im_schedule", "im_tick", "im_destroy",
-            "im_dual_update",
+            "im_dual_update", "im_set_rpm_limit",
             "im_read_state", "im_write_state", "im_set_enabled", "im_set_capacity",
             "im_get_error", "im_clear_error", "im_last_error")
 
@@ -55,10 +55,11 @@ MODEL_DT = np.dtype([("qlen", "<i4"), ("busy", "<i4"), ("ewma_q8", "<i4"), ("bac
                      ("capacity", "<i4"), ("enabled", "<i4"), ("_p0", "<i4"), ("_p1", "<i4"),
                      ("rej_overflow", "<i8"), ("enqueued", "<i8"), ("started", "<i8"),
                      ("completed", "<i8"), ("slo_met", "<i8"), ("lat_sum", "<i8"),
-                     ("wait_sum", "<i8"), ("cost_q16", "<i8")])
+                     ("wait_sum", "<i8"), ("cost_q16", "<i8"), ("rpm_limit", "<i4"),
+                     ("rpm_count", "<i4"), ("rpm_hist", "u1", (60,)), ("_p3", "<i4")])
 ENV_DT = np.dtype([("arrived", "<i8"), ("rej_nomodel", "<i8"), ("next_id", "<i4"), ("_p", "<i4")])
 assert ENTRY_DT.itemsize == 16 and SLOT_DT.itemsize == 16
-assert MODEL_DT.itemsize == 96 and ENV_DT.itemsize == 24
+assert MODEL_DT.itemsize == 168 and ENV_DT.itemsize == 24
 
 _lib = None
 
@@ -87,6 +88,7 @@ def load() -> ctypes.CDLL:
     L.im_write_state.argtypes = [P, I32, I32, I32, P, P, P, P, P]
     L.im_set_enabled.argtypes = [P, I32, I32, I32, P]
     L.im_set_capacity.argtypes = [P, I32, I32, I32, P]
+    L.im_set_rpm_limit.argtypes = [P, I32, I32, I32, P]
     L.im_get_error.argtypes = [P, ctypes.POINTER(I32)]
     L.im_clear_error.argtypes = [P]
     L.im_last_error.argtypes = [P]
@@ -213,6 +215,10 @@ def im_set_capacity(pool, env, model, capacity, stream=None):
     _check(load().im_set_capacity(pool, env, model, int(capacity), _stream(stream)), pool)
 
 
+def im_set_rpm_limit(pool, env, model, rpm_limit, stream=None):
+    _check(load().im_set_rpm_limit(pool, env, model, int(rpm_limit), _stream(stream)), pool)
+
+
 def im_get_error(pool) -> int:
     bits = ctypes.c_int32(0)
     st = load().im_get_error(pool, ctypes.byref(bits))
@@ -259,8 +265,9 @@ def im_read_state(pool, env_begin: int, env_count: int, M: int, A: int, S: int, 
                  ("cap", "capacity"), ("enabled", "enabled"), ("rej_overflow", "rej_overflow"),
                  ("enqueued", "enqueued"), ("started", "started"), ("completed", "completed"),
                  ("slo_met", "slo_met"), ("lat_sum", "lat_sum"), ("wait_sum", "wait_sum"),
-                 ("cost_q16", "cost_q16")):
+                 ("cost_q16", "cost_q16"), ("rpm_limit", "rpm_limit"), ("rpm_count", "rpm_count")):
         out[k] = md[f].astype(np.int64)
+    out["rpm_hist"] = md["rpm_hist"].copy()
     return out
 
 
@@ -277,8 +284,9 @@ def im_write_state(pool, env_begin: int, s: dict):
                  ("cap", "capacity"), ("enabled", "enabled"), ("rej_overflow", "rej_overflow"),
                  ("enqueued", "enqueued"), ("started", "started"), ("completed", "completed"),
                  ("slo_met", "slo_met"), ("lat_sum", "lat_sum"), ("wait_sum", "wait_sum"),
-                 ("cost_q16", "cost_q16")):
+                 ("cost_q16", "cost_q16"), ("rpm_limit", "rpm_limit"), ("rpm_count", "rpm_count")):
         models[f] = s[k]
+    models["rpm_hist"] = s["rpm_hist"]
     slots = np.zeros((E, M, S), SLOT_DT)
     for i, f in enumerate(("id", "t_arr", "rem", "budget")):
         slots[f] = s["slots"][..., i]

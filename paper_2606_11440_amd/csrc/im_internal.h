@@ -19,11 +19,15 @@ struct alignas(64) ModelRec {
                                        // (kept in the env's first record only)
   int32_t busy_mask;                   // bit s: slot s busy
   int32_t next_done;                   // earliest completion tick of a busy slot
-  int32_t pad3, pad4, pad5;
+  int32_t rpm_limit;                   // blackbox rate limit per kRpmWindow ticks (0: none)
+  int32_t rpm_count;                   // dispatches in the last kRpmWindow ticks
+  float inv_rpm;                       // 1 / rpm_limit rounded once to fp32
 };
 static_assert(sizeof(ModelRec) == 64, "ModelRec layout");
 
 constexpr int kFront = 64;       // front capacity (one entry per lane)
+constexpr int kRpmWindow = 60;   // blackbox dispatch window (ticks; App. C: 60 s)
+constexpr int kRpmRing = 64;     // bytes per (env, model) of the per-tick dispatch ring
 
 // Per-env snapshot row read by the route step, written by the schedule step
 // (and by snapshot_kernel after host-side state changes): the 4M load-stat
@@ -91,6 +95,7 @@ struct SchedArgs {
   int4* slots;        // [E*M*S]
   int4* front;        // [E*M*kFront]
   int4* pool;         // [E*M*qcap]
+  uint8_t* rpm_ring;  // [E*M*kRpmRing]: dispatches at tick tau in byte tau % kRpmWindow
   int32_t* err;
   float* snap;        // [E * snap_stride(M)]
   float inv_qcap, inv_lat;
@@ -105,7 +110,8 @@ hipError_t launch_dual_update(const int64_t* cnt, int64_t n_em, unsigned long lo
 bool route_supported(int dtype, int hidden, int n_layers, int out_tiles);
 hipError_t launch_route(const RouteArgs& a, int dtype, int hidden, int n_layers, int out_tiles,
                         hipStream_t s);
-hipError_t launch_schedule(const SchedArgs& a, hipStream_t s);
+// rpm: some model of the pool is (or was) rate-limited (blackbox windows tracked)
+hipError_t launch_schedule(const SchedArgs& a, bool rpm, hipStream_t s);
 // Recompute the snapshot rows of envs [e0, e0 + ne) from the model records.
 hipError_t launch_snapshot(const SchedArgs& a, int e0, int ne, hipStream_t s);
 

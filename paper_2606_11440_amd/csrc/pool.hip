@@ -34,6 +34,7 @@ struct im_pool {
   int4* slots = nullptr;
   int4* front = nullptr;
   int4* qpool = nullptr;
+  uint8_t* rpm_ring = nullptr;              // [E*M*kRpmRing] per-tick dispatches, tick % 60
   float* snap = nullptr;
   int32_t* err = nullptr;
   int32_t* act_buf = nullptr;
@@ -42,6 +43,7 @@ struct im_pool {
   int64_t* dual_last = nullptr;             // [2] totals at the previous dual update
   int32_t t = 0;
   int32_t cu_count = 0;
+  bool rpm_active = false;   // some model was given a rate limit (the windows are tracked from then on)
   std::string last_error;
 };
 
@@ -102,6 +104,13 @@ im_status zalloc(im_pool* p, T** dst, size_t n) {
 }
 
 __global__ void set_field_kernel(int32_t* ptr, int32_t v) { *ptr = v; }
+__global__ void set_rpm_kernel(ModelRec* r, int32_t limit, float inv) {
+  r->rpm_limit = limit;
+  r->inv_rpm = inv;
+}
+
+// Ring byte of tick tau (the device keeps the dispatches of tick tau at tau % 60).
+inline int rpm_slot(int64_t tau) { return (int)(((tau % im::kRpmWindow) + im::kRpmWindow) % im::kRpmWindow); }
 
 im_status check_arrivals(im_pool* p, const im_arrivals* arr) {
   if (!arr) return fail(p, IM_EINVAL, "arrivals is NULL");
@@ -120,7 +129,8 @@ void free_pool(im_pool* p) {
     if (p->bias[l]) (void)hipFree(p->bias[l]);
   }
   void* bufs[] = {p->inv_tab, p->ms, p->cnt, p->env_cnt, p->hist, p->slots,
-                  p->front, p->qpool, p->snap, p->err, p->act_buf, p->dual_acc, p->dual_last};
+                  p->front, p->qpool, p->snap, p->err, p->act_buf, p->dual_acc, p->dual_last,
+                  p->rpm_ring};
   for (void* b : bufs) if (b) (void)hipFree(b);
   delete p;
 }
@@ -261,6 +271,7 @@ im_status im_pool_create(const im_pool_desc* desc, const float* const* W, const 
   }
   if (st == IM_OK) st = zalloc(p, &p->front, EM * im::kFront);
   if (st == IM_OK) st = zalloc(p, &p->qpool, EM * (size_t)d.queue_cap);
+  if (st == IM_OK) st = zalloc(p, &p->rpm_ring, EM * (size_t)im::kRpmRing);
   if (st == IM_OK) st = zalloc(p, &p->snap, (size_t)d.n_envs * im::snap_stride(d.n_models));
   if (st == IM_OK) st = zalloc(p, &p->err, 1);
   if (st == IM_OK) st = zalloc(p, &p->dual_acc, 2);
@@ -364,7 +375,7 @@ im_status im_schedule(im_pool* p, const im_arrivals* arr, const int32_t* actions
   a.base_svc = arr->base_svc;
   a.actions = actions;
   a.n_total = arr->n_total;
-  IM_HIP(p, im::launch_schedule(a, (hipStream_t)stream));
+  IM_HIP(p, im::launch_schedule(a, p->rpm_active, (hipStream_t)stream));
   p->t += 1;
   return IM_OK;
 }
@@ -387,6 +398,7 @@ static im::SchedArgs sched_args(im_pool* p) {
   a.slots = p->slots;
   a.front = p->front;
   a.pool = p->qpool;
+  a.rpm_ring = p->rpm_ring;
   a.err = p->err;
   a.snap = p->snap;
   a.inv_qcap = p->inv_qcap;
@@ -433,6 +445,20 @@ im_status im_set_capacity(im_pool* p, int32_t env, int32_t model, int32_t capaci
   if (capacity < 0 || capacity > p->S) return fail(p, IM_EINVAL, "capacity outside [0, max_slots]");
   ModelRec* r = p->ms + (size_t)env * p->d.n_models + model;
   hipLaunchKernelGGL(set_field_kernel, dim3(1), dim3(1), 0, (hipStream_t)stream, &r->cap, capacity);
+  IM_HIP(p, hipGetLastError());
+  IM_HIP(p, im::launch_snapshot(sched_args(p), env, 1, (hipStream_t)stream));
+  return IM_OK;
+}
+
+im_status im_set_rpm_limit(im_pool* p, int32_t env, int32_t model, int32_t rpm_limit, void* stream) {
+  if (!p) return fail(nullptr, IM_EINVAL, "pool is NULL");
+  if (env < 0 || env >= p->d.n_envs || model < 0 || model >= p->d.n_models)
+    return fail(p, IM_EINVAL, "env/model out of range");
+  if (rpm_limit < 0 || rpm_limit > (1 << 30)) return fail(p, IM_EINVAL, "rpm_limit outside [0, 2^30]");
+  ModelRec* r = p->ms + (size_t)env * p->d.n_models + model;
+  const float inv = rpm_limit > 0 ? (float)(1.0 / rpm_limit) : 0.f;   // rounded once from fp64
+  if (rpm_limit > 0) p->rpm_active = true;
+  hipLaunchKernelGGL(set_rpm_kernel, dim3(1), dim3(1), 0, (hipStream_t)stream, r, rpm_limit, inv);
   IM_HIP(p, hipGetLastError());
   IM_HIP(p, im::launch_snapshot(sched_args(p), env, 1, (hipStream_t)stream));
   return IM_OK;
@@ -496,7 +522,15 @@ im_status im_read_state(im_pool* p, int32_t env_begin, int32_t env_count, int32_
       o.started = c[im::C_STARTED]; o.completed = c[im::C_COMPLETED]; o.slo_met = c[im::C_SLO_MET];
       o.lat_sum = c[im::C_LAT_SUM]; o.wait_sum = c[im::C_WAIT_SUM];
       o.cost_q16 = c[im::C_COST_Q16];
+      o.rpm_limit = recs[i].rpm_limit;
+      o.rpm_count = recs[i].rpm_count;
     }
+    std::vector<uint8_t> ring(EMc * im::kRpmRing);
+    if (EMc)
+      IM_HIP(p, hipMemcpy(ring.data(), p->rpm_ring + em0 * im::kRpmRing, ring.size(), hipMemcpyDeviceToHost));
+    for (size_t i = 0; i < EMc; ++i)
+      for (int k = 0; k < im::kRpmWindow; ++k)
+        models[i].rpm_hist[k] = (int64_t)p->t - 1 - k >= 0 ? ring[i * im::kRpmRing + rpm_slot((int64_t)p->t - 1 - k)] : 0;
   }
   if (slots && EMc) {
     // The device keeps a busy slot's completion tick; the state reports the
@@ -558,6 +592,7 @@ im_status im_write_state(im_pool* p, int32_t env_begin, int32_t env_count, int32
   std::vector<ModelRec> recs(EMc);
   std::memset(recs.data(), 0, EMc * sizeof(ModelRec));
   std::vector<int64_t> cnt(EMc * im::C_NUM, 0);
+  std::vector<uint8_t> ring(EMc * im::kRpmRing, 0);
   std::vector<int4> fr(EMc * im::kFront, make_int4(0, 0, 0, 0));
   std::vector<int4> pl(EMc * (size_t)qcap, make_int4(0, 0, 0, 0));
   std::vector<int4> sl(EMc * S);
@@ -610,6 +645,20 @@ im_status im_write_state(im_pool* p, int32_t env_begin, int32_t env_count, int32
     c[im::C_STARTED] = ms.started; c[im::C_COMPLETED] = ms.completed; c[im::C_SLO_MET] = ms.slo_met;
     c[im::C_LAT_SUM] = ms.lat_sum; c[im::C_WAIT_SUM] = ms.wait_sum;
     c[im::C_COST_Q16] = ms.cost_q16;
+    if (ms.rpm_limit < 0 || ms.rpm_limit > (1 << 30)) return fail(p, IM_ESTATE, "rpm_limit out of range");
+    int hsum = 0;
+    for (int k = 0; k < im::kRpmWindow; ++k) {
+      hsum += ms.rpm_hist[k];
+      if ((int64_t)tick - 1 - k >= 0)
+        ring[i * im::kRpmRing + rpm_slot((int64_t)tick - 1 - k)] = ms.rpm_hist[k];
+      else if (ms.rpm_hist[k] != 0)
+        return fail(p, IM_ESTATE, "dispatches before tick 0");
+    }
+    if (hsum != ms.rpm_count) return fail(p, IM_ESTATE, "rpm_count != sum of rpm_hist");
+    r.rpm_limit = ms.rpm_limit;
+    r.rpm_count = ms.rpm_count;
+    if (ms.rpm_limit > 0 || ms.rpm_count > 0) p->rpm_active = true;
+    r.inv_rpm = ms.rpm_limit > 0 ? (float)(1.0 / ms.rpm_limit) : 0.f;
   }
   std::vector<int64_t> ec((size_t)env_count * 2);
   for (int e = 0; e < env_count; ++e) { ec[2 * e] = envs[e].arrived; ec[2 * e + 1] = envs[e].rej_nomodel; }
@@ -620,6 +669,7 @@ im_status im_write_state(im_pool* p, int32_t env_begin, int32_t env_count, int32
     IM_HIP(p, hipMemcpy(p->front + em0 * im::kFront, fr.data(), fr.size() * sizeof(int4), hipMemcpyHostToDevice));
     IM_HIP(p, hipMemcpy(p->qpool + em0 * qcap, pl.data(), pl.size() * sizeof(int4), hipMemcpyHostToDevice));
     IM_HIP(p, hipMemcpy(p->slots + em0 * S, sl.data(), sl.size() * sizeof(int4), hipMemcpyHostToDevice));
+    IM_HIP(p, hipMemcpy(p->rpm_ring + em0 * im::kRpmRing, ring.data(), ring.size(), hipMemcpyHostToDevice));
   }
   if (env_count) {
     IM_HIP(p, hipMemcpy(p->env_cnt + (size_t)env_begin * 2, ec.data(), ec.size() * 8, hipMemcpyHostToDevice));

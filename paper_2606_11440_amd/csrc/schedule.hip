@@ -198,13 +198,21 @@ __device__ void refill(Queue& q, int4& fe, int4* pool, int64_t* pk, int32_t* pi,
 // Snapshot row entry of model m of env e from its state (one fp32 product
 // per load statistic; validity byte). `part` selects which value to write
 // (0..3: the four statistics, 4: validity), so lanes can share the work.
+// The queue-depth statistic: recent dispatches / RPM limit for a blackbox
+// model (Sec. 5.5), queue length / QCAP otherwise.
+__device__ __forceinline__ float queue_stat(const SchedArgs& a, int32_t qlen, int32_t rpm,
+                                            int32_t rcnt, float inv_rpm) {
+  return rpm > 0 ? (float)rcnt * inv_rpm : (float)qlen * a.inv_qcap;
+}
+
 __device__ __forceinline__ void write_snap_part(const SchedArgs& a, int e, int m, int part,
                                                 int32_t qlen, int32_t busy, int32_t ewma,
-                                                int32_t backlog, int32_t cap, int32_t enabled) {
+                                                int32_t backlog, int32_t cap, int32_t enabled,
+                                                int32_t rpm, int32_t rcnt, float inv_rpm) {
   float* row = a.snap + (size_t)e * snap_stride(a.M);
   const int c = cap < 0 ? 0 : (cap > IM_MAX_SLOTS ? IM_MAX_SLOTS : cap);
   switch (part) {
-    case 0: row[m] = (float)qlen * a.inv_qcap; break;
+    case 0: row[m] = queue_stat(a, qlen, rpm, rcnt, inv_rpm); break;
     case 1: row[a.M + m] = (float)busy * a.inv_tab[c]; break;
     case 2: row[2 * a.M + m] = (float)ewma * a.inv_lat; break;
     case 3: row[3 * a.M + m] = (float)backlog * a.inv_tab[IM_MAX_SLOTS + 1 + c]; break;
@@ -224,7 +232,8 @@ __global__ void snapshot_kernel(SchedArgs a, int e0, int ne) {
   const int e = (int)(em / a.M), m = (int)(em - (int64_t)e * a.M);
   const ModelRec r = a.ms[em];
   for (int part = 0; part < 5; ++part)
-    write_snap_part(a, e, m, part, r.qlen, r.busy, r.ewma, r.backlog, r.cap, r.enabled);
+    write_snap_part(a, e, m, part, r.qlen, r.busy, r.ewma, r.backlog, r.cap, r.enabled,
+                    r.rpm_limit, r.rpm_count, r.inv_rpm);
 }
 
 __device__ __forceinline__ int32_t wave_sum32(int32_t v) {
@@ -238,18 +247,24 @@ constexpr int kStageChunks = 4;   // arrival chunks (of 64) staged in LDS per ro
 // Per-model state of the env, one model per lane (lane m: model m) in
 // registers for the whole tick; read wave-uniformly with readlane.
 struct LaneState {
-  int32_t qlen, busy, ewma, backlog, cap, enabled, fh, fn, P, busy_mask, next_done;
+  int32_t qlen, busy, ewma, backlog, fh, fn, P, busy_mask, next_done;
+  int32_t rcnt;         // blackbox: dispatches in the window (limit and 1 / limit: LDS)
 };
 
 __device__ __forceinline__ int32_t rl(int32_t v, int m) { return __builtin_amdgcn_readlane(v, m); }
 
 // Inputs of one model fetched ahead of its turn: the live front window
-// (lane i: front[fh + i]), its slots (lane s < S) and counters (lane c).
+// (lane i: front[fh + i]) and its slots (lane s < S).
 struct ModelIn {
   int4 front;
   int4 slot;
-  int64_t cnt;
 };
+
+// Adds v to a 64-bit counter without reading it back (a vector atomic whose
+// result is unused: no wait, and integer sums do not depend on the order).
+__device__ __forceinline__ void counter_add(int64_t* p, int64_t v) {
+  atomicAdd(reinterpret_cast<unsigned long long*>(p), (unsigned long long)v);
+}
 
 // One wave per env. Every load that does not depend on the arrivals (the
 // model records, one per lane) is issued with the offsets; the env's arrivals
@@ -260,13 +275,22 @@ struct ModelIn {
 // sorted segment (a segmented sort), staged in LDS. The models are then
 // processed in order with the next model's front, slots and counters already
 // in flight: merge its segments into the queue, serve its slots, write back.
-// Record, counter, histogram and snapshot updates are plain stores of values
-// held in registers (no read-modify-write round trips).
+// Record and snapshot updates are plain stores of values held in registers;
+// counters and the histogram are added to with atomics whose result is unused
+// (no read-modify-write round trips).
+// RPM: the pool has (or had) a rate-limited model, so the blackbox dispatch
+// windows are tracked; pools that never had one run without that code.
+template <bool RPM>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void schedule_kernel(SchedArgs a) {
   __shared__ int4 stage[4][kStageChunks * 64];
   __shared__ int32_t hist_lds[4][IM_MAX_ACTIONS];
   __shared__ int32_t svc_lds[4][IM_MAX_MODELS];
   __shared__ int32_t acc_lds[4][IM_MAX_MODELS];
+  // per-model fields the tick does not change: rpm limit, 1 / limit, capacity, enabled
+  __shared__ int32_t rpm_lds[4][IM_MAX_MODELS];
+  __shared__ float inv_rpm_lds[4][IM_MAX_MODELS];
+  __shared__ int32_t cap_lds[4][IM_MAX_MODELS];
+  __shared__ int32_t en_lds[4][IM_MAX_MODELS];
   __shared__ int64_t pend_k[4][kFront];   // refill candidate staging
   __shared__ int32_t pend_i[4][kFront];
   __shared__ int2 pend_kb[4][4 * kFront];
@@ -337,8 +361,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
 
   LaneState L;
   L.qlen = r0.x; L.busy = r0.y; L.ewma = r0.z; L.backlog = r0.w;
-  L.cap = r1.x; L.enabled = r1.y; L.fh = r1.z; L.fn = r1.w;
+  L.fh = r1.z; L.fn = r1.w;
+  int32_t* cap_s = cap_lds[wv];
+  int32_t* en_s = en_lds[wv];
+  if (lane < M) { cap_s[lane] = r1.x; en_s[lane] = r1.y; }
   L.P = r2.x; L.busy_mask = r2.w; L.next_done = r3.x;
+  L.rcnt = RPM ? r3.z : 0;
+  const int32_t rpm_l = RPM && lane < M ? r3.y : 0;   // lane m: model m's limit (0: not a blackbox model)
+  int32_t* rpm_s = rpm_lds[wv];
+  float* inv_rpm_s = inv_rpm_lds[wv];
+  if (RPM && lane < M) { rpm_s[lane] = r3.y; inv_rpm_s[lane] = __int_as_float(r3.w); }
   // The tick and the next request id live in the env's first record in
   // device memory, so a captured sequence of ticks replays with the right time.
   const int32_t next_id = rl(r2.y, 0);
@@ -365,6 +397,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
       }
     }
     if (lane < M && L.busy_mask != 0) recs[lane].next_done = L.next_done + 1;
+    // a tracked window still slides: the dispatches of tick t - 60 leave it
+    if (RPM && lane < M && (rpm_l > 0 || L.rcnt > 0)) {
+      uint8_t* rb = a.rpm_ring + ((size_t)e * M + lane) * kRpmRing + (t % kRpmWindow);
+      const int32_t rold = *rb;
+      if (rold != 0) {
+        *rb = 0;
+        recs[lane].rpm_count = L.rcnt - rold;
+        a.snap[(size_t)e * snap_stride(M) + lane] = queue_stat(a, L.qlen, rpm_l, L.rcnt - rold, __int_as_float(r3.w));
+      }
+    }
     return;
   }
 
@@ -437,20 +479,22 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     if (lane < IM_MAX_MODELS) { acc_s[lane] = 0; svc_s[lane] = 0; }   // LDS accesses of one wave stay in order
 
     // What each model touches this round (lane m): its front (newcomers to
-    // insert, or slots to fill), its slots (fills or a completion due) and its
-    // counters. A model needing none of them is settled from its registers.
-    const int capc_l = L.cap < S ? (L.cap < 0 ? 0 : L.cap) : S;
+    // insert, or slots to fill), its slots (fills or a completion due), its
+    // counters (anything routed, started or completed) and its blackbox window.
+    // A model needing none of them is settled from its registers.
+    const int32_t cap_l = lane < M ? cap_s[lane] : 0;
+    const int capc_l = cap_l < S ? (cap_l < 0 ? 0 : cap_l) : S;
     const uint32_t free_l = ~(uint32_t)L.busy_mask & ((1u << capc_l) - 1u);
     const bool pops_l = last && free_l != 0 && L.qlen + acc_round_l > 0;
     const bool due_l = last && L.busy_mask != 0 && L.next_done <= t;
     const uint64_t need_front = ballot(lane < M && (acc_round_l > 0 || pops_l));
     const uint64_t need_slots = ballot(lane < M && (pops_l || due_l));
-    const uint64_t need_cnt = ballot(lane < M && last && (prior_l != 0 || pops_l || due_l));
+    // a window with dispatches in it, or of a rate-limited model, slides every tick
+    const uint64_t need_rpm = RPM ? ballot(lane < M && last && (rpm_l > 0 || L.rcnt > 0)) : 0ull;
     auto fetch = [&](int mm, ModelIn& in) {
       const size_t em = (size_t)e * M + mm;
       in.front = make_int4(0, 0, 0, 0);
       in.slot = make_int4(-1, 0, 0, 0);
-      in.cnt = 0;
       if ((need_front >> mm) & 1ull) {
         const int fh = rl(L.fh, mm), fn = rl(L.fn, mm);
         if (lane < fn) in.front = a.front[em * kFront + fh + lane];   // fh + fn <= kFront
@@ -458,14 +502,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
       if ((need_slots >> mm) & 1ull) {
         if (lane < S) in.slot = a.slots[em * S + lane];
       }
-      if ((need_cnt >> mm) & 1ull) {
-        if (lane < C_NUM) in.cnt = a.cnt[em * C_NUM + lane];
-      }
     };
     if (r > 0) wave_mem_sync();   // the fronts written in the previous round
     // ---- per model with work this round, in model order: insert its sorted
     // segments, serve, write back (the next such model's inputs in flight) ----
-    const uint64_t busy_models = need_front | need_slots | need_cnt;
+    const uint64_t busy_models =
+        need_front | need_slots | need_rpm | ballot(lane < M && last && prior_l != 0);
     ModelIn nxt;
     fetch(0, nxt);
     for (int m = 0; m < M; ++m) {
@@ -475,7 +517,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
       const size_t em = (size_t)e * M + m;
       Queue q;
       q.qlen = rl(L.qlen, m); q.busy = rl(L.busy, m); q.ewma = rl(L.ewma, m);
-      q.backlog = rl(L.backlog, m); q.cap = rl(L.cap, m); q.enabled = rl(L.enabled, m);
+      q.backlog = rl(L.backlog, m); q.cap = __builtin_amdgcn_readfirstlane(cap_s[m]);
+      q.enabled = __builtin_amdgcn_readfirstlane(en_s[m]);
       q.fh = rl(L.fh, m); q.fn = rl(L.fn, m); q.P = rl(L.P, m);
       q.busy_mask = rl(L.busy_mask, m); q.next_done = rl(L.next_done, m);
       int4* front = a.front + em * kFront;
@@ -529,9 +572,22 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
       }
 
       // ---- service: fill free slots below c_m from the queue head ----
+      // A blackbox model dispatches only while its window (ticks t-59..t)
+      // holds fewer than rpm dispatches (App. C): the rest wait in the queue.
+      const int32_t rpm = RPM ? __builtin_amdgcn_readfirstlane(rpm_s[m]) : 0;
+      // Dispatches are recorded while the model is rate-limited; a window with
+      // dispatches in it keeps sliding (also after its limit is lifted).
+      const int32_t rcnt0 = RPM ? rl(L.rcnt, m) : 0;
+      const bool track = RPM && (rpm > 0 || rcnt0 > 0);
+      // dispatches of tick t - kRpmWindow, leaving the window now
+      const int32_t rold = track ? __builtin_amdgcn_readfirstlane(
+                                       (int32_t)a.rpm_ring[em * kRpmRing + (t % kRpmWindow)])
+                                 : 0;
+      const int32_t window = rcnt0 - rold;
+      const int32_t allowed = rpm > 0 ? (rpm > window ? rpm - window : 0) : 0x7fffffff;
       const int capc = q.cap < S ? (q.cap < 0 ? 0 : q.cap) : S;
       const uint32_t free_m = ~(uint32_t)q.busy_mask & ((1u << capc) - 1u);
-      const bool pops = free_m != 0 && q.qlen > 0;
+      const bool pops = free_m != 0 && q.qlen > 0 && allowed > 0;
       const bool due = q.busy_mask != 0 && q.next_done <= t;
       int32_t started = 0, wait_add = 0, svc_out = 0;
       int32_t completed = 0, slo_add = 0, lat_add = 0;
@@ -541,14 +597,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         int4 sl = cur.slot;
         if (pops) {
           uint64_t empty = (uint64_t)free_m;
-          while (empty != 0 && q.qlen > 0) {
+          while (empty != 0 && q.qlen > 0 && started < allowed) {
             if (q.fn == 0) {
               refill(q, fe, pool, pend_k[wv], pend_i[wv], pend_kb[wv], a.key_mode);
               fe_base = 0;
               dirty = true;
             }
             if (q.fn == 0) break;   // unreachable while qlen == fn + P holds; never spin
-            const int need = popc64(empty);
+            int need = popc64(empty);
+            need = need < allowed - started ? need : allowed - started;
             const int take = need < q.fn ? need : q.fn;
             const int rnk = prefix_count(empty);
             const bool mine_slot = ((empty >> lane) & 1ull) && rnk < take;
@@ -587,13 +644,26 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
           dm &= dm - 1;
           const int32_t ls = rl(lat, s);
           lat_add += ls;
-          // cost latency / budget of Eq. 2 in Q16 (budget >= 1)
-          cost_add += (int64_t)(((uint64_t)(uint32_t)ls << 16) / (uint32_t)rl(sl.w, s));
           const int64_t delta = (int64_t)ls * 256 - ewma;
           const int64_t stepv = delta >= 0 ? (delta >> 3) : -((-delta + 7) >> 3);
           ewma = (int32_t)(ewma + stepv);
         }
         completed = popc64(done_mask);
+        if (done_mask) {
+          // cost latency / budget of Eq. 2 in Q16 (budget >= 1), one division
+          // per completed slot lane at once; 32 bits while latency < 2^16
+          uint64_t cq = 0;
+          if (done) {
+            const uint32_t bud = (uint32_t)sl.w;
+            cq = lat < 65536 ? (uint64_t)(((uint32_t)lat << 16) / bud)
+                             : ((uint64_t)(uint32_t)lat << 16) / bud;
+          }
+          int64_t cs = (int64_t)cq;               // sum over the slot lanes (S <= 8)
+          cs += xshfl<1>(cs);
+          cs += xshfl<2>(cs);
+          cs += xshfl<4>(cs);
+          cost_add = readlane64(cs, 0);
+        }
         slo_add = popc64(ballot(done && lat <= sl.w));
         if (done) sl = make_int4(-1, 0, 0, 0);
         const uint64_t bm = ballot(lane < S && sl.x >= 0);
@@ -612,6 +682,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
       // ---- write back what changed ----
       if (dirty && lane >= q.fh - fe_base && lane < q.fh - fe_base + q.fn)
         front[fe_base + lane] = fe;   // the live window [fh, fh + fn)
+      const int32_t rec = rpm > 0 ? started : 0;   // this tick's recorded dispatches
+      const int32_t rcnt_new = window + rec;
+      if (track && lane == 0 && rec != rold) a.rpm_ring[em * kRpmRing + (t % kRpmWindow)] = (uint8_t)rec;
       const int32_t routed_m = rl(prior_l, m);
       const int32_t acc_m = rl(acc_l, m);
       if (routed_m != 0 || started != 0 || completed != 0) {
@@ -627,12 +700,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
           case C_COST_Q16: add = cost_add; break;
           default: break;
         }
-        if (add != 0) a.cnt[em * C_NUM + lane] = cur.cnt + add;
+        if (add != 0) counter_add(a.cnt + em * C_NUM + lane, add);
       }
       if (lane == m) {
-        chg |= (q.qlen != L.qlen || q.busy != L.busy || q.ewma != L.ewma || q.backlog != L.backlog ? 1 : 0) |
+        chg |= (q.qlen != L.qlen || q.busy != L.busy || q.ewma != L.ewma || q.backlog != L.backlog ||
+                rcnt_new != L.rcnt ? 1 : 0) |
                (q.fh != L.fh || q.fn != L.fn ? 2 : 0) | (q.P != L.P || q.busy_mask != L.busy_mask ? 4 : 0) |
-               (q.next_done != L.next_done ? 8 : 0);
+               (q.next_done != L.next_done || rcnt_new != L.rcnt ? 8 : 0);
+        L.rcnt = rcnt_new;
         L.qlen = q.qlen; L.busy = q.busy; L.ewma = q.ewma; L.backlog = q.backlog;
         L.fh = q.fh; L.fn = q.fn; L.P = q.P; L.busy_mask = q.busy_mask; L.next_done = q.next_done;
       }
@@ -643,14 +718,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
   if (lane < M) {
     int4* rp = reinterpret_cast<int4*>(recs + lane);
     if (chg & 1) rp[0] = make_int4(L.qlen, L.busy, L.ewma, L.backlog);
-    if (chg & 2) rp[1] = make_int4(L.cap, L.enabled, L.fh, L.fn);
+    if (chg & 2) rp[1] = make_int4(cap_s[lane], en_s[lane], L.fh, L.fn);
     if (lane == 0) {
       rp[2] = make_int4(L.P, next_id + n, t + 1, L.busy_mask);
     } else if (chg & 4) {
       recs[lane].P = L.P;
       recs[lane].busy_mask = L.busy_mask;
     }
-    if (chg & 8) recs[lane].next_done = L.next_done;
+    if (chg & 8) {
+      if (RPM) rp[3] = make_int4(L.next_done, rpm_s[lane], L.rcnt, __float_as_int(inv_rpm_s[lane]));
+      else recs[lane].next_done = L.next_done;
+    }
   }
   // Snapshot row for the next tick's route step: lane i < 4M writes
   // statistic i / M of model i % M, lanes m < M the validity bytes.
@@ -662,12 +740,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
       const int sidx = i / M, mm = i - sidx * M;
       const int32_t vq = shfl(L.qlen, mm), vb = shfl(L.busy, mm), vw = shfl(L.ewma, mm),
                     vk = shfl(L.backlog, mm);
-      const int32_t cm = shfl(L.cap, mm);
+      const int32_t cm = cap_s[mm < M ? mm : 0];
+      const int32_t vr = RPM ? rpm_s[mm < M ? mm : 0] : 0, vrc = RPM ? shfl(L.rcnt, mm) : 0;
       const int c = cm < 0 ? 0 : (cm > IM_MAX_SLOTS ? IM_MAX_SLOTS : cm);
       if (i < 4 * M) {
         float v;
         switch (sidx) {
-          case 0: v = (float)vq * a.inv_qcap; break;
+          case 0: v = RPM ? queue_stat(a, vq, vr, vrc, inv_rpm_s[mm < M ? mm : 0]) : (float)vq * a.inv_qcap; break;
           case 1: v = (float)vb * a.inv_tab[c]; break;
           case 2: v = (float)vw * a.inv_lat; break;
           default: v = (float)vk * a.inv_tab[IM_MAX_SLOTS + 1 + c]; break;
@@ -677,16 +756,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     }
     if (lane < M) {
       uint8_t* vb8 = (uint8_t*)(row + snap_valid_offset(M));
-      vb8[lane] = (L.enabled != 0 && L.cap > 0 && L.qlen < a.qcap) ? 1 : 0;
+      vb8[lane] = (en_s[lane] != 0 && cap_s[lane] > 0 && L.qlen < a.qcap) ? 1 : 0;
     }
   }
   if (n > 0) {
     int64_t* hist_p = a.hist + (size_t)e * a.A;
     int64_t* envc_p = a.env_cnt + (size_t)e * 2;
-    if (lane < 2) envc_p[lane] += lane == 0 ? n : nomodel;
+    if (lane < 2) counter_add(envc_p + lane, lane == 0 ? n : nomodel);
     if (lane < a.A) {
       const int32_t h = hist_s[lane];
-      if (h != 0) hist_p[lane] += h;
+      if (h != 0) counter_add(hist_p + lane, h);
     }
   }
 }
@@ -754,10 +833,11 @@ hipError_t launch_snapshot(const SchedArgs& a, int e0, int ne, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_schedule(const SchedArgs& a, hipStream_t s) {
+hipError_t launch_schedule(const SchedArgs& a, bool rpm, hipStream_t s) {
   const int64_t waves = (int64_t)a.E;
   const unsigned blocks = (unsigned)((waves + 3) / 4);
-  hipLaunchKernelGGL(schedule_kernel, dim3(blocks), dim3(256), 0, s, a);
+  if (rpm) hipLaunchKernelGGL(schedule_kernel<true>, dim3(blocks), dim3(256), 0, s, a);
+  else hipLaunchKernelGGL(schedule_kernel<false>, dim3(blocks), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

@@ -8,6 +8,7 @@ import oracle
 import workload
 
 STATE_INT_KEYS = ("next_id", "arrived", "rej_nomodel", "qlen", "busy", "ewma", "backlog", "cost_q16",
+                  "rpm_limit", "rpm_count", "rpm_hist",
                   "cap", "enabled", "rej_overflow", "enqueued", "started", "completed",
                   "slo_met", "lat_sum", "wait_sum", "hist", "slots")
 
@@ -124,7 +125,8 @@ def check_invariants(s: dict, cfg: dict, prev: dict | None = None, ctx=""):
             if np.any(sl[sl[:, 0] >= 0, 2] < 1):
                 raise fail(f"busy slot with rem < 1 ({e},{m})")
             c = int(s["cap"][e, m])
-            if prev is not None and n > 0 and int(prev["cap"][e, m]) == c:
+            held = "rpm_limit" in s and 0 < int(s["rpm_limit"][e, m]) <= int(s["rpm_count"][e, m])
+            if prev is not None and n > 0 and int(prev["cap"][e, m]) == c and not held:
                 empty = int(np.sum(sl[:c, 0] < 0))
                 done = int(s["completed"][e, m] - prev["completed"][e, m])
                 if empty > done:
