@@ -18,7 +18,11 @@ _SRC = os.path.join(_HERE, "oracle.cpp")
 _LIB = os.path.join(_HERE, "liboracle.so")
 
 KEY_MODES = {"slack": 0, "deadline": 1, "fcfs": 2}
-ERR_QIDX, ERR_COUNT, ERR_BUDGET, ERR_SVC, ERR_ACTION = 1, 2, 4, 8, 16
+ERR_QIDX, ERR_COUNT, ERR_BUDGET, ERR_SVC, ERR_ACTION, ERR_ROLE = 1, 2, 4, 8, 16, 32
+
+# Parameters of the dual-pathway executor, in the order orc_create_dual takes them.
+DUAL_PARAMS = ("W_sem", "b_sem", "g_sem", "be_sem", "W_bud", "b_bud", "W_sys", "b_sys",
+               "W_res", "b_res", "g_res", "be_res", "W_merge", "b_merge", "W_act", "b_act")
 
 
 def build(force: bool = True) -> str:
@@ -38,7 +42,8 @@ class _Desc(ctypes.Structure):
                 ("n_layers", ctypes.c_int32), ("widths", ctypes.c_int32 * 4),
                 ("dtype", ctypes.c_int32), ("key_mode", ctypes.c_int32),
                 ("max_arrivals", ctypes.c_int32), ("budget_max", ctypes.c_int32),
-                ("value_head", ctypes.c_int32), ("Q", ctypes.c_int64)]
+                ("value_head", ctypes.c_int32), ("net", ctypes.c_int32),
+                ("n_roles", ctypes.c_int32), ("Q", ctypes.c_int64)]
 
 
 _lib = None
@@ -59,8 +64,11 @@ def _load():
         L.orc_error.argtypes = [P]
         L.orc_error.restype = ctypes.c_int32
         L.orc_clear_error.argtypes = [P]
-        L.orc_route.argtypes = [P, P, P, P, P, P, ctypes.c_int]
-        L.orc_schedule.argtypes = [P, ctypes.c_int32, P, P, P, P, P, ctypes.c_int]
+        L.orc_create_dual.restype = P
+        L.orc_create_dual.argtypes = [ctypes.POINTER(_Desc), P, P, P, P, P]
+        L.orc_dual_trace.argtypes = [P, ctypes.c_int, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, P]
+        L.orc_route.argtypes = [P, P, P, P, P, P, P, ctypes.c_int]
+        L.orc_schedule.argtypes = [P, ctypes.c_int32, P, P, P, P, P, P, ctypes.c_int]
         L.orc_features.argtypes = [P, ctypes.c_int, ctypes.c_int32, ctypes.c_int32, P]
         L.orc_round_bf16.argtypes = [ctypes.c_double]
         L.orc_round_bf16.restype = ctypes.c_double
@@ -69,8 +77,8 @@ def _load():
         L.orc_set_capacity.argtypes = [P, ctypes.c_int, ctypes.c_int, ctypes.c_int]
         L.orc_read_state.argtypes = [P] * 7
         U32 = ctypes.c_uint32
-        L.orc_route_rl.argtypes = [P, ctypes.c_int, P, P, P, U32, U32, ctypes.c_int, P, P, P, P, P,
-                                   ctypes.c_int]
+        L.orc_route_rl.argtypes = [P, ctypes.c_int, P, P, P, P, U32, U32, ctypes.c_int, P, P, P, P,
+                                   P, ctypes.c_int]
         L.orc_philox4x32_10.argtypes = [P, P, P]
         L.orc_gumbel.argtypes = [U32, U32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int]
         L.orc_gumbel.restype = ctypes.c_double
@@ -117,40 +125,57 @@ class Oracle:
 
     W, b: lists of fp32 arrays (W[l] is [out, in]); emb_values: float32
     [Q, E_d] (the value of each table entry); cap: int32 [E, M];
-    logit_bias: float32 [M] or None."""
+    logit_bias: float32 [M] or None. For a dual-pathway executor
+    (cfg["net"] == "dual", Sec. 4.2) W is a dict of its fp32 parameters
+    (names in DUAL_PARAMS), b is unused and roles is the fp32 role-embedding
+    table [n_roles, E_d]."""
 
-    def __init__(self, cfg, W, b, emb_values, cap, logit_bias=None, E=None, threads=1):
+    def __init__(self, cfg, W, b, emb_values, cap, logit_bias=None, E=None, threads=1, roles=None):
         L = _load()
         d = _Desc()
         self.E = cfg["E"] if E is None else E
+        self.dual = cfg.get("net") == "dual"
         d.E, d.M, d.K = self.E, cfg["M"], cfg["K"]
         d.qcap, d.max_slots = cfg["qcap"], cfg["max_slots"]
-        d.embed_dim, d.feat_dim, d.n_layers = cfg["embed_dim"], cfg["feat_dim"], len(cfg["widths"])
-        for i, w in enumerate(cfg["widths"]):
-            d.widths[i] = w
+        vh = 1 if cfg.get("value_head") else 0
+        d.value_head = vh
+        if self.dual:
+            d.embed_dim, d.feat_dim, d.n_layers = cfg["embed_dim"], cfg["embed_dim"] + 4 * cfg["M"] + 1, 0
+            d.net, d.n_roles = 1, cfg["n_roles"]
+        else:
+            d.embed_dim, d.feat_dim, d.n_layers = cfg["embed_dim"], cfg["feat_dim"], len(cfg["widths"])
+            for i, w in enumerate(cfg["widths"]):
+                d.widths[i] = w
+            d.widths[len(cfg["widths"]) - 1] = cfg["widths"][-1] + vh
         d.dtype = 1 if cfg["dtype"] == "bf16" else 0
         d.key_mode = KEY_MODES[cfg["key_mode"]]
         d.max_arrivals = cfg["max_arrivals"]
         d.budget_max = cfg["budget_max"]
-        vh = 1 if cfg.get("value_head") else 0
-        d.value_head = vh
-        d.widths[len(cfg["widths"]) - 1] = cfg["widths"][-1] + vh
         emb = np.ascontiguousarray(emb_values, np.float32)
         d.Q = emb.shape[0]
         self.cfg, self.M, self.K, self.A = cfg, cfg["M"], cfg["K"], cfg["M"] * cfg["K"]
         self.qcap, self.S = cfg["qcap"], cfg["max_slots"]
         self.threads = threads
-        self._W = [np.ascontiguousarray(w, np.float32) for w in W]
-        self._b = [np.ascontiguousarray(x, np.float32) for x in b]
-        Wp = (ctypes.c_void_p * len(W))(*[w.ctypes.data for w in self._W])
-        bp = (ctypes.c_void_p * len(b))(*[x.ctypes.data for x in self._b])
         cap = np.ascontiguousarray(cap, np.int32).reshape(-1)
         assert cap.size == self.E * self.M
         lb = None if logit_bias is None else np.ascontiguousarray(logit_bias, np.float32)
         self._d = d
-        self.p = L.orc_create(ctypes.byref(d), ctypes.cast(Wp, ctypes.c_void_p),
-                              ctypes.cast(bp, ctypes.c_void_p), _ptr(emb), _ptr(cap),
-                              None if lb is None else _ptr(lb))
+        if self.dual:
+            self._P = [np.ascontiguousarray(W[k], np.float32).reshape(-1) for k in DUAL_PARAMS]
+            self._roles = np.ascontiguousarray(roles, np.float32)
+            assert self._roles.shape == (cfg["n_roles"], cfg["embed_dim"])
+            Pp = (ctypes.c_void_p * len(self._P))(*[w.ctypes.data for w in self._P])
+            self.p = L.orc_create_dual(ctypes.byref(d), ctypes.cast(Pp, ctypes.c_void_p),
+                                       _ptr(self._roles), _ptr(emb), _ptr(cap),
+                                       None if lb is None else _ptr(lb))
+        else:
+            self._W = [np.ascontiguousarray(w, np.float32) for w in W]
+            self._b = [np.ascontiguousarray(x, np.float32) for x in b]
+            Wp = (ctypes.c_void_p * len(W))(*[w.ctypes.data for w in self._W])
+            bp = (ctypes.c_void_p * len(b))(*[x.ctypes.data for x in self._b])
+            self.p = L.orc_create(ctypes.byref(d), ctypes.cast(Wp, ctypes.c_void_p),
+                                  ctypes.cast(bp, ctypes.c_void_p), _ptr(emb), _ptr(cap),
+                                  None if lb is None else _ptr(lb))
         self._lib = L
 
     def __del__(self):
@@ -176,6 +201,11 @@ class Oracle:
                 np.ascontiguousarray(arr["budget"], np.int16),
                 np.ascontiguousarray(arr["base_svc"], np.int16))
 
+    @staticmethod
+    def _role(arr):
+        r = arr.get("role")
+        return None if r is None else np.ascontiguousarray(r, np.int16)
+
     def route(self, arr, want_logits=True):
         """Returns (actions int32 [n], logits float64 [n, A] or None)."""
         off, q, bud, _ = self._arr(arr)
@@ -183,7 +213,8 @@ class Oracle:
         n = int(q.size)
         act = np.empty(n, np.int32)
         lg = np.empty((n, self.A), np.float64) if want_logits else None
-        self._lib.orc_route(self.p, _ptr(off), _ptr(q), _ptr(bud),
+        ro = self._role(arr)
+        self._lib.orc_route(self.p, _ptr(off), _ptr(q), None if ro is None else _ptr(ro), _ptr(bud),
                             None if lg is None else _ptr(lg), _ptr(act), self.threads)
         return act, lg
 
@@ -197,7 +228,9 @@ class Oracle:
         out = dict(actions=np.empty(n, np.int32), logits=np.empty((n, self.A), np.float64),
                    logp=np.empty(n, np.float64), entropy=np.empty(n, np.float64),
                    value=np.empty(n, np.float64))
-        self._lib.orc_route_rl(self.p, env_base, _ptr(off), _ptr(q), _ptr(bud),
+        ro = self._role(arr)
+        self._lib.orc_route_rl(self.p, env_base, _ptr(off), _ptr(q),
+                               None if ro is None else _ptr(ro), _ptr(bud),
                                seed & 0xffffffff, (seed >> 32) & 0xffffffff, int(bool(greedy)),
                                _ptr(out["logits"]), _ptr(out["actions"]), _ptr(out["logp"]),
                                _ptr(out["entropy"]), _ptr(out["value"]), self.threads)
@@ -212,7 +245,9 @@ class Oracle:
     def schedule(self, arr, actions):
         off, q, bud, svc = self._arr(arr)
         act = np.ascontiguousarray(actions, np.int32)
-        self._lib.orc_schedule(self.p, int(q.size), _ptr(off), _ptr(q), _ptr(bud), _ptr(svc),
+        ro = self._role(arr)
+        self._lib.orc_schedule(self.p, int(q.size), _ptr(off), _ptr(q),
+                               None if ro is None else _ptr(ro), _ptr(bud), _ptr(svc),
                                _ptr(act), self.threads)
 
     def tick(self, arr):
@@ -221,9 +256,24 @@ class Oracle:
         return act
 
     def features(self, e, q_idx, budget):
-        out = np.empty(self.cfg["feat_dim"], np.float64)
+        out = np.empty(self._d.feat_dim, np.float64)
         self._lib.orc_features(self.p, e, q_idx, budget, _ptr(out))
         return out
+
+    def dual_trace(self, e, q_idx, role, budget) -> dict:
+        """Hidden vectors of one request of env e through the dual-pathway
+        executor: h_sem, h_bud, h_sys, h_res, h and z (logits and value row,
+        without the logit bias)."""
+        assert self.dual
+        sizes = [("h_sem", 128), ("h_bud", 16), ("h_sys", 16), ("h_res", 64), ("h", 128),
+                 ("z", self.A + self._d.value_head)]
+        out = np.empty(sum(n for _, n in sizes), np.float64)
+        self._lib.orc_dual_trace(self.p, e, q_idx, role, budget, _ptr(out))
+        res, o = {}, 0
+        for k, n in sizes:
+            res[k] = out[o:o + n]
+            o += n
+        return res
 
     def set_enabled(self, e, m, v):
         self._lib.orc_set_enabled(self.p, e, m, int(bool(v)))

@@ -10,9 +10,12 @@
 //     remaining budget and per-model queue depth, latency and KV-cache load.
 //   Sec. 3 "Action": a joint action a in [0, N*|S|) decodes to model a / K and
 //     reasoning depth a % K.
-//   Sec. 4.2: a policy network scores every joint action; the build deploys
-//     it greedily (masked argmax) with a plain MLP in place of the
-//     dual-pathway network. For RL rollouts (Sec. 4.4, Eq. 5 consumes
+//   Sec. 4.2: a policy network scores every joint action and is deployed
+//     greedily (masked argmax): either a plain MLP over the state vector or
+//     the paper's dual-pathway executor (a semantic pathway over the query
+//     and role embeddings, a resource pathway over the remaining budget and
+//     the per-model load, each ending in a LayerNorm, merged into one
+//     representation that feeds the action and value heads). For RL rollouts (Sec. 4.4, Eq. 5 consumes
 //     log pi, the entropy and V) the policy pi(a|s) is the softmax of the
 //     logits over the valid actions, sampled with the Gumbel-max trick from
 //     Philox4x32-10 noise (Salmon et al., SC 2011), and an optional value row
@@ -53,6 +56,7 @@ enum ErrBits {
   ERR_BUDGET = 4,    // budget < 1
   ERR_SVC = 8,       // base_svc outside [1, kSvcMax]
   ERR_ACTION = 16,   // action outside [-1, A)
+  ERR_ROLE = 32,     // role outside [0, n_roles) (dual-pathway executor only)
 };
 
 // ----- bf16 round-to-nearest-even of a real value ------------------------
@@ -130,7 +134,21 @@ struct orc_desc {
   int32_t max_arrivals;
   int32_t budget_max;
   int32_t value_head;     // 1: the last layer has M*K + 1 rows, row M*K is V(s)
+  int32_t net;            // 0 plain MLP, 1 dual-pathway executor (Sec. 4.2)
+  int32_t n_roles;        // dual-pathway executor: rows of the role-embedding table
   int64_t Q;
+};
+
+// Parameters of the dual-pathway executor (Sec. 4.2), matrices [out x in]
+// row-major. In bf16 pools the matrices and the role table hold bf16 values.
+struct orc_dual {
+  std::vector<double> W_sem, b_sem, g_sem, be_sem;   // 128 x 2 E_d; LayerNorm gain, bias
+  std::vector<double> W_bud, b_bud;                  // 16 x 1
+  std::vector<double> W_sys, b_sys;                  // 16 x 3M, input [queue | e2e | kv]
+  std::vector<double> W_res, b_res, g_res, be_res;   // 64 x 32, input [h_bud | h_sys]
+  std::vector<double> W_merge, b_merge;              // 128 x 192, input [h_sem | h_res]
+  std::vector<double> W_act, b_act;                  // (M K + value_head) x 128
+  std::vector<double> role;                          // n_roles x E_d
 };
 
 struct orc_pool {
@@ -138,6 +156,7 @@ struct orc_pool {
   int A;
   std::vector<std::vector<double>> W;   // [layer] out x in, row-major
   std::vector<std::vector<double>> b;   // [layer] out
+  orc_dual dual;                        // the dual-pathway executor (net == 1)
   std::vector<float> emb;               // Q x embed_dim (value of each entry)
   std::vector<double> logit_bias;       // M (0 when absent)
   std::vector<EnvState> envs;
@@ -220,6 +239,123 @@ void mlp(const orc_pool* p, const std::vector<double>& x, std::vector<double>& z
   for (int a = 0; a < p->A; ++a) z[a] += p->logit_bias[a / p->d.K];
 }
 
+// ----- the paper's dual-pathway executor (Sec. 4.2) -------------------------
+// Widths fixed by the paper: semantic pathway 128, budget and system heads 16
+// each, resource pathway 64, merged representation 128.
+const int kSem = 128, kBud = 16, kSys = 16, kRes = 64, kMerge = 128;
+// LayerNorm: the paper gives no epsilon; 1e-5 (the usual default) is taken.
+const double kLnEps = 1e-5;
+
+// y = W x + b for W [out x in] row-major.
+void linear(const std::vector<double>& W, const std::vector<double>& b, int out,
+            const std::vector<double>& x, std::vector<double>& y) {
+  const size_t in = x.size();
+  y.assign(out, 0.0);
+  for (int o = 0; o < out; ++o) {
+    double s = b[o];
+    for (size_t i = 0; i < in; ++i) s += W[(size_t)o * in + i] * x[i];
+    y[o] = s;
+  }
+}
+
+void relu_inplace(std::vector<double>& v) {
+  for (double& x : v) x = x > 0.0 ? x : 0.0;
+}
+
+// LayerNorm over the whole vector: (v - mean) / sqrt(var + eps) * gain + bias,
+// with the biased (1/n) variance.
+void layer_norm(std::vector<double>& v, const std::vector<double>& gain,
+                const std::vector<double>& bias) {
+  const double n = (double)v.size();
+  double mean = 0.0;
+  for (double x : v) mean += x;
+  mean /= n;
+  double var = 0.0;
+  for (double x : v) var += (x - mean) * (x - mean);
+  var /= n;
+  const double inv = 1.0 / std::sqrt(var + kLnEps);
+  for (size_t i = 0; i < v.size(); ++i) v[i] = (v[i] - mean) * inv * gain[i] + bias[i];
+}
+
+// Hidden vectors of one request through the dual-pathway executor, in fp64.
+// x is the request's feature vector (features()): query embedding, the four
+// per-model load statistics (stat-major: queue depth, KV proxy, latency,
+// backlog) and the normalised remaining budget, already bf16 in bf16 pools.
+// In bf16 pools every vector that enters a matrix product is bf16: h_bud and
+// h_sys after their ReLU, h_sem and h_res after their LayerNorm, h after its
+// ReLU (the weights were rounded at creation).
+struct DualTrace {
+  std::vector<double> h_sem, h_bud, h_sys, h_res, h, z;
+};
+
+void dual_net(const orc_pool* p, const std::vector<double>& x, int32_t role, DualTrace& t) {
+  const orc_desc& d = p->d;
+  const orc_dual& w = p->dual;
+  const int Ed = d.embed_dim, M = d.M;
+  auto rnd = [&](std::vector<double>& v) {
+    if (d.dtype == 1) for (double& a : v) a = round_bf16(a);
+  };
+  // semantic pathway: LN(ReLU(W_sem [e_q | e_r]))
+  std::vector<double> sem_in(2 * Ed);
+  for (int k = 0; k < Ed; ++k) sem_in[k] = x[k];
+  for (int k = 0; k < Ed; ++k) sem_in[Ed + k] = w.role[(size_t)role * Ed + k];
+  linear(w.W_sem, w.b_sem, kSem, sem_in, t.h_sem);
+  relu_inplace(t.h_sem);
+  layer_norm(t.h_sem, w.g_sem, w.be_sem);
+  rnd(t.h_sem);
+  // resource pathway: budget head over b, system head over
+  // [queue depth | end-to-end latency | KV-cache use] of every model
+  const std::vector<double> b_in = {x[Ed + 4 * M]};
+  linear(w.W_bud, w.b_bud, kBud, b_in, t.h_bud);
+  relu_inplace(t.h_bud);
+  rnd(t.h_bud);
+  std::vector<double> sys_in(3 * M);
+  for (int m = 0; m < M; ++m) {
+    sys_in[m] = x[Ed + 0 * M + m];           // queue depth
+    sys_in[M + m] = x[Ed + 2 * M + m];       // end-to-end latency
+    sys_in[2 * M + m] = x[Ed + 1 * M + m];   // KV-cache use
+  }
+  linear(w.W_sys, w.b_sys, kSys, sys_in, t.h_sys);
+  relu_inplace(t.h_sys);
+  rnd(t.h_sys);
+  std::vector<double> res_in(t.h_bud);
+  res_in.insert(res_in.end(), t.h_sys.begin(), t.h_sys.end());
+  linear(w.W_res, w.b_res, kRes, res_in, t.h_res);
+  relu_inplace(t.h_res);
+  layer_norm(t.h_res, w.g_res, w.be_res);
+  rnd(t.h_res);
+  // decision: h = ReLU(W_merge [h_sem | h_res]); logits W_act h (+ value row)
+  std::vector<double> mrg_in(t.h_sem);
+  mrg_in.insert(mrg_in.end(), t.h_res.begin(), t.h_res.end());
+  linear(w.W_merge, w.b_merge, kMerge, mrg_in, t.h);
+  relu_inplace(t.h);
+  rnd(t.h);
+  linear(w.W_act, w.b_act, p->A + d.value_head, t.h, t.z);
+}
+
+// Logits of one request (rows A.. hold the value head), with the per-model
+// logit bias on the action rows.
+void policy(const orc_pool* p, const EnvState& env, int32_t q_idx, int32_t role, int32_t budget,
+            std::vector<double>& z) {
+  std::vector<double> x;
+  features(p, env, q_idx, budget, x);
+  if (p->d.net == 1) {
+    DualTrace t;
+    dual_net(p, x, role, t);
+    z = t.z;
+    for (int a = 0; a < p->A; ++a) z[a] += p->logit_bias[a / p->d.K];
+  } else {
+    mlp(p, x, z);
+  }
+}
+
+// Role of row r: 0 for MLP pools; -1 when out of range or missing.
+int32_t role_of(const orc_pool* p, const int16_t* role, int32_t r) {
+  if (p->d.net != 1) return 0;
+  if (!role || role[r] < 0 || role[r] >= p->d.n_roles) return -1;
+  return role[r];
+}
+
 bool model_valid(const orc_pool* p, const ModelState& ms) {
   return ms.enabled != 0 && ms.cap > 0 && (int)ms.queue.size() < p->d.qcap;
 }
@@ -271,19 +407,20 @@ double gumbel(uint32_t seed_lo, uint32_t seed_hi, int32_t id, int32_t env, int a
 }
 
 // Route the requests of env e: logits (post-bias, pre-mask) and actions.
-void route_env(orc_pool* p, int e, const int32_t* off, const int32_t* q_idx,
+void route_env(orc_pool* p, int e, const int32_t* off, const int32_t* q_idx, const int16_t* role,
                const int16_t* budget, double* logits, int32_t* actions, int32_t* err) {
   const EnvState& env = p->envs[e];
-  std::vector<double> x, z;
+  std::vector<double> z;
   for (int32_t r = off[e]; r < off[e + 1]; ++r) {
-    if (q_idx[r] < 0 || (int64_t)q_idx[r] >= p->d.Q) {
-      *err |= ERR_QIDX;
+    const int32_t ro = role_of(p, role, r);
+    if (q_idx[r] < 0 || (int64_t)q_idx[r] >= p->d.Q || ro < 0) {
+      if (q_idx[r] < 0 || (int64_t)q_idx[r] >= p->d.Q) *err |= ERR_QIDX;
+      if (ro < 0) *err |= ERR_ROLE;
       actions[r] = -1;
       if (logits) for (int a = 0; a < p->A; ++a) logits[(size_t)r * p->A + a] = 0.0;
       continue;
     }
-    features(p, env, q_idx[r], budget[r], x);
-    mlp(p, x, z);
+    policy(p, env, q_idx[r], ro, budget[r], z);
     int best = -1;
     for (int a = 0; a < p->A; ++a) {
       const ModelState& ms = env.models[a / p->d.K];
@@ -301,22 +438,23 @@ void route_env(orc_pool* p, int e, const int32_t* off, const int32_t* q_idx,
 // greedy, the masked argmax; log pi of that action; the entropy of pi; and
 // the value row. No valid action: action -1, log-prob 0, entropy 0.
 void route_env_rl(orc_pool* p, int e, int env_base, const int32_t* off, const int32_t* q_idx,
-                  const int16_t* budget, uint32_t seed_lo, uint32_t seed_hi, int greedy,
-                  double* logits, int32_t* actions, double* logp, double* entropy,
+                  const int16_t* role, const int16_t* budget, uint32_t seed_lo, uint32_t seed_hi,
+                  int greedy, double* logits, int32_t* actions, double* logp, double* entropy,
                   double* value, int32_t* err) {
   const EnvState& env = p->envs[e];
   const int A = p->A;
-  std::vector<double> x, z;
+  std::vector<double> z;
   for (int32_t r = off[e]; r < off[e + 1]; ++r) {
-    if (q_idx[r] < 0 || (int64_t)q_idx[r] >= p->d.Q) {
-      *err |= ERR_QIDX;
+    const int32_t ro = role_of(p, role, r);
+    if (q_idx[r] < 0 || (int64_t)q_idx[r] >= p->d.Q || ro < 0) {
+      if (q_idx[r] < 0 || (int64_t)q_idx[r] >= p->d.Q) *err |= ERR_QIDX;
+      if (ro < 0) *err |= ERR_ROLE;
       actions[r] = -1;
       logp[r] = 0.0; entropy[r] = 0.0; value[r] = 0.0;
       if (logits) for (int a = 0; a < A; ++a) logits[(size_t)r * A + a] = 0.0;
       continue;
     }
-    features(p, env, q_idx[r], budget[r], x);
-    mlp(p, x, z);
+    policy(p, env, q_idx[r], ro, budget[r], z);
     value[r] = p->d.value_head ? z[A] : 0.0;
     if (logits) for (int a = 0; a < A; ++a) logits[(size_t)r * A + a] = z[a];
     std::vector<int> valid;
@@ -352,8 +490,8 @@ void route_env_rl(orc_pool* p, int e, int env_base, const int32_t* off, const in
 
 // Admission, queue insertion, service and accounting for env e at tick t.
 void schedule_env(orc_pool* p, int e, int32_t n_total, const int32_t* off,
-                  const int32_t* q_idx, const int16_t* budget, const int16_t* base_svc,
-                  const int32_t* actions, int32_t* err) {
+                  const int32_t* q_idx, const int16_t* role, const int16_t* budget,
+                  const int16_t* base_svc, const int32_t* actions, int32_t* err) {
   const orc_desc& d = p->d;
   EnvState& env = p->envs[e];
   const int32_t lo = off[e], hi = off[e + 1];
@@ -363,6 +501,7 @@ void schedule_env(orc_pool* p, int e, int32_t n_total, const int32_t* off,
   if (!bad) {
     for (int32_t r = lo; r < hi; ++r) {
       if (q_idx[r] < 0 || (int64_t)q_idx[r] >= d.Q) bad |= ERR_QIDX;
+      if (role_of(p, role, r) < 0) bad |= ERR_ROLE;
       if (budget[r] < 1) bad |= ERR_BUDGET;
       if (base_svc[r] < 1 || base_svc[r] > kSvcMax) bad |= ERR_SVC;
       if (actions[r] < -1 || actions[r] >= p->A) bad |= ERR_ACTION;
@@ -457,28 +596,10 @@ void for_envs(int E, int threads, F f) {
   for (auto& x : th) x.join();
 }
 
-}  // namespace
-
-extern "C" {
-
-// W[l]: fp32 [widths[l] x in_l] row-major; b[l]: fp32 [widths[l]];
-// emb: Q x embed_dim float values; cap: [E*M]; logit_bias: [M] or NULL.
-orc_pool* orc_create(const orc_desc* d, const float* const* W, const float* const* b,
-                     const float* emb, const int32_t* cap, const float* logit_bias) {
-  orc_pool* p = new orc_pool();
-  p->d = *d;
-  p->A = d->M * d->K;
-  int in = d->feat_dim;
-  for (int l = 0; l < d->n_layers; ++l) {
-    const int out = d->widths[l];
-    std::vector<double> w((size_t)out * in), bb(out);
-    for (size_t i = 0; i < w.size(); ++i)
-      w[i] = d->dtype == 1 ? round_bf16((double)W[l][i]) : (double)W[l][i];
-    for (int o = 0; o < out; ++o) bb[o] = (double)b[l][o];
-    p->W.push_back(w);
-    p->b.push_back(bb);
-    in = out;
-  }
+// Zero state (empty queues and slots, tick 0), the embedding values and the
+// per-model logit bias.
+void init_state(orc_pool* p, const float* emb, const int32_t* cap, const float* logit_bias) {
+  const orc_desc* d = &p->d;
   p->emb.assign(emb, emb + (size_t)d->Q * d->embed_dim);
   p->logit_bias.assign(d->M, 0.0);
   if (logit_bias) for (int m = 0; m < d->M; ++m) p->logit_bias[m] = (double)logit_bias[m];
@@ -492,7 +613,81 @@ orc_pool* orc_create(const orc_desc* d, const float* const* W, const float* cons
       env.models[m].cap = cap[e * d->M + m];
     }
   }
+}
+
+}  // namespace
+
+extern "C" {
+
+// W[l]: fp32 [widths[l] x in_l] row-major; b[l]: fp32 [widths[l]];
+// emb: Q x embed_dim float values; cap: [E*M]; logit_bias: [M] or NULL.
+orc_pool* orc_create(const orc_desc* d, const float* const* W, const float* const* b,
+                     const float* emb, const int32_t* cap, const float* logit_bias) {
+  orc_pool* p = new orc_pool();
+  p->d = *d;
+  p->d.net = 0;
+  p->A = d->M * d->K;
+  int in = d->feat_dim;
+  for (int l = 0; l < d->n_layers; ++l) {
+    const int out = d->widths[l];
+    std::vector<double> w((size_t)out * in), bb(out);
+    for (size_t i = 0; i < w.size(); ++i)
+      w[i] = d->dtype == 1 ? round_bf16((double)W[l][i]) : (double)W[l][i];
+    for (int o = 0; o < out; ++o) bb[o] = (double)b[l][o];
+    p->W.push_back(w);
+    p->b.push_back(bb);
+    in = out;
+  }
+  init_state(p, emb, cap, logit_bias);
   return p;
+}
+
+// The dual-pathway executor (Sec. 4.2). P holds, in this order, fp32 arrays:
+// W_sem [128 x 2E_d], b_sem, ln_sem gain, ln_sem bias [128]; W_bud [16 x 1],
+// b_bud [16]; W_sys [16 x 3M] (input order queue depth | end-to-end latency |
+// KV-cache use), b_sys [16]; W_res [64 x 32], b_res, ln_res gain, ln_res bias
+// [64]; W_merge [128 x 192], b_merge [128]; W_act [(M K + value_head) x 128],
+// b_act. role: fp32 [n_roles x E_d]. d->feat_dim must be E_d + 4M + 1.
+orc_pool* orc_create_dual(const orc_desc* d, const float* const* P, const float* role,
+                          const float* emb, const int32_t* cap, const float* logit_bias) {
+  orc_pool* p = new orc_pool();
+  p->d = *d;
+  p->d.net = 1;
+  p->A = d->M * d->K;
+  const int Ed = d->embed_dim, M = d->M, Ao = p->A + d->value_head;
+  auto mat = [&](int i, size_t n) {
+    std::vector<double> v(n);
+    for (size_t k = 0; k < n; ++k) v[k] = d->dtype == 1 ? round_bf16((double)P[i][k]) : (double)P[i][k];
+    return v;
+  };
+  auto vec = [&](int i, size_t n) { return std::vector<double>(P[i], P[i] + n); };
+  orc_dual& w = p->dual;
+  w.W_sem = mat(0, (size_t)kSem * 2 * Ed); w.b_sem = vec(1, kSem);
+  w.g_sem = vec(2, kSem); w.be_sem = vec(3, kSem);
+  w.W_bud = mat(4, kBud); w.b_bud = vec(5, kBud);
+  w.W_sys = mat(6, (size_t)kSys * 3 * M); w.b_sys = vec(7, kSys);
+  w.W_res = mat(8, (size_t)kRes * (kBud + kSys)); w.b_res = vec(9, kRes);
+  w.g_res = vec(10, kRes); w.be_res = vec(11, kRes);
+  w.W_merge = mat(12, (size_t)kMerge * (kSem + kRes)); w.b_merge = vec(13, kMerge);
+  w.W_act = mat(14, (size_t)Ao * kMerge); w.b_act = vec(15, Ao);
+  w.role.resize((size_t)d->n_roles * Ed);
+  for (size_t k = 0; k < w.role.size(); ++k)
+    w.role[k] = d->dtype == 1 ? round_bf16((double)role[k]) : (double)role[k];
+  init_state(p, emb, cap, logit_bias);
+  return p;
+}
+
+// Hidden vectors of one request of env e through the dual-pathway executor:
+// out = [h_sem (128) | h_bud (16) | h_sys (16) | h_res (64) | h (128) | logits
+// and value (M K + value_head), without the logit bias].
+void orc_dual_trace(const orc_pool* p, int e, int32_t q_idx, int32_t role, int32_t budget,
+                    double* out) {
+  std::vector<double> x;
+  features(p, p->envs[e], q_idx, budget, x);
+  DualTrace t;
+  dual_net(p, x, role, t);
+  for (const std::vector<double>* v : {&t.h_sem, &t.h_bud, &t.h_sys, &t.h_res, &t.h, &t.z})
+    out = std::copy(v->begin(), v->end(), out);
 }
 
 void orc_destroy(orc_pool* p) { delete p; }
@@ -501,33 +696,33 @@ int32_t orc_tick(const orc_pool* p) { return p->t; }
 int32_t orc_error(const orc_pool* p) { return p->err; }
 void orc_clear_error(orc_pool* p) { p->err = 0; }
 
-void orc_route(orc_pool* p, const int32_t* off, const int32_t* q_idx, const int16_t* budget,
-               double* logits, int32_t* actions, int threads) {
+void orc_route(orc_pool* p, const int32_t* off, const int32_t* q_idx, const int16_t* role,
+               const int16_t* budget, double* logits, int32_t* actions, int threads) {
   std::vector<int32_t> errs(p->d.E, 0);
   for_envs(p->d.E, threads, [&](int e) {
-    route_env(p, e, off, q_idx, budget, logits, actions, &errs[e]);
+    route_env(p, e, off, q_idx, role, budget, logits, actions, &errs[e]);
   });
   for (int32_t x : errs) p->err |= x;
 }
 
 void orc_schedule(orc_pool* p, int32_t n_total, const int32_t* off, const int32_t* q_idx,
-                  const int16_t* budget, const int16_t* base_svc, const int32_t* actions,
-                  int threads) {
+                  const int16_t* role, const int16_t* budget, const int16_t* base_svc,
+                  const int32_t* actions, int threads) {
   std::vector<int32_t> errs(p->d.E, 0);
   for_envs(p->d.E, threads, [&](int e) {
-    schedule_env(p, e, n_total, off, q_idx, budget, base_svc, actions, &errs[e]);
+    schedule_env(p, e, n_total, off, q_idx, role, budget, base_svc, actions, &errs[e]);
   });
   for (int32_t x : errs) p->err |= x;
   p->t += 1;
 }
 
 void orc_route_rl(orc_pool* p, int env_base, const int32_t* off, const int32_t* q_idx,
-                  const int16_t* budget, uint32_t seed_lo, uint32_t seed_hi, int greedy,
-                  double* logits, int32_t* actions, double* logp, double* entropy, double* value,
-                  int threads) {
+                  const int16_t* role, const int16_t* budget, uint32_t seed_lo, uint32_t seed_hi,
+                  int greedy, double* logits, int32_t* actions, double* logp, double* entropy,
+                  double* value, int threads) {
   std::vector<int32_t> errs(p->d.E, 0);
   for_envs(p->d.E, threads, [&](int e) {
-    route_env_rl(p, e, env_base, off, q_idx, budget, seed_lo, seed_hi, greedy, logits, actions,
+    route_env_rl(p, e, env_base, off, q_idx, role, budget, seed_lo, seed_hi, greedy, logits, actions,
                  logp, entropy, value, &errs[e]);
   });
   for (int32_t x : errs) p->err |= x;

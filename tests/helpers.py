@@ -26,11 +26,18 @@ def tiny_cfg(M=2, K=2, qcap=3, cap_hi=2, embed_dim=4, widths=None, dtype="f32",
 
 
 def make_oracle(cfg, seed=0, bias_scale=0.1, Q=None, E=None, cap=None, threads=1):
-    W, b = workload.gen.weights(cfg, seed, bias_scale)
+    """Oracle pool of cfg with seeded inputs. For the dual-pathway executor W
+    is the parameter dict and b the role-embedding table."""
+    if cfg.get("net") == "dual":
+        W, b = workload.gen.dual_weights(cfg, seed, bias_scale), workload.gen.roles(cfg, seed)
+    else:
+        W, b = workload.gen.weights(cfg, seed, bias_scale)
     _, emb = workload.gen.embedding(cfg, seed, rows=Q)
     cap = workload.gen.capacities(cfg, seed) if cap is None else cap
     lb = workload.gen.logit_bias(cfg)
-    return oracle.Oracle(cfg, W, b, emb, cap, lb, E=E, threads=threads), (W, b, emb, cap, lb)
+    o = oracle.Oracle(cfg, W, b, emb, cap, lb, E=E, threads=threads,
+                      roles=b if cfg.get("net") == "dual" else None)
+    return o, (W, b, emb, cap, lb)
 
 
 def assert_state_equal(a: dict, b: dict, envs=None, ctx=""):

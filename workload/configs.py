@@ -23,6 +23,13 @@ embed_dim  query-embedding width E_d (Sec. 3: Sentence-BERT vectors; here N(0,1)
 feat_dim   policy input width D_in; the features are
            [embedding | 4 load stats per model | remaining budget | zero pad]
 widths     layer output widths of the policy MLP, last = A
+net        "mlp" (default) or "dual": the paper's dual-pathway executor (Sec. 4.2),
+           whose widths are the paper's (128 / 16 / 16 / 64 / 128); it reads the
+           query embedding, a role embedding (n_roles rows, one role per
+           request), the remaining budget and three of the load statistics
+n_roles    rows of the role-embedding table (dual-pathway executor)
+value_head when true, the policy has a value row V(s) besides the A logits
+q_rows_cap upper bound on the embedding-table rows (default 2^22)
 dtype      "f32" or "bf16" (bf16 weights/activations, fp32 accumulate)
 zipf_s     when set, a per-model logit bias -s*ln(m+1) (unnormalised Zipf log-pmf)
 key_mode   "slack" (latest start time), "deadline" (EDF, Sec. 4.3) or "fcfs"
@@ -61,6 +68,12 @@ CONFIGS = {
     "c4": dict(_BASE, index=4, E=65536, M=8, K=3, lam=128.0, T=128, qcap=512,
                cap_lo=1, cap_hi=2, embed_dim=64, feat_dim=104,
                widths=[256, 24], dtype="bf16", zipf_s=1.2),
+    # c2's pools with the paper's dual-pathway executor (Sec. 4.2): 384-d query
+    # and role embeddings (Sentence-BERT width), 8 roles, 5 models x 3
+    # strategies, a value head; 2^20 table rows (768 MB in bf16)
+    "c2d": dict(_BASE, index=5, E=4096, lam=64.0, T=256, qcap=2048, net="dual",
+                embed_dim=384, n_roles=8, value_head=True, dtype="bf16",
+                q_rows_cap=1 << 20, lam_sweep=[4.0, 16.0, 64.0]),
 }
 
 
@@ -77,6 +90,13 @@ def finish(cfg: dict) -> dict:
     cfg["A"] = cfg["M"] * cfg["K"]
     cfg["max_slots"] = cfg["cap_hi"]
     cfg["budget_max"] = cfg["budget_hi"]
+    if cfg.get("net", "mlp") == "dual":
+        # the executor reads [emb | 4 load stats per model | budget] like the MLP
+        cfg["feat_dim"] = cfg["embed_dim"] + 4 * cfg["M"] + 1
+        cfg["widths"] = None
+        cfg["n_layers"] = None
+        return cfg
+    cfg["net"] = "mlp"
     cfg["n_layers"] = len(cfg["widths"])
     if cfg["widths"][-1] != cfg["A"]:
         raise ValueError("last layer width must equal M*K")

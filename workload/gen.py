@@ -9,7 +9,9 @@ sharing any part of the method.
 Streams: numpy.random.default_rng(SeedSequence([seed, cfg index, stream]))
   0 weights, 1 capacities, 2 embedding table, 3 Poisson counts [T, E],
   4 request fields, one sub-stream per tick: SeedSequence([seed, idx, 4, t]),
-  5 the value-head row (pools with cfg["value_head"]).
+  5 the value-head row (pools with cfg["value_head"]),
+  6 the dual-pathway executor's parameters, 7 its role-embedding table,
+  8 per-tick role of each request: SeedSequence([seed, idx, 8, t]).
 
 Inputs stand in for the paper's workloads (Sec. 5.1): the paper's LLM-quality
 benchmarks are replaced by N(0,1) query embeddings (Sec. 3 uses Sentence-BERT
@@ -31,7 +33,7 @@ def _rng(cfg: dict, seed: int, *stream: int) -> np.random.Generator:
 def table_rows(cfg: dict) -> int:
     """Embedding-table rows: min(expected total requests, 2^22), at least 16."""
     total = int(math.ceil(cfg["lam"] * cfg["E"] * cfg["T"]))
-    return max(16, min(total, _configs.Q_CAP_ROWS))
+    return max(16, min(total, cfg.get("q_rows_cap", _configs.Q_CAP_ROWS)))
 
 
 def weights(cfg: dict, seed: int = 0, bias_scale: float = 0.0):
@@ -62,6 +64,54 @@ def weights(cfg: dict, seed: int = 0, bias_scale: float = 0.0):
         Ws[-1] = np.concatenate([Ws[-1], w_val], axis=0)
         bs[-1] = np.concatenate([bs[-1], b_val])
     return Ws, bs
+
+
+def _glorot(rng, out, fan_in):
+    lim = math.sqrt(6.0 / (fan_in + out))
+    return rng.uniform(-lim, lim, size=(out, fan_in)).astype(np.float32)
+
+
+def dual_weights(cfg: dict, seed: int = 0, bias_scale: float = 0.0) -> dict:
+    """Parameters of the dual-pathway executor (Sec. 4.2) as fp32 arrays:
+    Glorot-uniform matrices [out, in], biases U(-bias_scale, bias_scale) (0 when
+    bias_scale is 0), LayerNorm gains 1 + U(-bias_scale, bias_scale) and
+    LayerNorm biases U(-bias_scale, bias_scale). Widths: W_sem 128 x 2E_d,
+    W_bud 16 x 1, W_sys 16 x 3M, W_res 64 x 32, W_merge 128 x 192, W_act
+    A x 128; with cfg["value_head"] one more W_act row (the value head, drawn
+    from its own stream)."""
+    rng = _rng(cfg, seed, 6)
+    Ed, M, A = cfg["embed_dim"], cfg["M"], cfg["A"]
+
+    def vec(n, center=0.0):
+        if bias_scale > 0:
+            return (center + rng.uniform(-bias_scale, bias_scale, size=n)).astype(np.float32)
+        return np.full(n, center, np.float32)
+
+    p = {}
+    p["W_sem"] = _glorot(rng, 128, 2 * Ed); p["b_sem"] = vec(128)
+    p["g_sem"] = vec(128, 1.0); p["be_sem"] = vec(128)
+    p["W_bud"] = _glorot(rng, 16, 1); p["b_bud"] = vec(16)
+    p["W_sys"] = _glorot(rng, 16, 3 * M); p["b_sys"] = vec(16)
+    p["W_res"] = _glorot(rng, 64, 32); p["b_res"] = vec(64)
+    p["g_res"] = vec(64, 1.0); p["be_res"] = vec(64)
+    p["W_merge"] = _glorot(rng, 128, 192); p["b_merge"] = vec(128)
+    p["W_act"] = _glorot(rng, A, 128); p["b_act"] = vec(A)
+    if cfg.get("value_head"):
+        vr = _rng(cfg, seed, 5)
+        lim = math.sqrt(6.0 / (128 + 1))
+        w_val = vr.uniform(-lim, lim, size=(1, 128)).astype(np.float32)
+        b_val = (vr.uniform(-bias_scale, bias_scale, size=1) if bias_scale > 0
+                 else np.zeros(1)).astype(np.float32)
+        p["W_act"] = np.concatenate([p["W_act"], w_val], axis=0)
+        p["b_act"] = np.concatenate([p["b_act"], b_val])
+    return p
+
+
+def roles(cfg: dict, seed: int = 0) -> np.ndarray:
+    """Role-embedding table [n_roles, E_d] of N(0,1) fp32 values (Sec. 4.2 uses
+    Sentence-BERT vectors of the role descriptions)."""
+    rng = _rng(cfg, seed, 7)
+    return rng.standard_normal(size=(cfg["n_roles"], cfg["embed_dim"]), dtype=np.float32)
 
 
 def capacities(cfg: dict, seed: int = 0) -> np.ndarray:
@@ -110,16 +160,23 @@ def tick(cfg: dict, seed: int, t: int, counts_row: np.ndarray, Q: int):
     ln = rng.lognormal(cfg["svc_mu"], cfg["svc_sigma"], size=n)
     base_svc = np.minimum(np.ceil(ln), _configs.SVC_MAX).astype(np.int16)
     base_svc = np.maximum(base_svc, 1).astype(np.int16)
-    return dict(offsets=offsets, q_idx=q_idx, budget=budget, base_svc=base_svc)
+    out = dict(offsets=offsets, q_idx=q_idx, budget=budget, base_svc=base_svc)
+    if cfg.get("n_roles"):
+        rr = _rng(cfg, seed, 8, t)
+        out["role"] = rr.integers(0, cfg["n_roles"], size=n).astype(np.int16)
+    return out
 
 
 def subset(arr: dict, e0: int, e1: int) -> dict:
     """The records of envs [e0, e1) of one tick, offsets rebased to 0."""
     off = arr["offsets"]
     lo, hi = int(off[e0]), int(off[e1])
-    return dict(offsets=(off[e0:e1 + 1] - lo).astype(np.int32),
-                q_idx=arr["q_idx"][lo:hi], budget=arr["budget"][lo:hi],
-                base_svc=arr["base_svc"][lo:hi])
+    out = dict(offsets=(off[e0:e1 + 1] - lo).astype(np.int32),
+               q_idx=arr["q_idx"][lo:hi], budget=arr["budget"][lo:hi],
+               base_svc=arr["base_svc"][lo:hi])
+    if "role" in arr:
+        out["role"] = arr["role"][lo:hi]
+    return out
 
 
 def logit_bias(cfg: dict):
