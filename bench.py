@@ -35,7 +35,20 @@ def algorithmic_flops_per_tick(cfg, n_requests):
     """Minimal policy FLOPs of one tick: per request the MLP without the
     per-env load-statistics columns of layer 1, plus once per env those 4M
     columns (they are shared by every request of the env). A value head adds
-    one more output row of the last layer."""
+    one more output row of the last layer.
+
+    Dual-pathway executor: per request the query half of the semantic layer
+    (128 x E_d), the budget head (16), the budget half of the resource layer
+    (64 x 16), the merge layer (128 x 192) and the action/value rows (x 128);
+    per env the system head (16 x 3M) and the system half of the resource
+    layer (64 x 16). The role half of the semantic layer takes n_roles
+    distinct inputs and is computed once per pool, not per tick. Matrix
+    products only (the LayerNorms add ~6 FLOP per feature)."""
+    if cfg.get("net") == "dual":
+        Ao = cfg["A"] + (1 if cfg.get("value_head") else 0)
+        per_req = 2 * (128 * cfg["embed_dim"] + 16 + 64 * 16 + 128 * 192 + Ao * 128)
+        per_env = 2 * (16 * 3 * cfg["M"] + 64 * 16)
+        return per_req * n_requests + per_env * cfg["E"]
     widths = list(cfg["widths"])
     if cfg.get("value_head"):
         widths[-1] += 1
@@ -87,7 +100,8 @@ def cpu_baseline(cfg, W, b, emb_vals, cap, lb, ticks, Q, budget_s=15.0):
     import workload
     threads = max(1, min(16, os.cpu_count() or 1))
     envs = min(cfg["E"], 8 * threads)
-    o = oracle.Oracle(cfg, W, b, emb_vals, cap[:envs], lb, E=envs, threads=threads)
+    o = oracle.Oracle(cfg, W, b, emb_vals, cap[:envs], lb, E=envs, threads=threads,
+                      roles=b if cfg.get("net") == "dual" else None)
     subs = [workload.gen.subset(a, 0, envs) for a in ticks]
     t0 = time.perf_counter()
     done = 0
@@ -222,7 +236,10 @@ def main():
 
     # ---- inputs (host generation, then resident in HBM) ----
     t_gen = time.perf_counter()
-    W, b = workload.gen.weights(cfg, args.seed)
+    if cfg.get("net") == "dual":
+        W, b = workload.gen.dual_weights(cfg, args.seed), workload.gen.roles(cfg, args.seed)
+    else:
+        W, b = workload.gen.weights(cfg, args.seed)
     Q = workload.gen.table_rows(cfg)
     table, emb_vals = workload.gen.embedding(cfg, args.seed, rows=Q)
     cap = workload.gen.capacities(cfg, args.seed)
@@ -347,13 +364,18 @@ def main():
         else:
             roof["frac_of_measured"] = roof["achieved"] / mp["copy_gbs_read_plus_write"]
 
+    if cfg.get("net") == "dual":
+        net_desc = (f"dual-pathway executor (Sec. 4.2), {cfg['embed_dim']}-d query and role "
+                    f"embeddings, {cfg['n_roles']} roles, widths 128/16/16/64/128"
+                    + (", value head" if cfg.get("value_head") else ""))
+    else:
+        net_desc = "MLP " + f"{cfg['feat_dim']}->" + "->".join(map(str, cfg["widths"]))
     line = {
         "metric": METRIC, "value": value, "unit": "env-ticks/s", "n_gpus": 1, "steps": K,
         "warmup": W_, "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": cfg["dtype"], "data": "synthetic",
         "config": {"workload": f"{args.config}: {cfg['E']} envs, M={cfg['M']} K={cfg['K']}, "
-                               f"lambda={cfg['lam']:g}/tick, qcap {cfg['qcap']}, MLP "
-                               f"{cfg['feat_dim']}->" + "->".join(map(str, cfg["widths"])) +
+                               f"lambda={cfg['lam']:g}/tick, qcap {cfg['qcap']}, {net_desc}"
                                f" {cfg['dtype']}, ticks {W_}..{W_ + K - 1} of {T}" +
                                ("; RL rollout: Gumbel-max sampled actions, log-probs, entropies, "
                                 "value head" if args.sample else ""),

@@ -65,6 +65,7 @@ typedef enum { IM_KEY_SLACK = 0, IM_KEY_DEADLINE = 1, IM_KEY_FCFS = 2 } im_key_m
 #define IM_ERR_BUDGET 4   /* budget < 1                                            */
 #define IM_ERR_SVC    8   /* base_svc outside [1, IM_SVC_MAX]                      */
 #define IM_ERR_ACTION 16  /* action outside [-1, M*K)                              */
+#define IM_ERR_ROLE   32  /* role outside [0, n_roles) (dual-pathway pools)          */
 
 /* Limits of this build. */
 #define IM_SVC_MAX     4095   /* largest base service time (ticks)              */
@@ -74,6 +75,12 @@ typedef enum { IM_KEY_SLACK = 0, IM_KEY_DEADLINE = 1, IM_KEY_FCFS = 2 } im_key_m
 #define IM_MAX_SLOTS   8
 #define IM_MAX_QCAP    16384
 #define IM_MAX_FEAT    512
+#define IM_MAX_ROLES   4096
+
+/* Policy network of a pool (Sec. 4.2). MLP: a plain MLP over the feature
+ * vector (widths from the description). DUAL: the paper's dual-pathway
+ * executor with its fixed widths (see im_dual_net). */
+typedef enum { IM_NET_MLP = 0, IM_NET_DUAL = 1 } im_net;
 
 /* Pool description.
  *   n_envs        E >= 1 independent envs
@@ -97,13 +104,18 @@ typedef enum { IM_KEY_SLACK = 0, IM_KEY_DEADLINE = 1, IM_KEY_FCFS = 2 } im_key_m
  *   value_head    0 or 1. With 1 the last layer has one more row, row M*K,
  *                 whose output is the state value V(s) = w_val . h + b_val of
  *                 the last hidden layer h (Sec. 4.2 "Decision"); it gets no
- *                 logit bias and takes no part in routing. */
+ *                 logit bias and takes no part in routing.
+ *   net           im_net; IM_NET_DUAL pools are created by im_pool_create_dual,
+ *                 which ignores feat_dim, n_layers and widths
+ *   n_roles       IM_NET_DUAL: rows of the role-embedding table, in
+ *                 [1, IM_MAX_ROLES]; ignored for IM_NET_MLP */
 typedef struct {
   int32_t n_envs, n_models, n_depths, queue_cap, max_slots;
   int32_t embed_dim, feat_dim, n_layers;
   int32_t widths[4];
   int32_t dtype, key_mode, max_arrivals_per_env_tick, budget_max;
   int32_t value_head;
+  int32_t net, n_roles;
 } im_pool_desc;
 
 /* The arrivals of ONE tick, in env-major CSR order (all device memory).
@@ -112,6 +124,9 @@ typedef struct {
  *   q_idx    [n]    row of the query-embedding table
  *   budget   [n]    time budget in ticks (>= 1)
  *   base_svc [n]    service time at depth 0 in ticks; at depth d it is base_svc*(d+1)
+ *   role     [n]    row of the role-embedding table: the role of the agent
+ *                   step that issues the request (Sec. 4.2). Required by
+ *                   IM_NET_DUAL pools, ignored (may be NULL) by IM_NET_MLP pools
  * Within an env, rows are in arrival order; request ids are assigned in that
  * order, continuing from the env's next_id. */
 typedef struct {
@@ -119,6 +134,7 @@ typedef struct {
   const int32_t* q_idx;
   const int16_t* budget;
   const int16_t* base_svc;
+  const int16_t* role;
   int32_t n_total;
 } im_arrivals;
 
@@ -139,11 +155,51 @@ im_status im_pool_create(const im_pool_desc* desc, const float* const* W, const 
                          const void* emb, int64_t n_queries, const int32_t* capacity,
                          const float* logit_bias, void* stream, im_pool** out);
 
+/* Parameters of the paper's dual-pathway executor (Sec. 4.2), all host fp32,
+ * matrices [out x in] row-major, copied at creation (matrices and role table
+ * rounded to bf16, biases and LayerNorm parameters kept in fp32):
+ *   semantic pathway  h_sem = LN(ReLU(W_sem [e_q | e_r] + b_sem)), 128 wide;
+ *                     W_sem [128 x 2 E_d], b_sem, ln_sem_gain, ln_sem_bias [128]
+ *   budget head       h_bud = ReLU(W_bud b + b_bud), 16 wide; W_bud [16 x 1], b_bud [16],
+ *                     b = budget / budget_max (the normalised remaining budget)
+ *   system head       h_sys = ReLU(W_sys [d_queue | d_e2e | d_kv] + b_sys), 16 wide;
+ *                     W_sys [16 x 3M], b_sys [16]; per model the queue-depth,
+ *                     latency-EWMA and busy-slot features of the MLP feature
+ *                     vector (im_pool_desc) in that order
+ *   resource pathway  h_res = LN(ReLU(W_res [h_bud | h_sys] + b_res)), 64 wide;
+ *                     W_res [64 x 32], b_res, ln_res_gain, ln_res_bias [64]
+ *   decision          h = ReLU(W_merge [h_sem | h_res] + b_merge), 128 wide;
+ *                     W_merge [128 x 192], b_merge [128]; logits W_act h + b_act,
+ *                     W_act [(M*K + value_head) x 128], b_act [M*K + value_head]
+ *                     (row M*K: the value head V(s))
+ *   role_emb          [n_roles x E_d] role-embedding table e_r
+ * LayerNorm: (x - mean) / sqrt(var + 1e-5) * gain + bias over the vector, with
+ * the biased variance. Every vector entering a matrix product is bf16. */
+typedef struct {
+  const float *W_sem, *b_sem, *ln_sem_gain, *ln_sem_bias;
+  const float *W_bud, *b_bud;
+  const float *W_sys, *b_sys;
+  const float *W_res, *b_res, *ln_res_gain, *ln_res_bias;
+  const float *W_merge, *b_merge;
+  const float *W_act, *b_act;
+  const float *role_emb;
+} im_dual_net;
+
+/* Create a pool whose policy is the dual-pathway executor (desc->net must be
+ * IM_NET_DUAL, desc->dtype IM_BF16; embed_dim in {64, 128, 256, 384}; M*K +
+ * value_head <= 32). The query-embedding table, capacities, logit bias,
+ * stream and errors are as for im_pool_create; every other call works on the
+ * pool unchanged, with arrivals carrying a role per row. */
+im_status im_pool_create_dual(const im_pool_desc* desc, const im_dual_net* net, const void* emb,
+                              int64_t n_queries, const int32_t* capacity, const float* logit_bias,
+                              void* stream, im_pool** out);
+
 /* Route one tick (Sec. 3 Eq. 1 features, Sec. 4.2 policy, masked argmax).
  * Reads the state left by the previous tick; does not change the state.
  *   actions  device int32 [n_total] out: chosen joint action, -1 when no
  *            action is valid (model disabled, c_m = 0 or its queue full) or
- *            the row's q_idx is out of range (IM_ERR_QIDX is raised)
+ *            the row's q_idx is out of range (IM_ERR_QIDX is raised) or, in
+ *            a dual-pathway pool, its role (IM_ERR_ROLE)
  *   logits   device fp32 [n_total x M*K] out (post logit-bias, pre-mask), or NULL
  * Argmax ties go to the lowest action index. */
 im_status im_route(im_pool* pool, const im_arrivals* arr, int32_t* actions, float* logits,

@@ -9,7 +9,8 @@ from __future__ import annotations
 from . import _lib
 from ._lib import (EXPORTED, IMError, im_clear_error, im_destroy, im_dual_update,  # noqa: F401
                    im_get_error,
-                   im_last_error, im_pool_create, im_read_state, im_route, im_route_sample,
+                   im_last_error, im_pool_create, im_pool_create_dual, im_read_state, im_route,
+                   im_route_sample,
                    im_schedule,
                    im_set_capacity, im_set_enabled, im_set_rpm_limit, im_tick, im_write_state,
                    make_arrivals,
@@ -17,11 +18,13 @@ from ._lib import (EXPORTED, IMError, im_clear_error, im_destroy, im_dual_update
 
 
 def device_arrivals(arr: dict, device="cuda"):
-    """Upload one tick's numpy arrivals (offsets, q_idx, budget, base_svc)."""
+    """Upload one tick's numpy arrivals (offsets, q_idx, budget, base_svc and,
+    when present, role)."""
     import torch
     t = lambda x, dt: torch.as_tensor(x, dtype=dt).to(device)  # noqa: E731
+    role = t(arr["role"], torch.int16) if "role" in arr else None
     return make_arrivals(t(arr["offsets"], torch.int32), t(arr["q_idx"], torch.int32),
-                         t(arr["budget"], torch.int16), t(arr["base_svc"], torch.int16))
+                         t(arr["budget"], torch.int16), t(arr["base_svc"], torch.int16), role)
 
 
 class Pool:
@@ -29,7 +32,9 @@ class Pool:
 
     W, b: host float32 weights/biases per layer; emb: device tensor holding the
     embedding table (float32, or bf16 bits as int16/uint16 for bf16 configs),
-    kept alive by this object; cap: int32 [E, M]; logit_bias: float32 [M] or None."""
+    kept alive by this object; cap: int32 [E, M]; logit_bias: float32 [M] or None.
+    For the dual-pathway executor (cfg["net"] == "dual") W is the parameter
+    dict of workload.gen.dual_weights and b the role-embedding table."""
 
     def __init__(self, cfg, W, b, emb, cap, logit_bias=None, stream=None):
         self.cfg = cfg
@@ -37,7 +42,10 @@ class Pool:
         self.A, self.S, self.qcap = cfg["M"] * cfg["K"], cfg["max_slots"], cfg["qcap"]
         self.emb = emb
         self.desc = make_desc(cfg)
-        self.h = im_pool_create(self.desc, W, b, emb, emb.shape[0], cap, logit_bias, stream)
+        if cfg.get("net") == "dual":
+            self.h = im_pool_create_dual(self.desc, W, b, emb, emb.shape[0], cap, logit_bias, stream)
+        else:
+            self.h = im_pool_create(self.desc, W, b, emb, emb.shape[0], cap, logit_bias, stream)
 
     def route(self, arr, actions, logits=None, stream=None):
         im_route(self.h, arr, actions, logits, stream)

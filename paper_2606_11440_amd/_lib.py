@@ -2,7 +2,7 @@
 only. Every step of the tick runs in the library's HIP kernels; torch tensors
 merely provide device memory and the current HIP stream.
 
-The functions keep the C names (im_pool_create, im_route, im_route_sample,
+The functions keep the C names (im_pool_create, im_pool_create_dual, im_route, im_route_sample,
 im_schedule, im_tick, im_destroy, im_read_state, im_write_state,
 im_set_enabled, im_set_capacity, im_get_error, im_clear_error, im_last_error)."""
 from __future__ import annotations
@@ -18,9 +18,10 @@ LIB_PATH = os.path.join(HERE, "libinframind.so")
 IM_OK, IM_EINVAL, IM_ENOMEM, IM_EHIP, IM_EDEVICE, IM_ESTATE, IM_EUNSUPPORTED = 0, -1, -2, -3, -4, -5, -6
 IM_F32, IM_BF16 = 0, 1
 KEY_MODES = {"slack": 0, "deadline": 1, "fcfs": 2}
-IM_ERR_QIDX, IM_ERR_COUNT, IM_ERR_BUDGET, IM_ERR_SVC, IM_ERR_ACTION = 1, 2, 4, 8, 16
+IM_ERR_QIDX, IM_ERR_COUNT, IM_ERR_BUDGET, IM_ERR_SVC, IM_ERR_ACTION, IM_ERR_ROLE = 1, 2, 4, 8, 16, 32
+IM_NET_MLP, IM_NET_DUAL = 0, 1
 
-EXPORTED = ("im_pool_create", "im_route", "im_route_sample", "im_schedule", "im_tick", "im_destroy",
+EXPORTED = ("im_pool_create", "im_pool_create_dual", "im_route", "im_route_sample", "im_schedule", "im_tick", "im_destroy",
             "im_dual_update", "im_set_rpm_limit",
             "im_read_state", "im_write_state", "im_set_enabled", "im_set_capacity",
             "im_get_error", "im_clear_error", "im_last_error")
@@ -33,13 +34,26 @@ class ImPoolDesc(ctypes.Structure):
                 ("feat_dim", ctypes.c_int32), ("n_layers", ctypes.c_int32),
                 ("widths", ctypes.c_int32 * 4), ("dtype", ctypes.c_int32),
                 ("key_mode", ctypes.c_int32), ("max_arrivals_per_env_tick", ctypes.c_int32),
-                ("budget_max", ctypes.c_int32), ("value_head", ctypes.c_int32)]
+                ("budget_max", ctypes.c_int32), ("value_head", ctypes.c_int32),
+                ("net", ctypes.c_int32), ("n_roles", ctypes.c_int32)]
 
 
 class ImArrivals(ctypes.Structure):
     _fields_ = [("offsets", ctypes.c_void_p), ("q_idx", ctypes.c_void_p),
                 ("budget", ctypes.c_void_p), ("base_svc", ctypes.c_void_p),
-                ("n_total", ctypes.c_int32)]
+                ("role", ctypes.c_void_p), ("n_total", ctypes.c_int32)]
+
+
+# im_dual_net fields, in order, and the workload parameter names they take.
+DUAL_FIELDS = (("W_sem", "W_sem"), ("b_sem", "b_sem"), ("ln_sem_gain", "g_sem"),
+               ("ln_sem_bias", "be_sem"), ("W_bud", "W_bud"), ("b_bud", "b_bud"),
+               ("W_sys", "W_sys"), ("b_sys", "b_sys"), ("W_res", "W_res"), ("b_res", "b_res"),
+               ("ln_res_gain", "g_res"), ("ln_res_bias", "be_res"), ("W_merge", "W_merge"),
+               ("b_merge", "b_merge"), ("W_act", "W_act"), ("b_act", "b_act"))
+
+
+class ImDualNet(ctypes.Structure):
+    _fields_ = [(f, ctypes.c_void_p) for f, _ in DUAL_FIELDS] + [("role_emb", ctypes.c_void_p)]
 
 
 class ImPolicyOut(ctypes.Structure):
@@ -76,6 +90,8 @@ def load() -> ctypes.CDLL:
     P, I32, I64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
     L.im_pool_create.argtypes = [ctypes.POINTER(ImPoolDesc), P, P, P, I64, P, P, P,
                                  ctypes.POINTER(P)]
+    L.im_pool_create_dual.argtypes = [ctypes.POINTER(ImPoolDesc), ctypes.POINTER(ImDualNet), P, I64,
+                                      P, P, P, ctypes.POINTER(P)]
     L.im_route.argtypes = [P, ctypes.POINTER(ImArrivals), P, P, P]
     L.im_route_sample.argtypes = [P, ctypes.POINTER(ImArrivals), ctypes.c_uint64, I32,
                                   ctypes.POINTER(ImPolicyOut), P]
@@ -132,28 +148,33 @@ def make_desc(cfg: dict) -> ImPoolDesc:
     d.n_envs, d.n_models, d.n_depths = cfg["E"], cfg["M"], cfg["K"]
     d.queue_cap, d.max_slots = cfg["qcap"], cfg["max_slots"]
     d.embed_dim, d.feat_dim = cfg["embed_dim"], cfg["feat_dim"]
-    d.n_layers = len(cfg["widths"])
-    for i, w in enumerate(cfg["widths"]):
-        d.widths[i] = w
     d.dtype = IM_BF16 if cfg["dtype"] == "bf16" else IM_F32
     d.key_mode = KEY_MODES[cfg["key_mode"]]
     d.max_arrivals_per_env_tick = cfg["max_arrivals"]
     d.budget_max = cfg["budget_max"]
     vh = 1 if cfg.get("value_head") else 0
     d.value_head = vh
+    if cfg.get("net") == "dual":
+        d.net, d.n_roles = IM_NET_DUAL, cfg["n_roles"]
+        return d
+    d.n_layers = len(cfg["widths"])
+    for i, w in enumerate(cfg["widths"]):
+        d.widths[i] = w
     d.widths[d.n_layers - 1] = cfg["widths"][-1] + vh
     return d
 
 
-def make_arrivals(offsets, q_idx, budget, base_svc) -> ImArrivals:
-    """Arrivals of one tick from device tensors (int32, int32, int16, int16)."""
+def make_arrivals(offsets, q_idx, budget, base_svc, role=None) -> ImArrivals:
+    """Arrivals of one tick from device tensors (int32, int32, int16, int16
+    and, for dual-pathway pools, int16 roles)."""
     a = ImArrivals()
     a.offsets = offsets.data_ptr()
     a.q_idx = q_idx.data_ptr() if q_idx.numel() else None
     a.budget = budget.data_ptr() if budget.numel() else None
     a.base_svc = base_svc.data_ptr() if base_svc.numel() else None
+    a.role = role.data_ptr() if role is not None and role.numel() else None
     a.n_total = int(q_idx.numel())
-    a._keep = (offsets, q_idx, budget, base_svc)
+    a._keep = (offsets, q_idx, budget, base_svc, role)
     return a
 
 
@@ -173,6 +194,24 @@ def im_pool_create(desc: ImPoolDesc, W, b, emb, n_queries: int, capacity, logit_
                             ctypes.cast(bp, ctypes.c_void_p), _dptr(emb), int(n_queries),
                             _hptr(cap), None if lb is None else _hptr(lb), _stream(stream),
                             ctypes.byref(out)))
+    return out
+
+
+def im_pool_create_dual(desc: ImPoolDesc, params: dict, roles, emb, n_queries: int, capacity,
+                        logit_bias=None, stream=None) -> ctypes.c_void_p:
+    """params: host float32 arrays of the dual-pathway executor (names of
+    workload.gen.dual_weights); roles: host float32 [n_roles, E_d]; emb: device
+    tensor (borrowed); capacity: host int32 [E*M]."""
+    L = load()
+    keep = {f: np.ascontiguousarray(params[k], np.float32) for f, k in DUAL_FIELDS}
+    keep["role_emb"] = np.ascontiguousarray(roles, np.float32)
+    net = ImDualNet(**{f: v.ctypes.data for f, v in keep.items()})
+    cap = np.ascontiguousarray(capacity, np.int32).reshape(-1)
+    lb = None if logit_bias is None else np.ascontiguousarray(logit_bias, np.float32)
+    out = ctypes.c_void_p()
+    _check(L.im_pool_create_dual(ctypes.byref(desc), ctypes.byref(net), _dptr(emb), int(n_queries),
+                                 _hptr(cap), None if lb is None else _hptr(lb), _stream(stream),
+                                 ctypes.byref(out)))
     return out
 
 

@@ -50,6 +50,29 @@ enum { C_REJ_OVERFLOW = 0, C_ENQUEUED, C_STARTED, C_COMPLETED, C_SLO_MET, C_LAT_
 // Slot in device memory: {id (-1 free), t_arr, tick at which it completes, budget};
 // the state export reports the service ticks left instead of the completion tick.
 
+// Dual-pathway executor (Sec. 4.2): fixed widths of the paper.
+constexpr int kDualSem = 128, kDualBud = 16, kDualSys = 16, kDualRes = 64, kDualMerge = 128;
+// Its fp32 parameter block (offsets in floats). Vectors in accumulator-register
+// order [tile][g][16] (feature 32 tile + 8 (v / 4) + 4 g + v % 4 at index
+// (2 tile + g) 16 + v). The first DP_LDS floats are staged in LDS.
+enum {
+  DP_LN_SEM_G = 0,      // [128] semantic LayerNorm gain
+  DP_LN_SEM_B = 128,    // [128] semantic LayerNorm bias
+  DP_B_RES = 256,       // [64] resource layer bias
+  DP_LN_RES_G = 320,    // [64] resource LayerNorm gain
+  DP_LN_RES_B = 384,    // [64] resource LayerNorm bias
+  DP_B_MERGE = 448,     // [128] merge bias
+  DP_B_ACT = 576,       // [32] action/value bias (+ per-model logit bias on action rows)
+  DP_LDS = 608,
+  DP_W_BUD = 608,       // [16] budget head (natural order)
+  DP_B_BUD = 624,       // [16]
+  DP_B_SYS = 640,       // [16] system head bias (natural order)
+  DP_W_SYS = 656        // [3M][16]: W_sys column of snapshot feature k (k < 3M), rows 0..15
+};
+// Role projections: [n_roles][4][2][16] = b_sem + W_sem[:, E_d:] e_r per role,
+// in accumulator order, after the system head weights (64-byte aligned).
+__host__ __device__ inline int dual_role_offset(int M) { return (DP_W_SYS + 3 * M * 16 + 15) & ~15; }
+
 struct RouteArgs {
   const int32_t* offsets;
   const int32_t* q_idx;
@@ -77,6 +100,13 @@ struct RouteArgs {
   float* logp;
   float* entropy;
   float* value;                       // row A of the last layer (value head), or NULL
+  // dual-pathway executor (net == IM_NET_DUAL): W[0] semantic (query half),
+  // W[1] merge, W[2] action/value fragments; W_res resource-layer fragments
+  int32_t net;
+  const int16_t* role;
+  int32_t n_roles;
+  const void* W_res;
+  const float* dual_p;                // fp32 parameter block (DP_* offsets)
 };
 
 struct SchedArgs {
@@ -96,6 +126,8 @@ struct SchedArgs {
   int4* front;        // [E*M*kFront]
   int4* pool;         // [E*M*qcap]
   uint8_t* rpm_ring;  // [E*M*kRpmRing]: dispatches at tick tau in byte tau % kRpmWindow
+  const int16_t* role;  // per-row role (dual-pathway pools; NULL otherwise)
+  int32_t n_roles;
   int32_t* err;
   float* snap;        // [E * snap_stride(M)]
   float inv_qcap, inv_lat;
@@ -108,6 +140,12 @@ struct SchedArgs {
 hipError_t launch_dual_update(const int64_t* cnt, int64_t n_em, unsigned long long* acc, int64_t* last,
                               double eta, double lambda_max, double* lambda, hipStream_t s);
 bool route_supported(int dtype, int hidden, int n_layers, int out_tiles);
+bool dual_supported(int embed_dim, int out_rows);
+// Role projections of the dual-pathway executor: out[r][tile][g][16] =
+// b_sem + W_sem[:, E_d:] e_r in fp32 for every role r (bf16 inputs).
+//   w_role [128 x E_d] bf16 bits, roles [n_roles x E_d] bf16 bits, b_sem [128]
+hipError_t launch_role_projection(const uint16_t* w_role, const uint16_t* roles, const float* b_sem,
+                                  int n_roles, int embed_dim, float* out, hipStream_t s);
 hipError_t launch_route(const RouteArgs& a, int dtype, int hidden, int n_layers, int out_tiles,
                         hipStream_t s);
 // rpm: some model of the pool is (or was) rate-limited (blackbox windows tracked)

@@ -39,6 +39,8 @@ struct im_pool {
   int32_t* err = nullptr;
   int32_t* act_buf = nullptr;
   int64_t act_cap = 0;
+  void* W_res = nullptr;                    // dual-pathway executor: resource-layer fragments
+  float* dual_p = nullptr;                  // dual-pathway executor: fp32 parameter block
   unsigned long long* dual_acc = nullptr;   // [2] completions, Q16 cost (zero between calls)
   int64_t* dual_last = nullptr;             // [2] totals at the previous dual update
   int32_t t = 0;
@@ -118,6 +120,8 @@ im_status check_arrivals(im_pool* p, const im_arrivals* arr) {
   if (!arr->offsets) return fail(p, IM_EINVAL, "offsets is NULL");
   if (arr->n_total > 0 && (!arr->q_idx || !arr->budget || !arr->base_svc))
     return fail(p, IM_EINVAL, "arrival field pointer is NULL");
+  if (arr->n_total > 0 && p->d.net == IM_NET_DUAL && !arr->role)
+    return fail(p, IM_EINVAL, "role is NULL (required by a dual-pathway pool)");
   if ((int64_t)arr->n_total > (int64_t)p->d.n_envs * p->d.max_arrivals_per_env_tick)
     return fail(p, IM_EINVAL, "n_total exceeds n_envs * max_arrivals_per_env_tick");
   return IM_OK;
@@ -130,9 +134,98 @@ void free_pool(im_pool* p) {
   }
   void* bufs[] = {p->inv_tab, p->ms, p->cnt, p->env_cnt, p->hist, p->slots,
                   p->front, p->qpool, p->snap, p->err, p->act_buf, p->dual_acc, p->dual_last,
-                  p->rpm_ring};
+                  p->rpm_ring, p->W_res, p->dual_p};
   for (void* b : bufs) if (b) (void)hipFree(b);
   delete p;
+}
+
+// Checks shared by both pool constructors (everything but the policy).
+im_status check_desc_common(const im_pool_desc& d, int64_t n_queries, const int32_t* capacity) {
+  const int A = d.n_models * d.n_depths;
+  if (d.n_envs < 1 || d.n_models < 1 || d.n_models > IM_MAX_MODELS || d.n_depths < 1 ||
+      d.n_depths > IM_MAX_DEPTHS || A > IM_MAX_ACTIONS)
+    return fail(nullptr, IM_EINVAL, "n_envs/n_models/n_depths out of range");
+  if (d.queue_cap < 1 || d.queue_cap > IM_MAX_QCAP) return fail(nullptr, IM_EINVAL, "queue_cap out of range");
+  if (d.max_slots < 1 || d.max_slots > IM_MAX_SLOTS) return fail(nullptr, IM_EINVAL, "max_slots out of range");
+  if (d.embed_dim < 1) return fail(nullptr, IM_EINVAL, "embed_dim < 1");
+  if (d.value_head != 0 && d.value_head != 1) return fail(nullptr, IM_EINVAL, "value_head must be 0 or 1");
+  if (d.key_mode < IM_KEY_SLACK || d.key_mode > IM_KEY_FCFS) return fail(nullptr, IM_EINVAL, "bad key_mode");
+  if (d.max_arrivals_per_env_tick < 1) return fail(nullptr, IM_EINVAL, "max_arrivals_per_env_tick < 1");
+  if (d.budget_max < 1) return fail(nullptr, IM_EINVAL, "budget_max < 1");
+  if (n_queries < 1 || n_queries > INT32_MAX) return fail(nullptr, IM_EINVAL, "n_queries out of range");
+  for (int64_t i = 0; i < (int64_t)d.n_envs * d.n_models; ++i)
+    if (capacity[i] < 0 || capacity[i] > d.max_slots)
+      return fail(nullptr, IM_EINVAL, "capacity outside [0, max_slots]");
+  return IM_OK;
+}
+
+im_pool* new_pool(const im_pool_desc& d, int64_t n_queries, const void* emb) {
+  im_pool* p = new im_pool();
+  p->d = d;
+  p->A = d.n_models * d.n_depths;
+  p->S = d.max_slots;
+  p->Q = n_queries;
+  p->emb = emb;
+  (void)hipGetDevice(&p->device);
+  if (hipDeviceGetAttribute(&p->cu_count, hipDeviceAttributeMultiprocessorCount, p->device) !=
+      hipSuccess)
+    p->cu_count = 0;
+  return p;
+}
+
+// Feature reciprocals (each rounded once from fp64 to fp32), the zero state
+// and the initial snapshot rows.
+im_status init_state(im_pool* p, const int32_t* capacity, hipStream_t s) {
+  const im_pool_desc& d = p->d;
+  im_status st = IM_OK;
+  p->inv_qcap = (float)(1.0 / d.queue_cap);
+  p->inv_lat = (float)(1.0 / (256.0 * d.budget_max));
+  p->inv_bud = (float)(1.0 / d.budget_max);
+  {
+    std::vector<float> tab(2 * (IM_MAX_SLOTS + 1));
+    for (int c = 0; c <= IM_MAX_SLOTS; ++c) {
+      const int cc = std::max(c, 1);
+      tab[c] = (float)(1.0 / cc);
+      tab[IM_MAX_SLOTS + 1 + c] = (float)(1.0 / ((double)cc * d.budget_max));
+    }
+    st = upload(p, &p->inv_tab, tab);
+  }
+  const size_t EM = (size_t)d.n_envs * d.n_models;
+  if (st == IM_OK) {
+    std::vector<ModelRec> recs(EM);
+    std::memset(recs.data(), 0, EM * sizeof(ModelRec));
+    for (size_t i = 0; i < EM; ++i) {
+      recs[i].cap = capacity[i];
+      recs[i].enabled = 1;
+      recs[i].next_done = INT32_MAX;
+    }
+    st = upload(p, &p->ms, recs);
+  }
+  if (st == IM_OK) st = zalloc(p, &p->cnt, EM * im::C_NUM);
+  if (st == IM_OK) st = zalloc(p, &p->env_cnt, (size_t)d.n_envs * 2);
+  if (st == IM_OK) st = zalloc(p, &p->hist, (size_t)d.n_envs * p->A);
+  if (st == IM_OK) {
+    std::vector<int4> sl(EM * d.max_slots, make_int4(-1, 0, 0, 0));
+    st = upload(p, &p->slots, sl);
+  }
+  if (st == IM_OK) st = zalloc(p, &p->front, EM * im::kFront);
+  if (st == IM_OK) st = zalloc(p, &p->qpool, EM * (size_t)d.queue_cap);
+  if (st == IM_OK) st = zalloc(p, &p->rpm_ring, EM * (size_t)im::kRpmRing);
+  if (st == IM_OK) st = zalloc(p, &p->snap, (size_t)d.n_envs * im::snap_stride(d.n_models));
+  if (st == IM_OK) st = zalloc(p, &p->err, 1);
+  if (st == IM_OK) st = zalloc(p, &p->dual_acc, 2);
+  if (st == IM_OK) st = zalloc(p, &p->dual_last, 2);
+  if (st == IM_OK) {
+    p->act_cap = (int64_t)d.n_envs * d.max_arrivals_per_env_tick;
+    st = zalloc(p, &p->act_buf, (size_t)p->act_cap);
+  }
+  if (st == IM_OK) {
+    hipError_t e = hipDeviceSynchronize();
+    if (e == hipSuccess) e = im::launch_snapshot(sched_args(p), 0, d.n_envs, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) st = hip_fail(p, e, "initial snapshot");
+  }
+  return st;
 }
 
 }  // namespace
@@ -145,46 +238,27 @@ im_status im_pool_create(const im_pool_desc* desc, const float* const* W, const 
   if (!desc || !W || !b || !emb || !capacity || !out)
     return fail(nullptr, IM_EINVAL, "NULL argument to im_pool_create");
   const im_pool_desc& d = *desc;
+  im_status st0 = check_desc_common(d, n_queries, capacity);
+  if (st0 != IM_OK) return st0;
+  if (d.net != IM_NET_MLP) return fail(nullptr, IM_EINVAL, "net must be IM_NET_MLP (dual: im_pool_create_dual)");
   const int A = d.n_models * d.n_depths;
-  if (d.n_envs < 1 || d.n_models < 1 || d.n_models > IM_MAX_MODELS || d.n_depths < 1 ||
-      d.n_depths > IM_MAX_DEPTHS || A > IM_MAX_ACTIONS)
-    return fail(nullptr, IM_EINVAL, "n_envs/n_models/n_depths out of range");
-  if (d.queue_cap < 1 || d.queue_cap > IM_MAX_QCAP) return fail(nullptr, IM_EINVAL, "queue_cap out of range");
-  if (d.max_slots < 1 || d.max_slots > IM_MAX_SLOTS) return fail(nullptr, IM_EINVAL, "max_slots out of range");
-  if (d.embed_dim < 1 || d.feat_dim > IM_MAX_FEAT || d.feat_dim < d.embed_dim + 4 * d.n_models + 1)
+  if (d.feat_dim > IM_MAX_FEAT || d.feat_dim < d.embed_dim + 4 * d.n_models + 1)
     return fail(nullptr, IM_EINVAL, "feat_dim must be in [embed_dim + 4M + 1, IM_MAX_FEAT]");
   if (d.n_layers != 2 && d.n_layers != 3) return fail(nullptr, IM_EINVAL, "n_layers must be 2 or 3");
-  if (d.value_head != 0 && d.value_head != 1) return fail(nullptr, IM_EINVAL, "value_head must be 0 or 1");
   if (d.widths[d.n_layers - 1] != A + d.value_head)
     return fail(nullptr, IM_EINVAL, "last width must be M*K + value_head");
   if (d.n_layers == 3 && d.widths[0] != d.widths[1])
     return fail(nullptr, IM_EUNSUPPORTED, "hidden widths must be equal");
   if (d.dtype != IM_F32 && d.dtype != IM_BF16) return fail(nullptr, IM_EINVAL, "bad dtype");
-  if (d.key_mode < IM_KEY_SLACK || d.key_mode > IM_KEY_FCFS) return fail(nullptr, IM_EINVAL, "bad key_mode");
-  if (d.max_arrivals_per_env_tick < 1) return fail(nullptr, IM_EINVAL, "max_arrivals_per_env_tick < 1");
-  if (d.budget_max < 1) return fail(nullptr, IM_EINVAL, "budget_max < 1");
-  if (n_queries < 1 || n_queries > INT32_MAX) return fail(nullptr, IM_EINVAL, "n_queries out of range");
   const int H = d.widths[0];
   const int out_tiles = (A + d.value_head + 31) / 32;
   if (!im::route_supported(d.dtype, H, d.n_layers, out_tiles))
     return fail(nullptr, IM_EUNSUPPORTED, "no route kernel for this dtype / hidden width");
-  for (int64_t i = 0; i < (int64_t)d.n_envs * d.n_models; ++i)
-    if (capacity[i] < 0 || capacity[i] > d.max_slots)
-      return fail(nullptr, IM_EINVAL, "capacity outside [0, max_slots]");
 
-  im_pool* p = new im_pool();
-  p->d = d;
-  p->A = A;
-  p->S = d.max_slots;
+  im_pool* p = new_pool(d, n_queries, emb);
   p->hidden = H;
   p->n_layers = d.n_layers;
   p->out_tiles = out_tiles;
-  p->Q = n_queries;
-  p->emb = emb;
-  (void)hipGetDevice(&p->device);
-  if (hipDeviceGetAttribute(&p->cu_count, hipDeviceAttributeMultiprocessorCount, p->device) !=
-      hipSuccess)
-    p->cu_count = 0;
   hipStream_t s = (hipStream_t)stream;
   im_status st = IM_OK;
 
@@ -237,55 +311,142 @@ im_status im_pool_create(const im_pool_desc* desc, const float* const* W, const 
     st = upload(p, &p->bias[l], bp);
     in = outw;
   }
-  // ---- feature reciprocals, each rounded once from fp64 to fp32 ----
+  if (st == IM_OK) st = init_state(p, capacity, s);
+  if (st != IM_OK) {
+    g_create_error = p->last_error;
+    free_pool(p);
+    return st;
+  }
+  *out = p;
+  return IM_OK;
+}
+
+im_status im_pool_create_dual(const im_pool_desc* desc, const im_dual_net* net, const void* emb,
+                              int64_t n_queries, const int32_t* capacity, const float* logit_bias,
+                              void* stream, im_pool** out) {
+  if (!desc || !net || !emb || !capacity || !out)
+    return fail(nullptr, IM_EINVAL, "NULL argument to im_pool_create_dual");
+  const im_pool_desc& d = *desc;
+  im_status st0 = check_desc_common(d, n_queries, capacity);
+  if (st0 != IM_OK) return st0;
+  if (d.net != IM_NET_DUAL) return fail(nullptr, IM_EINVAL, "net must be IM_NET_DUAL");
+  if (d.n_roles < 1 || d.n_roles > IM_MAX_ROLES) return fail(nullptr, IM_EINVAL, "n_roles out of range");
+  const float* need[] = {net->W_sem, net->b_sem, net->ln_sem_gain, net->ln_sem_bias, net->W_bud,
+                         net->b_bud, net->W_sys, net->b_sys, net->W_res, net->b_res, net->ln_res_gain,
+                         net->ln_res_bias, net->W_merge, net->b_merge, net->W_act, net->b_act,
+                         net->role_emb};
+  for (const float* q : need)
+    if (!q) return fail(nullptr, IM_EINVAL, "NULL parameter in im_dual_net");
+  if (d.dtype != IM_BF16) return fail(nullptr, IM_EUNSUPPORTED, "the dual-pathway executor runs in bf16 only");
+  const int A = d.n_models * d.n_depths;
+  const int Ao = A + d.value_head;
+  if (!im::dual_supported(d.embed_dim, Ao))
+    return fail(nullptr, IM_EUNSUPPORTED, "dual-pathway executor: embed_dim must be 64, 128, 256 or 384 and M*K + value_head <= 32");
+
+  im_pool* p = new_pool(d, n_queries, emb);
+  p->d.feat_dim = d.embed_dim + 4 * d.n_models + 1;
+  p->d.n_layers = 0;
+  hipStream_t s = (hipStream_t)stream;
+  im_status st = IM_OK;
+  const int Ed = d.embed_dim, M = d.n_models, KBQ = Ed / 16;
+  using im::kDualSem;
+  using im::kDualRes;
+  using im::kDualMerge;
+  // query half of W_sem: K step kb = 4 G + i of lane half g holds elements
+  // 64 G + 32 g + 8 i + j (each lane reads 64 contiguous bytes per group)
+  {
+    std::vector<uint16_t> pk((size_t)4 * KBQ * 64 * 8);
+    for (int T = 0; T < 4; ++T)
+      for (int kb = 0; kb < KBQ; ++kb)
+        for (int lane = 0; lane < 64; ++lane)
+          for (int j = 0; j < 8; ++j) {
+            const int o = 32 * T + (lane & 31);
+            const int k = 64 * (kb >> 2) + 32 * (lane >> 5) + 8 * (kb & 3) + j;
+            pk[(((size_t)T * KBQ + kb) * 64 + lane) * 8 + j] = to_bf16(net->W_sem[(size_t)o * 2 * Ed + k]);
+          }
+    st = upload(p, (uint16_t**)&p->W[0], pk);
+  }
+  // fragments of a layer whose input is (layer > 0) a previous accumulator or
+  // (layer == 0) a vector in natural order
+  auto pack = [&](const float* Wm, int outw, int in, int layer, int TO, void** dst) {
+    const int KB = in / 16;
+    std::vector<uint16_t> pk((size_t)TO * KB * 64 * 8, 0);
+    for (int T = 0; T < TO; ++T)
+      for (int kb = 0; kb < KB; ++kb)
+        for (int lane = 0; lane < 64; ++lane)
+          for (int j = 0; j < 8; ++j) {
+            const int o = 32 * T + (lane & 31);
+            const int k = bf16_k(layer, kb, lane >> 5, j);
+            if (o < outw) pk[(((size_t)T * KB + kb) * 64 + lane) * 8 + j] = to_bf16(Wm[(size_t)o * in + k]);
+          }
+    return upload(p, (uint16_t**)dst, pk);
+  };
+  if (st == IM_OK) st = pack(net->W_merge, kDualMerge, kDualSem + kDualRes, 1, 4, &p->W[1]);
+  if (st == IM_OK) st = pack(net->W_act, Ao, kDualMerge, 1, 1, &p->W[2]);
+  if (st == IM_OK) st = pack(net->W_res, kDualRes, 32, 0, 2, &p->W_res);
+  // fp32 parameter block
+  const int roff = im::dual_role_offset(M);
+  std::vector<float> dp((size_t)roff + (size_t)d.n_roles * kDualSem, 0.f);
+  auto acc_order = [&](int off, const float* v, int width, int tiles, bool logit) {
+    for (int T = 0; T < tiles; ++T)
+      for (int g = 0; g < 2; ++g)
+        for (int vv = 0; vv < 16; ++vv) {
+          const int o = 32 * T + 8 * (vv >> 2) + 4 * g + (vv & 3);
+          if (o >= width) continue;
+          float x = v[o];
+          if (logit && logit_bias && o < A) x += logit_bias[o / d.n_depths];
+          dp[off + (T * 2 + g) * 16 + vv] = x;
+        }
+  };
+  auto bfv = [](float x) {
+    const uint32_t u = (uint32_t)to_bf16(x) << 16;
+    float f;
+    std::memcpy(&f, &u, 4);
+    return f;
+  };
+  acc_order(im::DP_LN_SEM_G, net->ln_sem_gain, kDualSem, 4, false);
+  acc_order(im::DP_LN_SEM_B, net->ln_sem_bias, kDualSem, 4, false);
+  acc_order(im::DP_B_RES, net->b_res, kDualRes, 2, false);
+  acc_order(im::DP_LN_RES_G, net->ln_res_gain, kDualRes, 2, false);
+  acc_order(im::DP_LN_RES_B, net->ln_res_bias, kDualRes, 2, false);
+  acc_order(im::DP_B_MERGE, net->b_merge, kDualMerge, 4, false);
+  acc_order(im::DP_B_ACT, net->b_act, Ao, 1, true);
+  for (int k = 0; k < 16; ++k) {
+    dp[im::DP_W_BUD + k] = bfv(net->W_bud[k]);
+    dp[im::DP_B_BUD + k] = net->b_bud[k];
+    dp[im::DP_B_SYS + k] = net->b_sys[k];
+  }
+  // system head column of snapshot feature k = stat * M + m: the paper's
+  // input order is [queue depth | end-to-end latency | KV-cache use], the
+  // snapshot's [queue depth | busy / c_m | latency EWMA]
+  for (int k = 0; k < 3 * M; ++k) {
+    const int stat = k / M, m = k % M;
+    const int col = stat == 0 ? m : (stat == 1 ? 2 * M + m : M + m);
+    for (int r = 0; r < 16; ++r) dp[im::DP_W_SYS + k * 16 + r] = bfv(net->W_sys[(size_t)r * 3 * M + col]);
+  }
+  if (st == IM_OK) st = upload(p, &p->dual_p, dp);
+  // role projections b_sem + W_sem[:, E_d:] e_r, computed on the device
   if (st == IM_OK) {
-    p->inv_qcap = (float)(1.0 / d.queue_cap);
-    p->inv_lat = (float)(1.0 / (256.0 * d.budget_max));
-    p->inv_bud = (float)(1.0 / d.budget_max);
-    std::vector<float> tab(2 * (IM_MAX_SLOTS + 1));
-    for (int c = 0; c <= IM_MAX_SLOTS; ++c) {
-      const int cc = std::max(c, 1);
-      tab[c] = (float)(1.0 / cc);
-      tab[IM_MAX_SLOTS + 1 + c] = (float)(1.0 / ((double)cc * d.budget_max));
+    std::vector<uint16_t> wr((size_t)kDualSem * Ed), rt((size_t)d.n_roles * Ed);
+    for (int o = 0; o < kDualSem; ++o)
+      for (int k = 0; k < Ed; ++k) wr[(size_t)o * Ed + k] = to_bf16(net->W_sem[(size_t)o * 2 * Ed + Ed + k]);
+    for (size_t i = 0; i < rt.size(); ++i) rt[i] = to_bf16(net->role_emb[i]);
+    uint16_t *dwr = nullptr, *drt = nullptr;
+    float* dbs = nullptr;
+    std::vector<float> bs(net->b_sem, net->b_sem + kDualSem);
+    st = upload(p, &dwr, wr);
+    if (st == IM_OK) st = upload(p, &drt, rt);
+    if (st == IM_OK) st = upload(p, &dbs, bs);
+    if (st == IM_OK) {
+      hipError_t e = im::launch_role_projection(dwr, drt, dbs, d.n_roles, Ed, p->dual_p + roff, s);
+      if (e == hipSuccess) e = hipStreamSynchronize(s);
+      if (e != hipSuccess) st = hip_fail(p, e, "role projection");
     }
-    st = upload(p, &p->inv_tab, tab);
+    if (dwr) (void)hipFree(dwr);
+    if (drt) (void)hipFree(drt);
+    if (dbs) (void)hipFree(dbs);
   }
-  // ---- state ----
-  const size_t EM = (size_t)d.n_envs * d.n_models;
-  if (st == IM_OK) {
-    std::vector<ModelRec> recs(EM);
-    std::memset(recs.data(), 0, EM * sizeof(ModelRec));
-    for (size_t i = 0; i < EM; ++i) {
-      recs[i].cap = capacity[i];
-      recs[i].enabled = 1;
-      recs[i].next_done = INT32_MAX;
-    }
-    st = upload(p, &p->ms, recs);
-  }
-  if (st == IM_OK) st = zalloc(p, &p->cnt, EM * im::C_NUM);
-  if (st == IM_OK) st = zalloc(p, &p->env_cnt, (size_t)d.n_envs * 2);
-  if (st == IM_OK) st = zalloc(p, &p->hist, (size_t)d.n_envs * A);
-  if (st == IM_OK) {
-    std::vector<int4> sl(EM * d.max_slots, make_int4(-1, 0, 0, 0));
-    st = upload(p, &p->slots, sl);
-  }
-  if (st == IM_OK) st = zalloc(p, &p->front, EM * im::kFront);
-  if (st == IM_OK) st = zalloc(p, &p->qpool, EM * (size_t)d.queue_cap);
-  if (st == IM_OK) st = zalloc(p, &p->rpm_ring, EM * (size_t)im::kRpmRing);
-  if (st == IM_OK) st = zalloc(p, &p->snap, (size_t)d.n_envs * im::snap_stride(d.n_models));
-  if (st == IM_OK) st = zalloc(p, &p->err, 1);
-  if (st == IM_OK) st = zalloc(p, &p->dual_acc, 2);
-  if (st == IM_OK) st = zalloc(p, &p->dual_last, 2);
-  if (st == IM_OK) {
-    p->act_cap = (int64_t)d.n_envs * d.max_arrivals_per_env_tick;
-    st = zalloc(p, &p->act_buf, (size_t)p->act_cap);
-  }
-  if (st == IM_OK) {
-    hipError_t e = hipDeviceSynchronize();
-    if (e == hipSuccess) e = im::launch_snapshot(sched_args(p), 0, d.n_envs, s);
-    if (e == hipSuccess) e = hipStreamSynchronize(s);
-    if (e != hipSuccess) st = hip_fail(p, e, "initial snapshot");
-  }
+  if (st == IM_OK) st = init_state(p, capacity, s);
   if (st != IM_OK) {
     g_create_error = p->last_error;
     free_pool(p);
@@ -326,6 +487,13 @@ static im::RouteArgs route_args(im_pool* p, const im_arrivals* arr, int32_t* act
   a.logits = logits;
   a.err = p->err;
   a.persistent_blocks = p->cu_count;
+  a.net = p->d.net;
+  if (p->d.net == IM_NET_DUAL) {
+    a.role = arr->role;
+    a.n_roles = p->d.n_roles;
+    a.W_res = p->W_res;
+    a.dual_p = p->dual_p;
+  }
   return a;
 }
 
@@ -375,6 +543,10 @@ im_status im_schedule(im_pool* p, const im_arrivals* arr, const int32_t* actions
   a.base_svc = arr->base_svc;
   a.actions = actions;
   a.n_total = arr->n_total;
+  if (p->d.net == IM_NET_DUAL) {
+    a.role = arr->role;
+    a.n_roles = p->d.n_roles;
+  }
   IM_HIP(p, im::launch_schedule(a, p->rpm_active, (hipStream_t)stream));
   p->t += 1;
   return IM_OK;

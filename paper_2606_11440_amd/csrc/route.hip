@@ -38,7 +38,7 @@ __device__ __forceinline__ f32x16 mfma_f32(float a, float b, f32x16 c) {
 struct RowCtx {
   int32_t r;        // request row (tail lanes: >= n_total)
   bool live;        // r < n_total
-  bool bad_q;       // q_idx out of range
+  int32_t bad;      // error bits of the row (IM_ERR_QIDX, IM_ERR_ROLE); 0 when valid
   int32_t e;        // env of the row
   int32_t q;        // embedding row (0 when bad)
   int32_t budget;
@@ -119,8 +119,8 @@ __device__ __forceinline__ RowCtx row_setup(const RouteArgs& a, int32_t row0, in
   find_envs<1>(a, row0, rl, rows, env);
   c.e = env[0];
   const int32_t q = a.q_idx[rr];
-  c.bad_q = q < 0 || (int64_t)q >= a.Q;
-  c.q = c.bad_q ? 0 : q;
+  c.bad = (q < 0 || (int64_t)q >= a.Q) ? IM_ERR_QIDX : 0;
+  c.q = c.bad ? 0 : q;
   c.budget = a.budget[rr];
   c.amask = action_mask(a, c.e);
   return c;
@@ -322,13 +322,13 @@ __device__ __forceinline__ void rl_outputs(const RouteArgs& a, const RowCtx& c,
   const int obsa = __shfl_xor(bsa, 32, 64);
   if (obsa >= 0 && (bsa < 0 || obs > bs || (obs == bs && obsa < bsa))) { bs = obs; bsa = obsa; bz = obz; }
   if (!c.live || g != 0) return;
-  const bool any = amax >= 0 && !c.bad_q;
+  const bool any = amax >= 0 && !c.bad;
   const float lse = any ? zmax + __logf(s) : 0.f;
   a.actions[c.r] = any ? bsa : -1;
-  if (c.bad_q) atomicOr(a.err, IM_ERR_QIDX);
+  if (c.bad) atomicOr(a.err, c.bad);
   if (a.logp) a.logp[c.r] = any ? bz - lse : 0.f;
   if (a.entropy) a.entropy[c.r] = any ? lse - sz / s : 0.f;
-  if (a.value) a.value[c.r] = c.bad_q ? 0.f : val;
+  if (a.value) a.value[c.r] = c.bad ? 0.f : val;
 }
 
 // Masked argmax over the lane pair (n, n + 32), logits store, action store
@@ -357,8 +357,8 @@ __device__ __forceinline__ void epilogue(const RouteArgs& a, const RowCtx& c, f3
   if (RL == 1 || (RL == 2 && a.rl)) {
     rl_outputs<AT>(a, c, acc, g, best, ba);
   } else if (c.live && g == 0) {
-    a.actions[c.r] = c.bad_q ? -1 : ba;
-    if (c.bad_q) atomicOr(a.err, IM_ERR_QIDX);
+    a.actions[c.r] = c.bad ? -1 : ba;
+    if (c.bad) atomicOr(a.err, c.bad);
   }
   if (!c.live) return;
   if (a.logits) {
@@ -368,7 +368,7 @@ __device__ __forceinline__ void epilogue(const RouteArgs& a, const RowCtx& c, f3
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int act = 32 * T + 8 * (v >> 2) + 4 * g + (v & 3);
-        if (act < a.A) out[act] = c.bad_q ? 0.f : acc[T][v];
+        if (act < a.A) out[act] = c.bad ? 0.f : acc[T][v];
       }
     }
   }
@@ -547,8 +547,8 @@ __device__ __forceinline__ RowCtx row_setup_env(const RouteArgs& a, int32_t r, i
   const int32_t rr = c.live ? r : a.n_total - 1;
   c.e = e;
   const int32_t q = a.q_idx[rr];
-  c.bad_q = q < 0 || (int64_t)q >= a.Q;
-  c.q = c.bad_q ? 0 : q;
+  c.bad = (q < 0 || (int64_t)q >= a.Q) ? IM_ERR_QIDX : 0;
+  c.q = c.bad ? 0 : q;
   c.budget = a.budget[rr];
   c.amask = action_mask(a, e);
   return c;
@@ -856,6 +856,265 @@ __global__ __launch_bounds__(NW * 64, 1) void route_bf16_stream(RouteArgs a) {
   __builtin_amdgcn_s_waitcnt(0);   // the prefetched first stage of a step that does not exist
 }
 
+// ---------------------------------------------------------------------------
+// The paper's dual-pathway executor (Sec. 4.2), persistent, on MFMA.
+//
+// Per request: a semantic pathway LN(ReLU(W_sem [e_q | e_r])) (128), a
+// resource pathway LN(ReLU(W_res [h_bud | h_sys])) (64) over a budget head and
+// a system head (16 each), a merge layer ReLU(W_merge [h_sem | h_res]) (128)
+// and the action/value rows. The role half of the semantic layer takes only
+// n_roles distinct inputs, so its products (plus b_sem) are computed once per
+// pool (role_projection_kernel) and enter as the accumulator's initial value;
+// the per-request semantic work is the 128 x E_d query half.
+//
+// A wave owns NR x 32 rows. The query-half, merge and action weights live in
+// LDS (152 KB at E_d = 384); the small resource-layer fragments, the system
+// head and the role projections are read through the caches. The query half
+// of W_sem is packed so that each lane reads its row's embedding in 64-byte
+// runs: within a 64-element group, lane half g takes elements 32 g .. 32 g + 31
+// as four K steps of 8, so the two lanes of a row consume one 128-byte line
+// per group. Groups are prefetched one ahead of the MFMAs that use them.
+// ---------------------------------------------------------------------------
+
+// fp32 -> bf16 (round to nearest even) -> fp32.
+__device__ __forceinline__ float bf16_round(float x) { return __uint_as_float(pack2(x, 0.f) << 16); }
+
+// ReLU, then LayerNorm over the 32 NT features a lane pair (n, n + 32) holds
+// in NT accumulator tiles: (u - mean) / sqrt(var + 1e-5) * gain + bias with
+// the biased variance, rounded to bf16 B fragments for the next layer
+// (fragment 2T + h holds registers 8h .. 8h + 7 of tile T).
+template <int NT>
+__device__ __forceinline__ void relu_ln_frags(f32x16 (&acc)[NT], const float* gain, const float* bias,
+                                              int g, u32x4 (&f)[2 * NT]) {
+  constexpr float inv_n = 1.f / (32 * NT);
+  float s = 0.f;
+#pragma unroll
+  for (int T = 0; T < NT; ++T) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      acc[T][v] = relu(acc[T][v]);
+      s += acc[T][v];
+    }
+  }
+  s += __shfl_xor(s, 32, 64);
+  const float mean = s * inv_n;
+  float q = 0.f;
+#pragma unroll
+  for (int T = 0; T < NT; ++T) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const float d = acc[T][v] - mean;
+      q = fmaf(d, d, q);
+    }
+  }
+  q += __shfl_xor(q, 32, 64);
+  const float rstd = rsqrtf(fmaf(q, inv_n, 1e-5f));
+#pragma unroll
+  for (int T = 0; T < NT; ++T) {
+    // one tile's gains and biases at a time: loads hoisted above this point
+    // would keep all of them live at once
+    asm volatile("" ::: "memory");
+    float y[16];
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int i = (T * 2 + g) * 16 + v;
+      y[v] = fmaf((acc[T][v] - mean) * rstd, gain[i], bias[i]);
+    }
+    f[2 * T].x = pack2(y[0], y[1]);     f[2 * T].y = pack2(y[2], y[3]);
+    f[2 * T].z = pack2(y[4], y[5]);     f[2 * T].w = pack2(y[6], y[7]);
+    f[2 * T + 1].x = pack2(y[8], y[9]);   f[2 * T + 1].y = pack2(y[10], y[11]);
+    f[2 * T + 1].z = pack2(y[12], y[13]); f[2 * T + 1].w = pack2(y[14], y[15]);
+    // the tile's fragments are complete before the next tile's loads issue
+    asm volatile("" : "+v"(f[2 * T]), "+v"(f[2 * T + 1]));
+  }
+}
+
+// The 4 K-step fragments of 64-element group G of a row's query embedding.
+template <int ED>
+__device__ __forceinline__ void load_group(const RouteArgs& a, const RowCtx& c, int G, int g, u32x4 (&x)[4]) {
+  const u32x4* src = (const u32x4*)((const uint16_t*)a.emb + (size_t)c.q * ED + 64 * G + 32 * g);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) x[i] = src[i];
+}
+
+template <int ED, int NW, int NR, int RL>
+__global__ __launch_bounds__(NW * 64, 1) void route_dual_bf16(RouteArgs a) {
+  static_assert(ED % 64 == 0, "embedding width must be a multiple of 64");
+  constexpr int KBQ = ED / 16;          // K steps of the query half
+  constexpr int NG = ED / 64;           // 64-element groups
+  constexpr int N_SEM = 4 * KBQ * 64;   // 16-byte fragments
+  constexpr int N_MRG = 4 * 12 * 64;
+  constexpr int N_ACT = 8 * 64;
+  constexpr int WROWS = 32 * NR;
+  constexpr int ROWS = NW * WROWS;
+  __shared__ u32x4 lds[N_SEM + N_MRG + N_ACT];
+  __shared__ float lp[DP_LDS];
+  copy_to_lds<N_SEM, NW * 64>(lds, (const u32x4*)a.W[0]);
+  copy_to_lds<N_MRG, NW * 64>(lds + N_SEM, (const u32x4*)a.W[1]);
+  copy_to_lds<N_ACT, NW * 64>(lds + N_SEM + N_MRG, (const u32x4*)a.W[2]);
+  for (int i = threadIdx.x; i < DP_LDS; i += NW * 64) lp[i] = a.dual_p[i];
+  __syncthreads();
+  const u32x4* wsem = lds;
+  const u32x4* wmrg = lds + N_SEM;
+  const u32x4* wact = wmrg + N_MRG;
+  const u32x4* wres = (const u32x4*)a.W_res;
+  const float* gp = a.dual_p;
+  const float* proj = gp + dual_role_offset(a.M);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int n = lane & 31, g = lane >> 5;
+  const int n_tiles = (a.n_total + ROWS - 1) / ROWS;
+  const int n3 = 3 * a.M;
+  const int sstride = snap_stride(a.M);
+
+  for (int tile = blockIdx.x; tile < n_tiles; tile += gridDim.x) {
+    asm volatile("" ::: "memory");
+    int ln = lane, gg = g;
+    asm volatile("" : "+v"(ln), "+v"(gg));
+    const int32_t r0 = tile * ROWS + wave * WROWS;
+    if (r0 >= a.n_total) continue;
+    const int32_t rlast = (r0 + WROWS - 1 < a.n_total ? r0 + WROWS - 1 : a.n_total - 1);
+    int32_t rows[NR], envs[NR];
+#pragma unroll
+    for (int j = 0; j < NR; ++j) rows[j] = r0 + 32 * j + n;
+    find_envs<NR>(a, r0, rlast, rows, envs);
+    RowCtx c[NR];
+    int32_t role[NR];
+#pragma unroll
+    for (int j = 0; j < NR; ++j) {
+      c[j] = row_setup_env(a, rows[j], envs[j]);
+      const int32_t ro = a.role[c[j].live ? rows[j] : a.n_total - 1];
+      const bool bad_r = ro < 0 || ro >= a.n_roles;
+      if (bad_r) c[j].bad |= IM_ERR_ROLE;
+      role[j] = bad_r ? 0 : ro;
+    }
+
+    // ---- semantic pathway: role projection + W_sem (query half) e_q ----
+    u32x4 xa[NR][4], xb[NR][4];
+#pragma unroll
+    for (int j = 0; j < NR; ++j) load_group<ED>(a, c[j], 0, gg, xa[j]);
+    f32x16 s[NR][4];
+#pragma unroll
+    for (int j = 0; j < NR; ++j) {
+#pragma unroll
+      for (int T = 0; T < 4; ++T) s[j][T] = *(const f32x16*)(proj + ((role[j] * 4 + T) * 2 + gg) * 16);
+    }
+#pragma unroll
+    for (int G = 0; G < NG; ++G) {
+      if (G + 1 < NG) {
+#pragma unroll
+        for (int j = 0; j < NR; ++j) load_group<ED>(a, c[j], G + 1, gg, xb[j]);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int kb = 4 * G + i;
+#pragma unroll
+        for (int T = 0; T < 4; ++T) {
+          const u32x4 w = wsem[(T * KBQ + kb) * 64 + ln];
+#pragma unroll
+          for (int j = 0; j < NR; ++j) s[j][T] = mfma_bf16(w, xa[j][i], s[j][T]);
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < NR; ++j) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) xa[j][i] = xb[j][i];
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    u32x4 hs[NR][8];
+#pragma unroll
+    for (int j = 0; j < NR; ++j) relu_ln_frags<4>(s[j], lp + DP_LN_SEM_G, lp + DP_LN_SEM_B, gg, hs[j]);
+    __builtin_amdgcn_sched_barrier(0);
+
+    // ---- resource pathway ----
+    u32x4 hr[NR][4];
+#pragma unroll
+    for (int j = 0; j < NR; ++j) {
+      asm volatile("" ::: "memory");
+      // budget head: features 8 gg .. 8 gg + 7 of h_bud (K step 0 of W_res)
+      const float bfe = bf16_round((float)c[j].budget * a.inv_bud);
+      float hb[8], hy[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        hb[k] = relu(fmaf(gp[DP_W_BUD + 8 * gg + k], bfe, gp[DP_B_BUD + 8 * gg + k]));
+        hy[k] = gp[DP_B_SYS + 8 * gg + k];
+      }
+      // system head: features 8 gg .. 8 gg + 7 of h_sys (K step 1) over the
+      // env's queue-depth, KV-proxy and latency features
+      const float* srow = a.snap + (size_t)c[j].e * sstride;
+      for (int k = 0; k < n3; ++k) {
+        const float d = bf16_round(srow[k]);
+        const float4 w0 = *(const float4*)(gp + DP_W_SYS + k * 16 + 8 * gg);
+        const float4 w1 = *(const float4*)(gp + DP_W_SYS + k * 16 + 8 * gg + 4);
+        hy[0] = fmaf(w0.x, d, hy[0]); hy[1] = fmaf(w0.y, d, hy[1]);
+        hy[2] = fmaf(w0.z, d, hy[2]); hy[3] = fmaf(w0.w, d, hy[3]);
+        hy[4] = fmaf(w1.x, d, hy[4]); hy[5] = fmaf(w1.y, d, hy[5]);
+        hy[6] = fmaf(w1.z, d, hy[6]); hy[7] = fmaf(w1.w, d, hy[7]);
+      }
+      u32x4 f0, f1;
+      f0.x = relu_pack2(hb[0], hb[1]); f0.y = relu_pack2(hb[2], hb[3]);
+      f0.z = relu_pack2(hb[4], hb[5]); f0.w = relu_pack2(hb[6], hb[7]);
+      f1.x = relu_pack2(hy[0], hy[1]); f1.y = relu_pack2(hy[2], hy[3]);
+      f1.z = relu_pack2(hy[4], hy[5]); f1.w = relu_pack2(hy[6], hy[7]);
+      f32x16 rr[2];
+#pragma unroll
+      for (int T = 0; T < 2; ++T) {
+        rr[T] = *(const f32x16*)(lp + DP_B_RES + (T * 2 + gg) * 16);
+        rr[T] = mfma_bf16(wres[(T * 2 + 0) * 64 + ln], f0, rr[T]);
+        rr[T] = mfma_bf16(wres[(T * 2 + 1) * 64 + ln], f1, rr[T]);
+      }
+      relu_ln_frags<2>(rr, lp + DP_LN_RES_G, lp + DP_LN_RES_B, gg, hr[j]);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+
+    // ---- decision: merge layer, then the action/value rows ----
+    u32x4 hh[NR][8];
+#pragma unroll
+    for (int T = 0; T < 4; ++T) {
+      f32x16 m[NR];
+      m[0] = *(const f32x16*)(lp + DP_B_MERGE + (T * 2 + gg) * 16);
+#pragma unroll
+      for (int j = 1; j < NR; ++j) m[j] = m[0];
+#pragma unroll
+      for (int kb = 0; kb < 12; ++kb) {
+        const u32x4 w = wmrg[(T * 12 + kb) * 64 + ln];
+#pragma unroll
+        for (int j = 0; j < NR; ++j) m[j] = mfma_bf16(w, kb < 8 ? hs[j][kb] : hr[j][kb - 8], m[j]);
+      }
+#pragma unroll
+      for (int j = 0; j < NR; ++j) relu_to_frags(m[j], hh[j][2 * T], hh[j][2 * T + 1]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    f32x16 o[NR][1];
+    o[0][0] = *(const f32x16*)(lp + DP_B_ACT + gg * 16);
+#pragma unroll
+    for (int j = 1; j < NR; ++j) o[j][0] = o[0][0];
+#pragma unroll
+    for (int kb = 0; kb < 8; ++kb) {
+      const u32x4 w = wact[kb * 64 + ln];
+#pragma unroll
+      for (int j = 0; j < NR; ++j) o[j][0] = mfma_bf16(w, hh[j][kb], o[j][0]);
+    }
+#pragma unroll
+    for (int j = 0; j < NR; ++j) epilogue<1, RL>(a, c[j], o[j], nullptr, gg);
+  }
+}
+
+// Role projections, one thread per (role, output feature): fp32 sum of the
+// bf16 products, stored in accumulator-register order.
+__global__ void role_projection_kernel(const uint16_t* w_role, const uint16_t* roles, const float* b_sem,
+                                       int n_roles, int ed, float* out) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n_roles * kDualSem) return;
+  const int r = i / kDualSem, o = i % kDualSem;
+  float acc = b_sem[o];
+  for (int k = 0; k < ed; ++k)
+    acc = fmaf(bf16_to_f32(w_role[(size_t)o * ed + k]), bf16_to_f32(roles[(size_t)r * ed + k]), acc);
+  // feature o = 32 T + 8 (v / 4) + 4 g + v % 4
+  const int T = o >> 5, w = o & 31, v = ((w >> 3) << 2) | (w & 3), g = (w >> 2) & 1;
+  out[(((size_t)r * 4 + T) * 2 + g) * 16 + v] = acc;
+}
+
 typedef void (*RouteKernel)(RouteArgs);
 
 template <int H, int NL>
@@ -922,7 +1181,45 @@ RouteKernel pick_lds(int dtype, int hidden, int n_layers, int out_tiles, int k1,
   return nullptr;
 }
 
+// Dual-pathway kernels: kDualWaves waves per block, kDualRows row tiles per wave.
+constexpr int kDualWaves = 16;
+constexpr int kDualRows = 1;
+
+RouteKernel pick_dual(int ed, bool rl) {
+  switch (ed) {
+    case 64: return rl ? route_dual_bf16<64, kDualWaves, kDualRows, 1> : route_dual_bf16<64, kDualWaves, kDualRows, 0>;
+    case 128: return rl ? route_dual_bf16<128, kDualWaves, kDualRows, 1> : route_dual_bf16<128, kDualWaves, kDualRows, 0>;
+    case 256: return rl ? route_dual_bf16<256, kDualWaves, kDualRows, 1> : route_dual_bf16<256, kDualWaves, kDualRows, 0>;
+    case 384: return rl ? route_dual_bf16<384, kDualWaves, kDualRows, 1> : route_dual_bf16<384, kDualWaves, kDualRows, 0>;
+  }
+  return nullptr;
+}
+
+hipError_t launch_dual(const RouteArgs& a, hipStream_t s) {
+  RouteKernel k = pick_dual(a.embed_dim, a.rl != 0);
+  if (!k) return hipErrorInvalidValue;
+  const int rows = kDualWaves * 32 * kDualRows;
+  const int n_tiles = (a.n_total + rows - 1) / rows;
+  const unsigned blocks =
+      (unsigned)(a.persistent_blocks > 0 && n_tiles > a.persistent_blocks ? a.persistent_blocks : n_tiles);
+  hipLaunchKernelGGL(k, dim3(blocks), dim3(kDualWaves * 64), 0, s, a);
+  return hipGetLastError();
+}
+
 }  // namespace
+
+bool dual_supported(int embed_dim, int out_rows) {
+  return out_rows >= 1 && out_rows <= 32 && pick_dual(embed_dim, false) != nullptr;
+}
+
+hipError_t launch_role_projection(const uint16_t* w_role, const uint16_t* roles, const float* b_sem,
+                                  int n_roles, int embed_dim, float* out, hipStream_t s) {
+  const int n = n_roles * kDualSem;
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(role_projection_kernel, dim3((n + 255) / 256), dim3(256), 0, s, w_role, roles, b_sem,
+                     n_roles, embed_dim, out);
+  return hipGetLastError();
+}
 
 bool route_supported(int dtype, int hidden, int n_layers, int out_tiles) {
   if (out_tiles < 1 || out_tiles > 3) return false;
@@ -934,6 +1231,7 @@ bool route_supported(int dtype, int hidden, int n_layers, int out_tiles) {
 hipError_t launch_route(const RouteArgs& a, int dtype, int hidden, int n_layers, int out_tiles,
                         hipStream_t s) {
   if (a.n_total <= 0) return hipSuccess;
+  if (a.net == IM_NET_DUAL) return launch_dual(a, s);
   if (a.persistent_blocks > 0) {
     RouteKernel kl = pick_lds(dtype, hidden, n_layers, out_tiles, a.k1, a.embed_dim, a.rl != 0);
     if (kl) {

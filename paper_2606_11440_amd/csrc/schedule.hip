@@ -334,6 +334,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     const int32_t sv = a.base_svc[i];
     ac = a.actions[i];
     if (qi < 0 || (int64_t)qi >= a.Q) berr |= IM_ERR_QIDX;
+    if (a.role) {
+      const int32_t ro = a.role[i];
+      if (ro < 0 || ro >= a.n_roles) berr |= IM_ERR_ROLE;
+    }
     if (bu < 1) berr |= IM_ERR_BUDGET;
     if (sv < 1 || sv > IM_SVC_MAX) berr |= IM_ERR_SVC;
     if (ac < -1 || ac >= a.A) berr |= IM_ERR_ACTION;
@@ -357,6 +361,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     if (ballot(berr & IM_ERR_BUDGET)) bad |= IM_ERR_BUDGET;
     if (ballot(berr & IM_ERR_SVC)) bad |= IM_ERR_SVC;
     if (ballot(berr & IM_ERR_ACTION)) bad |= IM_ERR_ACTION;
+    if (a.role && ballot(berr & IM_ERR_ROLE)) bad |= IM_ERR_ROLE;
   }
 
   LaneState L;

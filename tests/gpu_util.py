@@ -37,7 +37,10 @@ class Pair:
         self.cfg, self.seed = cfg, seed
         self.Q = workload.gen.table_rows(cfg) if Q is None else Q
         self.e0, self.e1 = e0, (cfg["E"] if e1 is None else e1)
-        W, b = workload.gen.weights(cfg, seed, bias_scale)
+        if cfg.get("net") == "dual":
+            W, b = workload.gen.dual_weights(cfg, seed, bias_scale), workload.gen.roles(cfg, seed)
+        else:
+            W, b = workload.gen.weights(cfg, seed, bias_scale)
         table, emb_vals = workload.gen.embedding(cfg, seed, rows=self.Q)
         cap = workload.gen.capacities(cfg, seed)
         lb = workload.gen.logit_bias(cfg)
@@ -47,7 +50,8 @@ class Pair:
             emb_dev = torch.from_numpy(table).cuda()
         self.gpu = P.Pool(cfg, W, b, emb_dev, cap, lb)
         self.orc = oracle.Oracle(cfg, W, b, emb_vals, cap[self.e0:self.e1], lb,
-                                 E=self.e1 - self.e0, threads=threads)
+                                 E=self.e1 - self.e0, threads=threads,
+                                 roles=b if cfg.get("net") == "dual" else None)
         self.counts = workload.gen.counts(cfg, seed)
         self.flips = 0
         self.rows_checked = 0

@@ -1,0 +1,164 @@
+"""GPU parity of the dual-pathway executor (Sec. 4.2, im_pool_create_dual)
+against the oracle.
+
+Lockstep per tick: logits within the bf16 tolerance (2e-2 of the row's
+largest logit), actions equal except at near-ties (then the oracle follows the
+GPU), the integer state after im_schedule bit-exact; the RL-rollout outputs
+(log-prob, entropy, value) within the tolerances they inherit; every
+supported embedding width, several tiles with a ragged tail, the full-size
+pool of the benchmark on sampled envs, and the edge cases (bad roles,
+rejected descriptions, empty ticks)."""
+import ctypes
+
+import numpy as np
+import pytest
+
+import oracle
+import workload
+from gpu_util import Pair, need_gpu, note
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("Ed,E,T", [(64, 24, 30), (128, 8, 20), (256, 8, 15), (384, 40, 25)])
+def test_executor_lockstep(Ed, E, T):
+    cfg = workload.configs.get("c2d", E=E, T=T, embed_dim=Ed)
+    note(f"[executor_lockstep] E_d={Ed} E={E} T={T}")
+    p = Pair(cfg, seed=31, Q=512)
+    for t in range(T):
+        p.step(p.arrivals(t))
+        if t % 5 == 4 or t == T - 1:
+            p.compare_state(ctx=f"E_d={Ed} t={t}")
+    note(f"  rows={p.rows_checked} near-tie flips={p.flips}")
+    assert p.gpu.error() == 0
+    p.close()
+
+
+def test_executor_tick_entry_and_heavy_load():
+    """im_tick on the executor pool, lambda = 64 per env: several 512-row tiles
+    per launch with a ragged tail, queues building up."""
+    cfg = workload.configs.get("c2d", E=48, T=20)
+    note("[executor_tick] c2d E=48 lam=64")
+    p = Pair(cfg, seed=32, Q=1024)
+    for t in range(cfg["T"]):
+        p.step(p.arrivals(t), mode="tick" if t % 2 else "route+schedule")
+    p.compare_state(ctx="end")
+    assert p.gpu.error() == 0
+    p.close()
+
+
+def test_executor_rl_lockstep():
+    cfg = workload.configs.get("c2d", E=16, T=20)
+    note("[executor_rl] c2d E=16")
+    p = Pair(cfg, seed=33, Q=512)
+    for t in range(cfg["T"]):
+        p.step_rl(p.arrivals(t), seed=0xD0A1 + t)
+        if t % 5 == 4:
+            p.compare_state(ctx=f"rl t={t}")
+    note(f"  rows={p.rows_checked} flips={p.flips}")
+    p.close()
+
+
+def test_executor_full_size_sampled():
+    """The benchmark's pool (4096 envs, lambda 64, 384-d embeddings, 2^20
+    table rows) in its launch configuration; envs [3000, 3004) checked."""
+    cfg = workload.configs.get("c2d", T=12)
+    note(f"[executor_full_size] c2d E={cfg['E']} T={cfg['T']} envs [3000,3004)")
+    p = Pair(cfg, seed=0, e0=3000, e1=3004)
+    for t in range(cfg["T"]):
+        p.step(p.arrivals(t), check_logits=(t % 3 == 0))
+    p.compare_state(ctx="full size")
+    note(f"  rows={p.rows_checked} flips={p.flips}")
+    assert p.gpu.error() == 0
+    p.close()
+
+
+def test_executor_bad_role_env_untouched():
+    torch = need_gpu()
+    cfg = workload.configs.get("c2d", E=6, T=6, embed_dim=64)
+    note("[executor_bad_role] c2d E=6")
+    p = Pair(cfg, seed=34, Q=256)
+    for t in range(4):
+        p.step(p.arrivals(t))
+    arr = workload.gen.tick(cfg, 34, 4, np.array([3, 4, 0, 5, 2, 1], np.int32), p.Q)
+    arr["role"] = arr["role"].copy()
+    arr["role"][4] = cfg["n_roles"]      # env 1
+    arr["role"][9] = -3                  # env 3
+    before = p.gpu.state()
+    dev = p.P.device_arrivals(arr)
+    n = int(arr["q_idx"].size)
+    act = torch.full((n,), -7, dtype=torch.int32, device="cuda")
+    lg = torch.full((n, cfg["A"]), float("nan"), dtype=torch.float32, device="cuda")
+    p.gpu.route(dev, act, lg)
+    p.gpu.schedule(dev, act)
+    torch.cuda.synchronize()
+    g_act = act.cpu().numpy()
+    assert g_act[4] == -1 and g_act[9] == -1
+    assert np.all(lg[4].cpu().numpy() == 0) and np.all(lg[9].cpu().numpy() == 0)
+    o_act, _ = p.orc.route(arr)
+    p.orc.schedule(arr, g_act)
+    np.testing.assert_array_equal(g_act[o_act >= 0], o_act[o_act >= 0])
+    assert p.gpu.error() & oracle.ERR_ROLE and p.orc.error & oracle.ERR_ROLE
+    after = p.gpu.state()
+    for e in (1, 3):
+        for k in ("qlen", "enqueued", "started", "completed"):
+            np.testing.assert_array_equal(after[k][e], before[k][e], err_msg=f"{k} env {e}")
+        assert after["next_id"][e] == before["next_id"][e]
+    assert after["next_id"][0] == before["next_id"][0] + 3
+    p.compare_state(ctx="bad role")
+    p.close()
+
+
+def test_executor_create_rejections():
+    need_gpu()
+    import paper_2606_11440_amd as P
+    cfg = workload.configs.get("c2d", E=2, T=2, embed_dim=64)
+    prm = workload.gen.dual_weights(cfg, 0)
+    roles = workload.gen.roles(cfg, 0)
+    cap = workload.gen.capacities(cfg, 0)
+    import torch
+    emb = torch.zeros((16, 64), dtype=torch.int16, device="cuda")
+    for change, status in (({"embed_dim": 96}, P._lib.IM_EUNSUPPORTED),
+                           ({"dtype": "f32"}, P._lib.IM_EUNSUPPORTED),
+                           ({"n_roles": 0}, P._lib.IM_EINVAL),
+                           ({"K": 7}, P._lib.IM_EUNSUPPORTED)):
+        c = dict(cfg, **change)
+        c["A"] = c["M"] * c["K"]
+        d = P.make_desc(c)
+        p2 = dict(prm)
+        if "K" in change:
+            p2["W_act"] = np.zeros((c["A"] + 1, 128), np.float32)
+            p2["b_act"] = np.zeros(c["A"] + 1, np.float32)
+        r2 = roles if "embed_dim" not in change else np.zeros((c["n_roles"], 96), np.float32)
+        if "embed_dim" in change:
+            p2["W_sem"] = np.zeros((128, 192), np.float32)
+        with pytest.raises(P.IMError) as ei:
+            P.im_pool_create_dual(d, p2, r2, emb, 16, cap)
+        assert ei.value.status == status, (change, ei.value)
+    # an MLP description through the dual constructor, and the reverse
+    d = P.make_desc(cfg)
+    d.net = P._lib.IM_NET_MLP
+    with pytest.raises(P.IMError):
+        P.im_pool_create_dual(d, prm, roles, emb, 16, cap)
+    # arrivals without roles are refused by a dual pool
+    pool = P.Pool(cfg, prm, roles, emb, cap)
+    arr = workload.gen.tick(cfg, 0, 0, np.array([2, 1], np.int32), 16)
+    del arr["role"]
+    dev = P.device_arrivals(arr)
+    act = torch.zeros(3, dtype=torch.int32, device="cuda")
+    with pytest.raises(P.IMError) as ei:
+        pool.route(dev, act)
+    assert ei.value.status == P._lib.IM_EINVAL
+    pool.close()
+
+
+def test_executor_empty_ticks():
+    cfg = workload.configs.get("c2d", E=5, T=10, embed_dim=64)
+    note("[executor_empty] c2d E=5")
+    p = Pair(cfg, seed=35, Q=128)
+    zeros = np.zeros(cfg["E"], np.int32)
+    for t in range(cfg["T"]):
+        arr = p.arrivals(t) if t % 3 else workload.gen.tick(cfg, 35, t, zeros, p.Q)
+        p.step(arr)
+    p.compare_state(ctx="empty ticks")
+    p.close()
