@@ -52,6 +52,7 @@ enum { C_REJ_OVERFLOW = 0, C_ENQUEUED, C_STARTED, C_COMPLETED, C_SLO_MET, C_LAT_
 
 // Dual-pathway executor (Sec. 4.2): fixed widths of the paper.
 constexpr int kDualSem = 128, kDualBud = 16, kDualSys = 16, kDualRes = 64, kDualMerge = 128;
+constexpr int kDualMaxModels = 16;   // the system head's weights are staged in LDS
 // Its fp32 parameter block (offsets in floats). Vectors in accumulator-register
 // order [tile][g][16] (feature 32 tile + 8 (v / 4) + 4 g + v % 4 at index
 // (2 tile + g) 16 + v). The first DP_LDS floats are staged in LDS.
@@ -63,15 +64,15 @@ enum {
   DP_LN_RES_B = 384,    // [64] resource LayerNorm bias
   DP_B_MERGE = 448,     // [128] merge bias
   DP_B_ACT = 576,       // [32] action/value bias (+ per-model logit bias on action rows)
-  DP_LDS = 608,
   DP_W_BUD = 608,       // [16] budget head (natural order)
   DP_B_BUD = 624,       // [16]
   DP_B_SYS = 640,       // [16] system head bias (natural order)
-  DP_W_SYS = 656        // [3M][16]: W_sys column of snapshot feature k (k < 3M), rows 0..15
+  DP_W_SYS = 656,       // [3 kDualMaxModels][16]: W_sys column of snapshot feature k (zero
+                        // for k >= 3M), rows 0..15
+  DP_LDS = DP_W_SYS + 3 * kDualMaxModels * 16,
+  DP_ROLE = DP_LDS      // [n_roles][4][2][16]: b_sem + W_sem[:, E_d:] e_r per role, in
+                        // accumulator order
 };
-// Role projections: [n_roles][4][2][16] = b_sem + W_sem[:, E_d:] e_r per role,
-// in accumulator order, after the system head weights (64-byte aligned).
-__host__ __device__ inline int dual_role_offset(int M) { return (DP_W_SYS + 3 * M * 16 + 15) & ~15; }
 
 struct RouteArgs {
   const int32_t* offsets;

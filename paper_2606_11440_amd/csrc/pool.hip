@@ -340,8 +340,9 @@ im_status im_pool_create_dual(const im_pool_desc* desc, const im_dual_net* net, 
   if (d.dtype != IM_BF16) return fail(nullptr, IM_EUNSUPPORTED, "the dual-pathway executor runs in bf16 only");
   const int A = d.n_models * d.n_depths;
   const int Ao = A + d.value_head;
-  if (!im::dual_supported(d.embed_dim, Ao))
-    return fail(nullptr, IM_EUNSUPPORTED, "dual-pathway executor: embed_dim must be 64, 128, 256 or 384 and M*K + value_head <= 32");
+  if (!im::dual_supported(d.embed_dim, Ao) || d.n_models > im::kDualMaxModels)
+    return fail(nullptr, IM_EUNSUPPORTED,
+                "dual-pathway executor: embed_dim must be 64, 128, 256 or 384, M <= 16 and M*K + value_head <= 32");
 
   im_pool* p = new_pool(d, n_queries, emb);
   p->d.feat_dim = d.embed_dim + 4 * d.n_models + 1;
@@ -385,7 +386,7 @@ im_status im_pool_create_dual(const im_pool_desc* desc, const im_dual_net* net, 
   if (st == IM_OK) st = pack(net->W_act, Ao, kDualMerge, 1, 1, &p->W[2]);
   if (st == IM_OK) st = pack(net->W_res, kDualRes, 32, 0, 2, &p->W_res);
   // fp32 parameter block
-  const int roff = im::dual_role_offset(M);
+  const int roff = im::DP_ROLE;
   std::vector<float> dp((size_t)roff + (size_t)d.n_roles * kDualSem, 0.f);
   auto acc_order = [&](int off, const float* v, int width, int tiles, bool logit) {
     for (int T = 0; T < tiles; ++T)

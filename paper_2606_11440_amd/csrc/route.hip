@@ -937,6 +937,9 @@ __device__ __forceinline__ void load_group(const RouteArgs& a, const RowCtx& c, 
   for (int i = 0; i < 4; ++i) x[i] = src[i];
 }
 
+// 64-element embedding groups in flight ahead of the MFMAs
+constexpr int kDualPrefetch = 1;
+
 template <int ED, int NW, int NR, int RL>
 __global__ __launch_bounds__(NW * 64, 1) void route_dual_bf16(RouteArgs a) {
   static_assert(ED % 64 == 0, "embedding width must be a multiple of 64");
@@ -958,8 +961,7 @@ __global__ __launch_bounds__(NW * 64, 1) void route_dual_bf16(RouteArgs a) {
   const u32x4* wmrg = lds + N_SEM;
   const u32x4* wact = wmrg + N_MRG;
   const u32x4* wres = (const u32x4*)a.W_res;
-  const float* gp = a.dual_p;
-  const float* proj = gp + dual_role_offset(a.M);
+  const float* proj = a.dual_p + DP_ROLE;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n = lane & 31, g = lane >> 5;
   const int n_tiles = (a.n_total + ROWS - 1) / ROWS;
@@ -989,67 +991,41 @@ __global__ __launch_bounds__(NW * 64, 1) void route_dual_bf16(RouteArgs a) {
     }
 
     // ---- semantic pathway: role projection + W_sem (query half) e_q ----
-    u32x4 xa[NR][4], xb[NR][4];
+    // ring of PF + 1 groups: group G + PF is loaded while group G is multiplied
+    constexpr int PF = kDualPrefetch < NG ? kDualPrefetch : NG - 1;
+    u32x4 x[PF + 1][NR][4];
 #pragma unroll
-    for (int j = 0; j < NR; ++j) load_group<ED>(a, c[j], 0, gg, xa[j]);
-    f32x16 s[NR][4];
+    for (int G = 0; G < PF; ++G) {
 #pragma unroll
-    for (int j = 0; j < NR; ++j) {
-#pragma unroll
-      for (int T = 0; T < 4; ++T) s[j][T] = *(const f32x16*)(proj + ((role[j] * 4 + T) * 2 + gg) * 16);
+      for (int j = 0; j < NR; ++j) load_group<ED>(a, c[j], G, gg, x[G][j]);
     }
-#pragma unroll
-    for (int G = 0; G < NG; ++G) {
-      if (G + 1 < NG) {
-#pragma unroll
-        for (int j = 0; j < NR; ++j) load_group<ED>(a, c[j], G + 1, gg, xb[j]);
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int kb = 4 * G + i;
-#pragma unroll
-        for (int T = 0; T < 4; ++T) {
-          const u32x4 w = wsem[(T * KBQ + kb) * 64 + ln];
-#pragma unroll
-          for (int j = 0; j < NR; ++j) s[j][T] = mfma_bf16(w, xa[j][i], s[j][T]);
-        }
-      }
-#pragma unroll
-      for (int j = 0; j < NR; ++j) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) xa[j][i] = xb[j][i];
-      }
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    u32x4 hs[NR][8];
-#pragma unroll
-    for (int j = 0; j < NR; ++j) relu_ln_frags<4>(s[j], lp + DP_LN_SEM_G, lp + DP_LN_SEM_B, gg, hs[j]);
-    __builtin_amdgcn_sched_barrier(0);
-
-    // ---- resource pathway ----
+    // ---- resource pathway, computed while the first embedding groups load ----
     u32x4 hr[NR][4];
 #pragma unroll
     for (int j = 0; j < NR; ++j) {
-      asm volatile("" ::: "memory");
       // budget head: features 8 gg .. 8 gg + 7 of h_bud (K step 0 of W_res)
       const float bfe = bf16_round((float)c[j].budget * a.inv_bud);
       float hb[8], hy[8];
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
-        hb[k] = relu(fmaf(gp[DP_W_BUD + 8 * gg + k], bfe, gp[DP_B_BUD + 8 * gg + k]));
-        hy[k] = gp[DP_B_SYS + 8 * gg + k];
+        hb[k] = relu(fmaf(lp[DP_W_BUD + 8 * gg + k], bfe, lp[DP_B_BUD + 8 * gg + k]));
+        hy[k] = lp[DP_B_SYS + 8 * gg + k];
       }
       // system head: features 8 gg .. 8 gg + 7 of h_sys (K step 1) over the
-      // env's queue-depth, KV-proxy and latency features
+      // env's queue-depth, KV-proxy and latency features, read 8 at a time
+      // (weights of the features past 3M are zero)
       const float* srow = a.snap + (size_t)c[j].e * sstride;
-      for (int k = 0; k < n3; ++k) {
-        const float d = bf16_round(srow[k]);
-        const float4 w0 = *(const float4*)(gp + DP_W_SYS + k * 16 + 8 * gg);
-        const float4 w1 = *(const float4*)(gp + DP_W_SYS + k * 16 + 8 * gg + 4);
-        hy[0] = fmaf(w0.x, d, hy[0]); hy[1] = fmaf(w0.y, d, hy[1]);
-        hy[2] = fmaf(w0.z, d, hy[2]); hy[3] = fmaf(w0.w, d, hy[3]);
-        hy[4] = fmaf(w1.x, d, hy[4]); hy[5] = fmaf(w1.y, d, hy[5]);
-        hy[6] = fmaf(w1.z, d, hy[6]); hy[7] = fmaf(w1.w, d, hy[7]);
+      for (int k0 = 0; k0 < n3; k0 += 8) {
+        const float4 d0 = *(const float4*)(srow + k0);
+        const float4 d1 = *(const float4*)(srow + k0 + 4);
+        const float dv[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
+#pragma unroll
+        for (int kk = 0; kk < 8; ++kk) {
+          const float d = bf16_round(dv[kk]);
+          const float* w = lp + DP_W_SYS + (k0 + kk) * 16 + 8 * gg;
+#pragma unroll
+          for (int q = 0; q < 8; ++q) hy[q] = fmaf(w[q], d, hy[q]);
+        }
       }
       u32x4 f0, f1;
       f0.x = relu_pack2(hb[0], hb[1]); f0.y = relu_pack2(hb[2], hb[3]);
@@ -1065,6 +1041,35 @@ __global__ __launch_bounds__(NW * 64, 1) void route_dual_bf16(RouteArgs a) {
       }
       relu_ln_frags<2>(rr, lp + DP_LN_RES_G, lp + DP_LN_RES_B, gg, hr[j]);
     }
+    __builtin_amdgcn_sched_barrier(0);
+
+    f32x16 s[NR][4];
+#pragma unroll
+    for (int j = 0; j < NR; ++j) {
+#pragma unroll
+      for (int T = 0; T < 4; ++T) s[j][T] = *(const f32x16*)(proj + ((role[j] * 4 + T) * 2 + gg) * 16);
+    }
+#pragma unroll
+    for (int G = 0; G < NG; ++G) {
+      if (G + PF < NG) {
+#pragma unroll
+        for (int j = 0; j < NR; ++j) load_group<ED>(a, c[j], G + PF, gg, x[(G + PF) % (PF + 1)][j]);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int kb = 4 * G + i;
+#pragma unroll
+        for (int T = 0; T < 4; ++T) {
+          const u32x4 w = wsem[(T * KBQ + kb) * 64 + ln];
+#pragma unroll
+          for (int j = 0; j < NR; ++j) s[j][T] = mfma_bf16(w, x[G % (PF + 1)][j][i], s[j][T]);
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    u32x4 hs[NR][8];
+#pragma unroll
+    for (int j = 0; j < NR; ++j) relu_ln_frags<4>(s[j], lp + DP_LN_SEM_G, lp + DP_LN_SEM_B, gg, hs[j]);
     __builtin_amdgcn_sched_barrier(0);
 
     // ---- decision: merge layer, then the action/value rows ----
