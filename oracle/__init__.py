@@ -18,7 +18,7 @@ _SRC = os.path.join(_HERE, "oracle.cpp")
 _LIB = os.path.join(_HERE, "liboracle.so")
 
 KEY_MODES = {"slack": 0, "deadline": 1, "fcfs": 2}
-ERR_QIDX, ERR_COUNT, ERR_BUDGET, ERR_SVC, ERR_ACTION, ERR_ROLE = 1, 2, 4, 8, 16, 32
+ERR_QIDX, ERR_COUNT, ERR_BUDGET, ERR_SVC, ERR_ACTION, ERR_ROLE, ERR_STEPS = 1, 2, 4, 8, 16, 32, 64
 
 # Parameters of the dual-pathway executor, in the order orc_create_dual takes them.
 DUAL_PARAMS = ("W_sem", "b_sem", "g_sem", "be_sem", "W_bud", "b_bud", "W_sys", "b_sys",
@@ -43,7 +43,7 @@ class _Desc(ctypes.Structure):
                 ("dtype", ctypes.c_int32), ("key_mode", ctypes.c_int32),
                 ("max_arrivals", ctypes.c_int32), ("budget_max", ctypes.c_int32),
                 ("value_head", ctypes.c_int32), ("net", ctypes.c_int32),
-                ("n_roles", ctypes.c_int32), ("Q", ctypes.c_int64)]
+                ("n_roles", ctypes.c_int32), ("max_steps", ctypes.c_int32), ("Q", ctypes.c_int64)]
 
 
 _lib = None
@@ -67,8 +67,11 @@ def _load():
         L.orc_create_dual.restype = P
         L.orc_create_dual.argtypes = [ctypes.POINTER(_Desc), P, P, P, P, P]
         L.orc_dual_trace.argtypes = [P, ctypes.c_int, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, P]
-        L.orc_route.argtypes = [P, P, P, P, P, P, P, ctypes.c_int]
-        L.orc_schedule.argtypes = [P, ctypes.c_int32, P, P, P, P, P, P, ctypes.c_int]
+        I32 = ctypes.c_int32
+        L.orc_route.argtypes = [P, I32, P, P, P, P, P, P, P, ctypes.c_int]
+        L.orc_schedule.argtypes = [P, I32, P, P, P, P, P, P, P, ctypes.c_int]
+        L.orc_row_offsets.argtypes = [P, I32, P, P]
+        L.orc_read_chain.argtypes = [P, P, P, P, P, P]
         L.orc_features.argtypes = [P, ctypes.c_int, ctypes.c_int32, ctypes.c_int32, P]
         L.orc_round_bf16.argtypes = [ctypes.c_double]
         L.orc_round_bf16.restype = ctypes.c_double
@@ -77,8 +80,8 @@ def _load():
         L.orc_set_capacity.argtypes = [P, ctypes.c_int, ctypes.c_int, ctypes.c_int]
         L.orc_read_state.argtypes = [P] * 7
         U32 = ctypes.c_uint32
-        L.orc_route_rl.argtypes = [P, ctypes.c_int, P, P, P, P, U32, U32, ctypes.c_int, P, P, P, P,
-                                   P, ctypes.c_int]
+        L.orc_route_rl.argtypes = [P, ctypes.c_int, I32, P, P, P, P, P, U32, U32, ctypes.c_int, P,
+                                   P, P, P, P, ctypes.c_int]
         L.orc_philox4x32_10.argtypes = [P, P, P]
         L.orc_gumbel.argtypes = [U32, U32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int]
         L.orc_gumbel.restype = ctypes.c_double
@@ -148,6 +151,8 @@ class Oracle:
                 d.widths[i] = w
             d.widths[len(cfg["widths"]) - 1] = cfg["widths"][-1] + vh
         d.dtype = 1 if cfg["dtype"] == "bf16" else 0
+        d.max_steps = int(cfg.get("max_steps", 1))
+        self.chains = d.max_steps > 1
         d.key_mode = KEY_MODES[cfg["key_mode"]]
         d.max_arrivals = cfg["max_arrivals"]
         d.budget_max = cfg["budget_max"]
@@ -206,16 +211,32 @@ class Oracle:
         r = arr.get("role")
         return None if r is None else np.ascontiguousarray(r, np.int16)
 
+    @staticmethod
+    def _opt16(arr, key):
+        r = arr.get(key)
+        return None if r is None else _ptr(np.ascontiguousarray(r, np.int16))
+
+    def row_offsets(self, arr) -> np.ndarray:
+        """Start of each env's rows in the per-row outputs of the next route /
+        schedule call: the arrival offsets for single-step pools; for chain
+        pools each env's pending calls, then its arrivals (int32 [E + 1])."""
+        off = np.ascontiguousarray(arr["offsets"], np.int32)
+        out = np.empty(self.E + 1, np.int32)
+        self._lib.orc_row_offsets(self.p, int(np.asarray(arr["q_idx"]).size), _ptr(off), _ptr(out))
+        return out
+
     def route(self, arr, want_logits=True):
-        """Returns (actions int32 [n], logits float64 [n, A] or None)."""
+        """Returns (actions int32 [rows], logits float64 [rows, A] or None);
+        rows as in row_offsets (the arrivals for single-step pools)."""
         off, q, bud, _ = self._arr(arr)
         assert off.size == self.E + 1
-        n = int(q.size)
-        act = np.empty(n, np.int32)
-        lg = np.empty((n, self.A), np.float64) if want_logits else None
+        n = max(int(self.row_offsets(arr)[-1]), int(q.size)) if self.chains else int(q.size)
+        act = np.full(n, -1, np.int32)
+        lg = np.zeros((n, self.A), np.float64) if want_logits else None
         ro = self._role(arr)
-        self._lib.orc_route(self.p, _ptr(off), _ptr(q), None if ro is None else _ptr(ro), _ptr(bud),
-                            None if lg is None else _ptr(lg), _ptr(act), self.threads)
+        self._lib.orc_route(self.p, int(q.size), _ptr(off), _ptr(q), None if ro is None else _ptr(ro),
+                            _ptr(bud), self._opt16(arr, "n_steps"), None if lg is None else _ptr(lg),
+                            _ptr(act), self.threads)
         return act, lg
 
     def route_rl(self, arr, seed: int, greedy: bool = False, env_base: int = 0):
@@ -224,13 +245,13 @@ class Oracle:
         (the Philox counter uses global env indices)."""
         off, q, bud, _ = self._arr(arr)
         assert off.size == self.E + 1
-        n = int(q.size)
-        out = dict(actions=np.empty(n, np.int32), logits=np.empty((n, self.A), np.float64),
-                   logp=np.empty(n, np.float64), entropy=np.empty(n, np.float64),
-                   value=np.empty(n, np.float64))
+        n = max(int(self.row_offsets(arr)[-1]), int(q.size)) if self.chains else int(q.size)
+        out = dict(actions=np.full(n, -1, np.int32), logits=np.zeros((n, self.A), np.float64),
+                   logp=np.zeros(n, np.float64), entropy=np.zeros(n, np.float64),
+                   value=np.zeros(n, np.float64))
         ro = self._role(arr)
-        self._lib.orc_route_rl(self.p, env_base, _ptr(off), _ptr(q),
-                               None if ro is None else _ptr(ro), _ptr(bud),
+        self._lib.orc_route_rl(self.p, env_base, int(q.size), _ptr(off), _ptr(q),
+                               None if ro is None else _ptr(ro), _ptr(bud), self._opt16(arr, "n_steps"),
                                seed & 0xffffffff, (seed >> 32) & 0xffffffff, int(bool(greedy)),
                                _ptr(out["logits"]), _ptr(out["actions"]), _ptr(out["logp"]),
                                _ptr(out["entropy"]), _ptr(out["value"]), self.threads)
@@ -248,7 +269,7 @@ class Oracle:
         ro = self._role(arr)
         self._lib.orc_schedule(self.p, int(q.size), _ptr(off), _ptr(q),
                                None if ro is None else _ptr(ro), _ptr(bud), _ptr(svc),
-                               _ptr(act), self.threads)
+                               self._opt16(arr, "n_steps"), _ptr(act), self.threads)
 
     def tick(self, arr):
         act, _ = self.route(arr, want_logits=False)
@@ -274,6 +295,21 @@ class Oracle:
             res[k] = out[o:o + n]
             o += n
         return res
+
+    def chain_state(self) -> dict:
+        """Chain pools: per queued call (queue order, [E, M, qcap, 6]) and per
+        slot ([E, M, S, 6]) the fields (q_idx, k, n_steps, role0, base, beta);
+        the pending calls [E, M*S, 7] (+ deadline) and their count [E]; the
+        completed and on-time queries per env [E, 2]."""
+        E, M, S, Qc = self.E, self.M, self.S, self.qcap
+        qch = np.zeros((E, M, Qc, 6), np.int32)
+        sch = np.zeros((E, M, S, 6), np.int32)
+        pend = np.zeros((E, M * S, 7), np.int32)
+        pc = np.zeros(E, np.int32)
+        qc = np.zeros((E, 2), np.int64)
+        self._lib.orc_read_chain(self.p, _ptr(qch), _ptr(sch), _ptr(pend), _ptr(pc), _ptr(qc))
+        return dict(queue_chain=qch, slot_chain=sch, pending=pend, pending_count=pc,
+                    q_done=qc[:, 0].copy(), q_met=qc[:, 1].copy())
 
     def set_enabled(self, e, m, v):
         self._lib.orc_set_enabled(self.p, e, m, int(bool(v)))

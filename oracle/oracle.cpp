@@ -57,6 +57,7 @@ enum ErrBits {
   ERR_SVC = 8,       // base_svc outside [1, kSvcMax]
   ERR_ACTION = 16,   // action outside [-1, A)
   ERR_ROLE = 32,     // role outside [0, n_roles) (dual-pathway executor only)
+  ERR_STEPS = 64,    // n_steps outside [1, max_steps] (multi-step chains only)
 };
 
 // ----- bf16 round-to-nearest-even of a real value ------------------------
@@ -76,17 +77,34 @@ double round_bf16(double v) {
 }
 
 // ----- data -----------------------------------------------------------------
-struct Entry {            // a queued request
+// The query a call belongs to (multi-step chains; a single-step request is
+// a query of one call): its embedding row, the call's index k among the
+// query's n_steps sequential calls, the role of its first call, the base
+// service time of every call and the query's budget beta.
+struct Chain {
+  int32_t q_idx = 0, k = 0, n_steps = 1, role0 = 0, base = 0, beta = 0;
+};
+
+struct Entry {            // a queued request (one call)
   int32_t key;            // sort key (slack / deadline / arrival tick)
   int32_t id;             // per-env request id, increasing in arrival order
-  int32_t t_arr;          // arrival tick
+  int32_t t_arr;          // tick the call entered the queue
   int32_t svc;            // service time in ticks = base_svc * (depth + 1)
-  int32_t budget;         // time budget in ticks
+  int32_t budget;         // time budget in ticks (a later call: what is left of the query's)
+  Chain ch;
 };
 
 struct Slot {             // a service slot of a model
   bool busy = false;
   int32_t id = -1, t_arr = 0, rem = 0, budget = 0;
+  Chain ch;
+};
+
+// A call spawned by the completion of the previous call of its query, routed
+// at the next tick with the query's deadline.
+struct Pending {
+  Chain ch;
+  int32_t deadline;
 };
 
 struct ModelState {
@@ -119,6 +137,8 @@ struct EnvState {
   int32_t next_id = 0;
   int64_t arrived = 0, rej_nomodel = 0;
   std::vector<int64_t> hist;  // routed requests per joint action
+  std::vector<Pending> pending;      // calls to route at the next tick, in spawn order
+  int64_t q_done = 0, q_met = 0;     // chains: queries whose last call completed / on time
 };
 
 }  // namespace
@@ -136,6 +156,7 @@ struct orc_desc {
   int32_t value_head;     // 1: the last layer has M*K + 1 rows, row M*K is V(s)
   int32_t net;            // 0 plain MLP, 1 dual-pathway executor (Sec. 4.2)
   int32_t n_roles;        // dual-pathway executor: rows of the role-embedding table
+  int32_t max_steps;      // > 1: multi-step agent chains (calls per query up to this)
   int64_t Q;
 };
 
@@ -406,29 +427,107 @@ double gumbel(uint32_t seed_lo, uint32_t seed_hi, int32_t id, int32_t env, int a
   return -std::log(-std::log(u));
 }
 
-// Route the requests of env e: logits (post-bias, pre-mask) and actions.
-void route_env(orc_pool* p, int e, const int32_t* off, const int32_t* q_idx, const int16_t* role,
-               const int16_t* budget, double* logits, int32_t* actions, int32_t* err) {
+// ----- the rows of one env at one tick ---------------------------------------
+// Multi-step chains (Sec. 4.3, Fig. 3): a query of n_steps calls runs them in
+// sequence; the completion of call k spawns call k + 1, routed at the next
+// tick. Every call inherits the query's deadline t_arrive + beta: a call
+// routed at tick t has the remaining budget deadline - t. An env's rows at a
+// tick are its pending calls in spawn order, then its new arrivals in
+// arrival order; request ids follow that order. Single-step pools have no
+// pending calls and their rows are the arrivals.
+struct Row {
+  int32_t out;        // index of the row's outputs (actions, logits, ...)
+  int32_t src;        // arrival row, or -1 for a pending call
+  int32_t q_idx, role, budget, base_svc;   // role of this call; budget: what is left
+  Chain ch;
+};
+
+bool chains(const orc_pool* p) { return p->d.max_steps > 1; }
+
+// Arrival CSR entry of env e usable (chain pools route only such arrivals).
+bool csr_ok(const orc_pool* p, int e, int32_t n_total, const int32_t* off) {
+  const int32_t lo = off[e], hi = off[e + 1];
+  return lo >= 0 && hi >= lo && hi <= n_total && hi - lo <= p->d.max_arrivals;
+}
+
+// Start of env e's rows in the output arrays: the arrival offsets for
+// single-step pools; for chain pools the running sum over the envs before e
+// of their pending calls and usable arrivals.
+std::vector<int32_t> row_offsets(const orc_pool* p, int32_t n_total, const int32_t* off) {
+  std::vector<int32_t> o(p->d.E + 1, 0);
+  if (!chains(p)) {
+    for (int e = 0; e <= p->d.E; ++e) o[e] = off[e];
+    return o;
+  }
+  for (int e = 0; e < p->d.E; ++e)
+    o[e + 1] = o[e] + (int32_t)p->envs[e].pending.size() +
+               (csr_ok(p, e, n_total, off) ? off[e + 1] - off[e] : 0);
+  return o;
+}
+
+int32_t clamp16(int64_t v) { return (int32_t)std::max<int64_t>(-32768, std::min<int64_t>(32767, v)); }
+
+std::vector<Row> env_rows(const orc_pool* p, int e, int32_t n_total, const int32_t* off,
+                          const std::vector<int32_t>& ro, const int32_t* q_idx,
+                          const int16_t* role, const int16_t* budget, const int16_t* base_svc,
+                          const int16_t* n_steps) {
+  std::vector<Row> rows;
+  const EnvState& env = p->envs[e];
+  int32_t out = ro[e];
+  for (const Pending& pd : env.pending) {
+    Row r;
+    r.out = out++;
+    r.src = -1;
+    r.ch = pd.ch;
+    r.q_idx = pd.ch.q_idx;
+    r.role = p->d.net == 1 ? (pd.ch.role0 + pd.ch.k) % p->d.n_roles : 0;
+    r.budget = clamp16((int64_t)pd.deadline - p->t);
+    r.base_svc = pd.ch.base;
+    rows.push_back(r);
+  }
+  if (chains(p) && !csr_ok(p, e, n_total, off)) return rows;
+  for (int32_t i = off[e]; i < off[e + 1]; ++i) {
+    Row r;
+    r.out = chains(p) ? out++ : i;
+    r.src = i;
+    r.q_idx = q_idx[i];
+    r.role = role_of(p, role, i);
+    r.budget = budget[i];
+    r.base_svc = base_svc ? base_svc[i] : 1;
+    r.ch.q_idx = q_idx[i];
+    r.ch.k = 0;
+    r.ch.n_steps = chains(p) ? (n_steps ? n_steps[i] : 1) : 1;
+    r.ch.role0 = r.role < 0 ? 0 : r.role;
+    r.ch.base = r.base_svc;
+    r.ch.beta = budget[i];
+    rows.push_back(r);
+  }
+  return rows;
+}
+
+// Route the rows of env e: logits (post-bias, pre-mask) and actions.
+void route_env(orc_pool* p, int e, const std::vector<Row>& rows, double* logits,
+               int32_t* actions, int32_t* err) {
   const EnvState& env = p->envs[e];
   std::vector<double> z;
-  for (int32_t r = off[e]; r < off[e + 1]; ++r) {
-    const int32_t ro = role_of(p, role, r);
-    if (q_idx[r] < 0 || (int64_t)q_idx[r] >= p->d.Q || ro < 0) {
-      if (q_idx[r] < 0 || (int64_t)q_idx[r] >= p->d.Q) *err |= ERR_QIDX;
-      if (ro < 0) *err |= ERR_ROLE;
-      actions[r] = -1;
-      if (logits) for (int a = 0; a < p->A; ++a) logits[(size_t)r * p->A + a] = 0.0;
+  for (const Row& r : rows) {
+    const bool bad_q = r.q_idx < 0 || (int64_t)r.q_idx >= p->d.Q;
+    if (bad_q || r.role < 0) {
+      if (bad_q) *err |= ERR_QIDX;
+      if (r.role < 0) *err |= ERR_ROLE;
+      actions[r.out] = -1;
+      if (logits) for (int a = 0; a < p->A; ++a) logits[(size_t)r.out * p->A + a] = 0.0;
       continue;
     }
-    policy(p, env, q_idx[r], ro, budget[r], z);
+    policy(p, env, r.q_idx, r.role, r.budget, z);
     int best = -1;
     for (int a = 0; a < p->A; ++a) {
       const ModelState& ms = env.models[a / p->d.K];
       if (!model_valid(p, ms)) continue;
       if (best < 0 || z[a] > z[best]) best = a;   // strict: lowest index wins ties
     }
-    actions[r] = best;
-    if (logits) for (int a = 0; a < p->A; ++a) logits[(size_t)r * p->A + a] = z[a];
+    actions[r.out] = best;
+    if (logits) for (int a = 0; a < p->A; ++a) logits[(size_t)r.out * p->A + a] = z[a];
   }
 }
 
@@ -437,102 +536,104 @@ void route_env(orc_pool* p, int e, const int32_t* off, const int32_t* q_idx, con
 // (Gumbel-max: argmax over valid a of z_a + G_a, lowest index on ties) or, if
 // greedy, the masked argmax; log pi of that action; the entropy of pi; and
 // the value row. No valid action: action -1, log-prob 0, entropy 0.
-void route_env_rl(orc_pool* p, int e, int env_base, const int32_t* off, const int32_t* q_idx,
-                  const int16_t* role, const int16_t* budget, uint32_t seed_lo, uint32_t seed_hi,
-                  int greedy, double* logits, int32_t* actions, double* logp, double* entropy,
-                  double* value, int32_t* err) {
+void route_env_rl(orc_pool* p, int e, int env_base, const std::vector<Row>& rows,
+                  uint32_t seed_lo, uint32_t seed_hi, int greedy, double* logits,
+                  int32_t* actions, double* logp, double* entropy, double* value, int32_t* err) {
   const EnvState& env = p->envs[e];
   const int A = p->A;
   std::vector<double> z;
-  for (int32_t r = off[e]; r < off[e + 1]; ++r) {
-    const int32_t ro = role_of(p, role, r);
-    if (q_idx[r] < 0 || (int64_t)q_idx[r] >= p->d.Q || ro < 0) {
-      if (q_idx[r] < 0 || (int64_t)q_idx[r] >= p->d.Q) *err |= ERR_QIDX;
-      if (ro < 0) *err |= ERR_ROLE;
-      actions[r] = -1;
-      logp[r] = 0.0; entropy[r] = 0.0; value[r] = 0.0;
-      if (logits) for (int a = 0; a < A; ++a) logits[(size_t)r * A + a] = 0.0;
+  for (size_t i = 0; i < rows.size(); ++i) {
+    const Row& r = rows[i];
+    const int32_t o = r.out;
+    const bool bad_q = r.q_idx < 0 || (int64_t)r.q_idx >= p->d.Q;
+    if (bad_q || r.role < 0) {
+      if (bad_q) *err |= ERR_QIDX;
+      if (r.role < 0) *err |= ERR_ROLE;
+      actions[o] = -1;
+      logp[o] = 0.0; entropy[o] = 0.0; value[o] = 0.0;
+      if (logits) for (int a = 0; a < A; ++a) logits[(size_t)o * A + a] = 0.0;
       continue;
     }
-    policy(p, env, q_idx[r], ro, budget[r], z);
-    value[r] = p->d.value_head ? z[A] : 0.0;
-    if (logits) for (int a = 0; a < A; ++a) logits[(size_t)r * A + a] = z[a];
+    policy(p, env, r.q_idx, r.role, r.budget, z);
+    value[o] = p->d.value_head ? z[A] : 0.0;
+    if (logits) for (int a = 0; a < A; ++a) logits[(size_t)o * A + a] = z[a];
     std::vector<int> valid;
     for (int a = 0; a < A; ++a)
       if (model_valid(p, env.models[a / p->d.K])) valid.push_back(a);
     if (valid.empty()) {
-      actions[r] = -1; logp[r] = 0.0; entropy[r] = 0.0;
+      actions[o] = -1; logp[o] = 0.0; entropy[o] = 0.0;
       continue;
     }
     // log-sum-exp over the valid actions, shifted by their largest logit
     double zmax = z[valid[0]];
     for (int a : valid) zmax = std::max(zmax, z[a]);
-    double s = 0.0;
-    for (int a : valid) s += std::exp(z[a] - zmax);
-    const double lse = zmax + std::log(s);
+    double sum = 0.0;
+    for (int a : valid) sum += std::exp(z[a] - zmax);
+    const double lse = zmax + std::log(sum);
     double h = 0.0;                         // -sum pi log pi
     for (int a : valid) {
       const double lp = z[a] - lse;
       h -= std::exp(lp) * lp;
     }
-    const int32_t id = env.next_id + (r - off[e]);
+    const int32_t id = env.next_id + (int32_t)i;
     int best = -1;
     double best_score = 0.0;
     for (int a : valid) {
       const double sc = greedy ? z[a] : z[a] + gumbel(seed_lo, seed_hi, id, env_base + e, a);
       if (best < 0 || sc > best_score) { best = a; best_score = sc; }
     }
-    actions[r] = best;
-    logp[r] = z[best] - lse;
-    entropy[r] = h;
+    actions[o] = best;
+    logp[o] = z[best] - lse;
+    entropy[o] = h;
   }
 }
 
 // Admission, queue insertion, service and accounting for env e at tick t.
 void schedule_env(orc_pool* p, int e, int32_t n_total, const int32_t* off,
-                  const int32_t* q_idx, const int16_t* role, const int16_t* budget,
-                  const int16_t* base_svc, const int32_t* actions, int32_t* err) {
+                  const std::vector<Row>& rows, const int32_t* actions, int32_t* err) {
   const orc_desc& d = p->d;
   EnvState& env = p->envs[e];
-  const int32_t lo = off[e], hi = off[e + 1];
-  // Validate the whole env first; an invalid env is left untouched this tick.
+  // Validate the whole env first; an invalid env is left untouched this tick
+  // (its pending calls stay pending).
   int bad = 0;
+  const int32_t lo = off[e], hi = off[e + 1];
   if (lo < 0 || hi < lo || hi > n_total || hi - lo > d.max_arrivals) bad |= ERR_COUNT;
   if (!bad) {
-    for (int32_t r = lo; r < hi; ++r) {
-      if (q_idx[r] < 0 || (int64_t)q_idx[r] >= d.Q) bad |= ERR_QIDX;
-      if (role_of(p, role, r) < 0) bad |= ERR_ROLE;
-      if (budget[r] < 1) bad |= ERR_BUDGET;
-      if (base_svc[r] < 1 || base_svc[r] > kSvcMax) bad |= ERR_SVC;
-      if (actions[r] < -1 || actions[r] >= p->A) bad |= ERR_ACTION;
+    for (const Row& r : rows) {
+      if (actions[r.out] < -1 || actions[r.out] >= p->A) bad |= ERR_ACTION;
+      if (r.src < 0) continue;    // pending calls are valid by construction
+      if (r.q_idx < 0 || (int64_t)r.q_idx >= d.Q) bad |= ERR_QIDX;
+      if (r.role < 0) bad |= ERR_ROLE;
+      if (r.budget < 1) bad |= ERR_BUDGET;
+      if (r.base_svc < 1 || r.base_svc > kSvcMax) bad |= ERR_SVC;
+      if (chains(p) && (r.ch.n_steps < 1 || r.ch.n_steps > d.max_steps)) bad |= ERR_STEPS;
     }
   }
   if (bad) { *err |= bad; return; }
 
   const int32_t t = p->t;
-  const int32_t n = hi - lo;
+  const int32_t n = (int32_t)rows.size();
   env.arrived += n;
   // S2: admission in id order, tail-drop beyond the queue capacity.
   for (int m = 0; m < d.M; ++m) {
     ModelState& ms = env.models[m];
     const int room = d.qcap - (int)ms.queue.size();
     std::vector<Entry> accepted;
-    int routed = 0;
-    for (int32_t r = lo; r < hi; ++r) {
-      const int32_t a = actions[r];
+    for (int32_t i = 0; i < n; ++i) {
+      const Row& r = rows[i];
+      const int32_t a = actions[r.out];
       if (a < 0 || a / d.K != m) continue;
-      ++routed;
       if ((int)accepted.size() >= room) { ms.rej_overflow += 1; continue; }
       const int32_t depth = a % d.K;
       Entry en;
-      en.id = env.next_id + (r - lo);
+      en.id = env.next_id + i;
       en.t_arr = t;
-      en.svc = (int32_t)base_svc[r] * (depth + 1);
-      en.budget = budget[r];
+      en.svc = r.base_svc * (depth + 1);
+      en.budget = r.budget;
       en.key = sort_key(p, t, en.budget, en.svc);
+      en.ch = r.ch;
       accepted.push_back(en);
     }
-    (void)routed;
     for (const Entry& en : accepted) { ms.backlog += en.svc; ms.enqueued += 1; }
     // Stable sort of (existing queue ++ newcomers in id order) by key alone:
     // equal keys keep their order, i.e. older ids first.
@@ -540,12 +641,13 @@ void schedule_env(orc_pool* p, int e, int32_t n_total, const int32_t* off,
     std::stable_sort(ms.queue.begin(), ms.queue.end(),
                      [](const Entry& a, const Entry& b) { return a.key < b.key; });
   }
-  for (int32_t r = lo; r < hi; ++r) {
-    if (actions[r] < 0) env.rej_nomodel += 1;
-    else env.hist[actions[r]] += 1;
+  for (const Row& r : rows) {
+    if (actions[r.out] < 0) env.rej_nomodel += 1;
+    else env.hist[actions[r.out]] += 1;
   }
   // S3: per model, fill empty slots s < c_m from the queue head, then advance
   // every busy slot by one tick of service.
+  std::vector<Pending> spawned;
   for (int m = 0; m < d.M; ++m) {
     ModelState& ms = env.models[m];
     // forget dispatches that have left every window still to come
@@ -561,6 +663,7 @@ void schedule_env(orc_pool* p, int e, int32_t n_total, const int32_t* off,
       Entry en = ms.queue.front();
       ms.queue.erase(ms.queue.begin());
       sl.busy = true; sl.id = en.id; sl.t_arr = en.t_arr; sl.rem = en.svc; sl.budget = en.budget;
+      sl.ch = en.ch;
       ms.backlog -= en.svc;
       ms.started += 1;
       ms.wait_sum += t - en.t_arr;
@@ -577,12 +680,28 @@ void schedule_env(orc_pool* p, int e, int32_t n_total, const int32_t* off,
       ms.ewma_q8 = (int32_t)(ms.ewma_q8 + step);
       ms.completed += 1;
       ms.lat_sum += lat;
-      ms.slo_met += (lat <= sl.budget) ? 1 : 0;
-      // Sec. 3 cost C_k = latency / budget (Eq. 2), accumulated in Q16 for the dual update
-      ms.cost_q16 += ((int64_t)lat << 16) / sl.budget;
+      // a call is on time when it completes by its (inherited) deadline
+      const bool on_time = lat <= sl.budget;
+      ms.slo_met += on_time ? 1 : 0;
+      // Sec. 3 cost of the call, latency / beta with beta the query's budget
+      // (Eq. 2: the query's cost is the sum over its calls), in Q16
+      ms.cost_q16 += ((int64_t)lat << 16) / sl.ch.beta;
+      if (chains(p)) {
+        if (sl.ch.k + 1 < sl.ch.n_steps) {
+          Pending pd;
+          pd.ch = sl.ch;
+          pd.ch.k += 1;
+          pd.deadline = sl.t_arr + sl.budget;   // inherited: the query's deadline
+          spawned.push_back(pd);
+        } else {
+          env.q_done += 1;
+          env.q_met += on_time ? 1 : 0;
+        }
+      }
       sl = Slot();
     }
   }
+  env.pending.swap(spawned);
   env.next_id += n;
 }
 
@@ -696,46 +815,84 @@ int32_t orc_tick(const orc_pool* p) { return p->t; }
 int32_t orc_error(const orc_pool* p) { return p->err; }
 void orc_clear_error(orc_pool* p) { p->err = 0; }
 
-void orc_route(orc_pool* p, const int32_t* off, const int32_t* q_idx, const int16_t* role,
-               const int16_t* budget, double* logits, int32_t* actions, int threads) {
+// Arrival rows of env e the route step reads: single-step pools route
+// whatever lies inside the arrays (the schedule step rejects a bad CSR);
+// chain pools only a usable CSR entry.
+bool route_rows_ok(const orc_pool* p, int e, int32_t n_total, const int32_t* off) {
+  if (chains(p)) return csr_ok(p, e, n_total, off);
+  return off[e] >= 0 && off[e + 1] <= n_total;
+}
+
+// Arrivals: CSR `off` over n_total rows; `n_steps` (chain pools) calls per
+// query, NULL for one. Outputs are indexed by row_offsets(): the env's pending
+// calls, then its arrivals.
+void orc_route(orc_pool* p, int32_t n_total, const int32_t* off, const int32_t* q_idx,
+               const int16_t* role, const int16_t* budget, const int16_t* n_steps, double* logits,
+               int32_t* actions, int threads) {
   std::vector<int32_t> errs(p->d.E, 0);
+  const std::vector<int32_t> ro = row_offsets(p, n_total, off);
   for_envs(p->d.E, threads, [&](int e) {
-    route_env(p, e, off, q_idx, role, budget, logits, actions, &errs[e]);
+    std::vector<Row> rows;
+    if (route_rows_ok(p, e, n_total, off) || chains(p))
+      rows = env_rows(p, e, n_total, off, ro, q_idx, role, budget, nullptr, n_steps);
+    route_env(p, e, rows, logits, actions, &errs[e]);
   });
   for (int32_t x : errs) p->err |= x;
 }
 
 void orc_schedule(orc_pool* p, int32_t n_total, const int32_t* off, const int32_t* q_idx,
                   const int16_t* role, const int16_t* budget, const int16_t* base_svc,
-                  const int32_t* actions, int threads) {
+                  const int16_t* n_steps, const int32_t* actions, int threads) {
   std::vector<int32_t> errs(p->d.E, 0);
+  const std::vector<int32_t> ro = row_offsets(p, n_total, off);
   for_envs(p->d.E, threads, [&](int e) {
-    schedule_env(p, e, n_total, off, q_idx, role, budget, base_svc, actions, &errs[e]);
+    std::vector<Row> rows;
+    if (csr_ok(p, e, n_total, off) || chains(p))
+      rows = env_rows(p, e, n_total, off, ro, q_idx, role, budget, base_svc, n_steps);
+    schedule_env(p, e, n_total, off, rows, actions, &errs[e]);
   });
   for (int32_t x : errs) p->err |= x;
   p->t += 1;
 }
 
-void orc_route_rl(orc_pool* p, int env_base, const int32_t* off, const int32_t* q_idx,
-                  const int16_t* role, const int16_t* budget, uint32_t seed_lo, uint32_t seed_hi,
-                  int greedy, double* logits, int32_t* actions, double* logp, double* entropy,
-                  double* value, int threads) {
+void orc_route_rl(orc_pool* p, int env_base, int32_t n_total, const int32_t* off,
+                  const int32_t* q_idx, const int16_t* role, const int16_t* budget,
+                  const int16_t* n_steps, uint32_t seed_lo, uint32_t seed_hi, int greedy,
+                  double* logits, int32_t* actions, double* logp, double* entropy, double* value,
+                  int threads) {
   std::vector<int32_t> errs(p->d.E, 0);
+  const std::vector<int32_t> ro = row_offsets(p, n_total, off);
   for_envs(p->d.E, threads, [&](int e) {
-    route_env_rl(p, e, env_base, off, q_idx, role, budget, seed_lo, seed_hi, greedy, logits, actions,
-                 logp, entropy, value, &errs[e]);
+    std::vector<Row> rows;
+    if (route_rows_ok(p, e, n_total, off) || chains(p))
+      rows = env_rows(p, e, n_total, off, ro, q_idx, role, budget, nullptr, n_steps);
+    route_env_rl(p, e, env_base, rows, seed_lo, seed_hi, greedy, logits, actions, logp, entropy,
+                 value, &errs[e]);
   });
   for (int32_t x : errs) p->err |= x;
 }
 
-// Dual update of the Lagrange multiplier (Eq. 7): over the completions since
-// the previous update, C_bar = mean latency / budget (each term floor(2^16
-// l / beta) / 2^16), and lambda <- clip(lambda + eta (C_bar - 1), 0, lambda_max).
-// No completion since the previous update leaves lambda unchanged.
+// Row offsets of the next route/schedule call (E + 1 entries).
+void orc_row_offsets(const orc_pool* p, int32_t n_total, const int32_t* off, int32_t* out) {
+  const std::vector<int32_t> ro = row_offsets(p, n_total, off);
+  std::copy(ro.begin(), ro.end(), out);
+}
+
+// Dual update of the Lagrange multiplier (Eq. 7): over the queries completed
+// since the previous update, C_bar = mean of latency / budget (the summed
+// floor(2^16 l / beta) of their calls, / 2^16), and
+// lambda <- clip(lambda + eta (C_bar - 1), 0, lambda_max). A single-step
+// query is one call; a chain's query completes with its last call. No
+// completion since the previous update leaves lambda unchanged.
 void orc_dual_update(orc_pool* p, double eta, double lambda_max, double* lambda) {
   int64_t n = 0, cost = 0;
-  for (const EnvState& env : p->envs)
-    for (const ModelState& ms : env.models) { n += ms.completed; cost += ms.cost_q16; }
+  for (const EnvState& env : p->envs) {
+    for (const ModelState& ms : env.models) {
+      if (!chains(p)) n += ms.completed;
+      cost += ms.cost_q16;
+    }
+    if (chains(p)) n += env.q_done;
+  }
   const int64_t dn = n - p->dual_completed, dc = cost - p->dual_cost_q16;
   p->dual_completed = n;
   p->dual_cost_q16 = cost;
@@ -829,6 +986,43 @@ void orc_read_state(const orc_pool* p, int32_t* env_i32, int64_t* env_i64, int64
         qo[i * 5 + 3] = en.svc; qo[i * 5 + 4] = en.budget;
       }
     }
+  }
+}
+
+// Chain state (chain pools): per queued call (queue order) and per slot the
+// fields {q_idx, k, n_steps, role0, base, beta}; the pending calls
+// {q_idx, k, n_steps, role0, base, beta, deadline} (up to M * max_slots per
+// env) with their count; per env the completed and on-time queries.
+void orc_read_chain(const orc_pool* p, int32_t* qchain, int32_t* schain, int32_t* pend,
+                    int32_t* pcount, int64_t* qcnt) {
+  const orc_desc& d = p->d;
+  const int PM = d.M * d.max_slots;
+  auto put = [](int32_t* o, const Chain& c) {
+    o[0] = c.q_idx; o[1] = c.k; o[2] = c.n_steps; o[3] = c.role0; o[4] = c.base; o[5] = c.beta;
+  };
+  for (int e = 0; e < d.E; ++e) {
+    const EnvState& env = p->envs[e];
+    for (int m = 0; m < d.M; ++m) {
+      const ModelState& ms = env.models[m];
+      const size_t em = (size_t)e * d.M + m;
+      int32_t* qo = qchain + em * (size_t)d.qcap * 6;
+      std::memset(qo, 0, sizeof(int32_t) * (size_t)d.qcap * 6);
+      for (size_t i = 0; i < ms.queue.size(); ++i) put(qo + i * 6, ms.queue[i].ch);
+      for (int s = 0; s < d.max_slots; ++s) {
+        int32_t* so = schain + (em * d.max_slots + s) * 6;
+        if (ms.slots[s].busy) put(so, ms.slots[s].ch);
+        else std::memset(so, 0, sizeof(int32_t) * 6);
+      }
+    }
+    int32_t* po = pend + (size_t)e * PM * 7;
+    std::memset(po, 0, sizeof(int32_t) * (size_t)PM * 7);
+    for (size_t i = 0; i < env.pending.size() && (int)i < PM; ++i) {
+      put(po + i * 7, env.pending[i].ch);
+      po[i * 7 + 6] = env.pending[i].deadline;
+    }
+    pcount[e] = (int32_t)env.pending.size();
+    qcnt[2 * e] = env.q_done;
+    qcnt[2 * e + 1] = env.q_met;
   }
 }
 

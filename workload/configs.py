@@ -28,6 +28,10 @@ net        "mlp" (default) or "dual": the paper's dual-pathway executor (Sec. 4.
            query embedding, a role embedding (n_roles rows, one role per
            request), the remaining budget and three of the load statistics
 n_roles    rows of the role-embedding table (dual-pathway executor)
+max_steps  > 1: multi-step agent chains (Sec. 4.3): each query is a sequence of
+           n_steps calls, n_steps uniform in [1, max_steps]; the completion of a
+           call spawns the next, routed at the following tick with what is left
+           of the query's budget (the query's deadline is inherited)
 value_head when true, the policy has a value row V(s) besides the A logits
 q_rows_cap upper bound on the embedding-table rows (default 2^22)
 dtype      "f32" or "bf16" (bf16 weights/activations, fp32 accumulate)
@@ -71,6 +75,10 @@ CONFIGS = {
     # c2's pools with the paper's dual-pathway executor (Sec. 4.2): 384-d query
     # and role embeddings (Sentence-BERT width), 8 roles, 5 models x 3
     # strategies, a value head; 2^20 table rows (768 MB in bf16)
+    # c2's pools running multi-step agent chains: 16 queries per env-tick of
+    # 1-4 sequential calls (about 40 calls per env-tick), deadlines inherited
+    "c2c": dict(_BASE, index=6, E=4096, lam=16.0, T=256, qcap=2048, max_steps=4,
+                embed_dim=64, feat_dim=86, widths=[256, 256, 15], dtype="bf16"),
     "c2d": dict(_BASE, index=5, E=4096, lam=64.0, T=256, qcap=2048, net="dual",
                 embed_dim=384, n_roles=8, value_head=True, dtype="bf16",
                 q_rows_cap=1 << 20, lam_sweep=[4.0, 16.0, 64.0]),

@@ -11,7 +11,8 @@ Streams: numpy.random.default_rng(SeedSequence([seed, cfg index, stream]))
   4 request fields, one sub-stream per tick: SeedSequence([seed, idx, 4, t]),
   5 the value-head row (pools with cfg["value_head"]),
   6 the dual-pathway executor's parameters, 7 its role-embedding table,
-  8 per-tick role of each request: SeedSequence([seed, idx, 8, t]).
+  8 per-tick role of each request: SeedSequence([seed, idx, 8, t]),
+  9 per-tick number of calls of each query (chain pools): SeedSequence([seed, idx, 9, t]).
 
 Inputs stand in for the paper's workloads (Sec. 5.1): the paper's LLM-quality
 benchmarks are replaced by N(0,1) query embeddings (Sec. 3 uses Sentence-BERT
@@ -164,6 +165,9 @@ def tick(cfg: dict, seed: int, t: int, counts_row: np.ndarray, Q: int):
     if cfg.get("n_roles"):
         rr = _rng(cfg, seed, 8, t)
         out["role"] = rr.integers(0, cfg["n_roles"], size=n).astype(np.int16)
+    if cfg.get("max_steps", 1) > 1:
+        rs = _rng(cfg, seed, 9, t)
+        out["n_steps"] = rs.integers(1, cfg["max_steps"] + 1, size=n).astype(np.int16)
     return out
 
 
@@ -174,8 +178,9 @@ def subset(arr: dict, e0: int, e1: int) -> dict:
     out = dict(offsets=(off[e0:e1 + 1] - lo).astype(np.int32),
                q_idx=arr["q_idx"][lo:hi], budget=arr["budget"][lo:hi],
                base_svc=arr["base_svc"][lo:hi])
-    if "role" in arr:
-        out["role"] = arr["role"][lo:hi]
+    for k in ("role", "n_steps"):
+        if k in arr:
+            out[k] = arr[k][lo:hi]
     return out
 
 
