@@ -249,9 +249,12 @@ def main():
     emb_dev = torch.from_numpy(table.view(np.int16) if cfg["dtype"] == "bf16" else table).cuda()
     dev = [P.device_arrivals(a) for a in ticks]
     n_req = [int(a["q_idx"].size) for a in ticks]
-    acts = torch.empty(max(max(n_req), 1), dtype=torch.int32, device="cuda")
+    chains = cfg.get("max_steps", 1) > 1
+    # chain pools: a tick's rows are its pending calls and its arrivals
+    extra = cfg["E"] * cfg["M"] * cfg["max_slots"] if chains else 0
+    acts = torch.empty(max(max(n_req), 1) + extra, dtype=torch.int32, device="cuda")
     f32 = dict(dtype=torch.float32, device="cuda")
-    rl_out = [torch.empty(max(max(n_req), 1), **f32) for _ in range(3)] if args.sample else None
+    rl_out = [torch.empty(max(max(n_req), 1) + extra, **f32) for _ in range(3)] if args.sample else None
     pool = P.Pool(cfg, W, b, emb_dev, cap, lb)
 
     def route_step(pl, t, st=None, with_schedule=True):
@@ -319,6 +322,9 @@ def main():
         ev[k][1].record(stream)
         pool2.schedule(dev[t], acts, stream.cuda_stream)
         ev[k][2].record(stream)
+        if chains:
+            # the rows this tick routed: its pending calls and its arrivals
+            n_req[t] = pool2.rows()[1]
     torch.cuda.synchronize()
     route_ms = [ev[k][0].elapsed_time(ev[k][1]) for k in range(K)]
     sched_ms = [ev[k][1].elapsed_time(ev[k][2]) for k in range(K)]
@@ -380,6 +386,9 @@ def main():
                                ("; RL rollout: Gumbel-max sampled actions, log-probs, entropies, "
                                 "value head" if args.sample else ""),
                    "envs": cfg["E"], "requests_per_tick": routed / K, "parallelism": "single GPU",
+                   "chains": (f"queries of 1..{cfg['max_steps']} sequential calls (uniform), "
+                              "deadlines inherited; requests = calls routed (pending + arrivals)")
+                   if chains else None,
                    "launch": "eager" if args.eager else f"one HIP graph of {K} ticks, captured "
                                                         "before the timed region"},
         "routed_req_per_s": routed / (gpu_ms / 1e3),

@@ -66,6 +66,7 @@ typedef enum { IM_KEY_SLACK = 0, IM_KEY_DEADLINE = 1, IM_KEY_FCFS = 2 } im_key_m
 #define IM_ERR_SVC    8   /* base_svc outside [1, IM_SVC_MAX]                      */
 #define IM_ERR_ACTION 16  /* action outside [-1, M*K)                              */
 #define IM_ERR_ROLE   32  /* role outside [0, n_roles) (dual-pathway pools)          */
+#define IM_ERR_STEPS  64  /* n_steps outside [1, max_steps] (chain pools)          */
 
 /* Limits of this build. */
 #define IM_SVC_MAX     4095   /* largest base service time (ticks)              */
@@ -76,6 +77,7 @@ typedef enum { IM_KEY_SLACK = 0, IM_KEY_DEADLINE = 1, IM_KEY_FCFS = 2 } im_key_m
 #define IM_MAX_QCAP    16384
 #define IM_MAX_FEAT    512
 #define IM_MAX_ROLES   4096
+#define IM_MAX_STEPS   15     /* calls per query of a chain pool                */
 
 /* Policy network of a pool (Sec. 4.2). MLP: a plain MLP over the feature
  * vector (widths from the description). DUAL: the paper's dual-pathway
@@ -108,7 +110,18 @@ typedef enum { IM_NET_MLP = 0, IM_NET_DUAL = 1 } im_net;
  *   net           im_net; IM_NET_DUAL pools are created by im_pool_create_dual,
  *                 which ignores feat_dim, n_layers and widths
  *   n_roles       IM_NET_DUAL: rows of the role-embedding table, in
- *                 [1, IM_MAX_ROLES]; ignored for IM_NET_MLP */
+ *                 [1, IM_MAX_ROLES]; ignored for IM_NET_MLP
+ *   max_steps     0 or 1: every request is a single call. 2..IM_MAX_STEPS: a
+ *                 chain pool (multi-step agent chains, Sec. 4.3): an arriving
+ *                 query is a sequence of n_steps <= max_steps calls run one
+ *                 after the other; when call k completes at tick t, call k + 1
+ *                 is routed at tick t + 1 with the query's deadline
+ *                 t_arrive + budget, i.e. with the remaining budget
+ *                 deadline - (t + 1) (which may be <= 0). Every call of a
+ *                 query has the query's embedding row and base service time;
+ *                 in dual-pathway pools call k has role (role + k) mod n_roles.
+ *                 Chain pools need n_queries <= 2^24 and, for IM_NET_DUAL,
+ *                 n_roles <= 32. */
 typedef struct {
   int32_t n_envs, n_models, n_depths, queue_cap, max_slots;
   int32_t embed_dim, feat_dim, n_layers;
@@ -116,6 +129,7 @@ typedef struct {
   int32_t dtype, key_mode, max_arrivals_per_env_tick, budget_max;
   int32_t value_head;
   int32_t net, n_roles;
+  int32_t max_steps;
 } im_pool_desc;
 
 /* The arrivals of ONE tick, in env-major CSR order (all device memory).
@@ -127,14 +141,25 @@ typedef struct {
  *   role     [n]    row of the role-embedding table: the role of the agent
  *                   step that issues the request (Sec. 4.2). Required by
  *                   IM_NET_DUAL pools, ignored (may be NULL) by IM_NET_MLP pools
+ *   n_steps  [n]    chain pools: calls of the arriving query, in [1, max_steps]
+ *                   (required); ignored (may be NULL) by single-call pools
  * Within an env, rows are in arrival order; request ids are assigned in that
- * order, continuing from the env's next_id. */
+ * order, continuing from the env's next_id.
+ *
+ * Rows of a tick. In single-call pools the rows are the arrivals and every
+ * per-row output is indexed like them. In chain pools an env's rows are its
+ * pending calls (in the order they were spawned: by model, then slot), then
+ * its arrivals; per-row outputs are indexed by the row offsets im_get_rows
+ * reports (env e: rows [offsets[e], offsets[e+1])), and caller buffers must
+ * hold n_total + n_envs * n_models * max_slots rows. Request ids follow the
+ * row order. */
 typedef struct {
   const int32_t* offsets;
   const int32_t* q_idx;
   const int16_t* budget;
   const int16_t* base_svc;
   const int16_t* role;
+  const int16_t* n_steps;
   int32_t n_total;
 } im_arrivals;
 
@@ -231,6 +256,24 @@ typedef struct {
 im_status im_route_sample(im_pool* pool, const im_arrivals* arr, uint64_t seed, int32_t greedy,
                           const im_policy_out* out, void* stream);
 
+/* Rows of the current tick of a chain pool (device pointers owned by the
+ * pool). They are rebuilt from the pending calls and the arrivals by every
+ * im_route, im_route_sample, im_schedule and im_tick call (before it routes or
+ * schedules) and stay valid until the next such call.
+ *   offsets  [n_envs + 1] row range of each env (pending calls first)
+ *   n_rows   [1] rows of the tick
+ *   q_idx, budget, role  per row: query-embedding row, budget the call is
+ *            routed with (the remaining budget for a pending call), role
+ * IM_EINVAL for a single-call pool. */
+typedef struct {
+  const int32_t* offsets;
+  const int32_t* n_rows;
+  const int32_t* q_idx;
+  const int16_t* budget;
+  const int16_t* role;
+} im_rows;
+im_status im_get_rows(im_pool* pool, im_rows* out);
+
 /* Schedule one tick with the given actions (any actions in [-1, M*K), e.g.
  * sampled ones): admission in id order with tail-drop beyond queue_cap, keys
  * per key_mode, service of every model, accounting; then the tick advances.
@@ -249,7 +292,8 @@ void im_destroy(im_pool* pool);
 
 typedef struct {            /* a queued request, in service order             */
   int32_t key, id, t_arr;   /* sort key, per-env request id, arrival tick     */
-  uint16_t svc, budget;     /* service time, budget (ticks)                   */
+  uint16_t svc;             /* service time (ticks)                           */
+  int16_t budget;           /* budget (ticks; a chain's later call: what is left, may be <= 0) */
 } im_entry;
 
 typedef struct {            /* a service slot; id = -1 when free              */
@@ -267,8 +311,10 @@ typedef struct {
 } im_model_state;
 
 typedef struct {
-  int64_t arrived, rej_nomodel;
+  int64_t arrived, rej_nomodel;   /* rows (calls) seen; rows routed to no model   */
   int32_t next_id, _pad;
+  int64_t q_done, q_met;          /* chain pools: queries whose last call completed;
+                                     of them, those completed by their deadline */
 } im_env_state;
 
 /* Copy the state of envs [env_begin, env_begin + env_count) to host memory.
@@ -281,10 +327,35 @@ im_status im_read_state(im_pool* pool, int32_t env_begin, int32_t env_count, int
                         im_env_state* envs, im_model_state* models, im_slot* slots,
                         im_entry* queues, int64_t* hist);
 
+/* The chain words of a call (chain pools): its query's embedding row, its
+ * index k among the query's n_steps calls, the role of the query's first
+ * call, the base service time and the query's budget. */
+typedef struct {
+  int32_t q_idx;
+  int16_t k, n_steps, role0, base_svc;
+  int32_t beta;
+} im_chain;
+
+typedef struct {            /* a call waiting for the next tick's route step   */
+  im_chain ch;
+  int32_t deadline;         /* the query's deadline t_arrive + beta           */
+} im_pending;
+
+/* Chain state of envs [env_begin, env_begin + env_count) (chain pools; host
+ * memory; synchronises): the chain words of every queued call, in the order
+ * of im_read_state's queues ([count*M*queue_cap]), and of every busy slot
+ * ([count*M*max_slots], zero for a free slot); the pending calls of each env
+ * ([count*M*max_slots]) and their number ([count]). Any pointer may be NULL.
+ * IM_EINVAL for a single-call pool. */
+im_status im_read_chain_state(im_pool* pool, int32_t env_begin, int32_t env_count, im_chain* queues,
+                              im_chain* slots, im_pending* pending, int32_t* pending_count);
+
 /* Overwrite the state of envs [env_begin, env_begin + env_count) and the tick
  * from host memory (same layout as im_read_state; all pointers required).
  * Returns IM_ESTATE without changing anything if the snapshot is
- * inconsistent (unsorted queue, qlen/busy/backlog not matching, bounds). */
+ * inconsistent (unsorted queue, qlen/busy/backlog not matching, bounds).
+ * IM_EUNSUPPORTED for chain pools (their chain words and pending calls are
+ * not part of this snapshot). */
 im_status im_write_state(im_pool* pool, int32_t env_begin, int32_t env_count, int32_t tick,
                          const im_env_state* envs, const im_model_state* models,
                          const im_slot* slots, const im_entry* queues, const int64_t* hist);

@@ -6,10 +6,13 @@ include/inframind.h); this package only marshals arguments. Importing it does
 not load the library; the first call does, and fails loudly if it is missing."""
 from __future__ import annotations
 
+import numpy as np
+
 from . import _lib
 from ._lib import (EXPORTED, IMError, im_clear_error, im_destroy, im_dual_update,  # noqa: F401
                    im_get_error,
-                   im_last_error, im_pool_create, im_pool_create_dual, im_read_state, im_route,
+                   im_get_rows, im_last_error, im_pool_create, im_pool_create_dual,
+                   im_read_chain_state, im_read_state, im_route,
                    im_route_sample,
                    im_schedule,
                    im_set_capacity, im_set_enabled, im_set_rpm_limit, im_tick, im_write_state,
@@ -23,8 +26,9 @@ def device_arrivals(arr: dict, device="cuda"):
     import torch
     t = lambda x, dt: torch.as_tensor(x, dtype=dt).to(device)  # noqa: E731
     role = t(arr["role"], torch.int16) if "role" in arr else None
+    steps = t(arr["n_steps"], torch.int16) if "n_steps" in arr else None
     return make_arrivals(t(arr["offsets"], torch.int32), t(arr["q_idx"], torch.int32),
-                         t(arr["budget"], torch.int16), t(arr["base_svc"], torch.int16), role)
+                         t(arr["budget"], torch.int16), t(arr["base_svc"], torch.int16), role, steps)
 
 
 class Pool:
@@ -66,6 +70,18 @@ class Pool:
     def state(self, env_begin=0, env_count=None, with_queues=True):
         n = self.E - env_begin if env_count is None else env_count
         return im_read_state(self.h, env_begin, n, self.M, self.A, self.S, self.qcap, with_queues)
+
+    def chain_state(self, env_begin=0, env_count=None):
+        n = self.E - env_begin if env_count is None else env_count
+        return im_read_chain_state(self.h, env_begin, n, self.M, self.S, self.qcap)
+
+    def rows(self):
+        """Chain pools: (row offsets int32 [E + 1], row count) of the current
+        tick, copied to the host (synchronises)."""
+        r = im_get_rows(self.h)
+        off = _lib.device_to_host(r.offsets, np.int32, self.E + 1)
+        cnt = _lib.device_to_host(r.n_rows, np.int32, 1)
+        return off, int(cnt[0])
 
     def write_state(self, env_begin, s):
         im_write_state(self.h, env_begin, s)

@@ -19,10 +19,11 @@ IM_OK, IM_EINVAL, IM_ENOMEM, IM_EHIP, IM_EDEVICE, IM_ESTATE, IM_EUNSUPPORTED = 0
 IM_F32, IM_BF16 = 0, 1
 KEY_MODES = {"slack": 0, "deadline": 1, "fcfs": 2}
 IM_ERR_QIDX, IM_ERR_COUNT, IM_ERR_BUDGET, IM_ERR_SVC, IM_ERR_ACTION, IM_ERR_ROLE = 1, 2, 4, 8, 16, 32
+IM_ERR_STEPS = 64
 IM_NET_MLP, IM_NET_DUAL = 0, 1
 
 EXPORTED = ("im_pool_create", "im_pool_create_dual", "im_route", "im_route_sample", "im_schedule", "im_tick", "im_destroy",
-            "im_dual_update", "im_set_rpm_limit",
+            "im_dual_update", "im_set_rpm_limit", "im_get_rows", "im_read_chain_state",
             "im_read_state", "im_write_state", "im_set_enabled", "im_set_capacity",
             "im_get_error", "im_clear_error", "im_last_error")
 
@@ -35,13 +36,20 @@ class ImPoolDesc(ctypes.Structure):
                 ("widths", ctypes.c_int32 * 4), ("dtype", ctypes.c_int32),
                 ("key_mode", ctypes.c_int32), ("max_arrivals_per_env_tick", ctypes.c_int32),
                 ("budget_max", ctypes.c_int32), ("value_head", ctypes.c_int32),
-                ("net", ctypes.c_int32), ("n_roles", ctypes.c_int32)]
+                ("net", ctypes.c_int32), ("n_roles", ctypes.c_int32),
+                ("max_steps", ctypes.c_int32)]
 
 
 class ImArrivals(ctypes.Structure):
     _fields_ = [("offsets", ctypes.c_void_p), ("q_idx", ctypes.c_void_p),
                 ("budget", ctypes.c_void_p), ("base_svc", ctypes.c_void_p),
-                ("role", ctypes.c_void_p), ("n_total", ctypes.c_int32)]
+                ("role", ctypes.c_void_p), ("n_steps", ctypes.c_void_p),
+                ("n_total", ctypes.c_int32)]
+
+
+class ImRows(ctypes.Structure):
+    _fields_ = [("offsets", ctypes.c_void_p), ("n_rows", ctypes.c_void_p),
+                ("q_idx", ctypes.c_void_p), ("budget", ctypes.c_void_p), ("role", ctypes.c_void_p)]
 
 
 # im_dual_net fields, in order, and the workload parameter names they take.
@@ -63,7 +71,10 @@ class ImPolicyOut(ctypes.Structure):
 
 
 ENTRY_DT = np.dtype([("key", "<i4"), ("id", "<i4"), ("t_arr", "<i4"), ("svc", "<u2"),
-                     ("budget", "<u2")])
+                     ("budget", "<i2")])
+CHAIN_DT = np.dtype([("q_idx", "<i4"), ("k", "<i2"), ("n_steps", "<i2"), ("role0", "<i2"),
+                     ("base_svc", "<i2"), ("beta", "<i4")])
+PENDING_DT = np.dtype([("ch", CHAIN_DT), ("deadline", "<i4")])
 SLOT_DT = np.dtype([("id", "<i4"), ("t_arr", "<i4"), ("rem", "<i4"), ("budget", "<i4")])
 MODEL_DT = np.dtype([("qlen", "<i4"), ("busy", "<i4"), ("ewma_q8", "<i4"), ("backlog", "<i4"),
                      ("capacity", "<i4"), ("enabled", "<i4"), ("_p0", "<i4"), ("_p1", "<i4"),
@@ -71,9 +82,11 @@ MODEL_DT = np.dtype([("qlen", "<i4"), ("busy", "<i4"), ("ewma_q8", "<i4"), ("bac
                      ("completed", "<i8"), ("slo_met", "<i8"), ("lat_sum", "<i8"),
                      ("wait_sum", "<i8"), ("cost_q16", "<i8"), ("rpm_limit", "<i4"),
                      ("rpm_count", "<i4"), ("rpm_hist", "u1", (60,)), ("_p3", "<i4")])
-ENV_DT = np.dtype([("arrived", "<i8"), ("rej_nomodel", "<i8"), ("next_id", "<i4"), ("_p", "<i4")])
+ENV_DT = np.dtype([("arrived", "<i8"), ("rej_nomodel", "<i8"), ("next_id", "<i4"), ("_p", "<i4"),
+                   ("q_done", "<i8"), ("q_met", "<i8")])
 assert ENTRY_DT.itemsize == 16 and SLOT_DT.itemsize == 16
-assert MODEL_DT.itemsize == 168 and ENV_DT.itemsize == 24
+assert MODEL_DT.itemsize == 168 and ENV_DT.itemsize == 40
+assert CHAIN_DT.itemsize == 16 and PENDING_DT.itemsize == 20
 
 _lib = None
 
@@ -105,6 +118,8 @@ def load() -> ctypes.CDLL:
     L.im_set_enabled.argtypes = [P, I32, I32, I32, P]
     L.im_set_capacity.argtypes = [P, I32, I32, I32, P]
     L.im_set_rpm_limit.argtypes = [P, I32, I32, I32, P]
+    L.im_get_rows.argtypes = [P, ctypes.POINTER(ImRows)]
+    L.im_read_chain_state.argtypes = [P, I32, I32, P, P, P, P]
     L.im_get_error.argtypes = [P, ctypes.POINTER(I32)]
     L.im_clear_error.argtypes = [P]
     L.im_last_error.argtypes = [P]
@@ -154,6 +169,7 @@ def make_desc(cfg: dict) -> ImPoolDesc:
     d.budget_max = cfg["budget_max"]
     vh = 1 if cfg.get("value_head") else 0
     d.value_head = vh
+    d.max_steps = int(cfg.get("max_steps", 1))
     if cfg.get("net") == "dual":
         d.net, d.n_roles = IM_NET_DUAL, cfg["n_roles"]
         return d
@@ -164,17 +180,18 @@ def make_desc(cfg: dict) -> ImPoolDesc:
     return d
 
 
-def make_arrivals(offsets, q_idx, budget, base_svc, role=None) -> ImArrivals:
-    """Arrivals of one tick from device tensors (int32, int32, int16, int16
-    and, for dual-pathway pools, int16 roles)."""
+def make_arrivals(offsets, q_idx, budget, base_svc, role=None, n_steps=None) -> ImArrivals:
+    """Arrivals of one tick from device tensors (int32, int32, int16, int16;
+    int16 roles for dual-pathway pools, int16 calls per query for chain pools)."""
     a = ImArrivals()
     a.offsets = offsets.data_ptr()
     a.q_idx = q_idx.data_ptr() if q_idx.numel() else None
     a.budget = budget.data_ptr() if budget.numel() else None
     a.base_svc = base_svc.data_ptr() if base_svc.numel() else None
     a.role = role.data_ptr() if role is not None and role.numel() else None
+    a.n_steps = n_steps.data_ptr() if n_steps is not None and n_steps.numel() else None
     a.n_total = int(q_idx.numel())
-    a._keep = (offsets, q_idx, budget, base_svc, role)
+    a._keep = (offsets, q_idx, budget, base_svc, role, n_steps)
     return a
 
 
@@ -241,6 +258,53 @@ def im_dual_update(pool, eta: float, lambda_max: float, lam, stream=None):
     _check(load().im_dual_update(pool, float(eta), float(lambda_max), _dptr(lam), _stream(stream)), pool)
 
 
+_hip = None
+
+
+def device_to_host(ptr, dtype, count) -> np.ndarray:
+    """Copy `count` elements of `dtype` from a device pointer the library
+    returned (hipMemcpy of the HIP runtime; synchronises)."""
+    global _hip
+    if _hip is None:
+        _hip = ctypes.CDLL("libamdhip64.so")
+        _hip.hipDeviceSynchronize.restype = ctypes.c_int
+        _hip.hipMemcpy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int]
+        _hip.hipMemcpy.restype = ctypes.c_int
+    out = np.empty(count, dtype)
+    if count:
+        if _hip.hipDeviceSynchronize() != 0 or _hip.hipMemcpy(_hptr(out), ptr, out.nbytes, 2) != 0:
+            raise RuntimeError("hipMemcpy device-to-host failed")
+    return out
+
+
+def im_get_rows(pool) -> ImRows:
+    """Chain pools: device pointers to the current tick's rows."""
+    r = ImRows()
+    _check(load().im_get_rows(pool, ctypes.byref(r)), pool)
+    return r
+
+
+def im_read_chain_state(pool, env_begin: int, env_count: int, M: int, S: int, qcap: int) -> dict:
+    """Chain pools: chain words of the queued calls (service order, like
+    im_read_state's queues) and of the busy slots, the pending calls and their
+    counts, as numpy arrays in the oracle's chain_state layout (without the
+    query counters, which im_read_state reports per env)."""
+    E = env_count
+    q = np.zeros(E * M * qcap, CHAIN_DT)
+    sl = np.zeros(E * M * S, CHAIN_DT)
+    pend = np.zeros(E * M * S, PENDING_DT)
+    pc = np.zeros(E, np.int32)
+    _check(load().im_read_chain_state(pool, env_begin, env_count, _hptr(q), _hptr(sl), _hptr(pend),
+                                      _hptr(pc)), pool)
+
+    def six(c):
+        return np.stack([c["q_idx"], c["k"], c["n_steps"], c["role0"], c["base_svc"], c["beta"]],
+                        axis=-1).astype(np.int32)
+    pe = np.concatenate([six(pend["ch"]), pend["deadline"][:, None].astype(np.int32)], axis=-1)
+    return dict(queue_chain=six(q).reshape(E, M, qcap, 6), slot_chain=six(sl).reshape(E, M, S, 6),
+                pending=pe.reshape(E, M * S, 7), pending_count=pc)
+
+
 def im_destroy(pool):
     if pool:
         load().im_destroy(pool)
@@ -299,7 +363,7 @@ def im_read_state(pool, env_begin: int, env_count: int, M: int, A: int, S: int, 
     sarr = np.stack([sl["id"], sl["t_arr"], sl["rem"], sl["budget"]], axis=-1).astype(np.int32)
     out = dict(t=int(tick.value), next_id=envs["next_id"].copy(), arrived=envs["arrived"].copy(),
                rej_nomodel=envs["rej_nomodel"].copy(), slots=sarr, queues=qarr,
-               hist=hist.reshape(E, A))
+               hist=hist.reshape(E, A), q_done=envs["q_done"].copy(), q_met=envs["q_met"].copy())
     for k, f in (("qlen", "qlen"), ("busy", "busy"), ("ewma", "ewma_q8"), ("backlog", "backlog"),
                  ("cap", "capacity"), ("enabled", "enabled"), ("rej_overflow", "rej_overflow"),
                  ("enqueued", "enqueued"), ("started", "started"), ("completed", "completed"),
@@ -318,6 +382,8 @@ def im_write_state(pool, env_begin: int, s: dict):
     qcap = s["queues"].shape[2]
     envs = np.zeros(E, ENV_DT)
     envs["arrived"], envs["rej_nomodel"], envs["next_id"] = s["arrived"], s["rej_nomodel"], s["next_id"]
+    if "q_done" in s:
+        envs["q_done"], envs["q_met"] = s["q_done"], s["q_met"]
     models = np.zeros((E, M), MODEL_DT)
     for k, f in (("qlen", "qlen"), ("busy", "busy"), ("ewma", "ewma_q8"), ("backlog", "backlog"),
                  ("cap", "capacity"), ("enabled", "enabled"), ("rej_overflow", "rej_overflow"),

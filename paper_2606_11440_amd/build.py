@@ -10,7 +10,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libinframind.so")
-SOURCES = ["route.hip", "schedule.hip", "pool.hip"]
+SOURCES = ["route.hip", "schedule.hip", "rows.hip", "pool.hip"]
 # measurement probe used by the benchmark only (not part of the tick's library)
 PROBE_LIB = os.path.join(HERE, "libimprobe.so")
 PROBE_SOURCES = ["peak_probe.hip"]

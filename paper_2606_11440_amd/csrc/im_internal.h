@@ -46,7 +46,38 @@ __host__ __device__ inline int snap_valid_offset(int M) { return 4 * M; }   // i
 enum { C_REJ_OVERFLOW = 0, C_ENQUEUED, C_STARTED, C_COMPLETED, C_SLO_MET, C_LAT_SUM,
        C_WAIT_SUM, C_COST_Q16, C_NUM = 8 };
 
-// Queue entry in device memory: {key, id, t_arr, svc | budget << 16}.
+// Multi-step chains (Sec. 4.3): a call carries its query in two words that
+// travel with its queue entry, its slot and its pending record:
+//   A = q_idx | k << 24 | n_steps << 28   (call k of n_steps; q_idx < 2^24)
+//   B = base_svc | beta << 12 | role0 << 27   (base_svc < 2^12, query budget
+//       beta < 2^15, role of the first call < 32)
+// A pending call (spawned by the completion of call k - 1, routed at the next
+// tick) is {A, B, deadline, 0}. Env counters: arrived, rej_nomodel, completed
+// queries, queries completed by their deadline.
+constexpr int kMaxSteps = 15;
+constexpr int kEnvCnt = 4;
+enum { E_ARRIVED = 0, E_REJ_NOMODEL, E_Q_DONE, E_Q_MET };
+__host__ __device__ inline int32_t chain_a(int32_t q_idx, int k, int n_steps) {
+  return (int32_t)((uint32_t)q_idx | ((uint32_t)k << 24) | ((uint32_t)n_steps << 28));
+}
+__host__ __device__ inline int32_t chain_b(int base, int beta, int role0) {
+  return (int32_t)(((uint32_t)base & 0xfffu) | (((uint32_t)beta & 0x7fffu) << 12) |
+                   (((uint32_t)role0 & 31u) << 27));
+}
+__host__ __device__ inline int32_t chain_q(int32_t A) { return A & 0xffffff; }
+__host__ __device__ inline int chain_k(int32_t A) { return (A >> 24) & 15; }
+__host__ __device__ inline int chain_n(int32_t A) { return (int)((uint32_t)A >> 28); }
+__host__ __device__ inline int chain_base(int32_t B) { return B & 0xfff; }
+__host__ __device__ inline int chain_beta(int32_t B) { return (B >> 12) & 0x7fff; }
+__host__ __device__ inline int chain_role0(int32_t B) { return (int)((uint32_t)B >> 27); }
+// remaining budget of a call routed at tick t, in the int16 range of budgets
+__host__ __device__ inline int32_t remaining_budget(int32_t deadline, int32_t t) {
+  const int64_t b = (int64_t)deadline - t;
+  return (int32_t)(b < -32768 ? -32768 : (b > 32767 ? 32767 : b));
+}
+
+// Queue entry in device memory: {key, id, t_arr, svc | budget << 16} (budget
+// signed: a later call of a chain may be routed past its deadline).
 // Slot in device memory: {id (-1 free), t_arr, tick at which it completes, budget};
 // the state export reports the service ticks left instead of the completion tick.
 
@@ -101,6 +132,8 @@ struct RouteArgs {
   float* logp;
   float* entropy;
   float* value;                       // row A of the last layer (value head), or NULL
+  const int32_t* n_total_dev;         // chain pools: the tick's row count (device); n_total
+                                      // then bounds it
   // dual-pathway executor (net == IM_NET_DUAL): W[0] semantic (query half),
   // W[1] merge, W[2] action/value fragments; W_res resource-layer fragments
   int32_t net;
@@ -115,13 +148,25 @@ struct SchedArgs {
   const int32_t* q_idx;
   const int16_t* budget;
   const int16_t* base_svc;
-  const int32_t* actions;
+  const int32_t* actions;   // per row: at offsets[e] + i, or (chains) roff[e] + i
+  // multi-step chains: calls per arriving query, row offsets of the tick (the
+  // env's pending calls, then its arrivals), pending calls and their counts
+  // double-buffered by tick parity ([2][E * pend_cap], [2][E]), the ext words
+  // (A, B) of queue entries and slots
+  const int16_t* n_steps;
+  int32_t max_steps, pend_cap;
+  const int32_t* roff;
+  int4* pend;
+  int32_t* pcnt;
+  int2* front_ext;
+  int2* pool_ext;
+  int2* slot_ext;
   int32_t n_total;
   int32_t E, M, K, A, S, qcap, max_arrivals, key_mode;
   int64_t Q;
   ModelRec* ms;
   int64_t* cnt;       // [E*M*C_NUM]
-  int64_t* env_cnt;   // [E*2] arrived, rej_nomodel
+  int64_t* env_cnt;   // [E*kEnvCnt] arrived, rej_nomodel, completed queries, on-time queries
   int64_t* hist;      // [E*A]
   int4* slots;        // [E*M*S]
   int4* front;        // [E*M*kFront]
@@ -138,8 +183,11 @@ struct SchedArgs {
 // Host-side launchers (defined in the .hip files).
 // Dual update (Eq. 7): acc [2] device accumulators (zero between calls), last
 // [2] totals at the previous update, lambda device in/out.
-hipError_t launch_dual_update(const int64_t* cnt, int64_t n_em, unsigned long long* acc, int64_t* last,
-                              double eta, double lambda_max, double* lambda, hipStream_t s);
+// env_cnt (chain pools, else NULL): queries are counted from its completed-query
+// column instead of the per-model completions.
+hipError_t launch_dual_update(const int64_t* cnt, int64_t n_em, const int64_t* env_cnt, int64_t n_env,
+                              unsigned long long* acc, int64_t* last, double eta, double lambda_max,
+                              double* lambda, hipStream_t s);
 bool route_supported(int dtype, int hidden, int n_layers, int out_tiles);
 bool dual_supported(int embed_dim, int out_rows);
 // Role projections of the dual-pathway executor: out[r][tile][g][16] =
@@ -150,7 +198,26 @@ hipError_t launch_role_projection(const uint16_t* w_role, const uint16_t* roles,
 hipError_t launch_route(const RouteArgs& a, int dtype, int hidden, int n_layers, int out_tiles,
                         hipStream_t s);
 // rpm: some model of the pool is (or was) rate-limited (blackbox windows tracked)
-hipError_t launch_schedule(const SchedArgs& a, bool rpm, hipStream_t s);
+hipError_t launch_schedule(const SchedArgs& a, bool rpm, bool chain, hipStream_t s);
+// Rows of a chain pool's tick: row offsets (pending calls first, then the
+// usable arrivals of each env), the row count and the route step's per-row
+// inputs (q_idx, remaining budget, role of the call).
+struct RowsArgs {
+  const int32_t* offsets;   // arrival CSR [E+1]
+  int32_t n_total, E, M, max_arrivals, pend_cap, n_roles;   // n_roles: 0 for MLP pools
+  const int32_t* q_idx;
+  const int16_t* budget;
+  const int16_t* role;
+  const ModelRec* ms;       // the tick: ms[0].t
+  const int4* pend;         // [2][E * pend_cap]
+  const int32_t* pcnt;      // [2][E]
+  int32_t* roff;            // out [E+1]
+  int32_t* n_rows;          // out [1]
+  int32_t* rq;              // out per row
+  int16_t* rb;
+  int16_t* rr;
+};
+hipError_t launch_rows(const RowsArgs& a, hipStream_t s);
 // Recompute the snapshot rows of envs [e0, e0 + ne) from the model records.
 hipError_t launch_snapshot(const SchedArgs& a, int e0, int ne, hipStream_t s);
 

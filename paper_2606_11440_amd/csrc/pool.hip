@@ -43,6 +43,22 @@ struct im_pool {
   float* dual_p = nullptr;                  // dual-pathway executor: fp32 parameter block
   unsigned long long* dual_acc = nullptr;   // [2] completions, Q16 cost (zero between calls)
   int64_t* dual_last = nullptr;             // [2] totals at the previous dual update
+  // multi-step chains: pending calls [2][E * pend_cap] and their counts
+  // [2][E] (by tick parity), chain words of front, pool and slot entries, the
+  // tick's rows (offsets, count, per-row query row, budget, role)
+  bool chains = false;
+  int32_t pend_cap = 0;
+  int64_t rows_cap = 0;
+  int4* pend = nullptr;
+  int32_t* pcnt = nullptr;
+  int2* front_ext = nullptr;
+  int2* pool_ext = nullptr;
+  int2* slot_ext = nullptr;
+  int32_t* roff = nullptr;
+  int32_t* n_rows = nullptr;
+  int32_t* rq = nullptr;
+  int16_t* rb = nullptr;
+  int16_t* rr = nullptr;
   int32_t t = 0;
   int32_t cu_count = 0;
   bool rpm_active = false;   // some model was given a rate limit (the windows are tracked from then on)
@@ -122,6 +138,8 @@ im_status check_arrivals(im_pool* p, const im_arrivals* arr) {
     return fail(p, IM_EINVAL, "arrival field pointer is NULL");
   if (arr->n_total > 0 && p->d.net == IM_NET_DUAL && !arr->role)
     return fail(p, IM_EINVAL, "role is NULL (required by a dual-pathway pool)");
+  if (arr->n_total > 0 && p->chains && !arr->n_steps)
+    return fail(p, IM_EINVAL, "n_steps is NULL (required by a chain pool)");
   if ((int64_t)arr->n_total > (int64_t)p->d.n_envs * p->d.max_arrivals_per_env_tick)
     return fail(p, IM_EINVAL, "n_total exceeds n_envs * max_arrivals_per_env_tick");
   return IM_OK;
@@ -134,7 +152,8 @@ void free_pool(im_pool* p) {
   }
   void* bufs[] = {p->inv_tab, p->ms, p->cnt, p->env_cnt, p->hist, p->slots,
                   p->front, p->qpool, p->snap, p->err, p->act_buf, p->dual_acc, p->dual_last,
-                  p->rpm_ring, p->W_res, p->dual_p};
+                  p->rpm_ring, p->W_res, p->dual_p, p->pend, p->pcnt, p->front_ext,
+                  p->pool_ext, p->slot_ext, p->roff, p->n_rows, p->rq, p->rb, p->rr};
   for (void* b : bufs) if (b) (void)hipFree(b);
   delete p;
 }
@@ -153,6 +172,11 @@ im_status check_desc_common(const im_pool_desc& d, int64_t n_queries, const int3
   if (d.max_arrivals_per_env_tick < 1) return fail(nullptr, IM_EINVAL, "max_arrivals_per_env_tick < 1");
   if (d.budget_max < 1) return fail(nullptr, IM_EINVAL, "budget_max < 1");
   if (n_queries < 1 || n_queries > INT32_MAX) return fail(nullptr, IM_EINVAL, "n_queries out of range");
+  if (d.max_steps < 0 || d.max_steps > IM_MAX_STEPS) return fail(nullptr, IM_EINVAL, "max_steps out of range");
+  if (d.max_steps > 1 && n_queries > (1 << 24))
+    return fail(nullptr, IM_EUNSUPPORTED, "chain pools take at most 2^24 query-embedding rows");
+  if (d.max_steps > 1 && d.net == IM_NET_DUAL && d.n_roles > 32)
+    return fail(nullptr, IM_EUNSUPPORTED, "chain pools of the dual-pathway executor take at most 32 roles");
   for (int64_t i = 0; i < (int64_t)d.n_envs * d.n_models; ++i)
     if (capacity[i] < 0 || capacity[i] > d.max_slots)
       return fail(nullptr, IM_EINVAL, "capacity outside [0, max_slots]");
@@ -164,6 +188,8 @@ im_pool* new_pool(const im_pool_desc& d, int64_t n_queries, const void* emb) {
   p->d = d;
   p->A = d.n_models * d.n_depths;
   p->S = d.max_slots;
+  p->chains = d.max_steps > 1;
+  p->pend_cap = d.n_models * d.max_slots;
   p->Q = n_queries;
   p->emb = emb;
   (void)hipGetDevice(&p->device);
@@ -202,7 +228,7 @@ im_status init_state(im_pool* p, const int32_t* capacity, hipStream_t s) {
     st = upload(p, &p->ms, recs);
   }
   if (st == IM_OK) st = zalloc(p, &p->cnt, EM * im::C_NUM);
-  if (st == IM_OK) st = zalloc(p, &p->env_cnt, (size_t)d.n_envs * 2);
+  if (st == IM_OK) st = zalloc(p, &p->env_cnt, (size_t)d.n_envs * im::kEnvCnt);
   if (st == IM_OK) st = zalloc(p, &p->hist, (size_t)d.n_envs * p->A);
   if (st == IM_OK) {
     std::vector<int4> sl(EM * d.max_slots, make_int4(-1, 0, 0, 0));
@@ -215,8 +241,22 @@ im_status init_state(im_pool* p, const int32_t* capacity, hipStream_t s) {
   if (st == IM_OK) st = zalloc(p, &p->err, 1);
   if (st == IM_OK) st = zalloc(p, &p->dual_acc, 2);
   if (st == IM_OK) st = zalloc(p, &p->dual_last, 2);
+  if (st == IM_OK && p->chains) {
+    const size_t E = (size_t)d.n_envs;
+    p->rows_cap = (int64_t)E * (d.max_arrivals_per_env_tick + p->pend_cap);
+    st = zalloc(p, &p->pend, 2 * E * p->pend_cap);
+    if (st == IM_OK) st = zalloc(p, &p->pcnt, 2 * E);
+    if (st == IM_OK) st = zalloc(p, &p->front_ext, EM * im::kFront);
+    if (st == IM_OK) st = zalloc(p, &p->pool_ext, EM * (size_t)d.queue_cap);
+    if (st == IM_OK) st = zalloc(p, &p->slot_ext, EM * d.max_slots);
+    if (st == IM_OK) st = zalloc(p, &p->roff, E + 1);
+    if (st == IM_OK) st = zalloc(p, &p->n_rows, 1);
+    if (st == IM_OK) st = zalloc(p, &p->rq, (size_t)p->rows_cap);
+    if (st == IM_OK) st = zalloc(p, &p->rb, (size_t)p->rows_cap);
+    if (st == IM_OK) st = zalloc(p, &p->rr, (size_t)p->rows_cap);
+  }
   if (st == IM_OK) {
-    p->act_cap = (int64_t)d.n_envs * d.max_arrivals_per_env_tick;
+    p->act_cap = (int64_t)d.n_envs * d.max_arrivals_per_env_tick + (p->chains ? (int64_t)d.n_envs * p->pend_cap : 0);
     st = zalloc(p, &p->act_buf, (size_t)p->act_cap);
   }
   if (st == IM_OK) {
@@ -469,7 +509,6 @@ static im::RouteArgs route_args(im_pool* p, const im_arrivals* arr, int32_t* act
   a.q_idx = arr->q_idx;
   a.budget = arr->budget;
   a.n_total = arr->n_total;
-  a.envs_per_row = arr->n_total > 0 ? (float)((double)p->d.n_envs / arr->n_total) : 0.f;
   a.E = p->d.n_envs;
   a.M = p->d.n_models;
   a.K = p->d.n_depths;
@@ -495,7 +534,48 @@ static im::RouteArgs route_args(im_pool* p, const im_arrivals* arr, int32_t* act
     a.W_res = p->W_res;
     a.dual_p = p->dual_p;
   }
+  if (p->chains) {
+    // the tick's rows (pending calls, then arrivals) built on the device;
+    // their count is read there, n_total bounds it
+    a.offsets = p->roff;
+    a.q_idx = p->rq;
+    a.budget = p->rb;
+    a.role = p->d.net == IM_NET_DUAL ? p->rr : nullptr;
+    a.n_total = arr->n_total + p->d.n_envs * p->pend_cap;
+    a.n_total_dev = p->n_rows;
+  }
+  a.envs_per_row = a.n_total > 0 ? (float)((double)p->d.n_envs / a.n_total) : 0.f;
   return a;
+}
+
+// Chain pools: the tick's rows from the pending calls and the arrivals.
+static hipError_t build_rows(im_pool* p, const im_arrivals* arr, hipStream_t s) {
+  im::RowsArgs r{};
+  r.offsets = arr->offsets;
+  r.n_total = arr->n_total;
+  r.E = p->d.n_envs;
+  r.M = p->d.n_models;
+  r.max_arrivals = p->d.max_arrivals_per_env_tick;
+  r.pend_cap = p->pend_cap;
+  r.n_roles = p->d.net == IM_NET_DUAL ? p->d.n_roles : 0;
+  r.q_idx = arr->q_idx;
+  r.budget = arr->budget;
+  r.role = p->d.net == IM_NET_DUAL ? arr->role : nullptr;
+  r.ms = p->ms;
+  r.pend = p->pend;
+  r.pcnt = p->pcnt;
+  r.roff = p->roff;
+  r.n_rows = p->n_rows;
+  r.rq = p->rq;
+  r.rb = p->rb;
+  r.rr = p->rr;
+  return im::launch_rows(r, s);
+}
+
+static im_status route_impl(im_pool* p, const im_arrivals* arr, im::RouteArgs a, hipStream_t s) {
+  if (p->chains) IM_HIP(p, build_rows(p, arr, s));
+  IM_HIP(p, im::launch_route(a, p->d.dtype, p->hidden, p->n_layers, p->out_tiles, s));
+  return IM_OK;
 }
 
 im_status im_route(im_pool* p, const im_arrivals* arr, int32_t* actions, float* logits,
@@ -503,11 +583,8 @@ im_status im_route(im_pool* p, const im_arrivals* arr, int32_t* actions, float* 
   if (!p) return fail(nullptr, IM_EINVAL, "pool is NULL");
   im_status st = check_arrivals(p, arr);
   if (st != IM_OK) return st;
-  if (arr->n_total > 0 && !actions) return fail(p, IM_EINVAL, "actions is NULL");
-  const im::RouteArgs a = route_args(p, arr, actions, logits);
-  IM_HIP(p, im::launch_route(a, p->d.dtype, p->hidden, p->n_layers, p->out_tiles,
-                             (hipStream_t)stream));
-  return IM_OK;
+  if ((arr->n_total > 0 || p->chains) && !actions) return fail(p, IM_EINVAL, "actions is NULL");
+  return route_impl(p, arr, route_args(p, arr, actions, logits), (hipStream_t)stream);
 }
 
 im_status im_route_sample(im_pool* p, const im_arrivals* arr, uint64_t seed, int32_t greedy,
@@ -516,7 +593,7 @@ im_status im_route_sample(im_pool* p, const im_arrivals* arr, uint64_t seed, int
   im_status st = check_arrivals(p, arr);
   if (st != IM_OK) return st;
   if (!out) return fail(p, IM_EINVAL, "out is NULL");
-  if (arr->n_total > 0 && !out->actions) return fail(p, IM_EINVAL, "actions is NULL");
+  if ((arr->n_total > 0 || p->chains) && !out->actions) return fail(p, IM_EINVAL, "actions is NULL");
   if (out->value && !p->d.value_head) return fail(p, IM_EINVAL, "value requested from a pool without a value head");
   im::RouteArgs a = route_args(p, arr, out->actions, out->logits);
   a.rl = 1;
@@ -526,16 +603,13 @@ im_status im_route_sample(im_pool* p, const im_arrivals* arr, uint64_t seed, int
   a.logp = out->logp;
   a.entropy = out->entropy;
   a.value = out->value;
-  IM_HIP(p, im::launch_route(a, p->d.dtype, p->hidden, p->n_layers, p->out_tiles,
-                             (hipStream_t)stream));
-  return IM_OK;
+  return route_impl(p, arr, a, (hipStream_t)stream);
 }
 
-im_status im_schedule(im_pool* p, const im_arrivals* arr, const int32_t* actions, void* stream) {
-  if (!p) return fail(nullptr, IM_EINVAL, "pool is NULL");
-  im_status st = check_arrivals(p, arr);
-  if (st != IM_OK) return st;
-  if (arr->n_total > 0 && !actions) return fail(p, IM_EINVAL, "actions is NULL");
+// build: rebuild the chain pool's rows first (not needed right after a route
+// of the same tick).
+static im_status schedule_impl(im_pool* p, const im_arrivals* arr, const int32_t* actions, bool build,
+                               hipStream_t s) {
   if (p->t == INT32_MAX - 65536) return fail(p, IM_EINVAL, "tick counter exhausted");
   im::SchedArgs a = sched_args(p);
   a.offsets = arr->offsets;
@@ -548,9 +622,29 @@ im_status im_schedule(im_pool* p, const im_arrivals* arr, const int32_t* actions
     a.role = arr->role;
     a.n_roles = p->d.n_roles;
   }
-  IM_HIP(p, im::launch_schedule(a, p->rpm_active, (hipStream_t)stream));
+  if (p->chains) {
+    if (build) IM_HIP(p, build_rows(p, arr, s));
+    a.n_steps = arr->n_steps;
+    a.max_steps = p->d.max_steps;
+    a.pend_cap = p->pend_cap;
+    a.roff = p->roff;
+    a.pend = p->pend;
+    a.pcnt = p->pcnt;
+    a.front_ext = p->front_ext;
+    a.pool_ext = p->pool_ext;
+    a.slot_ext = p->slot_ext;
+  }
+  IM_HIP(p, im::launch_schedule(a, p->rpm_active, p->chains, s));
   p->t += 1;
   return IM_OK;
+}
+
+im_status im_schedule(im_pool* p, const im_arrivals* arr, const int32_t* actions, void* stream) {
+  if (!p) return fail(nullptr, IM_EINVAL, "pool is NULL");
+  im_status st = check_arrivals(p, arr);
+  if (st != IM_OK) return st;
+  if ((arr->n_total > 0 || p->chains) && !actions) return fail(p, IM_EINVAL, "actions is NULL");
+  return schedule_impl(p, arr, actions, true, (hipStream_t)stream);
 }
 
 static im::SchedArgs sched_args(im_pool* p) {
@@ -585,16 +679,28 @@ im_status im_tick(im_pool* p, const im_arrivals* arr, int32_t* actions_out, void
   im_status st = check_arrivals(p, arr);
   if (st != IM_OK) return st;
   int32_t* act = actions_out ? actions_out : p->act_buf;
-  st = im_route(p, arr, act, nullptr, stream);
+  st = route_impl(p, arr, route_args(p, arr, act, nullptr), (hipStream_t)stream);
   if (st != IM_OK) return st;
-  return im_schedule(p, arr, act, stream);
+  return schedule_impl(p, arr, act, false, (hipStream_t)stream);
+}
+
+im_status im_get_rows(im_pool* p, im_rows* out) {
+  if (!p || !out) return fail(p, IM_EINVAL, "NULL argument to im_get_rows");
+  if (!p->chains) return fail(p, IM_EINVAL, "im_get_rows: not a chain pool");
+  out->offsets = p->roff;
+  out->n_rows = p->n_rows;
+  out->q_idx = p->rq;
+  out->budget = p->rb;
+  out->role = p->rr;
+  return IM_OK;
 }
 
 im_status im_dual_update(im_pool* p, double eta, double lambda_max, double* lambda, void* stream) {
   if (!p) return fail(nullptr, IM_EINVAL, "pool is NULL");
   if (!lambda) return fail(p, IM_EINVAL, "lambda is NULL");
   if (!(eta >= 0.0) || !(lambda_max >= 0.0)) return fail(p, IM_EINVAL, "eta and lambda_max must be >= 0");
-  IM_HIP(p, im::launch_dual_update(p->cnt, (int64_t)p->d.n_envs * p->d.n_models, p->dual_acc,
+  IM_HIP(p, im::launch_dual_update(p->cnt, (int64_t)p->d.n_envs * p->d.n_models,
+                                   p->chains ? p->env_cnt : nullptr, p->d.n_envs, p->dual_acc,
                                    p->dual_last, eta, lambda_max, lambda, (hipStream_t)stream));
   return IM_OK;
 }
@@ -674,14 +780,17 @@ im_status im_read_state(im_pool* p, int32_t env_begin, int32_t env_count, int32_
   }
   if (tick) *tick = p->t;
   if (envs && env_count) {
-    std::vector<int64_t> ec((size_t)env_count * 2);
-    IM_HIP(p, hipMemcpy(ec.data(), p->env_cnt + (size_t)env_begin * 2, ec.size() * 8,
+    constexpr int EC = im::kEnvCnt;
+    std::vector<int64_t> ec((size_t)env_count * EC);
+    IM_HIP(p, hipMemcpy(ec.data(), p->env_cnt + (size_t)env_begin * EC, ec.size() * 8,
                         hipMemcpyDeviceToHost));
     for (int e = 0; e < env_count; ++e) {
-      envs[e].arrived = ec[2 * e];
-      envs[e].rej_nomodel = ec[2 * e + 1];
+      envs[e].arrived = ec[EC * e + im::E_ARRIVED];
+      envs[e].rej_nomodel = ec[EC * e + im::E_REJ_NOMODEL];
       envs[e].next_id = recs[(size_t)e * M].next_id;
       envs[e]._pad = 0;
+      envs[e].q_done = ec[EC * e + im::E_Q_DONE];
+      envs[e].q_met = ec[EC * e + im::E_Q_MET];
     }
   }
   if (models) {
@@ -745,7 +854,7 @@ im_status im_read_state(im_pool* p, int32_t env_begin, int32_t env_count, int32_
       for (size_t k = 0; k < tmp.size() && k < (size_t)qcap; ++k) {
         q[k].key = tmp[k].x; q[k].id = tmp[k].y; q[k].t_arr = tmp[k].z;
         q[k].svc = (uint16_t)(tmp[k].w & 0xffff);
-        q[k].budget = (uint16_t)((uint32_t)tmp[k].w >> 16);
+        q[k].budget = (int16_t)(tmp[k].w >> 16);
       }
     }
   }
@@ -756,6 +865,7 @@ im_status im_write_state(im_pool* p, int32_t env_begin, int32_t env_count, int32
                          const im_env_state* envs, const im_model_state* models,
                          const im_slot* slots, const im_entry* queues, const int64_t* hist) {
   if (!p) return fail(nullptr, IM_EINVAL, "pool is NULL");
+  if (p->chains) return fail(p, IM_EUNSUPPORTED, "im_write_state: chain pools are not supported");
   if (env_begin < 0 || env_count < 0 || (int64_t)env_begin + env_count > p->d.n_envs)
     return fail(p, IM_EINVAL, "env range out of bounds");
   if (!envs || !models || !slots || !queues || !hist) return fail(p, IM_EINVAL, "NULL argument");
@@ -833,8 +943,14 @@ im_status im_write_state(im_pool* p, int32_t env_begin, int32_t env_count, int32
     if (ms.rpm_limit > 0 || ms.rpm_count > 0) p->rpm_active = true;
     r.inv_rpm = ms.rpm_limit > 0 ? (float)(1.0 / ms.rpm_limit) : 0.f;
   }
-  std::vector<int64_t> ec((size_t)env_count * 2);
-  for (int e = 0; e < env_count; ++e) { ec[2 * e] = envs[e].arrived; ec[2 * e + 1] = envs[e].rej_nomodel; }
+  constexpr int EC = im::kEnvCnt;
+  std::vector<int64_t> ec((size_t)env_count * EC);
+  for (int e = 0; e < env_count; ++e) {
+    ec[EC * e + im::E_ARRIVED] = envs[e].arrived;
+    ec[EC * e + im::E_REJ_NOMODEL] = envs[e].rej_nomodel;
+    ec[EC * e + im::E_Q_DONE] = envs[e].q_done;
+    ec[EC * e + im::E_Q_MET] = envs[e].q_met;
+  }
   IM_HIP(p, hipDeviceSynchronize());
   if (EMc) {
     IM_HIP(p, hipMemcpy(p->ms + em0, recs.data(), EMc * sizeof(ModelRec), hipMemcpyHostToDevice));
@@ -845,12 +961,93 @@ im_status im_write_state(im_pool* p, int32_t env_begin, int32_t env_count, int32
     IM_HIP(p, hipMemcpy(p->rpm_ring + em0 * im::kRpmRing, ring.data(), ring.size(), hipMemcpyHostToDevice));
   }
   if (env_count) {
-    IM_HIP(p, hipMemcpy(p->env_cnt + (size_t)env_begin * 2, ec.data(), ec.size() * 8, hipMemcpyHostToDevice));
+    IM_HIP(p, hipMemcpy(p->env_cnt + (size_t)env_begin * EC, ec.data(), ec.size() * 8, hipMemcpyHostToDevice));
     IM_HIP(p, hipMemcpy(p->hist + (size_t)env_begin * A, hist, (size_t)env_count * A * 8, hipMemcpyHostToDevice));
   }
   IM_HIP(p, im::launch_snapshot(sched_args(p), env_begin, env_count, nullptr));
   IM_HIP(p, hipDeviceSynchronize());
   p->t = tick;
+  return IM_OK;
+}
+
+im_status im_read_chain_state(im_pool* p, int32_t env_begin, int32_t env_count, im_chain* queues,
+                              im_chain* slots, im_pending* pending, int32_t* pending_count) {
+  if (!p) return fail(nullptr, IM_EINVAL, "pool is NULL");
+  if (!p->chains) return fail(p, IM_EINVAL, "im_read_chain_state: not a chain pool");
+  if (env_begin < 0 || env_count < 0 || (int64_t)env_begin + env_count > p->d.n_envs)
+    return fail(p, IM_EINVAL, "env range out of bounds");
+  IM_HIP(p, hipDeviceSynchronize());
+  const int M = p->d.n_models, S = p->S, qcap = p->d.queue_cap, PM = p->pend_cap;
+  const size_t em0 = (size_t)env_begin * M, EMc = (size_t)env_count * M, E = p->d.n_envs;
+  if (EMc == 0) return IM_OK;
+  std::vector<ModelRec> recs(EMc);
+  IM_HIP(p, hipMemcpy(recs.data(), p->ms + em0, EMc * sizeof(ModelRec), hipMemcpyDeviceToHost));
+  const int32_t t = recs[0].t;
+  auto unpack = [](int2 x) {
+    im_chain c;
+    c.q_idx = im::chain_q(x.x);
+    c.k = (int16_t)im::chain_k(x.x);
+    c.n_steps = (int16_t)im::chain_n(x.x);
+    c.role0 = (int16_t)im::chain_role0(x.y);
+    c.base_svc = (int16_t)im::chain_base(x.y);
+    c.beta = im::chain_beta(x.y);
+    return c;
+  };
+  if (queues) {
+    // the same service order as im_read_state: the front, then the pool by (key, id)
+    std::vector<int4> fr(EMc * im::kFront), pl(EMc * (size_t)qcap);
+    std::vector<int2> frx(fr.size()), plx(pl.size());
+    IM_HIP(p, hipMemcpy(fr.data(), p->front + em0 * im::kFront, fr.size() * sizeof(int4), hipMemcpyDeviceToHost));
+    IM_HIP(p, hipMemcpy(frx.data(), p->front_ext + em0 * im::kFront, frx.size() * sizeof(int2), hipMemcpyDeviceToHost));
+    IM_HIP(p, hipMemcpy(pl.data(), p->qpool + em0 * qcap, pl.size() * sizeof(int4), hipMemcpyDeviceToHost));
+    IM_HIP(p, hipMemcpy(plx.data(), p->pool_ext + em0 * qcap, plx.size() * sizeof(int2), hipMemcpyDeviceToHost));
+    std::memset(queues, 0, EMc * qcap * sizeof(im_chain));
+    std::vector<std::pair<int4, int2>> tmp;
+    for (size_t i = 0; i < EMc; ++i) {
+      const ModelRec& r = recs[i];
+      tmp.clear();
+      for (int k = r.fh; k < r.fh + r.fn; ++k) tmp.push_back({fr[i * im::kFront + k], frx[i * im::kFront + k]});
+      const size_t f = tmp.size();
+      for (int k = 0; k < r.P; ++k) tmp.push_back({pl[i * qcap + k], plx[i * qcap + k]});
+      std::sort(tmp.begin() + f, tmp.end(), [](const std::pair<int4, int2>& x, const std::pair<int4, int2>& y) {
+        return x.first.x != y.first.x ? x.first.x < y.first.x : x.first.y < y.first.y;
+      });
+      for (size_t k = 0; k < tmp.size() && k < (size_t)qcap; ++k) queues[i * qcap + k] = unpack(tmp[k].second);
+    }
+  }
+  if (slots) {
+    std::vector<int4> sl(EMc * S);
+    std::vector<int2> slx(EMc * S);
+    IM_HIP(p, hipMemcpy(sl.data(), p->slots + em0 * S, sl.size() * sizeof(int4), hipMemcpyDeviceToHost));
+    IM_HIP(p, hipMemcpy(slx.data(), p->slot_ext + em0 * S, slx.size() * sizeof(int2), hipMemcpyDeviceToHost));
+    for (size_t i = 0; i < sl.size(); ++i) {
+      if (sl[i].x >= 0) slots[i] = unpack(slx[i]);
+      else std::memset(&slots[i], 0, sizeof(im_chain));
+    }
+  }
+  if (pending || pending_count) {
+    // the pending calls of the next tick: the buffer of parity t
+    std::vector<int32_t> pc(env_count);
+    std::vector<int4> pr((size_t)env_count * PM);
+    const size_t par = (size_t)(t & 1);
+    IM_HIP(p, hipMemcpy(pc.data(), p->pcnt + par * E + env_begin, pc.size() * 4, hipMemcpyDeviceToHost));
+    IM_HIP(p, hipMemcpy(pr.data(), p->pend + (par * E + env_begin) * PM, pr.size() * sizeof(int4),
+                        hipMemcpyDeviceToHost));
+    for (int e = 0; e < env_count; ++e) {
+      if (pending_count) pending_count[e] = pc[e];
+      if (!pending) continue;
+      for (int i = 0; i < PM; ++i) {
+        im_pending& o = pending[(size_t)e * PM + i];
+        if (i < pc[e]) {
+          const int4 v = pr[(size_t)e * PM + i];
+          o.ch = unpack(make_int2(v.x, v.y));
+          o.deadline = v.z;
+        } else {
+          std::memset(&o, 0, sizeof(o));
+        }
+      }
+    }
+  }
   return IM_OK;
 }
 

@@ -395,7 +395,10 @@ __device__ __forceinline__ void relu_to_frags(const f32x16& acc, u32x4& f0, u32x
 }
 
 template <int H, int NL, int AT>
-__global__ __launch_bounds__(256) void route_bf16(RouteArgs a) {
+__global__ __launch_bounds__(256) void route_bf16(RouteArgs a_in) {
+  // chain pools: the tick's row count is on the device
+  RouteArgs a = a_in;
+  if (a_in.n_total_dev) a.n_total = *a_in.n_total_dev;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n = lane & 31, g = lane >> 5;
   const int32_t row0 = (int32_t)(blockIdx.x * 4 + wave) * 32;
@@ -461,7 +464,10 @@ __global__ __launch_bounds__(256) void route_bf16(RouteArgs a) {
 }
 
 template <int H, int NL, int AT>
-__global__ __launch_bounds__(256) void route_f32(RouteArgs a) {
+__global__ __launch_bounds__(256) void route_f32(RouteArgs a_in) {
+  // chain pools: the tick's row count is on the device
+  RouteArgs a = a_in;
+  if (a_in.n_total_dev) a.n_total = *a_in.n_total_dev;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n = lane & 31, g = lane >> 5;
   const int32_t row0 = (int32_t)(blockIdx.x * 4 + wave) * 32;
@@ -577,7 +583,10 @@ __device__ __forceinline__ void copy_to_lds(u32x4* dst, const u32x4* src) {
 }
 
 template <int H, int NL, int AT, int KB1, bool W1L, int NW, int ED, int NR, int RL>
-__global__ __launch_bounds__(NW * 64, 1) void route_bf16_lds(RouteArgs a) {
+__global__ __launch_bounds__(NW * 64, 1) void route_bf16_lds(RouteArgs a_in) {
+  // chain pools: the tick's row count is on the device
+  RouteArgs a = a_in;
+  if (a_in.n_total_dev) a.n_total = *a_in.n_total_dev;
   constexpr int TH = H / 32;
   constexpr int KH = H / 16;
   constexpr int N_W1 = TH * KB1 * 64;
@@ -726,7 +735,10 @@ __device__ __forceinline__ void dma_frag(u32x4* dst, const u32x4* src, int lane)
 }
 
 template <int H, int AT, int KB1, int ED, int NW, int RL>
-__global__ __launch_bounds__(NW * 64, 1) void route_bf16_stream(RouteArgs a) {
+__global__ __launch_bounds__(NW * 64, 1) void route_bf16_stream(RouteArgs a_in) {
+  // chain pools: the tick's row count is on the device
+  RouteArgs a = a_in;
+  if (a_in.n_total_dev) a.n_total = *a_in.n_total_dev;
   constexpr int TH = H / 32, KH = H / 16;
   constexpr int S1 = TH / 2;                  // layer-1 stages (two output tiles each)
   constexpr int NST = S1 + TH;                // stages per block step
@@ -941,7 +953,10 @@ __device__ __forceinline__ void load_group(const RouteArgs& a, const RowCtx& c, 
 constexpr int kDualPrefetch = 1;
 
 template <int ED, int NW, int NR, int RL>
-__global__ __launch_bounds__(NW * 64, 1) void route_dual_bf16(RouteArgs a) {
+__global__ __launch_bounds__(NW * 64, 1) void route_dual_bf16(RouteArgs a_in) {
+  // chain pools: the tick's row count is on the device
+  RouteArgs a = a_in;
+  if (a_in.n_total_dev) a.n_total = *a_in.n_total_dev;
   static_assert(ED % 64 == 0, "embedding width must be a multiple of 64");
   constexpr int KBQ = ED / 16;          // K steps of the query half
   constexpr int NG = ED / 64;           // 64-element groups

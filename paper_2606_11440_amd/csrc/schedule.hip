@@ -45,7 +45,7 @@ __device__ __forceinline__ int32_t comp_id(int64_t c) { return (int32_t)(uint32_
 // (arrival order), so the arrival tick never has to travel with the entry
 // through a sort network.
 __device__ __forceinline__ int32_t t_arr_of(int32_t key, int32_t svcbud, int key_mode) {
-  const uint32_t svc = (uint32_t)svcbud & 0xffffu, bud = (uint32_t)svcbud >> 16;
+  const uint32_t svc = (uint32_t)svcbud & 0xffffu, bud = (uint32_t)(svcbud >> 16);   // budget signed
   const uint32_t k = (uint32_t)key;
   return (int32_t)(key_mode == IM_KEY_DEADLINE ? k - bud : (key_mode == IM_KEY_FCFS ? k : k - bud + svc));
 }
@@ -61,35 +61,58 @@ struct Queue {       // wave-uniform view of one (env, model) record
 // q.fn), all of them below the front's largest key or the pool empty. `seg`
 // is the model's sorted segment of a staged chunk in LDS (entries (key, id,
 // svc | budget << 16, model)). Only the key and the packed service/budget word
-// pass through the network; arrival ticks are recovered from them. The front followed
+// (and, with CHAIN, the two chain words: `fx`, `segx`, `pool_ext`) pass
+// through the network; arrival ticks are recovered from them. The front followed
 // by the reversed newcomers is a bitonic sequence of 128; its half-cleaner
 // leaves the 64 smallest in `lo` (bitonic, sorted by one merge network) and
 // the rest in `hi`, whose real entries spill to the pool.
-__device__ __forceinline__ void merge_front(Queue& q, int4& fe, const int4* seg, int lim,
-                                            int key_mode, int4* pool) {
+template <bool CHAIN>
+__device__ __forceinline__ void merge_front(Queue& q, int4& fe, int2& fx, const int4* seg,
+                                            const int2* segx, int lim, int key_mode, int4* pool,
+                                            int2* pool_ext) {
+  constexpr int NP = CHAIN ? 3 : 1;
   const int lane = lane_id();
   const int r = 63 - lane;
   int64_t kb = kKeyMax;
-  int32_t pb = 0;
+  int32_t pb[NP];
+#pragma unroll
+  for (int i = 0; i < NP; ++i) pb[i] = 0;
   if (r < lim) {
     const int4 v = seg[r];
     kb = composite(v.x, v.y);
-    pb = v.z;
+    pb[0] = v.z;
+    if constexpr (CHAIN) {
+      const int2 x = segx[r];
+      pb[1] = x.x;
+      pb[2] = x.y;
+    }
   }
   const int64_t ka = lane < q.fn ? composite(fe.x, fe.y) : kKeyMax;
+  int32_t pa[NP];
+  pa[0] = fe.w;
+  if constexpr (CHAIN) {
+    pa[1] = fx.x;
+    pa[2] = fx.y;
+  }
   const bool sw = kb < ka;
   int64_t klo = sw ? kb : ka;
   const int64_t khi = sw ? ka : kb;
-  int32_t plo[1] = {sw ? pb : fe.w};
-  const int32_t phi = sw ? fe.w : pb;
-  bitonic_merge64<1>(klo, plo);
+  int32_t plo[NP], phi[NP];
+#pragma unroll
+  for (int i = 0; i < NP; ++i) {
+    plo[i] = sw ? pb[i] : pa[i];
+    phi[i] = sw ? pa[i] : pb[i];
+  }
+  bitonic_merge64<NP>(klo, plo);
   const int total = q.fn + lim;
   const int keep = total < kFront ? total : kFront;
   const bool spill = khi != kKeyMax;
   const uint64_t sm = ballot(spill);
   if (spill) {
     const int32_t kk = comp_key(khi);
-    pool[q.P + prefix_count(sm)] = make_int4(kk, comp_id(khi), t_arr_of(kk, phi, key_mode), phi);
+    const int pos = q.P + prefix_count(sm);
+    pool[pos] = make_int4(kk, comp_id(khi), t_arr_of(kk, phi[0], key_mode), phi[0]);
+    if constexpr (CHAIN) pool_ext[pos] = make_int2(phi[1], phi[2]);
   }
   q.P += total - keep;
   q.fh = 0;
@@ -97,26 +120,41 @@ __device__ __forceinline__ void merge_front(Queue& q, int4& fe, const int4* seg,
   const int32_t kl = comp_key(klo);
   fe = lane < keep ? make_int4(kl, comp_id(klo), t_arr_of(kl, plo[0], key_mode), plo[0])
                    : make_int4(0, 0, 0, 0);
+  if constexpr (CHAIN) fx = lane < keep ? make_int2(plo[1], plo[2]) : make_int2(0, 0);
 }
 
 // Refill the (empty) front with the min(64, P) smallest pool entries; the new
 // front is returned in `fe` (lane i: entry i), the front array is not written.
 // `pk`/`pi` are this wave's LDS staging rows (64 keys, 64 pool indices), `kb`
 // its LDS buffer for 4 chunks of pool keys.
-__device__ void refill(Queue& q, int4& fe, int4* pool, int64_t* pk, int32_t* pi, int2* kb,
-                       int key_mode) {
+// With CHAIN the chain words move along: `fx`, `pool_ext`.
+template <bool CHAIN>
+__device__ void refill(Queue& q, int4& fe, int2& fx, int4* pool, int2* pool_ext, int64_t* pk,
+                       int32_t* pi, int2* kb, int key_mode) {
   const int lane = lane_id();
   const int P = q.P;
   wave_mem_sync();   // this tick's pool appends are read below
   if (P <= kFront) {
+    constexpr int NP = CHAIN ? 3 : 1;
     int4 e = make_int4(0, 0, 0, 0);
+    int2 x = make_int2(0, 0);
     int64_t ck = kKeyMax;
-    if (lane < P) { e = pool[lane]; ck = composite(e.x, e.y); }
-    int32_t pay[1] = {e.w};
-    bitonic_sort64<1>(ck, pay);
+    if (lane < P) {
+      e = pool[lane];
+      ck = composite(e.x, e.y);
+      if constexpr (CHAIN) x = pool_ext[lane];
+    }
+    int32_t pay[NP];
+    pay[0] = e.w;
+    if constexpr (CHAIN) {
+      pay[1] = x.x;
+      pay[2] = x.y;
+    }
+    bitonic_sort64<NP>(ck, pay);
     const int32_t kk = comp_key(ck);
     fe = lane < P ? make_int4(kk, comp_id(ck), t_arr_of(kk, pay[0], key_mode), pay[0])
                   : make_int4(0, 0, 0, 0);
+    if constexpr (CHAIN) fx = lane < P ? make_int2(pay[1], pay[2]) : make_int2(0, 0);
     q.fh = 0;
     q.fn = P;
     q.P = 0;
@@ -177,6 +215,7 @@ __device__ void refill(Queue& q, int4& fe, int4* pool, int64_t* pk, int32_t* pi,
   if (np > 0) flush();
   const int sel = idx[0];
   fe = pool[sel];
+  if constexpr (CHAIN) fx = pool_ext[sel];
   // Compact the pool: selected entries below the new size are holes, filled
   // with the unselected entries of the last 64 positions (same count).
   const int Pn = P - kFront;
@@ -184,12 +223,17 @@ __device__ void refill(Queue& q, int4& fe, int4* pool, int64_t* pk, int32_t* pi,
   const uint64_t fillers = ~tail_sel;
   const uint64_t holes = ballot(sel < Pn);
   int4 fill = make_int4(0, 0, 0, 0);
+  int2 fillx = make_int2(0, 0);
   if (sel < Pn) {
     const int f = nth_set_bit(fillers, prefix_count(holes));
     fill = pool[Pn + f];
+    if constexpr (CHAIN) fillx = pool_ext[Pn + f];
   }
   wave_mem_sync();
-  if (sel < Pn) pool[sel] = fill;
+  if (sel < Pn) {
+    pool[sel] = fill;
+    if constexpr (CHAIN) pool_ext[sel] = fillx;
+  }
   q.fh = 0;
   q.fn = kFront;
   q.P = Pn;
@@ -258,6 +302,7 @@ __device__ __forceinline__ int32_t rl(int32_t v, int m) { return __builtin_amdgc
 struct ModelIn {
   int4 front;
   int4 slot;
+  int2 fx, sx;   // chain words of the front entry and the slot (chain pools)
 };
 
 // Adds v to a 64-bit counter without reading it back (a vector atomic whose
@@ -280,9 +325,15 @@ __device__ __forceinline__ void counter_add(int64_t* p, int64_t v) {
 // (no read-modify-write round trips).
 // RPM: the pool has (or had) a rate-limited model, so the blackbox dispatch
 // windows are tracked; pools that never had one run without that code.
-template <bool RPM>
+// CHAIN: multi-step chains (Sec. 4.3). The env's rows are its pending calls
+// (spawned at the previous tick, in spawn order) then its arrivals; every
+// call carries its query's two chain words through the queue, and a
+// completion that is not its query's last call appends the next call, with
+// the query's deadline, to the pending list of the next tick.
+template <bool RPM, bool CHAIN>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void schedule_kernel(SchedArgs a) {
   __shared__ int4 stage[4][kStageChunks * 64];
+  __shared__ int2 stage_x[4][CHAIN ? kStageChunks * 64 : 1];
   __shared__ int32_t hist_lds[4][IM_MAX_ACTIONS];
   __shared__ int32_t svc_lds[4][IM_MAX_MODELS];
   __shared__ int32_t acc_lds[4][IM_MAX_MODELS];
@@ -317,51 +368,90 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
   const int32_t lo = a.offsets[e], hi = a.offsets[e + 1];
   int32_t bad = 0;
   if (lo < 0 || hi < lo || hi > a.n_total || hi - lo > a.max_arrivals) bad = IM_ERR_COUNT;
-  const int32_t n = bad ? 0 : hi - lo;
+  // The tick and the next request id live in the env's first record in
+  // device memory, so a captured sequence of ticks replays with the right time.
+  const int32_t next_id = rl(r2.y, 0);
+  const int32_t t = rl(r2.z, 0);
+  // chain pools: this tick's pending calls (buffer of parity t) and the next
+  // tick's (parity t + 1); the rows' outputs start at roff[e]
+  const int4* pend_cur = nullptr;
+  int4* pend_nxt = nullptr;
+  int32_t pc = 0, abase = lo;
+  if constexpr (CHAIN) {
+    const size_t E = (size_t)a.E;
+    pend_cur = a.pend + ((size_t)(t & 1) * E + e) * a.pend_cap;
+    pend_nxt = a.pend + ((size_t)((t + 1) & 1) * E + e) * a.pend_cap;
+    pc = a.pcnt[(size_t)(t & 1) * E + e];
+    abase = a.roff[e];
+  }
+  const int32_t n = bad ? 0 : hi - lo;   // arrivals
+  const int32_t nrows = pc + n;          // rows: pending calls, then arrivals
 
-  // ---- the env's arrivals: loaded once, validated; the first chunks kept ----
+  // ---- the env's rows: loaded once, validated; the first chunks kept ----
   constexpr int kKeep = 2;                            // chunks kept in registers
   int32_t c_ac[kKeep], c_bs[kKeep];                   // action; budget << 16 | base_svc (16 bits each)
+  int32_t c_xa[kKeep], c_xb[kKeep];                   // chain words (chain pools)
 #pragma unroll
   for (int c = 0; c < kKeep; ++c) {
     c_ac[c] = -1;
     c_bs[c] = 0;
+    c_xa[c] = 0;
+    c_xb[c] = 0;
   }
   int32_t berr = 0;
-  auto check = [&](int32_t i, int32_t& ac, int32_t& bs) {
+  // row r of the env: a pending call (r < pc, valid by construction; its
+  // budget is what is left of its query's) or arrival lo + r - pc
+  auto load_row = [&](int32_t r, int32_t& ac, int32_t& bs, int32_t& xa, int32_t& xb) {
+    ac = a.actions[abase + r];
+    if (ac < -1 || ac >= a.A) berr |= IM_ERR_ACTION;
+    if (CHAIN && r < pc) {
+      const int4 pr = pend_cur[r];
+      const int32_t bu = remaining_budget(pr.z, t);
+      xa = pr.x;
+      xb = pr.y;
+      bs = (int32_t)(((uint32_t)bu << 16) | ((uint32_t)chain_base(pr.y) & 0xffffu));
+      return;
+    }
+    const int32_t i = lo + (r - pc);
     const int32_t qi = a.q_idx[i];
     const int32_t bu = a.budget[i];
     const int32_t sv = a.base_svc[i];
-    ac = a.actions[i];
+    int32_t ro = 0;
     if (qi < 0 || (int64_t)qi >= a.Q) berr |= IM_ERR_QIDX;
     if (a.role) {
-      const int32_t ro = a.role[i];
+      ro = a.role[i];
       if (ro < 0 || ro >= a.n_roles) berr |= IM_ERR_ROLE;
     }
     if (bu < 1) berr |= IM_ERR_BUDGET;
     if (sv < 1 || sv > IM_SVC_MAX) berr |= IM_ERR_SVC;
-    if (ac < -1 || ac >= a.A) berr |= IM_ERR_ACTION;
+    if (CHAIN) {
+      const int32_t ns = a.n_steps[i];
+      if (ns < 1 || ns > a.max_steps) berr |= IM_ERR_STEPS;
+      xa = chain_a(qi, 0, ns);
+      xb = chain_b(sv, bu, ro);
+    }
     bs = (int32_t)(((uint32_t)bu << 16) | ((uint32_t)sv & 0xffffu));
   };
 #pragma unroll
   for (int c = 0; c < kKeep; ++c) {
-    if (c * 64 < n) {
-      const int32_t i = lo + c * 64 + lane;
-      if (i < hi) check(i, c_ac[c], c_bs[c]);
+    if (c * 64 < nrows) {
+      const int32_t r = c * 64 + lane;
+      if (r < nrows) load_row(r, c_ac[c], c_bs[c], c_xa[c], c_xb[c]);
     }
   }
-  for (int32_t base = lo + kKeep * 64; base < lo + n; base += 64) {
-    const int32_t i = base + lane;
-    int32_t ac, bs;
-    if (i < hi) check(i, ac, bs);
+  for (int32_t base = kKeep * 64; base < nrows; base += 64) {
+    const int32_t r = base + lane;
+    int32_t ac, bs, xa, xb;
+    if (r < nrows) load_row(r, ac, bs, xa, xb);
   }
-  if (n > 0) {
+  if (nrows > 0) {
     // wave-wide OR of the error bits, one ballot each
     if (ballot(berr & IM_ERR_QIDX)) bad |= IM_ERR_QIDX;
     if (ballot(berr & IM_ERR_BUDGET)) bad |= IM_ERR_BUDGET;
     if (ballot(berr & IM_ERR_SVC)) bad |= IM_ERR_SVC;
     if (ballot(berr & IM_ERR_ACTION)) bad |= IM_ERR_ACTION;
     if (a.role && ballot(berr & IM_ERR_ROLE)) bad |= IM_ERR_ROLE;
+    if (CHAIN && ballot(berr & IM_ERR_STEPS)) bad |= IM_ERR_STEPS;
   }
 
   LaneState L;
@@ -376,10 +466,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
   int32_t* rpm_s = rpm_lds[wv];
   float* inv_rpm_s = inv_rpm_lds[wv];
   if (RPM && lane < M) { rpm_s[lane] = r3.y; inv_rpm_s[lane] = __int_as_float(r3.w); }
-  // The tick and the next request id live in the env's first record in
-  // device memory, so a captured sequence of ticks replays with the right time.
-  const int32_t next_id = rl(r2.y, 0);
-  const int32_t t = rl(r2.z, 0);
   // lane m: which parts of model m's record changed (bit 0: load statistics,
   // 1: front window, 2: pool size or busy slots, 3: next completion tick)
   int32_t chg = 0;
@@ -402,6 +488,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
       }
     }
     if (lane < M && L.busy_mask != 0) recs[lane].next_done = L.next_done + 1;
+    if constexpr (CHAIN) {
+      // the env's pending calls stay pending
+      for (int i = lane; i < pc; i += 64) pend_nxt[i] = pend_cur[i];
+      if (lane == 0) a.pcnt[(size_t)((t + 1) & 1) * a.E + e] = pc;
+    }
     // a tracked window still slides: the dispatches of tick t - 60 leave it
     if (RPM && lane < M && (rpm_l > 0 || L.rcnt > 0)) {
       uint8_t* rb = a.rpm_ring + ((size_t)e * M + lane) * kRpmRing + (t % kRpmWindow);
@@ -422,7 +513,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
   int32_t prior_l = 0;      // lane m: requests routed to model m so far (id order)
   int32_t acc_l = 0;        // lane m: requests accepted by model m so far
   int32_t nomodel = 0;
-  const int n_chunks = (n + 63) / 64;
+  const int n_chunks = (nrows + 63) / 64;
+  int32_t pn = 0;            // pending calls spawned for the next tick
+  int32_t q_done = 0, q_met = 0;
+  int2* stx = stage_x[wv];
   const int rounds = n_chunks > 0 ? (n_chunks + kStageChunks - 1) / kStageChunks : 1;
 
   for (int r = 0; r < rounds; ++r) {
@@ -432,14 +526,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
 #pragma unroll
     for (int c = 0; c < kStageChunks; ++c) {
       if (c >= nch) break;
-      const int32_t base = lo + (c0 + c) * 64;
-      const int32_t i = base + lane;
-      const bool in = i < hi;
+      const int32_t base = (c0 + c) * 64;
+      const int32_t i = base + lane;   // row of the env
+      const bool in = i < nrows;
       int32_t ac = c < kKeep ? c_ac[c < kKeep ? c : 0] : -1;
       int32_t bs = c < kKeep ? c_bs[c < kKeep ? c : 0] : 0;
+      int32_t xa = c < kKeep ? c_xa[c < kKeep ? c : 0] : 0;
+      int32_t xb = c < kKeep ? c_xb[c < kKeep ? c : 0] : 0;
       if (r != 0 || c >= kKeep) {
-        ac = in ? a.actions[i] : -1;
-        bs = in ? (int32_t)(((uint32_t)a.budget[i] << 16) | ((uint32_t)a.base_svc[i] & 0xffffu)) : 0;
+        ac = -1;
+        bs = 0;
+        if (in) load_row(i, ac, bs, xa, xb);
       }
       const int32_t bu = bs >> 16, sv = bs & 0xffff;
       const int32_t mdl = ac >= 0 ? ac / K : -1;
@@ -462,19 +559,21 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         atomicAdd(&svc_s[mdl], svc);
       }
       // Sort key (32 bits): model (63 for rows not admitted) | key - t biased by
-      // 2^16 | lane. Every row of the chunk arrives at t, so ordering by key - t
-      // is ordering by key; with budget in [1, 32767] and svc in [1, 65520],
-      // key - t lies in [-65519, 32766] (17 bits once biased). The lane keeps
-      // ties in id order and locates the row's packed service/budget word.
+      // 2^17 | lane. Every row of the chunk enters at t, so ordering by key - t
+      // is ordering by key; with budget in [-32768, 32767] (a later call of a
+      // chain may be past its deadline) and svc in [1, 65520], key - t lies in
+      // [-98288, 32767] (18 bits once biased). The lane keeps ties in id order
+      // and locates the row's packed service/budget word.
       const int32_t rk = a.key_mode == IM_KEY_DEADLINE ? bu : (a.key_mode == IM_KEY_FCFS ? 0 : bu - svc);
-      uint32_t sk = ((uint32_t)(acc ? mdl : 63) << 23) | (((uint32_t)(rk + 65536) & 0x1ffffu) << 6) |
+      uint32_t sk = ((uint32_t)(acc ? mdl : 63) << 24) | (((uint32_t)(rk + 131072) & 0x3ffffu) << 6) |
                     (uint32_t)lane;
-      const int32_t pay = (int32_t)((uint32_t)svc | ((uint32_t)bu << 16));
+      const int32_t pay = (int32_t)(((uint32_t)svc & 0xffffu) | ((uint32_t)bu << 16));
       bitonic_sort64(sk);
       const int src = (int)(sk & 63u);
-      const int32_t skey = t + (int32_t)((sk >> 6) & 0x1ffffu) - 65536;
-      const int32_t sid = next_id + (base - lo) + src;
-      st[c * 64 + lane] = make_int4(skey, sid, shfl(pay, src), (int32_t)(sk >> 23));
+      const int32_t skey = t + (int32_t)((sk >> 6) & 0x3ffffu) - 131072;
+      const int32_t sid = next_id + base + src;
+      st[c * 64 + lane] = make_int4(skey, sid, shfl(pay, src), (int32_t)(sk >> 24));
+      if constexpr (CHAIN) stx[c * 64 + lane] = make_int2(shfl(xa, src), shfl(xb, src));
     }
     const bool last = r == rounds - 1;
 
@@ -500,12 +599,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
       const size_t em = (size_t)e * M + mm;
       in.front = make_int4(0, 0, 0, 0);
       in.slot = make_int4(-1, 0, 0, 0);
+      in.fx = make_int2(0, 0);
+      in.sx = make_int2(0, 0);
       if ((need_front >> mm) & 1ull) {
         const int fh = rl(L.fh, mm), fn = rl(L.fn, mm);
-        if (lane < fn) in.front = a.front[em * kFront + fh + lane];   // fh + fn <= kFront
+        if (lane < fn) {
+          in.front = a.front[em * kFront + fh + lane];   // fh + fn <= kFront
+          if constexpr (CHAIN) in.fx = a.front_ext[em * kFront + fh + lane];
+        }
       }
       if ((need_slots >> mm) & 1ull) {
-        if (lane < S) in.slot = a.slots[em * S + lane];
+        if (lane < S) {
+          in.slot = a.slots[em * S + lane];
+          if constexpr (CHAIN) in.sx = a.slot_ext[em * S + lane];
+        }
       }
     };
     if (r > 0) wave_mem_sync();   // the fronts written in the previous round
@@ -528,9 +635,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
       q.busy_mask = rl(L.busy_mask, m); q.next_done = rl(L.next_done, m);
       int4* front = a.front + em * kFront;
       int4* pool = a.pool + em * a.qcap;
+      int2* front_x = CHAIN ? a.front_ext + em * kFront : nullptr;
+      int2* pool_x = CHAIN ? a.pool_ext + em * a.qcap : nullptr;
       const int32_t k_tot = rl(acc_round_l, m);   // newcomers admitted this round
       const int32_t svc_in = rl(svc_round_l, m);
       int4 fe = cur.front;                         // lane i mirrors front[fe_base + i]
+      int2 fx = cur.fx;                            // its chain words (chain pools)
       int fe_base = q.fh;
       bool dirty = false;   // the front in registers differs from the front array
       if (k_tot > 0) {
@@ -553,10 +663,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
             const int64_t fmax = readlane64(composite(fe.x, fe.y), q.fn - 1);
             lim = popc64(ballot(mine && composite(en.x, en.y) < fmax));
           }
-          if (mine && o >= lim) pool[q.P + o - lim] = make_int4(en.x, en.y, t, en.z);
+          if (mine && o >= lim) {
+            pool[q.P + o - lim] = make_int4(en.x, en.y, t, en.z);
+            if constexpr (CHAIN) pool_x[q.P + o - lim] = stx[c * 64 + lane];
+          }
           q.P += k - lim;
           if (lim > 0) {
-            merge_front(q, fe, st + c * 64 + seg_lo, lim, a.key_mode, pool);
+            merge_front<CHAIN>(q, fe, fx, st + c * 64 + seg_lo, stx + c * 64 + seg_lo, lim, a.key_mode,
+                               pool, pool_x);
             fe_base = 0;
             dirty = true;
           }
@@ -566,8 +680,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         if (lane == m) acc_l += k_tot;
       }
       if (!last) {
-        if (dirty && lane >= q.fh - fe_base && lane < q.fh - fe_base + q.fn)
+        if (dirty && lane >= q.fh - fe_base && lane < q.fh - fe_base + q.fn) {
           front[fe_base + lane] = fe;   // the live window [fh, fh + fn)
+          if constexpr (CHAIN) front_x[fe_base + lane] = fx;
+        }
         if (lane == m) {
           chg |= (q.qlen != L.qlen || q.backlog != L.backlog ? 1 : 0) | (q.fh != L.fh || q.fn != L.fn ? 2 : 0) |
                  (q.P != L.P ? 4 : 0);
@@ -600,11 +716,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
       if (pops || due) {
         // slot: {id, t_arr, tick of completion, budget}; id -1 = empty
         int4 sl = cur.slot;
+        int2 sx = cur.sx;
         if (pops) {
           uint64_t empty = (uint64_t)free_m;
           while (empty != 0 && q.qlen > 0 && started < allowed) {
             if (q.fn == 0) {
-              refill(q, fe, pool, pend_k[wv], pend_i[wv], pend_kb[wv], a.key_mode);
+              refill<CHAIN>(q, fe, fx, pool, pool_x, pend_k[wv], pend_i[wv], pend_kb[wv], a.key_mode);
               fe_base = 0;
               dirty = true;
             }
@@ -621,7 +738,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
             en.z = shfl((int32_t)fe.z, src);
             en.w = shfl((int32_t)fe.w, src);
             const int32_t svc = en.w & 0xffff;
-            if (mine_slot) sl = make_int4(en.y, en.z, t + svc - 1, (int32_t)((uint32_t)en.w >> 16));
+            if (mine_slot) sl = make_int4(en.y, en.z, t + svc - 1, en.w >> 16);   // budget signed
+            if constexpr (CHAIN) {
+              const int32_t xa = shfl(fx.x, src), xb = shfl(fx.y, src);
+              if (mine_slot) sx = make_int2(xa, xb);
+            }
             uint64_t popped = ballot(mine_slot);
             empty &= ~popped;
             while (popped) {                       // at most max_slots lanes
@@ -659,7 +780,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
           // per completed slot lane at once; 32 bits while latency < 2^16
           uint64_t cq = 0;
           if (done) {
-            const uint32_t bud = (uint32_t)sl.w;
+            // beta: the query's budget (chains; the call's own for single steps)
+            const uint32_t bud = CHAIN ? (uint32_t)chain_beta(sx.y) : (uint32_t)sl.w;
             cq = lat < 65536 ? (uint64_t)(((uint32_t)lat << 16) / bud)
                              : ((uint64_t)(uint32_t)lat << 16) / bud;
           }
@@ -670,6 +792,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
           cost_add = readlane64(cs, 0);
         }
         slo_add = popc64(ballot(done && lat <= sl.w));
+        if constexpr (CHAIN) {
+          // call k + 1 of the query, for the next tick, with the query's deadline
+          const bool more = done && chain_k(sx.x) + 1 < chain_n(sx.x);
+          const uint64_t spawn = ballot(more);
+          if (more) pend_nxt[pn + prefix_count(spawn)] = make_int4(sx.x + (1 << 24), sx.y, sl.y + sl.w, 0);
+          pn += popc64(spawn);
+          const bool fin = done && !more;
+          q_done += popc64(ballot(fin));
+          q_met += popc64(ballot(fin && lat <= sl.w));
+        }
         if (done) sl = make_int4(-1, 0, 0, 0);
         const uint64_t bm = ballot(lane < S && sl.x >= 0);
         q.busy = popc64(bm);
@@ -681,12 +813,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         nd = min(nd, xshfl<2>(nd));
         nd = min(nd, xshfl<4>(nd));
         q.next_done = rl(nd, 0);
-        if (lane < S) a.slots[em * S + lane] = sl;
+        if (lane < S) {
+          a.slots[em * S + lane] = sl;
+          if constexpr (CHAIN) a.slot_ext[em * S + lane] = sx;
+        }
       }
 
       // ---- write back what changed ----
-      if (dirty && lane >= q.fh - fe_base && lane < q.fh - fe_base + q.fn)
+      if (dirty && lane >= q.fh - fe_base && lane < q.fh - fe_base + q.fn) {
         front[fe_base + lane] = fe;   // the live window [fh, fh + fn)
+        if constexpr (CHAIN) front_x[fe_base + lane] = fx;
+      }
       const int32_t rec = rpm > 0 ? started : 0;   // this tick's recorded dispatches
       const int32_t rcnt_new = window + rec;
       if (track && lane == 0 && rec != rold) a.rpm_ring[em * kRpmRing + (t % kRpmWindow)] = (uint8_t)rec;
@@ -725,7 +862,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     if (chg & 1) rp[0] = make_int4(L.qlen, L.busy, L.ewma, L.backlog);
     if (chg & 2) rp[1] = make_int4(cap_s[lane], en_s[lane], L.fh, L.fn);
     if (lane == 0) {
-      rp[2] = make_int4(L.P, next_id + n, t + 1, L.busy_mask);
+      rp[2] = make_int4(L.P, next_id + nrows, t + 1, L.busy_mask);
     } else if (chg & 4) {
       recs[lane].P = L.P;
       recs[lane].busy_mask = L.busy_mask;
@@ -764,25 +901,37 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
       vb8[lane] = (en_s[lane] != 0 && cap_s[lane] > 0 && L.qlen < a.qcap) ? 1 : 0;
     }
   }
-  if (n > 0) {
+  int64_t* envc_p = a.env_cnt + (size_t)e * kEnvCnt;
+  if (nrows > 0) {
     int64_t* hist_p = a.hist + (size_t)e * a.A;
-    int64_t* envc_p = a.env_cnt + (size_t)e * 2;
-    if (lane < 2) counter_add(envc_p + lane, lane == 0 ? n : nomodel);
+    if (lane < 2) counter_add(envc_p + lane, lane == 0 ? nrows : nomodel);
     if (lane < a.A) {
       const int32_t h = hist_s[lane];
       if (h != 0) counter_add(hist_p + lane, h);
     }
   }
+  if constexpr (CHAIN) {
+    if (lane == 0) a.pcnt[(size_t)((t + 1) & 1) * a.E + e] = pn;
+    if (lane == 0 && q_done != 0) counter_add(envc_p + E_Q_DONE, q_done);
+    if (lane == 0 && q_met != 0) counter_add(envc_p + E_Q_MET, q_met);
+  }
 }
 
 // Dual update, step 1: exact int64 sums of completions and Q16 cost over every
 // (env, model) counter row (order-independent: integer atomics).
-__global__ void dual_reduce_kernel(const int64_t* cnt, int64_t n_em, unsigned long long* acc) {
+// Chain pools count completed queries (env_cnt) instead of completed calls.
+__global__ void dual_reduce_kernel(const int64_t* cnt, int64_t n_em, const int64_t* env_cnt,
+                                   int64_t n_env, unsigned long long* acc) {
   uint64_t n = 0, c = 0;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_em;
        i += (int64_t)gridDim.x * blockDim.x) {
-    n += (uint64_t)cnt[i * C_NUM + C_COMPLETED];
+    if (!env_cnt) n += (uint64_t)cnt[i * C_NUM + C_COMPLETED];
     c += (uint64_t)cnt[i * C_NUM + C_COST_Q16];
+  }
+  if (env_cnt) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_env;
+         i += (int64_t)gridDim.x * blockDim.x)
+      n += (uint64_t)env_cnt[i * kEnvCnt + E_Q_DONE];
   }
 #pragma unroll
   for (int m = 32; m >= 1; m >>= 1) {
@@ -820,11 +969,12 @@ __global__ void dual_finish_kernel(unsigned long long* acc, int64_t* last, doubl
 
 }  // namespace
 
-hipError_t launch_dual_update(const int64_t* cnt, int64_t n_em, unsigned long long* acc, int64_t* last,
-                              double eta, double lambda_max, double* lambda, hipStream_t s) {
+hipError_t launch_dual_update(const int64_t* cnt, int64_t n_em, const int64_t* env_cnt, int64_t n_env,
+                              unsigned long long* acc, int64_t* last, double eta, double lambda_max,
+                              double* lambda, hipStream_t s) {
   const int64_t want = (n_em + 255) / 256;
   const unsigned blocks = (unsigned)(want < 1024 ? (want < 1 ? 1 : want) : 1024);
-  hipLaunchKernelGGL(dual_reduce_kernel, dim3(blocks), dim3(256), 0, s, cnt, n_em, acc);
+  hipLaunchKernelGGL(dual_reduce_kernel, dim3(blocks), dim3(256), 0, s, cnt, n_em, env_cnt, n_env, acc);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(dual_finish_kernel, dim3(1), dim3(1), 0, s, acc, last, eta, lambda_max, lambda);
@@ -838,11 +988,16 @@ hipError_t launch_snapshot(const SchedArgs& a, int e0, int ne, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_schedule(const SchedArgs& a, bool rpm, hipStream_t s) {
+hipError_t launch_schedule(const SchedArgs& a, bool rpm, bool chain, hipStream_t s) {
   const int64_t waves = (int64_t)a.E;
   const unsigned blocks = (unsigned)((waves + 3) / 4);
-  if (rpm) hipLaunchKernelGGL(schedule_kernel<true>, dim3(blocks), dim3(256), 0, s, a);
-  else hipLaunchKernelGGL(schedule_kernel<false>, dim3(blocks), dim3(256), 0, s, a);
+  if (chain) {
+    if (rpm) hipLaunchKernelGGL((schedule_kernel<true, true>), dim3(blocks), dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((schedule_kernel<false, true>), dim3(blocks), dim3(256), 0, s, a);
+  } else {
+    if (rpm) hipLaunchKernelGGL((schedule_kernel<true, false>), dim3(blocks), dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((schedule_kernel<false, false>), dim3(blocks), dim3(256), 0, s, a);
+  }
   return hipGetLastError();
 }
 

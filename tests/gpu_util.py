@@ -53,6 +53,7 @@ class Pair:
                                  E=self.e1 - self.e0, threads=threads,
                                  roles=b if cfg.get("net") == "dual" else None)
         self.counts = workload.gen.counts(cfg, seed)
+        self.chains = cfg.get("max_steps", 1) > 1
         self.flips = 0
         self.rows_checked = 0
         self.P = P
@@ -61,33 +62,50 @@ class Pair:
     def arrivals(self, t):
         return workload.gen.tick(self.cfg, self.seed, t, self.counts[t], self.Q)
 
+    def _rows(self, arr):
+        """Capacity of the per-row outputs of a tick (chain pools: the pending
+        calls come on top of the arrivals)."""
+        n = int(arr["q_idx"].size)
+        if self.chains:
+            n += self.cfg["E"] * self.cfg["M"] * self.cfg["max_slots"]
+        return max(n, 1)
+
+    def _span(self, arr, sub):
+        """GPU rows of envs [e0, e1) after a route: (first row, row count)."""
+        if self.chains:
+            off, _ = self.gpu.rows()
+            return int(off[self.e0]), int(off[self.e1] - off[self.e0])
+        return int(arr["offsets"][self.e0]), int(sub["q_idx"].size)
+
     def step(self, arr, mode="route+schedule", check_logits=True):
         """One lockstep tick. mode: 'route+schedule' (im_route with logits,
         then im_schedule) or 'tick' (im_tick with actions_out)."""
         torch, P = self.torch, self.P
         cfg = self.cfg
         dev = P.device_arrivals(arr)
-        n = int(arr["q_idx"].size)
-        act = torch.full((max(n, 1),), -7, dtype=torch.int32, device="cuda")
+        n = self._rows(arr)
+        act = torch.full((n,), -7, dtype=torch.int32, device="cuda")
         sub = workload.gen.subset(arr, self.e0, self.e1)
-        lo = int(arr["offsets"][self.e0])
-        ns = int(sub["q_idx"].size)
         if mode == "tick":
             self.gpu.tick(dev, act)
             torch.cuda.synchronize()
+            lo, ns = self._span(arr, sub)
             g_act = act[lo:lo + ns].cpu().numpy() if ns else np.zeros(0, np.int32)
             o_act, o_lg = self.orc.route(sub)
+            assert o_act.size == ns, (o_act.size, ns)
             self._check_actions(g_act, o_act, o_lg, None)
         else:
-            lg = torch.full((max(n, 1), cfg["A"]), float("nan"), dtype=torch.float32, device="cuda")
+            lg = torch.full((n, cfg["A"]), float("nan"), dtype=torch.float32, device="cuda")
             self.gpu.route(dev, act, lg if check_logits else None)
             torch.cuda.synchronize()
+            lo, ns = self._span(arr, sub)
             g_act = act[lo:lo + ns].cpu().numpy() if ns else np.zeros(0, np.int32)
             g_lg = lg[lo:lo + ns].cpu().numpy().astype(np.float64) if ns else None
             o_act, o_lg = self.orc.route(sub)
+            assert o_act.size == ns, (o_act.size, ns)
             self._check_actions(g_act, o_act, o_lg, g_lg if check_logits else None)
             self.gpu.schedule(dev, act)
-        self.orc.schedule(sub, g_act)
+        self.orc.schedule(sub, g_act)   # chain pools: the same rows in the same order
         return g_act
 
     def step_rl(self, arr, seed, greedy=False):
@@ -102,8 +120,7 @@ class Pair:
         A = cfg["A"]
         vh = bool(cfg.get("value_head"))
         dev = P.device_arrivals(arr)
-        n = int(arr["q_idx"].size)
-        nn = max(n, 1)
+        nn = self._rows(arr)
         f32 = dict(dtype=torch.float32, device="cuda")
         act = torch.full((nn,), -7, dtype=torch.int32, device="cuda")
         logp = torch.full((nn,), float("nan"), **f32)
@@ -113,8 +130,7 @@ class Pair:
         self.gpu.route_sample(dev, seed, act, logp, ent, val, lg, greedy=greedy)
         torch.cuda.synchronize()
         sub = workload.gen.subset(arr, self.e0, self.e1)
-        lo = int(arr["offsets"][self.e0])
-        ns = int(sub["q_idx"].size)
+        lo, ns = self._span(arr, sub)
         sl = slice(lo, lo + ns)
         g_act = act[sl].cpu().numpy()
         g_lg = lg[sl].cpu().numpy().astype(np.float64)
@@ -128,7 +144,7 @@ class Pair:
             if not ok.all():
                 r = int(np.argmin(ok))
                 raise AssertionError(f"logits outside tolerance at row {r}")
-        off = sub["offsets"]
+        off = self.orc.row_offsets(sub)
         env_of = np.repeat(np.arange(self.e1 - self.e0), np.diff(off))
         for r in range(ns):
             z = o["logits"][r]
@@ -178,6 +194,20 @@ class Pair:
         g = self.gpu.state(self.e0, self.e1 - self.e0)
         o = self.orc.state()
         assert_state_equal(g, o, ctx=ctx)
+        if self.chains:
+            gc = self.gpu.chain_state(self.e0, self.e1 - self.e0)
+            oc = self.orc.chain_state()
+            np.testing.assert_array_equal(gc["pending_count"], oc["pending_count"], err_msg=ctx)
+            np.testing.assert_array_equal(gc["pending"], oc["pending"], err_msg=ctx)
+            np.testing.assert_array_equal(gc["slot_chain"], oc["slot_chain"], err_msg=ctx)
+            ql = np.asarray(g["qlen"])
+            for e in range(ql.shape[0]):
+                for m in range(ql.shape[1]):
+                    n = int(ql[e, m])
+                    np.testing.assert_array_equal(gc["queue_chain"][e, m, :n], oc["queue_chain"][e, m, :n],
+                                                  err_msg=f"{ctx} queue chain ({e},{m})")
+            np.testing.assert_array_equal(g["q_done"], oc["q_done"], err_msg=ctx)
+            np.testing.assert_array_equal(g["q_met"], oc["q_met"], err_msg=ctx)
         if invariants:
             check_invariants(g, self.cfg, ctx=ctx)
         return g
