@@ -582,7 +582,7 @@ __device__ __forceinline__ void copy_to_lds(u32x4* dst, const u32x4* src) {
   }
 }
 
-template <int H, int NL, int AT, int KB1, bool W1L, int NW, int ED, int NR, int RL>
+template <int H, int NL, int AT, int KB1, bool W1L, int NW, int ED, int NR, int RL, int W1PF>
 __global__ __launch_bounds__(NW * 64, 1) void route_bf16_lds(RouteArgs a_in) {
   // chain pools: the tick's row count is on the device
   RouteArgs a = a_in;
@@ -639,12 +639,19 @@ __global__ __launch_bounds__(NW * 64, 1) void route_bf16_lds(RouteArgs a_in) {
     for (int j = 0; j < NR; ++j) gather_row<ED, 0, KB1>(a, c[j], gg, x[j]);
 
     u32x4 h[NR][KH];
+    // layer-1 fragments: W1PF of the next output tile's K steps are loaded
+    // while the current tile's MFMAs run (the rest just before they are used)
+    u32x4 wk[KB1], wn[KB1];
+#pragma unroll
+    for (int kb = 0; kb < KB1; ++kb) wn[kb] = w1[kb * 64 + ln];
 #pragma unroll
     for (int cc = 0; cc < TH; ++cc) {
-      // all layer-1 fragments of this output tile in flight at once
-      u32x4 wk[KB1];
 #pragma unroll
-      for (int kb = 0; kb < KB1; ++kb) wk[kb] = w1[(cc * KB1 + kb) * 64 + ln];
+      for (int kb = 0; kb < KB1; ++kb) wk[kb] = kb < W1PF || cc == 0 ? wn[kb] : w1[(cc * KB1 + kb) * 64 + ln];
+      if (cc + 1 < TH) {
+#pragma unroll
+        for (int kb = 0; kb < W1PF; ++kb) wn[kb] = w1[((cc + 1) * KB1 + kb) * 64 + ln];
+      }
       f32x16 p[NR];
       p[0] = *(const f32x16*)(lb0 + (cc * 2 + gg) * 16);
 #pragma unroll
@@ -1171,6 +1178,7 @@ RouteKernel pick(int dtype, int hidden, int at) {
 // each) per wave.
 constexpr int kLdsWaves = 16;
 constexpr int kLdsRows = 1;
+constexpr int kLdsW1Prefetch = 0;   // layer-1 K steps of the next output tile loaded ahead
 
 // Persistent LDS-resident variants for the shapes that fit (bytes of packed
 // weights in LDS <= 160 KiB): returns nullptr when none applies.
@@ -1193,11 +1201,11 @@ RouteKernel pick_stream(int dtype, int hidden, int n_layers, int out_tiles, int 
 RouteKernel pick_lds(int dtype, int hidden, int n_layers, int out_tiles, int k1, int ed, bool rl) {
   if (dtype != IM_BF16) return nullptr;
   if (hidden == 256 && n_layers == 3 && out_tiles == 1 && k1 == 6 && ed == 64)
-    return rl ? route_bf16_lds<256, 3, 1, 6, false, kLdsWaves, 64, kLdsRows, 1>
-              : route_bf16_lds<256, 3, 1, 6, false, kLdsWaves, 64, kLdsRows, 0>;
+    return rl ? route_bf16_lds<256, 3, 1, 6, false, kLdsWaves, 64, kLdsRows, 1, kLdsW1Prefetch>
+              : route_bf16_lds<256, 3, 1, 6, false, kLdsWaves, 64, kLdsRows, 0, kLdsW1Prefetch>;
   if (hidden == 256 && n_layers == 2 && out_tiles == 1 && k1 == 7 && ed == 64)
-    return rl ? route_bf16_lds<256, 2, 1, 7, true, kLdsWaves, 64, kLdsRows, 1>
-              : route_bf16_lds<256, 2, 1, 7, true, kLdsWaves, 64, kLdsRows, 0>;
+    return rl ? route_bf16_lds<256, 2, 1, 7, true, kLdsWaves, 64, kLdsRows, 1, kLdsW1Prefetch>
+              : route_bf16_lds<256, 2, 1, 7, true, kLdsWaves, 64, kLdsRows, 0, kLdsW1Prefetch>;
   return nullptr;
 }
 

@@ -20,34 +20,58 @@ __device__ __forceinline__ int32_t usable_arrivals(const RowsArgs& a, int e) {
   return (lo < 0 || hi < lo || hi > a.n_total || hi - lo > a.max_arrivals) ? 0 : hi - lo;
 }
 
-// One block: exclusive scan of (pending + usable arrivals) over the envs,
-// each thread summing a contiguous run of envs.
+// One block: exclusive scan of (pending + usable arrivals) over the envs.
+// Each thread holds the counts of kPer consecutive envs in registers; wave
+// scans by shuffles, the 16 wave totals scanned by the first wave; blocks of
+// 1024 * kPer envs in sequence with a carried total.
+constexpr int kPer = 8;
+
+__device__ __forceinline__ int32_t wave_incl_scan(int32_t x, int lane) {
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const int32_t y = __shfl_up(x, d, 64);
+    if (lane >= d) x += y;
+  }
+  return x;
+}
+
 __global__ __launch_bounds__(kScanThreads) void rows_scan_kernel(RowsArgs a) {
-  __shared__ int32_t part[kScanThreads];
-  const int tid = threadIdx.x;
+  constexpr int NWAVE = kScanThreads / 64;
+  __shared__ int32_t wsum[NWAVE];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int32_t t = a.ms[0].t;
   const int32_t* pc = a.pcnt + (size_t)(t & 1) * a.E;
-  const int per = (a.E + kScanThreads - 1) / kScanThreads;
-  const int e0 = tid * per, e1 = min(e0 + per, a.E);
-  int32_t sum = 0;
-  for (int e = e0; e < e1; ++e) sum += pc[e] + usable_arrivals(a, e);
-  part[tid] = sum;
-  __syncthreads();
-  // Hillis-Steele inclusive scan of the per-thread sums
-  for (int d = 1; d < kScanThreads; d <<= 1) {
-    const int32_t v = tid >= d ? part[tid - d] : 0;
+  int32_t carry = 0;
+  for (int base = 0; base < a.E; base += kScanThreads * kPer) {
+    int32_t c[kPer];
+    int32_t sum = 0;
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const int e = base + tid * kPer + j;
+      c[j] = e < a.E ? pc[e] + usable_arrivals(a, e) : 0;
+      sum += c[j];
+    }
+    const int32_t x = wave_incl_scan(sum, lane);
+    if (lane == 63) wsum[w] = x;
     __syncthreads();
-    part[tid] += v;
+    if (w == 0) {
+      const int32_t v = wave_incl_scan(lane < NWAVE ? wsum[lane] : 0, lane);
+      if (lane < NWAVE) wsum[lane] = v;
+    }
     __syncthreads();
+    int32_t run = carry + (w > 0 ? wsum[w - 1] : 0) + x - sum;
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const int e = base + tid * kPer + j;
+      if (e < a.E) a.roff[e] = run;
+      run += c[j];
+    }
+    carry += wsum[NWAVE - 1];
+    __syncthreads();   // wsum is rewritten by the next block of envs
   }
-  int32_t run = part[tid] - sum;
-  for (int e = e0; e < e1; ++e) {
-    a.roff[e] = run;
-    run += pc[e] + usable_arrivals(a, e);
-  }
-  if (tid == kScanThreads - 1) {
-    a.roff[a.E] = part[tid];
-    a.n_rows[0] = part[tid];
+  if (tid == 0) {
+    a.roff[a.E] = carry;
+    a.n_rows[0] = carry;
   }
 }
 

@@ -127,6 +127,15 @@ __device__ __forceinline__ void merge_front(Queue& q, int4& fe, int2& fx, const 
 // front is returned in `fe` (lane i: entry i), the front array is not written.
 // `pk`/`pi` are this wave's LDS staging rows (64 keys, 64 pool indices), `kb`
 // its LDS buffer for 4 chunks of pool keys.
+// Pool chunks (of 64 entries) per round of the refill scan (chain pools,
+// whose kernel holds more LDS, use fewer to keep 4 blocks per CU), and the
+// s_waitcnt immediate (gfx9 encoding: vmcnt in bits 3:0 and 15:14, expcnt
+// 6:4 and lgkmcnt 11:8 left at their maxima) that waits until at most n
+// vector-memory operations of this wave are outstanding (n < 16).
+template <bool CHAIN>
+constexpr int refill_chunks() { return CHAIN ? 2 : 4; }
+constexpr int wait_vm(int n) { return 0x0F70 | n; }
+
 // With CHAIN the chain words move along: `fx`, `pool_ext`.
 template <bool CHAIN>
 __device__ void refill(Queue& q, int4& fe, int2& fx, int4* pool, int2* pool_ext, int64_t* pk,
@@ -182,21 +191,49 @@ __device__ void refill(Queue& q, int4& fe, int2& fx, int4* pool, int2* pool_ext,
     thr = readlane64(ck, 63);
     np = 0;
   };
-  constexpr int G = 4;   // pool chunks whose loads are in flight together
-  const int2* keys = reinterpret_cast<const int2*>(pool);   // (key, id) of entry i at keys[2 i]
-  for (int c0 = kFront; c0 < P; c0 += G * kFront) {
-    int2 kv[G];
+  // The keys and ids of the remaining entries come into LDS through the LDS
+  // DMA path (no registers held by loads in flight), kRefillChunks chunks of
+  // 64 entries per round, double-buffered: the next round's loads are issued
+  // before the current round is scanned. Lanes past the pool's end load its
+  // last entry (an address in bounds) and are ignored.
+  constexpr int G = refill_chunks<CHAIN>();
+  int32_t* lk = reinterpret_cast<int32_t*>(kb);   // [2][G * kFront] keys
+  int32_t* li = lk + 2 * G * kFront;              // [2][G * kFront] ids
+  const int rounds = (P - kFront + G * kFront - 1) / (G * kFront);
+  auto issue = [&](int r) {
+    const int st = r & 1;
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-      const int i = c0 + g * kFront + lane;
-      kv[g] = i < P ? keys[2 * i] : make_int2(0x7fffffff, -1);   // (max, max) pads
+      const int i = kFront + (r * G + g) * kFront + lane;
+      const int32_t* src = reinterpret_cast<const int32_t*>(pool + (i < P ? i : P - 1));
+      __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)(lk + (st * G + g) * kFront),
+                                       4, 0, 0);
+      __builtin_amdgcn_global_load_lds(src + 1, (__attribute__((address_space(3))) void*)(li + (st * G + g) * kFront),
+                                       4, 0, 0);
     }
-#pragma unroll
-    for (int g = 0; g < G; ++g) kb[g * kFront + lane] = kv[g];
+  };
+  issue(0);
+  for (int r = 0; r < rounds; ++r) {
+    // vector-memory counter: wait for this round's 2G loads, keep the next round's in flight
+    if (r + 1 < rounds) {
+      issue(r + 1);
+      __builtin_amdgcn_s_waitcnt(wait_vm(2 * G));
+    } else {
+      __builtin_amdgcn_s_waitcnt(wait_vm(0));
+    }
+    const int st = r & 1;
 #pragma unroll 1
     for (int g = 0; g < G; ++g) {
-      const int2 v = kb[g * kFront + lane];
-      const int64_t kc = composite(v.x, v.y);
+      const int i = kFront + (r * G + g) * kFront + lane;
+      // Read through inline assembly: the compiler treats an LDS read after an
+      // LDS DMA as dependent on every DMA in flight and would wait for the
+      // next round's loads too; the explicit vmcnt wait above is the exact one.
+      int32_t kv, iv;
+      const uint32_t ak = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) int32_t*)(lk + (st * G + g) * kFront + lane);
+      const uint32_t ai = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) int32_t*)(li + (st * G + g) * kFront + lane);
+      asm volatile("ds_read_b32 %0, %2\n\tds_read_b32 %1, %3\n\ts_waitcnt lgkmcnt(0)"
+                   : "=v"(kv), "=v"(iv) : "v"(ak), "v"(ai));
+      const int64_t kc = i < P ? composite(kv, iv) : kKeyMax;
       uint64_t cm = ballot(kc < thr);
       if (cm == 0) continue;
       if (np + popc64(cm) > kFront) {
@@ -207,7 +244,7 @@ __device__ void refill(Queue& q, int4& fe, int2& fx, int4* pool, int2* pool_ext,
       if ((cm >> lane) & 1ull) {
         const int pos = np + prefix_count(cm);
         pk[pos] = kc;
-        pi[pos] = c0 + g * kFront + lane;
+        pi[pos] = i;
       }
       np += popc64(cm);
     }
@@ -344,7 +381,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
   __shared__ int32_t en_lds[4][IM_MAX_MODELS];
   __shared__ int64_t pend_k[4][kFront];   // refill candidate staging
   __shared__ int32_t pend_i[4][kFront];
-  __shared__ int2 pend_kb[4][4 * kFront];
+  __shared__ int2 pend_kb[4][2 * refill_chunks<CHAIN>() * kFront];   // refill keys and ids, two rounds
   const int lane = threadIdx.x & 63;
   const int wv = threadIdx.x >> 6;
   const int e = (int)blockIdx.x * 4 + wv;
