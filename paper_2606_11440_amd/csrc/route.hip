@@ -539,11 +539,11 @@ __global__ __launch_bounds__(256) void route_f32(RouteArgs a_in) {
 // ---------------------------------------------------------------------------
 // Persistent variant for policies whose deeper layers fit in LDS.
 //
-// Each block (4 waves, one per SIMD) copies the packed weights of layers >= 2
-// (and of layer 1 when it also fits) into LDS once, then loops over 256-row
-// tiles. A wave owns 64 rows as two 32-row MFMA column tiles, so every weight
-// fragment read from LDS feeds two MFMAs. Layer outputs are produced in chunks
-// of 128 features; each hidden chunk is rounded to bf16 fragments right away.
+// Each block (NW waves) copies the packed weights of layers >= 2 (and of
+// layer 1 when it also fits) into LDS once, then its waves take turns over
+// the block's share of wave tiles. A wave tile is NR 32-row MFMA column tiles,
+// so every weight fragment read feeds NR MFMAs. Layer-1 outputs are produced
+// one 32-feature tile at a time and rounded to bf16 fragments right away.
 // ---------------------------------------------------------------------------
 
 __device__ __forceinline__ RowCtx row_setup_env(const RouteArgs& a, int32_t r, int32_t e) {
@@ -582,6 +582,21 @@ __device__ __forceinline__ void copy_to_lds(u32x4* dst, const u32x4* src) {
   }
 }
 
+// Wave tiles (32 NR rows each) of block b in a persistent grid of G blocks:
+// the contiguous range [first, end) of an equal split of all n_units (the
+// shares differ by at most one tile). A row count just above a multiple of
+// the grid's capacity then adds one tile to a few blocks instead of a whole
+// extra round of tiles to one block.
+struct UnitRange {
+  int32_t first, end;
+};
+__device__ __forceinline__ UnitRange block_units(int32_t n_units) {
+  UnitRange u;
+  u.first = (int32_t)(((int64_t)blockIdx.x * n_units) / gridDim.x);
+  u.end = (int32_t)(((int64_t)(blockIdx.x + 1) * n_units) / gridDim.x);
+  return u;
+}
+
 template <int H, int NL, int AT, int KB1, bool W1L, int NW, int ED, int NR, int RL, int W1PF>
 __global__ __launch_bounds__(NW * 64, 1) void route_bf16_lds(RouteArgs a_in) {
   // chain pools: the tick's row count is on the device
@@ -595,8 +610,7 @@ __global__ __launch_bounds__(NW * 64, 1) void route_bf16_lds(RouteArgs a_in) {
   constexpr int N_LDS = (W1L ? N_W1 : 0) + N_W2 + N_W3;
   // biases in accumulator-register order: [tile][g][16] floats per layer
   constexpr int NB0 = TH * 32, NB1 = (NL == 3 ? TH : AT) * 32, NB2 = NL == 3 ? AT * 32 : 0;
-  constexpr int WROWS = 32 * NR;            // rows per wave
-  constexpr int ROWS = NW * WROWS;          // rows per block tile
+  constexpr int WROWS = 32 * NR;            // rows per wave tile
   __shared__ u32x4 lds[N_LDS];
   __shared__ float lbias[NB0 + NB1 + NB2];
   if constexpr (W1L) copy_to_lds<N_W1, NW * 64>(lds, (const u32x4*)a.W[0]);
@@ -613,9 +627,9 @@ __global__ __launch_bounds__(NW * 64, 1) void route_bf16_lds(RouteArgs a_in) {
   const u32x4* w3 = w2 + N_W2;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n = lane & 31, g = lane >> 5;
-  const int n_tiles = (a.n_total + ROWS - 1) / ROWS;
+  const UnitRange ur = block_units((a.n_total + WROWS - 1) / WROWS);
 
-  for (int tile = blockIdx.x; tile < n_tiles; tile += gridDim.x) {
+  for (int32_t u = ur.first + wave; u < ur.end; u += NW) {
     // Keeps loop-invariant loads (biases, weights) inside the loop: hoisted
     // out of it they would stay live in registers for the whole kernel.
     asm volatile("" ::: "memory");
@@ -624,8 +638,7 @@ __global__ __launch_bounds__(NW * 64, 1) void route_bf16_lds(RouteArgs a_in) {
     // (and kept live) across the whole loop.
     int ln = lane, gg = g;
     asm volatile("" : "+v"(ln), "+v"(gg));
-    const int32_t r0 = tile * ROWS + wave * WROWS;
-    if (r0 >= a.n_total) continue;
+    const int32_t r0 = u * WROWS;
     const int32_t rlast = (r0 + WROWS - 1 < a.n_total ? r0 + WROWS - 1 : a.n_total - 1);
     int32_t rows[NR], envs[NR];
 #pragma unroll
@@ -971,7 +984,6 @@ __global__ __launch_bounds__(NW * 64, 1) void route_dual_bf16(RouteArgs a_in) {
   constexpr int N_MRG = 4 * 12 * 64;
   constexpr int N_ACT = 8 * 64;
   constexpr int WROWS = 32 * NR;
-  constexpr int ROWS = NW * WROWS;
   __shared__ u32x4 lds[N_SEM + N_MRG + N_ACT];
   __shared__ float lp[DP_LDS];
   copy_to_lds<N_SEM, NW * 64>(lds, (const u32x4*)a.W[0]);
@@ -986,16 +998,15 @@ __global__ __launch_bounds__(NW * 64, 1) void route_dual_bf16(RouteArgs a_in) {
   const float* proj = a.dual_p + DP_ROLE;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n = lane & 31, g = lane >> 5;
-  const int n_tiles = (a.n_total + ROWS - 1) / ROWS;
   const int n3 = 3 * a.M;
   const int sstride = snap_stride(a.M);
+  const UnitRange ur = block_units((a.n_total + WROWS - 1) / WROWS);
 
-  for (int tile = blockIdx.x; tile < n_tiles; tile += gridDim.x) {
+  for (int32_t u = ur.first + wave; u < ur.end; u += NW) {
     asm volatile("" ::: "memory");
     int ln = lane, gg = g;
     asm volatile("" : "+v"(ln), "+v"(gg));
-    const int32_t r0 = tile * ROWS + wave * WROWS;
-    if (r0 >= a.n_total) continue;
+    const int32_t r0 = u * WROWS;
     const int32_t rlast = (r0 + WROWS - 1 < a.n_total ? r0 + WROWS - 1 : a.n_total - 1);
     int32_t rows[NR], envs[NR];
 #pragma unroll
@@ -1174,19 +1185,38 @@ RouteKernel pick(int dtype, int hidden, int at) {
   return nullptr;
 }
 
-// Persistent kernels: kLdsWaves waves per block, kLdsRows row tiles (32 rows
-// each) per wave.
-constexpr int kLdsWaves = 16;
-constexpr int kLdsRows = 1;
-constexpr int kLdsW1Prefetch = 0;   // layer-1 K steps of the next output tile loaded ahead
+// Persistent LDS-resident kernels and their launch shape (waves per block,
+// 32-row MFMA tiles per wave). The greedy route and the RL outputs are
+// separate instantiations, so each keeps only the registers its own epilogue
+// needs.
+struct LdsLaunch {
+  RouteKernel k;
+  int waves;
+  int rows;
+};
 
-// Persistent LDS-resident variants for the shapes that fit (bytes of packed
-// weights in LDS <= 160 KiB): returns nullptr when none applies.
-constexpr int kStreamWaves = 8;
+// 86 -> 256 -> 256 -> A, layer-1 weights through the caches: 8 waves (two
+// per SIMD) of 64 rows, so every weight fragment read from LDS or the caches
+// feeds two MFMAs, with the next output tile's layer-1 fragments loaded
+// while the current one is multiplied (up to 256 VGPRs per wave).
+// 104 -> 256 -> A, every layer in LDS: 16 waves of 32 rows (128 VGPRs).
+// Returns a null kernel when no LDS-resident variant applies.
+LdsLaunch pick_lds(int dtype, int hidden, int n_layers, int out_tiles, int k1, int ed, bool rl) {
+  if (dtype != IM_BF16) return {nullptr, 0, 0};
+  if (hidden == 256 && n_layers == 3 && out_tiles == 1 && k1 == 6 && ed == 64)
+    return {rl ? route_bf16_lds<256, 3, 1, 6, false, 8, 64, 2, 1, 6>
+               : route_bf16_lds<256, 3, 1, 6, false, 8, 64, 2, 0, 6>, 8, 2};
+  if (hidden == 256 && n_layers == 2 && out_tiles == 1 && k1 == 7 && ed == 64)
+    return {rl ? route_bf16_lds<256, 2, 1, 7, true, 16, 64, 1, 1, 0>
+               : route_bf16_lds<256, 2, 1, 7, true, 16, 64, 1, 0, 0>, 16, 1};
+  return {nullptr, 0, 0};
+}
 
 // Streaming kernels: kStreamWaves waves per block, 32 rows per wave. The
 // greedy route and the RL outputs are separate instantiations, so each keeps
 // only the registers its own epilogue needs.
+constexpr int kStreamWaves = 8;
+
 RouteKernel pick_stream(int dtype, int hidden, int n_layers, int out_tiles, int k1, int ed, bool rl) {
   if (dtype != IM_BF16) return nullptr;
   if (hidden == 512 && n_layers == 3 && out_tiles == 2 && k1 == 13 && ed == 128)
@@ -1195,17 +1225,6 @@ RouteKernel pick_stream(int dtype, int hidden, int n_layers, int out_tiles, int 
   if (hidden == 512 && n_layers == 3 && out_tiles == 3 && k1 == 13 && ed == 128)
     return rl ? route_bf16_stream<512, 3, 13, 128, kStreamWaves, 1>
               : route_bf16_stream<512, 3, 13, 128, kStreamWaves, 0>;
-  return nullptr;
-}
-
-RouteKernel pick_lds(int dtype, int hidden, int n_layers, int out_tiles, int k1, int ed, bool rl) {
-  if (dtype != IM_BF16) return nullptr;
-  if (hidden == 256 && n_layers == 3 && out_tiles == 1 && k1 == 6 && ed == 64)
-    return rl ? route_bf16_lds<256, 3, 1, 6, false, kLdsWaves, 64, kLdsRows, 1, kLdsW1Prefetch>
-              : route_bf16_lds<256, 3, 1, 6, false, kLdsWaves, 64, kLdsRows, 0, kLdsW1Prefetch>;
-  if (hidden == 256 && n_layers == 2 && out_tiles == 1 && k1 == 7 && ed == 64)
-    return rl ? route_bf16_lds<256, 2, 1, 7, true, kLdsWaves, 64, kLdsRows, 1, kLdsW1Prefetch>
-              : route_bf16_lds<256, 2, 1, 7, true, kLdsWaves, 64, kLdsRows, 0, kLdsW1Prefetch>;
   return nullptr;
 }
 
@@ -1261,12 +1280,12 @@ hipError_t launch_route(const RouteArgs& a, int dtype, int hidden, int n_layers,
   if (a.n_total <= 0) return hipSuccess;
   if (a.net == IM_NET_DUAL) return launch_dual(a, s);
   if (a.persistent_blocks > 0) {
-    RouteKernel kl = pick_lds(dtype, hidden, n_layers, out_tiles, a.k1, a.embed_dim, a.rl != 0);
-    if (kl) {
-      const int rows = kLdsWaves * 32 * kLdsRows;
+    const LdsLaunch kl = pick_lds(dtype, hidden, n_layers, out_tiles, a.k1, a.embed_dim, a.rl != 0);
+    if (kl.k) {
+      const int rows = kl.waves * 32 * kl.rows;
       const int n_tiles = (a.n_total + rows - 1) / rows;
       const unsigned blocks = (unsigned)(n_tiles < a.persistent_blocks ? n_tiles : a.persistent_blocks);
-      hipLaunchKernelGGL(kl, dim3(blocks), dim3(kLdsWaves * 64), 0, s, a);
+      hipLaunchKernelGGL(kl.k, dim3(blocks), dim3(kl.waves * 64), 0, s, a);
       return hipGetLastError();
     }
   }
