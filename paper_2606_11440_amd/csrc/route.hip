@@ -68,14 +68,27 @@ __device__ __forceinline__ int32_t find_env_bsearch(const RouteArgs& a, int32_t 
   return lo < a.E ? lo : a.E - 1;
 }
 
-template <int NR>
-__device__ __forceinline__ void find_envs(const RouteArgs& a, int32_t rfirst, int32_t rlast,
-                                          const int32_t (&r)[NR], int32_t (&e)[NR]) {
-  const int lane = lane_id();
+// First guess of the env window of rows from rfirst on, and its offsets
+// (lane i: offsets[e_lo + i]); find_envs_in completes the lookup.
+struct EnvWindow {
+  int32_t e_lo, ow;
+};
+__device__ __forceinline__ EnvWindow env_window(const RouteArgs& a, int32_t rfirst) {
+  EnvWindow w;
   int32_t e_lo = (int32_t)((float)rfirst * a.envs_per_row) - 16;
-  e_lo = e_lo < 0 ? 0 : (e_lo > a.E - 1 ? a.E - 1 : e_lo);
-  int32_t wi = e_lo + lane;
-  int32_t ow = a.offsets[wi < a.E ? wi : a.E];
+  w.e_lo = e_lo < 0 ? 0 : (e_lo > a.E - 1 ? a.E - 1 : e_lo);
+  const int32_t wi = w.e_lo + lane_id();
+  w.ow = a.offsets[wi < a.E ? wi : a.E];
+  return w;
+}
+
+template <int NR>
+__device__ __forceinline__ void find_envs_in(const RouteArgs& a, EnvWindow w, int32_t rfirst, int32_t rlast,
+                                             const int32_t (&r)[NR], int32_t (&e)[NR]) {
+  const int lane = lane_id();
+  int32_t e_lo = w.e_lo;
+  int32_t wi;
+  int32_t ow = w.ow;
   bool ok = __builtin_amdgcn_readfirstlane(ow) <= rfirst &&
             rlast < __builtin_amdgcn_readlane(ow, 63);
   if (!ok) {
@@ -105,6 +118,12 @@ __device__ __forceinline__ void find_envs(const RouteArgs& a, int32_t rfirst, in
   }
 #pragma unroll
   for (int j = 0; j < NR; ++j) e[j] = e[j] < 0 ? 0 : (e[j] > a.E - 1 ? a.E - 1 : e[j]);
+}
+
+template <int NR>
+__device__ __forceinline__ void find_envs(const RouteArgs& a, int32_t rfirst, int32_t rlast,
+                                          const int32_t (&r)[NR], int32_t (&e)[NR]) {
+  find_envs_in<NR>(a, env_window(a, rfirst), rfirst, rlast, r, e);
 }
 
 // Row context of row r (per lane) in a wave whose rows lie in [row0, row0 + 31].
@@ -546,6 +565,20 @@ __global__ __launch_bounds__(256) void route_f32(RouteArgs a_in) {
 // one 32-feature tile at a time and rounded to bf16 fragments right away.
 // ---------------------------------------------------------------------------
 
+// Row context of row r in env e from its already loaded record fields.
+__device__ __forceinline__ RowCtx row_ctx_from(const RouteArgs& a, int32_t r, int32_t e, int32_t q,
+                                               int32_t budget) {
+  RowCtx c;
+  c.r = r;
+  c.live = r < a.n_total;
+  c.e = e;
+  c.bad = (q < 0 || (int64_t)q >= a.Q) ? IM_ERR_QIDX : 0;
+  c.q = c.bad ? 0 : q;
+  c.budget = budget;
+  c.amask = action_mask(a, e);
+  return c;
+}
+
 __device__ __forceinline__ RowCtx row_setup_env(const RouteArgs& a, int32_t r, int32_t e) {
   RowCtx c;
   c.r = r;
@@ -597,7 +630,7 @@ __device__ __forceinline__ UnitRange block_units(int32_t n_units) {
   return u;
 }
 
-template <int H, int NL, int AT, int KB1, bool W1L, int NW, int ED, int NR, int RL, int W1PF>
+template <int H, int NL, int AT, int KB1, bool W1L, int NW, int ED, int NR, int RL, int W1PF, bool PIPE>
 __global__ __launch_bounds__(NW * 64, 1) void route_bf16_lds(RouteArgs a_in) {
   // chain pools: the tick's row count is on the device
   RouteArgs a = a_in;
@@ -613,23 +646,69 @@ __global__ __launch_bounds__(NW * 64, 1) void route_bf16_lds(RouteArgs a_in) {
   constexpr int WROWS = 32 * NR;            // rows per wave tile
   __shared__ u32x4 lds[N_LDS];
   __shared__ float lbias[NB0 + NB1 + NB2];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform loop control
+  const int n = lane & 31, g = lane >> 5;
+  const UnitRange ur = block_units((a.n_total + WROWS - 1) / WROWS);
+  // Wave tile u is set up in two steps: its first loads (the CSR window and
+  // the rows' q_idx and budget), then, once they have arrived, the env
+  // lookup, the env's snapshot row and the embedding rows (row contexts and
+  // layer-1 B fragments).
+  struct First {
+    EnvWindow w;
+    int32_t q[NR], bud[NR];
+  };
+  auto first_loads = [&](int32_t u) {
+    First f;
+    const int32_t r0 = u * WROWS;
+    f.w = env_window(a, r0);
+#pragma unroll
+    for (int j = 0; j < NR; ++j) {
+      const int32_t r = r0 + 32 * j + n;
+      const int32_t rr = r < a.n_total ? r : a.n_total - 1;
+      f.q[j] = a.q_idx[rr];
+      f.bud[j] = a.budget[rr];
+    }
+    return f;
+  };
+  auto setup = [&](int32_t u, const First& f, RowCtx (&c)[NR], u32x4 (&x)[NR][KB1], int gg) {
+    const int32_t r0 = u * WROWS;
+    const int32_t rlast = (r0 + WROWS - 1 < a.n_total ? r0 + WROWS - 1 : a.n_total - 1);
+    int32_t rows[NR], envs[NR];
+#pragma unroll
+    for (int j = 0; j < NR; ++j) rows[j] = r0 + 32 * j + n;
+    find_envs_in<NR>(a, f.w, r0, rlast, rows, envs);
+#pragma unroll
+    for (int j = 0; j < NR; ++j) c[j] = row_ctx_from(a, rows[j], envs[j], f.q[j], f.bud[j]);
+#pragma unroll
+    for (int j = 0; j < NR; ++j) gather_row<ED, 0, KB1>(a, c[j], gg, x[j]);
+  };
+  // PIPE: the loop is software-pipelined, the next wave tile's first loads
+  // being issued once the current tile's MFMAs have been, so that they are in
+  // flight during its epilogue, and the first tile's during the block's copy
+  // of the weights into LDS (this holds a few more registers across the
+  // epilogue, so it pays only where the registers are not all taken).
+  int32_t u = ur.first + wave;
+  RowCtx c[NR];
+  u32x4 x[NR][KB1];
+  First f0;
+  if (PIPE && u < ur.end) f0 = first_loads(u);
   if constexpr (W1L) copy_to_lds<N_W1, NW * 64>(lds, (const u32x4*)a.W[0]);
   copy_to_lds<N_W2, NW * 64>(lds + (W1L ? N_W1 : 0), (const u32x4*)a.W[1]);
   if constexpr (NL == 3) copy_to_lds<N_W3, NW * 64>(lds + (W1L ? N_W1 : 0) + N_W2, (const u32x4*)a.W[2]);
   for (int i = threadIdx.x; i < NB0 + NB1 + NB2; i += NW * 64)
     lbias[i] = i < NB0 ? a.bias[0][i] : (i < NB0 + NB1 ? a.bias[1][i - NB0] : a.bias[2][i - NB0 - NB1]);
   __syncthreads();
+  if (u >= ur.end) return;
+  if constexpr (PIPE) setup(u, f0, c, x, g);
   const float* lb0 = lbias;
   const float* lb1 = lbias + NB0;
   const float* lb2 = lbias + NB0 + NB1;
   const u32x4* w1 = W1L ? (const u32x4*)lds : (const u32x4*)a.W[0];
   const u32x4* w2 = lds + (W1L ? N_W1 : 0);
   const u32x4* w3 = w2 + N_W2;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int n = lane & 31, g = lane >> 5;
-  const UnitRange ur = block_units((a.n_total + WROWS - 1) / WROWS);
 
-  for (int32_t u = ur.first + wave; u < ur.end; u += NW) {
+  for (;;) {
     // Keeps loop-invariant loads (biases, weights) inside the loop: hoisted
     // out of it they would stay live in registers for the whole kernel.
     asm volatile("" ::: "memory");
@@ -638,18 +717,7 @@ __global__ __launch_bounds__(NW * 64, 1) void route_bf16_lds(RouteArgs a_in) {
     // (and kept live) across the whole loop.
     int ln = lane, gg = g;
     asm volatile("" : "+v"(ln), "+v"(gg));
-    const int32_t r0 = u * WROWS;
-    const int32_t rlast = (r0 + WROWS - 1 < a.n_total ? r0 + WROWS - 1 : a.n_total - 1);
-    int32_t rows[NR], envs[NR];
-#pragma unroll
-    for (int j = 0; j < NR; ++j) rows[j] = r0 + 32 * j + n;
-    find_envs<NR>(a, r0, rlast, rows, envs);
-    RowCtx c[NR];
-#pragma unroll
-    for (int j = 0; j < NR; ++j) c[j] = row_setup_env(a, rows[j], envs[j]);
-    u32x4 x[NR][KB1];
-#pragma unroll
-    for (int j = 0; j < NR; ++j) gather_row<ED, 0, KB1>(a, c[j], gg, x[j]);
+    if constexpr (!PIPE) setup(u, first_loads(u), c, x, gg);
 
     u32x4 h[NR][KH];
     // layer-1 fragments: W1PF of the next output tile's K steps are loaded
@@ -729,8 +797,18 @@ __global__ __launch_bounds__(NW * 64, 1) void route_bf16_lds(RouteArgs a_in) {
         }
       }
     }
+    const int32_t un = u + NW;
+    First fn;
+    if constexpr (PIPE) {
+      __builtin_amdgcn_sched_barrier(0);
+      if (un < ur.end) fn = first_loads(un);
+      __builtin_amdgcn_sched_barrier(0);
+    }
 #pragma unroll
     for (int j = 0; j < NR; ++j) epilogue<AT, RL>(a, c[j], o[j], nullptr, gg);
+    if (un >= ur.end) break;
+    u = un;
+    if constexpr (PIPE) setup(u, fn, c, x, gg);
   }
 }
 
@@ -1195,20 +1273,22 @@ struct LdsLaunch {
   int rows;
 };
 
-// 86 -> 256 -> 256 -> A, layer-1 weights through the caches: 8 waves (two
-// per SIMD) of 64 rows, so every weight fragment read from LDS or the caches
-// feeds two MFMAs, with the next output tile's layer-1 fragments loaded
-// while the current one is multiplied (up to 256 VGPRs per wave).
-// 104 -> 256 -> A, every layer in LDS: 16 waves of 32 rows (128 VGPRs).
-// Returns a null kernel when no LDS-resident variant applies.
+// 86 -> 256 -> 256 -> A, layer-1 weights through the caches: the greedy
+// route runs 8 waves (two per SIMD) of 64 rows, so every weight fragment read
+// from LDS or the caches feeds two MFMAs, with the next output tile's layer-1
+// fragments loaded while the current one is multiplied (up to 256 VGPRs per
+// wave); the RL outputs, whose epilogue needs more registers, run 16 waves of
+// 32 rows. 104 -> 256 -> A, every layer in LDS: 16 waves of 32 rows (128
+// VGPRs), software-pipelined. Returns a null kernel when no LDS-resident
+// variant applies.
 LdsLaunch pick_lds(int dtype, int hidden, int n_layers, int out_tiles, int k1, int ed, bool rl) {
   if (dtype != IM_BF16) return {nullptr, 0, 0};
   if (hidden == 256 && n_layers == 3 && out_tiles == 1 && k1 == 6 && ed == 64)
-    return {rl ? route_bf16_lds<256, 3, 1, 6, false, 8, 64, 2, 1, 6>
-               : route_bf16_lds<256, 3, 1, 6, false, 8, 64, 2, 0, 6>, 8, 2};
+    return {rl ? route_bf16_lds<256, 3, 1, 6, false, 16, 64, 1, 1, 0, false>
+               : route_bf16_lds<256, 3, 1, 6, false, 8, 64, 2, 0, 6, false>, rl ? 16 : 8, rl ? 1 : 2};
   if (hidden == 256 && n_layers == 2 && out_tiles == 1 && k1 == 7 && ed == 64)
-    return {rl ? route_bf16_lds<256, 2, 1, 7, true, 16, 64, 1, 1, 0>
-               : route_bf16_lds<256, 2, 1, 7, true, 16, 64, 1, 0, 0>, 16, 1};
+    return {rl ? route_bf16_lds<256, 2, 1, 7, true, 16, 64, 1, 1, 0, true>
+               : route_bf16_lds<256, 2, 1, 7, true, 16, 64, 1, 0, 0, true>, 16, 1};
   return {nullptr, 0, 0};
 }
 
