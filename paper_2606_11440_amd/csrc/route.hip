@@ -844,7 +844,6 @@ __global__ __launch_bounds__(NW * 64, 1) void route_bf16_stream(RouteArgs a_in) 
   constexpr int F2 = KH + 2 * AT;             // fragments of a layer-2 stage
   constexpr int FS = F1 > F2 ? F1 : F2;
   constexpr int NB0 = TH * 32, NB1 = TH * 32, NB2 = AT * 32;
-  constexpr int ROWS = NW * 32;
   static_assert(NST % 2 == 0, "stage parity must repeat every block step");
   static_assert(KH % NW == 0 && 2 * AT <= NW, "layer-2 stage split over the waves");
   __shared__ u32x4 ring[2][FS * 64];
@@ -880,8 +879,13 @@ __global__ __launch_bounds__(NW * 64, 1) void route_bf16_stream(RouteArgs a_in) 
   for (int i = threadIdx.x; i < NB0 + NB1 + NB2; i += NW * 64)
     lbias[i] = i < NB0 ? a.bias[0][i] : (i < NB0 + NB1 ? a.bias[1][i - NB0] : a.bias[2][i - NB0 - NB1]);
   issue(0, 0, __builtin_amdgcn_readfirstlane(wave), lane);
-  const int n_tiles = (a.n_total + ROWS - 1) / ROWS;
-  for (int tile = blockIdx.x; tile < n_tiles; tile += gridDim.x) {
+  // The block takes an equal contiguous share of the 32-row wave tiles (the
+  // shares differ by at most one), NW per block step; in its last step the
+  // waves without a tile still bring in their share of the weights and join
+  // the barriers, but skip the arithmetic.
+  const UnitRange ur = block_units((a.n_total + 31) / 32);
+  const int n_steps = (ur.end - ur.first + NW - 1) / NW;
+  for (int step = 0; step < n_steps; ++step) {
     // Per-iteration copies of the lane and wave indices: the fragment and
     // bias addresses derived from them are recomputed in each block step
     // instead of being hoisted out of the loop and kept live across it.
@@ -890,15 +894,32 @@ __global__ __launch_bounds__(NW * 64, 1) void route_bf16_stream(RouteArgs a_in) 
     int wv = __builtin_amdgcn_readfirstlane(wave);
     asm volatile("" : "+v"(ln), "+v"(gg));
     asm volatile("" : "+s"(wv));
-    const int32_t r0 = tile * ROWS + wv * 32;
-    const int32_t rf = r0 < a.n_total ? r0 : a.n_total - 1;   // waves past the end idle on a clamped row
+    const int32_t unit = ur.first + step * NW + wv;
+    const bool act = unit < ur.end;                             // wave-uniform
+    const int32_t r0 = act ? unit * 32 : a.n_total - 1;        // idle waves: a clamped row, nothing stored
     const int32_t rl = r0 + 31 < a.n_total ? r0 + 31 : a.n_total - 1;
-    const int32_t rows[1] = {r0 + (ln & 31)};
+    const int32_t rows[1] = {act ? r0 + (ln & 31) : a.n_total};
+    const int32_t rsel[1] = {rows[0] < a.n_total ? rows[0] : a.n_total - 1};
     int32_t envs[1];
-    find_envs<1>(a, rf, rl, rows, envs);
-    const RowCtx c = row_setup_env(a, rows[0], envs[0]);
+    RowCtx c;
     u32x4 x[KB1];
-    gather_row<ED, 0, KB1>(a, c, gg, x);
+    if (act) {
+      find_envs<1>(a, r0, rl, rsel, envs);
+      c = row_setup_env(a, rows[0], envs[0]);
+      gather_row<ED, 0, KB1>(a, c, gg, x);
+    }
+    if (!act) {
+      // the same stages, barriers and copies as a working wave (a barrier
+      // counts waves, wherever they wait), without the arithmetic
+      for (int s = 0; s < NST; ++s) {
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        int lns = ln;
+        asm volatile("" : "+v"(lns));
+        issue(s + 1 < NST ? s + 1 : 0, (s + 1) & 1, wv, lns);
+      }
+      continue;
+    }
     u32x4 h[KH];
     f32x16 z[AT];
 #pragma unroll
