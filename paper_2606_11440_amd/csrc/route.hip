@@ -1346,10 +1346,10 @@ RouteKernel pick_dual(int ed, bool rl) {
 hipError_t launch_dual(const RouteArgs& a, hipStream_t s) {
   RouteKernel k = pick_dual(a.embed_dim, a.rl != 0);
   if (!k) return hipErrorInvalidValue;
-  const int rows = kDualWaves * 32 * kDualRows;
-  const int n_tiles = (a.n_total + rows - 1) / rows;
+  const int rows = 32 * kDualRows;
+  const int units = (a.n_total + rows - 1) / rows;   // wave tiles, spread over up to one block per CU
   const unsigned blocks =
-      (unsigned)(a.persistent_blocks > 0 && n_tiles > a.persistent_blocks ? a.persistent_blocks : n_tiles);
+      (unsigned)(a.persistent_blocks > 0 && units > a.persistent_blocks ? a.persistent_blocks : units);
   hipLaunchKernelGGL(k, dim3(blocks), dim3(kDualWaves * 64), 0, s, a);
   return hipGetLastError();
 }
@@ -1383,9 +1383,11 @@ hipError_t launch_route(const RouteArgs& a, int dtype, int hidden, int n_layers,
   if (a.persistent_blocks > 0) {
     const LdsLaunch kl = pick_lds(dtype, hidden, n_layers, out_tiles, a.k1, a.embed_dim, a.rl != 0);
     if (kl.k) {
-      const int rows = kl.waves * 32 * kl.rows;
-      const int n_tiles = (a.n_total + rows - 1) / rows;
-      const unsigned blocks = (unsigned)(n_tiles < a.persistent_blocks ? n_tiles : a.persistent_blocks);
+      // one block per CU as long as there are wave tiles for them: a light
+      // tick spreads its few tiles over every CU instead of filling a few
+      const int rows = 32 * kl.rows;
+      const int units = (a.n_total + rows - 1) / rows;
+      const unsigned blocks = (unsigned)(units < a.persistent_blocks ? units : a.persistent_blocks);
       hipLaunchKernelGGL(kl.k, dim3(blocks), dim3(kl.waves * 64), 0, s, a);
       return hipGetLastError();
     }
