@@ -103,8 +103,12 @@ uint16_t to_bf16(float f) {
 int bf16_k(int layer, int kb, int g, int j) {
   return layer == 0 ? 16 * kb + 8 * g + j : 16 * kb + 8 * (j >> 2) + 4 * g + (j & 3);
 }
-int f32_k(int layer, int i, int g) {
-  return layer == 0 ? 2 * i + g : 32 * (i >> 4) + 8 * ((i & 15) >> 2) + 4 * g + (i & 3);
+// Feature read by K step i of lane group q (lane / 16) in the fp32 kernel's
+// 16x16x4 MFMA order: layer 1 in natural order; later layers in the previous
+// layer's accumulator order (tile i / 4, register i % 4: feature 16 (i / 4)
+// + 4 q + i % 4).
+int f32_k(int layer, int i, int q) {
+  return layer == 0 ? 4 * i + q : 16 * (i >> 2) + 4 * q + (i & 3);
 }
 
 template <class T>
@@ -291,7 +295,8 @@ im_status im_pool_create(const im_pool_desc* desc, const float* const* W, const 
     return fail(nullptr, IM_EUNSUPPORTED, "hidden widths must be equal");
   if (d.dtype != IM_F32 && d.dtype != IM_BF16) return fail(nullptr, IM_EINVAL, "bad dtype");
   const int H = d.widths[0];
-  const int out_tiles = (A + d.value_head + 31) / 32;
+  // output tiles of the last layer: 32 rows (bf16 kernels) or 16 rows (fp32)
+  const int out_tiles = d.dtype == IM_F32 ? (A + d.value_head + 15) / 16 : (A + d.value_head + 31) / 32;
   if (!im::route_supported(d.dtype, H, d.n_layers, out_tiles))
     return fail(nullptr, IM_EUNSUPPORTED, "no route kernel for this dtype / hidden width");
 
@@ -324,30 +329,34 @@ im_status im_pool_create(const im_pool_desc* desc, const float* const* W, const 
             }
       st = upload(p, (uint16_t**)&p->W[l], pk);
     } else {
-      const int KI = (in + 1) / 2;
-      if (l == 0) p->k1 = KI;
-      std::vector<float> pk((size_t)TO * KI * 64, 0.f);
-      for (int To = 0; To < TO; ++To)
-        for (int i = 0; i < KI; ++i)
+      // 16-row output tiles, K steps of 4 grouped by four: [To][group][lane][4]
+      const int TO16 = (outw + 15) / 16;
+      const int KS = (in + 3) / 4, KG = (KS + 3) / 4;
+      if (l == 0) p->k1 = KS;
+      std::vector<float> pk((size_t)TO16 * KG * 64 * 4, 0.f);
+      for (int To = 0; To < TO16; ++To)
+        for (int i = 0; i < KS; ++i)
           for (int lane = 0; lane < 64; ++lane) {
-            const int o = 32 * To + (lane & 31);
-            const int k = f32_k(l, i, lane >> 5);
-            if (o < outw && k < in) pk[((size_t)To * KI + i) * 64 + lane] = Wl[(size_t)o * in + k];
+            const int o = 16 * To + (lane & 15);
+            const int k = f32_k(l, i, lane >> 4);
+            if (o < outw && k < in)
+              pk[(((size_t)To * KG + (i >> 2)) * 64 + lane) * 4 + (i & 3)] = Wl[(size_t)o * in + k];
           }
       st = upload(p, (float**)&p->W[l], pk);
     }
     if (st != IM_OK) break;
-    // Bias in accumulator-register order: [To][g][v] -> feature 32To + 8(v/4) + 4g + v%4.
-    std::vector<float> bp((size_t)TO * 2 * 16, 0.f);
-    for (int To = 0; To < TO; ++To)
-      for (int g = 0; g < 2; ++g)
-        for (int v = 0; v < 16; ++v) {
-          const int o = 32 * To + 8 * (v >> 2) + 4 * g + (v & 3);
-          if (o >= outw) continue;
-          float val = b[l][o];
-          if (l == d.n_layers - 1 && logit_bias && o < A) val += logit_bias[o / d.n_depths];
-          bp[((size_t)To * 2 + g) * 16 + v] = val;
-        }
+    // Bias in accumulator-register order: bf16 [To][g][v] -> feature 32To + 8(v/4) + 4g + v%4;
+    // fp32 [To][q][r] -> feature 16To + 4q + r.
+    const bool f32 = d.dtype == IM_F32;
+    std::vector<float> bp((size_t)TO * 2 * 16, 0.f);   // TO 32-row tiles = 2 TO 16-row tiles
+    for (size_t i = 0; i < bp.size(); ++i) {
+      const int v = (int)(i % 16), g = (int)(i / 16) % 2, To = (int)(i / 32);
+      const int o = f32 ? (int)i : 32 * To + 8 * (v >> 2) + 4 * g + (v & 3);
+      if (o >= outw) continue;
+      float val = b[l][o];
+      if (l == d.n_layers - 1 && logit_bias && o < A) val += logit_bias[o / d.n_depths];
+      bp[i] = val;
+    }
     st = upload(p, &p->bias[l], bp);
     in = outw;
   }

@@ -14,7 +14,8 @@
 // pool creation to match, so activations never leave registers.
 //
 // bf16 pools use v_mfma_f32_32x32x16_bf16 (fp32 accumulate, hidden activations
-// rounded to bf16 after the ReLU); fp32 pools use v_mfma_f32_32x32x2_f32.
+// rounded to bf16 after the ReLU); fp32 pools use v_mfma_f32_16x16x4_f32 on
+// 16-row tiles in the same transposed scheme.
 #include <math.h>
 
 #include "im_internal.h"
@@ -31,8 +32,9 @@ __device__ __forceinline__ f32x16 mfma_bf16(u32x4 a, u32x4 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
                                                  __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
-__device__ __forceinline__ f32x16 mfma_f32(float a, float b, f32x16 c) {
-  return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ f32x4 mfma16_f32(float a, float b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }
 
 struct RowCtx {
@@ -142,6 +144,34 @@ __device__ __forceinline__ RowCtx row_setup(const RouteArgs& a, int32_t row0, in
   c.q = c.bad ? 0 : q;
   c.budget = a.budget[rr];
   c.amask = action_mask(a, c.e);
+  return c;
+}
+
+// Row context of row r in env e from its already loaded record fields.
+__device__ __forceinline__ RowCtx row_ctx_from(const RouteArgs& a, int32_t r, int32_t e, int32_t q,
+                                               int32_t budget) {
+  RowCtx c;
+  c.r = r;
+  c.live = r < a.n_total;
+  c.e = e;
+  c.bad = (q < 0 || (int64_t)q >= a.Q) ? IM_ERR_QIDX : 0;
+  c.q = c.bad ? 0 : q;
+  c.budget = budget;
+  c.amask = action_mask(a, e);
+  return c;
+}
+
+__device__ __forceinline__ RowCtx row_setup_env(const RouteArgs& a, int32_t r, int32_t e) {
+  RowCtx c;
+  c.r = r;
+  c.live = r < a.n_total;
+  const int32_t rr = c.live ? r : a.n_total - 1;
+  c.e = e;
+  const int32_t q = a.q_idx[rr];
+  c.bad = (q < 0 || (int64_t)q >= a.Q) ? IM_ERR_QIDX : 0;
+  c.q = c.bad ? 0 : q;
+  c.budget = a.budget[rr];
+  c.amask = action_mask(a, e);
   return c;
 }
 
@@ -482,77 +512,254 @@ __global__ __launch_bounds__(256) void route_bf16(RouteArgs a_in) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// fp32 policies on v_mfma_f32_16x16x4_f32, one wave per 16 rows (a light
+// fp32 tick, ~16 K requests, still gives every SIMD a wave).
+//
+// Transposed form Y^T = W X^T: lane l serves row n = l % 16 of the wave's
+// rows and K group q = l / 16. An output tile's accumulator holds features
+// 16 T + 4 q + r (r = 0..3) of the lane's row: exactly the B operand of the
+// next layer's K step (T, r), whose weight columns are permuted to match at
+// pool creation, so activations never leave registers. Weights are packed so
+// that one 16-byte load per lane covers four consecutive K steps; the hidden
+// layers' loads run D steps ahead of their MFMAs.
+// ---------------------------------------------------------------------------
+
+// Masked argmax over the four lanes of a row (q = 0..3), action and logits
+// stores, or the RL-rollout outputs; lane (n, q) holds actions 16 T + 4 q + r.
+// Same rules as the 32-row epilogue: lowest action on exact ties, Philox block
+// (id, env, action / 4) per four consecutive actions.
+template <int AT>
+__device__ __forceinline__ void epilogue16(const RouteArgs& a, const RowCtx& c, const f32x4 (&acc)[AT], int q) {
+  float best = 0.f;
+  int ba = -1;
+#pragma unroll
+  for (int T = 0; T < AT; ++T) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int act = 16 * T + 4 * q + r;
+      const float z = acc[T][r];
+      if (act < a.A && ((c.amask >> act) & 1ull)) {
+        if (ba < 0 || z > best) { best = z; ba = act; }
+      }
+    }
+  }
+#pragma unroll
+  for (int off = 16; off <= 32; off *= 2) {
+    const float ob = __shfl_xor(best, off, 64);
+    const int oa = __shfl_xor(ba, off, 64);
+    if (oa >= 0 && (ba < 0 || ob > best || (ob == best && oa < ba))) { best = ob; ba = oa; }
+  }
+  if (a.rl) {
+    const bool sample = a.greedy == 0;
+    uint32_t id = 0;
+    if (sample) {
+      const int32_t rr = c.live ? c.r : a.n_total - 1;
+      id = (uint32_t)(a.ms[(size_t)c.e * a.M].next_id + (rr - a.offsets[c.e]));
+    }
+    float sm = 0.f, sz = 0.f, val = 0.f, bs = 0.f, bz = 0.f;
+    int bsa = -1;
+#pragma unroll
+    for (int T = 0; T < AT; ++T) {
+      const int a0 = 16 * T + 4 * q;   // this lane's 4 consecutive actions: one Philox block
+      uint4 w = make_uint4(0, 0, 0, 0);
+      if (sample && a0 < a.A) w = philox10(make_uint4(id, (uint32_t)c.e, (uint32_t)(a0 >> 2), 0u), a.seed_lo, a.seed_hi);
+      const uint32_t wv[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int act = a0 + i;
+        const float z = acc[T][i];
+        if (act == a.A) val = z;
+        if (act < a.A && ((c.amask >> act) & 1ull)) {
+          const float ex = __expf(z - best);
+          sm += ex;
+          sz += ex * z;
+          const float sc = sample ? __fdividef(ex, expo_of(wv[i])) : z;
+          if (bsa < 0 || sc > bs) { bs = sc; bsa = act; bz = z; }   // actions ascend: ties keep the lowest
+        }
+      }
+    }
+#pragma unroll
+    for (int off = 16; off <= 32; off *= 2) {
+      sm += __shfl_xor(sm, off, 64);
+      sz += __shfl_xor(sz, off, 64);
+      val += __shfl_xor(val, off, 64);             // one lane of the row holds row A
+      const float obs = __shfl_xor(bs, off, 64), obz = __shfl_xor(bz, off, 64);
+      const int obsa = __shfl_xor(bsa, off, 64);
+      if (obsa >= 0 && (bsa < 0 || obs > bs || (obs == bs && obsa < bsa))) { bs = obs; bsa = obsa; bz = obz; }
+    }
+    if (c.live && q == 0) {
+      const bool any = ba >= 0 && !c.bad;
+      const float lse = any ? best + __logf(sm) : 0.f;
+      a.actions[c.r] = any ? bsa : -1;
+      if (c.bad) atomicOr(a.err, c.bad);
+      if (a.logp) a.logp[c.r] = any ? bz - lse : 0.f;
+      if (a.entropy) a.entropy[c.r] = any ? lse - sz / sm : 0.f;
+      if (a.value) a.value[c.r] = c.bad ? 0.f : val;
+    }
+  } else if (c.live && q == 0) {
+    a.actions[c.r] = c.bad ? -1 : ba;
+    if (c.bad) atomicOr(a.err, c.bad);
+  }
+  if (!c.live) return;
+  if (a.logits) {
+    float* out = a.logits + (size_t)c.r * a.A;
+#pragma unroll
+    for (int T = 0; T < AT; ++T) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int act = 16 * T + 4 * q + r;
+        if (act < a.A) out[act] = c.bad ? 0.f : acc[T][r];
+      }
+    }
+  }
+}
+
+// One hidden-input layer: out[To] = bias + W h over K = 4 KG steps, the
+// weights of step group (To, g) at W[(To KG + g) 64 + lane] (4 floats, one
+// per K step of the group). With one wave per SIMD the MFMAs are ordered so
+// that consecutive ones never share an accumulator: four output tiles at a
+// time (weights of D groups in flight), or, for fewer than four tiles, each
+// tile's K steps split over four partial sums added at the end.
+template <int TO, int KG, int D>
+__device__ __forceinline__ void layer16(const f32x4* W, const float* bias, const f32x4 (&h)[KG], int lane,
+                                        int q, f32x4 (&out)[TO]) {
+  if constexpr (TO % 4 == 0) {
+    constexpr int N = (TO / 4) * KG;   // (tile quad, group) steps
+    constexpr int DD = D < N ? D : N;
+    f32x4 wr[DD][4];
+    auto load = [&](int s, f32x4 (&w)[4]) {
+      const int T4 = s / KG, g = s % KG;
+#pragma unroll
+      for (int t = 0; t < 4; ++t) w[t] = W[((4 * T4 + t) * KG + g) * 64 + lane];
+    };
+#pragma unroll
+    for (int s = 0; s < DD; ++s) load(s, wr[s]);
+#pragma unroll
+    for (int T4 = 0; T4 < TO / 4; ++T4) {
+      f32x4 acc[4];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) acc[t] = *(const f32x4*)(bias + ((4 * T4 + t) * 4 + q) * 4);
+#pragma unroll
+      for (int g = 0; g < KG; ++g) {
+        const int st = T4 * KG + g;
+        f32x4 w[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) w[t] = wr[st % DD][t];
+        if (st + DD < N) load(st + DD, wr[st % DD]);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) acc[t] = mfma16_f32(w[t].x, h[g].x, acc[t]);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) acc[t] = mfma16_f32(w[t].y, h[g].y, acc[t]);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) acc[t] = mfma16_f32(w[t].z, h[g].z, acc[t]);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) acc[t] = mfma16_f32(w[t].w, h[g].w, acc[t]);
+      }
+#pragma unroll
+      for (int t = 0; t < 4; ++t) out[4 * T4 + t] = acc[t];
+    }
+  } else {
+    constexpr int N = TO * KG;
+    constexpr int DD = 4 * D < N ? 4 * D : N;
+    f32x4 wr[DD];
+#pragma unroll
+    for (int t = 0; t < DD; ++t) wr[t] = W[t * 64 + lane];
+#pragma unroll
+    for (int To = 0; To < TO; ++To) {
+      f32x4 p[4];
+      p[0] = *(const f32x4*)(bias + (To * 4 + q) * 4);
+      p[1] = p[2] = p[3] = f32x4{};
+#pragma unroll
+      for (int g = 0; g < KG; ++g) {
+        const int t = To * KG + g;
+        const f32x4 w = wr[t % DD];
+        if (t + DD < N) wr[t % DD] = W[(t + DD) * 64 + lane];
+        p[0] = mfma16_f32(w.x, h[g].x, p[0]);
+        p[1] = mfma16_f32(w.y, h[g].y, p[1]);
+        p[2] = mfma16_f32(w.z, h[g].z, p[2]);
+        p[3] = mfma16_f32(w.w, h[g].w, p[3]);
+      }
+      out[To] = (p[0] + p[1]) + (p[2] + p[3]);
+    }
+  }
+}
+
 template <int H, int NL, int AT>
 __global__ __launch_bounds__(256) void route_f32(RouteArgs a_in) {
   // chain pools: the tick's row count is on the device
   RouteArgs a = a_in;
   if (a_in.n_total_dev) a.n_total = *a_in.n_total_dev;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int n = lane & 31, g = lane >> 5;
-  const int32_t row0 = (int32_t)(blockIdx.x * 4 + wave) * 32;
+  const int n = lane & 15, q = lane >> 4;
+  const int32_t row0 = (int32_t)(blockIdx.x * 4 + wave) * 16;
   if (row0 >= a.n_total) return;
-  const RowCtx c = row_setup(a, row0, row0 + n);
-  constexpr int TH = H / 32;
-  constexpr int KH = H / 2;         // 2-wide K steps over a hidden layer
-  const float* W1 = (const float*)a.W[0];
-  const float* emb = (const float*)a.emb;
-  f32x16 acc[TH];
+  const int32_t rl = row0 + 15 < a.n_total ? row0 + 15 : a.n_total - 1;
+  const int32_t rows[1] = {row0 + n};
+  const int32_t rsel[1] = {rows[0] < a.n_total ? rows[0] : a.n_total - 1};
+  int32_t envs[1];
+  find_envs<1>(a, row0, rl, rsel, envs);
+  const RowCtx c = row_setup_env(a, rows[0], envs[0]);
+  constexpr int TH = H / 16;   // hidden output tiles
+  constexpr int KGH = H / 16;  // K step groups over a hidden layer (4 steps of 4 features)
+  const f32x4* W1 = (const f32x4*)a.W[0];
+  const float* emb = (const float*)a.emb + (size_t)c.q * a.embed_dim;
+  // layer 1: K step s, lane group q carries feature 4 s + q; four steps per group
+  const int KG1 = (a.k1 + 3) / 4;
+  f32x4 h1[TH];
 #pragma unroll
-  for (int T = 0; T < TH; ++T) acc[T] = f32x16{};
-  for (int i = 0; i < a.k1; ++i) {
-    const int k = 2 * i + g;
-    const float x = k < a.embed_dim ? emb[(size_t)c.q * a.embed_dim + k]
-                                    : tail_feature(a, c, k);
+  for (int T = 0; T < TH; ++T) h1[T] = *(const f32x4*)(a.bias[0] + (T * 4 + q) * 4);
+  auto feats = [&](int g) {
+    f32x4 x;
 #pragma unroll
-    for (int T = 0; T < TH; ++T) acc[T] = mfma_f32(W1[(T * a.k1 + i) * 64 + lane], x, acc[T]);
+    for (int j = 0; j < 4; ++j) {
+      const int k = 16 * g + 4 * j + q;
+      x[j] = k < a.embed_dim ? emb[k] : tail_feature(a, c, k);
+    }
+    return x;
+  };
+  f32x4 x = feats(0);
+  f32x4 wn[TH];
+#pragma unroll
+  for (int T = 0; T < TH; ++T) wn[T] = W1[(T * KG1) * 64 + lane];
+  for (int g = 0; g < KG1; ++g) {
+    f32x4 wc[TH];
+#pragma unroll
+    for (int T = 0; T < TH; ++T) wc[T] = wn[T];
+    const f32x4 xc = x;
+    if (g + 1 < KG1) {
+      x = feats(g + 1);
+#pragma unroll
+      for (int T = 0; T < TH; ++T) wn[T] = W1[(T * KG1 + g + 1) * 64 + lane];
+    }
+    // K step by K step across the output tiles: consecutive MFMAs never
+    // share an accumulator
+#pragma unroll
+    for (int T = 0; T < TH; ++T) h1[T] = mfma16_f32(wc[T].x, xc.x, h1[T]);
+#pragma unroll
+    for (int T = 0; T < TH; ++T) h1[T] = mfma16_f32(wc[T].y, xc.y, h1[T]);
+#pragma unroll
+    for (int T = 0; T < TH; ++T) h1[T] = mfma16_f32(wc[T].z, xc.z, h1[T]);
+#pragma unroll
+    for (int T = 0; T < TH; ++T) h1[T] = mfma16_f32(wc[T].w, xc.w, h1[T]);
   }
 #pragma unroll
-  for (int T = 0; T < TH; ++T) {
+  for (int T = 0; T < TH; ++T)
 #pragma unroll
-    for (int v = 0; v < 16; ++v) acc[T][v] = relu(acc[T][v] + a.bias[0][(T * 2 + g) * 16 + v]);
-  }
-  f32x16 out[AT];
-#pragma unroll
-  for (int T = 0; T < AT; ++T) out[T] = f32x16{};
+    for (int r = 0; r < 4; ++r) h1[T][r] = relu(h1[T][r]);
+  f32x4 out[AT];
   if constexpr (NL == 2) {
-    const float* W2 = (const float*)a.W[1];
-#pragma unroll
-    for (int i = 0; i < KH; ++i) {
-#pragma unroll
-      for (int T = 0; T < AT; ++T)
-        out[T] = mfma_f32(W2[(T * KH + i) * 64 + lane], acc[i >> 4][i & 15], out[T]);
-    }
-    epilogue<AT>(a, c, out, a.bias[1], g);
+    layer16<AT, KGH, 2>((const f32x4*)a.W[1], a.bias[1], h1, lane, q, out);
   } else {
-    constexpr int CH = H < 128 ? H : 128;
-    constexpr int TC = CH / 32;
-    const float* W2 = (const float*)a.W[1];
-    const float* W3 = (const float*)a.W[2];
-    for (int cc = 0; cc < H / CH; ++cc) {
-      f32x16 acc2[TC];
+    f32x4 h2[TH];
+    layer16<TH, KGH, 2>((const f32x4*)a.W[1], a.bias[1], h1, lane, q, h2);
 #pragma unroll
-      for (int T = 0; T < TC; ++T) acc2[T] = f32x16{};
+    for (int T = 0; T < TH; ++T)
 #pragma unroll
-      for (int i = 0; i < KH; ++i) {
-#pragma unroll
-        for (int T = 0; T < TC; ++T)
-          acc2[T] = mfma_f32(W2[((cc * TC + T) * KH + i) * 64 + lane], acc[i >> 4][i & 15], acc2[T]);
-      }
-#pragma unroll
-      for (int T = 0; T < TC; ++T) {
-        const int Tg = cc * TC + T;
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const float h = relu(acc2[T][v] + a.bias[1][(Tg * 2 + g) * 16 + v]);
-          const int i3 = 16 * Tg + v;
-#pragma unroll
-          for (int To = 0; To < AT; ++To)
-            out[To] = mfma_f32(W3[(To * KH + i3) * 64 + lane], h, out[To]);
-        }
-      }
-    }
-    epilogue<AT>(a, c, out, a.bias[2], g);
+      for (int r = 0; r < 4; ++r) h2[T][r] = relu(h2[T][r]);
+    layer16<AT, KGH, 2>((const f32x4*)a.W[2], a.bias[2], h2, lane, q, out);
   }
+  epilogue16<AT>(a, c, out, q);
 }
 
 // ---------------------------------------------------------------------------
@@ -564,34 +771,6 @@ __global__ __launch_bounds__(256) void route_f32(RouteArgs a_in) {
 // so every weight fragment read feeds NR MFMAs. Layer-1 outputs are produced
 // one 32-feature tile at a time and rounded to bf16 fragments right away.
 // ---------------------------------------------------------------------------
-
-// Row context of row r in env e from its already loaded record fields.
-__device__ __forceinline__ RowCtx row_ctx_from(const RouteArgs& a, int32_t r, int32_t e, int32_t q,
-                                               int32_t budget) {
-  RowCtx c;
-  c.r = r;
-  c.live = r < a.n_total;
-  c.e = e;
-  c.bad = (q < 0 || (int64_t)q >= a.Q) ? IM_ERR_QIDX : 0;
-  c.q = c.bad ? 0 : q;
-  c.budget = budget;
-  c.amask = action_mask(a, e);
-  return c;
-}
-
-__device__ __forceinline__ RowCtx row_setup_env(const RouteArgs& a, int32_t r, int32_t e) {
-  RowCtx c;
-  c.r = r;
-  c.live = r < a.n_total;
-  const int32_t rr = c.live ? r : a.n_total - 1;
-  c.e = e;
-  const int32_t q = a.q_idx[rr];
-  c.bad = (q < 0 || (int64_t)q >= a.Q) ? IM_ERR_QIDX : 0;
-  c.q = c.bad ? 0 : q;
-  c.budget = a.budget[rr];
-  c.amask = action_mask(a, e);
-  return c;
-}
 
 // Copies n 16-byte words from global memory to LDS with `nthreads` threads,
 // batches of 8 loads in flight per thread.
@@ -1260,7 +1439,9 @@ RouteKernel pick_bf16(int at) {
 }
 template <int H, int NL>
 RouteKernel pick_f32(int at) {
-  return at == 1 ? route_f32<H, NL, 1> : (at == 2 ? route_f32<H, NL, 2> : route_f32<H, NL, 3>);
+  // at: output tiles of 16 (fp32 pools)
+  return at == 1 ? route_f32<H, NL, 1>
+                 : (at == 2 ? route_f32<H, NL, 2> : (at == 3 ? route_f32<H, NL, 3> : route_f32<H, NL, 4>));
 }
 
 template <int NL>
@@ -1369,8 +1550,9 @@ hipError_t launch_role_projection(const uint16_t* w_role, const uint16_t* roles,
   return hipGetLastError();
 }
 
+// out_tiles: output tiles of the last layer, 32 rows (bf16) or 16 rows (fp32).
 bool route_supported(int dtype, int hidden, int n_layers, int out_tiles) {
-  if (out_tiles < 1 || out_tiles > 3) return false;
+  if (out_tiles < 1 || out_tiles > (dtype == IM_F32 ? 4 : 3)) return false;
   RouteKernel k = n_layers == 2 ? pick<2>(dtype, hidden, out_tiles)
                  : n_layers == 3 ? pick<3>(dtype, hidden, out_tiles) : nullptr;
   return k != nullptr;
@@ -1403,13 +1585,15 @@ hipError_t launch_route(const RouteArgs& a, int dtype, int hidden, int n_layers,
     }
   }
   RouteKernel k = nullptr;
-  if (out_tiles >= 1 && out_tiles <= 3) {
+  if (route_supported(dtype, hidden, n_layers, out_tiles)) {
     if (n_layers == 2) k = pick<2>(dtype, hidden, out_tiles);
     else if (n_layers == 3) k = pick<3>(dtype, hidden, out_tiles);
   }
   if (!k) return hipErrorInvalidValue;
   if (a.n_total <= 0) return hipSuccess;
-  const unsigned blocks = (unsigned)((a.n_total + 127) / 128);
+  // blocks of 4 waves: 32 rows per wave (bf16) or 16 (fp32)
+  const int rows = dtype == IM_F32 ? 64 : 128;
+  const unsigned blocks = (unsigned)((a.n_total + rows - 1) / rows);
   hipLaunchKernelGGL(k, dim3(blocks), dim3(256), 0, s, a);
   return hipGetLastError();
 }
