@@ -1011,6 +1011,21 @@ __device__ __forceinline__ void dma_frag(u32x4* dst, const u32x4* src, int lane)
                                    (__attribute__((address_space(3))) void*)dst, 16, 0, 0);
 }
 
+// 16 floats from LDS as four 16-byte reads (each keeps the LDS variable's
+// alias information, which a single 64-byte access loses when it is split).
+__device__ __forceinline__ f32x16 lds_f32x16(const u32x4* p) {
+  const u32x4 v0 = p[0], v1 = p[1], v2 = p[2], v3 = p[3];
+  f32x16 r;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    r[i] = __uint_as_float(v0[i]);
+    r[4 + i] = __uint_as_float(v1[i]);
+    r[8 + i] = __uint_as_float(v2[i]);
+    r[12 + i] = __uint_as_float(v3[i]);
+  }
+  return r;
+}
+
 template <int H, int AT, int KB1, int ED, int NW, int RL>
 __global__ __launch_bounds__(NW * 64, 1) void route_bf16_stream(RouteArgs a_in) {
   // chain pools: the tick's row count is on the device
@@ -1025,8 +1040,14 @@ __global__ __launch_bounds__(NW * 64, 1) void route_bf16_stream(RouteArgs a_in) 
   constexpr int NB0 = TH * 32, NB1 = TH * 32, NB2 = AT * 32;
   static_assert(NST % 2 == 0, "stage parity must repeat every block step");
   static_assert(KH % NW == 0 && 2 * AT <= NW, "layer-2 stage split over the waves");
-  __shared__ u32x4 ring[2][FS * 64];
-  __shared__ float lbias[NB0 + NB1 + NB2];
+  // Two separately declared buffers, each with its own copy of the biases
+  // behind the weight fragments: a stage reads only the buffer the copy in
+  // flight does not target, which the compiler can then tell apart (with one
+  // array it waits for the next stage's copy before every read).
+  constexpr int NBW = (NB0 + NB1 + NB2) / 4;   // biases in 16-byte words
+  static_assert((NB0 + NB1 + NB2) % 4 == 0, "bias rows move in 16-byte words");
+  __shared__ u32x4 ring0[FS * 64 + NBW];
+  __shared__ u32x4 ring1[FS * 64 + NBW];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int g = lane >> 5;
   const u32x4* W1 = (const u32x4*)a.W[0];
@@ -1037,7 +1058,7 @@ __global__ __launch_bounds__(NW * 64, 1) void route_bf16_stream(RouteArgs a_in) 
   // stage's last one again (the same bytes to the same place), so the code
   // has no branches.
   auto issue = [&](int st, int b, int wv, int ln) {
-    u32x4* dst = ring[b];
+    u32x4* dst = b ? ring1 : ring0;
     if (st < S1) {
 #pragma unroll
       for (int i = 0; i < (F1 + NW - 1) / NW; ++i) {
@@ -1055,8 +1076,11 @@ __global__ __launch_bounds__(NW * 64, 1) void route_bf16_stream(RouteArgs a_in) 
       dma_frag(dst + (KH + f3) * 64, W3 + ((f3 >> 1) * KH + 2 * j + (f3 & 1)) * 64, ln);
     }
   };
-  for (int i = threadIdx.x; i < NB0 + NB1 + NB2; i += NW * 64)
-    lbias[i] = i < NB0 ? a.bias[0][i] : (i < NB0 + NB1 ? a.bias[1][i - NB0] : a.bias[2][i - NB0 - NB1]);
+  for (int i = threadIdx.x; i < NB0 + NB1 + NB2; i += NW * 64) {
+    const float v = i < NB0 ? a.bias[0][i] : (i < NB0 + NB1 ? a.bias[1][i - NB0] : a.bias[2][i - NB0 - NB1]);
+    ((float*)(ring0 + FS * 64))[i] = v;
+    ((float*)(ring1 + FS * 64))[i] = v;
+  }
   issue(0, 0, __builtin_amdgcn_readfirstlane(wave), lane);
   // The block takes an equal contiguous share of the 32-row wave tiles (the
   // shares differ by at most one), NW per block step; in its last step the
@@ -1103,7 +1127,7 @@ __global__ __launch_bounds__(NW * 64, 1) void route_bf16_stream(RouteArgs a_in) 
     f32x16 z[AT];
 #pragma unroll
     for (int s = 0; s < NST; ++s) {
-      // stage s is in ring[s & 1]; every wave is done with ring[(s + 1) & 1]
+      // stage s is in buffer s & 1; every wave is done with buffer (s + 1) & 1
       __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();
       {
@@ -1112,7 +1136,8 @@ __global__ __launch_bounds__(NW * 64, 1) void route_bf16_stream(RouteArgs a_in) 
         asm volatile("" : "+v"(lns));
         issue(s + 1 < NST ? s + 1 : 0, (s + 1) & 1, wv, lns);
       }
-      const u32x4* wb = ring[s & 1];
+      const u32x4* wb = (s & 1) ? ring1 : ring0;
+      const u32x4* lb4 = wb + FS * 64;   // biases, 4 floats per word
       if (s < S1) {
         // fragment q = t * KB1 + kb, two LDS reads ahead of its MFMA
         u32x4 w_0 = wb[0 * 64 + ln];
@@ -1120,7 +1145,7 @@ __global__ __launch_bounds__(NW * 64, 1) void route_bf16_stream(RouteArgs a_in) 
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
           const int T = 2 * s + t;
-          f32x16 p = *(const f32x16*)(lbias + (T * 2 + gg) * 16);
+          f32x16 p = lds_f32x16(lb4 + (T * 2 + gg) * 4);
 #pragma unroll
           for (int kb = 0; kb < KB1; ++kb) {
             const int q = t * KB1 + kb;
@@ -1134,11 +1159,11 @@ __global__ __launch_bounds__(NW * 64, 1) void route_bf16_stream(RouteArgs a_in) 
         }
         if (s == S1 - 1) {
 #pragma unroll
-          for (int To = 0; To < AT; ++To) z[To] = *(const f32x16*)(lbias + NB0 + NB1 + (To * 2 + gg) * 16);
+          for (int To = 0; To < AT; ++To) z[To] = lds_f32x16(lb4 + (NB0 + NB1) / 4 + (To * 2 + gg) * 4);
         }
       } else {
         const int j = s - S1;
-        f32x16 p = *(const f32x16*)(lbias + NB0 + (j * 2 + gg) * 16);
+        f32x16 p = lds_f32x16(lb4 + NB0 / 4 + (j * 2 + gg) * 4);
         u32x4 w_0 = wb[0 * 64 + ln];
         u32x4 w_1 = wb[1 * 64 + ln];
 #pragma unroll
