@@ -762,6 +762,142 @@ __global__ __launch_bounds__(256) void route_f32(RouteArgs a_in) {
   epilogue16<AT>(a, c, out, q);
 }
 
+// TQ output tiles [To0, To0 + TQ) of a layer over its hidden input, read from
+// LDS (`hs`: tile g's 16-byte words at hs[g 64 + lane]) while the weights
+// (W[(To KG + g) 64 + lane], 4 floats) come through the caches D groups
+// ahead. Consecutive MFMAs use different accumulators: the tiles' own chains
+// when there are four or more, else four partial sums per tile.
+template <int TQ, int KG, int D>
+__device__ __forceinline__ void layer16_lds(const f32x4* W, const float* bias, const f32x4* hs, int To0,
+                                            int lane, int q, f32x4 (&out)[TQ]) {
+  constexpr int NP = TQ >= 4 ? 1 : 4;
+  constexpr int DD = D < KG ? D : KG;
+  f32x4 wr[DD][TQ];
+#pragma unroll
+  for (int g = 0; g < DD; ++g)
+#pragma unroll
+    for (int t = 0; t < TQ; ++t) wr[g][t] = W[((To0 + t) * KG + g) * 64 + lane];
+  f32x4 acc[TQ][NP];
+#pragma unroll
+  for (int t = 0; t < TQ; ++t) {
+    acc[t][0] = *(const f32x4*)(bias + ((To0 + t) * 4 + q) * 4);
+#pragma unroll
+    for (int i = 1; i < NP; ++i) acc[t][i] = f32x4{};
+  }
+  f32x4 bn = hs[lane];
+#pragma unroll
+  for (int g = 0; g < KG; ++g) {
+    const f32x4 b = bn;
+    if (g + 1 < KG) bn = hs[(g + 1) * 64 + lane];
+    f32x4 w[TQ];
+#pragma unroll
+    for (int t = 0; t < TQ; ++t) w[t] = wr[g % DD][t];
+    if (g + DD < KG) {
+#pragma unroll
+      for (int t = 0; t < TQ; ++t) wr[g % DD][t] = W[((To0 + t) * KG + g + DD) * 64 + lane];
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int t = 0; t < TQ; ++t) acc[t][j % NP] = mfma16_f32(w[t][j], b[j], acc[t][j % NP]);
+  }
+#pragma unroll
+  for (int t = 0; t < TQ; ++t) {
+    f32x4 r = acc[t][0];
+#pragma unroll
+    for (int i = 1; i < NP; ++i) r += acc[t][i];
+    out[t] = r;
+  }
+}
+
+// fp32 policies with hidden widths in whole tile quads, feature-split: one
+// block of 4 waves per 16-row tile, wave w computing output tiles
+// [w TH/4, (w + 1) TH/4) of each hidden layer; the block exchanges a layer's
+// activations through LDS (one 16-row x H buffer, h1 and then h2), and wave 0
+// computes the output layer and the epilogue. Each wave does about a quarter
+// of a tile's MFMAs, so four waves share each SIMD and hide each other's
+// latencies, and a tick slightly above a multiple of the machine's SIMDs
+// adds quarter tiles rather than whole ones.
+template <int H, int NL, int AT>
+__global__ __launch_bounds__(256) void route_f32s(RouteArgs a_in) {
+  // chain pools: the tick's row count is on the device
+  RouteArgs a = a_in;
+  if (a_in.n_total_dev) a.n_total = *a_in.n_total_dev;
+  constexpr int TH = H / 16, TQ = TH / 4, KGH = H / 16;
+  static_assert(TH % 4 == 0, "hidden tiles split four ways");
+  __shared__ f32x4 hs[TH * 64];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int n = lane & 15, q = lane >> 4;
+  const int32_t row0 = (int32_t)blockIdx.x * 16;
+  if (row0 >= a.n_total) return;   // the whole block (chain pools' bound launch)
+  const int32_t rl = row0 + 15 < a.n_total ? row0 + 15 : a.n_total - 1;
+  const int32_t rows[1] = {row0 + n};
+  const int32_t rsel[1] = {rows[0] < a.n_total ? rows[0] : a.n_total - 1};
+  int32_t envs[1];
+  find_envs<1>(a, row0, rl, rsel, envs);
+  const RowCtx c = row_setup_env(a, rows[0], envs[0]);
+  const int T0 = wave * TQ;
+  // layer 1 (this wave's tiles): K step s, lane group q carries feature 4 s + q
+  const f32x4* W1 = (const f32x4*)a.W[0];
+  const float* emb = (const float*)a.emb + (size_t)c.q * a.embed_dim;
+  const int KG1 = (a.k1 + 3) / 4;
+  f32x4 h1[TQ];
+#pragma unroll
+  for (int t = 0; t < TQ; ++t) h1[t] = *(const f32x4*)(a.bias[0] + ((T0 + t) * 4 + q) * 4);
+  auto feats = [&](int g) {
+    f32x4 x;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int k = 16 * g + 4 * j + q;
+      x[j] = k < a.embed_dim ? emb[k] : tail_feature(a, c, k);
+    }
+    return x;
+  };
+  f32x4 x = feats(0);
+  f32x4 wn[TQ];
+#pragma unroll
+  for (int t = 0; t < TQ; ++t) wn[t] = W1[((T0 + t) * KG1) * 64 + lane];
+  for (int g = 0; g < KG1; ++g) {
+    f32x4 wc[TQ];
+#pragma unroll
+    for (int t = 0; t < TQ; ++t) wc[t] = wn[t];
+    const f32x4 xc = x;
+    if (g + 1 < KG1) {
+      x = feats(g + 1);
+#pragma unroll
+      for (int t = 0; t < TQ; ++t) wn[t] = W1[((T0 + t) * KG1 + g + 1) * 64 + lane];
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int t = 0; t < TQ; ++t) h1[t] = mfma16_f32(wc[t][j], xc[j], h1[t]);
+  }
+#pragma unroll
+  for (int t = 0; t < TQ; ++t) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) h1[t][r] = relu(h1[t][r]);
+    hs[(T0 + t) * 64 + lane] = h1[t];
+  }
+  __syncthreads();
+  if constexpr (NL == 3) {
+    f32x4 h2[TQ];
+    layer16_lds<TQ, KGH, 2>((const f32x4*)a.W[1], a.bias[1], hs, T0, lane, q, h2);
+    __syncthreads();   // every wave is done reading h1
+#pragma unroll
+    for (int t = 0; t < TQ; ++t) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) h2[t][r] = relu(h2[t][r]);
+      hs[(T0 + t) * 64 + lane] = h2[t];
+    }
+    __syncthreads();
+  }
+  if (wave != 0) return;
+  f32x4 out[AT];
+  layer16_lds<AT, KGH, 2>((const f32x4*)a.W[NL - 1], a.bias[NL - 1], hs, 0, lane, q, out);
+  epilogue16<AT>(a, c, out, q);
+}
+
 // ---------------------------------------------------------------------------
 // Persistent variant for policies whose deeper layers fit in LDS.
 //
@@ -1464,7 +1600,11 @@ RouteKernel pick_bf16(int at) {
 }
 template <int H, int NL>
 RouteKernel pick_f32(int at) {
-  // at: output tiles of 16 (fp32 pools)
+  // at: output tiles of 16 (fp32 pools); feature-split kernel when the hidden
+  // tiles split four ways
+  if constexpr ((H / 16) % 4 == 0)
+    return at == 1 ? route_f32s<H, NL, 1>
+                   : (at == 2 ? route_f32s<H, NL, 2> : (at == 3 ? route_f32s<H, NL, 3> : route_f32s<H, NL, 4>));
   return at == 1 ? route_f32<H, NL, 1>
                  : (at == 2 ? route_f32<H, NL, 2> : (at == 3 ? route_f32<H, NL, 3> : route_f32<H, NL, 4>));
 }
@@ -1616,8 +1756,9 @@ hipError_t launch_route(const RouteArgs& a, int dtype, int hidden, int n_layers,
   }
   if (!k) return hipErrorInvalidValue;
   if (a.n_total <= 0) return hipSuccess;
-  // blocks of 4 waves: 32 rows per wave (bf16) or 16 (fp32)
-  const int rows = dtype == IM_F32 ? 64 : 128;
+  // blocks of 4 waves: 32 rows per wave (bf16), 16 rows per wave (fp32,
+  // hidden width 32) or 16 rows per block (fp32, feature-split)
+  const int rows = dtype == IM_F32 ? (hidden % 64 == 0 ? 16 : 64) : 128;
   const unsigned blocks = (unsigned)((a.n_total + rows - 1) / rows);
   hipLaunchKernelGGL(k, dim3(blocks), dim3(256), 0, s, a);
   return hipGetLastError();
