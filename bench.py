@@ -62,6 +62,21 @@ def algorithmic_flops_per_tick(cfg, n_requests):
     return per_req * n_requests + per_env * cfg["E"]
 
 
+def algorithmic_bytes_route(cfg, n_requests, sample=False):
+    """Bytes the route step must move: per request its record (q_idx 4 B,
+    budget 2 B, role 2 B for the dual-pathway executor), its embedding row
+    and its action (4 B; log-prob, entropy and value 4 B each for an RL
+    rollout); per env its snapshot row (4M fp32 statistics and M validity
+    bytes)."""
+    s = 2 if cfg["dtype"] == "bf16" else 4
+    per_req = 4 + 2 + cfg["embed_dim"] * s + 4
+    if cfg.get("net") == "dual":
+        per_req += 2
+    if sample:
+        per_req += 12
+    return per_req * n_requests + (16 * cfg["M"] + cfg["M"]) * cfg["E"]
+
+
 def algorithmic_bytes_schedule(cfg, n_requests, n_enqueued, n_started):
     """Bytes the schedule step must move: per request its record (budget,
     base_svc, action = 8 B); 16 B per queue entry written at enqueue and read
@@ -343,13 +358,23 @@ def main():
     peak_f = PEAK_BF16_TFLOPS if cfg["dtype"] == "bf16" else PEAK_F32_TFLOPS
     tag = f"{args.config}_lam{int(cfg['lam'])}" + ("_sample" if args.sample else "")
     if route_avg >= sched_avg:
-        achieved = flops / (route_avg * 1e-3) / 1e12
-        roof = {"kernel": ("route_sample_" if args.sample else "route_") + cfg["dtype"],
-                "bound": "mfma", "achieved": achieved,
-                "peak": peak_f, "unit": "TFLOP/s", "frac": achieved / peak_f,
-                "traffic": load_traffic("route", tag, source_hash("route.hip")),
-                "avg_launch_us": route_avg * 1e3,
-                "algorithmic_per_launch": f"{flops:.4g} FLOP"}
+        # the binding roof of the route step: the larger of its matrix time
+        # and its HBM time at nominal peaks
+        rbytes = np.mean([algorithmic_bytes_route(cfg, n, args.sample) for n in n_req[W_:W_ + K]])
+        kname = ("route_sample_" if args.sample else "route_") + cfg["dtype"]
+        traffic = load_traffic("route", tag, source_hash("route.hip"))
+        if flops / (peak_f * 1e12) >= rbytes / (PEAK_HBM_GBS * 1e9):
+            achieved = flops / (route_avg * 1e-3) / 1e12
+            roof = {"kernel": kname, "bound": "mfma", "achieved": achieved,
+                    "peak": peak_f, "unit": "TFLOP/s", "frac": achieved / peak_f,
+                    "traffic": traffic, "avg_launch_us": route_avg * 1e3,
+                    "algorithmic_per_launch": f"{flops:.4g} FLOP"}
+        else:
+            achieved = rbytes / (route_avg * 1e-3) / 1e9
+            roof = {"kernel": kname, "bound": "hbm", "achieved": achieved,
+                    "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS,
+                    "traffic": traffic, "avg_launch_us": route_avg * 1e3,
+                    "algorithmic_per_launch": f"{rbytes:.4g} B ({flops:.4g} FLOP)"}
     else:
         enq = int(st["enqueued"].sum())
         sta = int(st["started"].sum())
