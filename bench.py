@@ -326,6 +326,19 @@ def main():
     pool2 = P.Pool(cfg, W, b, emb_dev, cap, lb)
     warm(pool2)
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
+    if chains:
+        # The rows a chain tick routes (its pending calls and its arrivals) are
+        # counted on the device: each tick's count is copied on the stream, after
+        # the tick's last event, into a slot of its own and read once after the
+        # pass. A host read per tick would drain the stream and put the next
+        # tick's launch latency inside its route interval.
+        import ctypes
+        hip = ctypes.CDLL("libamdhip64.so")
+        hip.hipMemcpyAsync.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int,
+                                       ctypes.c_void_p]
+        hip.hipMemcpyAsync.restype = ctypes.c_int
+        n_rows_dev = P.im_get_rows(pool2.h).n_rows
+        row_counts = torch.zeros(K, dtype=torch.int32, device="cuda")
     torch.cuda.synchronize()
     for k in range(K):
         t = W_ + k
@@ -338,9 +351,13 @@ def main():
         pool2.schedule(dev[t], acts, stream.cuda_stream)
         ev[k][2].record(stream)
         if chains:
-            # the rows this tick routed: its pending calls and its arrivals
-            n_req[t] = pool2.rows()[1]
+            rc = hip.hipMemcpyAsync(row_counts.data_ptr() + 4 * k, n_rows_dev, 4, 3,   # device to device
+                                    stream.cuda_stream)
+            assert rc == 0, f"hipMemcpyAsync failed ({rc})"
     torch.cuda.synchronize()
+    if chains:
+        for k, n in enumerate(row_counts.cpu().numpy()):
+            n_req[W_ + k] = int(n)
     route_ms = [ev[k][0].elapsed_time(ev[k][1]) for k in range(K)]
     sched_ms = [ev[k][1].elapsed_time(ev[k][2]) for k in range(K)]
     assert pool2.error() == 0, "device error during the instrumented pass"
@@ -361,7 +378,7 @@ def main():
         # the binding roof of the route step: the larger of its matrix time
         # and its HBM time at nominal peaks
         rbytes = np.mean([algorithmic_bytes_route(cfg, n, args.sample) for n in n_req[W_:W_ + K]])
-        kname = ("route_sample_" if args.sample else "route_") + cfg["dtype"]
+        kname = ("route_sample_" if args.sample else "route_dual_" if cfg.get("net") == "dual" else "route_") + cfg["dtype"]
         traffic = load_traffic("route", tag, source_hash("route.hip"))
         if flops / (peak_f * 1e12) >= rbytes / (PEAK_HBM_GBS * 1e9):
             achieved = flops / (route_avg * 1e-3) / 1e12
@@ -418,7 +435,10 @@ def main():
                                                         "before the timed region"},
         "routed_req_per_s": routed / (gpu_ms / 1e3),
         "kernels_us": {"route_avg": route_avg * 1e3, "schedule_avg": sched_avg * 1e3,
-                       "note": "HIP events around each launch, separate identical pass",
+                       "note": "HIP events around each launch, separate identical pass" + (
+                           "; chain pools: each interval also holds a build of the tick's rows "
+                           "(im_route and a standalone im_schedule each build them; im_tick once)"
+                           if chains else ""),
                        "host_wall_ms_timed": wall * 1e3},
         "roofline": roof,
         "input_gen_s": gen_s,
