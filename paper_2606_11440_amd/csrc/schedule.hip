@@ -326,21 +326,34 @@ __device__ __forceinline__ int32_t wave_sum32(int32_t v) {
 constexpr int kStageChunks = 4;   // arrival chunks (of 64) staged in LDS per round
 
 // Per-model state of the env, one model per lane (lane m: model m) in
-// registers for the whole tick; read wave-uniformly with readlane.
+// registers for the whole tick.
 struct LaneState {
   int32_t qlen, busy, ewma, backlog, fh, fn, P, busy_mask, next_done;
-  int32_t rcnt;         // blackbox: dispatches in the window (limit and 1 / limit: LDS)
+  int32_t rcnt;         // blackbox: dispatches in the window
+  int32_t fmk, fmi;     // key and id of the front's last entry (its largest)
+  int32_t chg;          // parts of the record that changed (CH_* bits)
 };
+enum { CH_STATS = 1, CH_FRONT = 2, CH_POOL = 4, CH_DONE = 8 };
 
 __device__ __forceinline__ int32_t rl(int32_t v, int m) { return __builtin_amdgcn_readlane(v, m); }
 
-// Inputs of one model fetched ahead of its turn: the live front window
-// (lane i: front[fh + i]) and its slots (lane s < S).
-struct ModelIn {
-  int4 front;
-  int4 slot;
-  int2 fx, sx;   // chain words of the front entry and the slot (chain pools)
+// Per-model words of a wave's LDS scratch (one row of IM_MAX_MODELS each):
+// sums over the lanes that work for a model, added with LDS atomics.
+enum {
+  MW_ACC = 0,    // newcomers admitted this round
+  MW_SVC,        // their service time
+  MW_KF,         // newcomers of the current chunk merged into the front
+  MW_KP,         // newcomers of the current chunk appended to the pool
+  MW_SEG,        // first lane of the model's segment in the current chunk
+  MW_STARTED,    // slots filled this tick
+  MW_WAIT,       // their waiting time
+  MW_SVCOUT,     // their service time
+  MW_DONE,       // completions
+  MW_SLO,        // completions within budget
+  MW_ND,         // earliest completion tick among the busy slots
+  MW_NUM
 };
+enum { MD_LAT = 0, MD_COST, MD_NUM };   // 64-bit sums: latency, Q16 cost
 
 // Adds v to a 64-bit counter without reading it back (a vector atomic whose
 // result is unused: no wait, and integer sums do not depend on the order).
@@ -349,17 +362,29 @@ __device__ __forceinline__ void counter_add(int64_t* p, int64_t v) {
 }
 
 // One wave per env. Every load that does not depend on the arrivals (the
-// model records, one per lane) is issued with the offsets; the env's arrivals
-// are then loaded once (the first kStageChunks chunks stay in registers) and
-// validated. 64 at a time, they are partitioned by model (ballot + mbcnt
-// ranks in id order give the tail-drop admission) and sorted once by (model,
-// key, id) with a 64-lane bitonic network, so each model's newcomers form one
-// sorted segment (a segmented sort), staged in LDS. The models are then
-// processed in order with the next model's front, slots and counters already
-// in flight: merge its segments into the queue, serve its slots, write back.
-// Record and snapshot updates are plain stores of values held in registers;
-// counters and the histogram are added to with atomics whose result is unused
-// (no read-modify-write round trips).
+// model records, one per lane, then each front's largest entry and blackbox
+// window byte) is issued with the offsets; the env's rows are then loaded once
+// (the first chunks stay in registers) and validated. 64 at a time they are
+// partitioned by model (ballot + mbcnt ranks in id order give the tail-drop
+// admission) and sorted once by (model, key, id) with a 64-lane bitonic
+// network, so each model's newcomers form one sorted segment (a segmented
+// sort), staged in LDS.
+//
+// Insertion works on every model of a chunk at once: a lane's newcomer goes
+// to its model's front when it is below the front's largest entry (or the
+// pool is empty and the front has room), else to the pool, whose position
+// follows from a ballot over the lanes of its segment; one scattered store
+// appends every model's pool-bound newcomers. Only models with front-bound
+// newcomers then run a merge network, one model at a time.
+//
+// Service is also model-parallel: lane (model, slot) fills its slot from the
+// model's front (the head entries sit at known positions of the front array),
+// advances it and completes it; per-model sums go through LDS atomics and the
+// EWMA folds the completions in slot order. A model whose front runs dry is
+// refilled from its pool on its own (rare), and its remaining slots then read
+// the new front. Counters are added by lane (model, counter); records and
+// the snapshot row are written once at the end, where they changed.
+//
 // RPM: the pool has (or had) a rate-limited model, so the blackbox dispatch
 // windows are tracked; pools that never had one run without that code.
 // CHAIN: multi-step chains (Sec. 4.3). The env's rows are its pending calls
@@ -369,33 +394,35 @@ __device__ __forceinline__ void counter_add(int64_t* p, int64_t v) {
 // the query's deadline, to the pending list of the next tick.
 template <bool RPM, bool CHAIN>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void schedule_kernel(SchedArgs a) {
+  // sorted chunks; in the service phase the refill scan's key buffer, then
+  // the counter staging
   __shared__ int4 stage[4][kStageChunks * 64];
   __shared__ int2 stage_x[4][CHAIN ? kStageChunks * 64 : 1];
   __shared__ int32_t hist_lds[4][IM_MAX_ACTIONS];
-  __shared__ int32_t svc_lds[4][IM_MAX_MODELS];
-  __shared__ int32_t acc_lds[4][IM_MAX_MODELS];
-  // per-model fields the tick does not change: rpm limit, 1 / limit, capacity, enabled
-  __shared__ int32_t rpm_lds[4][IM_MAX_MODELS];
-  __shared__ float inv_rpm_lds[4][IM_MAX_MODELS];
-  __shared__ int32_t cap_lds[4][IM_MAX_MODELS];
-  __shared__ int32_t en_lds[4][IM_MAX_MODELS];
+  __shared__ int32_t mw_lds[4][MW_NUM][IM_MAX_MODELS];
+  __shared__ unsigned long long md_lds[4][MD_NUM][IM_MAX_MODELS];
   __shared__ int64_t pend_k[4][kFront];   // refill candidate staging
   __shared__ int32_t pend_i[4][kFront];
-  __shared__ int2 pend_kb[4][2 * refill_chunks<CHAIN>() * kFront];   // refill keys and ids, two rounds
+  static_assert(sizeof(int4) * kStageChunks * 64 >= sizeof(int2) * 2 * refill_chunks<CHAIN>() * kFront,
+                "the refill buffer fits the stage");
+  static_assert(kStageChunks * 64 >= (C_NUM / 2) * IM_MAX_MODELS, "the counter staging fits the stage");
+  static_assert(IM_MAX_MODELS < 63, "model 63 marks rows not admitted");
   const int lane = threadIdx.x & 63;
   const int wv = threadIdx.x >> 6;
   const int e = (int)blockIdx.x * 4 + wv;
   if (e >= a.E) return;
   int4* st = stage[wv];
   int32_t* hist_s = hist_lds[wv];
-  int32_t* svc_s = svc_lds[wv];
-  int32_t* acc_s = acc_lds[wv];
+  int32_t(*mw)[IM_MAX_MODELS] = mw_lds[wv];
+  unsigned long long(*md)[IM_MAX_MODELS] = md_lds[wv];
   const int M = a.M, K = a.K, S = a.S;
-  ModelRec* recs = a.ms + (size_t)e * M;
+  const size_t em0 = (size_t)e * M;
+  ModelRec* recs = a.ms + em0;
+  const bool ml = lane < M;   // this lane holds model `lane`
 
   // ---- model records (lane m: model m), issued before anything else ----
   int4 r0 = make_int4(0, 0, 0, 0), r1 = r0, r2 = r0, r3 = r0;
-  if (lane < M) {
+  if (ml) {
     const int4* rp = reinterpret_cast<const int4*>(recs + lane);
     r0 = rp[0];
     r1 = rp[1];
@@ -409,6 +436,18 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
   // device memory, so a captured sequence of ticks replays with the right time.
   const int32_t next_id = rl(r2.y, 0);
   const int32_t t = rl(r2.z, 0);
+  // Each front's largest entry (needed when newcomers arrive while the pool is
+  // not empty or the front is full) and the blackbox window byte leaving at
+  // this tick: in flight while the rows are loaded and sorted.
+  int32_t fmk = 0, fmi = 0, rold_l = 0;
+  if (ml && r1.w > 0 && (r2.x > 0 || r1.w == kFront)) {
+    const int2 f = *reinterpret_cast<const int2*>(a.front + (em0 + lane) * kFront + r1.z + r1.w - 1);
+    fmk = f.x;
+    fmi = f.y;
+  }
+  const int32_t rpm_l = RPM && ml ? r3.y : 0;   // lane m: model m's limit (0: not a blackbox model)
+  const bool track_l = RPM && ml && (rpm_l > 0 || r3.z > 0);
+  if (track_l) rold_l = a.rpm_ring[(em0 + lane) * kRpmRing + (t % kRpmWindow)];
   // chain pools: this tick's pending calls (buffer of parity t) and the next
   // tick's (parity t + 1); the rows' outputs start at roff[e]
   const int4* pend_cur = nullptr;
@@ -494,18 +533,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
   LaneState L;
   L.qlen = r0.x; L.busy = r0.y; L.ewma = r0.z; L.backlog = r0.w;
   L.fh = r1.z; L.fn = r1.w;
-  int32_t* cap_s = cap_lds[wv];
-  int32_t* en_s = en_lds[wv];
-  if (lane < M) { cap_s[lane] = r1.x; en_s[lane] = r1.y; }
   L.P = r2.x; L.busy_mask = r2.w; L.next_done = r3.x;
   L.rcnt = RPM ? r3.z : 0;
-  const int32_t rpm_l = RPM && lane < M ? r3.y : 0;   // lane m: model m's limit (0: not a blackbox model)
-  int32_t* rpm_s = rpm_lds[wv];
-  float* inv_rpm_s = inv_rpm_lds[wv];
-  if (RPM && lane < M) { rpm_s[lane] = r3.y; inv_rpm_s[lane] = __int_as_float(r3.w); }
-  // lane m: which parts of model m's record changed (bit 0: load statistics,
-  // 1: front window, 2: pool size or busy slots, 3: next completion tick)
-  int32_t chg = 0;
+  L.fmk = fmk; L.fmi = fmi;
+  L.chg = 0;
+  const int32_t cap_l = r1.x, en_l = r1.y;
+  const int32_t inv_rpm_bits = RPM ? r3.w : 0;
   if (bad) {
     // The env's state is untouched and time still advances: busy slots keep
     // their remaining service, so their completion ticks move one tick later.
@@ -515,7 +548,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     }
     for (int m = 0; m < M; ++m) {
       if (rl(L.busy_mask, m) == 0) continue;
-      int4* sl = a.slots + (size_t)(e * M + m) * S;
+      int4* sl = a.slots + (em0 + m) * S;
       if (lane < S) {
         int4 v = sl[lane];
         if (v.x >= 0) {
@@ -524,35 +557,35 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         }
       }
     }
-    if (lane < M && L.busy_mask != 0) recs[lane].next_done = L.next_done + 1;
+    if (ml && L.busy_mask != 0) recs[lane].next_done = L.next_done + 1;
     if constexpr (CHAIN) {
       // the env's pending calls stay pending
       for (int i = lane; i < pc; i += 64) pend_nxt[i] = pend_cur[i];
       if (lane == 0) a.pcnt[(size_t)((t + 1) & 1) * a.E + e] = pc;
     }
     // a tracked window still slides: the dispatches of tick t - 60 leave it
-    if (RPM && lane < M && (rpm_l > 0 || L.rcnt > 0)) {
-      uint8_t* rb = a.rpm_ring + ((size_t)e * M + lane) * kRpmRing + (t % kRpmWindow);
-      const int32_t rold = *rb;
-      if (rold != 0) {
-        *rb = 0;
-        recs[lane].rpm_count = L.rcnt - rold;
-        a.snap[(size_t)e * snap_stride(M) + lane] = queue_stat(a, L.qlen, rpm_l, L.rcnt - rold, __int_as_float(r3.w));
-      }
+    if (RPM && track_l && rold_l != 0) {
+      a.rpm_ring[(em0 + lane) * kRpmRing + (t % kRpmWindow)] = 0;
+      recs[lane].rpm_count = L.rcnt - rold_l;
+      a.snap[(size_t)e * snap_stride(M) + lane] = queue_stat(a, L.qlen, rpm_l, L.rcnt - rold_l, __int_as_float(inv_rpm_bits));
     }
     return;
   }
 
   hist_s[lane] = 0;                     // IM_MAX_ACTIONS == 64 lanes
-  if (lane < IM_MAX_MODELS) { svc_s[lane] = 0; acc_s[lane] = 0; }
+  if (lane < IM_MAX_MODELS) {
+    mw[MW_ACC][lane] = 0;
+    mw[MW_SVC][lane] = 0;
+  }
   // lane m < M: room left in model m's queue at the snapshot
-  const int32_t room_l = lane < M ? a.qcap - L.qlen : 0;
+  const int32_t room_l = ml ? a.qcap - L.qlen : 0;
   int32_t prior_l = 0;      // lane m: requests routed to model m so far (id order)
   int32_t acc_l = 0;        // lane m: requests accepted by model m so far
   int32_t nomodel = 0;
   const int n_chunks = (nrows + 63) / 64;
   int32_t pn = 0;            // pending calls spawned for the next tick
   int32_t q_done = 0, q_met = 0;
+  uint64_t wrote = 0;        // models whose front array was written this tick
   int2* stx = stage_x[wv];
   const int rounds = n_chunks > 0 ? (n_chunks + kStageChunks - 1) / kStageChunks : 1;
 
@@ -592,8 +625,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
       const int32_t d = ac - mdl * K;
       const int32_t svc = sv * (d + 1);
       if (acc) {                                     // admitted count and service time per model
-        atomicAdd(&acc_s[mdl], 1);
-        atomicAdd(&svc_s[mdl], svc);
+        atomicAdd(&mw[MW_ACC][mdl], 1);
+        atomicAdd(&mw[MW_SVC][mdl], svc);
       }
       // Sort key (32 bits): model (63 for rows not admitted) | key - t biased by
       // 2^17 | lane. Every row of the chunk enters at t, so ordering by key - t
@@ -615,222 +648,235 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     const bool last = r == rounds - 1;
 
     // lane m: newcomers admitted by model m this round and their service time
-    const int32_t acc_round_l = lane < IM_MAX_MODELS ? acc_s[lane] : 0;
-    const int32_t svc_round_l = lane < IM_MAX_MODELS ? svc_s[lane] : 0;
-    if (lane < IM_MAX_MODELS) { acc_s[lane] = 0; svc_s[lane] = 0; }   // LDS accesses of one wave stay in order
+    if (lane < IM_MAX_MODELS) {
+      const int32_t k_round = mw[MW_ACC][lane], svc_round = mw[MW_SVC][lane];
+      mw[MW_ACC][lane] = 0;   // LDS accesses of one wave stay in order
+      mw[MW_SVC][lane] = 0;
+      if (ml && k_round > 0) {
+        L.qlen += k_round;
+        L.backlog += svc_round;
+        acc_l += k_round;
+        L.chg |= CH_STATS;
+      }
+    }
 
-    // What each model touches this round (lane m): its front (newcomers to
-    // insert, or slots to fill), its slots (fills or a completion due), its
-    // counters (anything routed, started or completed) and its blackbox window.
-    // A model needing none of them is settled from its registers.
-    const int32_t cap_l = lane < M ? cap_s[lane] : 0;
-    const int capc_l = cap_l < S ? (cap_l < 0 ? 0 : cap_l) : S;
-    const uint32_t free_l = ~(uint32_t)L.busy_mask & ((1u << capc_l) - 1u);
-    const bool pops_l = last && free_l != 0 && L.qlen + acc_round_l > 0;
-    const bool due_l = last && L.busy_mask != 0 && L.next_done <= t;
-    const uint64_t need_front = ballot(lane < M && (acc_round_l > 0 || pops_l));
-    const uint64_t need_slots = ballot(lane < M && (pops_l || due_l));
-    // a window with dispatches in it, or of a rate-limited model, slides every tick
-    const uint64_t need_rpm = RPM ? ballot(lane < M && last && (rpm_l > 0 || L.rcnt > 0)) : 0ull;
-    auto fetch = [&](int mm, ModelIn& in) {
-      const size_t em = (size_t)e * M + mm;
-      in.front = make_int4(0, 0, 0, 0);
-      in.slot = make_int4(-1, 0, 0, 0);
-      in.fx = make_int2(0, 0);
-      in.sx = make_int2(0, 0);
-      if ((need_front >> mm) & 1ull) {
-        const int fh = rl(L.fh, mm), fn = rl(L.fn, mm);
-        if (lane < fn) {
-          in.front = a.front[em * kFront + fh + lane];   // fh + fn <= kFront
-          if constexpr (CHAIN) in.fx = a.front_ext[em * kFront + fh + lane];
-        }
+    // ---- insertion, every model of a chunk at once ----
+    for (int c = 0; c < nch; ++c) {
+      const int4 en = st[c * 64 + lane];
+      const int mdl = en.w;                  // 63: not admitted (sorted last)
+      const bool in = mdl < M;
+      if (ballot(in) == 0) continue;
+      const int src = in ? mdl : 0;
+      const int32_t Pm = shfl(L.P, src), fnm = shfl(L.fn, src);
+      const int64_t fm = composite(shfl(L.fmk, src), shfl(L.fmi, src));
+      const int64_t cp = composite(en.x, en.y);
+      // front-bound: below the front's largest entry, or the pool is empty and
+      // the front has room (every front key stays below every pool key)
+      const bool fb = in && ((Pm == 0 && fnm < kFront) || (fnm > 0 && cp < fm));
+      const bool pb = in && !fb;
+      const int prv = shfl(mdl, (lane + 63) & 63);
+      const int nxt = shfl(mdl, (lane + 1) & 63);
+      const uint64_t heads = ballot(in && (lane == 0 || prv != mdl));
+      const uint64_t upto = lane == 63 ? ~0ull : ((2ull << lane) - 1ull);   // lanes <= this one
+      const int seg = in ? 63 - __builtin_clzll((heads & upto) | 1ull) : 0;        // the segment's first lane
+      const uint64_t below_seg = (1ull << seg) - 1ull;
+      const uint64_t pbm = ballot(pb), fbm = ballot(fb);
+      if (pb) {
+        // position among the segment's pool-bound newcomers (a suffix of it)
+        const int o = prefix_count(pbm) - popc64(pbm & below_seg);
+        const size_t pos = (em0 + mdl) * a.qcap + Pm + o;
+        a.pool[pos] = make_int4(en.x, en.y, t, en.z);
+        if constexpr (CHAIN) a.pool_ext[pos] = stx[c * 64 + lane];
       }
-      if ((need_slots >> mm) & 1ull) {
-        if (lane < S) {
-          in.slot = a.slots[em * S + lane];
-          if constexpr (CHAIN) in.sx = a.slot_ext[em * S + lane];
-        }
+      if (ml) {
+        mw[MW_KF][lane] = 0;
+        mw[MW_KP][lane] = 0;
       }
-    };
-    if (r > 0) wave_mem_sync();   // the fronts written in the previous round
-    // ---- per model with work this round, in model order: insert its sorted
-    // segments, serve, write back (the next such model's inputs in flight) ----
-    const uint64_t busy_models =
-        need_front | need_slots | need_rpm | ballot(lane < M && last && prior_l != 0);
-    ModelIn nxt;
-    fetch(0, nxt);
-    for (int m = 0; m < M; ++m) {
-      const ModelIn cur = nxt;
-      if (m + 1 < M) fetch(m + 1, nxt);
-      if (((busy_models >> m) & 1ull) == 0) continue;   // nothing to insert, serve or count
-      const size_t em = (size_t)e * M + m;
-      Queue q;
-      q.qlen = rl(L.qlen, m); q.busy = rl(L.busy, m); q.ewma = rl(L.ewma, m);
-      q.backlog = rl(L.backlog, m); q.cap = __builtin_amdgcn_readfirstlane(cap_s[m]);
-      q.enabled = __builtin_amdgcn_readfirstlane(en_s[m]);
-      q.fh = rl(L.fh, m); q.fn = rl(L.fn, m); q.P = rl(L.P, m);
-      q.busy_mask = rl(L.busy_mask, m); q.next_done = rl(L.next_done, m);
-      int4* front = a.front + em * kFront;
-      int4* pool = a.pool + em * a.qcap;
-      int2* front_x = CHAIN ? a.front_ext + em * kFront : nullptr;
-      int2* pool_x = CHAIN ? a.pool_ext + em * a.qcap : nullptr;
-      const int32_t k_tot = rl(acc_round_l, m);   // newcomers admitted this round
-      const int32_t svc_in = rl(svc_round_l, m);
-      int4 fe = cur.front;                         // lane i mirrors front[fe_base + i]
-      int2 fx = cur.fx;                            // its chain words (chain pools)
-      int fe_base = q.fh;
-      bool dirty = false;   // the front in registers differs from the front array
-      if (k_tot > 0) {
-        for (int c = 0; c < nch; ++c) {
-          const int4 en = st[c * 64 + lane];
-          const bool mine = en.w == m;
-          const int k = popc64(ballot(mine));
-          if (k == 0) continue;
-          const int seg_lo = popc64(ballot(en.w < m));
-          const int o = lane - seg_lo;   // offset in the model's sorted segment
-          // newcomers merged into the front: those below its largest key, or
-          // all of them while the pool is empty (the front then holds the queue)
-          int lim;
-          if (q.P == 0) {
-            lim = k;
-          } else if (q.fn == 0) {
-            lim = 0;
-          } else {
-            // merges come before any pop of the tick: the window starts at lane 0
-            const int64_t fmax = readlane64(composite(fe.x, fe.y), q.fn - 1);
-            lim = popc64(ballot(mine && composite(en.x, en.y) < fmax));
-          }
-          if (mine && o >= lim) {
-            pool[q.P + o - lim] = make_int4(en.x, en.y, t, en.z);
-            if constexpr (CHAIN) pool_x[q.P + o - lim] = stx[c * 64 + lane];
-          }
-          q.P += k - lim;
-          if (lim > 0) {
-            merge_front<CHAIN>(q, fe, fx, st + c * 64 + seg_lo, stx + c * 64 + seg_lo, lim, a.key_mode,
-                               pool, pool_x);
-            fe_base = 0;
-            dirty = true;
-          }
-        }
-        q.qlen += k_tot;
-        q.backlog += svc_in;
-        if (lane == m) acc_l += k_tot;
+      if (in && (lane == 63 || nxt != mdl)) {   // the segment's last lane
+        const uint64_t segm = upto & ~below_seg;
+        mw[MW_KF][mdl] = popc64(fbm & segm);
+        mw[MW_KP][mdl] = popc64(pbm & segm);
+        mw[MW_SEG][mdl] = seg;
       }
-      if (!last) {
-        if (dirty && lane >= q.fh - fe_base && lane < q.fh - fe_base + q.fn) {
-          front[fe_base + lane] = fe;   // the live window [fh, fh + fn)
-          if constexpr (CHAIN) front_x[fe_base + lane] = fx;
+      const int32_t kf_l = ml ? mw[MW_KF][lane] : 0;
+      const int32_t kp_l = ml ? mw[MW_KP][lane] : 0;
+      if (kp_l > 0) {
+        L.P += kp_l;
+        L.chg |= CH_POOL;
+      }
+      // models with front-bound newcomers: merge them into the front
+      uint64_t merges = ballot(kf_l > 0);
+      while (merges) {
+        const int m = __builtin_ctzll(merges);
+        merges &= merges - 1;
+        const size_t em = em0 + m;
+        Queue q;
+        q.fh = rl(L.fh, m);
+        q.fn = rl(L.fn, m);
+        q.P = rl(L.P, m);
+        const int lim = rl(kf_l, m);
+        const int s0 = __builtin_amdgcn_readfirstlane(mw[MW_SEG][m]);
+        if ((wrote >> m) & 1ull) wave_mem_sync();   // this model's front was written this tick
+        int4 fe = make_int4(0, 0, 0, 0);
+        int2 fx = make_int2(0, 0);
+        if (lane < q.fn) {
+          fe = a.front[em * kFront + q.fh + lane];   // fh + fn <= kFront
+          if constexpr (CHAIN) fx = a.front_ext[em * kFront + q.fh + lane];
         }
+        const int32_t okey = fe.x, oid = fe.y;
+        const int ofh = q.fh, ofn = q.fn;
+        merge_front<CHAIN>(q, fe, fx, st + c * 64 + s0, stx + c * 64 + s0, lim, a.key_mode,
+                           a.pool + em * a.qcap, CHAIN ? a.pool_ext + em * a.qcap : nullptr);
+        // the front now starts at 0; entries that kept their position are not rewritten
+        const bool same = ofh == 0 && lane < ofn && okey == fe.x && oid == fe.y;
+        if (lane < q.fn && !same) {
+          a.front[em * kFront + lane] = fe;
+          if constexpr (CHAIN) a.front_ext[em * kFront + lane] = fx;
+        }
+        wrote |= 1ull << m;
+        const int32_t nk = rl(fe.x, q.fn - 1), ni = rl(fe.y, q.fn - 1);   // q.fn >= 1 after a merge
         if (lane == m) {
-          chg |= (q.qlen != L.qlen || q.backlog != L.backlog ? 1 : 0) | (q.fh != L.fh || q.fn != L.fn ? 2 : 0) |
-                 (q.P != L.P ? 4 : 0);
-          L.qlen = q.qlen; L.backlog = q.backlog; L.fh = q.fh; L.fn = q.fn; L.P = q.P;
+          L.fh = 0;
+          L.fn = q.fn;
+          L.P = q.P;
+          L.fmk = nk;
+          L.fmi = ni;
+          L.chg |= CH_FRONT | CH_POOL;
         }
-        continue;
       }
+    }
+    if (!last) continue;
 
-      // ---- service: fill free slots below c_m from the queue head ----
-      // A blackbox model dispatches only while its window (ticks t-59..t)
-      // holds fewer than rpm dispatches (App. C): the rest wait in the queue.
-      const int32_t rpm = RPM ? __builtin_amdgcn_readfirstlane(rpm_s[m]) : 0;
-      // Dispatches are recorded while the model is rate-limited; a window with
-      // dispatches in it keeps sliding (also after its limit is lifted).
-      const int32_t rcnt0 = RPM ? rl(L.rcnt, m) : 0;
-      const bool track = RPM && (rpm > 0 || rcnt0 > 0);
-      // dispatches of tick t - kRpmWindow, leaving the window now
-      const int32_t rold = track ? __builtin_amdgcn_readfirstlane(
-                                       (int32_t)a.rpm_ring[em * kRpmRing + (t % kRpmWindow)])
-                                 : 0;
-      const int32_t window = rcnt0 - rold;
-      const int32_t allowed = rpm > 0 ? (rpm > window ? rpm - window : 0) : 0x7fffffff;
-      const int capc = q.cap < S ? (q.cap < 0 ? 0 : q.cap) : S;
-      const uint32_t free_m = ~(uint32_t)q.busy_mask & ((1u << capc) - 1u);
-      const bool pops = free_m != 0 && q.qlen > 0 && allowed > 0;
-      const bool due = q.busy_mask != 0 && q.next_done <= t;
-      int32_t started = 0, wait_add = 0, svc_out = 0;
-      int32_t completed = 0, slo_add = 0, lat_add = 0;
-      int64_t cost_add = 0;
-      if (pops || due) {
+    // ---- service: fill free slots below c_m from the queue head, then one
+    // tick of service (every model at once: lane = (model, slot)) ----
+    // A blackbox model dispatches only while its window (ticks t-59..t)
+    // holds fewer than rpm dispatches (App. C): the rest wait in the queue.
+    const int capc_l = cap_l < 0 ? 0 : (cap_l > S ? S : cap_l);
+    const uint32_t free_l = ml ? (~(uint32_t)L.busy_mask & ((1u << capc_l) - 1u)) : 0u;
+    const int32_t window_l = L.rcnt - rold_l;
+    int32_t npop_l = min((int32_t)__popc(free_l), L.qlen);
+    if (RPM && rpm_l > 0) npop_l = min(npop_l, rpm_l > window_l ? rpm_l - window_l : 0);
+    const bool due_l = ml && L.busy_mask != 0 && L.next_done <= t;
+    const uint64_t serve = ballot(npop_l > 0 || due_l);
+    if (ml) {
+      mw[MW_STARTED][lane] = 0;
+      mw[MW_WAIT][lane] = 0;
+      mw[MW_SVCOUT][lane] = 0;
+      mw[MW_DONE][lane] = 0;
+      mw[MW_SLO][lane] = 0;
+      mw[MW_ND][lane] = 0x7fffffff;
+      md[MD_LAT][lane] = 0;
+      md[MD_COST][lane] = 0;
+    }
+    // Fronts that run dry this tick (rare): the remaining front entries stay
+    // at the head and the smallest pool entries follow them (a top-64
+    // selection over the pool); what does not fit goes back to the pool.
+    uint64_t dry = ballot(npop_l > L.fn);
+    if (dry != 0) {
+      if (dry & wrote) wave_mem_sync();
+      while (dry) {
+        const int m = __builtin_ctzll(dry);
+        dry &= dry - 1;
+        const size_t em = em0 + m;
+        const int ofh = rl(L.fh, m), ofn = rl(L.fn, m);
+        int4 old = make_int4(0, 0, 0, 0);
+        int2 oldx = make_int2(0, 0);
+        if (lane < ofn) {
+          old = a.front[em * kFront + ofh + lane];
+          if constexpr (CHAIN) oldx = a.front_ext[em * kFront + ofh + lane];
+        }
+        Queue q;
+        q.P = rl(L.P, m);
+        q.fh = 0;
+        q.fn = 0;
+        int4 fe;
+        int2 fx;
+        int4* pool = a.pool + em * a.qcap;
+        int2* pool_x = CHAIN ? a.pool_ext + em * a.qcap : nullptr;
+        refill<CHAIN>(q, fe, fx, pool, pool_x, pend_k[wv], pend_i[wv], reinterpret_cast<int2*>(st), a.key_mode);
+        const int nsel = q.fn;                                   // >= 1: P > 0
+        const int nf = ofn + nsel < kFront ? ofn + nsel : kFront;
+        const int back = ofn + nsel - nf;                        // largest selected entries returned
+        if (lane >= nsel - back && lane < nsel) {
+          pool[q.P + lane - (nsel - back)] = fe;
+          if constexpr (CHAIN) pool_x[q.P + lane - (nsel - back)] = fx;
+        }
+        q.P += back;
+        const int sh = (lane - ofn) & 63;
+        const int4 se = make_int4(shfl(fe.x, sh), shfl(fe.y, sh), shfl(fe.z, sh), shfl(fe.w, sh));
+        const int4 ne = lane < ofn ? old : se;
+        int2 nx = oldx;
+        if constexpr (CHAIN) {
+          const int2 sx2 = make_int2(shfl(fx.x, sh), shfl(fx.y, sh));
+          nx = lane < ofn ? oldx : sx2;
+        }
+        if (lane < nf) {
+          a.front[em * kFront + lane] = ne;
+          if constexpr (CHAIN) a.front_ext[em * kFront + lane] = nx;
+        }
+        const int32_t nk = rl(ne.x, nf - 1), ni = rl(ne.y, nf - 1);
+        if (lane == m) {
+          L.P = q.P;
+          L.fh = 0;
+          L.fn = nf;
+          L.fmk = nk;
+          L.fmi = ni;
+          L.chg |= CH_FRONT | CH_POOL;
+        }
+        wrote |= 1ull << m;
+      }
+      wave_mem_sync();
+    }
+    if (serve != 0) {
+      if (serve & wrote) wave_mem_sync();   // fronts written this tick are read below
+      const int mpp = kWave / S;             // models per pass
+      const int mi = lane / S, s = lane - mi * S;
+      for (int m0 = 0; m0 < M; m0 += mpp) {
+        const uint64_t pass = (mpp >= 64 ? ~0ull : ((1ull << mpp) - 1ull)) << m0;
+        if ((serve & pass) == 0) continue;
+        const int m = m0 + mi;
+        const bool sv = mi < mpp && m < M && ((serve >> m) & 1ull);   // lane serves slot s of model m
+        const int ms = sv ? m : 0;
+        const size_t em = em0 + ms;
+        const uint32_t fr = (uint32_t)shfl((int32_t)free_l, ms);
+        const int32_t np = shfl(npop_l, ms), fhm = shfl(L.fh, ms);
         // slot: {id, t_arr, tick of completion, budget}; id -1 = empty
-        int4 sl = cur.slot;
-        int2 sx = cur.sx;
-        if (pops) {
-          uint64_t empty = (uint64_t)free_m;
-          while (empty != 0 && q.qlen > 0 && started < allowed) {
-            if (q.fn == 0) {
-              refill<CHAIN>(q, fe, fx, pool, pool_x, pend_k[wv], pend_i[wv], pend_kb[wv], a.key_mode);
-              fe_base = 0;
-              dirty = true;
-            }
-            if (q.fn == 0) break;   // unreachable while qlen == fn + P holds; never spin
-            int need = popc64(empty);
-            need = need < allowed - started ? need : allowed - started;
-            const int take = need < q.fn ? need : q.fn;
-            const int rnk = prefix_count(empty);
-            const bool mine_slot = ((empty >> lane) & 1ull) && rnk < take;
-            int4 en;
-            const int src = (q.fh - fe_base + rnk) & 63;
-            en.x = shfl((int32_t)fe.x, src);
-            en.y = shfl((int32_t)fe.y, src);
-            en.z = shfl((int32_t)fe.z, src);
-            en.w = shfl((int32_t)fe.w, src);
-            const int32_t svc = en.w & 0xffff;
-            if (mine_slot) sl = make_int4(en.y, en.z, t + svc - 1, en.w >> 16);   // budget signed
-            if constexpr (CHAIN) {
-              const int32_t xa = shfl(fx.x, src), xb = shfl(fx.y, src);
-              if (mine_slot) sx = make_int2(xa, xb);
-            }
-            uint64_t popped = ballot(mine_slot);
-            empty &= ~popped;
-            while (popped) {                       // at most max_slots lanes
-              const int sp = __builtin_ctzll(popped);
-              popped &= popped - 1;
-              wait_add += t - rl(en.z, sp);
-              svc_out += rl(svc, sp);
-            }
-            q.fh += take;
-            q.fn -= take;
-            q.qlen -= take;
-            started += take;
-          }
-          q.backlog -= svc_out;
+        int4 sl = make_int4(-1, 0, 0, 0);
+        int2 sx = make_int2(0, 0);
+        if (sv) {
+          sl = a.slots[em * S + s];
+          if constexpr (CHAIN) sx = a.slot_ext[em * S + s];
         }
-        // ---- one tick of service; completions in slot order ----
-        const bool busy_slot = lane < S && sl.x >= 0;
+        // free slots are filled in slot order from the front's head
+        const int rank = __popc(fr & ((1u << s) - 1u));
+        const bool pop = sv && ((fr >> s) & 1u) && rank < np;
+        if (pop) {
+          const int4 pe = a.front[em * kFront + fhm + rank];
+          if constexpr (CHAIN) sx = a.front_ext[em * kFront + fhm + rank];
+          const int32_t svc = pe.w & 0xffff;
+          sl = make_int4(pe.y, pe.z, t + svc - 1, pe.w >> 16);   // budget signed
+          atomicAdd(&mw[MW_STARTED][m], 1);
+          atomicAdd(&mw[MW_WAIT][m], t - pe.z);
+          atomicAdd(&mw[MW_SVCOUT][m], svc);
+        }
+        // ---- one tick of service; a slot filled at t with svc = 1 completes at t ----
+        const bool busy_slot = sv && sl.x >= 0;
         const bool done = busy_slot && sl.z <= t;   // == t in every valid state
-        const uint64_t done_mask = ballot(done);
         const int32_t lat = t - sl.y + 1;
-        uint64_t dm = done_mask;
-        int32_t ewma = q.ewma;
-        while (dm) {
-          const int s = __builtin_ctzll(dm);
-          dm &= dm - 1;
-          const int32_t ls = rl(lat, s);
-          lat_add += ls;
-          const int64_t delta = (int64_t)ls * 256 - ewma;
-          const int64_t stepv = delta >= 0 ? (delta >> 3) : -((-delta + 7) >> 3);
-          ewma = (int32_t)(ewma + stepv);
+        if (done) {
+          // cost latency / budget of Eq. 2 in Q16 (budget >= 1); beta: the
+          // query's budget (chains; the call's own for single steps)
+          const uint32_t bud = CHAIN ? (uint32_t)chain_beta(sx.y) : (uint32_t)sl.w;
+          const uint64_t cq = lat < 65536 ? (uint64_t)(((uint32_t)lat << 16) / bud)
+                                          : ((uint64_t)(uint32_t)lat << 16) / bud;
+          atomicAdd(&mw[MW_DONE][m], 1);
+          if (lat <= sl.w) atomicAdd(&mw[MW_SLO][m], 1);
+          atomicAdd(&md[MD_LAT][m], (unsigned long long)(int64_t)lat);
+          atomicAdd(&md[MD_COST][m], (unsigned long long)cq);
         }
-        completed = popc64(done_mask);
-        if (done_mask) {
-          // cost latency / budget of Eq. 2 in Q16 (budget >= 1), one division
-          // per completed slot lane at once; 32 bits while latency < 2^16
-          uint64_t cq = 0;
-          if (done) {
-            // beta: the query's budget (chains; the call's own for single steps)
-            const uint32_t bud = CHAIN ? (uint32_t)chain_beta(sx.y) : (uint32_t)sl.w;
-            cq = lat < 65536 ? (uint64_t)(((uint32_t)lat << 16) / bud)
-                             : ((uint64_t)(uint32_t)lat << 16) / bud;
-          }
-          int64_t cs = (int64_t)cq;               // sum over the slot lanes (S <= 8)
-          cs += xshfl<1>(cs);
-          cs += xshfl<2>(cs);
-          cs += xshfl<4>(cs);
-          cost_add = readlane64(cs, 0);
-        }
-        slo_add = popc64(ballot(done && lat <= sl.w));
         if constexpr (CHAIN) {
           // call k + 1 of the query, for the next tick, with the query's deadline
+          // (spawn order: models in order, then slots, which is lane order)
           const bool more = done && chain_k(sx.x) + 1 < chain_n(sx.x);
           const uint64_t spawn = ballot(more);
           if (more) pend_nxt[pn + prefix_count(spawn)] = make_int4(sx.x + (1 << 24), sx.y, sl.y + sl.w, 0);
@@ -839,93 +885,115 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
           q_done += popc64(ballot(fin));
           q_met += popc64(ballot(fin && lat <= sl.w));
         }
-        if (done) sl = make_int4(-1, 0, 0, 0);
-        const uint64_t bm = ballot(lane < S && sl.x >= 0);
-        q.busy = popc64(bm);
-        q.busy_mask = (int32_t)(uint32_t)bm;
-        q.ewma = ewma;
-        // earliest completion tick among the busy slots (min over 8 lanes)
-        int32_t nd = (lane < S && sl.x >= 0) ? sl.z : 0x7fffffff;
-        nd = min(nd, xshfl<1>(nd));
-        nd = min(nd, xshfl<2>(nd));
-        nd = min(nd, xshfl<4>(nd));
-        q.next_done = rl(nd, 0);
-        if (lane < S) {
-          a.slots[em * S + lane] = sl;
-          if constexpr (CHAIN) a.slot_ext[em * S + lane] = sx;
+        if (busy_slot && !done) atomicMin(&mw[MW_ND][m], sl.z);
+        if (pop || done) {
+          if (done) sl = make_int4(-1, 0, 0, 0);
+          a.slots[em * S + s] = sl;
+          if constexpr (CHAIN) a.slot_ext[em * S + s] = sx;
+        }
+        const uint64_t bm = ballot(busy_slot && !done);
+        // lane m of this pass: its busy slots and the EWMA over its
+        // completions in slot order (alpha = 1/8, Q8, floor)
+        const int32_t latd = done ? lat : 0;
+        const bool mine = ml && (((pass & serve) >> lane) & 1ull);
+        const int base_l = mine ? (lane - m0) * S : 0;
+        int32_t ew = L.ewma;
+        for (int s2 = 0; s2 < S; ++s2) {
+          const int32_t ls = shfl(latd, base_l + s2);
+          if (mine && ls > 0) {
+            const int64_t delta = (int64_t)ls * 256 - ew;
+            const int64_t stepv = delta >= 0 ? (delta >> 3) : -((-delta + 7) >> 3);
+            ew = (int32_t)(ew + stepv);
+          }
+        }
+        if (mine) {
+          L.ewma = ew;
+          L.busy_mask = (int32_t)((bm >> base_l) & ((1ull << S) - 1ull));
         }
       }
+      // lane m: the model's queue after its pops
+      if (ml && ((serve >> lane) & 1ull)) {
+        L.qlen -= npop_l;
+        L.backlog -= mw[MW_SVCOUT][lane];
+        L.busy = __popc((uint32_t)L.busy_mask);
+        L.next_done = mw[MW_ND][lane];
+        L.fh += npop_l;
+        L.fn -= npop_l;
+        L.chg |= CH_STATS | CH_POOL | CH_DONE | (npop_l > 0 ? CH_FRONT : 0);
+      }
+    }
+    if constexpr (RPM) {
+      // this tick's recorded dispatches enter the window; those of tick t - 60 leave it
+      const int32_t rec = rpm_l > 0 ? mw[MW_STARTED][lane] : 0;
+      if (track_l && rec != rold_l) a.rpm_ring[(em0 + lane) * kRpmRing + (t % kRpmWindow)] = (uint8_t)rec;
+      if (ml && window_l + rec != L.rcnt) {
+        L.rcnt = window_l + rec;
+        L.chg |= CH_STATS | CH_DONE;
+      }
+    }
+  }
 
-      // ---- write back what changed ----
-      if (dirty && lane >= q.fh - fe_base && lane < q.fh - fe_base + q.fn) {
-        front[fe_base + lane] = fe;   // the live window [fh, fh + fn)
-        if constexpr (CHAIN) front_x[fe_base + lane] = fx;
-      }
-      const int32_t rec = rpm > 0 ? started : 0;   // this tick's recorded dispatches
-      const int32_t rcnt_new = window + rec;
-      if (track && lane == 0 && rec != rold) a.rpm_ring[em * kRpmRing + (t % kRpmWindow)] = (uint8_t)rec;
-      const int32_t routed_m = rl(prior_l, m);
-      const int32_t acc_m = rl(acc_l, m);
-      if (routed_m != 0 || started != 0 || completed != 0) {
-        int64_t add = 0;
-        switch (lane) {
-          case C_REJ_OVERFLOW: add = routed_m - acc_m; break;
-          case C_ENQUEUED: add = acc_m; break;
-          case C_STARTED: add = started; break;
-          case C_COMPLETED: add = completed; break;
-          case C_SLO_MET: add = slo_add; break;
-          case C_LAT_SUM: add = lat_add; break;
-          case C_WAIT_SUM: add = wait_add; break;
-          case C_COST_Q16: add = cost_add; break;
-          default: break;
+  // ---- counters, by lane (model, counter); service sums from LDS ----
+  {
+    const uint64_t act = ballot(ml && (prior_l != 0 || mw[MW_STARTED][lane] != 0 || mw[MW_DONE][lane] != 0));
+    static_assert(C_NUM == 8, "eight counters per model");
+    for (int m0 = 0; m0 < M; m0 += 8) {
+      if (((act >> m0) & 0xffull) == 0) continue;
+      const int m = m0 + (lane >> 3), c = lane & 7;
+      const int ms = m < M ? m : 0;
+      const int32_t pr = shfl(prior_l, ms), ac = shfl(acc_l, ms);
+      if (m < M && ((act >> m) & 1ull)) {
+        int64_t x;
+        switch (c) {
+          case C_REJ_OVERFLOW: x = pr - ac; break;
+          case C_ENQUEUED: x = ac; break;
+          case C_STARTED: x = mw[MW_STARTED][m]; break;
+          case C_COMPLETED: x = mw[MW_DONE][m]; break;
+          case C_SLO_MET: x = mw[MW_SLO][m]; break;
+          case C_LAT_SUM: x = (int64_t)md[MD_LAT][m]; break;
+          case C_WAIT_SUM: x = mw[MW_WAIT][m]; break;
+          default: x = (int64_t)md[MD_COST][m]; break;
         }
-        if (add != 0) counter_add(a.cnt + em * C_NUM + lane, add);
-      }
-      if (lane == m) {
-        chg |= (q.qlen != L.qlen || q.busy != L.busy || q.ewma != L.ewma || q.backlog != L.backlog ||
-                rcnt_new != L.rcnt ? 1 : 0) |
-               (q.fh != L.fh || q.fn != L.fn ? 2 : 0) | (q.P != L.P || q.busy_mask != L.busy_mask ? 4 : 0) |
-               (q.next_done != L.next_done || rcnt_new != L.rcnt ? 8 : 0);
-        L.rcnt = rcnt_new;
-        L.qlen = q.qlen; L.busy = q.busy; L.ewma = q.ewma; L.backlog = q.backlog;
-        L.fh = q.fh; L.fn = q.fn; L.P = q.P; L.busy_mask = q.busy_mask; L.next_done = q.next_done;
+        if (x != 0) counter_add(a.cnt + (em0 + m) * C_NUM + c, x);
       }
     }
   }
 
   // ---- records of the models whose state changed (lane m: model m) ----
-  if (lane < M) {
+  if (ml) {
     int4* rp = reinterpret_cast<int4*>(recs + lane);
-    if (chg & 1) rp[0] = make_int4(L.qlen, L.busy, L.ewma, L.backlog);
-    if (chg & 2) rp[1] = make_int4(cap_s[lane], en_s[lane], L.fh, L.fn);
+    if (L.chg & CH_STATS) rp[0] = make_int4(L.qlen, L.busy, L.ewma, L.backlog);
+    if (L.chg & CH_FRONT) rp[1] = make_int4(cap_l, en_l, L.fh, L.fn);
     if (lane == 0) {
       rp[2] = make_int4(L.P, next_id + nrows, t + 1, L.busy_mask);
-    } else if (chg & 4) {
+    } else if (L.chg & CH_POOL) {
       recs[lane].P = L.P;
       recs[lane].busy_mask = L.busy_mask;
     }
-    if (chg & 8) {
-      if (RPM) rp[3] = make_int4(L.next_done, rpm_s[lane], L.rcnt, __float_as_int(inv_rpm_s[lane]));
+    if (L.chg & CH_DONE) {
+      if (RPM) rp[3] = make_int4(L.next_done, rpm_l, L.rcnt, inv_rpm_bits);
       else recs[lane].next_done = L.next_done;
     }
   }
   // Snapshot row for the next tick's route step: lane i < 4M writes
   // statistic i / M of model i % M, lanes m < M the validity bytes.
-  const bool snap_dirty = ballot(lane < M && (chg & 1)) != 0;
-  if (snap_dirty) {
+  if (ballot(ml && (L.chg & CH_STATS)) != 0) {
     float* row = a.snap + (size_t)e * snap_stride(M);
+    const float inv_rpm_l = __int_as_float(inv_rpm_bits);
     for (int i0 = 0; i0 < 4 * M; i0 += 64) {
       const int i = i0 + lane;
       const int sidx = i / M, mm = i - sidx * M;
-      const int32_t vq = shfl(L.qlen, mm), vb = shfl(L.busy, mm), vw = shfl(L.ewma, mm),
-                    vk = shfl(L.backlog, mm);
-      const int32_t cm = cap_s[mm < M ? mm : 0];
-      const int32_t vr = RPM ? rpm_s[mm < M ? mm : 0] : 0, vrc = RPM ? shfl(L.rcnt, mm) : 0;
+      const int srcm = mm < M ? mm : 0;
+      const int32_t vq = shfl(L.qlen, srcm), vb = shfl(L.busy, srcm), vw = shfl(L.ewma, srcm),
+                    vk = shfl(L.backlog, srcm), cm = shfl(cap_l, srcm);
       const int c = cm < 0 ? 0 : (cm > IM_MAX_SLOTS ? IM_MAX_SLOTS : cm);
       if (i < 4 * M) {
         float v;
         switch (sidx) {
-          case 0: v = RPM ? queue_stat(a, vq, vr, vrc, inv_rpm_s[mm < M ? mm : 0]) : (float)vq * a.inv_qcap; break;
+          case 0:
+            v = RPM ? queue_stat(a, vq, shfl(rpm_l, srcm), shfl(L.rcnt, srcm), __int_as_float(shfl(__float_as_int(inv_rpm_l), srcm)))
+                    : (float)vq * a.inv_qcap;
+            break;
           case 1: v = (float)vb * a.inv_tab[c]; break;
           case 2: v = (float)vw * a.inv_lat; break;
           default: v = (float)vk * a.inv_tab[IM_MAX_SLOTS + 1 + c]; break;
@@ -933,9 +1001,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         row[i] = v;
       }
     }
-    if (lane < M) {
+    if (ml) {
       uint8_t* vb8 = (uint8_t*)(row + snap_valid_offset(M));
-      vb8[lane] = (en_s[lane] != 0 && cap_s[lane] > 0 && L.qlen < a.qcap) ? 1 : 0;
+      vb8[lane] = (en_l != 0 && cap_l > 0 && L.qlen < a.qcap) ? 1 : 0;
     }
   }
   int64_t* envc_p = a.env_cnt + (size_t)e * kEnvCnt;
