@@ -416,6 +416,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
   int32_t(*mw)[IM_MAX_MODELS] = mw_lds[wv];
   unsigned long long(*md)[IM_MAX_MODELS] = md_lds[wv];
   const int M = a.M, K = a.K, S = a.S;
+  // a / K for actions a < 64 as a multiply-high by ceil(2^32 / K) (exact for a < 2^32 / K)
+  const uint32_t kmag = K == 1 ? 0u : 0xffffffffu / (uint32_t)K + 1u;
   const size_t em0 = (size_t)e * M;
   ModelRec* recs = a.ms + em0;
   const bool ml = lane < M;   // this lane holds model `lane`
@@ -609,7 +611,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         if (in) load_row(i, ac, bs, xa, xb);
       }
       const int32_t bu = bs >> 16, sv = bs & 0xffff;
-      const int32_t mdl = ac >= 0 ? ac / K : -1;
+      const int32_t mdl = ac < 0 ? -1 : (K == 1 ? ac : (int32_t)__umulhi((uint32_t)ac, kmag));
       nomodel += popc64(ballot(in && ac < 0));
       if (in && ac >= 0) atomicAdd(&hist_s[ac], 1);   // routed requests per action
       int32_t rank = 0;
@@ -638,7 +640,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
       uint32_t sk = ((uint32_t)(acc ? mdl : 63) << 24) | (((uint32_t)(rk + 131072) & 0x3ffffu) << 6) |
                     (uint32_t)lane;
       const int32_t pay = (int32_t)(((uint32_t)svc & 0xffffu) | ((uint32_t)bu << 16));
-      bitonic_sort64(sk);
+      // rows of the chunk sit in its first lanes: sort only the smallest power
+      // of two of lanes holding them (the other lanes hold rows of model 63)
+      bitonic_sort_first(sk, nrows - base < 64 ? nrows - base : 64);
       const int src = (int)(sk & 63u);
       const int32_t skey = t + (int32_t)((sk >> 6) & 0x3ffffu) - 131072;
       const int32_t sid = next_id + base + src;
@@ -867,8 +871,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
           // cost latency / budget of Eq. 2 in Q16 (budget >= 1); beta: the
           // query's budget (chains; the call's own for single steps)
           const uint32_t bud = CHAIN ? (uint32_t)chain_beta(sx.y) : (uint32_t)sl.w;
-          const uint64_t cq = lat < 65536 ? (uint64_t)(((uint32_t)lat << 16) / bud)
-                                          : ((uint64_t)(uint32_t)lat << 16) / bud;
+          uint64_t cq = (uint64_t)(((uint32_t)lat << 16) / bud);   // latency < 2^16
+          if (lat >= 65536) cq = ((uint64_t)(uint32_t)lat << 16) / bud;
           atomicAdd(&mw[MW_DONE][m], 1);
           if (lat <= sl.w) atomicAdd(&mw[MW_SLO][m], 1);
           atomicAdd(&md[MD_LAT][m], (unsigned long long)(int64_t)lat);

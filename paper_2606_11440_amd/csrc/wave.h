@@ -210,6 +210,26 @@ __device__ __forceinline__ void bitonic_sort64(KT& k, int32_t (&p)[NP]) {
   bitonic_block<64, NP>(k, p);
 }
 
+// Ascending sort of the keys of the first n lanes (n <= 64), over the
+// smallest power of two of lanes >= n; keys in the other lanes end up in an
+// unspecified order. Fewer stages for short inputs: 6 for n <= 8, 10 for
+// n <= 16, 15 for n <= 32, 21 otherwise.
+template <typename KT>
+__device__ __forceinline__ void bitonic_sort_first(KT& k, int n) {
+  int32_t none[1] = {0};   // dead after the network; removed by the compiler
+  bitonic_block<2, 1>(k, none);
+  if (n <= 2) return;
+  bitonic_block<4, 1>(k, none);
+  if (n <= 4) return;
+  bitonic_block<8, 1>(k, none);
+  if (n <= 8) return;
+  bitonic_block<16, 1>(k, none);
+  if (n <= 16) return;
+  bitonic_block<32, 1>(k, none);
+  if (n <= 32) return;
+  bitonic_block<64, 1>(k, none);
+}
+
 // Key-only variants (no payload).
 template <typename KT>
 __device__ __forceinline__ void bitonic_sort64(KT& k) {
