@@ -61,7 +61,9 @@ typedef enum { IM_KEY_SLACK = 0, IM_KEY_DEADLINE = 1, IM_KEY_FCFS = 2 } im_key_m
 
 /* Bits of the sticky device error word. */
 #define IM_ERR_QIDX   1   /* q_idx outside [0, n_queries)                          */
-#define IM_ERR_COUNT  2   /* offsets not a CSR of n_total rows, or n_e > max       */
+#define IM_ERR_COUNT  2   /* offsets not a CSR of n_total rows, or n_e > max; in a
+                           * chain pool an offsets array that is not one monotone
+                           * partition of [0, n_total) skips every env            */
 #define IM_ERR_BUDGET 4   /* budget < 1                                            */
 #define IM_ERR_SVC    8   /* base_svc outside [1, IM_SVC_MAX]                      */
 #define IM_ERR_ACTION 16  /* action outside [-1, M*K)                              */
@@ -261,7 +263,9 @@ im_status im_route_sample(im_pool* pool, const im_arrivals* arr, uint64_t seed, 
  * im_route, im_route_sample, im_schedule and im_tick call (before it routes or
  * schedules) and stay valid until the next such call.
  *   offsets  [n_envs + 1] row range of each env (pending calls first)
- *   n_rows   [1] rows of the tick
+ *   n_rows   [2] rows of the tick, then 1 when the arrival offsets are not one
+ *            monotone partition of [0, n_total): no arrival is then routed and
+ *            every env skips the tick with IM_ERR_COUNT
  *   q_idx, budget, role  per row: query-embedding row, budget the call is
  *            routed with (the remaining budget for a pending call), role
  * IM_EINVAL for a single-call pool. */
@@ -277,10 +281,17 @@ im_status im_get_rows(im_pool* pool, im_rows* out);
 /* Schedule one tick with the given actions (any actions in [-1, M*K), e.g.
  * sampled ones): admission in id order with tail-drop beyond queue_cap, keys
  * per key_mode, service of every model, accounting; then the tick advances.
- *   actions  device int32 [n_total] */
+ * The scheduler of Sec. 4.3 (each model's queue served earliest deadline
+ * first; chain pools: a call inherits its query's deadline), the bounded
+ * per-model concurrency of Table 5 (c_m slots) and the latency moving
+ * average of Sec. 5.4. The load statistics the next im_route reads (Sec. 3,
+ * Eq. 1) are refreshed here.
+ *   actions  device int32 [n_total] (chain pools: the rows of im_get_rows) */
 im_status im_schedule(im_pool* pool, const im_arrivals* arr, const int32_t* actions, void* stream);
 
-/* im_route followed by im_schedule with the actions it chose.
+/* im_route followed by im_schedule with the actions it chose: one step of
+ * the executor's decision (Sec. 4.2, masked argmax over the joint actions of
+ * Sec. 3) and of the scheduler (Sec. 4.3) for every env.
  *   actions_out  device int32 [n_total] receiving the actions, or NULL
  *                (then a pool-owned buffer is used) */
 im_status im_tick(im_pool* pool, const im_arrivals* arr, int32_t* actions_out, void* stream);
@@ -317,7 +328,10 @@ typedef struct {
                                      of them, those completed by their deadline */
 } im_env_state;
 
-/* Copy the state of envs [env_begin, env_begin + env_count) to host memory.
+/* Copy the state of envs [env_begin, env_begin + env_count) to host memory:
+ * what the executor observes (Sec. 3, Eq. 1: per-model queue depth, latency
+ * moving average, busy slots standing in for KV-cache use), every queue in
+ * the scheduler's service order (Sec. 4.3) and the accounting counters.
  *   tick    out: ticks completed so far
  *   envs    [count], models [count*M], slots [count*M*max_slots],
  *   queues  [count*M*queue_cap] (entries beyond qlen are zeroed),
@@ -353,12 +367,35 @@ im_status im_read_chain_state(im_pool* pool, int32_t env_begin, int32_t env_coun
 /* Overwrite the state of envs [env_begin, env_begin + env_count) and the tick
  * from host memory (same layout as im_read_state; all pointers required).
  * Returns IM_ESTATE without changing anything if the snapshot is
- * inconsistent (unsorted queue, qlen/busy/backlog not matching, bounds).
- * IM_EUNSUPPORTED for chain pools (their chain words and pending calls are
- * not part of this snapshot). */
+ * inconsistent: a queue not strictly increasing in (key, id); qlen, busy or
+ * backlog not matching the queues and slots; a queued key other than the key
+ * mode's function of its arrival tick, budget and service time; an arrival
+ * tick outside [0, tick), an id at or above the env's next id, a service time
+ * outside [1, IM_SVC_MAX * n_depths], a budget below 1; other bounds.
+ * IM_EUNSUPPORTED for chain pools (restored with im_write_chain_state). */
 im_status im_write_state(im_pool* pool, int32_t env_begin, int32_t env_count, int32_t tick,
                          const im_env_state* envs, const im_model_state* models,
                          const im_slot* slots, const im_entry* queues, const int64_t* hist);
+
+/* Restore a chain pool (checkpoint/resume of the multi-step chains of
+ * Sec. 4.3, whose calls inherit their query's deadline): the snapshot of
+ * im_write_state (queued and running calls may carry a budget <= 0: what is
+ * left of their query's) plus, in the layouts of im_read_chain_state, the
+ * chain words of every queued call (queue order) and of every busy slot, and
+ * each env's pending calls ([count*M*max_slots], pending_count [count]),
+ * which the next im_route routes first. All pointers required (host memory;
+ * synchronises). IM_ESTATE without any change if inconsistent (the checks of
+ * im_write_state; chain words out of range: q_idx outside [0, n_queries),
+ * k outside [0, n_steps), n_steps outside [1, max_steps], base_svc outside
+ * [1, IM_SVC_MAX] or not dividing the queued service time in at most
+ * n_depths steps, beta outside [1, 32767], role0 outside [0, n_roles); a
+ * pending call with k = 0 or a count above M*max_slots). IM_EINVAL for a
+ * single-call pool. */
+im_status im_write_chain_state(im_pool* pool, int32_t env_begin, int32_t env_count, int32_t tick,
+                               const im_env_state* envs, const im_model_state* models,
+                               const im_slot* slots, const im_entry* queues, const int64_t* hist,
+                               const im_chain* queue_chains, const im_chain* slot_chains,
+                               const im_pending* pending, const int32_t* pending_count);
 
 /* Dual update of the Lagrange multiplier (Sec. 4.4, Eq. 7; App. C with no
  * monetary budget): over the requests completed since the previous call (or
@@ -369,6 +406,17 @@ im_status im_write_state(im_pool* pool, int32_t env_begin, int32_t env_count, in
  *   lambda  device fp64 [1], in/out
  * Stream-ordered; IM_EINVAL for eta < 0 or lambda_max < 0. */
 im_status im_dual_update(im_pool* pool, double eta, double lambda_max, double* lambda, void* stream);
+
+/* Launch shapes, for operations and tests of determinism (calls made after
+ * it use the new shapes; no result depends on them; not stream-ordered):
+ *   route_blocks  grid of the persistent route kernels: -1 one block per
+ *                 compute unit (the default), n > 0 at most n blocks sharing
+ *                 the tick's row tiles, 0 the kernels that launch one wave
+ *                 per row tile instead
+ *   sched_waves   envs (one wave each) per workgroup of the schedule step:
+ *                 1, 2 or 4 (the default); 0 keeps the current value
+ * IM_EINVAL for other values. */
+im_status im_set_launch(im_pool* pool, int32_t route_blocks, int32_t sched_waves);
 
 /* Host knobs (stream-ordered): take a model out of routing, or change its
  * number of service slots (requests in slots >= the new capacity finish but

@@ -15,7 +15,9 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "oracle.cpp")
-_LIB = os.path.join(_HERE, "liboracle.so")
+# IM_ORACLE_LIB: another build of oracle.cpp (the sanitizer test loads one
+# built with AddressSanitizer and UBSan)
+_LIB = os.environ.get("IM_ORACLE_LIB") or os.path.join(_HERE, "liboracle.so")
 
 KEY_MODES = {"slack": 0, "deadline": 1, "fcfs": 2}
 ERR_QIDX, ERR_COUNT, ERR_BUDGET, ERR_SVC, ERR_ACTION, ERR_ROLE, ERR_STEPS = 1, 2, 4, 8, 16, 32, 64

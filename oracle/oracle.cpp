@@ -184,6 +184,9 @@ struct orc_pool {
   int32_t t = 0;
   int32_t err = 0;
   int64_t dual_completed = 0, dual_cost_q16 = 0;   // totals at the last dual update
+  // chain pools: the arrival CSR of the current call starts at 0, never
+  // decreases and ends at n_total (set by each entry point that reads it)
+  mutable bool csr_whole = true;
 };
 
 }  // extern "C"
@@ -444,8 +447,19 @@ struct Row {
 
 bool chains(const orc_pool* p) { return p->d.max_steps > 1; }
 
+// Chain pools lay an env's rows out by a scan over the arrival CSR, after the
+// pending calls of the envs before it. Reading: a CSR that is not one
+// monotone partition of [0, n_total) makes no arrival usable; every env then
+// skips the tick with ERR_COUNT (its pending calls stay pending).
+void set_csr_whole(const orc_pool* p, int32_t n_total, const int32_t* off) {
+  bool w = off[0] == 0 && off[p->d.E] == n_total;
+  for (int e = 0; w && e < p->d.E; ++e) w = off[e + 1] >= off[e];
+  p->csr_whole = w;
+}
+
 // Arrival CSR entry of env e usable (chain pools route only such arrivals).
 bool csr_ok(const orc_pool* p, int e, int32_t n_total, const int32_t* off) {
+  if (chains(p) && !p->csr_whole) return false;
   const int32_t lo = off[e], hi = off[e + 1];
   return lo >= 0 && hi >= lo && hi <= n_total && hi - lo <= p->d.max_arrivals;
 }
@@ -598,6 +612,7 @@ void schedule_env(orc_pool* p, int e, int32_t n_total, const int32_t* off,
   int bad = 0;
   const int32_t lo = off[e], hi = off[e + 1];
   if (lo < 0 || hi < lo || hi > n_total || hi - lo > d.max_arrivals) bad |= ERR_COUNT;
+  if (chains(p) && !p->csr_whole) bad |= ERR_COUNT;
   if (!bad) {
     for (const Row& r : rows) {
       if (actions[r.out] < -1 || actions[r.out] >= p->A) bad |= ERR_ACTION;
@@ -829,6 +844,7 @@ bool route_rows_ok(const orc_pool* p, int e, int32_t n_total, const int32_t* off
 void orc_route(orc_pool* p, int32_t n_total, const int32_t* off, const int32_t* q_idx,
                const int16_t* role, const int16_t* budget, const int16_t* n_steps, double* logits,
                int32_t* actions, int threads) {
+  set_csr_whole(p, n_total, off);
   std::vector<int32_t> errs(p->d.E, 0);
   const std::vector<int32_t> ro = row_offsets(p, n_total, off);
   for_envs(p->d.E, threads, [&](int e) {
@@ -843,6 +859,7 @@ void orc_route(orc_pool* p, int32_t n_total, const int32_t* off, const int32_t* 
 void orc_schedule(orc_pool* p, int32_t n_total, const int32_t* off, const int32_t* q_idx,
                   const int16_t* role, const int16_t* budget, const int16_t* base_svc,
                   const int16_t* n_steps, const int32_t* actions, int threads) {
+  set_csr_whole(p, n_total, off);
   std::vector<int32_t> errs(p->d.E, 0);
   const std::vector<int32_t> ro = row_offsets(p, n_total, off);
   for_envs(p->d.E, threads, [&](int e) {
@@ -860,6 +877,7 @@ void orc_route_rl(orc_pool* p, int env_base, int32_t n_total, const int32_t* off
                   const int16_t* n_steps, uint32_t seed_lo, uint32_t seed_hi, int greedy,
                   double* logits, int32_t* actions, double* logp, double* entropy, double* value,
                   int threads) {
+  set_csr_whole(p, n_total, off);
   std::vector<int32_t> errs(p->d.E, 0);
   const std::vector<int32_t> ro = row_offsets(p, n_total, off);
   for_envs(p->d.E, threads, [&](int e) {
@@ -874,6 +892,7 @@ void orc_route_rl(orc_pool* p, int env_base, int32_t n_total, const int32_t* off
 
 // Row offsets of the next route/schedule call (E + 1 entries).
 void orc_row_offsets(const orc_pool* p, int32_t n_total, const int32_t* off, int32_t* out) {
+  set_csr_whole(p, n_total, off);
   const std::vector<int32_t> ro = row_offsets(p, n_total, off);
   std::copy(ro.begin(), ro.end(), out);
 }

@@ -15,7 +15,9 @@ from ._lib import (EXPORTED, IMError, im_clear_error, im_destroy, im_dual_update
                    im_read_chain_state, im_read_state, im_route,
                    im_route_sample,
                    im_schedule,
-                   im_set_capacity, im_set_enabled, im_set_rpm_limit, im_tick, im_write_state,
+                   im_set_capacity, im_set_enabled, im_set_launch, im_set_rpm_limit, im_tick,
+                   im_write_chain_state,
+                   im_write_state,
                    make_arrivals,
                    make_desc)
 
@@ -86,6 +88,10 @@ class Pool:
     def write_state(self, env_begin, s):
         im_write_state(self.h, env_begin, s)
 
+    def write_chain_state(self, env_begin, s, c):
+        """Chain pools: s from state(), c from chain_state()."""
+        im_write_chain_state(self.h, env_begin, s, c)
+
     def set_enabled(self, e, m, v, stream=None):
         im_set_enabled(self.h, e, m, v, stream)
 
@@ -94,6 +100,12 @@ class Pool:
 
     def set_rpm_limit(self, e, m, r, stream=None):
         im_set_rpm_limit(self.h, e, m, r, stream)
+
+    def set_launch(self, route_blocks, sched_waves=0):
+        """Launch shapes (results do not depend on them): route_blocks -1
+        default, n > 0 persistent grid of n blocks, 0 one wave per tile;
+        sched_waves 1, 2 or 4 envs per schedule workgroup (0: keep)."""
+        im_set_launch(self.h, route_blocks, sched_waves)
 
     def error(self) -> int:
         return im_get_error(self.h)

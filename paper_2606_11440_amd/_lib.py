@@ -24,8 +24,8 @@ IM_NET_MLP, IM_NET_DUAL = 0, 1
 
 EXPORTED = ("im_pool_create", "im_pool_create_dual", "im_route", "im_route_sample", "im_schedule", "im_tick", "im_destroy",
             "im_dual_update", "im_set_rpm_limit", "im_get_rows", "im_read_chain_state",
-            "im_read_state", "im_write_state", "im_set_enabled", "im_set_capacity",
-            "im_get_error", "im_clear_error", "im_last_error")
+            "im_read_state", "im_write_state", "im_write_chain_state", "im_set_enabled", "im_set_capacity",
+            "im_get_error", "im_clear_error", "im_last_error", "im_set_launch")
 
 
 class ImPoolDesc(ctypes.Structure):
@@ -115,9 +115,11 @@ def load() -> ctypes.CDLL:
     L.im_destroy.restype = None
     L.im_read_state.argtypes = [P, I32, I32, ctypes.POINTER(I32), P, P, P, P, P]
     L.im_write_state.argtypes = [P, I32, I32, I32, P, P, P, P, P]
+    L.im_write_chain_state.argtypes = [P, I32, I32, I32, P, P, P, P, P, P, P, P, P]
     L.im_set_enabled.argtypes = [P, I32, I32, I32, P]
     L.im_set_capacity.argtypes = [P, I32, I32, I32, P]
     L.im_set_rpm_limit.argtypes = [P, I32, I32, I32, P]
+    L.im_set_launch.argtypes = [P, I32, I32]
     L.im_get_rows.argtypes = [P, ctypes.POINTER(ImRows)]
     L.im_read_chain_state.argtypes = [P, I32, I32, P, P, P, P]
     L.im_get_error.argtypes = [P, ctypes.POINTER(I32)]
@@ -322,6 +324,10 @@ def im_set_rpm_limit(pool, env, model, rpm_limit, stream=None):
     _check(load().im_set_rpm_limit(pool, env, model, int(rpm_limit), _stream(stream)), pool)
 
 
+def im_set_launch(pool, route_blocks: int, sched_waves: int = 0):
+    _check(load().im_set_launch(pool, int(route_blocks), int(sched_waves)), pool)
+
+
 def im_get_error(pool) -> int:
     bits = ctypes.c_int32(0)
     st = load().im_get_error(pool, ctypes.byref(bits))
@@ -374,8 +380,8 @@ def im_read_state(pool, env_begin: int, env_count: int, M: int, A: int, S: int, 
     return out
 
 
-def im_write_state(pool, env_begin: int, s: dict):
-    """Inverse of im_read_state (same dict layout)."""
+def _state_arrays(s: dict):
+    """Host arrays of a state dict in im_read_state's layout."""
     E, M = s["qlen"].shape
     A = s["hist"].shape[1]
     S = s["slots"].shape[2]
@@ -399,5 +405,33 @@ def im_write_state(pool, env_begin: int, s: dict):
     for i, f in enumerate(("key", "id", "t_arr", "svc", "budget")):
         queues[f] = s["queues"][..., i]
     hist = np.ascontiguousarray(s["hist"], np.int64)
+    return E, envs, models, slots, queues, hist
+
+
+def im_write_state(pool, env_begin: int, s: dict):
+    """Inverse of im_read_state (same dict layout)."""
+    E, envs, models, slots, queues, hist = _state_arrays(s)
     _check(load().im_write_state(pool, env_begin, E, int(s["t"]), _hptr(envs), _hptr(models),
                                  _hptr(slots), _hptr(queues), _hptr(hist)), pool)
+
+
+def im_write_chain_state(pool, env_begin: int, s: dict, c: dict):
+    """Restore a chain pool: s as from im_read_state, c as from
+    im_read_chain_state (queue_chain, slot_chain, pending, pending_count)."""
+    E, envs, models, slots, queues, hist = _state_arrays(s)
+
+    def chains(six):
+        out = np.zeros(six.shape[:-1], CHAIN_DT)
+        for i, f in enumerate(("q_idx", "k", "n_steps", "role0", "base_svc", "beta")):
+            out[f] = six[..., i]
+        return out
+    qch = chains(np.asarray(c["queue_chain"]))
+    sch = chains(np.asarray(c["slot_chain"]))
+    pe = np.asarray(c["pending"])
+    pend = np.zeros(pe.shape[:-1], PENDING_DT)
+    pend["ch"] = chains(pe[..., :6])
+    pend["deadline"] = pe[..., 6]
+    pc = np.ascontiguousarray(c["pending_count"], np.int32)
+    _check(load().im_write_chain_state(pool, env_begin, E, int(s["t"]), _hptr(envs), _hptr(models),
+                                       _hptr(slots), _hptr(queues), _hptr(hist), _hptr(qch), _hptr(sch),
+                                       _hptr(pend), _hptr(pc)), pool)

@@ -161,6 +161,7 @@ struct SchedArgs {
   int2* front_ext;
   int2* pool_ext;
   int2* slot_ext;
+  const int32_t* csr_bad;   // chain pools: set when the rows build found the arrival CSR broken
   int32_t n_total;
   int32_t E, M, K, A, S, qcap, max_arrivals, key_mode;
   int64_t Q;
@@ -197,8 +198,9 @@ hipError_t launch_role_projection(const uint16_t* w_role, const uint16_t* roles,
                                   int n_roles, int embed_dim, float* out, hipStream_t s);
 hipError_t launch_route(const RouteArgs& a, int dtype, int hidden, int n_layers, int out_tiles,
                         hipStream_t s);
-// rpm: some model of the pool is (or was) rate-limited (blackbox windows tracked)
-hipError_t launch_schedule(const SchedArgs& a, bool rpm, bool chain, hipStream_t s);
+// rpm: some model of the pool is (or was) rate-limited (blackbox windows tracked);
+// waves_per_block: envs per block (1, 2 or 4)
+hipError_t launch_schedule(const SchedArgs& a, bool rpm, bool chain, int waves_per_block, hipStream_t s);
 // Rows of a chain pool's tick: row offsets (pending calls first, then the
 // usable arrivals of each env), the row count and the route step's per-row
 // inputs (q_idx, remaining budget, role of the call).
@@ -212,7 +214,8 @@ struct RowsArgs {
   const int4* pend;         // [2][E * pend_cap]
   const int32_t* pcnt;      // [2][E]
   int32_t* roff;            // out [E+1]
-  int32_t* n_rows;          // out [1]
+  int32_t* n_rows;          // out [2]: the row count, then 1 when the arrival CSR is not
+                            // one monotone partition of [0, n_total) (no arrival is then usable)
   int32_t* rq;              // out per row
   int16_t* rb;
   int16_t* rr;

@@ -61,6 +61,8 @@ struct im_pool {
   int16_t* rr = nullptr;
   int32_t t = 0;
   int32_t cu_count = 0;
+  int32_t route_blocks = -1;   // grid of the persistent route kernels (-1: one block per CU; 0: none)
+  int32_t sched_waves = 4;     // envs per block of the schedule kernel
   bool rpm_active = false;   // some model was given a rate limit (the windows are tracked from then on)
   std::string last_error;
 };
@@ -254,7 +256,7 @@ im_status init_state(im_pool* p, const int32_t* capacity, hipStream_t s) {
     if (st == IM_OK) st = zalloc(p, &p->pool_ext, EM * (size_t)d.queue_cap);
     if (st == IM_OK) st = zalloc(p, &p->slot_ext, EM * d.max_slots);
     if (st == IM_OK) st = zalloc(p, &p->roff, E + 1);
-    if (st == IM_OK) st = zalloc(p, &p->n_rows, 1);
+    if (st == IM_OK) st = zalloc(p, &p->n_rows, 2);
     if (st == IM_OK) st = zalloc(p, &p->rq, (size_t)p->rows_cap);
     if (st == IM_OK) st = zalloc(p, &p->rb, (size_t)p->rows_cap);
     if (st == IM_OK) st = zalloc(p, &p->rr, (size_t)p->rows_cap);
@@ -535,7 +537,7 @@ static im::RouteArgs route_args(im_pool* p, const im_arrivals* arr, int32_t* act
   a.actions = actions;
   a.logits = logits;
   a.err = p->err;
-  a.persistent_blocks = p->cu_count;
+  a.persistent_blocks = p->route_blocks < 0 ? p->cu_count : p->route_blocks;
   a.net = p->d.net;
   if (p->d.net == IM_NET_DUAL) {
     a.role = arr->role;
@@ -642,8 +644,9 @@ static im_status schedule_impl(im_pool* p, const im_arrivals* arr, const int32_t
     a.front_ext = p->front_ext;
     a.pool_ext = p->pool_ext;
     a.slot_ext = p->slot_ext;
+    a.csr_bad = p->n_rows + 1;
   }
-  IM_HIP(p, im::launch_schedule(a, p->rpm_active, p->chains, s));
+  IM_HIP(p, im::launch_schedule(a, p->rpm_active, p->chains, p->sched_waves, s));
   p->t += 1;
   return IM_OK;
 }
@@ -749,6 +752,16 @@ im_status im_set_rpm_limit(im_pool* p, int32_t env, int32_t model, int32_t rpm_l
   hipLaunchKernelGGL(set_rpm_kernel, dim3(1), dim3(1), 0, (hipStream_t)stream, r, rpm_limit, inv);
   IM_HIP(p, hipGetLastError());
   IM_HIP(p, im::launch_snapshot(sched_args(p), env, 1, (hipStream_t)stream));
+  return IM_OK;
+}
+
+im_status im_set_launch(im_pool* p, int32_t route_blocks, int32_t sched_waves) {
+  if (!p) return fail(nullptr, IM_EINVAL, "pool is NULL");
+  if (route_blocks < -1) return fail(p, IM_EINVAL, "route_blocks < -1");
+  if (sched_waves != 0 && sched_waves != 1 && sched_waves != 2 && sched_waves != 4)
+    return fail(p, IM_EINVAL, "sched_waves not in {0, 1, 2, 4}");
+  p->route_blocks = route_blocks;
+  if (sched_waves) p->sched_waves = sched_waves;
   return IM_OK;
 }
 
@@ -870,15 +883,33 @@ im_status im_read_state(im_pool* p, int32_t env_begin, int32_t env_count, int32_
   return IM_OK;
 }
 
-im_status im_write_state(im_pool* p, int32_t env_begin, int32_t env_count, int32_t tick,
-                         const im_env_state* envs, const im_model_state* models,
-                         const im_slot* slots, const im_entry* queues, const int64_t* hist) {
-  if (!p) return fail(nullptr, IM_EINVAL, "pool is NULL");
-  if (p->chains) return fail(p, IM_EUNSUPPORTED, "im_write_state: chain pools are not supported");
+}  // extern "C"
+
+// Validated restore of envs [env_begin, env_begin + env_count) and the tick;
+// chain pools also take the chain words of queued and running calls and the
+// pending calls (qch, sch, pend, pcount; NULL for single-call pools).
+static im_status write_state_impl(im_pool* p, int32_t env_begin, int32_t env_count, int32_t tick,
+                                  const im_env_state* envs, const im_model_state* models,
+                                  const im_slot* slots, const im_entry* queues, const int64_t* hist,
+                                  const im_chain* qch, const im_chain* sch, const im_pending* pend,
+                                  const int32_t* pcount) {
   if (env_begin < 0 || env_count < 0 || (int64_t)env_begin + env_count > p->d.n_envs)
     return fail(p, IM_EINVAL, "env range out of bounds");
   if (!envs || !models || !slots || !queues || !hist) return fail(p, IM_EINVAL, "NULL argument");
+  if (p->chains && (!qch || !sch || !pend || !pcount)) return fail(p, IM_EINVAL, "NULL argument");
   if (tick < 0) return fail(p, IM_EINVAL, "tick < 0");
+  const bool ch = p->chains;
+  // chain words: the call's query row, its index among n_steps calls, the
+  // first call's role, the base service time and the query's budget
+  auto chain_ok = [&](const im_chain& c) {
+    return c.q_idx >= 0 && (int64_t)c.q_idx < p->Q && c.q_idx < (1 << 24) && c.n_steps >= 1 &&
+           c.n_steps <= p->d.max_steps && c.k >= 0 && c.k < c.n_steps && c.base_svc >= 1 &&
+           c.base_svc <= IM_SVC_MAX && c.beta >= 1 && c.beta <= 32767 && c.role0 >= 0 &&
+           c.role0 < (p->d.net == IM_NET_DUAL ? p->d.n_roles : 1) && c.role0 < 32;
+  };
+  auto pack = [](const im_chain& c) {
+    return make_int2(im::chain_a(c.q_idx, c.k, c.n_steps), im::chain_b(c.base_svc, c.beta, c.role0));
+  };
   const int M = p->d.n_models, S = p->S, qcap = p->d.queue_cap, A = p->A;
   const size_t EMc = (size_t)env_count * M, em0 = (size_t)env_begin * M;
   std::vector<ModelRec> recs(EMc);
@@ -888,6 +919,8 @@ im_status im_write_state(im_pool* p, int32_t env_begin, int32_t env_count, int32
   std::vector<int4> fr(EMc * im::kFront, make_int4(0, 0, 0, 0));
   std::vector<int4> pl(EMc * (size_t)qcap, make_int4(0, 0, 0, 0));
   std::vector<int4> sl(EMc * S);
+  std::vector<int2> frx(ch ? fr.size() : 0, make_int2(0, 0)), plx(ch ? pl.size() : 0, make_int2(0, 0)),
+      slx(ch ? sl.size() : 0, make_int2(0, 0));
   for (size_t i = 0; i < EMc; ++i) {
     const im_model_state& ms = models[i];
     const int e = (int)(i / M);
@@ -900,6 +933,22 @@ im_status im_write_state(im_pool* p, int32_t env_begin, int32_t env_count, int32
       if (k > 0 && !(q[k - 1].key < q[k].key || (q[k - 1].key == q[k].key && q[k - 1].id < q[k].id)))
         return fail(p, IM_ESTATE, "queue not strictly increasing in (key, id)");
       if (q[k].id < 0 || q[k].id >= envs[e].next_id) return fail(p, IM_ESTATE, "queue id out of range");
+      // the schedule step recovers an entry's arrival tick from its key, budget
+      // and service time, so the three must agree with the key mode
+      if (q[k].svc < 1 || q[k].svc > IM_SVC_MAX * p->d.n_depths)
+        return fail(p, IM_ESTATE, "queued service time out of range");
+      // a chain's later call is queued with what is left of its query's budget (maybe <= 0)
+      if (!ch && q[k].budget < 1) return fail(p, IM_ESTATE, "queued budget < 1");
+      if (ch) {
+        const im_chain& c = qch[i * qcap + k];
+        if (!chain_ok(c) || q[k].svc % c.base_svc != 0 || q[k].svc / c.base_svc > p->d.n_depths)
+          return fail(p, IM_ESTATE, "queued call's chain words out of range");
+      }
+      if (q[k].t_arr < 0 || q[k].t_arr >= tick) return fail(p, IM_ESTATE, "queued arrival tick out of range");
+      const int64_t key = p->d.key_mode == IM_KEY_FCFS ? (int64_t)q[k].t_arr
+                          : (p->d.key_mode == IM_KEY_DEADLINE ? (int64_t)q[k].t_arr + q[k].budget
+                                                              : (int64_t)q[k].t_arr + q[k].budget - q[k].svc);
+      if (key != q[k].key) return fail(p, IM_ESTATE, "queue key does not match t_arr, budget and svc");
     }
     if (bl != ms.backlog) return fail(p, IM_ESTATE, "backlog != sum of queued svc");
     int busy = 0, busy_mask = 0, next_done = INT32_MAX;
@@ -908,6 +957,9 @@ im_status im_write_state(im_pool* p, int32_t env_begin, int32_t env_count, int32
       if (x.id >= 0) {
         ++busy;
         if (x.rem < 1) return fail(p, IM_ESTATE, "busy slot with rem < 1");
+        if (x.t_arr < 0 || x.t_arr >= tick || (!ch && x.budget < 1) || x.id >= envs[e].next_id)
+          return fail(p, IM_ESTATE, "slot arrival tick, budget or id out of range");
+        if (ch && !chain_ok(sch[i * S + s])) return fail(p, IM_ESTATE, "running call's chain words out of range");
         if ((int64_t)x.rem + tick - 1 > INT32_MAX) return fail(p, IM_ESTATE, "slot rem too large");
         busy_mask |= 1 << s;
         next_done = std::min(next_done, x.rem + tick - 1);
@@ -915,6 +967,7 @@ im_status im_write_state(im_pool* p, int32_t env_begin, int32_t env_count, int32
       // device slot: {id, t_arr, completion tick, budget}
       sl[i * S + s] = x.id >= 0 ? make_int4(x.id, x.t_arr, x.rem + tick - 1, x.budget)
                                 : make_int4(-1, 0, 0, 0);
+      if (ch && x.id >= 0) slx[i * S + s] = pack(sch[i * S + s]);
     }
     if (busy != ms.busy) return fail(p, IM_ESTATE, "busy != occupied slots");
     ModelRec& r = recs[i];
@@ -931,6 +984,11 @@ im_status im_write_state(im_pool* p, int32_t env_begin, int32_t env_count, int32
                                (int32_t)((uint32_t)q[k].svc | ((uint32_t)q[k].budget << 16)));
       if (k < im::kFront) fr[i * im::kFront + k] = v;
       else pl[i * qcap + (k - im::kFront)] = v;
+      if (ch) {
+        const int2 x = pack(qch[i * qcap + k]);
+        if (k < im::kFront) frx[i * im::kFront + k] = x;
+        else plx[i * qcap + (k - im::kFront)] = x;
+      }
     }
     int64_t* c = &cnt[i * im::C_NUM];
     c[im::C_REJ_OVERFLOW] = ms.rej_overflow; c[im::C_ENQUEUED] = ms.enqueued;
@@ -952,6 +1010,20 @@ im_status im_write_state(im_pool* p, int32_t env_begin, int32_t env_count, int32
     if (ms.rpm_limit > 0 || ms.rpm_count > 0) p->rpm_active = true;
     r.inv_rpm = ms.rpm_limit > 0 ? (float)(1.0 / ms.rpm_limit) : 0.f;
   }
+  // pending calls, routed at the next tick: the buffer of parity `tick`
+  const int PM = p->pend_cap;
+  std::vector<int4> pr(ch ? (size_t)env_count * PM : 0, make_int4(0, 0, 0, 0));
+  std::vector<int32_t> pcv(ch ? env_count : 0, 0);
+  for (int e = 0; ch && e < env_count; ++e) {
+    if (pcount[e] < 0 || pcount[e] > PM) return fail(p, IM_ESTATE, "pending count out of range");
+    pcv[e] = pcount[e];
+    for (int i = 0; i < pcount[e]; ++i) {
+      const im_pending& x = pend[(size_t)e * PM + i];
+      if (!chain_ok(x.ch) || x.ch.k < 1) return fail(p, IM_ESTATE, "pending call's chain words out of range");
+      const int2 w = pack(x.ch);
+      pr[(size_t)e * PM + i] = make_int4(w.x, w.y, x.deadline, 0);
+    }
+  }
   constexpr int EC = im::kEnvCnt;
   std::vector<int64_t> ec((size_t)env_count * EC);
   for (int e = 0; e < env_count; ++e) {
@@ -968,6 +1040,17 @@ im_status im_write_state(im_pool* p, int32_t env_begin, int32_t env_count, int32
     IM_HIP(p, hipMemcpy(p->qpool + em0 * qcap, pl.data(), pl.size() * sizeof(int4), hipMemcpyHostToDevice));
     IM_HIP(p, hipMemcpy(p->slots + em0 * S, sl.data(), sl.size() * sizeof(int4), hipMemcpyHostToDevice));
     IM_HIP(p, hipMemcpy(p->rpm_ring + em0 * im::kRpmRing, ring.data(), ring.size(), hipMemcpyHostToDevice));
+    if (ch) {
+      IM_HIP(p, hipMemcpy(p->front_ext + em0 * im::kFront, frx.data(), frx.size() * sizeof(int2), hipMemcpyHostToDevice));
+      IM_HIP(p, hipMemcpy(p->pool_ext + em0 * qcap, plx.data(), plx.size() * sizeof(int2), hipMemcpyHostToDevice));
+      IM_HIP(p, hipMemcpy(p->slot_ext + em0 * S, slx.data(), slx.size() * sizeof(int2), hipMemcpyHostToDevice));
+    }
+  }
+  if (ch && env_count) {
+    const size_t par = (size_t)(tick & 1), E = p->d.n_envs;
+    IM_HIP(p, hipMemcpy(p->pcnt + par * E + env_begin, pcv.data(), pcv.size() * 4, hipMemcpyHostToDevice));
+    IM_HIP(p, hipMemcpy(p->pend + (par * E + env_begin) * PM, pr.data(), pr.size() * sizeof(int4),
+                        hipMemcpyHostToDevice));
   }
   if (env_count) {
     IM_HIP(p, hipMemcpy(p->env_cnt + (size_t)env_begin * EC, ec.data(), ec.size() * 8, hipMemcpyHostToDevice));
@@ -977,6 +1060,28 @@ im_status im_write_state(im_pool* p, int32_t env_begin, int32_t env_count, int32
   IM_HIP(p, hipDeviceSynchronize());
   p->t = tick;
   return IM_OK;
+}
+
+extern "C" {
+
+im_status im_write_state(im_pool* p, int32_t env_begin, int32_t env_count, int32_t tick,
+                         const im_env_state* envs, const im_model_state* models,
+                         const im_slot* slots, const im_entry* queues, const int64_t* hist) {
+  if (!p) return fail(nullptr, IM_EINVAL, "pool is NULL");
+  if (p->chains) return fail(p, IM_EUNSUPPORTED, "im_write_state: chain pools restore with im_write_chain_state");
+  return write_state_impl(p, env_begin, env_count, tick, envs, models, slots, queues, hist, nullptr, nullptr,
+                          nullptr, nullptr);
+}
+
+im_status im_write_chain_state(im_pool* p, int32_t env_begin, int32_t env_count, int32_t tick,
+                               const im_env_state* envs, const im_model_state* models,
+                               const im_slot* slots, const im_entry* queues, const int64_t* hist,
+                               const im_chain* queue_chains, const im_chain* slot_chains,
+                               const im_pending* pending, const int32_t* pending_count) {
+  if (!p) return fail(nullptr, IM_EINVAL, "pool is NULL");
+  if (!p->chains) return fail(p, IM_EINVAL, "im_write_chain_state: not a chain pool");
+  return write_state_impl(p, env_begin, env_count, tick, envs, models, slots, queues, hist, queue_chains,
+                          slot_chains, pending, pending_count);
 }
 
 im_status im_read_chain_state(im_pool* p, int32_t env_begin, int32_t env_count, im_chain* queues,

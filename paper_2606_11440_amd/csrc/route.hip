@@ -222,10 +222,15 @@ __device__ __forceinline__ u32x4 gather_bf16(const RouteArgs& a, const RowCtx& c
   if (aligned && k0 >= a.embed_dim) {
     // 8 tail features: two aligned float4 loads of the snapshot row, then
     // the budget feature and zero padding selected by index.
+    // The row is read only when the block holds a load statistic (k2 < 4M):
+    // the 8 floats from k2 then lie inside the row's stride (>= 4M + 9).
     const int k2 = k0 - a.embed_dim;
-    const float* row = a.snap + (size_t)c.e * snap_stride(a.M) + k2;
-    const float4 lo = *(const float4*)row;
-    const float4 hi = *(const float4*)(row + 4);
+    float4 lo = make_float4(0.f, 0.f, 0.f, 0.f), hi = lo;
+    if (k2 < 4 * a.M) {
+      const float* row = a.snap + (size_t)c.e * snap_stride(a.M) + k2;
+      lo = *(const float4*)row;
+      hi = *(const float4*)(row + 4);
+    }
     const float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
     const float fb = (float)c.budget * a.inv_bud;
 #pragma unroll
@@ -261,13 +266,18 @@ __device__ __forceinline__ u32x4 gather_ct(const RouteArgs& a, const RowCtx& c, 
     const uint16_t* emb = (const uint16_t*)a.emb;
     return *(const u32x4*)(emb + (size_t)c.q * ED + k0);
   } else {
+    // the row is read only when the block holds a load statistic (k2 < 4M):
+    // the 8 floats from k2 then lie inside the row's stride (>= 4M + 9)
     const int k2 = k0 - ED;
-    const float* row = a.snap + (size_t)c.e * snap_stride(a.M) + k2;
-    const float4 lo = *(const float4*)row;
-    const float4 hi = *(const float4*)(row + 4);
+    const int n4 = 4 * a.M;
+    float4 lo = make_float4(0.f, 0.f, 0.f, 0.f), hi = lo;
+    if (k2 < n4) {
+      const float* row = a.snap + (size_t)c.e * snap_stride(a.M) + k2;
+      lo = *(const float4*)row;
+      hi = *(const float4*)(row + 4);
+    }
     const float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
     const float fb = (float)c.budget * a.inv_bud;
-    const int n4 = 4 * a.M;
     float f[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
@@ -447,7 +457,7 @@ template <int H, int NL, int AT>
 __global__ __launch_bounds__(256) void route_bf16(RouteArgs a_in) {
   // chain pools: the tick's row count is on the device
   RouteArgs a = a_in;
-  if (a_in.n_total_dev) a.n_total = *a_in.n_total_dev;
+  if (a_in.n_total_dev) a.n_total = min(*a_in.n_total_dev, a_in.n_total);   // the caller's buffers bound it
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n = lane & 31, g = lane >> 5;
   const int32_t row0 = (int32_t)(blockIdx.x * 4 + wave) * 32;
@@ -689,7 +699,7 @@ template <int H, int NL, int AT>
 __global__ __launch_bounds__(256) void route_f32(RouteArgs a_in) {
   // chain pools: the tick's row count is on the device
   RouteArgs a = a_in;
-  if (a_in.n_total_dev) a.n_total = *a_in.n_total_dev;
+  if (a_in.n_total_dev) a.n_total = min(*a_in.n_total_dev, a_in.n_total);   // the caller's buffers bound it
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n = lane & 15, q = lane >> 4;
   const int32_t row0 = (int32_t)(blockIdx.x * 4 + wave) * 16;
@@ -822,7 +832,7 @@ template <int H, int NL, int AT>
 __global__ __launch_bounds__(256) void route_f32s(RouteArgs a_in) {
   // chain pools: the tick's row count is on the device
   RouteArgs a = a_in;
-  if (a_in.n_total_dev) a.n_total = *a_in.n_total_dev;
+  if (a_in.n_total_dev) a.n_total = min(*a_in.n_total_dev, a_in.n_total);   // the caller's buffers bound it
   constexpr int TH = H / 16, TQ = TH / 4, KGH = H / 16;
   static_assert(TH % 4 == 0, "hidden tiles split four ways");
   __shared__ f32x4 hs[TH * 64];
@@ -949,7 +959,7 @@ template <int H, int NL, int AT, int KB1, bool W1L, int NW, int ED, int NR, int 
 __global__ __launch_bounds__(NW * 64, 1) void route_bf16_lds(RouteArgs a_in) {
   // chain pools: the tick's row count is on the device
   RouteArgs a = a_in;
-  if (a_in.n_total_dev) a.n_total = *a_in.n_total_dev;
+  if (a_in.n_total_dev) a.n_total = min(*a_in.n_total_dev, a_in.n_total);   // the caller's buffers bound it
   constexpr int TH = H / 32;
   constexpr int KH = H / 16;
   constexpr int N_W1 = TH * KB1 * 64;
@@ -1166,7 +1176,7 @@ template <int H, int AT, int KB1, int ED, int NW, int RL>
 __global__ __launch_bounds__(NW * 64, 1) void route_bf16_stream(RouteArgs a_in) {
   // chain pools: the tick's row count is on the device
   RouteArgs a = a_in;
-  if (a_in.n_total_dev) a.n_total = *a_in.n_total_dev;
+  if (a_in.n_total_dev) a.n_total = min(*a_in.n_total_dev, a_in.n_total);   // the caller's buffers bound it
   constexpr int TH = H / 32, KH = H / 16;
   constexpr int S1 = TH / 2;                  // layer-1 stages (two output tiles each)
   constexpr int NST = S1 + TH;                // stages per block step
@@ -1415,7 +1425,7 @@ template <int ED, int NW, int NR, int RL>
 __global__ __launch_bounds__(NW * 64, 1) void route_dual_bf16(RouteArgs a_in) {
   // chain pools: the tick's row count is on the device
   RouteArgs a = a_in;
-  if (a_in.n_total_dev) a.n_total = *a_in.n_total_dev;
+  if (a_in.n_total_dev) a.n_total = min(*a_in.n_total_dev, a_in.n_total);   // the caller's buffers bound it
   static_assert(ED % 64 == 0, "embedding width must be a multiple of 64");
   constexpr int KBQ = ED / 16;          // K steps of the query half
   constexpr int NG = ED / 64;           // 64-element groups

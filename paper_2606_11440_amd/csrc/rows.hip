@@ -41,6 +41,13 @@ __global__ __launch_bounds__(kScanThreads) void rows_scan_kernel(RowsArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int32_t t = a.ms[0].t;
   const int32_t* pc = a.pcnt + (size_t)(t & 1) * a.E;
+  // The rows are laid out by a scan over the arrival CSR, so it must be one
+  // monotone partition of [0, n_total); otherwise no arrival is usable (every
+  // env then skips the tick in the schedule step).
+  int broken = 0;
+  if (tid == 0) broken = a.offsets[0] != 0 || a.offsets[a.E] != a.n_total;
+  for (int e = tid; e < a.E; e += kScanThreads) broken |= a.offsets[e + 1] < a.offsets[e];
+  const bool whole = __syncthreads_or(broken) == 0;
   int32_t carry = 0;
   for (int base = 0; base < a.E; base += kScanThreads * kPer) {
     int32_t c[kPer];
@@ -48,7 +55,7 @@ __global__ __launch_bounds__(kScanThreads) void rows_scan_kernel(RowsArgs a) {
 #pragma unroll
     for (int j = 0; j < kPer; ++j) {
       const int e = base + tid * kPer + j;
-      c[j] = e < a.E ? pc[e] + usable_arrivals(a, e) : 0;
+      c[j] = e < a.E ? pc[e] + (whole ? usable_arrivals(a, e) : 0) : 0;
       sum += c[j];
     }
     const int32_t x = wave_incl_scan(sum, lane);
@@ -72,6 +79,7 @@ __global__ __launch_bounds__(kScanThreads) void rows_scan_kernel(RowsArgs a) {
   if (tid == 0) {
     a.roff[a.E] = carry;
     a.n_rows[0] = carry;
+    a.n_rows[1] = whole ? 0 : 1;
   }
 }
 
@@ -91,7 +99,7 @@ __global__ __launch_bounds__(256) void rows_gather_kernel(RowsArgs a) {
     a.rb[base + i] = (int16_t)remaining_budget(p.z, t);
     a.rr[base + i] = (int16_t)(a.n_roles > 0 ? (chain_role0(p.y) + chain_k(p.x)) % a.n_roles : 0);
   }
-  const int32_t na = usable_arrivals(a, e);
+  const int32_t na = a.n_rows[1] == 0 ? usable_arrivals(a, e) : 0;   // written by the scan kernel
   const int32_t lo = a.offsets[e];
   for (int i = lane; i < na; i += 64) {
     a.rq[base + pc + i] = a.q_idx[lo + i];

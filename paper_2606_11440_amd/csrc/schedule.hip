@@ -409,7 +409,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
   static_assert(IM_MAX_MODELS < 63, "model 63 marks rows not admitted");
   const int lane = threadIdx.x & 63;
   const int wv = threadIdx.x >> 6;
-  const int e = (int)blockIdx.x * 4 + wv;
+  const int e = (int)blockIdx.x * (int)(blockDim.x >> 6) + wv;   // 1, 2 or 4 envs per block
   if (e >= a.E) return;
   int4* st = stage[wv];
   int32_t* hist_s = hist_lds[wv];
@@ -434,6 +434,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
   const int32_t lo = a.offsets[e], hi = a.offsets[e + 1];
   int32_t bad = 0;
   if (lo < 0 || hi < lo || hi > a.n_total || hi - lo > a.max_arrivals) bad = IM_ERR_COUNT;
+  if (CHAIN && *a.csr_bad != 0) bad = IM_ERR_COUNT;   // the rows build found no usable arrival
   // The tick and the next request id live in the env's first record in
   // device memory, so a captured sequence of ticks replays with the right time.
   const int32_t next_id = rl(r2.y, 0);
@@ -1097,15 +1098,16 @@ hipError_t launch_snapshot(const SchedArgs& a, int e0, int ne, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_schedule(const SchedArgs& a, bool rpm, bool chain, hipStream_t s) {
-  const int64_t waves = (int64_t)a.E;
-  const unsigned blocks = (unsigned)((waves + 3) / 4);
+hipError_t launch_schedule(const SchedArgs& a, bool rpm, bool chain, int waves_per_block, hipStream_t s) {
+  const int w = waves_per_block == 1 || waves_per_block == 2 ? waves_per_block : 4;
+  const unsigned blocks = (unsigned)(((int64_t)a.E + w - 1) / w);
+  const dim3 threads(64 * w);
   if (chain) {
-    if (rpm) hipLaunchKernelGGL((schedule_kernel<true, true>), dim3(blocks), dim3(256), 0, s, a);
-    else hipLaunchKernelGGL((schedule_kernel<false, true>), dim3(blocks), dim3(256), 0, s, a);
+    if (rpm) hipLaunchKernelGGL((schedule_kernel<true, true>), dim3(blocks), threads, 0, s, a);
+    else hipLaunchKernelGGL((schedule_kernel<false, true>), dim3(blocks), threads, 0, s, a);
   } else {
-    if (rpm) hipLaunchKernelGGL((schedule_kernel<true, false>), dim3(blocks), dim3(256), 0, s, a);
-    else hipLaunchKernelGGL((schedule_kernel<false, false>), dim3(blocks), dim3(256), 0, s, a);
+    if (rpm) hipLaunchKernelGGL((schedule_kernel<true, false>), dim3(blocks), threads, 0, s, a);
+    else hipLaunchKernelGGL((schedule_kernel<false, false>), dim3(blocks), threads, 0, s, a);
   }
   return hipGetLastError();
 }

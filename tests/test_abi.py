@@ -53,3 +53,95 @@ def test_binding_fails_loudly_without_library(tmp_path, monkeypatch):
     monkeypatch.setattr(L, "_lib", None)
     with pytest.raises(RuntimeError):
         L.load()
+
+
+def test_null_pool_rejected_by_every_entry_point():
+    """Every call that takes a pool answers IM_EINVAL for a NULL pool (and
+    im_destroy ignores it) without touching a device."""
+    import paper_2606_11440_amd as P
+    L = P._lib.load()
+    E = P._lib.IM_EINVAL
+    calls = {
+        "im_route": lambda: L.im_route(None, None, None, None, None),
+        "im_route_sample": lambda: L.im_route_sample(None, None, 0, 0, None, None),
+        "im_schedule": lambda: L.im_schedule(None, None, None, None),
+        "im_tick": lambda: L.im_tick(None, None, None, None),
+        "im_get_rows": lambda: L.im_get_rows(None, None),
+        "im_dual_update": lambda: L.im_dual_update(None, 0.1, 1.0, None, None),
+        "im_set_enabled": lambda: L.im_set_enabled(None, 0, 0, 1, None),
+        "im_set_capacity": lambda: L.im_set_capacity(None, 0, 0, 1, None),
+        "im_set_rpm_limit": lambda: L.im_set_rpm_limit(None, 0, 0, 1, None),
+        "im_set_launch": lambda: L.im_set_launch(None, -1, 4),
+        "im_get_error": lambda: L.im_get_error(None, None),
+        "im_clear_error": lambda: L.im_clear_error(None),
+        "im_read_state": lambda: L.im_read_state(None, 0, 1, None, None, None, None, None, None),
+        "im_write_state": lambda: L.im_write_state(None, 0, 1, 0, None, None, None, None, None),
+        "im_write_chain_state": lambda: L.im_write_chain_state(None, 0, 1, 0, None, None, None, None,
+                                                               None, None, None, None, None),
+        "im_read_chain_state": lambda: L.im_read_chain_state(None, 0, 1, None, None, None, None),
+    }
+    for name, f in calls.items():
+        assert f() == E, name
+    L.im_destroy(None)
+    assert isinstance(P.im_last_error(None), str)
+
+
+def _valid_c2_desc():
+    import paper_2606_11440_amd as P
+    import workload
+    cfg = workload.configs.get("c2", E=4)
+    return cfg, P._lib.make_desc(cfg)
+
+
+def test_invalid_descriptions_rejected_without_gpu_work():
+    """im_pool_create checks the description, the capacities and its pointer
+    arguments before any device allocation: each case below is IM_EINVAL (or
+    IM_EUNSUPPORTED for shapes no kernel covers)."""
+    import numpy as np
+    import paper_2606_11440_amd as P
+    L = P._lib.load()
+    cfg, base = _valid_c2_desc()
+    W = [np.zeros((w, i), np.float32) for w, i in zip(cfg["widths"], [cfg["feat_dim"]] + cfg["widths"][:-1])]
+    b = [np.zeros(w, np.float32) for w in cfg["widths"]]
+    Wp = (ctypes.c_void_p * 3)(*[w.ctypes.data for w in W])
+    bp = (ctypes.c_void_p * 3)(*[x.ctypes.data for x in b])
+    cap_ok = np.ones(cfg["E"] * cfg["M"], np.int32)
+    emb = ctypes.c_void_p(1)   # never dereferenced: every case is rejected first
+
+    def create(mut=None, cap=cap_ok, nq=16, w=Wp, bb=bp):
+        d = P._lib.ImPoolDesc()
+        ctypes.memmove(ctypes.byref(d), ctypes.byref(base), ctypes.sizeof(d))
+        if mut:
+            mut(d)
+        out = ctypes.c_void_p()
+        st = L.im_pool_create(ctypes.byref(d), w, bb, emb, nq, cap.ctypes.data, None, None, ctypes.byref(out))
+        assert not out.value
+        return st
+
+    def setw(i, v):
+        return lambda d: d.widths.__setitem__(i, v)
+
+    cases = [
+        lambda d: setattr(d, "n_envs", 0), lambda d: setattr(d, "n_models", 0),
+        lambda d: setattr(d, "n_models", 33), lambda d: setattr(d, "n_depths", 0),
+        lambda d: setattr(d, "n_depths", 13),                     # M*K = 65 > 64
+        lambda d: setattr(d, "queue_cap", 0), lambda d: setattr(d, "queue_cap", 16385),
+        lambda d: setattr(d, "max_slots", 0), lambda d: setattr(d, "max_slots", 9),
+        lambda d: setattr(d, "embed_dim", 0), lambda d: setattr(d, "feat_dim", 84),
+        lambda d: setattr(d, "feat_dim", 513), lambda d: setattr(d, "n_layers", 1),
+        lambda d: setattr(d, "n_layers", 4), setw(2, 14),         # last width != M*K
+        lambda d: setattr(d, "dtype", 7), lambda d: setattr(d, "key_mode", 3),
+        lambda d: setattr(d, "max_arrivals_per_env_tick", 0), lambda d: setattr(d, "budget_max", 0),
+        lambda d: setattr(d, "value_head", 2), lambda d: setattr(d, "max_steps", 16),
+        lambda d: setattr(d, "net", 5),
+    ]
+    for i, mut in enumerate(cases):
+        assert create(mut) in (P._lib.IM_EINVAL, P._lib.IM_EUNSUPPORTED), i
+    assert create(setw(0, 100)) == P._lib.IM_EUNSUPPORTED      # hidden widths differ
+    for c in (-1, cfg["max_slots"] + 1):
+        bad = cap_ok.copy()
+        bad[3] = c
+        assert create(cap=bad) == P._lib.IM_EINVAL
+    assert create(nq=0) == P._lib.IM_EINVAL
+    assert create(w=None) == P._lib.IM_EINVAL
+    assert create(bb=None) == P._lib.IM_EINVAL

@@ -155,6 +155,29 @@ def test_checkpoint_resume_equals_uninterrupted():
     b.close()
 
 
+def test_write_state_rejects_inconsistent_entries():
+    """A queued entry whose key is not the key mode's function of its arrival
+    tick, budget and service time, or whose arrival tick is not before the
+    snapshot's tick, is IM_ESTATE (the schedule step recovers arrival ticks
+    from keys); nothing changes."""
+    torch = need_gpu()
+    import paper_2606_11440_amd as P
+    cfg = workload.configs.get("c2", E=4, T=12, lam=16.0)
+    p = Pair(cfg, seed=28, Q=128)
+    for t in range(10):
+        p.step(p.arrivals(t))
+    snap = p.gpu.state()
+    e, m = np.argwhere(snap["qlen"] > 0)[0]
+    for field, delta in ((0, 1), (2, 1), (4, 1), (2, 10**6)):    # key, t_arr, budget, t_arr >= tick
+        s2 = {k: np.array(v) for k, v in snap.items()}
+        s2["queues"][e, m, 0, field] += delta
+        with pytest.raises(P.IMError) as ei:
+            p.gpu.write_state(0, s2)
+        assert ei.value.status == P._lib.IM_ESTATE, (field, delta)
+    assert_state_equal(p.gpu.state(), snap, ctx="unchanged")
+    p.close()
+
+
 def test_determinism_two_runs():
     torch = need_gpu()
     import paper_2606_11440_amd as P

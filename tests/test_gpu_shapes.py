@@ -19,6 +19,9 @@ SHAPES = [
     ("f32_h64_3layer_64act", "c1", dict(M=16, K=4, feat_dim=130, widths=[64, 64, 64])),
     ("bf16_h128_3layer", "c2", dict(widths=[128, 128, 15])),
     ("bf16_h64_2layer_64act", "c2", dict(M=16, K=4, feat_dim=130, widths=[64, 64])),
+    # 40 zero features past [emb | 4M stats | budget]: the vector gather must not read the
+    # snapshot row past the load statistics
+    ("bf16_h256_3layer_feat_pad40", "c2", dict(feat_dim=64 + 4 * 5 + 1 + 40)),
 ]
 
 

@@ -345,3 +345,36 @@ def test_dual_pool_rotates_roles():
                 checked += 1
         o.schedule(arr, act)
     assert checked > 5
+
+
+def test_broken_csr_skips_every_env():
+    """Chain pools lay each env's rows out by a scan over the arrival offsets,
+    so offsets that are not one monotone partition of [0, n_total) (here env 2
+    re-reads env 0's records) make no arrival usable: every env keeps its
+    state and pending calls, only the tick advances; a single-step pool with
+    the same offsets still judges each env on its own range."""
+    cfg = workload.configs.get("c2c", E=3, T=10)
+    o, _ = make_oracle(cfg, seed=8, Q=64)
+    cnt = workload.gen.counts(cfg, 8)
+    for t in range(6):
+        o.tick(workload.gen.tick(cfg, 8, t, cnt[t], 64))
+    arr = workload.gen.tick(cfg, 8, 6, np.array([4, 2, 2], np.int32), 64)
+    arr["offsets"] = np.array([0, 4, 2, 8], np.int32)     # env 1 [4, 2), env 2 [2, 8)
+    before, ch0, t0 = o.state(), o.chain_state(), o.t
+    ro = o.row_offsets(arr)
+    np.testing.assert_array_equal(np.diff(ro), ch0["pending_count"])   # pending calls only
+    o.tick(arr)
+    assert o.error & oracle.ERR_COUNT and o.t == t0 + 1
+    after, ch1 = o.state(), o.chain_state()
+    for k in ("qlen", "enqueued", "started", "completed", "arrived", "busy", "ewma", "backlog"):
+        np.testing.assert_array_equal(after[k], before[k], err_msg=k)
+    np.testing.assert_array_equal(ch1["pending_count"], ch0["pending_count"])
+    np.testing.assert_array_equal(ch1["pending"], ch0["pending"])
+    # single-step pool: env 1 alone is rejected, envs 0 and 2 are served
+    cfg1 = workload.configs.get("c2", E=3, T=10)
+    o1, _ = make_oracle(cfg1, seed=8, Q=64)
+    arr1 = {k: v for k, v in arr.items() if k != "n_steps"}
+    o1.tick(arr1)
+    assert o1.error & oracle.ERR_COUNT
+    s1 = o1.state()
+    assert s1["arrived"][0] == 4 and s1["arrived"][1] == 0 and s1["arrived"][2] == 6
