@@ -296,6 +296,18 @@ im_status im_schedule(im_pool* pool, const im_arrivals* arr, const int32_t* acti
  *                (then a pool-owned buffer is used) */
 im_status im_tick(im_pool* pool, const im_arrivals* arr, int32_t* actions_out, void* stream);
 
+/* im_tick for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation): the
+ * actions passed from the route step to the schedule step are staged in a
+ * static device array of 2^21 rows (8 MiB; each GPU holds its own from the
+ * first pool created on it until the process ends) instead of a pool buffer.
+ * Allocates nothing. All calls on one GPU share that array: calls that
+ * overlap on one GPU (concurrent streams, other threads) race and must not be
+ * issued. IM_EINVAL when the tick's rows (n_total, plus n_envs * n_models *
+ * max_slots pending calls in a chain pool) exceed 2^21; the results equal
+ * im_tick's. */
+im_status im_tick_noalloc(im_pool* pool, const im_arrivals* arr, void* stream);
+
 /* Free every resource of the pool (synchronises). NULL is ignored. */
 void im_destroy(im_pool* pool);
 

@@ -16,6 +16,7 @@ from ._lib import (EXPORTED, IMError, im_clear_error, im_destroy, im_dual_update
                    im_route_sample,
                    im_schedule,
                    im_set_capacity, im_set_enabled, im_set_launch, im_set_rpm_limit, im_tick,
+                   im_tick_noalloc,
                    im_write_chain_state,
                    im_write_state,
                    make_arrivals,
@@ -68,6 +69,9 @@ class Pool:
 
     def tick(self, arr, actions_out=None, stream=None):
         im_tick(self.h, arr, actions_out, stream)
+
+    def tick_noalloc(self, arr, stream=None):
+        im_tick_noalloc(self.h, arr, stream)
 
     def state(self, env_begin=0, env_count=None, with_queues=True):
         n = self.E - env_begin if env_count is None else env_count

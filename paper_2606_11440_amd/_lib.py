@@ -25,7 +25,7 @@ IM_NET_MLP, IM_NET_DUAL = 0, 1
 EXPORTED = ("im_pool_create", "im_pool_create_dual", "im_route", "im_route_sample", "im_schedule", "im_tick", "im_destroy",
             "im_dual_update", "im_set_rpm_limit", "im_get_rows", "im_read_chain_state",
             "im_read_state", "im_write_state", "im_write_chain_state", "im_set_enabled", "im_set_capacity",
-            "im_get_error", "im_clear_error", "im_last_error", "im_set_launch")
+            "im_get_error", "im_clear_error", "im_last_error", "im_set_launch", "im_tick_noalloc")
 
 
 class ImPoolDesc(ctypes.Structure):
@@ -120,6 +120,7 @@ def load() -> ctypes.CDLL:
     L.im_set_capacity.argtypes = [P, I32, I32, I32, P]
     L.im_set_rpm_limit.argtypes = [P, I32, I32, I32, P]
     L.im_set_launch.argtypes = [P, I32, I32]
+    L.im_tick_noalloc.argtypes = [P, ctypes.POINTER(ImArrivals), P]
     L.im_get_rows.argtypes = [P, ctypes.POINTER(ImRows)]
     L.im_read_chain_state.argtypes = [P, I32, I32, P, P, P, P]
     L.im_get_error.argtypes = [P, ctypes.POINTER(I32)]
@@ -253,6 +254,11 @@ def im_schedule(pool, arr: ImArrivals, actions, stream=None):
 
 def im_tick(pool, arr: ImArrivals, actions_out=None, stream=None):
     _check(load().im_tick(pool, ctypes.byref(arr), _dptr(actions_out), _stream(stream)), pool)
+
+
+def im_tick_noalloc(pool, arr: ImArrivals, stream=None):
+    """im_tick with the actions staged in the library's static device array."""
+    _check(load().im_tick_noalloc(pool, ctypes.byref(arr), _stream(stream)), pool)
 
 
 def im_dual_update(pool, eta: float, lambda_max: float, lam, stream=None):

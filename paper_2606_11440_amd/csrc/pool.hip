@@ -9,6 +9,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -63,6 +64,7 @@ struct im_pool {
   int32_t cu_count = 0;
   int32_t route_blocks = -1;   // grid of the persistent route kernels (-1: one block per CU; 0: none)
   int32_t sched_waves = 4;     // envs per block of the schedule kernel
+  int32_t* scratch = nullptr;  // this device's static actions staging (im_tick_noalloc)
   bool rpm_active = false;   // some model was given a rate limit (the windows are tracked from then on)
   std::string last_error;
 };
@@ -70,6 +72,35 @@ struct im_pool {
 static im::SchedArgs sched_args(im_pool* p);
 
 namespace {
+
+// Actions staging of im_tick_noalloc (one int32 per row of a tick, written by
+// the route step and read by the schedule step), for callers that cannot
+// allocate. A file-scope device array: every GPU the library runs on holds
+// its own copy until the process ends, and calls on one GPU share it (each
+// call overwrites every row it reads, so nothing has to start at zero; calls
+// that overlap on one GPU race). In host code `scratch` names a host-side
+// stand-in: its device address on the current device comes from
+// hipGetSymbolAddress, resolved once per device (scratch_on) and used from
+// then on.
+constexpr int64_t kScratchRows = int64_t(1) << 21;   // 8 MiB
+static __device__ __align__(256) int32_t scratch[kScratchRows];
+std::mutex g_scratch_mu;
+std::vector<int32_t*> g_scratch_dev;   // per device ordinal; nullptr until resolved
+
+// The address of `scratch` on device `dev`, which must be the current device.
+hipError_t scratch_on(int dev, int32_t** out) {
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (dev < 0) return hipErrorInvalidDevice;
+  if ((size_t)dev >= g_scratch_dev.size()) g_scratch_dev.resize((size_t)dev + 1, nullptr);
+  if (!g_scratch_dev[dev]) {
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_dev[dev] = static_cast<int32_t*>(ptr);
+  }
+  *out = g_scratch_dev[dev];
+  return hipSuccess;
+}
 
 std::string g_create_error = "no error";
 
@@ -202,6 +233,8 @@ im_pool* new_pool(const im_pool_desc& d, int64_t n_queries, const void* emb) {
   if (hipDeviceGetAttribute(&p->cu_count, hipDeviceAttributeMultiprocessorCount, p->device) !=
       hipSuccess)
     p->cu_count = 0;
+  // the static actions staging of this device (im_tick_noalloc reports its absence)
+  if (scratch_on(p->device, &p->scratch) != hipSuccess) p->scratch = nullptr;
   return p;
 }
 
@@ -691,6 +724,22 @@ im_status im_tick(im_pool* p, const im_arrivals* arr, int32_t* actions_out, void
   im_status st = check_arrivals(p, arr);
   if (st != IM_OK) return st;
   int32_t* act = actions_out ? actions_out : p->act_buf;
+  st = route_impl(p, arr, route_args(p, arr, act, nullptr), (hipStream_t)stream);
+  if (st != IM_OK) return st;
+  return schedule_impl(p, arr, act, false, (hipStream_t)stream);
+}
+
+im_status im_tick_noalloc(im_pool* p, const im_arrivals* arr, void* stream) {
+  if (!p) return fail(nullptr, IM_EINVAL, "pool is NULL");
+  im_status st = check_arrivals(p, arr);
+  if (st != IM_OK) return st;
+  // rows of the tick: the arrivals, and a chain pool's pending calls on top
+  const int64_t rows = (int64_t)arr->n_total + (p->chains ? (int64_t)p->d.n_envs * p->pend_cap : 0);
+  if (rows > kScratchRows)
+    return fail(p, IM_EINVAL, "im_tick_noalloc: the tick's rows (" + std::to_string(rows) +
+                                  ") exceed its static staging of 2^21 rows; use im_tick");
+  if (!p->scratch) return fail(p, IM_EHIP, "im_tick_noalloc: static staging unavailable on this device");
+  int32_t* act = p->scratch;
   st = route_impl(p, arr, route_args(p, arr, act, nullptr), (hipStream_t)stream);
   if (st != IM_OK) return st;
   return schedule_impl(p, arr, act, false, (hipStream_t)stream);
