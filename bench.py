@@ -108,28 +108,77 @@ def load_traffic(kernel, workload_tag, src_hash):
     return d.get("hbm_bytes_per_launch")
 
 
+def cpu_model():
+    """The host CPU's model name (lscpu, else /proc/cpuinfo)."""
+    try:
+        import subprocess
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in out.splitlines():
+            if line.startswith("Model name:"):
+                return line.split(":", 1)[1].strip()
+    except (OSError, ValueError, subprocess.SubprocessError):
+        pass
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+# Worker threads of the oracle baseline: the host cores this process may use,
+# at most the 16 a one-GPU share of the host provides.
+CPU_SHARE = 16
+
+
 def cpu_baseline(cfg, W, b, emb_vals, cap, lb, ticks, Q, budget_s=15.0):
-    """The oracle on the host cores over a bounded sample: the first
-    `envs` envs over as many of the timed ticks as fit in ~budget_s."""
+    """The oracle on the host cores over a bounded sample of the workload:
+    blocks of `envs` consecutive envs, each over the timed ticks, for about
+    2/3 of budget_s with every worker thread; then blocks of envs / threads
+    envs on one thread for the rest (the single-thread rate)."""
     import oracle
     import workload
-    threads = max(1, min(16, os.cpu_count() or 1))
+    usable = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
+    threads = max(1, min(CPU_SHARE, usable))
     envs = min(cfg["E"], 8 * threads)
-    o = oracle.Oracle(cfg, W, b, emb_vals, cap[:envs], lb, E=envs, threads=threads,
-                      roles=b if cfg.get("net") == "dual" else None)
-    subs = [workload.gen.subset(a, 0, envs) for a in ticks]
-    t0 = time.perf_counter()
-    done = 0
-    for a in subs:
-        o.tick(a)
-        done += 1
-        if time.perf_counter() - t0 > budget_s:
-            break
-    dt = time.perf_counter() - t0
-    nreq = sum(int(s["q_idx"].size) for s in subs[:done])
-    return {"value": envs * done / dt, "unit": "env-ticks/s", "cores": threads, "kind": "oracle",
-            "sample": f"envs [0,{envs}) x first {done} ticks ({nreq} requests), "
-                      f"{dt:.1f} s wall, {nreq / dt:.0f} routed req/s"}
+    roles = b if cfg.get("net") == "dual" else None
+
+    def run(nthreads, n_envs, seconds):
+        """Blocks of n_envs consecutive envs, each over the timed ticks, until
+        `seconds` have passed (at least one tick)."""
+        t0 = time.perf_counter()
+        env_ticks, nreq, blocks, done = 0, 0, 0, 0
+        for e0 in range(0, cfg["E"] - n_envs + 1, n_envs):
+            o = oracle.Oracle(cfg, W, b, emb_vals, cap[e0:e0 + n_envs], lb, E=n_envs, threads=nthreads,
+                              roles=roles)
+            blocks += 1
+            for a in ticks:
+                sub = workload.gen.subset(a, e0, e0 + n_envs)
+                o.tick(sub)
+                env_ticks += n_envs
+                nreq += int(sub["q_idx"].size)
+                done += 1
+                if time.perf_counter() - t0 > seconds:
+                    break
+            if time.perf_counter() - t0 > seconds:
+                break
+        dt = time.perf_counter() - t0
+        return env_ticks / dt, nreq / dt, blocks, done, nreq, dt
+
+    v, rq, blocks, done, nreq, dt = run(threads, envs, budget_s * 2 / 3)
+    env1 = max(1, envs // threads)
+    v1, rq1, blocks1, done1, _, dt1 = run(1, env1, budget_s / 3)
+    return {"value": v, "unit": "env-ticks/s", "cores": threads, "kind": "oracle",
+            "sample": f"{blocks} block(s) of {envs} envs over the {len(ticks)} timed ticks ({done} env-block "
+                      f"ticks, {nreq} requests), {dt:.1f} s wall, {rq:.0f} routed req/s",
+            "nproc": os.cpu_count(), "usable_cpus": usable, "cpu_model": cpu_model(),
+            "threads_note": f"one oracle worker thread per env block, min({CPU_SHARE}, usable CPUs): "
+                            f"{CPU_SHARE} is the host share of one GPU on the machines this runs on",
+            "single_thread": {"value": v1, "unit": "env-ticks/s", "routed_req_per_s": rq1,
+                              "sample": f"{blocks1} block(s) of {env1} envs, {done1} env-block ticks, "
+                                        f"{dt1:.1f} s wall"}}
 
 
 def mfma_probe(torch, zeros=False):
@@ -211,6 +260,9 @@ def main():
                          "value head) then im_schedule with the sampled actions")
     ap.add_argument("--no-peak-probe", action="store_true",
                     help="skip the measured-peak probes (a large bf16 GEMM and a device copy)")
+    ap.add_argument("--per-tick", default=None, metavar="FILE",
+                    help="write the instrumented pass's route and schedule durations of every "
+                         "timed tick (microseconds) to FILE as JSON")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run 5 device-to-device copies of MIB MiB (calibrates "
                          "the HBM byte counters of a profiler against a known size)")
@@ -368,13 +420,22 @@ def main():
     routed = sum(n_req[W_:W_ + K])
     value = env_ticks / (gpu_ms / 1e3)
 
-    # ---- roofline of the dominant kernel ----
+    if args.per_tick:
+        with open(args.per_tick, "w") as f:
+            json.dump({"workload": args.config, "lam": cfg["lam"], "first_tick": W_,
+                       "route_us": [x * 1e3 for x in route_ms], "schedule_us": [x * 1e3 for x in sched_ms],
+                       "requests": n_req[W_:W_ + K]}, f)
+
+    # ---- rooflines: the dominant kernel ("roofline"), then the other one ----
     route_avg = float(np.mean(route_ms))
     sched_avg = float(np.mean(sched_ms))
     flops = np.mean([algorithmic_flops_per_tick(cfg, n) for n in n_req[W_:W_ + K]])
     peak_f = PEAK_BF16_TFLOPS if cfg["dtype"] == "bf16" else PEAK_F32_TFLOPS
     tag = f"{args.config}_lam{int(cfg['lam'])}" + ("_sample" if args.sample else "")
-    if route_avg >= sched_avg:
+
+    def route_roof():
+        # the binding roof of the route step: the larger of its matrix time
+        # and its HBM time at nominal peaks
         # the binding roof of the route step: the larger of its matrix time
         # and its HBM time at nominal peaks
         rbytes = np.mean([algorithmic_bytes_route(cfg, n, args.sample) for n in n_req[W_:W_ + K]])
@@ -382,26 +443,33 @@ def main():
         traffic = load_traffic("route", tag, source_hash("route.hip"))
         if flops / (peak_f * 1e12) >= rbytes / (PEAK_HBM_GBS * 1e9):
             achieved = flops / (route_avg * 1e-3) / 1e12
-            roof = {"kernel": kname, "bound": "mfma", "achieved": achieved,
+            return {"kernel": kname, "bound": "mfma", "achieved": achieved,
                     "peak": peak_f, "unit": "TFLOP/s", "frac": achieved / peak_f,
                     "traffic": traffic, "avg_launch_us": route_avg * 1e3,
                     "algorithmic_per_launch": f"{flops:.4g} FLOP"}
-        else:
-            achieved = rbytes / (route_avg * 1e-3) / 1e9
-            roof = {"kernel": kname, "bound": "hbm", "achieved": achieved,
-                    "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS,
-                    "traffic": traffic, "avg_launch_us": route_avg * 1e3,
-                    "algorithmic_per_launch": f"{rbytes:.4g} B ({flops:.4g} FLOP)"}
-    else:
+        achieved = rbytes / (route_avg * 1e-3) / 1e9
+        return {"kernel": kname, "bound": "hbm", "achieved": achieved,
+                "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS,
+                "traffic": traffic, "avg_launch_us": route_avg * 1e3,
+                "algorithmic_per_launch": f"{rbytes:.4g} B ({flops:.4g} FLOP)"}
+
+    def schedule_roof():
+        # per-tick averages over the ticks that ran (warm-up and timed)
+        ran = W_ + K
         enq = int(st["enqueued"].sum())
         sta = int(st["started"].sum())
-        byts = algorithmic_bytes_schedule(cfg, routed / K, enq / T, sta / T)
+        byts = algorithmic_bytes_schedule(cfg, routed / K, enq / ran, sta / ran)
         achieved = byts / (sched_avg * 1e-3) / 1e9
-        roof = {"kernel": "schedule", "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS,
+        return {"kernel": "schedule", "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS,
                 "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS,
                 "traffic": load_traffic("schedule", tag, source_hash("schedule.hip")),
                 "avg_launch_us": sched_avg * 1e3,
-                "algorithmic_per_launch": f"{byts:.4g} B"}
+                "algorithmic_per_launch": f"{byts:.4g} B",
+                "note": "issue- and latency-bound: one wave per env at 4 waves per SIMD; the HBM "
+                        "fraction is reported, not a bound it approaches"}
+
+    roof, roof_other = (route_roof(), schedule_roof()) if route_avg >= sched_avg else \
+        (schedule_roof(), route_roof())
 
     if not args.no_peak_probe:
         mp = measured_peaks(torch)
@@ -441,6 +509,7 @@ def main():
                            if chains else ""),
                        "host_wall_ms_timed": wall * 1e3},
         "roofline": roof,
+        "roofline_other_kernel": roof_other,
         "input_gen_s": gen_s,
     }
     if not args.no_cpu_baseline:
