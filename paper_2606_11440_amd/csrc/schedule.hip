@@ -50,6 +50,13 @@ __device__ __forceinline__ int32_t t_arr_of(int32_t key, int32_t svcbud, int key
   return (int32_t)(key_mode == IM_KEY_DEADLINE ? k - bud : (key_mode == IM_KEY_FCFS ? k : k - bud + svc));
 }
 
+// A wave-uniform 32-bit load through the scalar data cache, for data no
+// kernel of the tick writes while this one runs (the offsets, the rows
+// build's results).
+__device__ __forceinline__ int32_t load_uniform(const int32_t* p) {
+  return *(const __attribute__((address_space(4))) int32_t*)p;
+}
+
 // Makes this wave's earlier global stores visible to its later loads.
 __device__ __forceinline__ void wave_mem_sync() { __threadfence_block(); }
 
@@ -393,7 +400,7 @@ __device__ __forceinline__ void counter_add(int64_t* p, int64_t v) {
 // completion that is not its query's last call appends the next call, with
 // the query's deadline, to the pending list of the next tick.
 template <bool RPM, bool CHAIN>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void schedule_kernel(SchedArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5, 8))) void schedule_kernel(SchedArgs a) {
   // sorted chunks; in the service phase the refill scan's key buffer, then
   // the counter staging
   __shared__ int4 stage[4][kStageChunks * 64];
@@ -408,7 +415,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
   static_assert(kStageChunks * 64 >= (C_NUM / 2) * IM_MAX_MODELS, "the counter staging fits the stage");
   static_assert(IM_MAX_MODELS < 63, "model 63 marks rows not admitted");
   const int lane = threadIdx.x & 63;
-  const int wv = threadIdx.x >> 6;
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
   const int e = (int)blockIdx.x * (int)(blockDim.x >> 6) + wv;   // 1, 2 or 4 envs per block
   if (e >= a.E) return;
   int4* st = stage[wv];
@@ -422,85 +429,89 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
   ModelRec* recs = a.ms + em0;
   const bool ml = lane < M;   // this lane holds model `lane`
 
-  // ---- model records (lane m: model m), issued before anything else ----
-  int4 r0 = make_int4(0, 0, 0, 0), r1 = r0, r2 = r0, r3 = r0;
-  if (ml) {
-    const int4* rp = reinterpret_cast<const int4*>(recs + lane);
-    r0 = rp[0];
-    r1 = rp[1];
-    r2 = rp[2];
-    r3 = rp[3];
-  }
-  const int32_t lo = a.offsets[e], hi = a.offsets[e + 1];
+  // ---- first loads, issued together: the model records (lane m: model m;
+  // the other lanes read model M - 1's and clear theirs once the rows' loads
+  // are issued) and the env's CSR offsets (scalar loads, so waiting for them
+  // does not wait for the records) ----
+  const int4* rp = reinterpret_cast<const int4*>(recs + (ml ? lane : M - 1));
+  int4 r0 = rp[0], r1 = rp[1], r2 = rp[2], r3 = rp[3];
+  const int32_t lo = load_uniform(a.offsets + e), hi = load_uniform(a.offsets + e + 1);
+  int32_t abase = lo;
+  if constexpr (CHAIN) abase = load_uniform(a.roff + e);   // the rows' outputs start at roff[e]
   int32_t bad = 0;
   if (lo < 0 || hi < lo || hi > a.n_total || hi - lo > a.max_arrivals) bad = IM_ERR_COUNT;
-  if (CHAIN && *a.csr_bad != 0) bad = IM_ERR_COUNT;   // the rows build found no usable arrival
+  if (CHAIN && load_uniform(a.csr_bad) != 0) bad = IM_ERR_COUNT;   // the rows build found no usable arrival
+  const int32_t n = bad ? 0 : hi - lo;   // arrivals
+
+  // ---- the env's rows: the first chunks are loaded (and kept) before
+  // anything waits for them, then validated ----
+  // Row r of the env is a pending call (r < pc, chain pools: valid by
+  // construction; its budget is what is left of its query's) or arrival
+  // lo + r - pc. Single-call pools need only the offsets to load their rows,
+  // so those loads are in flight with the records.
+  constexpr int kKeep = 2;                            // chunks kept in registers
+  int32_t c_ac[kKeep], c_qi[kKeep], c_bu[kKeep], c_sv[kKeep], c_ro[kKeep];
+#pragma unroll
+  for (int c = 0; c < kKeep; ++c) {
+    c_ac[c] = -1;
+    c_qi[c] = 0;
+    c_bu[c] = 1;
+    c_sv[c] = 1;
+    c_ro[c] = 0;
+  }
+  auto load_arrival = [&](int32_t r, int32_t i, int32_t& ac, int32_t& qi, int32_t& bu, int32_t& sv, int32_t& ro) {
+    ac = a.actions[abase + r];
+    qi = a.q_idx[i];
+    bu = a.budget[i];
+    sv = a.base_svc[i];
+    if (a.role) ro = a.role[i];
+  };
+  if constexpr (!CHAIN) {
+#pragma unroll
+    for (int c = 0; c < kKeep; ++c) {
+      const int32_t r = c * 64 + lane;
+      if (r < n) load_arrival(r, lo + r, c_ac[c], c_qi[c], c_bu[c], c_sv[c], c_ro[c]);
+    }
+  }
+  if (!ml) {
+    r0 = make_int4(0, 0, 0, 0);
+    r1 = r0;
+    r2 = r0;
+    r3 = r0;
+  }
   // The tick and the next request id live in the env's first record in
   // device memory, so a captured sequence of ticks replays with the right time.
   const int32_t next_id = rl(r2.y, 0);
   const int32_t t = rl(r2.z, 0);
-  // Each front's largest entry (needed when newcomers arrive while the pool is
-  // not empty or the front is full) and the blackbox window byte leaving at
-  // this tick: in flight while the rows are loaded and sorted.
-  int32_t fmk = 0, fmi = 0, rold_l = 0;
-  if (ml && r1.w > 0 && (r2.x > 0 || r1.w == kFront)) {
-    const int2 f = *reinterpret_cast<const int2*>(a.front + (em0 + lane) * kFront + r1.z + r1.w - 1);
-    fmk = f.x;
-    fmi = f.y;
-  }
-  const int32_t rpm_l = RPM && ml ? r3.y : 0;   // lane m: model m's limit (0: not a blackbox model)
-  const bool track_l = RPM && ml && (rpm_l > 0 || r3.z > 0);
-  if (track_l) rold_l = a.rpm_ring[(em0 + lane) * kRpmRing + (t % kRpmWindow)];
   // chain pools: this tick's pending calls (buffer of parity t) and the next
-  // tick's (parity t + 1); the rows' outputs start at roff[e]
+  // tick's (parity t + 1)
   const int4* pend_cur = nullptr;
   int4* pend_nxt = nullptr;
-  int32_t pc = 0, abase = lo;
+  int32_t pc = 0;
   if constexpr (CHAIN) {
     const size_t E = (size_t)a.E;
     pend_cur = a.pend + ((size_t)(t & 1) * E + e) * a.pend_cap;
     pend_nxt = a.pend + ((size_t)((t + 1) & 1) * E + e) * a.pend_cap;
     pc = a.pcnt[(size_t)(t & 1) * E + e];
-    abase = a.roff[e];
   }
-  const int32_t n = bad ? 0 : hi - lo;   // arrivals
   const int32_t nrows = pc + n;          // rows: pending calls, then arrivals
 
-  // ---- the env's rows: loaded once, validated; the first chunks kept ----
-  constexpr int kKeep = 2;                            // chunks kept in registers
-  int32_t c_ac[kKeep], c_bs[kKeep];                   // action; budget << 16 | base_svc (16 bits each)
+  int32_t c_bs[kKeep];                                // budget << 16 | base_svc (16 bits each)
   int32_t c_xa[kKeep], c_xb[kKeep];                   // chain words (chain pools)
 #pragma unroll
   for (int c = 0; c < kKeep; ++c) {
-    c_ac[c] = -1;
     c_bs[c] = 0;
     c_xa[c] = 0;
     c_xb[c] = 0;
   }
   int32_t berr = 0;
-  // row r of the env: a pending call (r < pc, valid by construction; its
-  // budget is what is left of its query's) or arrival lo + r - pc
-  auto load_row = [&](int32_t r, int32_t& ac, int32_t& bs, int32_t& xa, int32_t& xb) {
-    ac = a.actions[abase + r];
+  // validation of an arrival, its packed service/budget word and (chain
+  // pools) its chain words
+  auto check_arrival = [&](int32_t i, int32_t ac, int32_t qi, int32_t bu, int32_t sv, int32_t ro, int32_t& bs,
+                           int32_t& xa, int32_t& xb) {
     if (ac < -1 || ac >= a.A) berr |= IM_ERR_ACTION;
-    if (CHAIN && r < pc) {
-      const int4 pr = pend_cur[r];
-      const int32_t bu = remaining_budget(pr.z, t);
-      xa = pr.x;
-      xb = pr.y;
-      bs = (int32_t)(((uint32_t)bu << 16) | ((uint32_t)chain_base(pr.y) & 0xffffu));
-      return;
-    }
-    const int32_t i = lo + (r - pc);
-    const int32_t qi = a.q_idx[i];
-    const int32_t bu = a.budget[i];
-    const int32_t sv = a.base_svc[i];
-    int32_t ro = 0;
     if (qi < 0 || (int64_t)qi >= a.Q) berr |= IM_ERR_QIDX;
-    if (a.role) {
-      ro = a.role[i];
-      if (ro < 0 || ro >= a.n_roles) berr |= IM_ERR_ROLE;
-    }
+    if (a.role && (ro < 0 || ro >= a.n_roles)) berr |= IM_ERR_ROLE;
     if (bu < 1) berr |= IM_ERR_BUDGET;
     if (sv < 1 || sv > IM_SVC_MAX) berr |= IM_ERR_SVC;
     if (CHAIN) {
@@ -511,11 +522,32 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     }
     bs = (int32_t)(((uint32_t)bu << 16) | ((uint32_t)sv & 0xffffu));
   };
+  // row r of a chain pool's env, loaded and validated
+  auto load_row = [&](int32_t r, int32_t& ac, int32_t& bs, int32_t& xa, int32_t& xb) {
+    if (CHAIN && r < pc) {
+      ac = a.actions[abase + r];
+      if (ac < -1 || ac >= a.A) berr |= IM_ERR_ACTION;
+      const int4 pr = pend_cur[r];
+      const int32_t bu = remaining_budget(pr.z, t);
+      xa = pr.x;
+      xb = pr.y;
+      bs = (int32_t)(((uint32_t)bu << 16) | ((uint32_t)chain_base(pr.y) & 0xffffu));
+      return;
+    }
+    const int32_t i = lo + (r - pc);
+    int32_t qi = 0, bu = 1, sv = 1, ro = 0;
+    load_arrival(r, i, ac, qi, bu, sv, ro);
+    check_arrival(i, ac, qi, bu, sv, ro, bs, xa, xb);
+  };
 #pragma unroll
   for (int c = 0; c < kKeep; ++c) {
-    if (c * 64 < nrows) {
-      const int32_t r = c * 64 + lane;
-      if (r < nrows) load_row(r, c_ac[c], c_bs[c], c_xa[c], c_xb[c]);
+    const int32_t r = c * 64 + lane;
+    if (r < nrows) {
+      if constexpr (CHAIN) {
+        load_row(r, c_ac[c], c_bs[c], c_xa[c], c_xb[c]);
+      } else {
+        check_arrival(lo + r, c_ac[c], c_qi[c], c_bu[c], c_sv[c], c_ro[c], c_bs[c], c_xa[c], c_xb[c]);
+      }
     }
   }
   for (int32_t base = kKeep * 64; base < nrows; base += 64) {
@@ -532,6 +564,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     if (a.role && ballot(berr & IM_ERR_ROLE)) bad |= IM_ERR_ROLE;
     if (CHAIN && ballot(berr & IM_ERR_STEPS)) bad |= IM_ERR_STEPS;
   }
+  // Each front's largest entry (needed when newcomers arrive while the pool is
+  // not empty or the front is full) and the blackbox window byte leaving at
+  // this tick: issued once the rows are validated (a
+  // wait for them would otherwise wait for these too), in flight while they
+  // are sorted.
+  int32_t fmk = 0, fmi = 0, rold_l = 0;
+  if (ml && r1.w > 0 && (r2.x > 0 || r1.w == kFront)) {
+    const int2 f = *reinterpret_cast<const int2*>(a.front + (em0 + lane) * kFront + r1.z + r1.w - 1);
+    fmk = f.x;
+    fmi = f.y;
+  }
+  const int32_t rpm_l = RPM && ml ? r3.y : 0;   // lane m: model m's limit (0: not a blackbox model)
+  const bool track_l = RPM && ml && (rpm_l > 0 || r3.z > 0);
+  if (track_l) rold_l = a.rpm_ring[(em0 + lane) * kRpmRing + (t % kRpmWindow)];
 
   LaneState L;
   L.qlen = r0.x; L.busy = r0.y; L.ewma = r0.z; L.backlog = r0.w;
