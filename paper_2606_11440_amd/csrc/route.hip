@@ -1044,7 +1044,19 @@ __global__ __launch_bounds__(NW * 64, 1) void route_bf16_lds(RouteArgs a_in) {
     asm volatile("" : "+v"(ln), "+v"(gg));
     if constexpr (!PIPE) setup(u, first_loads(u), c, x, gg);
 
-    u32x4 h[NR][KH];
+    u32x4 h[NR][NL == 3 ? KH : 1];
+    // two-layer policies: the output layer consumes each layer-1 output tile
+    // as soon as it is rounded (its two K steps), so the hidden layer is
+    // never held whole
+    f32x16 o[NR][AT];
+    if constexpr (NL == 2) {
+#pragma unroll
+      for (int T = 0; T < AT; ++T) {
+        o[0][T] = *(const f32x16*)(lb1 + (T * 2 + gg) * 16);
+#pragma unroll
+        for (int j = 1; j < NR; ++j) o[j][T] = o[0][T];
+      }
+    }
     // layer-1 fragments: W1PF of the next output tile's K steps are loaded
     // while the current tile's MFMAs run (the rest just before they are used)
     u32x4 wk[KB1], wn[KB1];
@@ -1067,28 +1079,33 @@ __global__ __launch_bounds__(NW * 64, 1) void route_bf16_lds(RouteArgs a_in) {
 #pragma unroll
         for (int j = 0; j < NR; ++j) p[j] = mfma_bf16(wk[kb], x[j][kb], p[j]);
       }
+      if constexpr (NL == 2) {
+        u32x4 f[NR][2];
 #pragma unroll
-      for (int j = 0; j < NR; ++j) relu_to_frags(p[j], h[j][2 * cc], h[j][2 * cc + 1]);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    f32x16 o[NR][AT];
-#pragma unroll
-    for (int T = 0; T < AT; ++T) {
-      o[0][T] = *(const f32x16*)((NL == 2 ? lb1 : lb2) + (T * 2 + gg) * 16);
-#pragma unroll
-      for (int j = 1; j < NR; ++j) o[j][T] = o[0][T];
-    }
-    if constexpr (NL == 2) {
-#pragma unroll
-      for (int kb = 0; kb < KH; ++kb) {
+        for (int j = 0; j < NR; ++j) relu_to_frags(p[j], f[j][0], f[j][1]);
 #pragma unroll
         for (int T = 0; T < AT; ++T) {
-          const u32x4 w = w2[(T * KH + kb) * 64 + ln];
+          const u32x4 wa = w2[(T * KH + 2 * cc) * 64 + ln];
+          const u32x4 wb = w2[(T * KH + 2 * cc + 1) * 64 + ln];
 #pragma unroll
-          for (int j = 0; j < NR; ++j) o[j][T] = mfma_bf16(w, h[j][kb], o[j][T]);
+          for (int j = 0; j < NR; ++j) {
+            o[j][T] = mfma_bf16(wa, f[j][0], o[j][T]);
+            o[j][T] = mfma_bf16(wb, f[j][1], o[j][T]);
+          }
         }
+      } else {
+#pragma unroll
+        for (int j = 0; j < NR; ++j) relu_to_frags(p[j], h[j][2 * cc], h[j][2 * cc + 1]);
       }
-    } else {
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if constexpr (NL == 3) {
+#pragma unroll
+      for (int T = 0; T < AT; ++T) {
+        o[0][T] = *(const f32x16*)(lb2 + (T * 2 + gg) * 16);
+#pragma unroll
+        for (int j = 1; j < NR; ++j) o[j][T] = o[0][T];
+      }
 #pragma unroll
       for (int cc = 0; cc < TH; ++cc) {
         f32x16 p[NR];
@@ -1646,8 +1663,8 @@ RouteKernel pick(int dtype, int hidden, int at) {
 // needs.
 struct LdsLaunch {
   RouteKernel k;
-  int waves;
-  int rows;
+  int waves;   // per block
+  int rows;    // 32-row MFMA tiles per wave
 };
 
 // 86 -> 256 -> 256 -> A, layer-1 weights through the caches: the greedy
@@ -1655,9 +1672,10 @@ struct LdsLaunch {
 // from LDS or the caches feeds two MFMAs, with the next output tile's layer-1
 // fragments loaded while the current one is multiplied (up to 256 VGPRs per
 // wave); the RL outputs, whose epilogue needs more registers, run 16 waves of
-// 32 rows. 104 -> 256 -> A, every layer in LDS: 16 waves of 32 rows (128
-// VGPRs), software-pipelined. Returns a null kernel when no LDS-resident
-// variant applies.
+// 32 rows. 104 -> 256 -> A, every layer in LDS: 16 waves of 32 rows,
+// software-pipelined, the output layer consuming each hidden tile as soon as
+// it is produced (96 VGPRs greedy, 102 with the RL outputs). Returns a null kernel when no LDS-resident variant
+// applies.
 LdsLaunch pick_lds(int dtype, int hidden, int n_layers, int out_tiles, int k1, int ed, bool rl) {
   if (dtype != IM_BF16) return {nullptr, 0, 0};
   if (hidden == 256 && n_layers == 3 && out_tiles == 1 && k1 == 6 && ed == 64)
