@@ -1672,9 +1672,11 @@ struct LdsLaunch {
 // from LDS or the caches feeds two MFMAs, with the next output tile's layer-1
 // fragments loaded while the current one is multiplied (up to 256 VGPRs per
 // wave); the RL outputs, whose epilogue needs more registers, run 16 waves of
-// 32 rows. 104 -> 256 -> A, every layer in LDS: 16 waves of 32 rows,
-// software-pipelined, the output layer consuming each hidden tile as soon as
-// it is produced (96 VGPRs greedy, 102 with the RL outputs). Returns a null kernel when no LDS-resident variant
+// 32 rows. 104 -> 256 -> A, every layer in LDS, software-pipelined, the
+// output layer consuming each hidden tile as soon as it is produced: the
+// greedy route runs 12 waves (three per SIMD, 168 VGPRs) of 64 rows, so each
+// weight fragment read from LDS feeds two MFMAs; the RL outputs run 16 waves
+// of 32 rows (102 VGPRs). Returns a null kernel when no LDS-resident variant
 // applies.
 LdsLaunch pick_lds(int dtype, int hidden, int n_layers, int out_tiles, int k1, int ed, bool rl) {
   if (dtype != IM_BF16) return {nullptr, 0, 0};
@@ -1683,7 +1685,7 @@ LdsLaunch pick_lds(int dtype, int hidden, int n_layers, int out_tiles, int k1, i
                : route_bf16_lds<256, 3, 1, 6, false, 8, 64, 2, 0, 6, false>, rl ? 16 : 8, rl ? 1 : 2};
   if (hidden == 256 && n_layers == 2 && out_tiles == 1 && k1 == 7 && ed == 64)
     return {rl ? route_bf16_lds<256, 2, 1, 7, true, 16, 64, 1, 1, 0, true>
-               : route_bf16_lds<256, 2, 1, 7, true, 16, 64, 1, 0, 0, true>, 16, 1};
+               : route_bf16_lds<256, 2, 1, 7, true, 12, 64, 2, 0, 0, true>, rl ? 16 : 12, rl ? 1 : 2};
   return {nullptr, 0, 0};
 }
 
