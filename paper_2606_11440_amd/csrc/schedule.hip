@@ -575,6 +575,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5, 8))) voi
     fmk = f.x;
     fmi = f.y;
   }
+  // lane m: the reciprocals its snapshot statistics are multiplied by,
+  // 1/max(c_m,1) and 1/(max(c_m,1) budget_max) (c_m is not changed by a tick)
+  float inv_busy_l = 0.f, inv_back_l = 0.f;
+  if (ml) {
+    const int c = r1.x < 0 ? 0 : (r1.x > IM_MAX_SLOTS ? IM_MAX_SLOTS : r1.x);
+    inv_busy_l = a.inv_tab[c];
+    inv_back_l = a.inv_tab[IM_MAX_SLOTS + 1 + c];
+  }
   const int32_t rpm_l = RPM && ml ? r3.y : 0;   // lane m: model m's limit (0: not a blackbox model)
   const bool track_l = RPM && ml && (rpm_l > 0 || r3.z > 0);
   if (track_l) rold_l = a.rpm_ring[(em0 + lane) * kRpmRing + (t % kRpmWindow)];
@@ -1031,26 +1039,21 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5, 8))) voi
   if (ballot(ml && (L.chg & CH_STATS)) != 0) {
     float* row = a.snap + (size_t)e * snap_stride(M);
     const float inv_rpm_l = __int_as_float(inv_rpm_bits);
+    // i / M for i < 4 M <= 128 as a multiply-high by ceil(2^32 / M)
+    const uint32_t mmag = M == 1 ? 0u : 0xffffffffu / (uint32_t)M + 1u;
     for (int i0 = 0; i0 < 4 * M; i0 += 64) {
       const int i = i0 + lane;
-      const int sidx = i / M, mm = i - sidx * M;
+      const int sidx = M == 1 ? i : (int)__umulhi((uint32_t)i, mmag), mm = i - sidx * M;
       const int srcm = mm < M ? mm : 0;
       const int32_t vq = shfl(L.qlen, srcm), vb = shfl(L.busy, srcm), vw = shfl(L.ewma, srcm),
-                    vk = shfl(L.backlog, srcm), cm = shfl(cap_l, srcm);
-      const int c = cm < 0 ? 0 : (cm > IM_MAX_SLOTS ? IM_MAX_SLOTS : cm);
-      if (i < 4 * M) {
-        float v;
-        switch (sidx) {
-          case 0:
-            v = RPM ? queue_stat(a, vq, shfl(rpm_l, srcm), shfl(L.rcnt, srcm), __int_as_float(shfl(__float_as_int(inv_rpm_l), srcm)))
-                    : (float)vq * a.inv_qcap;
-            break;
-          case 1: v = (float)vb * a.inv_tab[c]; break;
-          case 2: v = (float)vw * a.inv_lat; break;
-          default: v = (float)vk * a.inv_tab[IM_MAX_SLOTS + 1 + c]; break;
-        }
-        row[i] = v;
-      }
+                    vk = shfl(L.backlog, srcm);
+      const float ib = __int_as_float(shfl(__float_as_int(inv_busy_l), srcm));
+      const float ik = __int_as_float(shfl(__float_as_int(inv_back_l), srcm));
+      const float v0 = RPM ? queue_stat(a, vq, shfl(rpm_l, srcm), shfl(L.rcnt, srcm),
+                                        __int_as_float(shfl(__float_as_int(inv_rpm_l), srcm)))
+                           : (float)vq * a.inv_qcap;
+      const float v = sidx == 0 ? v0 : (sidx == 1 ? (float)vb * ib : (sidx == 2 ? (float)vw * a.inv_lat : (float)vk * ik));
+      if (i < 4 * M) row[i] = v;
     }
     if (ml) {
       uint8_t* vb8 = (uint8_t*)(row + snap_valid_offset(M));
