@@ -695,9 +695,21 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5, 8))) voi
       uint32_t sk = ((uint32_t)(acc ? mdl : 63) << 24) | (((uint32_t)(rk + 131072) & 0x3ffffu) << 6) |
                     (uint32_t)lane;
       const int32_t pay = (int32_t)(((uint32_t)svc & 0xffffu) | ((uint32_t)bu << 16));
-      // rows of the chunk sit in its first lanes: sort only the smallest power
-      // of two of lanes holding them (the other lanes hold rows of model 63)
-      bitonic_sort_first(sk, nrows - base < 64 ? nrows - base : 64);
+      // Rows of the chunk sit in its first lanes: sort only the smallest power
+      // of two of lanes holding them (the other lanes hold rows of model 63).
+      // When at most a quarter of them are admitted (full queues drop the
+      // rest), the admitted rows' keys are first moved to the lowest lanes, in
+      // lane order, and only those are sorted; every key keeps its row's lane.
+      const int nr = nrows - base < 64 ? nrows - base : 64;
+      const uint64_t am = ballot(acc);
+      const int na = popc64(am);
+      if (4 * na <= nr) {
+        const int pos = acc ? prefix_count(am) : na + prefix_count(~am);
+        sk = (uint32_t)__builtin_amdgcn_ds_permute(pos * 4, (int32_t)sk);
+        if (na > 1) bitonic_sort_first(sk, na);
+      } else {
+        bitonic_sort_first(sk, nr);
+      }
       const int src = (int)(sk & 63u);
       const int32_t skey = t + (int32_t)((sk >> 6) & 0x3ffffu) - 131072;
       const int32_t sid = next_id + base + src;
