@@ -349,6 +349,7 @@ __device__ __forceinline__ int32_t rl(int32_t v, int m) { return __builtin_amdgc
 enum {
   MW_ACC = 0,    // newcomers admitted this round
   MW_SVC,        // their service time
+  MW_CNT,        // rows of the current chunk routed to the model
   MW_KF,         // newcomers of the current chunk merged into the front
   MW_KP,         // newcomers of the current chunk appended to the pool
   MW_SEG,        // first lane of the model's segment in the current chunk
@@ -425,6 +426,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5, 8))) voi
   const int M = a.M, K = a.K, S = a.S;
   // a / K for actions a < 64 as a multiply-high by ceil(2^32 / K) (exact for a < 2^32 / K)
   const uint32_t kmag = K == 1 ? 0u : 0xffffffffu / (uint32_t)K + 1u;
+  // bits of a model index (M <= 32)
+  const int mbits = M <= 1 ? 0 : 32 - __builtin_clz((uint32_t)(M - 1));
   const size_t em0 = (size_t)e * M;
   ModelRec* recs = a.ms + em0;
   const bool ml = lane < M;   // this lane holds model `lane`
@@ -669,15 +672,24 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5, 8))) voi
       const int32_t mdl = ac < 0 ? -1 : (K == 1 ? ac : (int32_t)__umulhi((uint32_t)ac, kmag));
       nomodel += popc64(ballot(in && ac < 0));
       if (in && ac >= 0) atomicAdd(&hist_s[ac], 1);   // routed requests per action
-      int32_t rank = 0;
-      for (int m = 0; m < M; ++m) {
-        const uint64_t bal = ballot(in && mdl == m);
-        if (bal == 0) continue;
-        const int32_t pm = rl(prior_l, m);
-        if (mdl == m) rank = pm + prefix_count(bal);
-        if (lane == m) prior_l += popc64(bal);
+      // The lanes routed to this row's model: one ballot per bit of the
+      // model index. A row's rank among its model's rows in id order is the
+      // model's count before this chunk plus its lanes below; the first lane
+      // of each model passes the chunk's count to the model's lane.
+      const bool routed = in && mdl >= 0;
+      uint64_t same = ballot(routed);
+      for (int b = 0; b < mbits; ++b) {
+        const bool bit = ((mdl >> b) & 1) != 0;
+        const uint64_t bb = ballot(routed && bit);
+        same &= bit ? bb : ~bb;
       }
-      const int32_t room = shfl(room_l, mdl >= 0 ? mdl : 0);
+      const int msrc = mdl >= 0 ? mdl : 0;
+      const int below = prefix_count(same);
+      const int32_t rank = shfl(prior_l, msrc) + below;
+      if (ml) mw[MW_CNT][lane] = 0;
+      if (routed && below == 0) mw[MW_CNT][mdl] = popc64(same);
+      if (ml) prior_l += mw[MW_CNT][lane];
+      const int32_t room = shfl(room_l, msrc);
       const bool acc = in && mdl >= 0 && rank < room;
       const int32_t d = ac - mdl * K;
       const int32_t svc = sv * (d + 1);
