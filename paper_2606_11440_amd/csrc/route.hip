@@ -1671,18 +1671,21 @@ struct LdsLaunch {
 // route runs 8 waves (two per SIMD) of 64 rows, so every weight fragment read
 // from LDS or the caches feeds two MFMAs, with the next output tile's layer-1
 // fragments loaded while the current one is multiplied (up to 256 VGPRs per
-// wave); the RL outputs, whose epilogue needs more registers, run 16 waves of
-// 32 rows. 104 -> 256 -> A, every layer in LDS, software-pipelined, the
+// wave); the RL outputs, whose epilogue needs more registers, and light
+// ticks, whose few tiles would leave most waves idle, run 16 waves of 32
+// rows. 104 -> 256 -> A, every layer in LDS, software-pipelined, the
 // output layer consuming each hidden tile as soon as it is produced: the
 // greedy route runs 12 waves (three per SIMD, 168 VGPRs) of 64 rows, so each
 // weight fragment read from LDS feeds two MFMAs; the RL outputs run 16 waves
 // of 32 rows (102 VGPRs). Returns a null kernel when no LDS-resident variant
 // applies.
-LdsLaunch pick_lds(int dtype, int hidden, int n_layers, int out_tiles, int k1, int ed, bool rl) {
+LdsLaunch pick_lds(int dtype, int hidden, int n_layers, int out_tiles, int k1, int ed, bool rl, bool light) {
   if (dtype != IM_BF16) return {nullptr, 0, 0};
-  if (hidden == 256 && n_layers == 3 && out_tiles == 1 && k1 == 6 && ed == 64)
-    return {rl ? route_bf16_lds<256, 3, 1, 6, false, 16, 64, 1, 1, 0, false>
-               : route_bf16_lds<256, 3, 1, 6, false, 8, 64, 2, 0, 6, false>, rl ? 16 : 8, rl ? 1 : 2};
+  if (hidden == 256 && n_layers == 3 && out_tiles == 1 && k1 == 6 && ed == 64) {
+    if (rl) return {route_bf16_lds<256, 3, 1, 6, false, 16, 64, 1, 1, 0, false>, 16, 1};
+    if (light) return {route_bf16_lds<256, 3, 1, 6, false, 16, 64, 1, 0, 0, false>, 16, 1};
+    return {route_bf16_lds<256, 3, 1, 6, false, 8, 64, 2, 0, 6, false>, 8, 2};
+  }
   if (hidden == 256 && n_layers == 2 && out_tiles == 1 && k1 == 7 && ed == 64)
     return {rl ? route_bf16_lds<256, 2, 1, 7, true, 16, 64, 1, 1, 0, true>
                : route_bf16_lds<256, 2, 1, 7, true, 12, 64, 2, 0, 0, true>, rl ? 16 : 12, rl ? 1 : 2};
@@ -1758,7 +1761,10 @@ hipError_t launch_route(const RouteArgs& a, int dtype, int hidden, int n_layers,
   if (a.n_total <= 0) return hipSuccess;
   if (a.net == IM_NET_DUAL) return launch_dual(a, s);
   if (a.persistent_blocks > 0) {
-    const LdsLaunch kl = pick_lds(dtype, hidden, n_layers, out_tiles, a.k1, a.embed_dim, a.rl != 0);
+    // a light tick (at most three 64-row tiles per four waves of 8-wave
+    // blocks) runs the 16-wave, 32-row shape: twice the waves share its rows
+    const bool light = (int64_t)a.n_total * 4 <= (int64_t)3 * 64 * 8 * a.persistent_blocks;
+    const LdsLaunch kl = pick_lds(dtype, hidden, n_layers, out_tiles, a.k1, a.embed_dim, a.rl != 0, light);
     if (kl.k) {
       // one block per CU as long as there are wave tiles for them: a light
       // tick spreads its few tiles over every CU instead of filling a few
