@@ -1673,17 +1673,18 @@ struct LdsLaunch {
 // fragments loaded while the current one is multiplied (up to 256 VGPRs per
 // wave); the RL outputs, whose epilogue needs more registers, and light
 // ticks, whose few tiles would leave most waves idle, run 16 waves of 32
-// rows. 104 -> 256 -> A, every layer in LDS, software-pipelined, the
+// rows; very light ticks 8 waves of 32 rows, software-pipelined. 104 -> 256 -> A, every layer in LDS, software-pipelined, the
 // output layer consuming each hidden tile as soon as it is produced: the
 // greedy route runs 12 waves (three per SIMD, 168 VGPRs) of 64 rows, so each
 // weight fragment read from LDS feeds two MFMAs; the RL outputs run 16 waves
 // of 32 rows (102 VGPRs). Returns a null kernel when no LDS-resident variant
 // applies.
-LdsLaunch pick_lds(int dtype, int hidden, int n_layers, int out_tiles, int k1, int ed, bool rl, bool light) {
+LdsLaunch pick_lds(int dtype, int hidden, int n_layers, int out_tiles, int k1, int ed, bool rl, int light) {
   if (dtype != IM_BF16) return {nullptr, 0, 0};
   if (hidden == 256 && n_layers == 3 && out_tiles == 1 && k1 == 6 && ed == 64) {
     if (rl) return {route_bf16_lds<256, 3, 1, 6, false, 16, 64, 1, 1, 0, false>, 16, 1};
-    if (light) return {route_bf16_lds<256, 3, 1, 6, false, 16, 64, 1, 0, 0, false>, 16, 1};
+    if (light == 2) return {route_bf16_lds<256, 3, 1, 6, false, 8, 64, 1, 0, 6, true>, 8, 1};
+    if (light == 1) return {route_bf16_lds<256, 3, 1, 6, false, 16, 64, 1, 0, 0, false>, 16, 1};
     return {route_bf16_lds<256, 3, 1, 6, false, 8, 64, 2, 0, 6, false>, 8, 2};
   }
   if (hidden == 256 && n_layers == 2 && out_tiles == 1 && k1 == 7 && ed == 64)
@@ -1762,8 +1763,11 @@ hipError_t launch_route(const RouteArgs& a, int dtype, int hidden, int n_layers,
   if (a.net == IM_NET_DUAL) return launch_dual(a, s);
   if (a.persistent_blocks > 0) {
     // a light tick (at most three 64-row tiles per four waves of 8-wave
-    // blocks) runs the 16-wave, 32-row shape: twice the waves share its rows
-    const bool light = (int64_t)a.n_total * 4 <= (int64_t)3 * 64 * 8 * a.persistent_blocks;
+    // blocks) runs the 16-wave, 32-row shape: twice the waves share its rows;
+    // a very light one (at most one 32-row tile per two waves) runs 8 waves
+    // of 32 rows whose first tile's loads overlap the block's weight copy
+    const int64_t rows = a.n_total, cap = (int64_t)64 * 8 * a.persistent_blocks;
+    const int light = rows * 4 <= cap ? 2 : (rows * 4 <= 3 * cap ? 1 : 0);
     const LdsLaunch kl = pick_lds(dtype, hidden, n_layers, out_tiles, a.k1, a.embed_dim, a.rl != 0, light);
     if (kl.k) {
       // one block per CU as long as there are wave tiles for them: a light
