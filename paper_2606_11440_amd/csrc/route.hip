@@ -1673,12 +1673,12 @@ struct LdsLaunch {
 // fragments loaded while the current one is multiplied (up to 256 VGPRs per
 // wave); the RL outputs, whose epilogue needs more registers, and light
 // ticks, whose few tiles would leave most waves idle, run 16 waves of 32
-// rows; very light ticks 8 waves of 32 rows, software-pipelined. 104 -> 256 -> A, every layer in LDS, software-pipelined, the
-// output layer consuming each hidden tile as soon as it is produced: the
-// greedy route runs 12 waves (three per SIMD, 168 VGPRs) of 64 rows, so each
-// weight fragment read from LDS feeds two MFMAs; the RL outputs run 16 waves
-// of 32 rows (102 VGPRs). Returns a null kernel when no LDS-resident variant
-// applies.
+// rows; very light ticks 8 waves of 32 rows, software-pipelined.
+// 104 -> 256 -> A, every layer in LDS, software-pipelined, the output layer
+// consuming each hidden tile as soon as it is produced: the greedy route runs
+// 12 waves (three per SIMD, 168 VGPRs) of 64 rows, so each weight fragment
+// read from LDS feeds two MFMAs; the RL outputs run 16 waves of 32 rows (102
+// VGPRs). Returns a null kernel when no LDS-resident variant applies.
 LdsLaunch pick_lds(int dtype, int hidden, int n_layers, int out_tiles, int k1, int ed, bool rl, int light) {
   if (dtype != IM_BF16) return {nullptr, 0, 0};
   if (hidden == 256 && n_layers == 3 && out_tiles == 1 && k1 == 6 && ed == 64) {
