@@ -49,14 +49,42 @@ struct RowCtx {
 
 // Valid actions of env e: bit a set when model a / K is valid in the env's
 // snapshot row (enabled, c_m > 0, queue below capacity).
-__device__ __forceinline__ uint64_t action_mask(const RouteArgs& a, int e) {
-  const uint8_t* v = (const uint8_t*)(a.snap + (size_t)e * snap_stride(a.M) + snap_valid_offset(a.M));
+// The M <= 32 validity bytes start 16-byte aligned (byte 16 M of a row whose
+// stride is a multiple of 32 bytes) and the row's padding covers two 16-byte
+// words from there, so they arrive in one or two independent loads (a byte
+// loop would wait for each byte in turn).
+__device__ __forceinline__ uint32_t nonzero_bytes(uint32_t x) {
+  // bit i of the result: byte i of x is nonzero (OR-fold each byte into its
+  // low bit, then gather bits 0, 8, 16, 24 with one multiply: the shifted
+  // copies land on distinct bits, so no carries)
+  x |= x >> 4;
+  x |= x >> 2;
+  x |= x >> 1;
+  return ((x & 0x01010101u) * 0x00204081u) >> 21 & 0xfu;
+}
+__device__ __forceinline__ uint32_t valid_models16(const u32x4 w) {
+  return nonzero_bytes(w.x) | nonzero_bytes(w.y) << 4 | nonzero_bytes(w.z) << 8 | nonzero_bytes(w.w) << 12;
+}
+// The raw validity words of env e (both loaded for every M: the row's padding
+// covers them) and the action mask computed from them once they have arrived.
+struct ValidRaw {
+  u32x4 w0, w1;
+};
+__device__ __forceinline__ ValidRaw load_valid(const RouteArgs& a, int e) {
+  const u32x4* v = (const u32x4*)(a.snap + (size_t)e * snap_stride(a.M) + snap_valid_offset(a.M));
+  return {v[0], v[1]};
+}
+__device__ __forceinline__ uint64_t mask_of(const RouteArgs& a, const ValidRaw& v) {
+  uint32_t vm = valid_models16(v.w0);
+  if (a.M > 16) vm |= valid_models16(v.w1) << 16;
+  if (a.M < 32) vm &= (1u << a.M) - 1u;   // bytes past the M-th are padding
   const uint64_t kmask = (a.K >= 64) ? ~0ull : ((1ull << a.K) - 1ull);
   uint64_t am = 0;
   for (int m = 0; m < a.M; ++m)
-    if (v[m]) am |= kmask << (m * a.K);
+    if ((vm >> m) & 1u) am |= kmask << (m * a.K);
   return am;
 }
+__device__ __forceinline__ uint64_t action_mask(const RouteArgs& a, int e) { return mask_of(a, load_valid(a, e)); }
 
 // Env of rows r[] (per lane) for a wave whose rows lie in [rfirst, rlast]:
 // one coalesced load of a 64-entry window of offsets around an interpolated
@@ -157,7 +185,7 @@ __device__ __forceinline__ RowCtx row_ctx_from(const RouteArgs& a, int32_t r, in
   c.bad = (q < 0 || (int64_t)q >= a.Q) ? IM_ERR_QIDX : 0;
   c.q = c.bad ? 0 : q;
   c.budget = budget;
-  c.amask = action_mask(a, e);
+  c.amask = 0;   // set by the caller from load_valid / mask_of
   return c;
 }
 
@@ -172,6 +200,23 @@ __device__ __forceinline__ RowCtx row_setup_env(const RouteArgs& a, int32_t r, i
   c.q = c.bad ? 0 : q;
   c.budget = a.budget[rr];
   c.amask = action_mask(a, e);
+  return c;
+}
+
+// The same, leaving the action mask to the caller (load_valid's words are in
+// flight with the row's q_idx and budget).
+__device__ __forceinline__ RowCtx row_setup_env_raw(const RouteArgs& a, int32_t r, int32_t e, ValidRaw& vr) {
+  RowCtx c;
+  c.r = r;
+  c.live = r < a.n_total;
+  const int32_t rr = c.live ? r : a.n_total - 1;
+  c.e = e;
+  const int32_t q = a.q_idx[rr];
+  c.bad = (q < 0 || (int64_t)q >= a.Q) ? IM_ERR_QIDX : 0;
+  c.q = c.bad ? 0 : q;
+  c.budget = a.budget[rr];
+  vr = load_valid(a, e);
+  c.amask = 0;   // mask_of(a, vr) once the words have arrived
   return c;
 }
 
@@ -298,6 +343,61 @@ __device__ __forceinline__ void gather_row(const RouteArgs& a, const RowCtx& c, 
   if constexpr (KB < N) {
     x[KB] = gather_ct<ED, KB>(a, c, g);
     gather_row<ED, KB + 1, N>(a, c, g, x);
+  }
+}
+
+// Layer-1 B fragments of a row in two steps, so that a wave tile's gather is
+// one round trip: gather_issue loads every embedding word and the raw
+// snapshot words of the tail blocks (the load statistics; a lane whose block
+// starts past them reads from the row's last statistic on, which stays inside
+// the row, and ignores the words), gather_finish converts the tail blocks once
+// they have arrived (the arithmetic of gather_ct).
+template <int ED, int KB1>
+struct TailRaw {
+  static constexpr int KE = ED / 16 < KB1 ? ED / 16 : KB1;   // K blocks inside the embedding
+  static constexpr int KT = KB1 - KE;                          // tail blocks
+  float4 t[KT > 0 ? KT : 1][2];
+};
+template <int ED, int KB1>
+__device__ __forceinline__ void gather_issue(const RouteArgs& a, const RowCtx& c, int g, u32x4 (&x)[KB1],
+                                             TailRaw<ED, KB1>& raw) {
+  static_assert(ED % 16 == 0, "embedding width must be a multiple of 16");
+  using TR = TailRaw<ED, KB1>;
+  const uint16_t* emb = (const uint16_t*)a.emb;
+#pragma unroll
+  for (int kb = 0; kb < TR::KE; ++kb) x[kb] = *(const u32x4*)(emb + (size_t)c.q * ED + 16 * kb + 8 * g);
+  const int n4 = 4 * a.M;
+#pragma unroll
+  for (int t = 0; t < TR::KT; ++t) {
+    const int k2 = 16 * t + 8 * g;
+    const float* row = a.snap + (size_t)c.e * snap_stride(a.M) + (k2 < n4 ? k2 : n4 - 1);
+    raw.t[t][0] = *(const float4*)row;
+    raw.t[t][1] = *(const float4*)(row + 4);
+  }
+}
+template <int ED, int KB1>
+__device__ __forceinline__ void gather_finish(const RouteArgs& a, const RowCtx& c, int g, u32x4 (&x)[KB1],
+                                              const TailRaw<ED, KB1>& raw) {
+  using TR = TailRaw<ED, KB1>;
+  const int n4 = 4 * a.M;
+  const float fb = (float)c.budget * a.inv_bud;
+#pragma unroll
+  for (int t = 0; t < TR::KT; ++t) {
+    const int k2 = 16 * t + 8 * g;
+    const float4 lo = raw.t[t][0], hi = raw.t[t][1];
+    const float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+    float f[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int kk = k2 + i;
+      f[i] = kk < n4 ? v[i] : (kk == n4 ? fb : 0.f);
+    }
+    u32x4 r;
+    r.x = pack2(f[0], f[1]);
+    r.y = pack2(f[2], f[3]);
+    r.z = pack2(f[4], f[5]);
+    r.w = pack2(f[6], f[7]);
+    x[TR::KE + t] = r;
   }
 }
 
@@ -1003,10 +1103,21 @@ __global__ __launch_bounds__(NW * 64, 1) void route_bf16_lds(RouteArgs a_in) {
 #pragma unroll
     for (int j = 0; j < NR; ++j) rows[j] = r0 + 32 * j + n;
     find_envs_in<NR>(a, f.w, r0, rlast, rows, envs);
+    ValidRaw vr[NR];
 #pragma unroll
-    for (int j = 0; j < NR; ++j) c[j] = row_ctx_from(a, rows[j], envs[j], f.q[j], f.bud[j]);
+    for (int j = 0; j < NR; ++j) {
+      c[j] = row_ctx_from(a, rows[j], envs[j], f.q[j], f.bud[j]);
+      vr[j] = load_valid(a, envs[j]);
+    }
+    TailRaw<ED, KB1> raw[NR];
 #pragma unroll
-    for (int j = 0; j < NR; ++j) gather_row<ED, 0, KB1>(a, c[j], gg, x[j]);
+    for (int j = 0; j < NR; ++j) gather_issue<ED, KB1>(a, c[j], gg, x[j], raw[j]);
+    // the masks wait only for their own words: the embedding and snapshot
+    // loads issued after them stay in flight
+#pragma unroll
+    for (int j = 0; j < NR; ++j) c[j].amask = mask_of(a, vr[j]);
+#pragma unroll
+    for (int j = 0; j < NR; ++j) gather_finish<ED, KB1>(a, c[j], gg, x[j], raw[j]);
   };
   // PIPE: the loop is software-pipelined, the next wave tile's first loads
   // being issued once the current tile's MFMAs have been, so that they are in
@@ -1271,8 +1382,12 @@ __global__ __launch_bounds__(NW * 64, 1) void route_bf16_stream(RouteArgs a_in) 
     u32x4 x[KB1];
     if (act) {
       find_envs<1>(a, r0, rl, rsel, envs);
-      c = row_setup_env(a, rows[0], envs[0]);
-      gather_row<ED, 0, KB1>(a, c, gg, x);
+      ValidRaw vr;
+      c = row_setup_env_raw(a, rows[0], envs[0], vr);
+      TailRaw<ED, KB1> raw;
+      gather_issue<ED, KB1>(a, c, gg, x, raw);
+      c.amask = mask_of(a, vr);
+      gather_finish<ED, KB1>(a, c, gg, x, raw);
     }
     if (!act) {
       // the same stages, barriers and copies as a working wave (a barrier
@@ -1480,9 +1595,10 @@ __global__ __launch_bounds__(NW * 64, 1) void route_dual_bf16(RouteArgs a_in) {
     find_envs<NR>(a, r0, rlast, rows, envs);
     RowCtx c[NR];
     int32_t role[NR];
+    ValidRaw vr[NR];
 #pragma unroll
     for (int j = 0; j < NR; ++j) {
-      c[j] = row_setup_env(a, rows[j], envs[j]);
+      c[j] = row_setup_env_raw(a, rows[j], envs[j], vr[j]);
       const int32_t ro = a.role[c[j].live ? rows[j] : a.n_total - 1];
       const bool bad_r = ro < 0 || ro >= a.n_roles;
       if (bad_r) c[j].bad |= IM_ERR_ROLE;
@@ -1498,6 +1614,8 @@ __global__ __launch_bounds__(NW * 64, 1) void route_dual_bf16(RouteArgs a_in) {
 #pragma unroll
       for (int j = 0; j < NR; ++j) load_group<ED>(a, c[j], G, gg, x[G][j]);
     }
+#pragma unroll
+    for (int j = 0; j < NR; ++j) c[j].amask = mask_of(a, vr[j]);
     // ---- resource pathway, computed while the first embedding groups load ----
     u32x4 hr[NR][4];
 #pragma unroll
