@@ -400,8 +400,8 @@ __device__ __forceinline__ void counter_add(int64_t* p, int64_t v) {
 // call carries its query's two chain words through the queue, and a
 // completion that is not its query's last call appends the next call, with
 // the query's deadline, to the pending list of the next tick.
-template <bool RPM, bool CHAIN>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5, 8))) void schedule_kernel(SchedArgs a) {
+template <bool RPM, bool CHAIN, int PF>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(PF > 1 ? 4 : 5, 8))) void schedule_kernel(SchedArgs a) {
   // sorted chunks; in the service phase the refill scan's key buffer, then
   // the counter staging
   __shared__ int4 stage[4][kStageChunks * 64];
@@ -787,11 +787,38 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5, 8))) voi
         L.P += kp_l;
         L.chg |= CH_POOL;
       }
-      // models with front-bound newcomers: merge them into the front
+      // models with front-bound newcomers: merge them into the front, PF
+      // models at a time, whose fronts are loaded together (one round trip
+      // per group instead of one per model)
       uint64_t merges = ballot(kf_l > 0);
       while (merges) {
-        const int m = __builtin_ctzll(merges);
-        merges &= merges - 1;
+        int gm[PF];
+        uint64_t gmask = 0;
+#pragma unroll
+        for (int d = 0; d < PF; ++d) {
+          gm[d] = merges ? __builtin_ctzll(merges) : -1;
+          if (gm[d] >= 0) gmask |= 1ull << gm[d];
+          merges &= merges - 1;
+        }
+        if (wrote & gmask) wave_mem_sync();   // a front written earlier this tick is read below
+        int4 pfe[PF];
+        int2 pfx[PF];
+#pragma unroll
+        for (int d = 0; d < PF; ++d) {
+          pfe[d] = make_int4(0, 0, 0, 0);
+          pfx[d] = make_int2(0, 0);
+          if (gm[d] >= 0) {
+            const int fh = rl(L.fh, gm[d]), fn = rl(L.fn, gm[d]);
+            if (lane < fn) {
+              pfe[d] = a.front[(em0 + gm[d]) * kFront + fh + lane];   // fh + fn <= kFront
+              if constexpr (CHAIN) pfx[d] = a.front_ext[(em0 + gm[d]) * kFront + fh + lane];
+            }
+          }
+        }
+#pragma unroll
+        for (int d = 0; d < PF; ++d) {
+        const int m = gm[d];
+        if (m < 0) break;
         const size_t em = em0 + m;
         Queue q;
         q.fh = rl(L.fh, m);
@@ -799,13 +826,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5, 8))) voi
         q.P = rl(L.P, m);
         const int lim = rl(kf_l, m);
         const int s0 = __builtin_amdgcn_readfirstlane(mw[MW_SEG][m]);
-        if ((wrote >> m) & 1ull) wave_mem_sync();   // this model's front was written this tick
-        int4 fe = make_int4(0, 0, 0, 0);
-        int2 fx = make_int2(0, 0);
-        if (lane < q.fn) {
-          fe = a.front[em * kFront + q.fh + lane];   // fh + fn <= kFront
-          if constexpr (CHAIN) fx = a.front_ext[em * kFront + q.fh + lane];
-        }
+        int4 fe = pfe[d];
+        int2 fx = pfx[d];
         const int32_t okey = fe.x, oid = fe.y;
         const int ofh = q.fh, ofn = q.fn;
         merge_front<CHAIN>(q, fe, fx, st + c * 64 + s0, stx + c * 64 + s0, lim, a.key_mode,
@@ -825,6 +847,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5, 8))) voi
           L.fmk = nk;
           L.fmi = ni;
           L.chg |= CH_FRONT | CH_POOL;
+        }
         }
       }
     }
@@ -1171,16 +1194,24 @@ hipError_t launch_snapshot(const SchedArgs& a, int e0, int ne, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_schedule(const SchedArgs& a, bool rpm, bool chain, int waves_per_block, hipStream_t s) {
+// When the whole grid is resident at 4 waves per SIMD (16 env waves per CU),
+// the single-call kernels load the fronts of up to 4 merging models together:
+// more registers, one wave fewer per SIMD, which such a grid does not need.
+hipError_t launch_schedule(const SchedArgs& a, bool rpm, bool chain, int waves_per_block, int cu_count,
+                           hipStream_t s) {
   const int w = waves_per_block == 1 || waves_per_block == 2 ? waves_per_block : 4;
   const unsigned blocks = (unsigned)(((int64_t)a.E + w - 1) / w);
   const dim3 threads(64 * w);
+  const bool pf = !chain && cu_count > 0 && (int64_t)a.E <= (int64_t)16 * cu_count;
   if (chain) {
-    if (rpm) hipLaunchKernelGGL((schedule_kernel<true, true>), dim3(blocks), threads, 0, s, a);
-    else hipLaunchKernelGGL((schedule_kernel<false, true>), dim3(blocks), threads, 0, s, a);
+    if (rpm) hipLaunchKernelGGL((schedule_kernel<true, true, 1>), dim3(blocks), threads, 0, s, a);
+    else hipLaunchKernelGGL((schedule_kernel<false, true, 1>), dim3(blocks), threads, 0, s, a);
+  } else if (pf) {
+    if (rpm) hipLaunchKernelGGL((schedule_kernel<true, false, 4>), dim3(blocks), threads, 0, s, a);
+    else hipLaunchKernelGGL((schedule_kernel<false, false, 4>), dim3(blocks), threads, 0, s, a);
   } else {
-    if (rpm) hipLaunchKernelGGL((schedule_kernel<true, false>), dim3(blocks), threads, 0, s, a);
-    else hipLaunchKernelGGL((schedule_kernel<false, false>), dim3(blocks), threads, 0, s, a);
+    if (rpm) hipLaunchKernelGGL((schedule_kernel<true, false, 1>), dim3(blocks), threads, 0, s, a);
+    else hipLaunchKernelGGL((schedule_kernel<false, false, 1>), dim3(blocks), threads, 0, s, a);
   }
   return hipGetLastError();
 }
