@@ -787,67 +787,108 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(PF > 1 ? 4 
         L.P += kp_l;
         L.chg |= CH_POOL;
       }
-      // models with front-bound newcomers: merge them into the front, PF
-      // models at a time, whose fronts are loaded together (one round trip
-      // per group instead of one per model)
+      // models with front-bound newcomers: merge them into the front
       uint64_t merges = ballot(kf_l > 0);
-      while (merges) {
-        int gm[PF];
-        uint64_t gmask = 0;
-#pragma unroll
-        for (int d = 0; d < PF; ++d) {
-          gm[d] = merges ? __builtin_ctzll(merges) : -1;
-          if (gm[d] >= 0) gmask |= 1ull << gm[d];
+      if constexpr (PF == 1) {
+        while (merges) {
+          const int m = __builtin_ctzll(merges);
           merges &= merges - 1;
-        }
-        if (wrote & gmask) wave_mem_sync();   // a front written earlier this tick is read below
-        int4 pfe[PF];
-        int2 pfx[PF];
-#pragma unroll
-        for (int d = 0; d < PF; ++d) {
-          pfe[d] = make_int4(0, 0, 0, 0);
-          pfx[d] = make_int2(0, 0);
-          if (gm[d] >= 0) {
-            const int fh = rl(L.fh, gm[d]), fn = rl(L.fn, gm[d]);
-            if (lane < fn) {
-              pfe[d] = a.front[(em0 + gm[d]) * kFront + fh + lane];   // fh + fn <= kFront
-              if constexpr (CHAIN) pfx[d] = a.front_ext[(em0 + gm[d]) * kFront + fh + lane];
-            }
+          const size_t em = em0 + m;
+          Queue q;
+          q.fh = rl(L.fh, m);
+          q.fn = rl(L.fn, m);
+          q.P = rl(L.P, m);
+          const int lim = rl(kf_l, m);
+          const int s0 = __builtin_amdgcn_readfirstlane(mw[MW_SEG][m]);
+          if ((wrote >> m) & 1ull) wave_mem_sync();   // this model's front was written this tick
+          int4 fe = make_int4(0, 0, 0, 0);
+          int2 fx = make_int2(0, 0);
+          if (lane < q.fn) {
+            fe = a.front[em * kFront + q.fh + lane];   // fh + fn <= kFront
+            if constexpr (CHAIN) fx = a.front_ext[em * kFront + q.fh + lane];
+          }
+          const int32_t okey = fe.x, oid = fe.y;
+          const int ofh = q.fh, ofn = q.fn;
+          merge_front<CHAIN>(q, fe, fx, st + c * 64 + s0, stx + c * 64 + s0, lim, a.key_mode,
+                             a.pool + em * a.qcap, CHAIN ? a.pool_ext + em * a.qcap : nullptr);
+          // the front now starts at 0; entries that kept their position are not rewritten
+          const bool same = ofh == 0 && lane < ofn && okey == fe.x && oid == fe.y;
+          if (lane < q.fn && !same) {
+            a.front[em * kFront + lane] = fe;
+            if constexpr (CHAIN) a.front_ext[em * kFront + lane] = fx;
+          }
+          wrote |= 1ull << m;
+          const int32_t nk = rl(fe.x, q.fn - 1), ni = rl(fe.y, q.fn - 1);   // q.fn >= 1 after a merge
+          if (lane == m) {
+            L.fh = 0;
+            L.fn = q.fn;
+            L.P = q.P;
+            L.fmk = nk;
+            L.fmi = ni;
+            L.chg |= CH_FRONT | CH_POOL;
           }
         }
-#pragma unroll
-        for (int d = 0; d < PF; ++d) {
-        const int m = gm[d];
-        if (m < 0) break;
-        const size_t em = em0 + m;
-        Queue q;
-        q.fh = rl(L.fh, m);
-        q.fn = rl(L.fn, m);
-        q.P = rl(L.P, m);
-        const int lim = rl(kf_l, m);
-        const int s0 = __builtin_amdgcn_readfirstlane(mw[MW_SEG][m]);
-        int4 fe = pfe[d];
-        int2 fx = pfx[d];
-        const int32_t okey = fe.x, oid = fe.y;
-        const int ofh = q.fh, ofn = q.fn;
-        merge_front<CHAIN>(q, fe, fx, st + c * 64 + s0, stx + c * 64 + s0, lim, a.key_mode,
-                           a.pool + em * a.qcap, CHAIN ? a.pool_ext + em * a.qcap : nullptr);
-        // the front now starts at 0; entries that kept their position are not rewritten
-        const bool same = ofh == 0 && lane < ofn && okey == fe.x && oid == fe.y;
-        if (lane < q.fn && !same) {
-          a.front[em * kFront + lane] = fe;
-          if constexpr (CHAIN) a.front_ext[em * kFront + lane] = fx;
-        }
-        wrote |= 1ull << m;
-        const int32_t nk = rl(fe.x, q.fn - 1), ni = rl(fe.y, q.fn - 1);   // q.fn >= 1 after a merge
-        if (lane == m) {
-          L.fh = 0;
-          L.fn = q.fn;
-          L.P = q.P;
-          L.fmk = nk;
-          L.fmi = ni;
-          L.chg |= CH_FRONT | CH_POOL;
-        }
+      } else {
+        // PF models at a time, whose fronts are loaded together (one round trip
+        // per group instead of one per model)
+        while (merges) {
+          int gm[PF];
+          uint64_t gmask = 0;
+  #pragma unroll
+          for (int d = 0; d < PF; ++d) {
+            gm[d] = merges ? __builtin_ctzll(merges) : -1;
+            if (gm[d] >= 0) gmask |= 1ull << gm[d];
+            merges &= merges - 1;
+          }
+          if (wrote & gmask) wave_mem_sync();   // a front written earlier this tick is read below
+          int4 pfe[PF];
+          int2 pfx[PF];
+  #pragma unroll
+          for (int d = 0; d < PF; ++d) {
+            pfe[d] = make_int4(0, 0, 0, 0);
+            pfx[d] = make_int2(0, 0);
+            if (gm[d] >= 0) {
+              const int fh = rl(L.fh, gm[d]), fn = rl(L.fn, gm[d]);
+              if (lane < fn) {
+                pfe[d] = a.front[(em0 + gm[d]) * kFront + fh + lane];
+                if constexpr (CHAIN) pfx[d] = a.front_ext[(em0 + gm[d]) * kFront + fh + lane];
+              }
+            }
+          }
+  #pragma unroll
+          for (int d = 0; d < PF; ++d) {
+            const int m = gm[d];
+            if (m < 0) break;
+            const size_t em = em0 + m;
+            Queue q;
+            q.fh = rl(L.fh, m);
+            q.fn = rl(L.fn, m);
+            q.P = rl(L.P, m);
+            const int lim = rl(kf_l, m);
+            const int s0 = __builtin_amdgcn_readfirstlane(mw[MW_SEG][m]);
+            int4 fe = pfe[d];
+            int2 fx = pfx[d];
+            const int32_t okey = fe.x, oid = fe.y;
+            const int ofh = q.fh, ofn = q.fn;
+            merge_front<CHAIN>(q, fe, fx, st + c * 64 + s0, stx + c * 64 + s0, lim, a.key_mode,
+                               a.pool + em * a.qcap, CHAIN ? a.pool_ext + em * a.qcap : nullptr);
+            // the front now starts at 0; entries that kept their position are not rewritten
+            const bool same = ofh == 0 && lane < ofn && okey == fe.x && oid == fe.y;
+            if (lane < q.fn && !same) {
+              a.front[em * kFront + lane] = fe;
+              if constexpr (CHAIN) a.front_ext[em * kFront + lane] = fx;
+            }
+            wrote |= 1ull << m;
+            const int32_t nk = rl(fe.x, q.fn - 1), ni = rl(fe.y, q.fn - 1);   // q.fn >= 1 after a merge
+            if (lane == m) {
+              L.fh = 0;
+              L.fn = q.fn;
+              L.P = q.P;
+              L.fmk = nk;
+              L.fmi = ni;
+              L.chg |= CH_FRONT | CH_POOL;
+            }
+          }
         }
       }
     }
