@@ -1119,11 +1119,11 @@ __global__ __launch_bounds__(NW * 64, 1) void route_bf16_lds(RouteArgs a_in) {
 #pragma unroll
     for (int j = 0; j < NR; ++j) gather_finish<ED, KB1>(a, c[j], gg, x[j], raw[j]);
   };
-  // PIPE: the loop is software-pipelined, the next wave tile's first loads
-  // being issued once the current tile's MFMAs have been, so that they are in
-  // flight during its epilogue, and the first tile's during the block's copy
-  // of the weights into LDS (this holds a few more registers across the
-  // epilogue, so it pays only where the registers are not all taken).
+  // PIPE: the first wave tile is set up (first loads, then its gather)
+  // while the block copies the weights into LDS, before the barrier, and each
+  // later tile at the end of the previous iteration, so the loop starts with
+  // layer 1 (its inputs are loop-carried: this pays only where the registers
+  // are not all taken).
   int32_t u = ur.first + wave;
   RowCtx c[NR];
   u32x4 x[NR][KB1];
@@ -1134,9 +1134,11 @@ __global__ __launch_bounds__(NW * 64, 1) void route_bf16_lds(RouteArgs a_in) {
   if constexpr (NL == 3) copy_to_lds<N_W3, NW * 64>(lds + (W1L ? N_W1 : 0) + N_W2, (const u32x4*)a.W[2]);
   for (int i = threadIdx.x; i < NB0 + NB1 + NB2; i += NW * 64)
     lbias[i] = i < NB0 ? a.bias[0][i] : (i < NB0 + NB1 ? a.bias[1][i - NB0] : a.bias[2][i - NB0 - NB1]);
+  if constexpr (PIPE) {
+    if (u < ur.end) setup(u, f0, c, x, g);
+  }
   __syncthreads();
   if (u >= ur.end) return;
-  if constexpr (PIPE) setup(u, f0, c, x, g);
   const float* lb0 = lbias;
   const float* lb1 = lbias + NB0;
   const float* lb2 = lbias + NB0 + NB1;
@@ -1251,17 +1253,11 @@ __global__ __launch_bounds__(NW * 64, 1) void route_bf16_lds(RouteArgs a_in) {
       }
     }
     const int32_t un = u + NW;
-    First fn;
-    if constexpr (PIPE) {
-      __builtin_amdgcn_sched_barrier(0);
-      if (un < ur.end) fn = first_loads(un);
-      __builtin_amdgcn_sched_barrier(0);
-    }
 #pragma unroll
     for (int j = 0; j < NR; ++j) epilogue<AT, RL>(a, c[j], o[j], nullptr, gg);
     if (un >= ur.end) break;
     u = un;
-    if constexpr (PIPE) setup(u, fn, c, x, gg);
+    if constexpr (PIPE) setup(u, first_loads(u), c, x, gg);
   }
 }
 
