@@ -830,7 +830,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(PF > 1 ? 4 
         }
       } else {
         // PF models at a time, whose fronts are loaded together (one round trip
-        // per group instead of one per model)
+        // per group instead of one per model); each is merged by the same
+        // steps as in the loop above (two copies: sharing them through one
+        // inlined helper costs the one-model kernels registers)
         while (merges) {
           int gm[PF];
           uint64_t gmask = 0;
