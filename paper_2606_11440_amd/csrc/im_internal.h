@@ -200,8 +200,7 @@ hipError_t launch_route(const RouteArgs& a, int dtype, int hidden, int n_layers,
                         hipStream_t s);
 // rpm: some model of the pool is (or was) rate-limited (blackbox windows tracked);
 // waves_per_block: envs per block (1, 2 or 4)
-hipError_t launch_schedule(const SchedArgs& a, bool rpm, bool chain, int waves_per_block, int cu_count,
-                           hipStream_t s);
+hipError_t launch_schedule(const SchedArgs& a, bool rpm, bool chain, int waves_per_block, hipStream_t s);
 // Rows of a chain pool's tick: row offsets (pending calls first, then the
 // usable arrivals of each env), the row count and the route step's per-row
 // inputs (q_idx, remaining budget, role of the call).

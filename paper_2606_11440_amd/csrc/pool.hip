@@ -679,7 +679,7 @@ static im_status schedule_impl(im_pool* p, const im_arrivals* arr, const int32_t
     a.slot_ext = p->slot_ext;
     a.csr_bad = p->n_rows + 1;
   }
-  IM_HIP(p, im::launch_schedule(a, p->rpm_active, p->chains, p->sched_waves, p->cu_count, s));
+  IM_HIP(p, im::launch_schedule(a, p->rpm_active, p->chains, p->sched_waves, s));
   p->t += 1;
   return IM_OK;
 }

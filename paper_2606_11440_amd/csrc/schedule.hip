@@ -383,7 +383,8 @@ __device__ __forceinline__ void counter_add(int64_t* p, int64_t v) {
 // pool is empty and the front has room), else to the pool, whose position
 // follows from a ballot over the lanes of its segment; one scattered store
 // appends every model's pool-bound newcomers. Only models with front-bound
-// newcomers then run a merge network, one model at a time.
+// newcomers then run a merge network, one model at a time (single-call pools
+// load the fronts of two such models before merging either).
 //
 // Service is also model-parallel: lane (model, slot) fills its slot from the
 // model's front (the head entries sit at known positions of the front array),
@@ -401,7 +402,7 @@ __device__ __forceinline__ void counter_add(int64_t* p, int64_t v) {
 // completion that is not its query's last call appends the next call, with
 // the query's deadline, to the pending list of the next tick.
 template <bool RPM, bool CHAIN, int PF>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(PF > 1 ? 4 : 5, 8))) void schedule_kernel(SchedArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5, 8))) void schedule_kernel(SchedArgs a) {
   // sorted chunks; in the service phase the refill scan's key buffer, then
   // the counter staging
   __shared__ int4 stage[4][kStageChunks * 64];
@@ -1237,24 +1238,18 @@ hipError_t launch_snapshot(const SchedArgs& a, int e0, int ne, hipStream_t s) {
   return hipGetLastError();
 }
 
-// When the whole grid is resident at 4 waves per SIMD (16 env waves per CU),
-// the single-call kernels load the fronts of up to 4 merging models together:
-// more registers, one wave fewer per SIMD, which such a grid does not need.
-hipError_t launch_schedule(const SchedArgs& a, bool rpm, bool chain, int waves_per_block, int cu_count,
-                           hipStream_t s) {
+// Single-call pools load the fronts of two merging models at a time (the
+// 5-wave register budget holds both); chain pools merge one model at a time.
+hipError_t launch_schedule(const SchedArgs& a, bool rpm, bool chain, int waves_per_block, hipStream_t s) {
   const int w = waves_per_block == 1 || waves_per_block == 2 ? waves_per_block : 4;
   const unsigned blocks = (unsigned)(((int64_t)a.E + w - 1) / w);
   const dim3 threads(64 * w);
-  const bool pf = !chain && cu_count > 0 && (int64_t)a.E <= (int64_t)16 * cu_count;
   if (chain) {
     if (rpm) hipLaunchKernelGGL((schedule_kernel<true, true, 1>), dim3(blocks), threads, 0, s, a);
     else hipLaunchKernelGGL((schedule_kernel<false, true, 1>), dim3(blocks), threads, 0, s, a);
-  } else if (pf) {
-    if (rpm) hipLaunchKernelGGL((schedule_kernel<true, false, 4>), dim3(blocks), threads, 0, s, a);
-    else hipLaunchKernelGGL((schedule_kernel<false, false, 4>), dim3(blocks), threads, 0, s, a);
   } else {
-    if (rpm) hipLaunchKernelGGL((schedule_kernel<true, false, 1>), dim3(blocks), threads, 0, s, a);
-    else hipLaunchKernelGGL((schedule_kernel<false, false, 1>), dim3(blocks), threads, 0, s, a);
+    if (rpm) hipLaunchKernelGGL((schedule_kernel<true, false, 2>), dim3(blocks), threads, 0, s, a);
+    else hipLaunchKernelGGL((schedule_kernel<false, false, 2>), dim3(blocks), threads, 0, s, a);
   }
   return hipGetLastError();
 }
