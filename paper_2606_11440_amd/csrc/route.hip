@@ -1228,6 +1228,10 @@ __global__ __launch_bounds__(NW * 64, 1) void route_bf16_lds(RouteArgs a_in) {
         // LDS fragments two K steps ahead of the MFMAs that use them
         u32x4 w_0 = w2[(cc * KH + 0) * 64 + ln];
         u32x4 w_1 = w2[(cc * KH + 1) * 64 + ln];
+        // the wave raises its issue priority for the chain of MFMAs, so that
+        // the other wave of its SIMD runs its ReLU, packing and loads in the
+        // chain's shadow instead of taking turns on the matrix pipe
+        if constexpr (!PIPE && NR == 2) __builtin_amdgcn_s_setprio(1);
 #pragma unroll
         for (int kb = 0; kb < KH; ++kb) {
           const u32x4 w_2 = w2[(cc * KH + (kb + 2 < KH ? kb + 2 : KH - 1)) * 64 + ln];
@@ -1237,6 +1241,7 @@ __global__ __launch_bounds__(NW * 64, 1) void route_bf16_lds(RouteArgs a_in) {
           w_1 = w_2;
           __builtin_amdgcn_sched_barrier(0);
         }
+        if constexpr (!PIPE && NR == 2) __builtin_amdgcn_s_setprio(0);
         u32x4 f[NR][2];
 #pragma unroll
         for (int j = 0; j < NR; ++j) relu_to_frags(p[j], f[j][0], f[j][1]);
