@@ -258,6 +258,11 @@ def main():
     ap.add_argument("--sample", action="store_true",
                     help="RL-rollout tick: im_route_sample (Gumbel-max sample, log-prob, entropy, "
                          "value head) then im_schedule with the sampled actions")
+    ap.add_argument("--blackbox", action="store_true",
+                    help="half the models of every env rate-limited blackboxes (dispatch limits "
+                         "uniform in [60, 600] per 60-tick window: the congestion feature and the "
+                         "backpressure of App. C), and the dual update of lambda (Eq. 7, eta 1e-3, "
+                         "lambda_max 1, lambda_0 0.2) after every tick")
     ap.add_argument("--no-peak-probe", action="store_true",
                     help="skip the measured-peak probes (a large bf16 GEMM and a device copy)")
     ap.add_argument("--per-tick", default=None, metavar="FILE",
@@ -322,16 +327,33 @@ def main():
     acts = torch.empty(max(max(n_req), 1) + extra, dtype=torch.int32, device="cuda")
     f32 = dict(dtype=torch.float32, device="cuda")
     rl_out = [torch.empty(max(max(n_req), 1) + extra, **f32) for _ in range(3)] if args.sample else None
-    pool = P.Pool(cfg, W, b, emb_dev, cap, lb)
+    bb_limits, lam_dev = [], None
+    if args.blackbox:
+        rng_bb = np.random.default_rng(args.seed + 7)
+        pick = rng_bb.random((cfg["E"], cfg["M"])) < 0.5
+        lim = rng_bb.integers(60, 601, size=(cfg["E"], cfg["M"]))
+        bb_limits = [(int(e), int(m), int(lim[e, m])) for e, m in zip(*np.nonzero(pick))]
+        lam_dev = torch.full((1,), 0.2, dtype=torch.float64, device="cuda")
+
+    def new_pool():
+        pl = P.Pool(cfg, W, b, emb_dev, cap, lb)
+        for e, m, r in bb_limits:
+            pl.set_rpm_limit(e, m, r)
+        return pl
+
+    pool = new_pool()
 
     def route_step(pl, t, st=None, with_schedule=True):
-        """One tick: im_tick, or im_route_sample + im_schedule (RL rollout)."""
+        """One tick: im_tick, or im_route_sample + im_schedule (RL rollout);
+        with --blackbox the dual update follows."""
         if args.sample:
             pl.route_sample(dev[t], 1000 + t, acts, *rl_out, stream=st)
             if with_schedule:
                 pl.schedule(dev[t], acts, st)
         else:
             pl.tick(dev[t], acts, st)
+        if args.blackbox and with_schedule:
+            pl.dual_update(1e-3, 1.0, lam_dev, st)
     torch.cuda.synchronize()
     gen_s = time.perf_counter() - t_gen
 
@@ -371,11 +393,15 @@ def main():
     assert pool.error() == 0, "device error during the benchmark"
     st = pool.state(0, cfg["E"], with_queues=False)
     pool.close()
+    lam_after = None
+    if args.blackbox:
+        lam_after = float(lam_dev.cpu().item())   # after the warm-up and timed ticks
+        lam_dev.fill_(0.2)
 
     # ---- the same K ticks on an identical pool, HIP events on the launch
     # stream around every route and schedule launch (per-kernel durations;
     # the event records themselves add a gap, so this pass is not the value) ----
-    pool2 = P.Pool(cfg, W, b, emb_dev, cap, lb)
+    pool2 = new_pool()
     warm(pool2)
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
     if chains:
@@ -402,6 +428,8 @@ def main():
         ev[k][1].record(stream)
         pool2.schedule(dev[t], acts, stream.cuda_stream)
         ev[k][2].record(stream)
+        if args.blackbox:
+            pool2.dual_update(1e-3, 1.0, lam_dev, stream.cuda_stream)
         if chains:
             rc = hip.hipMemcpyAsync(row_counts.data_ptr() + 4 * k, n_rows_dev, 4, 3,   # device to device
                                     stream.cuda_stream)
@@ -431,7 +459,8 @@ def main():
     sched_avg = float(np.mean(sched_ms))
     flops = np.mean([algorithmic_flops_per_tick(cfg, n) for n in n_req[W_:W_ + K]])
     peak_f = PEAK_BF16_TFLOPS if cfg["dtype"] == "bf16" else PEAK_F32_TFLOPS
-    tag = f"{args.config}_lam{int(cfg['lam'])}" + ("_sample" if args.sample else "")
+    tag = f"{args.config}_lam{int(cfg['lam'])}" + ("_sample" if args.sample else "") + \
+        ("_blackbox" if args.blackbox else "")
 
     def route_roof():
         # the binding roof of the route step: the larger of its matrix time
@@ -494,7 +523,10 @@ def main():
                                f"lambda={cfg['lam']:g}/tick, qcap {cfg['qcap']}, {net_desc}"
                                f" {cfg['dtype']}, ticks {W_}..{W_ + K - 1} of {T}" +
                                ("; RL rollout: Gumbel-max sampled actions, log-probs, entropies, "
-                                "value head" if args.sample else ""),
+                                "value head" if args.sample else "") +
+                               (f"; blackbox models: {len(bb_limits)} of {cfg['E'] * cfg['M']} (env, model) "
+                                "pairs rate-limited (60-tick dispatch window, limits uniform in [60, 600]), "
+                                "dual update of lambda after every tick" if args.blackbox else ""),
                    "envs": cfg["E"], "requests_per_tick": routed / K, "parallelism": "single GPU",
                    "chains": (f"queries of 1..{cfg['max_steps']} sequential calls (uniform), "
                               "deadlines inherited; requests = calls routed (pending + arrivals)")
@@ -512,7 +544,9 @@ def main():
         "roofline_other_kernel": roof_other,
         "input_gen_s": gen_s,
     }
-    if not args.no_cpu_baseline:
+    if args.blackbox:
+        line["lambda_after_timed_ticks"] = lam_after
+    if not args.no_cpu_baseline and not args.blackbox:
         line["cpu_baseline"] = cpu_baseline(cfg, W, b, emb_vals, cap, lb, ticks[W_:W_ + K], Q,
                                             args.cpu_seconds)
     else:

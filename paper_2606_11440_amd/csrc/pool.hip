@@ -42,7 +42,7 @@ struct im_pool {
   int64_t act_cap = 0;
   void* W_res = nullptr;                    // dual-pathway executor: resource-layer fragments
   float* dual_p = nullptr;                  // dual-pathway executor: fp32 parameter block
-  unsigned long long* dual_acc = nullptr;   // [2] completions, Q16 cost (zero between calls)
+  unsigned long long* dual_acc = nullptr;   // [3] completions, Q16 cost, block tickets (zero between calls)
   int64_t* dual_last = nullptr;             // [2] totals at the previous dual update
   // multi-step chains: pending calls [2][E * pend_cap] and their counts
   // [2][E] (by tick parity), chain words of front, pool and slot entries, the
@@ -278,7 +278,7 @@ im_status init_state(im_pool* p, const int32_t* capacity, hipStream_t s) {
   if (st == IM_OK) st = zalloc(p, &p->rpm_ring, EM * (size_t)im::kRpmRing);
   if (st == IM_OK) st = zalloc(p, &p->snap, (size_t)d.n_envs * im::snap_stride(d.n_models));
   if (st == IM_OK) st = zalloc(p, &p->err, 1);
-  if (st == IM_OK) st = zalloc(p, &p->dual_acc, 2);
+  if (st == IM_OK) st = zalloc(p, &p->dual_acc, 3);
   if (st == IM_OK) st = zalloc(p, &p->dual_last, 2);
   if (st == IM_OK && p->chains) {
     const size_t E = (size_t)d.n_envs;

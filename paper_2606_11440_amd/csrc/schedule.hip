@@ -1170,8 +1170,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5, 8))) voi
 // Dual update, step 1: exact int64 sums of completions and Q16 cost over every
 // (env, model) counter row (order-independent: integer atomics).
 // Chain pools count completed queries (env_cnt) instead of completed calls.
-__global__ void dual_reduce_kernel(const int64_t* cnt, int64_t n_em, const int64_t* env_cnt,
-                                   int64_t n_env, unsigned long long* acc) {
+// Dual update (Sec. 4.4, Eq. 7) in one launch: every block sums its share of
+// the completion and Q16 cost counters (waves by shuffles, the block through
+// LDS) and adds them to acc[0..1] with one atomic each; the block that takes
+// the last ticket (acc[2]) then finishes: over the completions since the
+// previous update, C_bar = cost / (2^16 n) and lambda <- clip(lambda +
+// eta (C_bar - 1), 0, lambda_max) in correctly rounded fp64 steps (no
+// completion leaves lambda unchanged), and it resets acc for the next call.
+__global__ __launch_bounds__(256) void dual_update_kernel(const int64_t* cnt, int64_t n_em,
+                                                          const int64_t* env_cnt, int64_t n_env,
+                                                          unsigned long long* acc, int64_t* last, double eta,
+                                                          double lambda_max, double* lambda) {
+  __shared__ unsigned long long part[2][4];
+  __shared__ bool finisher;
   uint64_t n = 0, c = 0;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_em;
        i += (int64_t)gridDim.x * blockDim.x) {
@@ -1188,24 +1199,33 @@ __global__ void dual_reduce_kernel(const int64_t* cnt, int64_t n_em, const int64
     n += (uint64_t)shfl_xor((int64_t)n, m);
     c += (uint64_t)shfl_xor((int64_t)c, m);
   }
-  if ((threadIdx.x & 63) == 0 && (n | c) != 0) {
-    atomicAdd(acc, (unsigned long long)n);
-    atomicAdd(acc + 1, (unsigned long long)c);
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+    part[0][w] = n;
+    part[1][w] = c;
   }
-}
-
-// Dual update, step 2 (one thread): over the completions since the previous
-// update, C_bar = cost / (2^16 n) and lambda <- clip(lambda + eta (C_bar - 1),
-// 0, lambda_max) in correctly rounded fp64 steps; no completion leaves lambda
-// unchanged. Resets the accumulators for the next call.
-__global__ void dual_finish_kernel(unsigned long long* acc, int64_t* last, double eta,
-                                   double lambda_max, double* lambda) {
-  const int64_t n = (int64_t)acc[0], c = (int64_t)acc[1];
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint64_t bn = 0, bc = 0;
+    for (int i = 0; i < (int)(blockDim.x >> 6); ++i) {
+      bn += part[0][i];
+      bc += part[1][i];
+    }
+    if (bn != 0) atomicAdd(acc, (unsigned long long)bn);
+    if (bc != 0) atomicAdd(acc + 1, (unsigned long long)bc);
+    __threadfence();   // this block's sums are visible before its ticket
+    finisher = atomicAdd(acc + 2, 1ull) == (unsigned long long)gridDim.x - 1;
+  }
+  __syncthreads();
+  if (!finisher || threadIdx.x != 0) return;
+  __threadfence();
+  const int64_t tn = (int64_t)atomicAdd(acc, 0ull), tc = (int64_t)atomicAdd(acc + 1, 0ull);
   acc[0] = 0;
   acc[1] = 0;
-  const int64_t dn = n - last[0], dc = c - last[1];
-  last[0] = n;
-  last[1] = c;
+  acc[2] = 0;
+  const int64_t dn = tn - last[0], dc = tc - last[1];
+  last[0] = tn;
+  last[1] = tc;
   if (dn <= 0) return;
   {
     // one rounding per operation, as written (no fused multiply-add)
@@ -1222,12 +1242,11 @@ __global__ void dual_finish_kernel(unsigned long long* acc, int64_t* last, doubl
 hipError_t launch_dual_update(const int64_t* cnt, int64_t n_em, const int64_t* env_cnt, int64_t n_env,
                               unsigned long long* acc, int64_t* last, double eta, double lambda_max,
                               double* lambda, hipStream_t s) {
-  const int64_t want = (n_em + 255) / 256;
+  const int64_t n = n_em > n_env ? n_em : n_env;
+  const int64_t want = (n + 255) / 256;
   const unsigned blocks = (unsigned)(want < 1024 ? (want < 1 ? 1 : want) : 1024);
-  hipLaunchKernelGGL(dual_reduce_kernel, dim3(blocks), dim3(256), 0, s, cnt, n_em, env_cnt, n_env, acc);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(dual_finish_kernel, dim3(1), dim3(1), 0, s, acc, last, eta, lambda_max, lambda);
+  hipLaunchKernelGGL(dual_update_kernel, dim3(blocks), dim3(256), 0, s, cnt, n_em, env_cnt, n_env, acc, last,
+                     eta, lambda_max, lambda);
   return hipGetLastError();
 }
 
